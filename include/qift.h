@@ -1,0 +1,218 @@
+/*
+ * qift.h - C ABI of the MI355X (gfx950) rotated W2A4 quantized linear.
+ *
+ * The operation (Qift, arXiv 2606.02823):
+ *
+ *   y[m, n] = s_w[n] * s_x[m] * sum_k level[n, k] * q[m, k]
+ *
+ * where level[n, :] is a row of a weight matrix quantized to a fixed
+ * four-level set with one scale per output channel and no zero-point
+ * (Sec. 3.3, Sec. 3.5), q[m, :] is the per-token INT4 quantization of the
+ * Hadamard-rotated activation (Sec. 3.1; Sec. 4.1 "Quantization
+ * configuration"), and both scales are applied after the exact integer
+ * accumulation (Sec. 1; Sec. 3.6).
+ *
+ * Level sets ("formats"):
+ *   QIFT_W2_MNZ  mirror no-zero {-1.5,-0.5,+0.5,+1.5}*s, stored as the odd
+ *                integers {-3,-1,+1,+3} with the half scale s_w = s/2
+ *                (Sec. 3.3 Eqs. (13)-(14)).
+ *   QIFT_W2_POT  power-of-two no-zero {-4,-1,+1,+4}*s_w (Sec. 3.3 Eq. (17)).
+ *   QIFT_W4_SYM  symmetric 4-bit integers -7..7 (Eq. (1) with b = 4, used on
+ *                the symmetric range); the sibling format of the L-layer
+ *                W2/W4 schedule (Sec. 4.4).
+ *
+ * Conventions shared by every call:
+ *   - fp16 values travel as uint16_t bit patterns (IEEE binary16).
+ *   - Matrices are row-major and dense: x, act_q and y are [M][K] or [M][N];
+ *     weights are [N][K] (output x input).
+ *   - Every pointer argument is DEVICE memory owned by the caller unless the
+ *     comment says "host".  The library allocates nothing, keeps no pointer
+ *     after a call returns, and never frees caller memory.  Buffers must stay
+ *     alive until the work enqueued on the stream has completed.
+ *   - Device pointers must be 16-byte aligned (QIFT_ERR_ALIGN otherwise).
+ *   - K must be a positive multiple of 64; M >= 1; N >= 1 (no alignment).
+ *   - Every call enqueues asynchronously on the caller's stream and returns
+ *     a status; no call synchronizes.  Argument validation happens on the
+ *     host before any HIP call, so an error return means nothing was
+ *     enqueued.  Faults inside kernels surface at the caller's next
+ *     synchronization.  No C++ exception crosses this interface.
+ *   - The library is stateless apart from a thread-local copy of the last
+ *     HIP error; calls are thread-safe.
+ */
+#ifndef QIFT_H
+#define QIFT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t (a pointer to the runtime's opaque stream). */
+typedef struct ihipStream_t *qift_stream_t;
+
+/* ---- status codes ----------------------------------------------------- */
+enum {
+  QIFT_OK = 0,
+  QIFT_ERR_NULL = -1,      /* a required pointer is NULL                    */
+  QIFT_ERR_SHAPE = -2,     /* M < 1, N < 1, K % 64 != 0, or beyond a limit  */
+  QIFT_ERR_SPEC = -3,      /* bad Hadamard block or clip ratio              */
+  QIFT_ERR_FORMAT = -4,    /* wrong level-set format or layout for the call */
+  QIFT_ERR_CODE = -5,      /* reserved: reported through invalid_count      */
+  QIFT_ERR_ALIGN = -6,     /* a device pointer is not 16-byte aligned       */
+  QIFT_ERR_HIP = -7,       /* a HIP launch failed: see qift_last_hip_error  */
+  QIFT_ERR_WORKSPACE = -8  /* workspace smaller than qift_workspace_bytes   */
+};
+
+/* ---- level-set formats and packed layouts ----------------------------- */
+enum { QIFT_W2_MNZ = 0, QIFT_W2_POT = 1, QIFT_W4_SYM = 2 };
+
+/*
+ * QIFT_LAYOUT_V1 word layouts (uint32 words, little-endian, row-major):
+ *
+ *   W2 ("QW2v1"), words [N][K/16]: 2-bit code c = index of the level in the
+ *     ascending list of its set (MNZ: level = 2c - 3, the unsigned code of
+ *     the fractional-midpoint quantizer of Sec. 3.3 Eqs. (15)-(16); PoT:
+ *     {-4,-1,+1,+4} -> 0..3, so bit 1 is the sign and the magnitude is 4
+ *     exactly when both bits agree).  Weight k = 16j + 4t + b (t, b in 0..3)
+ *     occupies bits [8b + 2t, 8b + 2t + 1] of word j; hence
+ *     (word >> 2t) & 0x03030303 holds the codes of k = 16j+4t .. 16j+4t+3 in
+ *     its four byte lanes.
+ *
+ *   W4 ("QW4v1"), words [N][K/8]: nibble u = q + 8 (1..15).  Weight
+ *     k = 8j + 4t + b (t in 0..1, b in 0..3) occupies bits
+ *     [8b + 4t, 8b + 4t + 3] of word j.
+ */
+enum { QIFT_LAYOUT_V1 = 1 };
+
+/* Packed weight matrix: a non-owning view (all pointers device). */
+typedef struct {
+  int32_t fmt;             /* QIFT_W2_MNZ, QIFT_W2_POT or QIFT_W4_SYM         */
+  int32_t layout;          /* QIFT_LAYOUT_V1                                  */
+  int64_t N, K;            /* output and input features                       */
+  const uint32_t *packed;  /* words, qift_packed_bytes(fmt, N, K) bytes       */
+  const uint16_t *scales;  /* fp16 s_w[N]; for MNZ this is the half scale s/2 */
+} qift_packed_w;
+
+/*
+ * Online rotation + activation quantizer settings.
+ *   K        input features of the token (K % block == 0).
+ *   block    Hadamard block b: a power of two in [2, 8192].  The rotation is
+ *            block-diagonal, I_{K/b} (x) H_b, with the Sylvester matrix
+ *            H_b[i][j] = (-1)^popcount(i & j) (deterministic, no random signs;
+ *            Sec. 4.1 "Quantization configuration").
+ *   clip_num, clip_den   clip ratio c = clip_num / clip_den of the symmetric
+ *            INT4 quantizer, 1 <= clip_num <= clip_den <= 16.  {1, 1} is the
+ *            plain absmax/7 scale; {9, 10} is the paper's 0.9 setting.
+ */
+typedef struct {
+  int64_t K;
+  int32_t block;
+  int32_t clip_num;
+  int32_t clip_den;
+} qift_hadamard_spec;
+
+/* Bytes of packed words: N*K/4 (W2) or N*K/2 (W4); 0 for an invalid query. */
+size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K);
+
+/*
+ * Pack decoded W2 levels into QW2v1 words (Sec. 3.3: a fixed four-level set
+ * with a per-output-channel scale, no zero-point).
+ *   levels        int8 [N][K], each in {-3,-1,+1,+3} (MNZ) or {-4,-1,+1,+4}
+ *                 (PoT).  Passing levels rather than codes keeps this
+ *                 boundary independent of the code assignment.
+ *   scales        fp16 s_w[N]; not read, recorded in *out.
+ *   fmt           QIFT_W2_MNZ or QIFT_W2_POT.
+ *   packed        out: uint32 [N][K/16].
+ *   out           host, out, nullable: filled with the view of the result.
+ *   invalid_count device int32, nullable.  When given, the call first sets it
+ *                 to 0 and then adds the number of levels outside the set;
+ *                 such a level is packed as code 0.  Read it after the stream
+ *                 completes.
+ */
+int qift_pack_w2(const int8_t *levels, const uint16_t *scales, int64_t N, int64_t K,
+                 int32_t fmt, uint32_t *packed, qift_packed_w *out,
+                 int32_t *invalid_count, qift_stream_t stream);
+
+/*
+ * Pack W4 levels q in -7..7 (int8 [N][K]) into QW4v1 words uint32 [N][K/8].
+ * Same conventions as qift_pack_w2; a level outside -7..7 is packed as 0 and
+ * counted.
+ */
+int qift_pack_w4(const int8_t *levels, const uint16_t *scales, int64_t N, int64_t K,
+                 uint32_t *packed, qift_packed_w *out, int32_t *invalid_count,
+                 qift_stream_t stream);
+
+/*
+ * Online Hadamard rotation + per-token symmetric INT4 quantization
+ * (Sec. 3.1; Sec. 4.1 "Quantization configuration").  For each token m:
+ *   X      = (I_{K/b} (x) H_b) x[m]   computed exactly (each fp16 input is an
+ *            integer multiple of 2^-24, and the sums stay below 2^53 units);
+ *   A      = max_k |X_k|;
+ *   q[m,k] = sign(X_k) * min(7, rne(7 |X_k| / (c A)))  (round half to even,
+ *            decided in exact integer arithmetic; A = 0 gives q = 0);
+ *   s_x[m] = fp32( (A * clip_num) / ((clip_den * 7) * sqrt(b)) ), i.e.
+ *            c * max|X| / 7 for the orthonormal rotation H_b / sqrt(b);
+ *   sum[m] = sum_k q[m, k].
+ * Arguments:
+ *   x          fp16 [M][spec.K], finite values (non-finite input is outside
+ *              the contract).
+ *   act_q      out: int8 [M][K].
+ *   act_scale  out: fp32 [M].
+ *   act_sum    out: int32 [M] (required; the linear layers consume it).
+ * Limits: spec.K <= 32768.
+ */
+int qift_rotate_quant_act(const uint16_t *x, int64_t M, qift_hadamard_spec spec,
+                          int8_t *act_q, float *act_scale, int32_t *act_sum,
+                          qift_stream_t stream);
+
+/*
+ * Quantized linear with 2-bit weights (Sec. 1; Sec. 3.6):
+ *   acc[m][n] = sum_k level[n][k] * act_q[m][k]   exact int32
+ *   y[m][n]   = fp16( fp32( fp32(acc) * act_scale[m] ) * fp32(s_w[n]) )
+ * with each fp32 product and the fp16 conversion rounded to nearest even.
+ *   w          host: packed weights with fmt QIFT_W2_MNZ or QIFT_W2_POT.
+ *   act_q, act_scale, act_sum   the outputs of qift_rotate_quant_act for M
+ *              tokens of width w->K (act_sum must be sum_k act_q[m][k]).
+ *   out        out: fp16 y [M][N].
+ * M <= 64 runs the skinny decode kernel; larger M runs the tiled prefill
+ * kernel; both give identical results.
+ */
+int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
+                     const int32_t *act_sum, int64_t M, uint16_t *out, qift_stream_t stream);
+
+/*
+ * Same as qift_w2a4_linear, and additionally:
+ *   acc_out    out, nullable: int32 [M][N], the exact accumulators.
+ *   workspace, workspace_bytes   device scratch of at least
+ *              qift_workspace_bytes(w, M) bytes (nullable when that is 0).
+ */
+int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
+                        const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
+                        void *workspace, size_t workspace_bytes, qift_stream_t stream);
+
+/* The W4 sibling (fmt QIFT_W4_SYM); same arguments and results. */
+int qift_w4a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
+                     const int32_t *act_sum, int64_t M, uint16_t *out, qift_stream_t stream);
+int qift_w4a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
+                        const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
+                        void *workspace, size_t workspace_bytes, qift_stream_t stream);
+
+/* Workspace bytes the _ex calls need for this weight and M (host query). */
+size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
+
+/* Static text for a status code. */
+const char *qift_status_string(int status);
+
+/* The hipError_t value behind the calling thread's last QIFT_ERR_HIP. */
+int qift_last_hip_error(void);
+
+/* Library version string, e.g. "qift 0.1 gfx950". */
+const char *qift_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QIFT_H */

@@ -1,0 +1,152 @@
+// C ABI of libqift: host-side validation, then dispatch to the launchers.
+// Every check runs before the first HIP call, so an error return means
+// nothing was enqueued (and these paths run on machines without a GPU).
+#include <math.h>
+#include <string.h>
+
+#include "../../include/qift.h"
+#include "qift_internal.h"
+
+namespace {
+
+thread_local int g_last_hip = 0;
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline int hip_status(hipError_t e) {
+  if (e == hipSuccess) return QIFT_OK;
+  g_last_hip = (int)e;
+  return QIFT_ERR_HIP;
+}
+
+inline bool is_w2(int32_t fmt) { return fmt == QIFT_W2_MNZ || fmt == QIFT_W2_POT; }
+
+inline bool shape_ok(int64_t N, int64_t K) {
+  // K: multiple of 64; sizes kept below 2^31 per dimension (int indexing inside tiles)
+  return N >= 1 && K >= 64 && K % 64 == 0 && N < (int64_t(1) << 31) && K < (int64_t(1) << 31);
+}
+
+int check_linear(const qift_packed_w* w, bool want_w4, const int8_t* act_q, const float* act_scale,
+                 const int32_t* act_sum, int64_t M, const uint16_t* out, const int32_t* acc_out) {
+  if (!w || !act_q || !act_scale || !act_sum || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
+  if (w->layout != QIFT_LAYOUT_V1) return QIFT_ERR_FORMAT;
+  if (want_w4 ? w->fmt != QIFT_W4_SYM : !is_w2(w->fmt)) return QIFT_ERR_FORMAT;
+  if (!shape_ok(w->N, w->K) || M < 1 || M >= (int64_t(1) << 31)) return QIFT_ERR_SHAPE;
+  // exact int32 accumulation: |acc| <= 7 * 7 * K stays far below 2^31 for K < 2^24
+  if (w->K >= (int64_t(1) << 24)) return QIFT_ERR_SHAPE;
+  if (!aligned16(w->packed) || !aligned16(act_q) || !aligned16(w->scales) || !aligned16(act_scale) ||
+      !aligned16(act_sum) || !aligned16(out) || (acc_out && !aligned16(acc_out)))
+    return QIFT_ERR_ALIGN;
+  return QIFT_OK;
+}
+
+int linear_common(const qift_packed_w* w, bool w4, const int8_t* act_q, const float* act_scale,
+                  const int32_t* act_sum, int64_t M, uint16_t* out, int32_t* acc_out, void* ws,
+                  size_t ws_bytes, qift_stream_t stream) {
+  int st = check_linear(w, w4, act_q, act_scale, act_sum, M, out, acc_out);
+  if (st != QIFT_OK) return st;
+  if (ws_bytes < qift_workspace_bytes(w, M) || (ws_bytes > 0 && !ws)) return QIFT_ERR_WORKSPACE;
+  return hip_status(qift::launch_linear(w->fmt, w->packed, w->scales, w->N, w->K, act_q, act_scale,
+                                        act_sum, M, out, acc_out, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K) {
+  if (!shape_ok(N, K)) return 0;
+  if (is_w2(fmt)) return (size_t)(N * (K / 4));
+  if (fmt == QIFT_W4_SYM) return (size_t)(N * (K / 2));
+  return 0;
+}
+
+int qift_pack_w2(const int8_t* levels, const uint16_t* scales, int64_t N, int64_t K, int32_t fmt,
+                 uint32_t* packed, qift_packed_w* out, int32_t* invalid_count, qift_stream_t stream) {
+  if (!levels || !packed) return QIFT_ERR_NULL;
+  if (!is_w2(fmt)) return QIFT_ERR_FORMAT;
+  if (!shape_ok(N, K)) return QIFT_ERR_SHAPE;
+  if (!aligned16(levels) || !aligned16(packed) || (scales && !aligned16(scales)) ||
+      (invalid_count && (reinterpret_cast<uintptr_t>(invalid_count) & 3u)))
+    return QIFT_ERR_ALIGN;
+  int st = hip_status(qift::launch_pack_w2(levels, N, K, fmt, packed, invalid_count, (hipStream_t)stream));
+  if (st == QIFT_OK && out) *out = qift_packed_w{fmt, QIFT_LAYOUT_V1, N, K, packed, scales};
+  return st;
+}
+
+int qift_pack_w4(const int8_t* levels, const uint16_t* scales, int64_t N, int64_t K, uint32_t* packed,
+                 qift_packed_w* out, int32_t* invalid_count, qift_stream_t stream) {
+  if (!levels || !packed) return QIFT_ERR_NULL;
+  if (!shape_ok(N, K)) return QIFT_ERR_SHAPE;
+  if (!aligned16(levels) || !aligned16(packed) || (scales && !aligned16(scales)) ||
+      (invalid_count && (reinterpret_cast<uintptr_t>(invalid_count) & 3u)))
+    return QIFT_ERR_ALIGN;
+  int st = hip_status(qift::launch_pack_w4(levels, N, K, packed, invalid_count, (hipStream_t)stream));
+  if (st == QIFT_OK && out) *out = qift_packed_w{QIFT_W4_SYM, QIFT_LAYOUT_V1, N, K, packed, scales};
+  return st;
+}
+
+int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,
+                          float* act_scale, int32_t* act_sum, qift_stream_t stream) {
+  if (!x || !act_q || !act_scale || !act_sum) return QIFT_ERR_NULL;
+  if (M < 1 || M >= (int64_t(1) << 31) || spec.K < 64 || spec.K % 64 || spec.K > qift::kActMaxK)
+    return QIFT_ERR_SHAPE;
+  const int32_t b = spec.block;
+  if (b < 2 || b > 8192 || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
+  if (spec.clip_num < 1 || spec.clip_den < spec.clip_num || spec.clip_den > 16) return QIFT_ERR_SPEC;
+  if (!aligned16(x) || !aligned16(act_q) || !aligned16(act_scale) || !aligned16(act_sum))
+    return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_rotate_quant_act(x, M, spec.K, b, spec.clip_num, spec.clip_den, act_q,
+                                                  act_scale, act_sum, (hipStream_t)stream));
+}
+
+int qift_w2a4_linear(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
+                     const int32_t* act_sum, int64_t M, uint16_t* out, qift_stream_t stream) {
+  return linear_common(w, false, act_q, act_scale, act_sum, M, out, nullptr, nullptr, 0, stream);
+}
+
+int qift_w2a4_linear_ex(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
+                        const int32_t* act_sum, int64_t M, uint16_t* out, int32_t* acc_out,
+                        void* workspace, size_t workspace_bytes, qift_stream_t stream) {
+  return linear_common(w, false, act_q, act_scale, act_sum, M, out, acc_out, workspace, workspace_bytes,
+                       stream);
+}
+
+int qift_w4a4_linear(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
+                     const int32_t* act_sum, int64_t M, uint16_t* out, qift_stream_t stream) {
+  return linear_common(w, true, act_q, act_scale, act_sum, M, out, nullptr, nullptr, 0, stream);
+}
+
+int qift_w4a4_linear_ex(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
+                        const int32_t* act_sum, int64_t M, uint16_t* out, int32_t* acc_out,
+                        void* workspace, size_t workspace_bytes, qift_stream_t stream) {
+  return linear_common(w, true, act_q, act_scale, act_sum, M, out, acc_out, workspace, workspace_bytes,
+                       stream);
+}
+
+size_t qift_workspace_bytes(const qift_packed_w* w, int64_t M) {
+  (void)w;
+  (void)M;
+  return 0;
+}
+
+const char* qift_status_string(int status) {
+  switch (status) {
+    case QIFT_OK: return "ok";
+    case QIFT_ERR_NULL: return "null pointer argument";
+    case QIFT_ERR_SHAPE: return "invalid shape (M, N >= 1; K a positive multiple of 64; limits)";
+    case QIFT_ERR_SPEC: return "invalid Hadamard block or clip ratio";
+    case QIFT_ERR_FORMAT: return "wrong level-set format or layout for this call";
+    case QIFT_ERR_CODE: return "level outside the format's level set";
+    case QIFT_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case QIFT_ERR_HIP: return "HIP launch failed";
+    case QIFT_ERR_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+int qift_last_hip_error(void) { return g_last_hip; }
+
+const char* qift_version(void) { return "qift 0.1 gfx950"; }
+
+}  // extern "C"

@@ -1,0 +1,264 @@
+"""Python binding of libqift (ctypes): argument marshalling only.
+
+Every function here checks tensor dtypes, shapes and devices, passes raw
+device pointers and the current HIP stream to the C ABI declared in
+``include/qift.h``, and raises on a non-zero status.  All arithmetic happens
+in the library's HIP kernels; there is no fallback path.  PyTorch serves only
+for device memory and streams.
+
+Names follow the C entry points without the ``qift_`` prefix.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libqift.so")
+
+W2_MNZ, W2_POT, W4_SYM = 0, 1, 2
+LAYOUT_V1 = 1
+
+STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR_SPEC",
+          -4: "QIFT_ERR_FORMAT", -5: "QIFT_ERR_CODE", -6: "QIFT_ERR_ALIGN", -7: "QIFT_ERR_HIP",
+          -8: "QIFT_ERR_WORKSPACE"}
+
+# every symbol declared in include/qift.h
+EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_rotate_quant_act",
+           "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w4a4_linear", "qift_w4a4_linear_ex",
+           "qift_workspace_bytes", "qift_status_string", "qift_last_hip_error", "qift_version")
+
+
+class QiftError(RuntimeError):
+    def __init__(self, fn: str, status: int, lib):
+        msg = lib.qift_status_string(status).decode()
+        extra = f" (hipError {lib.qift_last_hip_error()})" if status == -7 else ""
+        super().__init__(f"{fn}: {STATUS.get(status, status)}: {msg}{extra}")
+        self.status = status
+
+
+class PackedW(ctypes.Structure):
+    _fields_ = [("fmt", ctypes.c_int32), ("layout", ctypes.c_int32), ("N", ctypes.c_int64),
+                ("K", ctypes.c_int64), ("packed", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
+class HadamardSpec(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int64), ("block", ctypes.c_int32), ("clip_num", ctypes.c_int32),
+                ("clip_den", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_02823_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    pw = ctypes.POINTER(PackedW)
+    sig = {
+        "qift_packed_bytes": (sz, [i32, i64, i64]),
+        "qift_pack_w2": (ctypes.c_int, [vp, vp, i64, i64, i32, vp, pw, vp, vp]),
+        "qift_pack_w4": (ctypes.c_int, [vp, vp, i64, i64, vp, pw, vp, vp]),
+        "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
+        "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
+        "qift_w2a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
+        "qift_w4a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
+        "qift_w4a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
+        "qift_workspace_bytes": (sz, [pw, i64]),
+        "qift_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "qift_last_hip_error": (ctypes.c_int, []),
+        "qift_version": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype, f.argtypes = res, args
+    _lib = L
+    return L
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise QiftError(fn, status, lib())
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _dev(t: torch.Tensor, dtype, shape, name):
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _fp16_bits(t: torch.Tensor) -> torch.Tensor:
+    return t.view(torch.int16) if t.dtype == torch.float16 else t
+
+
+@dataclass
+class Packed:
+    """A packed weight matrix: the C view plus the tensors that own its memory."""
+    fmt: int
+    N: int
+    K: int
+    words: torch.Tensor   # uint32 words as int32 [N, K/16] or [N, K/8]
+    scales: torch.Tensor  # fp16 [N]
+
+    def cview(self) -> PackedW:
+        return PackedW(self.fmt, LAYOUT_V1, self.N, self.K, self.words.data_ptr(), self.scales.data_ptr())
+
+    @property
+    def nbytes(self) -> int:
+        return self.words.numel() * 4
+
+
+def packed_bytes(fmt: int, N: int, K: int) -> int:
+    return int(lib().qift_packed_bytes(fmt, N, K))
+
+
+def workspace_bytes(w: Packed, M: int) -> int:
+    v = w.cview()
+    return int(lib().qift_workspace_bytes(ctypes.byref(v), M))
+
+
+def pack_w2(levels: torch.Tensor, scales: torch.Tensor, fmt: int = W2_MNZ, out: torch.Tensor | None = None,
+            invalid_count: torch.Tensor | None = None, check: bool = True, stream=None) -> Packed:
+    """Pack int8 levels [N, K] ({-3,-1,1,3} MNZ or {-4,-1,1,4} PoT) into QW2v1 words.
+
+    With ``check`` (default) a device counter of out-of-set levels is read back
+    after the stream completes and a ValueError is raised when it is non-zero.
+    """
+    N, K = levels.shape
+    _dev(levels, torch.int8, (N, K), "levels")
+    _dev(scales, torch.float16, (N,), "scales")
+    if out is None:
+        out = torch.empty((N, K // 16), dtype=torch.int32, device=levels.device)
+    _dev(out, torch.int32, (N, K // 16), "out")
+    if check and invalid_count is None:
+        invalid_count = torch.empty(1, dtype=torch.int32, device=levels.device)
+    st = lib().qift_pack_w2(levels.data_ptr(), scales.data_ptr(), N, K, fmt, out.data_ptr(), None,
+                            _ptr(invalid_count), _stream(stream))
+    _check("qift_pack_w2", st)
+    if check:
+        bad = int(invalid_count.item())
+        if bad:
+            raise ValueError(f"qift_pack_w2: {bad} levels outside the level set (QIFT_ERR_CODE)")
+    return Packed(fmt, N, K, out, scales)
+
+
+def pack_w4(levels: torch.Tensor, scales: torch.Tensor, out: torch.Tensor | None = None,
+            invalid_count: torch.Tensor | None = None, check: bool = True, stream=None) -> Packed:
+    """Pack int8 W4 levels [N, K] in -7..7 into QW4v1 words."""
+    N, K = levels.shape
+    _dev(levels, torch.int8, (N, K), "levels")
+    _dev(scales, torch.float16, (N,), "scales")
+    if out is None:
+        out = torch.empty((N, K // 8), dtype=torch.int32, device=levels.device)
+    _dev(out, torch.int32, (N, K // 8), "out")
+    if check and invalid_count is None:
+        invalid_count = torch.empty(1, dtype=torch.int32, device=levels.device)
+    st = lib().qift_pack_w4(levels.data_ptr(), scales.data_ptr(), N, K, out.data_ptr(), None,
+                            _ptr(invalid_count), _stream(stream))
+    _check("qift_pack_w4", st)
+    if check:
+        bad = int(invalid_count.item())
+        if bad:
+            raise ValueError(f"qift_pack_w4: {bad} levels outside -7..7 (QIFT_ERR_CODE)")
+    return Packed(W4_SYM, N, K, out, scales)
+
+
+@dataclass
+class QAct:
+    """Quantized activations of M tokens: the triple every linear consumes."""
+    q: torch.Tensor       # int8 [M, K]
+    scale: torch.Tensor   # fp32 [M]
+    sum: torch.Tensor     # int32 [M]
+
+    @property
+    def M(self):
+        return self.q.shape[0]
+
+
+def alloc_act(M: int, K: int, device="cuda") -> QAct:
+    return QAct(torch.empty((M, K), dtype=torch.int8, device=device),
+                torch.empty(M, dtype=torch.float32, device=device),
+                torch.empty(M, dtype=torch.int32, device=device))
+
+
+def rotate_quant_act(x: torch.Tensor, block: int, clip=(1, 1), out: QAct | None = None, stream=None) -> QAct:
+    """Exact block-Hadamard rotation + per-token INT4 quantization of fp16 x [M, K]."""
+    M, K = x.shape
+    _dev(x, torch.float16, (M, K), "x")
+    if out is None:
+        out = alloc_act(M, K, x.device)
+    _dev(out.q, torch.int8, (M, K), "act_q")
+    _dev(out.scale, torch.float32, (M,), "act_scale")
+    _dev(out.sum, torch.int32, (M,), "act_sum")
+    spec = HadamardSpec(K, block, int(clip[0]), int(clip[1]))
+    st = lib().qift_rotate_quant_act(x.data_ptr(), M, spec, out.q.data_ptr(), out.scale.data_ptr(),
+                                     out.sum.data_ptr(), _stream(stream))
+    _check("qift_rotate_quant_act", st)
+    return out
+
+
+def _linear(name: str, w: Packed, act: QAct, out, acc_out, workspace, stream):
+    M, K = act.q.shape
+    if K != w.K:
+        raise ValueError(f"activation width {K} != weight K {w.K}")
+    _dev(act.scale, torch.float32, (M,), "act_scale")
+    _dev(act.sum, torch.int32, (M,), "act_sum")
+    if out is None:
+        out = torch.empty((M, w.N), dtype=torch.float16, device=act.q.device)
+    _dev(out, torch.float16, (M, w.N), "out")
+    if acc_out is not None:
+        _dev(acc_out, torch.int32, (M, w.N), "acc_out")
+    v = w.cview()
+    L = lib()
+    if acc_out is None and workspace is None:
+        st = getattr(L, name)(ctypes.byref(v), act.q.data_ptr(), act.scale.data_ptr(), act.sum.data_ptr(),
+                              M, out.data_ptr(), _stream(stream))
+    else:
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        st = getattr(L, name + "_ex")(ctypes.byref(v), act.q.data_ptr(), act.scale.data_ptr(),
+                                      act.sum.data_ptr(), M, out.data_ptr(), _ptr(acc_out),
+                                      _ptr(workspace), ws_bytes, _stream(stream))
+    _check(name, st)
+    return out
+
+
+def w2a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:
+    """fp16 y [M, N] of the 2-bit quantized linear (MNZ or PoT weights)."""
+    return _linear("qift_w2a4_linear", w, act, out, acc_out, workspace, stream)
+
+
+def w4a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:
+    """fp16 y [M, N] of the W4 sibling."""
+    return _linear("qift_w4a4_linear", w, act, out, acc_out, workspace, stream)
+
+
+def linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:
+    """Dispatch on the weight format."""
+    f = w4a4_linear if w.fmt == W4_SYM else w2a4_linear
+    return f(w, act, out=out, acc_out=acc_out, workspace=workspace, stream=stream)
+
+
+def version() -> str:
+    return lib().qift_version().decode()

@@ -1,0 +1,123 @@
+"""Host-only checks of libqift's C ABI: it loads, exports every declared symbol,
+and rejects bad arguments with the documented status before any HIP call.
+
+No call here reaches a kernel launch: every argument set fails validation
+(the pointers passed are never dereferenced on the host or the device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_02823_amd import qift
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qift.h")
+
+OK, E_NULL, E_SHAPE, E_SPEC, E_FORMAT, E_ALIGN, E_WS = 0, -1, -2, -3, -4, -6, -8
+A = 0x10000       # a 16-byte aligned fake device address (never dereferenced)
+MIS = 0x10008     # an 8-byte aligned, not 16-byte aligned fake address
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(qift.LIB_PATH):
+        pytest.skip("libqift.so not built")
+    return qift.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(qift_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) == 12
+    assert sorted(qift.EXPORTS) == names
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings(L):
+    assert qift.version().startswith("qift")
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8):
+        assert L.qift_status_string(code)
+    assert L.qift_status_string(12345) == b"unknown status"
+
+
+def test_packed_bytes(L):
+    assert qift.packed_bytes(qift.W2_MNZ, 512, 256) == 512 * 256 // 4
+    assert qift.packed_bytes(qift.W2_POT, 14336, 4096) == 14_680_064
+    assert qift.packed_bytes(qift.W4_SYM, 4096, 14336) == 4096 * 14336 // 2
+    assert qift.packed_bytes(qift.W2_MNZ, 4096, 100) == 0     # K % 64
+    assert qift.packed_bytes(7, 4096, 4096) == 0              # unknown format
+    assert qift.packed_bytes(qift.W2_MNZ, 0, 4096) == 0
+
+
+def _spec(K=256, block=256, num=1, den=1):
+    return qift.HadamardSpec(K, block, num, den)
+
+
+def test_rotate_quant_act_validation(L):
+    f = L.qift_rotate_quant_act
+    assert f(None, 4, _spec(), A, A, A, None) == E_NULL
+    assert f(A, 4, _spec(), A, A, None, None) == E_NULL
+    assert f(A, 0, _spec(), A, A, A, None) == E_SHAPE
+    assert f(A, 4, _spec(K=100, block=4), A, A, A, None) == E_SHAPE
+    assert f(A, 4, _spec(K=65536, block=4096), A, A, A, None) == E_SHAPE
+    assert f(A, 4, _spec(block=48), A, A, A, None) == E_SPEC
+    assert f(A, 4, _spec(block=1), A, A, A, None) == E_SPEC
+    assert f(A, 4, _spec(K=16384, block=16384), A, A, A, None) == E_SPEC
+    assert f(A, 4, _spec(K=192, block=128), A, A, A, None) == E_SPEC
+    assert f(A, 4, _spec(num=0, den=1), A, A, A, None) == E_SPEC
+    assert f(A, 4, _spec(num=3, den=2), A, A, A, None) == E_SPEC
+    assert f(A, 4, _spec(num=9, den=17), A, A, A, None) == E_SPEC
+    assert f(MIS, 4, _spec(), A, A, A, None) == E_ALIGN
+    assert f(A, 4, _spec(), A, A, MIS, None) == E_ALIGN
+
+
+def _pw(fmt=qift.W2_MNZ, N=512, K=256, packed=A, scales=A, layout=1):
+    return qift.PackedW(fmt, layout, N, K, packed, scales)
+
+
+def test_linear_validation(L):
+    w2 = L.qift_w2a4_linear
+    w4 = L.qift_w4a4_linear
+    w2x = L.qift_w2a4_linear_ex
+    P = ctypes.byref
+    assert w2(None, A, A, A, 4, A, None) == E_NULL
+    assert w2(P(_pw()), None, A, A, 4, A, None) == E_NULL
+    assert w2(P(_pw()), A, A, None, 4, A, None) == E_NULL
+    assert w2(P(_pw(packed=None)), A, A, A, 4, A, None) == E_NULL
+    assert w2(P(_pw(fmt=qift.W4_SYM)), A, A, A, 4, A, None) == E_FORMAT
+    assert w4(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 4, A, None) == E_FORMAT
+    assert w2(P(_pw(layout=2)), A, A, A, 4, A, None) == E_FORMAT
+    assert w2(P(_pw(K=100)), A, A, A, 4, A, None) == E_SHAPE
+    assert w2(P(_pw(N=0)), A, A, A, 4, A, None) == E_SHAPE
+    assert w2(P(_pw()), A, A, A, 0, A, None) == E_SHAPE
+    assert w2(P(_pw(packed=MIS)), A, A, A, 4, A, None) == E_ALIGN
+    assert w2(P(_pw()), A, A, A, 4, MIS, None) == E_ALIGN
+    assert w2x(P(_pw()), A, A, A, 4, A, MIS, None, 0, None) == E_ALIGN
+    assert w2x(P(_pw()), A, A, A, 4, A, None, None, 64, None) == E_WS
+    assert L.qift_workspace_bytes(P(_pw()), 4) == 0
+
+
+def test_pack_validation(L):
+    f2, f4 = L.qift_pack_w2, L.qift_pack_w4
+    assert f2(None, A, 512, 256, 0, A, None, None, None) == E_NULL
+    assert f2(A, A, 512, 256, qift.W4_SYM, A, None, None, None) == E_FORMAT
+    assert f2(A, A, 512, 100, 0, A, None, None, None) == E_SHAPE
+    assert f2(A, A, 0, 256, 0, A, None, None, None) == E_SHAPE
+    assert f2(MIS, A, 512, 256, 0, A, None, None, None) == E_ALIGN
+    assert f2(A, A, 512, 256, 0, A, None, 0x10002, None) == E_ALIGN
+    assert f4(A, A, 512, 256, None, None, None, None) == E_NULL
+    assert f4(A, A, 512, 96, A, None, None, None) == E_SHAPE
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(qift, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(qift, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        qift.lib()
