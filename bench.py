@@ -1,0 +1,338 @@
+"""Throughput of the rotated W2A4 quantized linear on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-prefill] [--no-cpu]
+
+Decode (the headline ``value``): LLaMA-2-7B-shaped layers (q,k,v,o 4096x4096;
+gate,up 11008x4096; down 4096x11008 with 172 Hadamard blocks of 64), MNZ
+2-bit weights, M = 1 token.  A step pushes one token through 32 distinct
+seeded layers (1.62 GB of packed words, the depth of LLaMA-2-7B) so that the
+weights stream from HBM rather than the 256 MB Infinity Cache.  Per layer:
+4 x rotate_quant_act (inputs of q|k|v, o, gate|up, down) and 4 linears
+(q|k|v and gate|up stacked along N since they share their input).  The step
+is captured once as a hipGraph and replayed.
+``value`` = packed-weight bytes per step / step time (GB/s).
+
+Prefill (reported under "prefill"): LLaMA-3.1-8B-shaped layers at M = 2048,
+layers 0-15 W4 and 16-31 W2 MNZ, 7 linears + 4 rotate_quant_act per layer;
+int8 TOPS = sum 2 M N K / step time.
+
+All inputs are seeded synthetic data resident in HBM before timing starts.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "W2A4 linear packed-weight GB/s (% HBM peak) at M=1; int8 TOPS at M=2048"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS
+DECODE_KERNEL = "k_linear_skinny<0, 1>"   # MNZ decode kernel, one 16-token tile
+
+
+def _sources_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_02823_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def _traffic_record():
+    """HBM bytes per launch of the decode kernel from the committed rocprofv3 PMC summary.
+
+    Returns None unless the summary was taken on the current kernel sources.
+    """
+    path = os.path.join(ROOT, "profiles", "decode_linear_cfg1_m1_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("sources_sha") != _sources_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+class DecodeStack:
+    """cfg1 layer shapes x 32 distinct layers, M tokens, MNZ."""
+
+    def __init__(self, torch, qift, synth, layers=32, M=1):
+        self.torch, self.qift, self.synth = torch, qift, synth
+        self.layers, self.M = layers, M
+        c = synth.CONFIGS[1]
+        sh = {s.name: s for s in c.linears}
+        # (name, N, K, block, activation site); q|k|v and gate|up stacked along N
+        self.plan = [("qkv", 3 * sh["q"].N, sh["q"].K, sh["q"].block, 0),
+                     ("o", sh["o"].N, sh["o"].K, sh["o"].block, 1),
+                     ("gate_up", 2 * sh["gate"].N, sh["gate"].K, sh["gate"].block, 2),
+                     ("down", sh["down"].N, sh["down"].K, sh["down"].block, 3)]
+        self.workload = ("LLaMA-2-7B-shaped decode layer (q,k,v,o 4096x4096; gate,up 11008x4096; "
+                         "down 4096x11008, Hadamard 4096 / 172x64), MNZ W2, M=%d; 32 distinct seeded "
+                         "layers per step (q|k|v and gate|up stacked along N)" % M)
+
+    def setup(self):
+        torch, qift, synth = self.torch, self.qift, self.synth
+        dev = torch.device("cuda")
+        c = synth.CONFIGS[1]
+        self.weights, self.x, self.acts, self.outs = [], [], [], []
+        for layer in range(self.layers):
+            ws = []
+            for slot, (name, N, K, b, site) in enumerate(self.plan):
+                lev = synth.draw_levels_torch(qift.W2_MNZ, N, K, seed=1_000_003 * layer + slot, device=dev)
+                sc = torch.from_numpy(synth.draw_scales(qift.W2_MNZ, N, cfg=1, layer=layer, slot=slot)).to(dev)
+                ws.append(qift.pack_w2(lev, sc, qift.W2_MNZ, check=False))
+                del lev
+            self.weights.append(ws)
+            self.x.append([torch.from_numpy(synth.config_activations(c, layer, site, self.M, K)).to(dev)
+                           for (_, _, K, _, site) in self.plan])
+        self.acts = [qift.alloc_act(self.M, K, dev) for (_, _, K, _, _) in self.plan]
+        self.outs = [torch.empty((self.M, N), dtype=torch.float16, device=dev) for (_, N, _, _, _) in self.plan]
+        torch.cuda.synchronize()
+        self.packed_bytes = sum(w.nbytes for ws in self.weights for w in ws)
+        # algorithmic bytes of one linear launch: packed words + fp16 scales + int8 act
+        # + act scale and sum + fp16 output
+        M = self.M
+        self.alg_bytes = [N * K // 4 + 2 * N + M * K + 8 * M + 2 * M * N for (_, N, K, _, _) in self.plan]
+
+    def step(self):
+        qift = self.qift
+        for layer in range(self.layers):
+            ws, xs = self.weights[layer], self.x[layer]
+            for i, (name, N, K, b, site) in enumerate(self.plan):
+                act = qift.rotate_quant_act(xs[i], b, out=self.acts[i])
+                qift.w2a4_linear(ws[i], act, out=self.outs[i])
+
+    def linear_launches(self):
+        """Only the linear launches of one step (on the activations left in the buffers)."""
+        qift = self.qift
+        for layer in range(self.layers):
+            for i in range(len(self.plan)):
+                qift.w2a4_linear(self.weights[layer][i], self.acts[i], out=self.outs[i])
+
+    @property
+    def launches_per_step(self):
+        return self.layers * len(self.plan)
+
+
+class PrefillStack:
+    """cfg4: LLaMA-3.1-8B shapes, M=2048, layers 0-15 W4, 16-31 W2 MNZ."""
+
+    def __init__(self, torch, qift, synth, layers=32, M=2048):
+        self.torch, self.qift, self.synth = torch, qift, synth
+        self.layers, self.M = layers, M
+        self.c = synth.CONFIGS[4]
+        self.shapes = {s.name: s for s in self.c.linears}
+        self.sites = [("q", "k", "v"), ("o",), ("gate", "up"), ("down",)]
+
+    def setup(self):
+        torch, qift, synth = self.torch, self.qift, self.synth
+        dev = torch.device("cuda")
+        self.weights = []
+        for layer in range(self.layers):
+            fmt = self.c.fmt_of_layer[layer]
+            ws = {}
+            for slot, s in enumerate(self.c.linears):
+                lev = synth.draw_levels_torch(fmt, s.N, s.K, seed=7_000_003 * layer + slot, device=dev)
+                sc = torch.from_numpy(synth.draw_scales(fmt, s.N, cfg=4, layer=layer, slot=slot)).to(dev)
+                ws[s.name] = (qift.pack_w4(lev, sc, check=False) if fmt == qift.W4_SYM
+                              else qift.pack_w2(lev, sc, fmt, check=False))
+                del lev
+            self.weights.append(ws)
+        # one synthetic input per activation site, shared by the layers
+        self.x = [torch.from_numpy(synth.config_activations(self.c, 0, i, self.M, self.shapes[g[0]].K)).to(dev)
+                  for i, g in enumerate(self.sites)]
+        self.acts = [qift.alloc_act(self.M, self.shapes[g[0]].K, dev) for g in self.sites]
+        self.outs = {s.name: torch.empty((self.M, s.N), dtype=torch.float16, device=dev) for s in self.c.linears}
+        torch.cuda.synchronize()
+        self.ops = self.layers * sum(2 * self.M * s.N * s.K for s in self.c.linears)
+
+    def step(self):
+        qift = self.qift
+        for layer in range(self.layers):
+            ws = self.weights[layer]
+            for i, group in enumerate(self.sites):
+                act = qift.rotate_quant_act(self.x[i], self.shapes[group[0]].block, out=self.acts[i])
+                for name in group:
+                    qift.linear(ws[name], act, out=self.outs[name])
+
+
+def cpu_baseline(synth, budget_s=20.0):
+    """The oracle as it stands, on one cfg1 layer at M=1 (4 act quantizations + 7 linears)."""
+    import numpy as np
+    from oracle import levels as olev, linear as olin, pack as opack, quant
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    c = synth.CONFIGS[1]
+    sites = {}
+    prepared = []
+    for s in c.linears:
+        L = synth.draw_levels(olev.FMT_W2_MNZ, s.N, s.K, cfg=1, layer=0, slot=synth.LINEAR_ID[s.name])
+        sw = synth.draw_scales(olev.FMT_W2_MNZ, s.N, cfg=1, layer=0, slot=synth.LINEAR_ID[s.name])
+        prepared.append((s, opack.pack_qw2(L, olev.FMT_W2_MNZ), sw))
+        site = synth.SITE_OF[s.name]
+        sites.setdefault(site, (synth.config_activations(c, 0, site, 1, s.K), s.block))
+    packed = sum(P.nbytes for _, P, _ in prepared)
+
+    def one_layer():
+        qa = {site: quant.act_quant(x, b) for site, (x, b) in sites.items()}
+        for s, P, sw in prepared:
+            q, sx, _, _ = qa[synth.SITE_OF[s.name]]
+            olin.linear(P, sw, olev.FMT_W2_MNZ, s.K, q, sx)
+
+    one_layer()                         # warm the oracle's cached Hadamard matrices
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        one_layer()
+        n += 1
+        if time.perf_counter() - t0 > budget_s / 2 or n >= 2:
+            break
+    dt = (time.perf_counter() - t0) / n
+    return {"value": round(packed / dt / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one cfg1 layer (7 linears, 4 activation quantizations) at M=1, {n} timed pass(es) "
+                      f"of {dt:.2f} s after one warm-up; {packed} packed bytes per pass; host has "
+                      f"{os.cpu_count()} logical CPUs"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--layers", type=int, default=32)
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--prefill-steps", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="launch the decode step eagerly")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run 1 GiB device copies (HBM byte-counter calibration under rocprofv3)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the quantized linear shards by output rows with no "
+              "exchange, so the job throughput is the per-GPU figure; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_02823_amd import qift, synth
+    qift.lib()
+    torch.cuda.set_device(0)
+
+    # ---------------------------------------------------------------- decode (headline)
+    dec = DecodeStack(torch, qift, synth, layers=args.layers, M=1)
+    dec.setup()
+    dec.step()                                   # eager warm-up
+    torch.cuda.synchronize()
+    graph = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            dec.step()
+        torch.cuda.current_stream().wait_stream(s)
+        with torch.cuda.graph(graph):
+            dec.step()
+    run = graph.replay if graph is not None else dec.step
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t0.record()
+    for _ in range(args.steps):
+        run()
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = t0.elapsed_time(t1) / args.steps
+    gbs = dec.packed_bytes / (ms * 1e-3) / 1e9
+
+    # per-launch duration of the decode kernel: HIP events around back-to-back replays of a graph
+    # holding just this step's linear launches (same stream, shapes and weights); inside a graph
+    # the launches run without gaps, so this is the kernel's own average duration
+    lin_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(lin_graph):
+        dec.linear_launches()
+    lin_graph.replay()
+    torch.cuda.synchronize()
+    la, lb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    la.record()
+    for _ in range(args.steps):
+        lin_graph.replay()
+    lb.record()
+    torch.cuda.synchronize()
+    avg_dur = la.elapsed_time(lb) * 1e-3 / (args.steps * dec.launches_per_step)
+    del lin_graph
+    bytes_per_launch = sum(dec.alg_bytes) / len(dec.alg_bytes)
+    achieved = bytes_per_launch / avg_dur / 1e9
+    traffic = _traffic_record()
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": DECODE_KERNEL, "avg_launch_us": round(avg_dur * 1e6, 3),
+                "alg_bytes_per_launch": int(bytes_per_launch)}
+
+    out = {"metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "i8xi2->i32", "data": "synthetic",
+           "config": {"workload": dec.workload, "tokens_per_step": dec.M, "layers": dec.layers,
+                      "packed_bytes_per_step": dec.packed_bytes, "launch": "hipGraph" if graph else "eager"},
+           "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+           "tokens_per_s": round(dec.M / (ms * 1e-3), 1),
+           "host_wall_s": round(wall, 3),
+           "roofline": roofline}
+    del graph
+    dec = None
+    torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- prefill
+    if not args.no_prefill:
+        pre = PrefillStack(torch, qift, synth, layers=args.layers)
+        pre.setup()
+        pre.step()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(args.prefill_steps):
+            pre.step()
+        b.record()
+        torch.cuda.synchronize()
+        pms = a.elapsed_time(b) / args.prefill_steps
+        tops = pre.ops / (pms * 1e-3) / 1e12
+        out["prefill"] = {"workload": "LLaMA-3.1-8B-shaped prefill, M=2048, layers 0-15 W4 / 16-31 W2 MNZ, "
+                                      "7 linears + 4 rotate_quant_act per layer",
+                          "ms_per_step": round(pms, 3), "int8_tops": round(tops, 2),
+                          "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
+                          "steps": args.prefill_steps}
+        pre = None
+        torch.cuda.empty_cache()
+
+    if args.copy_probe:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # ---------------------------------------------------------------- CPU oracle baseline
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(synth)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
