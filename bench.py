@@ -33,7 +33,8 @@ sys.path.insert(0, ROOT)
 METRIC = "W2A4 linear packed-weight GB/s (% HBM peak) at M=1; int8 TOPS at M=2048"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS
-DECODE_KERNEL = "k_linear_skinny<0, 1>"   # MNZ decode kernel, one 16-token tile
+DECODE_KERNEL_FUSED = "k_decode_deep<0, 2, *, *>"   # MNZ decode kernel with the fused rotation
+DECODE_KERNEL = "k_decode_deep<0, 1, 1, *>"          # MNZ decode kernel on staged act_q
 
 
 def _sources_hash() -> str:
@@ -64,9 +65,9 @@ def _traffic_record():
 class DecodeStack:
     """cfg1 layer shapes x 32 distinct layers, M tokens, MNZ."""
 
-    def __init__(self, torch, qift, synth, layers=32, M=1):
+    def __init__(self, torch, qift, synth, layers=32, M=1, fused=True):
         self.torch, self.qift, self.synth = torch, qift, synth
-        self.layers, self.M = layers, M
+        self.layers, self.M, self.fused = layers, M, fused
         c = synth.CONFIGS[1]
         sh = {s.name: s for s in c.linears}
         # (name, N, K, block, activation site); q|k|v and gate|up stacked along N
@@ -97,25 +98,34 @@ class DecodeStack:
         self.outs = [torch.empty((self.M, N), dtype=torch.float16, device=dev) for (_, N, _, _, _) in self.plan]
         torch.cuda.synchronize()
         self.packed_bytes = sum(w.nbytes for ws in self.weights for w in ws)
-        # algorithmic bytes of one linear launch: packed words + fp16 scales + int8 act
-        # + act scale and sum + fp16 output
+        # algorithmic bytes of one linear launch: packed words + fp16 scales + the activation it
+        # reads (fp16 x when the rotation is fused, else int8 act_q + fp32 scale + int32 sum)
+        # + fp16 output
         M = self.M
-        self.alg_bytes = [N * K // 4 + 2 * N + M * K + 8 * M + 2 * M * N for (_, N, K, _, _) in self.plan]
+        act_b = (lambda K: 2 * M * K) if self.fused else (lambda K: M * K + 8 * M)
+        self.alg_bytes = [N * K // 4 + 2 * N + act_b(K) + 2 * M * N for (_, N, K, _, _) in self.plan]
 
     def step(self):
+        """One token through the stack: per linear, rotate + quantize its input, then the linear."""
         qift = self.qift
         for layer in range(self.layers):
             ws, xs = self.weights[layer], self.x[layer]
             for i, (name, N, K, b, site) in enumerate(self.plan):
-                act = qift.rotate_quant_act(xs[i], b, out=self.acts[i])
-                qift.w2a4_linear(ws[i], act, out=self.outs[i])
+                if self.fused:
+                    qift.rotate_quant_linear(ws[i], xs[i], b, out=self.outs[i])
+                else:
+                    act = qift.rotate_quant_act(xs[i], b, out=self.acts[i])
+                    qift.w2a4_linear(ws[i], act, out=self.outs[i])
 
     def linear_launches(self):
-        """Only the linear launches of one step (on the activations left in the buffers)."""
+        """Only the launches of the decode linear kernel of one step."""
         qift = self.qift
         for layer in range(self.layers):
-            for i in range(len(self.plan)):
-                qift.w2a4_linear(self.weights[layer][i], self.acts[i], out=self.outs[i])
+            for i, (name, N, K, b, site) in enumerate(self.plan):
+                if self.fused:
+                    qift.rotate_quant_linear(self.weights[layer][i], self.x[layer][i], b, out=self.outs[i])
+                else:
+                    qift.w2a4_linear(self.weights[layer][i], self.acts[i], out=self.outs[i])
 
     @property
     def launches_per_step(self):
@@ -215,6 +225,8 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch the decode step eagerly")
+    ap.add_argument("--unfused", action="store_true",
+                    help="decode step as separate rotate_quant_act + w2a4_linear launches")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run 1 GiB device copies (HBM byte-counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -229,7 +241,7 @@ def main():
     torch.cuda.set_device(0)
 
     # ---------------------------------------------------------------- decode (headline)
-    dec = DecodeStack(torch, qift, synth, layers=args.layers, M=1)
+    dec = DecodeStack(torch, qift, synth, layers=args.layers, M=1, fused=not args.unfused)
     dec.setup()
     dec.step()                                   # eager warm-up
     torch.cuda.synchronize()
@@ -280,14 +292,16 @@ def main():
     traffic = _traffic_record()
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": DECODE_KERNEL, "avg_launch_us": round(avg_dur * 1e6, 3),
+                "kernel": DECODE_KERNEL if args.unfused else DECODE_KERNEL_FUSED,
+                "avg_launch_us": round(avg_dur * 1e6, 3),
                 "alg_bytes_per_launch": int(bytes_per_launch)}
 
     out = {"metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "i8xi2->i32", "data": "synthetic",
            "config": {"workload": dec.workload, "tokens_per_step": dec.M, "layers": dec.layers,
-                      "packed_bytes_per_step": dec.packed_bytes, "launch": "hipGraph" if graph else "eager"},
+                      "packed_bytes_per_step": dec.packed_bytes, "launch": "hipGraph" if graph else "eager",
+                      "rotation": "separate rotate_quant_act" if args.unfused else "fused into each linear"},
            "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
            "tokens_per_s": round(dec.M / (ms * 1e-3), 1),
            "host_wall_s": round(wall, 3),

@@ -199,6 +199,25 @@ int qift_w4a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float
                         const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
                         void *workspace, size_t workspace_bytes, qift_stream_t stream);
 
+/*
+ * Fused decode form of qift_rotate_quant_act followed by qift_w2a4_linear or
+ * qift_w4a4_linear (any w->fmt), for a few tokens: every workgroup rotates and
+ * quantizes the tokens itself on chip while its first weight tiles stream
+ * in, so the activations never make a round trip through HBM.  Results are
+ * bit-identical to the two-call form.
+ *   x          fp16 [M][w->K] (finite values).
+ *   spec       as for qift_rotate_quant_act; spec.K must equal w->K.
+ *   out        out: fp16 y [M][N].
+ *   acc_out    out, nullable: int32 [M][N].
+ *   act_q, act_scale, act_sum   out, nullable (all three or none): the
+ *              quantized activations, identical to qift_rotate_quant_act's.
+ * Limits: 1 <= M <= 4, w->K <= 16384, spec.block <= 4096 (QIFT_ERR_SHAPE /
+ * QIFT_ERR_SPEC otherwise).
+ */
+int qift_rotate_quant_linear(const qift_packed_w *w, const uint16_t *x, int64_t M, qift_hadamard_spec spec,
+                             uint16_t *out, int32_t *acc_out, int8_t *act_q, float *act_scale,
+                             int32_t *act_sum, qift_stream_t stream);
+
 /* Workspace bytes the _ex calls need for this weight and M (host query). */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
 

@@ -34,6 +34,8 @@ int check_linear(const qift_packed_w* w, bool want_w4, const int8_t* act_q, cons
   if (!shape_ok(w->N, w->K) || M < 1 || M >= (int64_t(1) << 31)) return QIFT_ERR_SHAPE;
   // exact int32 accumulation: |acc| <= 7 * 7 * K stays far below 2^31 for K < 2^24
   if (w->K >= (int64_t(1) << 24)) return QIFT_ERR_SHAPE;
+  // buffer-resource loads address each operand with 32-bit offsets below 2^31
+  if (qift_packed_bytes(w->fmt, w->N, w->K) >= (size_t(1) << 31)) return QIFT_ERR_SHAPE;
   if (!aligned16(w->packed) || !aligned16(act_q) || !aligned16(w->scales) || !aligned16(act_scale) ||
       !aligned16(act_sum) || !aligned16(out) || (acc_out && !aligned16(acc_out)))
     return QIFT_ERR_ALIGN;
@@ -122,6 +124,27 @@ int qift_w4a4_linear_ex(const qift_packed_w* w, const int8_t* act_q, const float
                         void* workspace, size_t workspace_bytes, qift_stream_t stream) {
   return linear_common(w, true, act_q, act_scale, act_sum, M, out, acc_out, workspace, workspace_bytes,
                        stream);
+}
+
+int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t M, qift_hadamard_spec spec,
+                             uint16_t* out, int32_t* acc_out, int8_t* act_q, float* act_scale,
+                             int32_t* act_sum, qift_stream_t stream) {
+  if (!w || !x || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
+  const int given = (act_q != nullptr) + (act_scale != nullptr) + (act_sum != nullptr);
+  if (given != 0 && given != 3) return QIFT_ERR_NULL;
+  if (w->layout != QIFT_LAYOUT_V1 || !(is_w2(w->fmt) || w->fmt == QIFT_W4_SYM)) return QIFT_ERR_FORMAT;
+  if (!shape_ok(w->N, w->K) || M < 1 || M > qift::kFusedMaxM || w->K > qift::kFusedMaxK) return QIFT_ERR_SHAPE;
+  if (qift_packed_bytes(w->fmt, w->N, w->K) >= (size_t(1) << 31)) return QIFT_ERR_SHAPE;
+  const int32_t b = spec.block;
+  if (spec.K != w->K || b < 2 || b > qift::kFusedMaxBlock || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
+  if (spec.clip_num < 1 || spec.clip_den < spec.clip_num || spec.clip_den > 16) return QIFT_ERR_SPEC;
+  if (!aligned16(w->packed) || !aligned16(w->scales) || !aligned16(x) || !aligned16(out) ||
+      (acc_out && !aligned16(acc_out)) || (act_q && !aligned16(act_q)) ||
+      (act_scale && !aligned16(act_scale)) || (act_sum && !aligned16(act_sum)))
+    return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_linear_fused(w->fmt, w->packed, w->scales, w->N, w->K, x, b, spec.clip_num,
+                                              spec.clip_den, M, out, acc_out, act_q, act_scale, act_sum,
+                                              (hipStream_t)stream));
 }
 
 size_t qift_workspace_bytes(const qift_packed_w* w, int64_t M) {

@@ -23,8 +23,19 @@ hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
                          uint16_t* out, int32_t* acc_out, hipStream_t s);
 
-// Largest M served by the skinny decode kernel.
-constexpr int64_t kDecodeMaxM = 64;
+// Fused rotation + quantization + linear for a few decode tokens (qift_linear.hip).
+hipError_t launch_linear_fused(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
+                               const uint16_t* x, int block, int clip_num, int clip_den, int64_t M,
+                               uint16_t* out, int32_t* acc_out, int8_t* act_q, float* act_scale,
+                               int32_t* act_sum, hipStream_t s);
+
+// (den * 7) * sqrt(b): the fixed divisor of the per-token activation scale.
+double act_denominator(int block, int clip_den);
+
+// Limits of the fused entry point.
+constexpr int64_t kFusedMaxM = 4;
+constexpr int64_t kFusedMaxK = 16384;
+constexpr int kFusedMaxBlock = 4096;
 // Largest K accepted by the activation quantizer.
 constexpr int64_t kActMaxK = 32768;
 

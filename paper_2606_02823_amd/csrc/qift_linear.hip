@@ -23,8 +23,13 @@
 //   the 16 activation bytes of token m at the same 16 k, so the k-slot
 //   assignment inside the instruction is the same for both and cancels.
 //   Result: lane l, register r holds D[n = 4 (l >> 4) + r][m = l & 15].
+//
+// A lane's 16-byte load of packed words covers 4 MFMAs: lane group g of a
+// 256-k block reads words [4g, 4g + 4) of that block for each of its rows,
+// and MFMA s uses word 4g + s, i.e. k = 64g + 16s .. +15 within the block.
 #include <hip/hip_fp16.h>
 
+#include "qift_fwht.h"
 #include "qift_internal.h"
 
 namespace qift {
@@ -43,20 +48,18 @@ template <int FMT>
 __device__ __forceinline__ v4i decode_w2(uint32_t w) {
   const uint32_t c0 = w & 0x03030303u, c1 = (w >> 2) & 0x03030303u;
   const uint32_t c2 = (w >> 4) & 0x03030303u, c3 = (w >> 6) & 0x03030303u;
+  v4i r;
   if constexpr (FMT == FMT_POT) {
     // byte table {-4, -1, +1, +4} indexed by the code
     constexpr uint32_t lut = 0x0401FFFCu;
-    v4i r;
     r[0] = (int)__builtin_amdgcn_perm(0u, lut, c0);
     r[1] = (int)__builtin_amdgcn_perm(0u, lut, c1);
     r[2] = (int)__builtin_amdgcn_perm(0u, lut, c2);
     r[3] = (int)__builtin_amdgcn_perm(0u, lut, c3);
-    return r;
   } else {
-    v4i r;
     r[0] = (int)c0; r[1] = (int)c1; r[2] = (int)c2; r[3] = (int)c3;
-    return r;
   }
+  return r;
 }
 
 // Two packed 4-bit words (16 weights) -> 16 unsigned nibbles u = q + 8 as bytes.
@@ -67,6 +70,18 @@ __device__ __forceinline__ v4i decode_w4(uint32_t w0, uint32_t w1) {
   r[2] = (int)(w1 & 0x0F0F0F0Fu);
   r[3] = (int)((w1 >> 4) & 0x0F0F0F0Fu);
   return r;
+}
+
+// Operand s (0..3) of a lane's 64-weight unit: W2 uses one 16-byte load, W4 two.
+template <int FMT>
+__device__ __forceinline__ v4i decode_unit(const uint4 (&u)[FMT == FMT_W4 ? 2 : 1], int s) {
+  if constexpr (FMT == FMT_W4) {
+    const uint4 h = u[s >> 1];
+    return (s & 1) ? decode_w4(h.z, h.w) : decode_w4(h.x, h.y);
+  } else {
+    const uint32_t w = s == 0 ? u[0].x : s == 1 ? u[0].y : s == 2 ? u[0].z : u[0].w;
+    return decode_w2<FMT>(w);
+  }
 }
 
 template <int FMT>
@@ -89,119 +104,659 @@ __device__ __forceinline__ uint16_t epilogue(int acc, float s_x, uint16_t s_w_bi
   return __half_as_ushort(__float2half_rn(t2));
 }
 
-// ---------------------------------------------------------------------------
-// Skinny kernel for M <= 16 * MT tokens per workgroup column.
-// Workgroup = 4 waves on one 16-row tile; wave w takes the 1024-k chunks
-// w, w+4, ...; inside a chunk, lane group g covers k0 = 1024c + 256u + 64g,
-// u = 0..3 (64 weights per lane per unit, 16 B of W2 words).  Partial
-// accumulators are summed across the waves through LDS.
-// ---------------------------------------------------------------------------
-template <int FMT, int MT>
-__global__ __launch_bounds__(256) void k_linear_skinny(
-    const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
-    const int8_t* __restrict__ act, const float* __restrict__ sx, const int32_t* __restrict__ asum,
-    int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
-  constexpr bool W4 = FMT == FMT_W4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, g = lane >> 4;
-  const int n0 = blockIdx.x * 16;
-  const int mbase = blockIdx.y * 16 * MT;
-  const int n = n0 + r16;
-  const bool nvalid = n < N;
-  const int64_t rowbytes = W4 ? (int64_t)K / 2 : (int64_t)K / 4;
-  const char* prow = reinterpret_cast<const char*>(P) + (int64_t)(nvalid ? n : 0) * rowbytes;
-
-  v4i acc[MT];
+// Store the 4 consecutive outputs n0..n0+3 of token m held in D (and their accumulators).
+template <int FMT>
+__device__ __forceinline__ void store4(const v4i& D, int m, int n0, int N, float s_x, int sum_q,
+                                       const uint16_t* __restrict__ sw, uint16_t* __restrict__ y,
+                                       int32_t* __restrict__ acc_out) {
+  int a[4];
+  uint16_t h[4];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[mt] = v4i{0, 0, 0, 0};
-
-  const int nchunks = (K + 1023) >> 10;
-  for (int c = wave; c < nchunks; c += 4) {
-    uint4 wq[4][W4 ? 2 : 1];
+  for (int r = 0; r < 4; ++r) {
+    const int n = n0 + r;
+    a[r] = finish_acc<FMT>(D[r], sum_q);
+    h[r] = n < N ? epilogue(a[r], s_x, sw[n]) : 0;
+  }
+  const int64_t o = (int64_t)m * N + n0;
+  if (n0 + 3 < N && (o & 3) == 0) {
+    *reinterpret_cast<uint2*>(y + o) =
+        make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+    if (acc_out) *reinterpret_cast<int4*>(acc_out + o) = make_int4(a[0], a[1], a[2], a[3]);
+  } else {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int k0 = (c << 10) + (u << 8) + (g << 6);
-      const bool ok = nvalid && k0 < K;
-#pragma unroll
-      for (int h = 0; h < (W4 ? 2 : 1); ++h) {
-        const uint4* src = reinterpret_cast<const uint4*>(prow + (W4 ? k0 / 2 : k0 / 4)) + h;
-        wq[u][h] = ok ? *src : make_uint4(0, 0, 0, 0);
+    for (int r = 0; r < 4; ++r) {
+      if (n0 + r < N) {
+        y[o + r] = h[r];
+        if (acc_out) acc_out[o + r] = a[r];
       }
     }
+  }
+}
+
+// ===========================================================================
+// Decode kernel: M <= 16 tokens (one 16-token MFMA column).
+//
+// Workgroup = 4 waves on one 16-row tile at a time; wave w takes the 1024-k
+// chunks w, w+4, ... of the tile; inside a chunk, lane group g covers
+// k0 = 1024c + 256u + 64g, u = 0..3 (one 16-byte W2 load per unit).  The
+// workgroup walks row tiles blockIdx.x, +gridDim.x, ...; each wave issues
+// the loads of its next chunk (possibly of the next tile) before computing
+// the current one, so weight traffic stays in flight across tiles and during
+// the cross-wave reduction.  Partial accumulators meet in LDS.
+//
+// Activations (ACT):
+//   0  B operands read from act_q in global memory (large M*K),
+//   1  act_q staged once per workgroup into LDS,
+//   2  fused: each workgroup rotates and quantizes the fp16 tokens itself
+//      into LDS (qift_fwht.h), overlapping its first weight loads.
+// ===========================================================================
+constexpr int kRedBytes = 4 * 64 * 16;   // one v4i per lane per wave
+
+template <int FMT>
+struct WChunk {
+  uint4 v[4][FMT == FMT_W4 ? 2 : 1];
+};
+
+template <int FMT>
+__device__ __forceinline__ void load_chunk(WChunk<FMT>& ck, const char* prow, bool rowok, int K, int c,
+                                           int g) {
+  constexpr int NH = FMT == FMT_W4 ? 2 : 1;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if ((c << 10) + (u << 8) >= K) break;   // wave-uniform tail
-      const int k0 = (c << 10) + (u << 8) + (g << 6);
-      const bool kok = k0 < K;
-      uint32_t wd[W4 ? 8 : 4];
-      wd[0] = wq[u][0].x; wd[1] = wq[u][0].y; wd[2] = wq[u][0].z; wd[3] = wq[u][0].w;
-      if constexpr (W4) {
-        wd[4] = wq[u][1].x; wd[5] = wq[u][1].y; wd[6] = wq[u][1].z; wd[7] = wq[u][1].w;
+  for (int u = 0; u < 4; ++u) {
+    const int k0 = (c << 10) + (u << 8) + (g << 6);
+    const bool ok = rowok && k0 < K;
+    const uint4* src = reinterpret_cast<const uint4*>(prow + (FMT == FMT_W4 ? k0 / 2 : k0 / 4));
+#pragma unroll
+    for (int h = 0; h < NH; ++h) ck.v[u][h] = ok ? src[h] : make_uint4(0, 0, 0, 0);
+  }
+}
+
+template <int FMT, int ACT>
+__device__ __forceinline__ void mma_chunk(const WChunk<FMT>& ck, v4i& acc, int K, int c, int g, int m, int M,
+                                          const int8_t* __restrict__ act_g, const int8_t* act_l, int Kpad) {
+  const bool mok = m < M;
+  // B operands of the whole chunk first (independent loads, one wait)
+  v4i b[4][4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int k0 = (c << 10) + (u << 8) + (g << 6);
+    const bool ok = mok && k0 < K;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      uint4 bb = make_uint4(0, 0, 0, 0);
+      if (ok) {
+        bb = ACT == 0 ? *reinterpret_cast<const uint4*>(act_g + (int64_t)m * K + k0 + 16 * s)
+                      : *reinterpret_cast<const uint4*>(act_l + m * Kpad + k0 + 16 * s);
       }
+      b[u][s] = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
+    }
+  }
 #pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        v4i a;
-        if constexpr (W4) a = decode_w4(wd[2 * d], wd[2 * d + 1]);
-        else a = decode_w2<FMT>(wd[d]);
+  for (int u = 0; u < 4; ++u) {
+    if ((c << 10) + (u << 8) >= K) break;   // wave-uniform tail
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int m = mbase + mt * 16 + r16;
-          v4i b = v4i{0, 0, 0, 0};
-          if (kok && m < M) {
-            const uint4 bb = *reinterpret_cast<const uint4*>(act + (int64_t)m * K + k0 + 16 * d);
-            b = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
-          }
-          acc[mt] = mfma_i8(a, b, acc[mt]);
+    for (int s = 0; s < 4; ++s) acc = mfma_i8(decode_unit<FMT>(ck.v[u], s), b[u][s], acc);
+  }
+}
+
+template <int FMT, int ACT, int NTILES>
+__global__ __launch_bounds__(256) void k_decode(
+    const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
+    const int8_t* __restrict__ act, const float* __restrict__ sx, const int32_t* __restrict__ asum,
+    const uint16_t* __restrict__ x, int L, int num, int den, double denom,
+    int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
+    int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+  constexpr int kScratch = ACT == 2 ? (dev::Tile<256, 16>::LDS_DOUBLES * 8 > kRedBytes
+                                           ? dev::Tile<256, 16>::LDS_DOUBLES * 8 : kRedBytes)
+                                    : kRedBytes;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int ntiles = (N + 15) >> 4;
+  const int NC = (K + 1023) >> 10;
+  const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
+
+  const int act_bytes = ACT >= 1 ? ((M * Kpad + 15) & ~15) : 0;
+  int8_t* act_l = reinterpret_cast<int8_t*>(smem);
+  unsigned char* scratch = smem + act_bytes;
+  float* s_scale = reinterpret_cast<float*>(scratch + kScratch);
+  int* s_sum = reinterpret_cast<int*>(s_scale + 16);
+  double* red_d = reinterpret_cast<double*>(s_sum + 16);
+  int* red_i = reinterpret_cast<int*>(red_d + 4);
+
+  // first chunk of this wave's first tile: in flight while the activations are prepared
+  int tile = blockIdx.x;
+  WChunk<FMT> cur;
+  {
+    const int n = tile * 16 + r16;
+    const bool rowok = tile < ntiles && n < N && wave < NC;
+    const char* prow = reinterpret_cast<const char*>(P) + (int64_t)(rowok ? n : 0) * rowbytes;
+    load_chunk<FMT>(cur, prow, rowok, K, wave, g);
+  }
+
+  if constexpr (ACT == 1) {
+    const int per_row = K >> 4;
+    for (int i = tid; i < M * per_row; i += 256) {
+      const int m = i / per_row, j = i - m * per_row;
+      *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) =
+          *reinterpret_cast<const uint4*>(act + (int64_t)m * K + 16 * j);
+    }
+  }
+  if constexpr (ACT == 2) {
+    for (int m = 0; m < M; ++m) {
+      int sq;
+      float sc;
+      dev::quant_token<256, NTILES>(x + (int64_t)m * K, K, L, num, den, denom,
+                                        reinterpret_cast<double*>(scratch), red_d, red_i, act_l + m * Kpad,
+                                        sq, sc);
+      if (tid == 0) {
+        s_scale[m] = sc;
+        s_sum[m] = sq;
+      }
+    }
+    if (blockIdx.x == 0 && act_q_out) {
+      __syncthreads();
+      const int per_row = K >> 4;
+      for (int i = tid; i < M * per_row; i += 256) {
+        const int m = i / per_row, j = i - m * per_row;
+        *reinterpret_cast<uint4*>(act_q_out + (int64_t)m * K + 16 * j) =
+            *reinterpret_cast<const uint4*>(act_l + m * Kpad + 16 * j);
+      }
+      if (tid < M) {
+        scale_out[tid] = s_scale[tid];
+        sum_out[tid] = s_sum[tid];
+      }
+    }
+  } else {
+    if (tid < M) {
+      s_scale[tid] = sx[tid];
+      s_sum[tid] = asum[tid];
+    }
+  }
+  __syncthreads();
+
+  v4i* red = reinterpret_cast<v4i*>(scratch);
+  const int m = r16;   // token of this lane's B operand and outputs
+  for (; tile < ntiles; tile += gridDim.x) {
+    v4i acc = v4i{0, 0, 0, 0};
+    for (int c = wave; c < NC; c += 4) {
+      // prefetch the wave's next chunk: same tile, or the first chunk of the next tile
+      int nc = c + 4, nt = tile;
+      if (nc >= NC) {
+        nc = wave;
+        nt = tile + gridDim.x;
+      }
+      WChunk<FMT> nxt;
+      {
+        const int n = nt * 16 + r16;
+        const bool rowok = nt < ntiles && n < N;
+        const char* prow = reinterpret_cast<const char*>(P) + (int64_t)(rowok ? n : 0) * rowbytes;
+        load_chunk<FMT>(nxt, prow, rowok, K, nc, g);
+      }
+      mma_chunk<FMT, ACT>(cur, acc, K, c, g, m, M, act, act_l, Kpad);
+      cur = nxt;
+    }
+    red[wave * 64 + lane] = acc;
+    __syncthreads();
+    if (wave == 0) {
+      v4i D = red[lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) D += red[w * 64 + lane];
+      if (m < M) store4<FMT>(D, m, tile * 16 + 4 * g, N, s_scale[m], s_sum[m], sw, y, acc_out);
+    }
+    __syncthreads();
+  }
+}
+
+// ===========================================================================
+// Decode kernel with deep loads: M <= 16 tokens whose int8 activations fit in
+// LDS (staged, ACT = 1, or produced in place by the fused rotation and
+// quantization, ACT = 2).
+//
+// A workgroup (4 waves) owns T consecutive 16-row tiles; wave w owns the
+// w-th quarter of K of each of them: NC = ceil(K/1024) units of 256 k, in
+// each of which lane group g reads 64 weights (one 16-byte W2 load).  A wave
+// holds UPT units per tile in registers and issues all of them before it
+// waits, so a workgroup keeps 4*T*UPT KB (W2) of packed weights in flight.
+// The activation (or fp16 x) loads are issued before the weight loads: the
+// vector-memory counter retires loads in order, so this lets the staging or
+// the fused rotation run while the weights are still in flight.  T is
+// chosen per launch so that the grid covers every CU.  The four quarters of
+// a tile meet in LDS and wave j stores tile j (4 consecutive outputs per
+// lane).
+// ===========================================================================
+template <int FMT, int ACT, int NTILES, int T, int UPT>
+__global__ __launch_bounds__(256) void k_decode_deep(
+    const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
+    const int8_t* __restrict__ act, const float* __restrict__ sx, const int32_t* __restrict__ asum,
+    const uint16_t* __restrict__ x, int L, int num, int den, double denom,
+    int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
+    int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+  constexpr int NH = FMT == FMT_W4 ? 2 : 1;
+  constexpr int kRed = 4 * T * 64 * 16;
+  constexpr int kFwht = dev::Tile<256, 16>::LDS_DOUBLES * 8;
+  constexpr int kScratch = ACT == 2 ? (kFwht > kRed ? kFwht : kRed) : kRed;
+  constexpr int kPre = 4;                   // activation pieces per thread loaded ahead of the weights
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
+  const int NC = (K + 1023) >> 10;          // 256-k units per quarter of K
+  const int kq0 = wave * NC * 256;          // first k of this wave's quarter
+
+  const int act_bytes = (M * Kpad + 15) & ~15;
+  int8_t* act_l = reinterpret_cast<int8_t*>(smem);
+  unsigned char* scratch = smem + act_bytes;
+  float* s_scale = reinterpret_cast<float*>(scratch + kScratch);
+  int* s_sum = reinterpret_cast<int*>(s_scale + 16);
+  double* red_d = reinterpret_cast<double*>(s_sum + 16);
+  int* red_i = reinterpret_cast<int*>(red_d + 4);
+
+  const int tile0 = blockIdx.x * T;
+  const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
+  uint32_t rowoff[T];
+  bool rowok[T];
+#pragma unroll
+  for (int j = 0; j < T; ++j) {
+    const int n = (tile0 + j) * 16 + r16;
+    rowok[j] = n < N;
+    rowoff[j] = (uint32_t)(n * rowbytes);
+  }
+
+  // (1) activation loads first
+  const int per_row = K >> 4;               // 16-byte pieces per activation row
+  uint4 apre[ACT == 1 ? kPre : 1];
+  float sx_pre = 0.f;
+  int sum_pre = 0;
+  dev::TokenRaw<NTILES> raw;
+  if constexpr (ACT == 1) {
+    const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act, (uint32_t)(M * K));
+#pragma unroll
+    for (int q = 0; q < kPre; ++q) {
+      const int i = tid + 256 * q;
+      apre[q] = dev::bload16(ars, i < M * per_row ? (uint32_t)(16 * i) : dev::kOutOfRange);
+    }
+    const int mm = tid < M ? tid : 0;
+    sx_pre = sx[mm];
+    sum_pre = asum[mm];
+  } else {
+    dev::load_token_raw<256, NTILES>(raw, x, K);
+  }
+  // keep every activation load ahead of the weight loads in the instruction stream
+  __builtin_amdgcn_sched_barrier(0);
+
+  // (2) the first batch of weights (zeros for rows past N and k past K)
+  uint4 w[T][UPT][NH];
+  auto load_batch = [&](int b) {
+#pragma unroll
+    for (int j = 0; j < T; ++j)
+#pragma unroll
+      for (int u = 0; u < UPT; ++u) {
+        const int uu = b * UPT + u;
+        const int k0 = kq0 + (uu << 8) + (g << 6);
+        const bool ok = rowok[j] && uu < NC && k0 < K;
+        const uint32_t off = ok ? rowoff[j] + (uint32_t)(FMT == FMT_W4 ? k0 / 2 : k0 / 4) : dev::kOutOfRange;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) w[j][u][h] = dev::bload16(wrs, off + 16 * h);
+      }
+  };
+  load_batch(0);
+
+  // (3) activations into LDS
+  if constexpr (ACT == 1) {
+#pragma unroll
+    for (int q = 0; q < kPre; ++q) {
+      const int i = tid + 256 * q;
+      const int m = i / per_row, j = i - m * per_row;
+      if (i < M * per_row) *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) = apre[q];
+    }
+    for (int i = tid + 256 * kPre; i < M * per_row; i += 256) {
+      const int m = i / per_row, j = i - m * per_row;
+      *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) =
+          *reinterpret_cast<const uint4*>(act + (int64_t)m * K + 16 * j);
+    }
+    if (tid < M) {
+      s_scale[tid] = sx_pre;
+      s_sum[tid] = sum_pre;
+    }
+  } else {
+    {
+      // token 0 from the bits loaded ahead of the weights (kept out of the loop below so that
+      // waiting for x does not mean waiting for the weight loads issued after it)
+      int sq;
+      float sc;
+      dev::quant_token_raw<256, NTILES>(raw, K, L, num, den, denom, reinterpret_cast<double*>(scratch), red_d,
+                                        red_i, act_l, sq, sc);
+      if (tid == 0) {
+        s_scale[0] = sc;
+        s_sum[0] = sq;
+      }
+    }
+    for (int m = 1; m < M; ++m) {
+      int sq;
+      float sc;
+      dev::quant_token<256, NTILES>(x + (int64_t)m * K, K, L, num, den, denom, reinterpret_cast<double*>(scratch),
+                                    red_d, red_i, act_l + m * Kpad, sq, sc);
+      if (tid == 0) {
+        s_scale[m] = sc;
+        s_sum[m] = sq;
+      }
+    }
+    if (blockIdx.x == 0 && act_q_out) {
+      __syncthreads();
+      for (int i = tid; i < M * per_row; i += 256) {
+        const int m = i / per_row, j = i - m * per_row;
+        *reinterpret_cast<uint4*>(act_q_out + (int64_t)m * K + 16 * j) =
+            *reinterpret_cast<const uint4*>(act_l + m * Kpad + 16 * j);
+      }
+      if (tid < M) {
+        scale_out[tid] = s_scale[tid];
+        sum_out[tid] = s_sum[tid];
+      }
+    }
+  }
+  __syncthreads();
+
+  // (4) MFMAs, batch by batch (one batch unless K > 4096 * UPT)
+  v4i acc[T];
+#pragma unroll
+  for (int j = 0; j < T; ++j) acc[j] = v4i{0, 0, 0, 0};
+  const int m = r16;
+  const bool mok = m < M;
+  const int8_t* arow = act_l + m * Kpad;
+  for (int b = 0; b * UPT < NC; ++b) {
+    if (b > 0) load_batch(b);
+#pragma unroll
+    for (int j = 0; j < T; ++j) {
+#pragma unroll
+      for (int u = 0; u < UPT; ++u) {
+        const int uu = b * UPT + u;
+        const int kb = kq0 + (uu << 8);
+        if (uu >= NC || kb >= K) break;       // wave-uniform
+        const int k0 = kb + (g << 6);
+        const bool ok = mok && k0 < K;
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+          uint4 bb = make_uint4(0, 0, 0, 0);
+          if (ok) bb = *reinterpret_cast<const uint4*>(arow + k0 + 16 * s2);
+          acc[j] = mfma_i8(decode_unit<FMT>(w[j][u], s2), v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w},
+                           acc[j]);
         }
       }
     }
   }
 
-  __shared__ v4i red[4][MT][64];
+  // (5) quarters of each tile meet in LDS; wave j stores tile j
+  v4i* red = reinterpret_cast<v4i*>(scratch);   // the FWHT scratch is free again
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) red[wave][mt][lane] = acc[mt];
+  for (int j = 0; j < T; ++j) red[(j * 4 + wave) * 64 + lane] = acc[j];
   __syncthreads();
-  // wave w finishes token tiles mt = w, w+4, ... (only mt < MT exist)
-  for (int mt = wave; mt < MT; mt += 4) {
-    v4i D = red[0][mt][lane];
+  if (wave < T) {
+    const int j = wave;
+    v4i D = red[(j * 4) * 64 + lane];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) D += red[w][mt][lane];
-    const int m = mbase + mt * 16 + r16;
+    for (int q = 1; q < 4; ++q) D += red[(j * 4 + q) * 64 + lane];
+    const int tile = tile0 + j;
+    if (mok && tile * 16 < N) store4<FMT>(D, m, tile * 16 + 4 * g, N, s_scale[m], s_sum[m], sw, y, acc_out);
+  }
+}
+
+// ===========================================================================
+// Prefill kernel: tiles of 256 weight rows x 16*MTILES tokens.
+//
+// Workgroup = 4 waves; wave w owns weight rows [64w, 64w+64) of the tile
+// (4 MFMA row tiles) and all 16*MTILES tokens (MTILES column tiles), i.e.
+// 4*MTILES int32 accumulator tiles.  K advances in 256-k steps: the
+// activation tile [16*MTILES][256] int8 is double-buffered in LDS (global
+// loads for step k+1 are issued before the MFMAs of step k), and each wave
+// reads its own packed weights straight into registers (one 16-byte load
+// per lane per row tile: 4 MFMAs' worth of A operands), also one step ahead.
+// ===========================================================================
+constexpr int kGemmBK = 256;
+constexpr int kGemmLdsRow = kGemmBK + 16;   // padded row (bytes) of the LDS activation tile
+
+template <int FMT, int MTILES>
+__global__ __launch_bounds__(256) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
+                                              int N, int K, const int8_t* __restrict__ act,
+                                              const float* __restrict__ sx, const int32_t* __restrict__ asum,
+                                              int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+  constexpr int NH = FMT == FMT_W4 ? 2 : 1;
+  constexpr int BM = 16 * MTILES;
+  constexpr int TILE_BYTES = BM * kGemmLdsRow;
+  constexpr int STAGE_U4 = BM * (kGemmBK / 16) / 256;   // 16-byte activation loads per thread per step
+  __shared__ __align__(16) int8_t lds[2][TILE_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int n_base = blockIdx.x * 256 + wave * 64;
+  const int m_base = blockIdx.y * BM;
+  const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
+  const int KT = (K + kGemmBK - 1) / kGemmBK;
+
+  // weight rows of this lane (one per row tile); zeros for rows past N and k past K
+  const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
+  uint32_t rowoff[4];
+  bool rowok[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int n = n_base + 16 * j + r16;
+    rowok[j] = n < N;
+    rowoff[j] = (uint32_t)(n * rowbytes);
+  }
+  auto load_w = [&](uint4 (&w)[4][NH], int kt) {
+    const int k0 = kt * kGemmBK + 64 * g;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool ok = rowok[j] && k0 < K;
+      const uint32_t off = ok ? rowoff[j] + (uint32_t)(FMT == FMT_W4 ? k0 / 2 : k0 / 4) : dev::kOutOfRange;
+#pragma unroll
+      for (int h = 0; h < NH; ++h) w[j][h] = dev::bload16(wrs, off + 16 * h);
+    }
+  };
+  // activation staging: thread tid moves 16-byte pieces i = tid + 256 q of the [BM][256] tile
+  // (the activation block of this workgroup's tokens; zeros past M and K)
+  const int mrows = M - m_base < BM ? M - m_base : BM;
+  const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act + (int64_t)m_base * K, (uint32_t)(mrows * K));
+  auto load_a = [&](uint4 (&st)[STAGE_U4], int kt) {
+#pragma unroll
+    for (int q = 0; q < STAGE_U4; ++q) {
+      const int i = tid + 256 * q;
+      const int row = i >> 4, col = (i & 15) * 16;
+      const int k = kt * kGemmBK + col;
+      st[q] = dev::bload16(ars, (row < mrows && k < K) ? (uint32_t)(row * K + k) : dev::kOutOfRange);
+    }
+  };
+  auto store_a = [&](const uint4 (&st)[STAGE_U4], int buf) {
+#pragma unroll
+    for (int q = 0; q < STAGE_U4; ++q) {
+      const int i = tid + 256 * q;
+      const int row = i >> 4, col = (i & 15) * 16;
+      *reinterpret_cast<uint4*>(&lds[buf][row * kGemmLdsRow + col]) = st[q];
+    }
+  };
+
+  v4i acc[4][MTILES];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int t = 0; t < MTILES; ++t) acc[j][t] = v4i{0, 0, 0, 0};
+
+  uint4 wcur[4][NH], wnxt[4][NH];
+  uint4 st[STAGE_U4];
+  load_w(wcur, 0);
+  load_a(st, 0);
+  store_a(st, 0);
+  __syncthreads();
+
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    const bool more = kt + 1 < KT;
+    if (more) {
+      load_w(wnxt, kt + 1);
+      load_a(st, kt + 1);
+    }
+    const int8_t* tileb = lds[buf];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      v4i a[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) a[j] = decode_unit<FMT>(wcur[j], s);
+#pragma unroll
+      for (int t = 0; t < MTILES; ++t) {
+        const uint4 bb = *reinterpret_cast<const uint4*>(&tileb[(16 * t + r16) * kGemmLdsRow + 64 * g + 16 * s]);
+        const v4i b = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j][t] = mfma_i8(a[j], b, acc[j][t]);
+      }
+    }
+    if (more) {
+      store_a(st, buf ^ 1);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int h = 0; h < NH; ++h) wcur[j][h] = wnxt[j][h];
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int t = 0; t < MTILES; ++t) {
+    const int m = m_base + 16 * t + r16;
     if (m < M) {
       const float s_x = sx[m];
       const int sq = asum[m];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int nn = n0 + 4 * g + r;
-        if (nn < N) {
-          const int a = finish_acc<FMT>(D[r], sq);
-          y[(int64_t)m * N + nn] = epilogue(a, s_x, sw[nn]);
-          if (acc_out) acc_out[(int64_t)m * N + nn] = a;
-        }
-      }
+      for (int j = 0; j < 4; ++j) store4<FMT>(acc[j][t], m, n_base + 16 * j + 4 * g, N, s_x, sq, sw, y, acc_out);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+constexpr int kDecodeMaxLds = 96 * 1024;   // activation bytes staged in LDS by the decode kernel
+constexpr int kDecodeGrid = 512;           // workgroups of the decode kernel (2 per CU)
+
+inline int kpad_of(int64_t K) { return (int)K + 16; }
+
+template <int FMT, int ACT, int NTILES>
+hipError_t launch_decode(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
+                         const float* sx, const int32_t* asum, const uint16_t* x, int L, int num, int den,
+                         double denom, int8_t* aq_out, float* sc_out, int32_t* sum_out, int64_t M, uint16_t* y,
+                         int32_t* acc_out, hipStream_t s) {
+  const int Kpad = kpad_of(K);
+  const int ntiles = (int)((N + 15) / 16);
+  const int grid = ntiles < kDecodeGrid ? ntiles : kDecodeGrid;
+  const int act_bytes = ACT >= 1 ? (((int)M * Kpad + 15) & ~15) : 0;
+  const int scratch = ACT == 2 ? (dev::Tile<256, 16>::LDS_DOUBLES * 8 > kRedBytes
+                                      ? dev::Tile<256, 16>::LDS_DOUBLES * 8 : kRedBytes)
+                               : kRedBytes;
+  const size_t shmem = (size_t)act_bytes + scratch + 16 * 4 + 16 * 4 + 4 * 8 + 4 * 4;
+  if (shmem > 65536) {
+    // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&k_decode<FMT, ACT, NTILES>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (attr != hipSuccess) return attr;
+  }
+  hipLaunchKernelGGL((k_decode<FMT, ACT, NTILES>), dim3(grid), dim3(256), shmem, s, P, sw, (int)N, (int)K, act,
+                     sx, asum, x, L, num, den, denom, aq_out, sc_out, sum_out, (int)M, Kpad, y, acc_out);
+  return hipGetLastError();
+}
+
+template <int FMT, int ACT, int NTILES, int T, int UPT>
+hipError_t launch_deep_t(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
+                         const float* sx, const int32_t* asum, const uint16_t* x, int L, int num, int den,
+                         double denom, int8_t* aq_out, float* sc_out, int32_t* sum_out, int64_t M, uint16_t* y,
+                         int32_t* acc_out, hipStream_t s) {
+  const int Kpad = kpad_of(K);
+  const int ntiles = (int)((N + 15) / 16);
+  const int grid = (ntiles + T - 1) / T;
+  constexpr int kRed = 4 * T * 64 * 16;
+  constexpr int kFwht = dev::Tile<256, 16>::LDS_DOUBLES * 8;
+  const int scratch = ACT == 2 ? (kFwht > kRed ? kFwht : kRed) : kRed;
+  const size_t shmem = (size_t)((((int)M * Kpad) + 15) & ~15) + scratch + 16 * 4 + 16 * 4 + 4 * 8 + 4 * 4;
+  if (shmem > 65536) {
+    // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&k_decode_deep<FMT, ACT, NTILES, T, UPT>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (attr != hipSuccess) return attr;
+  }
+  hipLaunchKernelGGL((k_decode_deep<FMT, ACT, NTILES, T, UPT>), dim3(grid), dim3(256), shmem, s, P, sw, (int)N,
+                     (int)K, act, sx, asum, x, L, num, den, denom, aq_out, sc_out, sum_out, (int)M, Kpad, y,
+                     acc_out);
+  return hipGetLastError();
+}
+
+// K <= 4096: 4 units per wave and tile, T tiles per workgroup (as many as keep the grid at >= 256
+// workgroups, up to 4).  Longer K: one tile per workgroup and up to 16 (W4: 8) units per batch.
+template <int FMT, int ACT, int NTILES>
+hipError_t launch_deep(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
+                       const float* sx, const int32_t* asum, const uint16_t* x, int L, int num, int den,
+                       double denom, int8_t* aq_out, float* sc_out, int32_t* sum_out, int64_t M, uint16_t* y,
+                       int32_t* acc_out, hipStream_t s) {
+#define QIFT_DEEP(TT, UU) launch_deep_t<FMT, ACT, NTILES, TT, UU>(P, sw, N, K, act, sx, asum, x, L, num, den, \
+                                                                  denom, aq_out, sc_out, sum_out, M, y, acc_out, s)
+  // (a fused token of K <= 4096 is one rotation tile, so NTILES > 1 implies K > 4096)
+  if constexpr (!(ACT == 2 && NTILES > 1)) {
+    if (K <= 4096) {
+      const int64_t t = (N + 15) / 16 / 256;
+      if (t <= 1) return QIFT_DEEP(1, 4);
+      if (t == 2) return QIFT_DEEP(2, 4);
+      if (t == 3) return QIFT_DEEP(3, 4);
+      return QIFT_DEEP(4, 4);
+    }
+  }
+  if constexpr (!(ACT == 2 && NTILES == 1)) {
+    if constexpr (FMT == FMT_W4) return QIFT_DEEP(1, 8);
+    else return QIFT_DEEP(1, 16);
+  }
+  return hipErrorInvalidValue;
+#undef QIFT_DEEP
 }
 
 template <int FMT>
 hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
                       const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
                       hipStream_t s) {
-  const unsigned gx = (unsigned)((N + 15) / 16);
-  const int Ni = (int)N, Ki = (int)K, Mi = (int)M;
   if (M <= 16) {
-    hipLaunchKernelGGL((k_linear_skinny<FMT, 1>), dim3(gx, 1), dim3(256), 0, s, P, sw, Ni, Ki, act, sx,
-                       asum, Mi, y, acc_out);
-  } else if (M <= 32) {
-    hipLaunchKernelGGL((k_linear_skinny<FMT, 2>), dim3(gx, 1), dim3(256), 0, s, P, sw, Ni, Ki, act, sx,
-                       asum, Mi, y, acc_out);
+    if (M * kpad_of(K) <= kDecodeMaxLds)
+      return launch_deep<FMT, 1, 1>(P, sw, N, K, act, sx, asum, nullptr, 0, 1, 1, 1.0, nullptr, nullptr, nullptr,
+                                    M, y, acc_out, s);
+    return launch_decode<FMT, 0, 1>(P, sw, N, K, act, sx, asum, nullptr, 0, 1, 1, 1.0, nullptr, nullptr, nullptr,
+                                    M, y, acc_out, s);
+  }
+  const unsigned gx = (unsigned)((N + 255) / 256);
+  if (M <= 64) {
+    hipLaunchKernelGGL((k_gemm<FMT, 4>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P, sw, (int)N,
+                       (int)K, act, sx, asum, (int)M, y, acc_out);
   } else {
-    // 64 tokens per workgroup column; larger M tiles the grid in y
-    const unsigned gy = (unsigned)((M + 63) / 64);
-    hipLaunchKernelGGL((k_linear_skinny<FMT, 4>), dim3(gx, gy), dim3(256), 0, s, P, sw, Ni, Ki, act, sx,
-                       asum, Mi, y, acc_out);
+    hipLaunchKernelGGL((k_gemm<FMT, 8>), dim3(gx, (unsigned)((M + 127) / 128)), dim3(256), 0, s, P, sw, (int)N,
+                       (int)K, act, sx, asum, (int)M, y, acc_out);
   }
   return hipGetLastError();
+}
+
+template <int FMT, int NTILES>
+hipError_t launch_fused_nt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
+                           int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M,
+                           uint16_t* y, int32_t* acc_out, hipStream_t s) {
+  return launch_deep<FMT, 2, NTILES>(P, sw, N, K, nullptr, nullptr, nullptr, x, L, num, den, denom, aq, sc, sm,
+                                     M, y, acc_out, s);
+}
+
+template <int FMT>
+hipError_t launch_fused_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x,
+                            int L, int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M,
+                            uint16_t* y, int32_t* acc_out, hipStream_t s) {
+  switch ((K + 4095) / 4096) {
+    case 1: return launch_fused_nt<FMT, 1>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    case 2: return launch_fused_nt<FMT, 2>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    case 3: return launch_fused_nt<FMT, 3>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    case 4: return launch_fused_nt<FMT, 4>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
@@ -213,6 +768,20 @@ hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales
     case FMT_MNZ: return launch_fmt<FMT_MNZ>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, s);
     case FMT_POT: return launch_fmt<FMT_POT>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, s);
     case FMT_W4: return launch_fmt<FMT_W4>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_linear_fused(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
+                               const uint16_t* x, int block, int clip_num, int clip_den, int64_t M,
+                               uint16_t* out, int32_t* acc_out, int8_t* act_q, float* act_scale,
+                               int32_t* act_sum, hipStream_t s) {
+  const int L = dev::ilog2c(block);
+  const double denom = act_denominator(block, clip_den);
+  switch (fmt) {
+    case FMT_MNZ: return launch_fused_fmt<FMT_MNZ>(packed, scales, N, K, x, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, M, out, acc_out, s);
+    case FMT_POT: return launch_fused_fmt<FMT_POT>(packed, scales, N, K, x, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, M, out, acc_out, s);
+    case FMT_W4: return launch_fused_fmt<FMT_W4>(packed, scales, N, K, x, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, M, out, acc_out, s);
     default: return hipErrorInvalidValue;
   }
 }

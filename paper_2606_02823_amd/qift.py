@@ -29,7 +29,8 @@ STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR
 # every symbol declared in include/qift.h
 EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_rotate_quant_act",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w4a4_linear", "qift_w4a4_linear_ex",
-           "qift_workspace_bytes", "qift_status_string", "qift_last_hip_error", "qift_version")
+           "qift_rotate_quant_linear", "qift_workspace_bytes", "qift_status_string", "qift_last_hip_error",
+           "qift_version")
 
 
 class QiftError(RuntimeError):
@@ -72,6 +73,7 @@ def lib():
         "qift_w2a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
         "qift_w4a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
         "qift_w4a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
+        "qift_rotate_quant_linear": (ctypes.c_int, [pw, vp, i64, HadamardSpec, vp, vp, vp, vp, vp, vp]),
         "qift_workspace_bytes": (sz, [pw, i64]),
         "qift_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "qift_last_hip_error": (ctypes.c_int, []),
@@ -258,6 +260,32 @@ def linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=
     """Dispatch on the weight format."""
     f = w4a4_linear if w.fmt == W4_SYM else w2a4_linear
     return f(w, act, out=out, acc_out=acc_out, workspace=workspace, stream=stream)
+
+
+def rotate_quant_linear(w: Packed, x: torch.Tensor, block: int, clip=(1, 1), out=None, acc_out=None,
+                        act_out: QAct | None = None, stream=None) -> torch.Tensor:
+    """Fused rotate_quant_act + linear for M <= 4 fp16 tokens [M, K]; optional act_out receives the act triple."""
+    M, K = x.shape
+    _dev(x, torch.float16, (M, K), "x")
+    if K != w.K:
+        raise ValueError(f"activation width {K} != weight K {w.K}")
+    if out is None:
+        out = torch.empty((M, w.N), dtype=torch.float16, device=x.device)
+    _dev(out, torch.float16, (M, w.N), "out")
+    if acc_out is not None:
+        _dev(acc_out, torch.int32, (M, w.N), "acc_out")
+    if act_out is not None:
+        _dev(act_out.q, torch.int8, (M, K), "act_q")
+        _dev(act_out.scale, torch.float32, (M,), "act_scale")
+        _dev(act_out.sum, torch.int32, (M,), "act_sum")
+    v = w.cview()
+    spec = HadamardSpec(K, block, int(clip[0]), int(clip[1]))
+    st = lib().qift_rotate_quant_linear(
+        ctypes.byref(v), x.data_ptr(), M, spec, out.data_ptr(), _ptr(acc_out),
+        None if act_out is None else act_out.q.data_ptr(), None if act_out is None else act_out.scale.data_ptr(),
+        None if act_out is None else act_out.sum.data_ptr(), _stream(stream))
+    _check("qift_rotate_quant_linear", st)
+    return out
 
 
 def version() -> str:

@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -102,6 +102,20 @@ def test_linear_validation(L):
     assert w2x(P(_pw()), A, A, A, 4, A, MIS, None, 0, None) == E_ALIGN
     assert w2x(P(_pw()), A, A, A, 4, A, None, None, 64, None) == E_WS
     assert L.qift_workspace_bytes(P(_pw()), 4) == 0
+
+
+def test_fused_validation(L):
+    f = L.qift_rotate_quant_linear
+    P = ctypes.byref
+    sp = _spec(K=256, block=256)
+    assert f(None, A, 1, sp, A, None, None, None, None, None) == E_NULL
+    assert f(P(_pw()), A, 1, sp, A, None, A, None, None, None) == E_NULL       # act outputs: all or none
+    assert f(P(_pw(layout=3)), A, 1, sp, A, None, None, None, None, None) == E_FORMAT
+    assert f(P(_pw()), A, 5, sp, A, None, None, None, None, None) == E_SHAPE     # M > 4
+    assert f(P(_pw(K=32768)), A, 1, _spec(K=32768, block=4096), A, None, None, None, None, None) == E_SHAPE
+    assert f(P(_pw()), A, 1, _spec(K=512, block=256), A, None, None, None, None, None) == E_SPEC
+    assert f(P(_pw(K=8192)), A, 1, _spec(K=8192, block=8192), A, None, None, None, None, None) == E_SPEC
+    assert f(P(_pw()), MIS, 1, sp, A, None, None, None, None, None) == E_ALIGN
 
 
 def test_pack_validation(L):

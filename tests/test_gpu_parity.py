@@ -270,3 +270,108 @@ def test_linear_deterministic(Q):
     y1, a1 = run_linear(Q, pk, act, M, N)
     y2, a2 = run_linear(Q, pk, act, M, N)
     assert torch.equal(a1, a2) and torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+# ----------------------------------------------------------------------------- decode paths
+
+
+@pytest.mark.parametrize("M,K,b", [(8, 14336, 2048), (16, 14336, 2048), (16, 4096, 4096), (12, 11008, 64)])
+def test_decode_activation_paths(Q, M, K, b):
+    # activations staged in LDS (M*K small), above 64 KiB of LDS, or read from global (M*K large)
+    N = 784
+    fmt = levels.FMT_W2_MNZ
+    L = synth.draw_levels(fmt, N, K, cfg=95, layer=M)
+    s_w = synth.draw_scales(fmt, N, cfg=95, layer=M)
+    x = synth.activations_fp16(95, M, 1, M, K, K // 100, 30.0)
+    pk = pack_dev(Q, L, s_w, fmt)
+    act = Q.rotate_quant_act(dev(x), b)
+    q_ref, sx_ref = check_act(act, x, b)
+    y, acc = run_linear(Q, pk, act, M, N)
+    check_linear(y, acc, L, q_ref, sx_ref, s_w)
+
+
+FUSED_SHAPES = [(512, 256, 256), (1000, 1088, 64), (4096, 4096, 4096), (2064, 11008, 64),
+                (4096, 14336, 2048), (1040, 16384, 4096), (784, 8192, 8)]
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("N,K,b", FUSED_SHAPES)
+@pytest.mark.parametrize("M", [1, 4])
+def test_fused_rotate_quant_linear(Q, fmt, N, K, b, M):
+    L = synth.draw_levels(fmt, N, K, cfg=96, layer=K + M)
+    s_w = synth.draw_scales(fmt, N, cfg=96, layer=K + M)
+    x = synth.activations_fp16(96, K + M, 2, M, K, max(1, K // 100), 30.0)
+    pk = pack_dev(Q, L, s_w, fmt)
+    xd = dev(x)
+    act = Q.alloc_act(M, K)
+    acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    y = Q.rotate_quant_linear(pk, xd, b, acc_out=acc, act_out=act)
+    torch.cuda.synchronize()
+    q_ref, sx_ref = check_act(act, x, b)
+    check_linear(y, acc, L, q_ref, sx_ref, s_w)
+    # bit-identical to the two-call form
+    act2 = Q.rotate_quant_act(xd, b)
+    y2, acc2 = run_linear(Q, pk, act2, M, N)
+    assert torch.equal(acc, acc2) and torch.equal(y.view(torch.int16), y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("M", [2, 3])
+def test_fused_clip_and_no_act_output(Q, M):
+    N, K, b = 1024, 4096, 4096
+    fmt = levels.FMT_W2_POT
+    L = synth.draw_levels(fmt, N, K, cfg=97, layer=M)
+    s_w = synth.draw_scales(fmt, N, cfg=97, layer=M)
+    x = synth.activations_fp16(97, M, 0, M, K, 41, 30.0)
+    x[M - 1] = 0                                    # a zero token inside the batch
+    pk = pack_dev(Q, L, s_w, fmt)
+    y = Q.rotate_quant_linear(pk, dev(x), b, clip=(9, 10))
+    torch.cuda.synchronize()
+    q_ref, sx_ref, _, _ = quant.act_quant(x, b, (9, 10))
+    acc_ref = olin.int_dot(L, q_ref)
+    assert np.array_equal(bits16(host(y)), bits16(olin.epilogue_fp32(acc_ref, sx_ref, s_w)))
+
+
+# ----------------------------------------------------------------------------- graph replay
+
+
+def test_graph_replay_matches_eager(Q):
+    # one decode layer slice captured as a hipGraph, replayed several times with eager work
+    # and synchronizations in between; every replay must equal the eager result
+    K, b = 4096, 4096
+    shapes = [(3 * 1024, levels.FMT_W2_MNZ), (2048, levels.FMT_W2_POT), (1024, levels.FMT_W4_SYM)]
+    pks = []
+    for i, (N, fmt) in enumerate(shapes):
+        L = synth.draw_levels(fmt, N, K, cfg=98, layer=i)
+        pks.append(pack_dev(Q, L, synth.draw_scales(fmt, N, cfg=98, layer=i), fmt))
+    x = dev(synth.activations_fp16(98, 0, 0, 1, K, 41, 30.0))
+    xs = dev(synth.activations_fp16(98, 1, 0, 16, K, 41, 30.0))
+    acts = Q.alloc_act(16, K)
+    outs = [torch.empty((1, N), dtype=torch.float16, device="cuda") for N, _ in shapes]
+    outs16 = [torch.empty((16, N), dtype=torch.float16, device="cuda") for N, _ in shapes]
+
+    def step():
+        for pk, o in zip(pks, outs):
+            Q.rotate_quant_linear(pk, x, b, out=o)
+        Q.rotate_quant_act(xs, b, out=acts)
+        for pk, o in zip(pks, outs16):
+            Q.linear(pk, acts, out=o)
+
+    step()
+    torch.cuda.synchronize()
+    eager = [o.clone() for o in outs + outs16]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(4):
+        for o in outs + outs16:
+            o.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for o, e in zip(outs + outs16, eager):
+            assert torch.equal(o.view(torch.int16), e.view(torch.int16))
