@@ -71,17 +71,19 @@ __device__ __forceinline__ void reg_stages(double (&v)[E], int r_lo, int r_hi) {
 // Window W: register e of thread t holds tile element
 //   i = (t & (2^W - 1)) | (e << W) | ((t >> W) << (W + 4)),
 // i.e. index bits [W, W + 4) are in registers (W = 0 is the natural layout,
-// element 16t + e).  With W a compile-time constant and W = 0 or W >= 4, the
-// padded LDS slot is a per-thread base plus a compile-time offset per e.
+// element 16t + e).  LDS slot of element i: i + 2 (i/16) (two spare doubles
+// per 16, the fastest of the paddings measured for these exchanges).  With W
+// a compile-time constant and W = 0 or W >= 4 the slot is a per-thread base
+// plus a compile-time offset per e.
+template <int W>
+__device__ __forceinline__ int win_elem(int t) {
+  return W == 0 ? 16 * t : ((t & ((1 << W) - 1)) | ((t >> W) << (W + 4)));
+}
 template <int W>
 __device__ __forceinline__ int win_pbase(int t) {
-  if constexpr (W == 0) {
-    return 18 * t;
-  } else {
-    static_assert(W >= 4, "window");
-    const int base = (t & ((1 << W) - 1)) | ((t >> W) << (W + 4));
-    return base + 2 * (base >> 4);
-  }
+  static_assert(W == 0 || W >= 4, "window");
+  const int base = win_elem<W>(t);
+  return base + 2 * (base >> 4);
 }
 template <int W>
 constexpr int win_step() { return W == 0 ? 1 : (1 << W) + (1 << (W - 3)); }
@@ -101,44 +103,48 @@ __device__ __forceinline__ void lds_load_w(const double* lds, double (&v)[16], i
 }
 
 // In-place transform of one tile over index bits [0, L) (block 2^L, L <= TB).
-// Natural layout on entry and on exit.  All NT threads must call it.
-// Index bits are brought into registers four at a time: windows 0, 4, 8 and,
-// for 8192-element tiles, 9 (its only new bit is 12).
-template <int NT, int E>
-__device__ __forceinline__ void fwht_tile(double (&v)[E], double* lds, int t, int L) {
+// Natural layout on entry.  With NATURAL the values are back in the natural
+// layout on exit; otherwise they stay in the last window used, which is
+// returned (0, 4, 8 or 9) so the caller can address elements with
+// win_elem/win_step.  All NT threads must call it.
+template <int NT, int E, bool NATURAL>
+__device__ __forceinline__ int fwht_tile(double (&v)[E], double* lds, int t, int L) {
   static_assert(E == 16, "16 elements per thread");
   using S = Tile<NT, E>;
   static_assert(S::TB == 12 || S::TB == 13, "tile of 4096 or 8192");
   reg_stages<E>(v, 0, L < 4 ? L : 4);
-  if (L <= 4) return;
+  if (L <= 4) return 0;
+  int w = 4;
   lds_store_w<0>(lds, v, t);
   __syncthreads();
   lds_load_w<4>(lds, v, t);
   reg_stages<E>(v, 0, (L < 8 ? L : 8) - 4);
   if (L > 8) {
+    // a thread's window-4 slots were read only by itself, so it may overwrite them at once
     lds_store_w<4>(lds, v, t);
     __syncthreads();
     lds_load_w<8>(lds, v, t);
     reg_stages<E>(v, 0, (L < 12 ? L : 12) - 8);
+    w = 8;
     if constexpr (S::TB == 13) {
       if (L > 12) {
         lds_store_w<8>(lds, v, t);
         __syncthreads();
         lds_load_w<9>(lds, v, t);
         reg_stages<E>(v, 3, 4);   // register bit 3 of window 9 is index bit 12
-        lds_store_w<9>(lds, v, t);
-      } else {
-        lds_store_w<8>(lds, v, t);
+        w = 9;
       }
-    } else {
-      lds_store_w<8>(lds, v, t);
     }
-  } else {
-    lds_store_w<4>(lds, v, t);
   }
-  __syncthreads();
-  lds_load_w<0>(lds, v, t);
-  __syncthreads();
+  if constexpr (NATURAL) {
+    if (w == 4) lds_store_w<4>(lds, v, t);
+    else if (w == 8) lds_store_w<8>(lds, v, t);
+    else lds_store_w<9>(lds, v, t);
+    __syncthreads();
+    lds_load_w<0>(lds, v, t);
+    return 0;
+  }
+  return w;
 }
 
 // Per-token rounding constants: q = sign(X) min(7, rne(7 den |X| / (num A))).
@@ -175,31 +181,69 @@ __device__ __attribute__((noinline)) int quant_exact(double ax, double f, int64_
   return (int)(q < 7 ? q : 7);
 }
 
-// Exact rounding of one magnitude.  The fp64 quotient v = |X| c1 is within
-// 1e-13 of the exact 7 den |X| / (num A) (v <= 112), so when its fractional
-// part is farther than 1e-9 from 1/2 the nearest integer is decided;
-// otherwise the exact int64 remainder decides.
-__device__ __forceinline__ int quant_mag(double ax, const QuantParams& p) {
-  const double v = ax * p.c1;       // c1 = 0 when A = 0, giving q = 0
-  const double f = floor(v);
-  const double fr = v - f;
-  if (fabs(fr - 0.5) <= 1e-9 && p.Ai > 0) return quant_exact(ax, f, p.Ai, p.num, p.den);
-  const double r = fr > 0.5 ? f + 1.0 : f;
-  return (int)fmin(r, 7.0);
+// Rounding of 16 values.  The fp64 quotient v = |X| c1 is within 1e-13 of the
+// exact 7 den |X| / (num A) (v <= 112), so unless v lies within 1e-9 of a
+// half-integer its nearest integer is rint(v).  That branch-free fast path
+// covers all 16 values; only when some lane of the wave has a value that
+// close to a half (a wave-uniform, rare branch) are those values redone with
+// the exact int64 test.
+__device__ __forceinline__ void quant16(const double (&v)[16], const QuantParams& p, int (&q)[16]) {
+  int near = 0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const double vv = fabs(v[e]) * p.c1;   // c1 = 0 when A = 0, giving q = 0
+    const double r = rint(vv);
+    near |= fabs(vv - r) > 0.5 - 1e-9;
+    const int qq = (int)fmin(r, 7.0);
+    q[e] = v[e] < 0.0 ? -qq : qq;
+  }
+  if (__any(near)) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const double ax = fabs(v[e]);
+      const double vv = ax * p.c1;
+      if (p.Ai > 0 && fabs(vv - rint(vv)) > 0.5 - 1e-9) {
+        const int qq = quant_exact(ax, floor(vv), p.Ai, p.num, p.den);
+        q[e] = v[e] < 0.0 ? -qq : qq;
+      }
+    }
+  }
 }
 
-__device__ __forceinline__ int quant_one(double val, const QuantParams& p) {
-  const int q0 = quant_mag(fabs(val), p);
-  return val < 0.0 ? -q0 : q0;
+// Wave-wide max / sum with DPP moves inside rows of 16 lanes and lane reads
+// across the four rows (no LDS traffic).
+#define QIFT_DPP_F64(x, CTRL)                                                                  \
+  __hiloint2double(__builtin_amdgcn_update_dpp(__double2hiint(x), __double2hiint(x), CTRL, 0xf, 0xf, false), \
+                   __builtin_amdgcn_update_dpp(__double2loint(x), __double2loint(x), CTRL, 0xf, 0xf, false))
+
+__device__ __forceinline__ double wave_max(double x) {
+  x = fmax(x, QIFT_DPP_F64(x, 0xb1));    // quad_perm [1,0,3,2]
+  x = fmax(x, QIFT_DPP_F64(x, 0x4e));    // quad_perm [2,3,0,1]
+  x = fmax(x, QIFT_DPP_F64(x, 0x141));   // row_half_mirror
+  x = fmax(x, QIFT_DPP_F64(x, 0x140));   // row_mirror
+  double r = x;
+#pragma unroll
+  for (int row = 1; row < 4; ++row)
+    r = fmax(r, __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(x), row * 16),
+                                 __builtin_amdgcn_readlane(__double2loint(x), row * 16)));
+  return r;   // lane 0 holds the wave maximum (the others hold partial results)
+}
+
+__device__ __forceinline__ int wave_sum(int x) {
+  x += __builtin_amdgcn_update_dpp(x, x, 0xb1, 0xf, 0xf, false);
+  x += __builtin_amdgcn_update_dpp(x, x, 0x4e, 0xf, 0xf, false);
+  x += __builtin_amdgcn_update_dpp(x, x, 0x141, 0xf, 0xf, false);
+  x += __builtin_amdgcn_update_dpp(x, x, 0x140, 0xf, 0xf, false);
+  return __builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16) + __builtin_amdgcn_readlane(x, 32) +
+         __builtin_amdgcn_readlane(x, 48);
 }
 
 // Block-wide max of a non-negative double; red must hold NT/64 doubles.
 template <int NT>
 __device__ __forceinline__ double block_max(double v, double* red) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+  v = wave_max(v);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
+  __syncthreads();   // red may still be read from a previous call
   if (lane == 0) red[wave] = v;
   __syncthreads();
   double r = red[0];
@@ -210,8 +254,7 @@ __device__ __forceinline__ double block_max(double v, double* red) {
 
 template <int NT>
 __device__ __forceinline__ int block_sum(int v, int* red) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  v = wave_sum(v);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) red[wave] = v;
@@ -269,7 +312,7 @@ __device__ __forceinline__ void quant_token_raw(const TokenRaw<NTILES>& raw, int
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
     unpack_fp16(v[tau], raw.d[tau]);
-    fwht_tile<NT, 16>(v[tau], lds, t, L);
+    fwht_tile<NT, 16, true>(v[tau], lds, t, L);
 #pragma unroll
     for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[tau][e]));
   }
@@ -279,14 +322,90 @@ __device__ __forceinline__ void quant_token_raw(const TokenRaw<NTILES>& raw, int
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
     const int64_t base = (int64_t)tau * S::T + 16 * t;
+    int q[16];
+    quant16(v[tau], p, q);
     uint32_t w[4] = {0, 0, 0, 0};
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const int q = quant_one(v[tau][e], p);
-      qs += q;
-      w[e >> 2] |= ((uint32_t)q & 0xFFu) << (8 * (e & 3));
+      qs += q[e];
+      w[e >> 2] |= ((uint32_t)q[e] & 0xFFu) << (8 * (e & 3));
     }
     if (base < K) *reinterpret_cast<uint4*>(dst + base) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  sum_q = block_sum<NT>(qs, red_i);
+  scale = (float)((A * (double)num) / denom);
+}
+
+// Rotate + quantize one token whose raw fp16 bits are staged in LDS (raw_l,
+// K halves, 16-byte aligned), writing int8 codes to LDS (dst).  The tile loops
+// are rolled so that the code is one compact tile body executed from the
+// instruction cache: pass 1 transforms every tile and keeps the running
+// absmax; pass 2 transforms each tile again and quantizes it (a token of a
+// single tile is transformed once).  Values are quantized in the layout the
+// transform ends in and the codes scattered bytewise, which saves the
+// exchange back to the natural layout.  All NT threads must call it.
+template <int W>
+__device__ __forceinline__ void store_codes(int8_t* dst, const int (&q)[16], int t) {
+  int8_t* d = dst + win_elem<W>(t);
+#pragma unroll
+  for (int e = 0; e < 16; ++e) d[e * (W == 0 ? 1 : (1 << W))] = (int8_t)q[e];
+}
+
+template <int NT>
+__device__ __forceinline__ void quant_token_staged(const uint16_t* raw_l, int64_t K, int L, int num, int den,
+                                                   double denom, double* xch, double* red_d, int* red_i,
+                                                   int8_t* dst, int& sum_q, float& scale) {
+  using S = Tile<NT, 16>;
+  const int t = threadIdx.x;
+  const int ntiles = (int)((K + S::T - 1) / S::T);
+  double v[16];
+  auto load_tile = [&](int tau) {
+    const int64_t base = (int64_t)tau * S::T + 16 * t;
+    uint4 d[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
+    if (base < K) {
+      d[0] = *reinterpret_cast<const uint4*>(raw_l + base);
+      d[1] = *reinterpret_cast<const uint4*>(raw_l + base + 8);
+    }
+    unpack_fp16(v, d);
+  };
+  double amax = 0.0;
+  int wend = 0;
+#pragma unroll 1
+  for (int tau = 0; tau < ntiles; ++tau) {
+    load_tile(tau);
+    wend = fwht_tile<NT, 16, false>(v, xch, t, L);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
+    if (tau + 1 < ntiles) __syncthreads();   // the exchange buffer is reused by the next tile
+  }
+  const double A = block_max<NT>(amax, red_d);
+  const QuantParams p = make_qparams(A, num, den);
+  int qs = 0;
+#pragma unroll 1
+  for (int tau = 0; tau < ntiles; ++tau) {
+    if (ntiles > 1) {
+      __syncthreads();
+      load_tile(tau);
+      fwht_tile<NT, 16, false>(v, xch, t, L);
+    }
+    int q[16];
+    quant16(v, p, q);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) qs += q[e];
+    // elements past K belong to whole blocks past K and to the padding of dst: skipped
+    int8_t* tile_dst = dst + (int64_t)tau * S::T;
+    const bool whole = (int64_t)(tau + 1) * S::T <= K;
+    if (whole) {
+      if (wend == 0) store_codes<0>(tile_dst, q, t);
+      else if (wend == 4) store_codes<4>(tile_dst, q, t);
+      else store_codes<8>(tile_dst, q, t);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int i = wend == 0 ? 16 * t + e : wend == 4 ? win_elem<4>(t) + (e << 4) : win_elem<8>(t) + (e << 8);
+        if ((int64_t)tau * S::T + i < K) tile_dst[i] = (int8_t)q[e];
+      }
+    }
   }
   sum_q = block_sum<NT>(qs, red_i);
   scale = (float)((A * (double)num) / denom);

@@ -321,9 +321,9 @@ __global__ __launch_bounds__(256) void k_decode(
 // The activation (or fp16 x) loads are issued before the weight loads: the
 // vector-memory counter retires loads in order, so this lets the staging or
 // the fused rotation run while the weights are still in flight.  T is
-// chosen per launch so that the grid covers every CU.  The four quarters of
-// a tile meet in LDS and wave j stores tile j (4 consecutive outputs per
-// lane).
+// chosen per launch so that the grid covers every CU with one workgroup
+// each (up to 6 tiles).  The four quarters of a tile meet in LDS and wave
+// j mod 4 stores tile j (4 consecutive outputs per lane).
 // ===========================================================================
 template <int FMT, int ACT, int NTILES, int T, int UPT>
 __global__ __launch_bounds__(256) void k_decode_deep(
@@ -345,8 +345,10 @@ __global__ __launch_bounds__(256) void k_decode_deep(
   const int kq0 = wave * NC * 256;          // first k of this wave's quarter
 
   const int act_bytes = (M * Kpad + 15) & ~15;
+  const int raw_bytes = ACT == 2 ? ((2 * K + 15) & ~15) : 0;
   int8_t* act_l = reinterpret_cast<int8_t*>(smem);
-  unsigned char* scratch = smem + act_bytes;
+  uint16_t* raw_l = reinterpret_cast<uint16_t*>(smem + act_bytes);   // staged fp16 token (ACT 2)
+  unsigned char* scratch = smem + act_bytes + raw_bytes;
   float* s_scale = reinterpret_cast<float*>(scratch + kScratch);
   int* s_sum = reinterpret_cast<int*>(s_scale + 16);
   double* red_d = reinterpret_cast<double*>(s_sum + 16);
@@ -420,23 +422,28 @@ __global__ __launch_bounds__(256) void k_decode_deep(
       s_sum[tid] = sum_pre;
     }
   } else {
-    {
-      // token 0 from the bits loaded ahead of the weights (kept out of the loop below so that
-      // waiting for x does not mean waiting for the weight loads issued after it)
-      int sq;
-      float sc;
-      dev::quant_token_raw<256, NTILES>(raw, K, L, num, den, denom, reinterpret_cast<double*>(scratch), red_d,
-                                        red_i, act_l, sq, sc);
-      if (tid == 0) {
-        s_scale[0] = sc;
-        s_sum[0] = sq;
+    // token 0: its raw bits were loaded ahead of the weights; park them in LDS, then rotate and
+    // quantize with the compact two-pass routine.  Later tokens are staged straight from memory.
+    using S = dev::Tile<256, 16>;
+#pragma unroll
+    for (int tau = 0; tau < NTILES; ++tau) {
+      const int64_t base = (int64_t)tau * S::T + 16 * tid;
+      if (base < K) {
+        *reinterpret_cast<uint4*>(raw_l + base) = raw.d[tau][0];
+        *reinterpret_cast<uint4*>(raw_l + base + 8) = raw.d[tau][1];
       }
     }
-    for (int m = 1; m < M; ++m) {
+    for (int m = 0; m < M; ++m) {
+      if (m > 0) {
+        __syncthreads();   // the previous token's raw bits are consumed
+        for (int i = tid; i < per_row * 2; i += 256)
+          *reinterpret_cast<uint4*>(raw_l + 8 * i) = *reinterpret_cast<const uint4*>(x + (int64_t)m * K + 8 * i);
+      }
+      __syncthreads();
       int sq;
       float sc;
-      dev::quant_token<256, NTILES>(x + (int64_t)m * K, K, L, num, den, denom, reinterpret_cast<double*>(scratch),
-                                    red_d, red_i, act_l + m * Kpad, sq, sc);
+      dev::quant_token_staged<256>(raw_l, K, L, num, den, denom, reinterpret_cast<double*>(scratch), red_d, red_i,
+                                   act_l + m * Kpad, sq, sc);
       if (tid == 0) {
         s_scale[m] = sc;
         s_sum[m] = sq;
@@ -491,8 +498,7 @@ __global__ __launch_bounds__(256) void k_decode_deep(
 #pragma unroll
   for (int j = 0; j < T; ++j) red[(j * 4 + wave) * 64 + lane] = acc[j];
   __syncthreads();
-  if (wave < T) {
-    const int j = wave;
+  for (int j = wave; j < T; j += 4) {   // wave j (and j + 4) stores tile j
     v4i D = red[(j * 4) * 64 + lane];
 #pragma unroll
     for (int q = 1; q < 4; ++q) D += red[(j * 4 + q) * 64 + lane];
@@ -675,7 +681,9 @@ hipError_t launch_deep_t(const uint32_t* P, const uint16_t* sw, int64_t N, int64
   constexpr int kRed = 4 * T * 64 * 16;
   constexpr int kFwht = dev::Tile<256, 16>::LDS_DOUBLES * 8;
   const int scratch = ACT == 2 ? (kFwht > kRed ? kFwht : kRed) : kRed;
-  const size_t shmem = (size_t)((((int)M * Kpad) + 15) & ~15) + scratch + 16 * 4 + 16 * 4 + 4 * 8 + 4 * 4;
+  const size_t raw_bytes = ACT == 2 ? (size_t)((2 * K + 15) & ~15) : 0;
+  const size_t shmem =
+      (size_t)((((int)M * Kpad) + 15) & ~15) + raw_bytes + scratch + 16 * 4 + 16 * 4 + 4 * 8 + 4 * 4;
   if (shmem > 65536) {
     // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
     static const hipError_t attr = hipFuncSetAttribute(
@@ -701,11 +709,15 @@ hipError_t launch_deep(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t
   // (a fused token of K <= 4096 is one rotation tile, so NTILES > 1 implies K > 4096)
   if constexpr (!(ACT == 2 && NTILES > 1)) {
     if (K <= 4096) {
-      const int64_t t = (N + 15) / 16 / 256;
+      // enough tiles per workgroup that the grid fits in one workgroup per CU (at most 6)
+      const int64_t ntiles = (N + 15) / 16;
+      const int64_t t = (ntiles + 255) / 256;
       if (t <= 1) return QIFT_DEEP(1, 4);
       if (t == 2) return QIFT_DEEP(2, 4);
       if (t == 3) return QIFT_DEEP(3, 4);
-      return QIFT_DEEP(4, 4);
+      if (t == 4) return QIFT_DEEP(4, 4);
+      if (t == 5) return QIFT_DEEP(5, 4);
+      return QIFT_DEEP(6, 4);
     }
   }
   if constexpr (!(ACT == 2 && NTILES == 1)) {
