@@ -142,9 +142,11 @@ int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t 
       (acc_out && !aligned16(acc_out)) || (act_q && !aligned16(act_q)) ||
       (act_scale && !aligned16(act_scale)) || (act_sum && !aligned16(act_sum)))
     return QIFT_ERR_ALIGN;
-  return hip_status(qift::launch_linear_fused(w->fmt, w->packed, w->scales, w->N, w->K, x, b, spec.clip_num,
-                                              spec.clip_den, M, out, acc_out, act_q, act_scale, act_sum,
-                                              (hipStream_t)stream));
+  auto launch = w->fmt == QIFT_W2_MNZ ? qift::launch_fused_mnz
+               : w->fmt == QIFT_W2_POT ? qift::launch_fused_pot
+                                       : qift::launch_fused_w4;
+  return hip_status(launch(w->packed, w->scales, w->N, w->K, x, b, spec.clip_num, spec.clip_den, M, out, acc_out,
+                           act_q, act_scale, act_sum, (hipStream_t)stream));
 }
 
 size_t qift_workspace_bytes(const qift_packed_w* w, int64_t M) {

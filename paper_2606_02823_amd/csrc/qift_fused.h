@@ -1,0 +1,294 @@
+// Fused online rotation + INT4 quantization + quantized linear for decode
+// (M <= 4 tokens): y = s_w[n] s_x[m] sum_k level[n,k] q[m,k] with q, s_x
+// computed in the kernel from the fp16 tokens (Sec. 3.1 for the rotation and
+// the per-token quantizer, Sec. 3.6 for the integer dot product).
+//
+// Workgroup = 8 waves in two roles, one of each per SIMD:
+//   waves 0-3 (activation waves) load the tokens, rotate them exactly in fp64
+//     registers (qift_fwht.h), find the absmax, quantize and write the int8
+//     codes to LDS.  They synchronize only among themselves (an LDS counter),
+//     so their x loads are never queued behind weight loads and their
+//     arithmetic never waits for the weight waves;
+//   waves 4-7 (weight waves) own the T consecutive 16-row tiles of the
+//     workgroup, wave 4 + w the w-th quarter of K of each: they issue every
+//     weight load of the workgroup at once (4*T*UPT KB of W2 in flight) and
+//     then wait at one barrier for the codes, so the weight stream overlaps
+//     the whole activation phase.  Their MFMAs read the codes from LDS once
+//     per 64-k group and reuse them across the T tiles; consecutive MFMAs go
+//     to independent accumulators (T tiles, or 4 / T partial sums per tile
+//     for T < 3), so they pipeline instead of waiting on each other.
+// The four K-quarters of each tile meet in LDS and all 8 waves store one tile
+// each (4 consecutive outputs per lane, epilogue in qift_mma.h); the storing
+// lanes load their four s_w values at kernel start.
+//
+// The block exponent L of the rotation is a template parameter (LC) for the
+// block sizes in common use, which makes the transform straight-line code;
+// LC = 0 covers any other block size with L read at run time.
+//
+// Included once per weight format (qift_fused_<fmt>.hip), so the instances
+// of the three formats compile in parallel.
+#pragma once
+
+#include "qift_fwht.h"
+#include "qift_internal.h"
+#include "qift_mma.h"
+
+namespace qift {
+namespace {
+
+using namespace mma;
+
+constexpr int kXchBytes = dev::Tile<256, 16>::LDS_DOUBLES * 8;   // one exchange buffer
+
+template <int NTILES>
+constexpr int xch_count() { return NTILES > 1 ? 2 : 1; }
+
+// LDS bytes after the codes: exchange buffers, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, counter.
+template <int NTILES>
+constexpr int tail_bytes() { return xch_count<NTILES>() * kXchBytes + 64 + 128 + 64 + 16; }
+
+template <int FMT, int NTILES, int T, int UPT, int LC>
+__global__ __launch_bounds__(512) void k_fused_decode(
+    const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
+    const uint16_t* __restrict__ x, int L, int num, int den, double denom,
+    int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
+    int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+  constexpr int NH = FMT == FMT_W4 ? 2 : 1;
+  constexpr int NA = T >= 3 ? 1 : 4 / T;   // accumulators per tile
+  static_assert(4 * T * 64 * 16 <= kXchBytes, "reduction scratch aliases the first exchange buffer");
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: role branches stay scalar
+  const int r16 = lane & 15, g = lane >> 4;
+
+  const int act_bytes = (M * Kpad + 15) & ~15;
+  int8_t* act_l = reinterpret_cast<int8_t*>(smem);
+  double* xch0 = reinterpret_cast<double*>(smem + act_bytes);
+  double* xch1 = xch0 + (xch_count<NTILES>() - 1) * (kXchBytes / 8);
+  unsigned char* tl = smem + act_bytes + xch_count<NTILES>() * kXchBytes;
+  float* s_scale = reinterpret_cast<float*>(tl);
+  double* red_d = reinterpret_cast<double*>(tl + 64);
+  int* red_i = reinterpret_cast<int*>(tl + 64 + 128);
+  unsigned* ctr = reinterpret_cast<unsigned*>(tl + 64 + 128 + 64);
+
+  if (tid == 0) *ctr = 0u;
+  __syncthreads();   // nothing is in flight yet: this costs only the launch skew of the waves
+
+  const int tile0 = blockIdx.x * T;
+  const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
+  const int NC = (K + 1023) >> 10;          // 256-k units per quarter of K
+  const int wq = wave - 4;                  // quarter of K of a weight wave
+  const int kq0 = wq * NC * 256;
+  const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
+  uint32_t rowoff[T];
+  bool rowok[T];
+#pragma unroll
+  for (int j = 0; j < T; ++j) {
+    const int n = (tile0 + j) * 16 + r16;
+    rowok[j] = n < N;
+    rowoff[j] = (uint32_t)(n * rowbytes);
+  }
+  uint4 w[T][UPT][NH];
+  auto load_batch = [&](int b) {   // in the order the MFMAs consume them (unit-major)
+#pragma unroll
+    for (int u = 0; u < UPT; ++u)
+#pragma unroll
+      for (int j = 0; j < T; ++j) {
+        const int uu = b * UPT + u;
+        const int k0 = kq0 + (uu << 8) + (g << 6);
+        const bool ok = rowok[j] && uu < NC && k0 < K;
+        const uint32_t off = ok ? rowoff[j] + (uint32_t)(FMT == FMT_W4 ? k0 / 2 : k0 / 4) : dev::kOutOfRange;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) w[j][u][h] = dev::bload16(wrs, off + 16 * h);
+      }
+  };
+  // s_w of the 4 outputs this lane stores (wave j stores tile j)
+  const int n_st = (tile0 + wave) * 16 + 4 * g;
+  const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(sw, (uint32_t)(N * 2));
+  uint2 swq = make_uint2(0u, 0u);
+
+  if (wave < 4) {
+    // ---- activation waves: rotate and quantize every token into LDS
+    dev::GroupSync<4> sync{ctr, 0u};
+    dev::TokenRaw<NTILES> raw;
+    dev::load_token_raw<256, NTILES>(raw, x, K);
+    swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
+    for (int m = 0; m < M; ++m) {
+      dev::TokenRaw<NTILES> cur = raw;
+      if constexpr (NTILES <= 2) {
+        if (m + 1 < M) dev::load_token_raw<256, NTILES>(raw, x + (int64_t)(m + 1) * K, K);   // next token in flight
+      } else {
+        if (m > 0) dev::load_token_raw<256, NTILES>(cur, x + (int64_t)m * K, K);
+      }
+      const double A = dev::quant_token_group<NTILES, LC>(cur, K, L, num, den, xch0, xch1, red_d + 4 * m,
+                                                          red_i + 4 * m, sync, act_l + m * Kpad);
+      if (tid == 0) s_scale[m] = (float)((A * (double)num) / denom);
+    }
+  } else {
+    // ---- weight waves: the first batch of weights (zeros for rows past N and k past K)
+    swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
+    load_batch(0);
+  }
+  dev::lds_barrier();   // codes, scales and partial sums are in LDS; weight loads stay in flight
+
+  v4i acc[T][NA];
+#pragma unroll
+  for (int j = 0; j < T; ++j)
+#pragma unroll
+    for (int a = 0; a < NA; ++a) acc[j][a] = v4i{0, 0, 0, 0};
+  if (wave >= 4) {
+    const int m = r16;
+    const bool mok = m < M;
+    const int8_t* arow = act_l + (mok ? m : 0) * Kpad;   // lanes of absent tokens read row 0, then zero it
+    for (int b = 0; b * UPT < NC; ++b) {
+      if (b > 0) load_batch(b);
+#pragma unroll
+      for (int u = 0; u < UPT; ++u) {
+        const int uu = b * UPT + u;
+        const int kb = kq0 + (uu << 8);
+        if (uu >= NC || kb >= K) break;     // wave-uniform
+        const int k0 = kb + (g << 6);
+        const bool ok = mok && k0 < K;
+        const int8_t* bp = arow + (k0 < K ? k0 : 0);
+        v4i bq[4];
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+          const uint4 bb = *reinterpret_cast<const uint4*>(bp + 16 * s2);
+          bq[s2] = ok ? v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w} : v4i{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+          for (int j = 0; j < T; ++j)
+            acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), bq[s2], acc[j][s2 % NA]);
+      }
+    }
+  } else if (blockIdx.x == 0 && act_q_out) {
+    // the codes of the first workgroup double as the stand-alone quantizer's outputs
+    const int per_row = K >> 4;
+    for (int i = tid; i < M * per_row; i += 256) {
+      const int m = i / per_row, j = i - m * per_row;
+      *reinterpret_cast<uint4*>(act_q_out + (int64_t)m * K + 16 * j) =
+          *reinterpret_cast<const uint4*>(act_l + m * Kpad + 16 * j);
+    }
+    if (tid < M) {
+      scale_out[tid] = s_scale[tid];
+      sum_out[tid] = red_i[4 * tid] + red_i[4 * tid + 1] + red_i[4 * tid + 2] + red_i[4 * tid + 3];
+    }
+  }
+
+  // quarters of each tile meet in LDS (the exchange buffers are free again)
+  v4i* red = reinterpret_cast<v4i*>(xch0);
+  if (wave >= 4) {
+#pragma unroll
+    for (int j = 0; j < T; ++j) {
+      v4i s = acc[j][0];
+#pragma unroll
+      for (int a = 1; a < NA; ++a) s += acc[j][a];
+      red[(j * 4 + wq) * 64 + lane] = s;
+    }
+  }
+  __syncthreads();
+  if (wave < T) {
+    const int j = wave;
+    v4i D = red[(j * 4) * 64 + lane];
+#pragma unroll
+    for (int q = 1; q < 4; ++q) D += red[(j * 4 + q) * 64 + lane];
+    const int m = r16;
+    if (m < M && n_st < N) {
+      const int sq = red_i[4 * m] + red_i[4 * m + 1] + red_i[4 * m + 2] + red_i[4 * m + 3];
+      store4_sw<FMT>(D, m, n_st, N, s_scale[m], sq, swq, y, acc_out);
+    }
+  }
+}
+
+inline int kpad_of(int64_t K) { return (int)K + 16; }
+
+template <int FMT, int NTILES, int T, int UPT, int LC>
+hipError_t launch_t(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
+                    int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
+                    int32_t* acc_out, hipStream_t s) {
+  const int Kpad = kpad_of(K);
+  const int ntiles = (int)((N + 15) / 16);
+  const int grid = (ntiles + T - 1) / T;
+  const size_t shmem = (size_t)((((int)M * Kpad) + 15) & ~15) + tail_bytes<NTILES>();
+  if (shmem > 65536) {
+    // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&k_fused_decode<FMT, NTILES, T, UPT, LC>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (attr != hipSuccess) return attr;
+  }
+  hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, UPT, LC>), dim3(grid), dim3(512), shmem, s, P, sw, (int)N,
+                     (int)K, x, L, num, den, denom, aq, sc, sm, (int)M, Kpad, y, acc_out);
+  return hipGetLastError();
+}
+
+// Block exponents compiled as constants: 12 and 8 for tokens of one rotation
+// tile (K <= 4096), 12, 11 and 6 for longer tokens; anything else at run time.
+template <int FMT, int NTILES, int T, int UPT>
+hipError_t launch_l(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
+                    int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
+                    int32_t* acc_out, hipStream_t s) {
+#define QIFT_FUSED_L(LL) \
+  launch_t<FMT, NTILES, T, UPT, LL>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
+  if constexpr (NTILES == 1) {
+    if (L == 12) return QIFT_FUSED_L(12);
+    if (L == 8) return QIFT_FUSED_L(8);
+  } else {
+    if (L == 12) return QIFT_FUSED_L(12);
+    if (L == 11) return QIFT_FUSED_L(11);
+    if (L == 6) return QIFT_FUSED_L(6);
+  }
+  return QIFT_FUSED_L(0);
+#undef QIFT_FUSED_L
+}
+
+// K <= 4096 (one rotation tile): 4 units of 256 k per weight wave and tile, and as many tiles
+// per workgroup as keep the grid within one workgroup per CU (at most 6; W4, whose units take
+// twice the registers, at most 3).  Longer K: one tile per workgroup, up to 16 (W4: 8) units
+// per batch.
+template <int FMT, int NTILES>
+hipError_t launch_nt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
+                     int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
+                     int32_t* acc_out, hipStream_t s) {
+#define QIFT_FUSED(TT, UU) \
+  launch_l<FMT, NTILES, TT, UU>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
+  if constexpr (NTILES == 1) {
+    const int64_t ntiles = (N + 15) / 16;
+    int64_t t = (ntiles + 255) / 256;
+    if (FMT == FMT_W4 && t > 3) t = 3;
+    if (t <= 1) return QIFT_FUSED(1, 4);
+    if (t == 2) return QIFT_FUSED(2, 4);
+    if (t == 3) return QIFT_FUSED(3, 4);
+    if constexpr (FMT != FMT_W4) {
+      if (t == 4) return QIFT_FUSED(4, 4);
+      if (t == 5) return QIFT_FUSED(5, 4);
+      return QIFT_FUSED(6, 4);
+    }
+    return hipErrorInvalidValue;
+  } else {
+    if constexpr (FMT == FMT_W4) return QIFT_FUSED(1, 8);
+    else return QIFT_FUSED(1, 16);
+  }
+#undef QIFT_FUSED
+}
+
+template <int FMT>
+hipError_t launch_fused_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x,
+                            int block, int num, int den, int64_t M, uint16_t* y, int32_t* acc_out, int8_t* aq,
+                            float* sc, int32_t* sm, hipStream_t s) {
+  if (M < 1 || M > kFusedMaxM || K > kFusedMaxK || block > kFusedMaxBlock) return hipErrorInvalidValue;
+  const int L = dev::ilog2c(block);
+  const double denom = act_denominator(block, den);
+  switch ((K + 4095) / 4096) {
+    case 1: return launch_nt<FMT, 1>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    case 2: return launch_nt<FMT, 2>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    case 3: return launch_nt<FMT, 3>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    case 4: return launch_nt<FMT, 4>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+}  // namespace qift

@@ -39,6 +39,11 @@ __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off)
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
+__device__ __forceinline__ uint2 bload8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  return make_uint2(v[0], v[1]);
+}
+
 template <int NT, int E>
 struct Tile {
   static constexpr int EB = ilog2c(E);
@@ -107,8 +112,43 @@ __device__ __forceinline__ void lds_load_w(const double* lds, double (&v)[16], i
 // layout on exit; otherwise they stay in the last window used, which is
 // returned (0, 4, 8 or 9) so the caller can address elements with
 // win_elem/win_step.  All NT threads must call it.
-template <int NT, int E, bool NATURAL>
-__device__ __forceinline__ int fwht_tile(double (&v)[E], double* lds, int t, int L) {
+struct BlockSync {
+  __device__ void operator()() const { __syncthreads(); }
+};
+
+// Barrier among the first NW waves of a workgroup that leaves its other waves
+// running: lane 0 of each wave bumps a counter in LDS once the wave's LDS
+// accesses have completed, and the wave spins until the counter reaches the
+// next multiple of NW.  The counter is zeroed once before first use (under a
+// full workgroup barrier) and never reset.  All NW waves make the same
+// sequence of calls, so every wait ends; the spin is bounded all the same.
+template <int NW>
+struct GroupSync {
+  unsigned* ctr;
+  unsigned target;
+  __device__ void operator()() {
+    target += NW;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    for (int spin = 0; spin < (1 << 22); ++spin) {
+      const unsigned c = __builtin_amdgcn_readfirstlane(
+          __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+      if (c >= target) break;
+    }
+    asm volatile("" ::: "memory");
+  }
+};
+
+// Workgroup barrier that waits only for this wave's LDS accesses (not for its
+// outstanding global loads, which a plain __syncthreads would also drain).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int NT, int E, bool NATURAL, typename Sync>
+__device__ __forceinline__ int fwht_tile_s(double (&v)[E], double* lds, int t, int L, Sync& sync) {
   static_assert(E == 16, "16 elements per thread");
   using S = Tile<NT, E>;
   static_assert(S::TB == 12 || S::TB == 13, "tile of 4096 or 8192");
@@ -116,20 +156,20 @@ __device__ __forceinline__ int fwht_tile(double (&v)[E], double* lds, int t, int
   if (L <= 4) return 0;
   int w = 4;
   lds_store_w<0>(lds, v, t);
-  __syncthreads();
+  sync();
   lds_load_w<4>(lds, v, t);
   reg_stages<E>(v, 0, (L < 8 ? L : 8) - 4);
   if (L > 8) {
     // a thread's window-4 slots were read only by itself, so it may overwrite them at once
     lds_store_w<4>(lds, v, t);
-    __syncthreads();
+    sync();
     lds_load_w<8>(lds, v, t);
     reg_stages<E>(v, 0, (L < 12 ? L : 12) - 8);
     w = 8;
     if constexpr (S::TB == 13) {
       if (L > 12) {
         lds_store_w<8>(lds, v, t);
-        __syncthreads();
+        sync();
         lds_load_w<9>(lds, v, t);
         reg_stages<E>(v, 3, 4);   // register bit 3 of window 9 is index bit 12
         w = 9;
@@ -140,11 +180,17 @@ __device__ __forceinline__ int fwht_tile(double (&v)[E], double* lds, int t, int
     if (w == 4) lds_store_w<4>(lds, v, t);
     else if (w == 8) lds_store_w<8>(lds, v, t);
     else lds_store_w<9>(lds, v, t);
-    __syncthreads();
+    sync();
     lds_load_w<0>(lds, v, t);
     return 0;
   }
   return w;
+}
+
+template <int NT, int E, bool NATURAL>
+__device__ __forceinline__ int fwht_tile(double (&v)[E], double* lds, int t, int L) {
+  BlockSync sync;
+  return fwht_tile_s<NT, E, NATURAL>(v, lds, t, L, sync);
 }
 
 // Per-token rounding constants: q = sign(X) min(7, rne(7 den |X| / (num A))).
@@ -409,6 +455,65 @@ __device__ __forceinline__ void quant_token_staged(const uint16_t* raw_l, int64_
   }
   sum_q = block_sum<NT>(qs, red_i);
   scale = (float)((A * (double)num) / denom);
+}
+
+// Rotate + quantize one token held in registers by the 256 threads of the
+// first four waves of a workgroup, synchronizing only those waves (sync), so
+// that other waves of the workgroup keep running.  Every tile is transformed
+// once and stays in registers until the absmax is known; tiles alternate
+// between two exchange buffers (xch0, xch1), so a tile's first exchange never
+// overwrites slots a slower wave still reads from the tile before (the
+// exchange of the tile in between orders them).  Codes go to dst (16-byte
+// aligned) bytewise in the layout the transform ends in; elements past K are
+// skipped.  Returns A = max |X|; each wave's sum of codes lands in red_i[wave]
+// (red_d holds 4 doubles).  LC > 0 fixes the block exponent L = LC at compile
+// time (every butterfly stage and exchange is then straight-line code); LC = 0
+// takes L at run time.
+template <int NTILES, int LC, typename Sync>
+__device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw, int64_t K, int L_rt, int num,
+                                                    int den, double* xch0, double* xch1, double* red_d,
+                                                    int* red_i, Sync& sync, int8_t* dst) {
+  using S = Tile<256, 16>;
+  const int L = LC > 0 ? LC : L_rt;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  double v[NTILES][16];
+  double amax = 0.0;
+  int wend = 0;
+#pragma unroll
+  for (int tau = 0; tau < NTILES; ++tau) {
+    unpack_fp16(v[tau], raw.d[tau]);
+    wend = fwht_tile_s<256, 16, false>(v[tau], (tau & 1) ? xch1 : xch0, t, L, sync);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[tau][e]));
+  }
+  amax = wave_max(amax);
+  if (lane == 0) red_d[wave] = amax;
+  sync();
+  const double A = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
+  const QuantParams p = make_qparams(A, num, den);
+  int qs = 0;
+#pragma unroll
+  for (int tau = 0; tau < NTILES; ++tau) {
+    int q[16];
+    quant16(v[tau], p, q);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) qs += q[e];
+    int8_t* tile_dst = dst + tau * S::T;
+    if ((int64_t)(tau + 1) * S::T <= K) {
+      if (wend == 0) store_codes<0>(tile_dst, q, t);
+      else if (wend == 4) store_codes<4>(tile_dst, q, t);
+      else store_codes<8>(tile_dst, q, t);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int i = wend == 0 ? 16 * t + e : wend == 4 ? win_elem<4>(t) + (e << 4) : win_elem<8>(t) + (e << 8);
+        if ((int64_t)tau * S::T + i < K) tile_dst[i] = (int8_t)q[e];
+      }
+    }
+  }
+  qs = wave_sum(qs);
+  if (lane == 0) red_i[wave] = qs;
+  return A;
 }
 
 template <int NT, int NTILES>

@@ -23,11 +23,16 @@ hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
                          uint16_t* out, int32_t* acc_out, hipStream_t s);
 
-// Fused rotation + quantization + linear for a few decode tokens (qift_linear.hip).
-hipError_t launch_linear_fused(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
-                               const uint16_t* x, int block, int clip_num, int clip_den, int64_t M,
-                               uint16_t* out, int32_t* acc_out, int8_t* act_q, float* act_scale,
-                               int32_t* act_sum, hipStream_t s);
+// Fused rotation + quantization + linear for a few decode tokens, one launcher
+// per weight format (qift_fused_<fmt>.hip).
+#define QIFT_FUSED_LAUNCHER(NAME)                                                                          \
+  hipError_t NAME(const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K, const uint16_t* x, \
+                  int block, int clip_num, int clip_den, int64_t M, uint16_t* out, int32_t* acc_out,       \
+                  int8_t* act_q, float* act_scale, int32_t* act_sum, hipStream_t s)
+QIFT_FUSED_LAUNCHER(launch_fused_mnz);
+QIFT_FUSED_LAUNCHER(launch_fused_pot);
+QIFT_FUSED_LAUNCHER(launch_fused_w4);
+#undef QIFT_FUSED_LAUNCHER
 
 // (den * 7) * sqrt(b): the fixed divisor of the per-token activation scale.
 double act_denominator(int block, int clip_den);
