@@ -15,8 +15,10 @@
 //     then wait at one barrier for the codes, so the weight stream overlaps
 //     the whole activation phase.  Their MFMAs read the codes from LDS once
 //     per 64-k group and reuse them across the T tiles; consecutive MFMAs go
-//     to independent accumulators (T tiles, or 4 / T partial sums per tile
-//     for T < 3), so they pipeline instead of waiting on each other.
+//     to independent accumulators, so they pipeline instead of waiting on
+//     each other.  MNZ weights are decoded by bit plane (one AND per packed
+//     word and plane, qift_mma.h), with the codes stored in the matching
+//     planar order in LDS and one accumulator per plane.
 // The four K-quarters of each tile meet in LDS and all 8 waves store one tile
 // each (4 consecutive outputs per lane, epilogue in qift_mma.h); the storing
 // lanes load their four s_w values at kernel start.
@@ -43,9 +45,10 @@ constexpr int kXchBytes = dev::Tile<256, 16>::LDS_DOUBLES * 8;   // one exchange
 template <int NTILES>
 constexpr int xch_count() { return NTILES > 1 ? 2 : 1; }
 
-// LDS bytes after the codes: exchange buffers, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, counter.
+// LDS bytes after the codes: exchange buffers, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, counter,
+// and 64 zero bytes (the activation operand of k-groups past K).
 template <int NTILES>
-constexpr int tail_bytes() { return xch_count<NTILES>() * kXchBytes + 64 + 128 + 64 + 16; }
+constexpr int tail_bytes() { return xch_count<NTILES>() * kXchBytes + 64 + 128 + 64 + 16 + 64; }
 
 template <int FMT, int NTILES, int T, int UPT, int LC>
 __global__ __launch_bounds__(512) void k_fused_decode(
@@ -54,7 +57,8 @@ __global__ __launch_bounds__(512) void k_fused_decode(
     int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
     int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
-  constexpr int NA = T >= 3 ? 1 : 4 / T;   // accumulators per tile
+  constexpr bool PLANAR = FMT == FMT_MNZ;                   // plane decode, codes in planar layout
+  constexpr int NA = PLANAR ? 4 : T >= 3 ? 1 : 4 / T;     // accumulators per tile (MNZ: one per plane)
   static_assert(4 * T * 64 * 16 <= kXchBytes, "reduction scratch aliases the first exchange buffer");
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -70,8 +74,10 @@ __global__ __launch_bounds__(512) void k_fused_decode(
   double* red_d = reinterpret_cast<double*>(tl + 64);
   int* red_i = reinterpret_cast<int*>(tl + 64 + 128);
   unsigned* ctr = reinterpret_cast<unsigned*>(tl + 64 + 128 + 64);
+  int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 64 + 128 + 64 + 16);
 
   if (tid == 0) *ctr = 0u;
+  if (tid < 4) reinterpret_cast<uint4*>(zero64)[tid] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();   // nothing is in flight yet: this costs only the launch skew of the waves
 
   const int tile0 = blockIdx.x * T;
@@ -120,7 +126,7 @@ __global__ __launch_bounds__(512) void k_fused_decode(
       } else {
         if (m > 0) dev::load_token_raw<256, NTILES>(cur, x + (int64_t)m * K, K);
       }
-      const double A = dev::quant_token_group<NTILES, LC>(cur, K, L, num, den, xch0, xch1, red_d + 4 * m,
+      const double A = dev::quant_token_group<NTILES, LC, PLANAR>(cur, K, L, num, den, xch0, xch1, red_d + 4 * m,
                                                           red_i + 4 * m, sync, act_l + m * Kpad);
       if (tid == 0) s_scale[m] = (float)((A * (double)num) / denom);
     }
@@ -139,28 +145,36 @@ __global__ __launch_bounds__(512) void k_fused_decode(
   if (wave >= 4) {
     const int m = r16;
     const bool mok = m < M;
-    const int8_t* arow = act_l + (mok ? m : 0) * Kpad;   // lanes of absent tokens read row 0, then zero it
+    // lanes of absent tokens read row 0: their MFMA output columns are never stored
+    const int8_t* arow = act_l + (mok ? m : 0) * Kpad;
+    // activation operands of unit uu (k-groups past K take zero codes: a zero PoT word decodes to -4)
+    auto load_b = [&](int uu, v4i (&bq)[4]) {
+      const int k0 = kq0 + (uu << 8) + (g << 6);
+      const int8_t* bp = uu < NC && k0 < K ? arow + k0 : zero64;
+#pragma unroll
+      for (int s2 = 0; s2 < 4; ++s2) {
+        const uint4 bb = *reinterpret_cast<const uint4*>(bp + 16 * s2);
+        bq[s2] = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
+      }
+    };
     for (int b = 0; b * UPT < NC; ++b) {
       if (b > 0) load_batch(b);
+      v4i bq[2][4];   // double buffer: the next unit's operands are read during this unit's MFMAs
+      load_b(b * UPT, bq[0]);
 #pragma unroll
       for (int u = 0; u < UPT; ++u) {
         const int uu = b * UPT + u;
-        const int kb = kq0 + (uu << 8);
-        if (uu >= NC || kb >= K) break;     // wave-uniform
-        const int k0 = kb + (g << 6);
-        const bool ok = mok && k0 < K;
-        const int8_t* bp = arow + (k0 < K ? k0 : 0);
-        v4i bq[4];
-#pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2) {
-          const uint4 bb = *reinterpret_cast<const uint4*>(bp + 16 * s2);
-          bq[s2] = ok ? v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w} : v4i{0, 0, 0, 0};
-        }
+        if (uu >= NC || kq0 + (uu << 8) >= K) break;     // wave-uniform
+        if (u + 1 < UPT) load_b(uu + 1, bq[(u + 1) & 1]);
+        const v4i (&cur)[4] = bq[u & 1];
 #pragma unroll
         for (int s2 = 0; s2 < 4; ++s2)
 #pragma unroll
-          for (int j = 0; j < T; ++j)
-            acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), bq[s2], acc[j][s2 % NA]);
+          for (int j = 0; j < T; ++j) {
+            // MNZ: operand s2 is bit-plane s2 of the unit's four words; else word s2
+            if constexpr (PLANAR) acc[j][s2] = mfma_i8(decode_plane(w[j][u][0], s2), cur[s2], acc[j][s2]);
+            else acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), cur[s2], acc[j][s2 % NA]);
+          }
       }
     }
   } else if (blockIdx.x == 0 && act_q_out) {
@@ -168,8 +182,16 @@ __global__ __launch_bounds__(512) void k_fused_decode(
     const int per_row = K >> 4;
     for (int i = tid; i < M * per_row; i += 256) {
       const int m = i / per_row, j = i - m * per_row;
-      *reinterpret_cast<uint4*>(act_q_out + (int64_t)m * K + 16 * j) =
-          *reinterpret_cast<const uint4*>(act_l + m * Kpad + 16 * j);
+      uint4 c;
+      if constexpr (PLANAR) {
+        // bytes 4t..4t+3 of natural chunk j sit at 16t + 4 (j mod 4) of its 64-k chunk
+        const int8_t* src = act_l + m * Kpad + 64 * (j >> 2) + 4 * (j & 3);
+        c = make_uint4(*reinterpret_cast<const uint32_t*>(src), *reinterpret_cast<const uint32_t*>(src + 16),
+                       *reinterpret_cast<const uint32_t*>(src + 32), *reinterpret_cast<const uint32_t*>(src + 48));
+      } else {
+        c = *reinterpret_cast<const uint4*>(act_l + m * Kpad + 16 * j);
+      }
+      *reinterpret_cast<uint4*>(act_q_out + (int64_t)m * K + 16 * j) = c;
     }
     if (tid < M) {
       scale_out[tid] = s_scale[tid];
@@ -182,9 +204,14 @@ __global__ __launch_bounds__(512) void k_fused_decode(
   if (wave >= 4) {
 #pragma unroll
     for (int j = 0; j < T; ++j) {
-      v4i s = acc[j][0];
+      v4i s;
+      if constexpr (PLANAR) {
+        s = combine_planes(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+      } else {
+        s = acc[j][0];
 #pragma unroll
-      for (int a = 1; a < NA; ++a) s += acc[j][a];
+        for (int a = 1; a < NA; ++a) s += acc[j][a];
+      }
       red[(j * 4 + wq) * 64 + lane] = s;
     }
   }

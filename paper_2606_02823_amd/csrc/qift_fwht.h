@@ -73,6 +73,24 @@ __device__ __forceinline__ void reg_stages(double (&v)[E], int r_lo, int r_hi) {
   }
 }
 
+// Butterflies on lane bit B (B = 0, 1) of the natural layout, i.e. on index
+// bit 4 + B: the partner value comes from lane ^ (1 << B) of the same quad by
+// a DPP move, and sum / difference become one exact fma with a sign that
+// depends on the lane: self + partner, or partner - self for the upper lane.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  return __hiloint2double(__builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, 0xf, 0xf, false),
+                          __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xf, 0xf, false));
+}
+
+template <int B, int E>
+__device__ __forceinline__ void lane_stage(double (&v)[E]) {
+  constexpr int CTRL = B == 0 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] / [2,3,0,1]
+  const double sgn = ((threadIdx.x >> B) & 1) ? -1.0 : 1.0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) v[e] = fma(v[e], sgn, dpp_f64<CTRL>(v[e]));
+}
+
 // Window W: register e of thread t holds tile element
 //   i = (t & (2^W - 1)) | (e << W) | ((t >> W) << (W + 4)),
 // i.e. index bits [W, W + 4) are in registers (W = 0 is the natural layout,
@@ -154,6 +172,12 @@ __device__ __forceinline__ int fwht_tile_s(double (&v)[E], double* lds, int t, i
   static_assert(S::TB == 12 || S::TB == 13, "tile of 4096 or 8192");
   reg_stages<E>(v, 0, L < 4 ? L : 4);
   if (L <= 4) return 0;
+  if (L <= 6) {
+    // index bits 4 and 5 are lane bits 0 and 1: quad DPP, no exchange, natural layout throughout
+    lane_stage<0>(v);
+    if (L == 6) lane_stage<1>(v);
+    return 0;
+  }
   int w = 4;
   lds_store_w<0>(lds, v, t);
   sync();
@@ -238,9 +262,13 @@ __device__ __forceinline__ void quant16(const double (&v)[16], const QuantParams
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const double vv = fabs(v[e]) * p.c1;   // c1 = 0 when A = 0, giving q = 0
-    const double r = rint(vv);
+    // vv + 1.5 * 2^52 rounds vv to the nearest integer (ties to even) into the low word, since
+    // 0 <= vv < 2^31; subtracting the constant again gives that integer as a double, exactly
+    const double tt = vv + 0x1.8p52;
+    const double r = tt - 0x1.8p52;
     near |= fabs(vv - r) > 0.5 - 1e-9;
-    const int qq = (int)fmin(r, 7.0);
+    const int ri = __double2loint(tt);
+    const int qq = ri < 7 ? ri : 7;
     q[e] = v[e] < 0.0 ? -qq : qq;
   }
   if (__any(near)) {
@@ -390,11 +418,38 @@ __device__ __forceinline__ void quant_token_raw(const TokenRaw<NTILES>& raw, int
 // single tile is transformed once).  Values are quantized in the layout the
 // transform ends in and the codes scattered bytewise, which saves the
 // exchange back to the natural layout.  All NT threads must call it.
-template <int W>
+// Byte position of code k in LDS.  Natural: k.  Planar (PLANAR = true): inside
+// each 64-k chunk, k = 16i + 4t + b goes to 16t + 4i + b, so that the 16 codes
+// {16i + 4t + b : i, b} that meet bit-plane t of four consecutive packed W2
+// words in one MFMA are 16 contiguous bytes (qift_mma.h).
+template <bool PLANAR>
+__device__ __forceinline__ int code_pos(int k) {
+  if constexpr (PLANAR) return (k & ~63) | ((k & 0x0C) << 2) | ((k & 0x30) >> 2) | (k & 3);
+  else return k;
+}
+
+template <int W, bool PLANAR = false>
 __device__ __forceinline__ void store_codes(int8_t* dst, const int (&q)[16], int t) {
-  int8_t* d = dst + win_elem<W>(t);
+  if constexpr (W == 0) {
+    // natural layout: the thread's 16 codes are k = 16t .. 16t + 15, i.e. four packed words
+    uint32_t wd[4];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) d[e * (W == 0 ? 1 : (1 << W))] = (int8_t)q[e];
+    for (int a = 0; a < 4; ++a)
+      wd[a] = ((uint32_t)q[4 * a] & 0xFFu) | (((uint32_t)q[4 * a + 1] & 0xFFu) << 8) |
+              (((uint32_t)q[4 * a + 2] & 0xFFu) << 16) | ((uint32_t)q[4 * a + 3] << 24);
+    if constexpr (PLANAR) {
+      // word a (k = 16t + 4a + b) goes to 16a + 4 (t mod 4) + b of the 64-k chunk t / 4
+      int8_t* d = dst + 64 * (t >> 2) + 4 * (t & 3);
+#pragma unroll
+      for (int a = 0; a < 4; ++a) *reinterpret_cast<uint32_t*>(d + 16 * a) = wd[a];
+    } else {
+      *reinterpret_cast<uint4*>(dst + 16 * t) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+    }
+  } else {
+    const int base = win_elem<W>(t);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dst[code_pos<PLANAR>(base + e * (1 << W))] = (int8_t)q[e];
+  }
 }
 
 template <int NT>
@@ -464,12 +519,12 @@ __device__ __forceinline__ void quant_token_staged(const uint16_t* raw_l, int64_
 // between two exchange buffers (xch0, xch1), so a tile's first exchange never
 // overwrites slots a slower wave still reads from the tile before (the
 // exchange of the tile in between orders them).  Codes go to dst (16-byte
-// aligned) bytewise in the layout the transform ends in; elements past K are
-// skipped.  Returns A = max |X|; each wave's sum of codes lands in red_i[wave]
+// aligned) bytewise from the layout the transform ends in, at code_pos<PLANAR>;
+// elements past K are skipped.  Returns A = max |X|; each wave's sum of codes lands in red_i[wave]
 // (red_d holds 4 doubles).  LC > 0 fixes the block exponent L = LC at compile
 // time (every butterfly stage and exchange is then straight-line code); LC = 0
 // takes L at run time.
-template <int NTILES, int LC, typename Sync>
+template <int NTILES, int LC, bool PLANAR, typename Sync>
 __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw, int64_t K, int L_rt, int num,
                                                     int den, double* xch0, double* xch1, double* red_d,
                                                     int* red_i, Sync& sync, int8_t* dst) {
@@ -500,14 +555,17 @@ __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw,
     for (int e = 0; e < 16; ++e) qs += q[e];
     int8_t* tile_dst = dst + tau * S::T;
     if ((int64_t)(tau + 1) * S::T <= K) {
-      if (wend == 0) store_codes<0>(tile_dst, q, t);
-      else if (wend == 4) store_codes<4>(tile_dst, q, t);
-      else store_codes<8>(tile_dst, q, t);
+      if (wend == 0) store_codes<0, PLANAR>(tile_dst, q, t);
+      else if (wend == 4) store_codes<4, PLANAR>(tile_dst, q, t);
+      else store_codes<8, PLANAR>(tile_dst, q, t);
+    } else if (wend == 0) {
+      // K is a multiple of 64: a thread's 16 consecutive elements are all in or all past K
+      if ((int64_t)tau * S::T + 16 * t < K) store_codes<0, PLANAR>(tile_dst, q, t);
     } else {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int i = wend == 0 ? 16 * t + e : wend == 4 ? win_elem<4>(t) + (e << 4) : win_elem<8>(t) + (e << 8);
-        if ((int64_t)tau * S::T + i < K) tile_dst[i] = (int8_t)q[e];
+        const int i = wend == 4 ? win_elem<4>(t) + (e << 4) : win_elem<8>(t) + (e << 8);
+        if ((int64_t)tau * S::T + i < K) tile_dst[code_pos<PLANAR>(i)] = (int8_t)q[e];
       }
     }
   }

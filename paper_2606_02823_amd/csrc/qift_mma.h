@@ -87,6 +87,29 @@ __device__ __forceinline__ v4i decode_unit(const uint4 (&u)[FMT == FMT_W4 ? 2 : 
   }
 }
 
+// Bit-plane decode of a lane's four packed MNZ words (u.x .. u.w, 64 weights):
+// operand t takes the 2-bit field t of every byte of the four words, i.e. the
+// codes of k = 16i + 4t + b (word i, byte b), left in place (scaled by 4^t)
+// for t < 3, which costs one AND per word, and shifted down for t = 3.  With
+// the codes of the same k as B operand (the planar code layout) and one
+// accumulator per plane, the unit's code dot product is
+//     D = acc0 + acc1 / 4 + acc2 / 16 + acc3,
+// where every division is exact (acc_t is 4^t times an integer sum).
+__device__ __forceinline__ v4i decode_plane(const uint4& u, int t) {
+  if (t == 3)
+    return v4i{(int)((u.x >> 6) & 0x03030303u), (int)((u.y >> 6) & 0x03030303u),
+               (int)((u.z >> 6) & 0x03030303u), (int)((u.w >> 6) & 0x03030303u)};
+  const uint32_t mk = 0x03030303u << (2 * t);
+  return v4i{(int)(u.x & mk), (int)(u.y & mk), (int)(u.z & mk), (int)(u.w & mk)};
+}
+
+__device__ __forceinline__ v4i combine_planes(const v4i& a0, const v4i& a1, const v4i& a2, const v4i& a3) {
+  v4i d;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) d[r] = a0[r] + (a1[r] >> 2) + (a2[r] >> 4) + a3[r];
+  return d;
+}
+
 template <int FMT>
 __device__ __forceinline__ int finish_acc(int D, int sum_q) {
   if constexpr (FMT == FMT_MNZ) return 2 * D - 3 * sum_q;
