@@ -6,10 +6,12 @@ Decode (the headline ``value``): LLaMA-2-7B-shaped layers (q,k,v,o 4096x4096;
 gate,up 11008x4096; down 4096x11008 with 172 Hadamard blocks of 64), MNZ
 2-bit weights, M = 1 token.  A step pushes one token through 32 distinct
 seeded layers (1.62 GB of packed words, the depth of LLaMA-2-7B) so that the
-weights stream from HBM rather than the 256 MB Infinity Cache.  Per layer:
-4 x rotate_quant_act (inputs of q|k|v, o, gate|up, down) and 4 linears
-(q|k|v and gate|up stacked along N since they share their input).  The step
-is captured once as a hipGraph and replayed.
+weights stream from HBM rather than the 256 MB Infinity Cache.  Per layer: 4
+rotate_quant_linear launches (q|k|v, o, gate|up, down; q|k|v and gate|up are
+stacked along N since they share their input), each rotating and quantizing
+its fp16 input inside the kernel; with --unfused, 4 rotate_quant_act + 4
+w2a4_linear launches instead.  The step is captured once as a hipGraph and
+replayed.
 ``value`` = packed-weight bytes per step / step time (GB/s).
 
 Prefill (reported under "prefill"): LLaMA-3.1-8B-shaped layers at M = 2048,
@@ -33,7 +35,7 @@ sys.path.insert(0, ROOT)
 METRIC = "W2A4 linear packed-weight GB/s (% HBM peak) at M=1; int8 TOPS at M=2048"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS
-DECODE_KERNEL_FUSED = "k_decode_deep<0, 2, *, *>"   # MNZ decode kernel with the fused rotation
+DECODE_KERNEL_FUSED = "k_fused_decode<0, *, *, *, *>"   # MNZ decode kernel with the fused rotation
 DECODE_KERNEL = "k_decode_deep<0, 1, 1, *>"          # MNZ decode kernel on staged act_q
 
 
@@ -51,7 +53,7 @@ def _traffic_record():
 
     Returns None unless the summary was taken on the current kernel sources.
     """
-    path = os.path.join(ROOT, "profiles", "decode_linear_cfg1_m1_traffic.json")
+    path = os.path.join(ROOT, "profiles", "decode_fused_cfg1_m1_traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f)
