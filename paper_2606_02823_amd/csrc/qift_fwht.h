@@ -8,9 +8,10 @@
 //
 // Layout: a tile of T = NT * E elements; thread t holds E consecutive elements
 // (natural layout, element 16t+e for E = 16).  The butterflies on the EB index
-// bits held in registers run in registers; the next EB index bits are brought
-// into registers by an exchange through LDS (two spare doubles after every 16
-// to spread the banks).
+// bits held in registers run in registers; blocks of up to 64 finish with two
+// quad-DPP stages on lane bits 0 and 1; larger blocks bring the next EB index
+// bits into registers by an exchange through LDS (two spare doubles after
+// every 16 to spread the banks).
 #pragma once
 
 #include <hip/hip_fp16.h>
@@ -410,14 +411,6 @@ __device__ __forceinline__ void quant_token_raw(const TokenRaw<NTILES>& raw, int
   scale = (float)((A * (double)num) / denom);
 }
 
-// Rotate + quantize one token whose raw fp16 bits are staged in LDS (raw_l,
-// K halves, 16-byte aligned), writing int8 codes to LDS (dst).  The tile loops
-// are rolled so that the code is one compact tile body executed from the
-// instruction cache: pass 1 transforms every tile and keeps the running
-// absmax; pass 2 transforms each tile again and quantizes it (a token of a
-// single tile is transformed once).  Values are quantized in the layout the
-// transform ends in and the codes scattered bytewise, which saves the
-// exchange back to the natural layout.  All NT threads must call it.
 // Byte position of code k in LDS.  Natural: k.  Planar (PLANAR = true): inside
 // each 64-k chunk, k = 16i + 4t + b goes to 16t + 4i + b, so that the 16 codes
 // {16i + 4t + b : i, b} that meet bit-plane t of four consecutive packed W2
@@ -452,66 +445,6 @@ __device__ __forceinline__ void store_codes(int8_t* dst, const int (&q)[16], int
   }
 }
 
-template <int NT>
-__device__ __forceinline__ void quant_token_staged(const uint16_t* raw_l, int64_t K, int L, int num, int den,
-                                                   double denom, double* xch, double* red_d, int* red_i,
-                                                   int8_t* dst, int& sum_q, float& scale) {
-  using S = Tile<NT, 16>;
-  const int t = threadIdx.x;
-  const int ntiles = (int)((K + S::T - 1) / S::T);
-  double v[16];
-  auto load_tile = [&](int tau) {
-    const int64_t base = (int64_t)tau * S::T + 16 * t;
-    uint4 d[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
-    if (base < K) {
-      d[0] = *reinterpret_cast<const uint4*>(raw_l + base);
-      d[1] = *reinterpret_cast<const uint4*>(raw_l + base + 8);
-    }
-    unpack_fp16(v, d);
-  };
-  double amax = 0.0;
-  int wend = 0;
-#pragma unroll 1
-  for (int tau = 0; tau < ntiles; ++tau) {
-    load_tile(tau);
-    wend = fwht_tile<NT, 16, false>(v, xch, t, L);
-#pragma unroll
-    for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
-    if (tau + 1 < ntiles) __syncthreads();   // the exchange buffer is reused by the next tile
-  }
-  const double A = block_max<NT>(amax, red_d);
-  const QuantParams p = make_qparams(A, num, den);
-  int qs = 0;
-#pragma unroll 1
-  for (int tau = 0; tau < ntiles; ++tau) {
-    if (ntiles > 1) {
-      __syncthreads();
-      load_tile(tau);
-      fwht_tile<NT, 16, false>(v, xch, t, L);
-    }
-    int q[16];
-    quant16(v, p, q);
-#pragma unroll
-    for (int e = 0; e < 16; ++e) qs += q[e];
-    // elements past K belong to whole blocks past K and to the padding of dst: skipped
-    int8_t* tile_dst = dst + (int64_t)tau * S::T;
-    const bool whole = (int64_t)(tau + 1) * S::T <= K;
-    if (whole) {
-      if (wend == 0) store_codes<0>(tile_dst, q, t);
-      else if (wend == 4) store_codes<4>(tile_dst, q, t);
-      else store_codes<8>(tile_dst, q, t);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int i = wend == 0 ? 16 * t + e : wend == 4 ? win_elem<4>(t) + (e << 4) : win_elem<8>(t) + (e << 8);
-        if ((int64_t)tau * S::T + i < K) tile_dst[i] = (int8_t)q[e];
-      }
-    }
-  }
-  sum_q = block_sum<NT>(qs, red_i);
-  scale = (float)((A * (double)num) / denom);
-}
-
 // Rotate + quantize one token held in registers by the 256 threads of the
 // first four waves of a workgroup, synchronizing only those waves (sync), so
 // that other waves of the workgroup keep running.  Every tile is transformed
@@ -520,8 +453,8 @@ __device__ __forceinline__ void quant_token_staged(const uint16_t* raw_l, int64_
 // overwrites slots a slower wave still reads from the tile before (the
 // exchange of the tile in between orders them).  Codes go to dst (16-byte
 // aligned) bytewise from the layout the transform ends in, at code_pos<PLANAR>;
-// elements past K are skipped.  Returns A = max |X|; each wave's sum of codes lands in red_i[wave]
-// (red_d holds 4 doubles).  LC > 0 fixes the block exponent L = LC at compile
+// elements past K are skipped.  Returns A = max |X|; each wave's sum of codes
+// lands in red_i[wave] (red_d holds 4 doubles).  LC > 0 fixes the block exponent L = LC at compile
 // time (every butterfly stage and exchange is then straight-line code); LC = 0
 // takes L at run time.
 template <int NTILES, int LC, bool PLANAR, typename Sync>

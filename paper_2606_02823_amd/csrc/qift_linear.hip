@@ -1,7 +1,7 @@
 // Quantized linear kernels on int8 MFMA (operand layout and decoding:
 // qift_mma.h): the decode kernels for up to 16 tokens and the tiled prefill
 // GEMM.
-#include "qift_fwht.h"
+#include "qift_fwht.h"   // buffer-load helpers
 #include "qift_internal.h"
 #include "qift_mma.h"
 
@@ -11,7 +11,8 @@ namespace {
 using namespace mma;
 
 // ===========================================================================
-// Decode kernel: M <= 16 tokens (one 16-token MFMA column).
+// Decode kernel for act_q in global memory: M <= 16 tokens (one 16-token
+// MFMA column) whose codes do not fit in LDS.
 //
 // Workgroup = 4 waves on one 16-row tile at a time; wave w takes the 1024-k
 // chunks w, w+4, ... of the tile; inside a chunk, lane group g covers
@@ -19,15 +20,9 @@ using namespace mma;
 // workgroup walks row tiles blockIdx.x, +gridDim.x, ...; each wave issues
 // the loads of its next chunk (possibly of the next tile) before computing
 // the current one, so weight traffic stays in flight across tiles and during
-// the cross-wave reduction.  Partial accumulators meet in LDS.
-//
-// Activations (ACT):
-//   0  B operands read from act_q in global memory (large M*K),
-//   1  act_q staged once per workgroup into LDS,
-//   2  fused: each workgroup rotates and quantizes the fp16 tokens itself
-//      into LDS (qift_fwht.h), overlapping its first weight loads.
+// the cross-wave reduction.  B operands come straight from act_q; partial
+// accumulators meet in LDS.
 // ===========================================================================
-constexpr int kRedBytes = 4 * 64 * 16;   // one v4i per lane per wave
 
 template <int FMT>
 struct WChunk {
@@ -48,9 +43,9 @@ __device__ __forceinline__ void load_chunk(WChunk<FMT>& ck, const char* prow, bo
   }
 }
 
-template <int FMT, int ACT>
+template <int FMT>
 __device__ __forceinline__ void mma_chunk(const WChunk<FMT>& ck, v4i& acc, int K, int c, int g, int m, int M,
-                                          const int8_t* __restrict__ act_g, const int8_t* act_l, int Kpad) {
+                                          const int8_t* __restrict__ act) {
   const bool mok = m < M;
   // B operands of the whole chunk first (independent loads, one wait)
   v4i b[4][4];
@@ -61,10 +56,7 @@ __device__ __forceinline__ void mma_chunk(const WChunk<FMT>& ck, v4i& acc, int K
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       uint4 bb = make_uint4(0, 0, 0, 0);
-      if (ok) {
-        bb = ACT == 0 ? *reinterpret_cast<const uint4*>(act_g + (int64_t)m * K + k0 + 16 * s)
-                      : *reinterpret_cast<const uint4*>(act_l + m * Kpad + k0 + 16 * s);
-      }
+      if (ok) bb = *reinterpret_cast<const uint4*>(act + (int64_t)m * K + k0 + 16 * s);
       b[u][s] = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
     }
   }
@@ -76,32 +68,21 @@ __device__ __forceinline__ void mma_chunk(const WChunk<FMT>& ck, v4i& acc, int K
   }
 }
 
-template <int FMT, int ACT, int NTILES>
+template <int FMT>
 __global__ __launch_bounds__(256) void k_decode(
     const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
     const int8_t* __restrict__ act, const float* __restrict__ sx, const int32_t* __restrict__ asum,
-    const uint16_t* __restrict__ x, int L, int num, int den, double denom,
-    int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
-    int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
-  constexpr int kScratch = ACT == 2 ? (dev::Tile<256, 16>::LDS_DOUBLES * 8 > kRedBytes
-                                           ? dev::Tile<256, 16>::LDS_DOUBLES * 8 : kRedBytes)
-                                    : kRedBytes;
-  extern __shared__ __align__(16) unsigned char smem[];
+    int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+  __shared__ v4i red[4 * 64];
+  __shared__ float s_scale[16];
+  __shared__ int s_sum[16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int ntiles = (N + 15) >> 4;
   const int NC = (K + 1023) >> 10;
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
 
-  const int act_bytes = ACT >= 1 ? ((M * Kpad + 15) & ~15) : 0;
-  int8_t* act_l = reinterpret_cast<int8_t*>(smem);
-  unsigned char* scratch = smem + act_bytes;
-  float* s_scale = reinterpret_cast<float*>(scratch + kScratch);
-  int* s_sum = reinterpret_cast<int*>(s_scale + 16);
-  double* red_d = reinterpret_cast<double*>(s_sum + 16);
-  int* red_i = reinterpret_cast<int*>(red_d + 4);
-
-  // first chunk of this wave's first tile: in flight while the activations are prepared
+  // first chunk of this wave's first tile
   int tile = blockIdx.x;
   WChunk<FMT> cur;
   {
@@ -110,49 +91,12 @@ __global__ __launch_bounds__(256) void k_decode(
     const char* prow = reinterpret_cast<const char*>(P) + (int64_t)(rowok ? n : 0) * rowbytes;
     load_chunk<FMT>(cur, prow, rowok, K, wave, g);
   }
-
-  if constexpr (ACT == 1) {
-    const int per_row = K >> 4;
-    for (int i = tid; i < M * per_row; i += 256) {
-      const int m = i / per_row, j = i - m * per_row;
-      *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) =
-          *reinterpret_cast<const uint4*>(act + (int64_t)m * K + 16 * j);
-    }
-  }
-  if constexpr (ACT == 2) {
-    for (int m = 0; m < M; ++m) {
-      int sq;
-      float sc;
-      dev::quant_token<256, NTILES>(x + (int64_t)m * K, K, L, num, den, denom,
-                                        reinterpret_cast<double*>(scratch), red_d, red_i, act_l + m * Kpad,
-                                        sq, sc);
-      if (tid == 0) {
-        s_scale[m] = sc;
-        s_sum[m] = sq;
-      }
-    }
-    if (blockIdx.x == 0 && act_q_out) {
-      __syncthreads();
-      const int per_row = K >> 4;
-      for (int i = tid; i < M * per_row; i += 256) {
-        const int m = i / per_row, j = i - m * per_row;
-        *reinterpret_cast<uint4*>(act_q_out + (int64_t)m * K + 16 * j) =
-            *reinterpret_cast<const uint4*>(act_l + m * Kpad + 16 * j);
-      }
-      if (tid < M) {
-        scale_out[tid] = s_scale[tid];
-        sum_out[tid] = s_sum[tid];
-      }
-    }
-  } else {
-    if (tid < M) {
-      s_scale[tid] = sx[tid];
-      s_sum[tid] = asum[tid];
-    }
+  if (tid < M) {
+    s_scale[tid] = sx[tid];
+    s_sum[tid] = asum[tid];
   }
   __syncthreads();
 
-  v4i* red = reinterpret_cast<v4i*>(scratch);
   const int m = r16;   // token of this lane's B operand and outputs
   for (; tile < ntiles; tile += gridDim.x) {
     v4i acc = v4i{0, 0, 0, 0};
@@ -170,7 +114,7 @@ __global__ __launch_bounds__(256) void k_decode(
         const char* prow = reinterpret_cast<const char*>(P) + (int64_t)(rowok ? n : 0) * rowbytes;
         load_chunk<FMT>(nxt, prow, rowok, K, nc, g);
       }
-      mma_chunk<FMT, ACT>(cur, acc, K, c, g, m, M, act, act_l, Kpad);
+      mma_chunk<FMT>(cur, acc, K, c, g, m, M, act);
       cur = nxt;
     }
     red[wave * 64 + lane] = acc;
@@ -186,33 +130,29 @@ __global__ __launch_bounds__(256) void k_decode(
 }
 
 // ===========================================================================
-// Decode kernel with deep loads: M <= 16 tokens whose int8 activations fit in
-// LDS (staged, ACT = 1, or produced in place by the fused rotation and
-// quantization, ACT = 2).
+// Decode kernel with deep loads: M <= 16 tokens whose int8 activation codes
+// fit in LDS (the unfused path; the fused rotation has its own kernel in
+// qift_fused.h).
 //
 // A workgroup (4 waves) owns T consecutive 16-row tiles; wave w owns the
 // w-th quarter of K of each of them: NC = ceil(K/1024) units of 256 k, in
 // each of which lane group g reads 64 weights (one 16-byte W2 load).  A wave
 // holds UPT units per tile in registers and issues all of them before it
 // waits, so a workgroup keeps 4*T*UPT KB (W2) of packed weights in flight.
-// The activation (or fp16 x) loads are issued before the weight loads: the
-// vector-memory counter retires loads in order, so this lets the staging or
-// the fused rotation run while the weights are still in flight.  T is
-// chosen per launch so that the grid covers every CU with one workgroup
-// each (up to 6 tiles).  The four quarters of a tile meet in LDS and wave
-// j mod 4 stores tile j (4 consecutive outputs per lane).
+// The first activation loads are issued before the weight loads: the
+// vector-memory counter retires loads in order, so staging the codes into
+// LDS overlaps the weight stream.  T is chosen per launch so that the grid
+// covers every CU with one workgroup each (up to 6 tiles).  The four
+// quarters of a tile meet in LDS and wave j mod 4 stores tile j (4
+// consecutive outputs per lane).
 // ===========================================================================
-template <int FMT, int ACT, int NTILES, int T, int UPT>
+template <int FMT, int T, int UPT>
 __global__ __launch_bounds__(256) void k_decode_deep(
     const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
     const int8_t* __restrict__ act, const float* __restrict__ sx, const int32_t* __restrict__ asum,
-    const uint16_t* __restrict__ x, int L, int num, int den, double denom,
-    int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
     int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
   constexpr int kRed = 4 * T * 64 * 16;
-  constexpr int kFwht = dev::Tile<256, 16>::LDS_DOUBLES * 8;
-  constexpr int kScratch = ACT == 2 ? (kFwht > kRed ? kFwht : kRed) : kRed;
   constexpr int kPre = 4;                   // activation pieces per thread loaded ahead of the weights
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -222,14 +162,10 @@ __global__ __launch_bounds__(256) void k_decode_deep(
   const int kq0 = wave * NC * 256;          // first k of this wave's quarter
 
   const int act_bytes = (M * Kpad + 15) & ~15;
-  const int raw_bytes = ACT == 2 ? ((2 * K + 15) & ~15) : 0;
   int8_t* act_l = reinterpret_cast<int8_t*>(smem);
-  uint16_t* raw_l = reinterpret_cast<uint16_t*>(smem + act_bytes);   // staged fp16 token (ACT 2)
-  unsigned char* scratch = smem + act_bytes + raw_bytes;
-  float* s_scale = reinterpret_cast<float*>(scratch + kScratch);
+  unsigned char* scratch = smem + act_bytes;
+  float* s_scale = reinterpret_cast<float*>(scratch + kRed);
   int* s_sum = reinterpret_cast<int*>(s_scale + 16);
-  double* red_d = reinterpret_cast<double*>(s_sum + 16);
-  int* red_i = reinterpret_cast<int*>(red_d + 4);
 
   const int tile0 = blockIdx.x * T;
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
@@ -244,23 +180,18 @@ __global__ __launch_bounds__(256) void k_decode_deep(
 
   // (1) activation loads first
   const int per_row = K >> 4;               // 16-byte pieces per activation row
-  uint4 apre[ACT == 1 ? kPre : 1];
-  float sx_pre = 0.f;
-  int sum_pre = 0;
-  dev::TokenRaw<NTILES> raw;
-  if constexpr (ACT == 1) {
+  uint4 apre[kPre];
+  {
     const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act, (uint32_t)(M * K));
 #pragma unroll
     for (int q = 0; q < kPre; ++q) {
       const int i = tid + 256 * q;
       apre[q] = dev::bload16(ars, i < M * per_row ? (uint32_t)(16 * i) : dev::kOutOfRange);
     }
-    const int mm = tid < M ? tid : 0;
-    sx_pre = sx[mm];
-    sum_pre = asum[mm];
-  } else {
-    dev::load_token_raw<256, NTILES>(raw, x, K);
   }
+  const int mm = tid < M ? tid : 0;
+  const float sx_pre = sx[mm];
+  const int sum_pre = asum[mm];
   // keep every activation load ahead of the weight loads in the instruction stream
   __builtin_amdgcn_sched_barrier(0);
 
@@ -282,62 +213,20 @@ __global__ __launch_bounds__(256) void k_decode_deep(
   load_batch(0);
 
   // (3) activations into LDS
-  if constexpr (ACT == 1) {
 #pragma unroll
-    for (int q = 0; q < kPre; ++q) {
-      const int i = tid + 256 * q;
-      const int m = i / per_row, j = i - m * per_row;
-      if (i < M * per_row) *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) = apre[q];
-    }
-    for (int i = tid + 256 * kPre; i < M * per_row; i += 256) {
-      const int m = i / per_row, j = i - m * per_row;
-      *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) =
-          *reinterpret_cast<const uint4*>(act + (int64_t)m * K + 16 * j);
-    }
-    if (tid < M) {
-      s_scale[tid] = sx_pre;
-      s_sum[tid] = sum_pre;
-    }
-  } else {
-    // token 0: its raw bits were loaded ahead of the weights; park them in LDS, then rotate and
-    // quantize with the compact two-pass routine.  Later tokens are staged straight from memory.
-    using S = dev::Tile<256, 16>;
-#pragma unroll
-    for (int tau = 0; tau < NTILES; ++tau) {
-      const int64_t base = (int64_t)tau * S::T + 16 * tid;
-      if (base < K) {
-        *reinterpret_cast<uint4*>(raw_l + base) = raw.d[tau][0];
-        *reinterpret_cast<uint4*>(raw_l + base + 8) = raw.d[tau][1];
-      }
-    }
-    for (int m = 0; m < M; ++m) {
-      if (m > 0) {
-        __syncthreads();   // the previous token's raw bits are consumed
-        for (int i = tid; i < per_row * 2; i += 256)
-          *reinterpret_cast<uint4*>(raw_l + 8 * i) = *reinterpret_cast<const uint4*>(x + (int64_t)m * K + 8 * i);
-      }
-      __syncthreads();
-      int sq;
-      float sc;
-      dev::quant_token_staged<256>(raw_l, K, L, num, den, denom, reinterpret_cast<double*>(scratch), red_d, red_i,
-                                   act_l + m * Kpad, sq, sc);
-      if (tid == 0) {
-        s_scale[m] = sc;
-        s_sum[m] = sq;
-      }
-    }
-    if (blockIdx.x == 0 && act_q_out) {
-      __syncthreads();
-      for (int i = tid; i < M * per_row; i += 256) {
-        const int m = i / per_row, j = i - m * per_row;
-        *reinterpret_cast<uint4*>(act_q_out + (int64_t)m * K + 16 * j) =
-            *reinterpret_cast<const uint4*>(act_l + m * Kpad + 16 * j);
-      }
-      if (tid < M) {
-        scale_out[tid] = s_scale[tid];
-        sum_out[tid] = s_sum[tid];
-      }
-    }
+  for (int q = 0; q < kPre; ++q) {
+    const int i = tid + 256 * q;
+    const int m = i / per_row, j = i - m * per_row;
+    if (i < M * per_row) *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) = apre[q];
+  }
+  for (int i = tid + 256 * kPre; i < M * per_row; i += 256) {
+    const int m = i / per_row, j = i - m * per_row;
+    *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) =
+        *reinterpret_cast<const uint4*>(act + (int64_t)m * K + 16 * j);
+  }
+  if (tid < M) {
+    s_scale[tid] = sx_pre;
+    s_sum[tid] = sum_pre;
   }
   __syncthreads();
 
@@ -370,12 +259,12 @@ __global__ __launch_bounds__(256) void k_decode_deep(
     }
   }
 
-  // (5) quarters of each tile meet in LDS; wave j stores tile j
-  v4i* red = reinterpret_cast<v4i*>(scratch);   // the FWHT scratch is free again
+  // (5) quarters of each tile meet in LDS; wave j mod 4 stores tile j
+  v4i* red = reinterpret_cast<v4i*>(scratch);
 #pragma unroll
   for (int j = 0; j < T; ++j) red[(j * 4 + wave) * 64 + lane] = acc[j];
   __syncthreads();
-  for (int j = wave; j < T; j += 4) {   // wave j (and j + 4) stores tile j
+  for (int j = wave; j < T; j += 4) {
     v4i D = red[(j * 4) * 64 + lane];
 #pragma unroll
     for (int q = 1; q < 4; ++q) D += red[(j * 4 + q) * 64 + lane];
@@ -522,86 +411,56 @@ constexpr int kDecodeGrid = 512;           // workgroups of the decode kernel (2
 
 inline int kpad_of(int64_t K) { return (int)K + 16; }
 
-template <int FMT, int ACT, int NTILES>
+template <int FMT>
 hipError_t launch_decode(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
-                         const float* sx, const int32_t* asum, const uint16_t* x, int L, int num, int den,
-                         double denom, int8_t* aq_out, float* sc_out, int32_t* sum_out, int64_t M, uint16_t* y,
-                         int32_t* acc_out, hipStream_t s) {
-  const int Kpad = kpad_of(K);
+                         const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
+                         hipStream_t s) {
   const int ntiles = (int)((N + 15) / 16);
   const int grid = ntiles < kDecodeGrid ? ntiles : kDecodeGrid;
-  const int act_bytes = ACT >= 1 ? (((int)M * Kpad + 15) & ~15) : 0;
-  const int scratch = ACT == 2 ? (dev::Tile<256, 16>::LDS_DOUBLES * 8 > kRedBytes
-                                      ? dev::Tile<256, 16>::LDS_DOUBLES * 8 : kRedBytes)
-                               : kRedBytes;
-  const size_t shmem = (size_t)act_bytes + scratch + 16 * 4 + 16 * 4 + 4 * 8 + 4 * 4;
-  if (shmem > 65536) {
-    // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
-    static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&k_decode<FMT, ACT, NTILES>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (attr != hipSuccess) return attr;
-  }
-  hipLaunchKernelGGL((k_decode<FMT, ACT, NTILES>), dim3(grid), dim3(256), shmem, s, P, sw, (int)N, (int)K, act,
-                     sx, asum, x, L, num, den, denom, aq_out, sc_out, sum_out, (int)M, Kpad, y, acc_out);
+  hipLaunchKernelGGL((k_decode<FMT>), dim3(grid), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M,
+                     y, acc_out);
   return hipGetLastError();
 }
 
-template <int FMT, int ACT, int NTILES, int T, int UPT>
+template <int FMT, int T, int UPT>
 hipError_t launch_deep_t(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
-                         const float* sx, const int32_t* asum, const uint16_t* x, int L, int num, int den,
-                         double denom, int8_t* aq_out, float* sc_out, int32_t* sum_out, int64_t M, uint16_t* y,
-                         int32_t* acc_out, hipStream_t s) {
+                         const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
+                         hipStream_t s) {
   const int Kpad = kpad_of(K);
   const int ntiles = (int)((N + 15) / 16);
   const int grid = (ntiles + T - 1) / T;
   constexpr int kRed = 4 * T * 64 * 16;
-  constexpr int kFwht = dev::Tile<256, 16>::LDS_DOUBLES * 8;
-  const int scratch = ACT == 2 ? (kFwht > kRed ? kFwht : kRed) : kRed;
-  const size_t raw_bytes = ACT == 2 ? (size_t)((2 * K + 15) & ~15) : 0;
-  const size_t shmem =
-      (size_t)((((int)M * Kpad) + 15) & ~15) + raw_bytes + scratch + 16 * 4 + 16 * 4 + 4 * 8 + 4 * 4;
+  const size_t shmem = (size_t)((((int)M * Kpad) + 15) & ~15) + kRed + 16 * 4 + 16 * 4;
   if (shmem > 65536) {
     // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
-    static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&k_decode_deep<FMT, ACT, NTILES, T, UPT>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_deep<FMT, T, UPT>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (attr != hipSuccess) return attr;
   }
-  hipLaunchKernelGGL((k_decode_deep<FMT, ACT, NTILES, T, UPT>), dim3(grid), dim3(256), shmem, s, P, sw, (int)N,
-                     (int)K, act, sx, asum, x, L, num, den, denom, aq_out, sc_out, sum_out, (int)M, Kpad, y,
-                     acc_out);
+  hipLaunchKernelGGL((k_decode_deep<FMT, T, UPT>), dim3(grid), dim3(256), shmem, s, P, sw, (int)N, (int)K, act,
+                     sx, asum, (int)M, Kpad, y, acc_out);
   return hipGetLastError();
 }
 
-// K <= 4096: 4 units per wave and tile, T tiles per workgroup (as many as keep the grid at >= 256
-// workgroups, up to 4).  Longer K: one tile per workgroup and up to 16 (W4: 8) units per batch.
-template <int FMT, int ACT, int NTILES>
+// K <= 4096: 4 units per wave and tile, T tiles per workgroup (as many as keep the grid within one
+// workgroup per CU, up to 6).  Longer K: one tile per workgroup and up to 16 (W4: 8) units per batch.
+template <int FMT>
 hipError_t launch_deep(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
-                       const float* sx, const int32_t* asum, const uint16_t* x, int L, int num, int den,
-                       double denom, int8_t* aq_out, float* sc_out, int32_t* sum_out, int64_t M, uint16_t* y,
-                       int32_t* acc_out, hipStream_t s) {
-#define QIFT_DEEP(TT, UU) launch_deep_t<FMT, ACT, NTILES, TT, UU>(P, sw, N, K, act, sx, asum, x, L, num, den, \
-                                                                  denom, aq_out, sc_out, sum_out, M, y, acc_out, s)
-  // (a fused token of K <= 4096 is one rotation tile, so NTILES > 1 implies K > 4096)
-  if constexpr (!(ACT == 2 && NTILES > 1)) {
-    if (K <= 4096) {
-      // enough tiles per workgroup that the grid fits in one workgroup per CU (at most 6)
-      const int64_t ntiles = (N + 15) / 16;
-      const int64_t t = (ntiles + 255) / 256;
-      if (t <= 1) return QIFT_DEEP(1, 4);
-      if (t == 2) return QIFT_DEEP(2, 4);
-      if (t == 3) return QIFT_DEEP(3, 4);
-      if (t == 4) return QIFT_DEEP(4, 4);
-      if (t == 5) return QIFT_DEEP(5, 4);
-      return QIFT_DEEP(6, 4);
-    }
+                       const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
+                       hipStream_t s) {
+#define QIFT_DEEP(TT, UU) launch_deep_t<FMT, TT, UU>(P, sw, N, K, act, sx, asum, M, y, acc_out, s)
+  if (K <= 4096) {
+    const int64_t ntiles = (N + 15) / 16;
+    const int64_t t = (ntiles + 255) / 256;
+    if (t <= 1) return QIFT_DEEP(1, 4);
+    if (t == 2) return QIFT_DEEP(2, 4);
+    if (t == 3) return QIFT_DEEP(3, 4);
+    if (t == 4) return QIFT_DEEP(4, 4);
+    if (t == 5) return QIFT_DEEP(5, 4);
+    return QIFT_DEEP(6, 4);
   }
-  if constexpr (!(ACT == 2 && NTILES == 1)) {
-    if constexpr (FMT == FMT_W4) return QIFT_DEEP(1, 8);
-    else return QIFT_DEEP(1, 16);
-  }
-  return hipErrorInvalidValue;
+  if constexpr (FMT == FMT_W4) return QIFT_DEEP(1, 8);
+  else return QIFT_DEEP(1, 16);
 #undef QIFT_DEEP
 }
 
@@ -610,11 +469,8 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
                       const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
                       hipStream_t s) {
   if (M <= 16) {
-    if (M * kpad_of(K) <= kDecodeMaxLds)
-      return launch_deep<FMT, 1, 1>(P, sw, N, K, act, sx, asum, nullptr, 0, 1, 1, 1.0, nullptr, nullptr, nullptr,
-                                    M, y, acc_out, s);
-    return launch_decode<FMT, 0, 1>(P, sw, N, K, act, sx, asum, nullptr, 0, 1, 1, 1.0, nullptr, nullptr, nullptr,
-                                    M, y, acc_out, s);
+    if (M * kpad_of(K) <= kDecodeMaxLds) return launch_deep<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
+    return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
   }
   const unsigned gx = (unsigned)((N + 255) / 256);
   if (M <= 64) {
