@@ -18,6 +18,13 @@ Prefill (reported under "prefill"): LLaMA-3.1-8B-shaped layers at M = 2048,
 layers 0-15 W4 and 16-31 W2 MNZ, 7 linears + 4 rotate_quant_act per layer;
 int8 TOPS = sum 2 M N K / step time.
 
+Also reported (measurement helpers): ``read_probe`` = the achievable HBM read
+bandwidth (a plain streaming-read kernel over 2 GiB); ``decode_per_shape`` =
+each decode shape's kernel looped over >= 1 GiB of distinct weight replicas
+(fused kernel, linear on precomputed act_q, and the read probe over the same
+replicas, i.e. the floor for that launch size); ``stack_kernel_sum_ms`` = the
+decode step's kernels back to back.
+
 All inputs are seeded synthetic data resident in HBM before timing starts.
 """
 from __future__ import annotations
@@ -176,6 +183,84 @@ class PrefillStack:
                     qift.linear(ws[name], act, out=self.outs[name])
 
 
+def _time_graph(torch, fn, reps):
+    """Mean seconds per replay of a graph holding fn's launches (one warm replay first)."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    with torch.cuda.graph(g):
+        fn()
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    del g
+    return a.elapsed_time(b) * 1e-3 / reps
+
+
+def read_probe(torch, qift, nbytes=1 << 31, reps=10):
+    """Achievable HBM read bandwidth: the streaming-read probe over one large buffer."""
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    parts = torch.empty(qift.read_probe_slots(nbytes), dtype=torch.int32, device="cuda")
+    dt = _time_graph(torch, lambda: qift.hbm_read_probe(buf, parts), reps)
+    del buf
+    return {"bytes": nbytes, "GBs": round(nbytes / dt / 1e9, 1), "pct_hbm_peak": round(100 * nbytes / dt / 1e9 / HBM_PEAK_GBS, 1)}
+
+
+def decode_per_shape(torch, qift, synth, min_bytes=1 << 30, reps=10):
+    """Each decode shape's kernel looped over >= min_bytes of distinct weight replicas (M = 1)."""
+    c = synth.CONFIGS[1]
+    sh = {s.name: s for s in c.linears}
+    plan = [("q,k,v", 3 * sh["q"].N, sh["q"].K, sh["q"].block, 0), ("o", sh["o"].N, sh["o"].K, sh["o"].block, 1),
+            ("gate,up", 2 * sh["gate"].N, sh["gate"].K, sh["gate"].block, 2),
+            ("down", sh["down"].N, sh["down"].K, sh["down"].block, 3)]
+    rows = []
+    for name, N, K, b, site in plan:
+        dev = torch.device("cuda")
+        lev = synth.draw_levels_torch(qift.W2_MNZ, N, K, seed=99 + site, device=dev)
+        sc = torch.from_numpy(synth.draw_scales(qift.W2_MNZ, N, cfg=1, layer=0, slot=site)).to(dev)
+        base = qift.pack_w2(lev, sc, qift.W2_MNZ, check=False)
+        del lev
+        R = -(-min_bytes // base.nbytes)
+        reps_w = [qift.Packed(base.fmt, N, K, base.words.clone(), sc) for _ in range(R)]
+        x = torch.from_numpy(synth.config_activations(c, 0, site, 1, K)).to(dev)
+        act = qift.rotate_quant_act(x, b)
+        y = torch.empty((1, N), dtype=torch.float16, device=dev)
+        parts = torch.empty(qift.read_probe_slots(base.nbytes), dtype=torch.int32, device=dev)
+        total = R * base.nbytes
+
+        def fused():
+            for w in reps_w:
+                qift.rotate_quant_linear(w, x, b, out=y)
+
+        def lin():
+            for w in reps_w:
+                qift.w2a4_linear(w, act, out=y)
+
+        def probe():
+            for w in reps_w:
+                qift.hbm_read_probe(w.words, parts)
+
+        t_f, t_l, t_p = (_time_graph(torch, f, reps) for f in (fused, lin, probe))
+        gbs = lambda t: round(total / t / 1e9, 1)
+        rows.append({"linear": name, "N": N, "K": K, "packed_bytes": base.nbytes, "replicas": R,
+                     "fused_GBs": gbs(t_f), "fused_us": round(t_f / R * 1e6, 2),
+                     "linear_on_act_q_GBs": gbs(t_l), "linear_on_act_q_us": round(t_l / R * 1e6, 2),
+                     "read_probe_GBs": gbs(t_p), "read_probe_us": round(t_p / R * 1e6, 2),
+                     "fused_pct_hbm_peak": round(100 * total / t_f / 1e9 / HBM_PEAK_GBS, 1),
+                     "fused_pct_of_read_probe": round(100 * t_p / t_f, 1)})
+        del reps_w, base
+        torch.cuda.empty_cache()
+    return rows
+
+
 def cpu_baseline(synth, budget_s=20.0):
     """The oracle as it stands, on one cfg1 layer at M=1 (4 act quantizations + 7 linears)."""
     import numpy as np
@@ -229,6 +314,8 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="launch the decode step eagerly")
     ap.add_argument("--unfused", action="store_true",
                     help="decode step as separate rotate_quant_act + w2a4_linear launches")
+    ap.add_argument("--no-per-shape", action="store_true",
+                    help="skip the per-shape replica loops and the read probe")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run 1 GiB device copies (HBM byte-counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -297,6 +384,7 @@ def main():
                 "kernel": DECODE_KERNEL if args.unfused else DECODE_KERNEL_FUSED,
                 "avg_launch_us": round(avg_dur * 1e6, 3),
                 "alg_bytes_per_launch": int(bytes_per_launch)}
+    stack_kernel_sum_ms = avg_dur * dec.launches_per_step * 1e3
 
     out = {"metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
@@ -307,10 +395,17 @@ def main():
            "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
            "tokens_per_s": round(dec.M / (ms * 1e-3), 1),
            "host_wall_s": round(wall, 3),
+           "stack_kernel_sum_ms": round(stack_kernel_sum_ms, 4),
            "roofline": roofline}
     del graph
     dec = None
     torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- per-shape loops, read probe
+    if not args.no_per_shape:
+        out["read_probe"] = read_probe(torch, qift)
+        out["decode_per_shape"] = decode_per_shape(torch, qift, synth)
+        torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- prefill
     if not args.no_prefill:

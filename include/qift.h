@@ -218,6 +218,19 @@ int qift_rotate_quant_linear(const qift_packed_w *w, const uint16_t *x, int64_t 
                              uint16_t *out, int32_t *acc_out, int8_t *act_q, float *act_scale,
                              int32_t *act_sum, qift_stream_t stream);
 
+/*
+ * Measurement helper, not part of the method: the achievable HBM read
+ * bandwidth, the floor of the decode kernels' weight streams.  Reads the
+ * device buffer buf[0 .. bytes) once with 16-byte loads spread over every CU;
+ * workgroup b XORs the 32-bit words of the 64 KiB segment b of the buffer
+ * into partials[b] (device, uint32[(bytes + 65535) / 65536], every slot
+ * written), so the XOR of all partials is the XOR of the buffer's words.
+ *   bytes      a positive multiple of 16 (QIFT_ERR_SHAPE); buf 16-byte
+ *              aligned, partials 4-byte aligned (QIFT_ERR_ALIGN).
+ *   Asynchronous on stream.
+ */
+int qift_hbm_read_probe(const void *buf, size_t bytes, uint32_t *partials, qift_stream_t stream);
+
 /* Workspace bytes the _ex calls need for this weight and M (host query). */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
 

@@ -149,6 +149,13 @@ int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t 
                            act_q, act_scale, act_sum, (hipStream_t)stream));
 }
 
+int qift_hbm_read_probe(const void* buf, size_t bytes, uint32_t* partials, qift_stream_t stream) {
+  if (!buf || !partials) return QIFT_ERR_NULL;
+  if (bytes == 0 || bytes % 16 || qift::read_probe_slots(bytes) > 0x7fffffffu) return QIFT_ERR_SHAPE;
+  if (!aligned16(buf) || (reinterpret_cast<uintptr_t>(partials) & 3u)) return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_read_probe(buf, bytes, partials, (hipStream_t)stream));
+}
+
 size_t qift_workspace_bytes(const qift_packed_w* w, int64_t M) {
   (void)w;
   (void)M;

@@ -34,6 +34,12 @@ QIFT_FUSED_LAUNCHER(launch_fused_pot);
 QIFT_FUSED_LAUNCHER(launch_fused_w4);
 #undef QIFT_FUSED_LAUNCHER
 
+// Streaming-read probe (qift_probe.hip): reads bytes (a multiple of 16) once; workgroup b XORs the
+// words of the 64 KiB segment b into partials[b].
+constexpr size_t kReadProbeSegment = 65536;
+size_t read_probe_slots(size_t bytes);
+hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* partials, hipStream_t s);
+
 // (den * 7) * sqrt(b): the fixed divisor of the per-token activation scale.
 double act_denominator(int block, int clip_den);
 

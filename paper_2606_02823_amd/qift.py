@@ -29,8 +29,8 @@ STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR
 # every symbol declared in include/qift.h
 EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_rotate_quant_act",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w4a4_linear", "qift_w4a4_linear_ex",
-           "qift_rotate_quant_linear", "qift_workspace_bytes", "qift_status_string", "qift_last_hip_error",
-           "qift_version")
+           "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
+           "qift_last_hip_error", "qift_version")
 
 
 class QiftError(RuntimeError):
@@ -74,6 +74,7 @@ def lib():
         "qift_w4a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
         "qift_w4a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
         "qift_rotate_quant_linear": (ctypes.c_int, [pw, vp, i64, HadamardSpec, vp, vp, vp, vp, vp, vp]),
+        "qift_hbm_read_probe": (ctypes.c_int, [vp, sz, vp, vp]),
         "qift_workspace_bytes": (sz, [pw, i64]),
         "qift_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "qift_last_hip_error": (ctypes.c_int, []),
@@ -286,6 +287,26 @@ def rotate_quant_linear(w: Packed, x: torch.Tensor, block: int, clip=(1, 1), out
         None if act_out is None else act_out.sum.data_ptr(), _stream(stream))
     _check("qift_rotate_quant_linear", st)
     return out
+
+
+READ_PROBE_SEGMENT = 65536   # bytes read by one workgroup of the read probe
+
+
+def read_probe_slots(nbytes: int) -> int:
+    return -(-nbytes // READ_PROBE_SEGMENT)
+
+
+def hbm_read_probe(buf: torch.Tensor, partials: torch.Tensor, stream=None) -> torch.Tensor:
+    """Read buf once on the GPU; partials[b] (int32, read_probe_slots(buf bytes) entries) receives the XOR
+    of the 32-bit words of the b-th 64 KiB segment.  A measurement helper (achievable HBM read bandwidth),
+    not part of the method."""
+    if not isinstance(buf, torch.Tensor) or buf.device.type != "cuda" or not buf.is_contiguous():
+        raise TypeError("buf must be a contiguous CUDA (HIP) tensor")
+    nbytes = buf.numel() * buf.element_size()
+    _dev(partials, torch.int32, (read_probe_slots(nbytes),), "partials")
+    _check("qift_hbm_read_probe", lib().qift_hbm_read_probe(buf.data_ptr(), nbytes, partials.data_ptr(),
+                                                            _stream(stream)))
+    return partials
 
 
 def version() -> str:

@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -116,6 +116,17 @@ def test_fused_validation(L):
     assert f(P(_pw()), A, 1, _spec(K=512, block=256), A, None, None, None, None, None) == E_SPEC
     assert f(P(_pw(K=8192)), A, 1, _spec(K=8192, block=8192), A, None, None, None, None, None) == E_SPEC
     assert f(P(_pw()), MIS, 1, sp, A, None, None, None, None, None) == E_ALIGN
+
+
+def test_read_probe_validation(L):
+    f = L.qift_hbm_read_probe
+    assert f(None, 1024, A, None) == E_NULL
+    assert f(A, 1024, None, None) == E_NULL
+    assert f(A, 0, A, None) == E_SHAPE
+    assert f(A, 1000, A, None) == E_SHAPE
+    assert f(MIS, 1024, A, None) == E_ALIGN
+    assert f(A, 1024, 0x10002, None) == E_ALIGN
+    assert f(A, 1 << 50, A, None) == E_SHAPE     # more workgroups than a grid holds
 
 
 def test_pack_validation(L):

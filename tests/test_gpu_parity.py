@@ -378,3 +378,16 @@ def test_graph_replay_matches_eager(Q):
         torch.cuda.synchronize()
         for o, e in zip(outs + outs16, eager):
             assert torch.equal(o.view(torch.int16), e.view(torch.int16))
+
+
+@pytest.mark.parametrize("nwords", [4, 16_388, 262_156, 10_485_764])
+def test_hbm_read_probe_reads_every_word(Q, nwords):
+    # the bandwidth probe must touch every 32-bit word once: its per-segment XORs are the host's
+    words = np.random.default_rng(nwords).integers(0, 2**32, size=nwords, dtype=np.uint64).astype(np.uint32)
+    buf = dev(words)
+    parts = torch.full((Q.read_probe_slots(4 * nwords),), -1, dtype=torch.int32, device="cuda")
+    Q.hbm_read_probe(buf, parts)
+    torch.cuda.synchronize()
+    seg = Q.READ_PROBE_SEGMENT // 4
+    expect = [np.bitwise_xor.reduce(words[i:i + seg]) for i in range(0, nwords, seg)]
+    assert np.array_equal(host(parts).view(np.uint32), np.array(expect, dtype=np.uint32))
