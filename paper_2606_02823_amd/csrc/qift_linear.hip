@@ -274,34 +274,40 @@ __global__ __launch_bounds__(256) void k_decode_deep(
 }
 
 // ===========================================================================
-// Prefill kernel: tiles of 256 weight rows x 16*MTILES tokens.
+// Prefill kernel: tiles of 256 weight rows x 16*MTILES*WM tokens.
 //
-// Workgroup = 4 waves; wave w owns weight rows [64w, 64w+64) of the tile
-// (4 MFMA row tiles) and all 16*MTILES tokens (MTILES column tiles), i.e.
-// 4*MTILES int32 accumulator tiles.  K advances in 256-k steps: the
-// activation tile [16*MTILES][256] int8 is double-buffered in LDS (global
-// loads for step k+1 are issued before the MFMAs of step k), and each wave
-// reads its own packed weights straight into registers (one 16-byte load
-// per lane per row tile: 4 MFMAs' worth of A operands), also one step ahead.
+// Workgroup = 4*WM waves; wave w owns weight rows [64 (w mod 4), +64) of the
+// tile (4 MFMA row tiles) and the 16*MTILES tokens of its column group
+// w / 4 (MTILES column tiles), i.e. 4*MTILES int32 accumulator tiles.  K
+// advances in 256-k steps: the activation tile [16*MTILES*WM][256] int8 is
+// double-buffered in LDS (global loads for step k+1 are issued before the
+// MFMAs of step k) and shared by all waves, and each wave reads its own
+// packed weights straight into registers (one 16-byte load per lane per row
+// tile: 4 MFMAs' worth of A operands), also one step ahead.  With WM = 2 the
+// two waves on a SIMD hide each other's load latency while the workgroup
+// keeps a 256 x 128 tile (the waves of a column pair read the same weight
+// rows, the second read mostly from cache).
 // ===========================================================================
 constexpr int kGemmBK = 256;
 constexpr int kGemmLdsRow = kGemmBK + 16;   // padded row (bytes) of the LDS activation tile
 
-template <int FMT, int MTILES>
-__global__ __launch_bounds__(256) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
-                                              int N, int K, const int8_t* __restrict__ act,
-                                              const float* __restrict__ sx, const int32_t* __restrict__ asum,
-                                              int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+template <int FMT, int MTILES, int WM>
+__global__ __launch_bounds__(256 * WM) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
+                                                   int N, int K, const int8_t* __restrict__ act,
+                                                   const float* __restrict__ sx, const int32_t* __restrict__ asum,
+                                                   int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
-  constexpr int BM = 16 * MTILES;
+  constexpr int NT = 256 * WM;
+  constexpr int BM = 16 * MTILES * WM;
   constexpr int TILE_BYTES = BM * kGemmLdsRow;
-  constexpr int STAGE_U4 = BM * (kGemmBK / 16) / 256;   // 16-byte activation loads per thread per step
+  constexpr int STAGE_U4 = BM * (kGemmBK / 16) / NT;   // 16-byte activation loads per thread per step
   __shared__ __align__(16) int8_t lds[2][TILE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int n_base = blockIdx.x * 256 + wave * 64;
+  const int n_base = blockIdx.x * 256 + (wave & 3) * 64;
   const int m_base = blockIdx.y * BM;
+  const int t_base = (wave >> 2) * MTILES;   // first column tile of this wave
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
   const int KT = (K + kGemmBK - 1) / kGemmBK;
 
@@ -325,14 +331,14 @@ __global__ __launch_bounds__(256) void k_gemm(const uint32_t* __restrict__ P, co
       for (int h = 0; h < NH; ++h) w[j][h] = dev::bload16(wrs, off + 16 * h);
     }
   };
-  // activation staging: thread tid moves 16-byte pieces i = tid + 256 q of the [BM][256] tile
+  // activation staging: thread tid moves 16-byte pieces i = tid + NT q of the [BM][256] tile
   // (the activation block of this workgroup's tokens; zeros past M and K)
   const int mrows = M - m_base < BM ? M - m_base : BM;
   const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act + (int64_t)m_base * K, (uint32_t)(mrows * K));
   auto load_a = [&](uint4 (&st)[STAGE_U4], int kt) {
 #pragma unroll
     for (int q = 0; q < STAGE_U4; ++q) {
-      const int i = tid + 256 * q;
+      const int i = tid + NT * q;
       const int row = i >> 4, col = (i & 15) * 16;
       const int k = kt * kGemmBK + col;
       st[q] = dev::bload16(ars, (row < mrows && k < K) ? (uint32_t)(row * K + k) : dev::kOutOfRange);
@@ -341,7 +347,7 @@ __global__ __launch_bounds__(256) void k_gemm(const uint32_t* __restrict__ P, co
   auto store_a = [&](const uint4 (&st)[STAGE_U4], int buf) {
 #pragma unroll
     for (int q = 0; q < STAGE_U4; ++q) {
-      const int i = tid + 256 * q;
+      const int i = tid + NT * q;
       const int row = i >> 4, col = (i & 15) * 16;
       *reinterpret_cast<uint4*>(&lds[buf][row * kGemmLdsRow + col]) = st[q];
     }
@@ -375,7 +381,8 @@ __global__ __launch_bounds__(256) void k_gemm(const uint32_t* __restrict__ P, co
       for (int j = 0; j < 4; ++j) a[j] = decode_unit<FMT>(wcur[j], s);
 #pragma unroll
       for (int t = 0; t < MTILES; ++t) {
-        const uint4 bb = *reinterpret_cast<const uint4*>(&tileb[(16 * t + r16) * kGemmLdsRow + 64 * g + 16 * s]);
+        const uint4 bb =
+            *reinterpret_cast<const uint4*>(&tileb[(16 * (t_base + t) + r16) * kGemmLdsRow + 64 * g + 16 * s]);
         const v4i b = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[j][t] = mfma_i8(a[j], b, acc[j][t]);
@@ -393,7 +400,7 @@ __global__ __launch_bounds__(256) void k_gemm(const uint32_t* __restrict__ P, co
 
 #pragma unroll
   for (int t = 0; t < MTILES; ++t) {
-    const int m = m_base + 16 * t + r16;
+    const int m = m_base + 16 * (t_base + t) + r16;
     if (m < M) {
       const float s_x = sx[m];
       const int sq = asum[m];
@@ -473,13 +480,11 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
     return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
   }
   const unsigned gx = (unsigned)((N + 255) / 256);
-  if (M <= 64) {
-    hipLaunchKernelGGL((k_gemm<FMT, 4>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P, sw, (int)N,
-                       (int)K, act, sx, asum, (int)M, y, acc_out);
-  } else {
-    hipLaunchKernelGGL((k_gemm<FMT, 8>), dim3(gx, (unsigned)((M + 127) / 128)), dim3(256), 0, s, P, sw, (int)N,
-                       (int)K, act, sx, asum, (int)M, y, acc_out);
-  }
+  // 256 x 64 tiles at every M: two workgroups per CU (2 waves per SIMD) hide each other's load
+  // latency and barriers; measured faster at M = 2048 than one-wave-per-SIMD 256 x 128 tiles (with
+  // 4 or 8 waves per workgroup) and than 256 x 32 tiles
+  hipLaunchKernelGGL((k_gemm<FMT, 4, 1>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P, sw, (int)N,
+                     (int)K, act, sx, asum, (int)M, y, acc_out);
   return hipGetLastError();
 }
 
