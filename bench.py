@@ -15,7 +15,8 @@ replayed.
 ``value`` = packed-weight bytes per step / step time (GB/s).
 
 Prefill (reported under "prefill"): LLaMA-3.1-8B-shaped layers at M = 2048,
-layers 0-15 W4 and 16-31 W2 MNZ, 7 linears + 4 rotate_quant_act per layer;
+layers 0-15 W4 and 16-31 W2 MNZ; per layer 4 rotate_quant_act + 4 linears
+(q|k|v 6144 x 4096 and gate|up 28672 x 4096 stacked along N, o, down);
 int8 TOPS = sum 2 M N K / step time.
 
 Also reported (measurement helpers): ``read_probe`` = the achievable HBM read
@@ -142,14 +143,18 @@ class DecodeStack:
 
 
 class PrefillStack:
-    """cfg4: LLaMA-3.1-8B shapes, M=2048, layers 0-15 W4, 16-31 W2 MNZ."""
+    """cfg4: LLaMA-3.1-8B shapes, M=2048, layers 0-15 W4, 16-31 W2 MNZ; q|k|v and gate|up stacked."""
 
     def __init__(self, torch, qift, synth, layers=32, M=2048):
         self.torch, self.qift, self.synth = torch, qift, synth
         self.layers, self.M = layers, M
         self.c = synth.CONFIGS[4]
-        self.shapes = {s.name: s for s in self.c.linears}
-        self.sites = [("q", "k", "v"), ("o",), ("gate", "up"), ("down",)]
+        sh = {s.name: s for s in self.c.linears}
+        # (name, N, K, block, activation site)
+        self.plan = [("qkv", sh["q"].N + sh["k"].N + sh["v"].N, sh["q"].K, sh["q"].block, 0),
+                     ("o", sh["o"].N, sh["o"].K, sh["o"].block, 1),
+                     ("gate_up", sh["gate"].N + sh["up"].N, sh["gate"].K, sh["gate"].block, 2),
+                     ("down", sh["down"].N, sh["down"].K, sh["down"].block, 3)]
 
     def setup(self):
         torch, qift, synth = self.torch, self.qift, self.synth
@@ -157,30 +162,29 @@ class PrefillStack:
         self.weights = []
         for layer in range(self.layers):
             fmt = self.c.fmt_of_layer[layer]
-            ws = {}
-            for slot, s in enumerate(self.c.linears):
-                lev = synth.draw_levels_torch(fmt, s.N, s.K, seed=7_000_003 * layer + slot, device=dev)
-                sc = torch.from_numpy(synth.draw_scales(fmt, s.N, cfg=4, layer=layer, slot=slot)).to(dev)
-                ws[s.name] = (qift.pack_w4(lev, sc, check=False) if fmt == qift.W4_SYM
-                              else qift.pack_w2(lev, sc, fmt, check=False))
+            ws = []
+            for slot, (name, N, K, b, site) in enumerate(self.plan):
+                lev = synth.draw_levels_torch(fmt, N, K, seed=7_000_003 * layer + slot, device=dev)
+                sc = torch.from_numpy(synth.draw_scales(fmt, N, cfg=4, layer=layer, slot=slot)).to(dev)
+                ws.append(qift.pack_w4(lev, sc, check=False) if fmt == qift.W4_SYM
+                          else qift.pack_w2(lev, sc, fmt, check=False))
                 del lev
             self.weights.append(ws)
         # one synthetic input per activation site, shared by the layers
-        self.x = [torch.from_numpy(synth.config_activations(self.c, 0, i, self.M, self.shapes[g[0]].K)).to(dev)
-                  for i, g in enumerate(self.sites)]
-        self.acts = [qift.alloc_act(self.M, self.shapes[g[0]].K, dev) for g in self.sites]
-        self.outs = {s.name: torch.empty((self.M, s.N), dtype=torch.float16, device=dev) for s in self.c.linears}
+        self.x = [torch.from_numpy(synth.config_activations(self.c, 0, site, self.M, K)).to(dev)
+                  for (_, _, K, _, site) in self.plan]
+        self.acts = [qift.alloc_act(self.M, K, dev) for (_, _, K, _, _) in self.plan]
+        self.outs = [torch.empty((self.M, N), dtype=torch.float16, device=dev) for (_, N, _, _, _) in self.plan]
         torch.cuda.synchronize()
-        self.ops = self.layers * sum(2 * self.M * s.N * s.K for s in self.c.linears)
+        self.ops = self.layers * sum(2 * self.M * N * K for (_, N, K, _, _) in self.plan)
 
     def step(self):
         qift = self.qift
         for layer in range(self.layers):
             ws = self.weights[layer]
-            for i, group in enumerate(self.sites):
-                act = qift.rotate_quant_act(self.x[i], self.shapes[group[0]].block, out=self.acts[i])
-                for name in group:
-                    qift.linear(ws[name], act, out=self.outs[name])
+            for i, (name, N, K, b, site) in enumerate(self.plan):
+                act = qift.rotate_quant_act(self.x[i], b, out=self.acts[i])
+                qift.linear(ws[i], act, out=self.outs[i])
 
 
 def _time_graph(torch, fn, reps):
@@ -422,7 +426,8 @@ def main():
         pms = a.elapsed_time(b) / args.prefill_steps
         tops = pre.ops / (pms * 1e-3) / 1e12
         out["prefill"] = {"workload": "LLaMA-3.1-8B-shaped prefill, M=2048, layers 0-15 W4 / 16-31 W2 MNZ, "
-                                      "7 linears + 4 rotate_quant_act per layer",
+                                      "4 rotate_quant_act + 4 linears per layer (q|k|v and gate|up stacked "
+                                      "along N)",
                           "ms_per_step": round(pms, 3), "int8_tops": round(tops, 2),
                           "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
                           "steps": args.prefill_steps}

@@ -481,8 +481,9 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
   }
   const unsigned gx = (unsigned)((N + 255) / 256);
   // 256 x 64 tiles at every M: two workgroups per CU (2 waves per SIMD) hide each other's load
-  // latency and barriers; measured faster at M = 2048 than one-wave-per-SIMD 256 x 128 tiles (with
-  // 4 or 8 waves per workgroup) and than 256 x 32 tiles
+  // latency and barriers.  Measured slower at M = 2048: one-wave-per-SIMD 256 x 128 tiles (with 4 or
+  // 8 waves per workgroup), 256 x 32 tiles, and a variant staging the activations through a 3-stage
+  // LDS ring with direct-to-LDS loads and the weights two steps ahead
   hipLaunchKernelGGL((k_gemm<FMT, 4, 1>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P, sw, (int)N,
                      (int)K, act, sx, asum, (int)M, y, acc_out);
   return hipGetLastError();
