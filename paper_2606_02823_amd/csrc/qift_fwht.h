@@ -454,9 +454,10 @@ __device__ __forceinline__ void store_codes(int8_t* dst, const int (&q)[16], int
 // exchange of the tile in between orders them).  Codes go to dst (16-byte
 // aligned) bytewise from the layout the transform ends in, at code_pos<PLANAR>;
 // elements past K are skipped.  Returns A = max |X|; each wave's sum of codes
-// lands in red_i[wave] (red_d holds 4 doubles).  LC > 0 fixes the block exponent L = LC at compile
-// time (every butterfly stage and exchange is then straight-line code); LC = 0
-// takes L at run time.
+// lands in red_i[wave] (red_d holds 4 doubles).  LC > 0 fixes the block
+// exponent L = LC at compile time (every butterfly stage and exchange is then
+// straight-line code); LC = 0 takes L at run time.  With xch0 == xch1 (one
+// exchange buffer) every tile after the first starts with a sync instead.
 template <int NTILES, int LC, bool PLANAR, typename Sync>
 __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw, int64_t K, int L_rt, int num,
                                                     int den, double* xch0, double* xch1, double* red_d,
@@ -470,6 +471,7 @@ __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw,
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
     unpack_fp16(v[tau], raw.d[tau]);
+    if (tau > 0 && xch0 == xch1 && L > 6) sync();   // the previous tile's exchange reads are done
     wend = fwht_tile_s<256, 16, false>(v[tau], (tau & 1) ? xch1 : xch0, t, L, sync);
 #pragma unroll
     for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[tau][e]));
