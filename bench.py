@@ -43,7 +43,7 @@ sys.path.insert(0, ROOT)
 METRIC = "W2A4 linear packed-weight GB/s (% HBM peak) at M=1; int8 TOPS at M=2048"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOPS
-DECODE_KERNEL_FUSED = "k_fused_decode<0, *, *, *, *>"   # MNZ decode kernel with the fused rotation
+DECODE_KERNEL_FUSED = "k_fused_decode<0, *, *, *>"   # MNZ decode kernel with the fused rotation
 DECODE_KERNEL = "k_decode_deep<0, 1, 1, *>"          # MNZ decode kernel on staged act_q
 
 

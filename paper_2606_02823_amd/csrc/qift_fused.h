@@ -3,25 +3,35 @@
 // computed in the kernel from the fp16 tokens (Sec. 3.1 for the rotation and
 // the per-token quantizer, Sec. 3.6 for the integer dot product).
 //
-// Workgroup = 8 waves in two roles, one of each per SIMD:
-//   waves 0-3 (activation waves) load the tokens, rotate them exactly in fp64
-//     registers (qift_fwht.h), find the absmax, quantize and write the int8
-//     codes to LDS.  They synchronize only among themselves (an LDS counter),
-//     so their x loads are never queued behind weight loads and their
-//     arithmetic never waits for the weight waves;
-//   waves 4-7 (weight waves) own the T consecutive 16-row tiles of the
-//     workgroup, wave 4 + w the w-th quarter of K of each: they issue every
-//     weight load of the workgroup at once (4*T*UPT KB of W2 in flight) and
-//     then wait at one barrier for the codes, so the weight stream overlaps
-//     the whole activation phase.  Their MFMAs read the codes from LDS once
-//     per 64-k group and reuse them across the T tiles; consecutive MFMAs go
-//     to independent accumulators, so they pipeline instead of waiting on
-//     each other.  MNZ weights are decoded by bit plane (one AND per packed
-//     word and plane, qift_mma.h), with the codes stored in the matching
-//     planar order in LDS and one accumulator per plane.
-// The four K-quarters of each tile meet in LDS and all 8 waves store one tile
-// each (4 consecutive outputs per lane, epilogue in qift_mma.h); the storing
-// lanes load their four s_w values at kernel start.
+// The workgroup owns T consecutive 16-row tiles and cuts K into NS slices;
+// each slice wave owns one slice of K of every tile.  Waves 0-3 (activation
+// waves) load the tokens, rotate them exactly in fp64 registers
+// (qift_fwht.h), find the absmax, quantize and write the int8 codes to LDS;
+// they synchronize only among themselves (an LDS counter), so their
+// arithmetic never waits for the other waves.  Three shapes of workgroup:
+//   * tokens of one rotation tile, T <= 2 (light weight stream): 8 waves, all
+//     of them slice waves (NS = 8).  The activation waves issue the loads of
+//     their slice once the first token has arrived; with few loads per CU
+//     the memory pipeline accepts them at once;
+//   * tokens of one rotation tile, T >= 3: 12 waves, the activation waves and
+//     8 slice waves (waves 4-11).  The activation waves issue no weight loads:
+//     a wave that issues loads into a full memory pipeline stalls until they
+//     are accepted, and here the pipeline is full for microseconds;
+//   * longer tokens (the activation waves need all their registers): 8 waves,
+//     4 slice waves (waves 4-7).
+// Slice waves that are not activation waves issue their weight loads at once
+// and wait at one barrier for the codes, so the weight stream overlaps the
+// whole activation phase.  After the barrier every slice wave runs the MFMAs
+// of its slice; with NS = 8 two per SIMD, so one wave's decode arithmetic
+// overlaps the other's MFMAs.
+// The MFMAs read the codes from LDS once per 64-k group and reuse them across
+// the T tiles; consecutive MFMAs go to independent accumulators, so they
+// pipeline instead of waiting on each other.  MNZ weights are decoded by bit plane (one
+// AND per packed word and plane, qift_mma.h), with the codes stored in the
+// matching planar order in LDS and one accumulator per plane.
+// The K-slices of each tile meet in LDS and wave j < T stores tile j
+// (4 consecutive outputs per lane, epilogue in qift_mma.h); the storing lanes
+// load their four s_w values at kernel start.
 //
 // The block exponent L of the rotation is a template parameter (LC) for the
 // block sizes in common use, which makes the transform straight-line code;
@@ -45,13 +55,36 @@ constexpr int kXchBytes = dev::Tile<256, 16>::LDS_DOUBLES * 8;   // one exchange
 template <int NTILES>
 constexpr int xch_count() { return NTILES > 1 ? 2 : 1; }
 
-// LDS bytes after the codes: exchange buffers, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, counter,
-// and 64 zero bytes (the activation operand of k-groups past K).
+// K-slices: 8 for tokens of one rotation tile (whose activation waves fit in the registers of 3
+// waves per SIMD), else 4.
 template <int NTILES>
-constexpr int tail_bytes() { return xch_count<NTILES>() * kXchBytes + 64 + 128 + 64 + 16 + 64; }
+constexpr int k_slices() { return NTILES == 1 ? 8 : 4; }
 
-template <int FMT, int NTILES, int T, int UPT, int LC>
-__global__ __launch_bounds__(512) void k_fused_decode(
+// Whether the activation waves own slices 0-3 (tokens of one tile, T <= 2).
+template <int NTILES, int T>
+constexpr bool act_slices() { return NTILES == 1 && T <= 2; }
+
+template <int NTILES, int T>
+constexpr int fused_threads() { return act_slices<NTILES, T>() ? 512 : 64 * (4 + k_slices<NTILES>()); }
+
+// 256-k units per wave and tile loaded in one batch.
+template <int FMT, int NTILES>
+constexpr int units_per_batch() { return NTILES == 1 ? 2 : FMT == mma::FMT_W4 ? 8 : 16; }
+
+// The exchange buffers, reused after the MFMAs for the K-slice partial sums of T tiles.
+template <int NTILES, int T>
+constexpr int xch_region() {
+  return xch_count<NTILES>() * kXchBytes > k_slices<NTILES>() * T * 1024 ? xch_count<NTILES>() * kXchBytes
+                                                                            : k_slices<NTILES>() * T * 1024;
+}
+
+// LDS bytes after the codes: exchange region, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, counter,
+// and 64 zero bytes (the activation operand of k-groups past K).
+template <int NTILES, int T>
+constexpr int tail_bytes() { return xch_region<NTILES, T>() + 64 + 128 + 64 + 16 + 64; }
+
+template <int FMT, int NTILES, int T, int LC>
+__global__ __launch_bounds__((fused_threads<NTILES, T>())) void k_fused_decode(
     const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
     const uint16_t* __restrict__ x, int L, int num, int den, double denom,
     int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
@@ -59,7 +92,8 @@ __global__ __launch_bounds__(512) void k_fused_decode(
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
   constexpr bool PLANAR = FMT == FMT_MNZ;                   // plane decode, codes in planar layout
   constexpr int NA = PLANAR ? 4 : T >= 3 ? 1 : 4 / T;     // accumulators per tile (MNZ: one per plane)
-  static_assert(4 * T * 64 * 16 <= kXchBytes, "reduction scratch aliases the first exchange buffer");
+  constexpr int NS = k_slices<NTILES>();
+  constexpr int UPT = units_per_batch<FMT, NTILES>();
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: role branches stay scalar
@@ -69,7 +103,7 @@ __global__ __launch_bounds__(512) void k_fused_decode(
   int8_t* act_l = reinterpret_cast<int8_t*>(smem);
   double* xch0 = reinterpret_cast<double*>(smem + act_bytes);
   double* xch1 = xch0 + (xch_count<NTILES>() - 1) * (kXchBytes / 8);
-  unsigned char* tl = smem + act_bytes + xch_count<NTILES>() * kXchBytes;
+  unsigned char* tl = smem + act_bytes + xch_region<NTILES, T>();
   float* s_scale = reinterpret_cast<float*>(tl);
   double* red_d = reinterpret_cast<double*>(tl + 64);
   int* red_i = reinterpret_cast<int*>(tl + 64 + 128);
@@ -82,9 +116,10 @@ __global__ __launch_bounds__(512) void k_fused_decode(
 
   const int tile0 = blockIdx.x * T;
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
-  const int NC = (K + 1023) >> 10;          // 256-k units per quarter of K
-  const int wq = wave - 4;                  // quarter of K of a weight wave
-  const int kq0 = wq * NC * 256;
+  const int NC = (K + NS * 256 - 1) / (NS * 256);   // 256-k units per K-slice
+  constexpr bool ACTS = act_slices<NTILES, T>();
+  const int slice = ACTS ? wave : wave - 4;          // K-slice of this wave (negative: none)
+  const int kq0 = slice * NC * 256;                  // first k of the slice
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
   uint32_t rowoff[T];
   bool rowok[T];
@@ -119,6 +154,12 @@ __global__ __launch_bounds__(512) void k_fused_decode(
     dev::TokenRaw<NTILES> raw;
     dev::load_token_raw<256, NTILES>(raw, x, K);
     swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
+    if constexpr (ACTS) {
+      // loads of this wave's slice, issued once the first token is in: waiting for the token then
+      // never waits for weights in flight (vmcnt counts in issue order)
+      dev::wait_token(raw);
+      load_batch(0);
+    }
     for (int m = 0; m < M; ++m) {
       dev::TokenRaw<NTILES> cur = raw;
       if constexpr (NTILES <= 2) {
@@ -142,7 +183,7 @@ __global__ __launch_bounds__(512) void k_fused_decode(
   for (int j = 0; j < T; ++j)
 #pragma unroll
     for (int a = 0; a < NA; ++a) acc[j][a] = v4i{0, 0, 0, 0};
-  if (wave >= 4) {
+  if (slice >= 0) {
     const int m = r16;
     const bool mok = m < M;
     // lanes of absent tokens read row 0: their MFMA output columns are never stored
@@ -157,27 +198,40 @@ __global__ __launch_bounds__(512) void k_fused_decode(
         bq[s2] = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
       }
     };
-    for (int b = 0; b * UPT < NC; ++b) {
-      if (b > 0) load_batch(b);
-      v4i bq[2][4];   // double buffer: the next unit's operands are read during this unit's MFMAs
-      load_b(b * UPT, bq[0]);
+    auto unit_mfmas = [&](int u, const v4i (&cur)[4]) {
 #pragma unroll
-      for (int u = 0; u < UPT; ++u) {
-        const int uu = b * UPT + u;
-        if (uu >= NC || kq0 + (uu << 8) >= K) break;     // wave-uniform
-        if (u + 1 < UPT) load_b(uu + 1, bq[(u + 1) & 1]);
-        const v4i (&cur)[4] = bq[u & 1];
+      for (int s2 = 0; s2 < 4; ++s2)
 #pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2)
+        for (int j = 0; j < T; ++j) {
+          // MNZ: operand s2 is bit-plane s2 of the unit's four words; else word s2
+          if constexpr (PLANAR) acc[j][s2] = mfma_i8(decode_plane(w[j][u][0], s2), cur[s2], acc[j][s2]);
+          else acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), cur[s2], acc[j][s2 % NA]);
+        }
+    };
+    if constexpr (NTILES == 1) {
+      // one batch; every operand of the slice is read up front, and units past the slice or past
+      // K run on zero weights and zero codes instead of branching (no block boundary between them)
+      v4i bq[UPT][4];
 #pragma unroll
-          for (int j = 0; j < T; ++j) {
-            // MNZ: operand s2 is bit-plane s2 of the unit's four words; else word s2
-            if constexpr (PLANAR) acc[j][s2] = mfma_i8(decode_plane(w[j][u][0], s2), cur[s2], acc[j][s2]);
-            else acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), cur[s2], acc[j][s2 % NA]);
-          }
+      for (int u = 0; u < UPT; ++u) load_b(u, bq[u]);
+#pragma unroll
+      for (int u = 0; u < UPT; ++u) unit_mfmas(u, bq[u]);
+    } else {
+      for (int b = 0; b * UPT < NC; ++b) {
+        if (b > 0) load_batch(b);
+        v4i bq[2][4];   // double buffer: the next unit's operands are read during this unit's MFMAs
+        load_b(b * UPT, bq[0]);
+#pragma unroll
+        for (int u = 0; u < UPT; ++u) {
+          const int uu = b * UPT + u;
+          if (uu >= NC || kq0 + (uu << 8) >= K) break;     // wave-uniform
+          if (u + 1 < UPT) load_b(uu + 1, bq[(u + 1) & 1]);
+          unit_mfmas(u, bq[u & 1]);
+        }
       }
     }
-  } else if (blockIdx.x == 0 && act_q_out) {
+  }
+  if (wave < 4 && blockIdx.x == 0 && act_q_out) {
     // the codes of the first workgroup double as the stand-alone quantizer's outputs
     const int per_row = K >> 4;
     for (int i = tid; i < M * per_row; i += 256) {
@@ -199,9 +253,9 @@ __global__ __launch_bounds__(512) void k_fused_decode(
     }
   }
 
-  // quarters of each tile meet in LDS (the exchange buffers are free again)
+  // the K-slices of each tile meet in LDS (the exchange region is free again)
   v4i* red = reinterpret_cast<v4i*>(xch0);
-  if (wave >= 4) {
+  if (slice >= 0) {
 #pragma unroll
     for (int j = 0; j < T; ++j) {
       v4i s;
@@ -212,15 +266,15 @@ __global__ __launch_bounds__(512) void k_fused_decode(
 #pragma unroll
         for (int a = 1; a < NA; ++a) s += acc[j][a];
       }
-      red[(j * 4 + wq) * 64 + lane] = s;
+      red[(j * NS + slice) * 64 + lane] = s;
     }
   }
   __syncthreads();
   if (wave < T) {
     const int j = wave;
-    v4i D = red[(j * 4) * 64 + lane];
+    v4i D = red[(j * NS) * 64 + lane];
 #pragma unroll
-    for (int q = 1; q < 4; ++q) D += red[(j * 4 + q) * 64 + lane];
+    for (int q = 1; q < NS; ++q) D += red[(j * NS + q) * 64 + lane];
     const int m = r16;
     if (m < M && n_st < N) {
       const int sq = red_i[4 * m] + red_i[4 * m + 1] + red_i[4 * m + 2] + red_i[4 * m + 3];
@@ -231,34 +285,34 @@ __global__ __launch_bounds__(512) void k_fused_decode(
 
 inline int kpad_of(int64_t K) { return (int)K + 16; }
 
-template <int FMT, int NTILES, int T, int UPT, int LC>
+template <int FMT, int NTILES, int T, int LC>
 hipError_t launch_t(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
                     int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
                     int32_t* acc_out, hipStream_t s) {
   const int Kpad = kpad_of(K);
   const int ntiles = (int)((N + 15) / 16);
   const int grid = (ntiles + T - 1) / T;
-  const size_t shmem = (size_t)((((int)M * Kpad) + 15) & ~15) + tail_bytes<NTILES>();
+  const size_t shmem = (size_t)((((int)M * Kpad) + 15) & ~15) + tail_bytes<NTILES, T>();
   if (shmem > 65536) {
     // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
     static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&k_fused_decode<FMT, NTILES, T, UPT, LC>),
+        reinterpret_cast<const void*>(&k_fused_decode<FMT, NTILES, T, LC>),
         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (attr != hipSuccess) return attr;
   }
-  hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, UPT, LC>), dim3(grid), dim3(512), shmem, s, P, sw, (int)N,
+  hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, LC>), dim3(grid), dim3(fused_threads<NTILES, T>()), shmem, s, P, sw, (int)N,
                      (int)K, x, L, num, den, denom, aq, sc, sm, (int)M, Kpad, y, acc_out);
   return hipGetLastError();
 }
 
 // Block exponents compiled as constants: 12 and 8 for tokens of one rotation
 // tile (K <= 4096), 12, 11 and 6 for longer tokens; anything else at run time.
-template <int FMT, int NTILES, int T, int UPT>
+template <int FMT, int NTILES, int T>
 hipError_t launch_l(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
                     int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
                     int32_t* acc_out, hipStream_t s) {
 #define QIFT_FUSED_L(LL) \
-  launch_t<FMT, NTILES, T, UPT, LL>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
+  launch_t<FMT, NTILES, T, LL>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
   if constexpr (NTILES == 1) {
     if (L == 12) return QIFT_FUSED_L(12);
     if (L == 8) return QIFT_FUSED_L(8);
@@ -271,32 +325,30 @@ hipError_t launch_l(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
 #undef QIFT_FUSED_L
 }
 
-// K <= 4096 (one rotation tile): 4 units of 256 k per weight wave and tile, and as many tiles
-// per workgroup as keep the grid within one workgroup per CU (at most 6; W4, whose units take
-// twice the registers, at most 3).  Longer K: one tile per workgroup, up to 16 (W4: 8) units
-// per batch.
+// K <= 4096 (one rotation tile): as many tiles per workgroup as keep the grid within one
+// workgroup per CU (at most 6; W4, whose units take twice the registers, at most 3).  Longer K:
+// one tile per workgroup.
 template <int FMT, int NTILES>
 hipError_t launch_nt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
                      int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
                      int32_t* acc_out, hipStream_t s) {
-#define QIFT_FUSED(TT, UU) \
-  launch_l<FMT, NTILES, TT, UU>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
+#define QIFT_FUSED(TT) \
+  launch_l<FMT, NTILES, TT>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
   if constexpr (NTILES == 1) {
     const int64_t ntiles = (N + 15) / 16;
     int64_t t = (ntiles + 255) / 256;
     if (FMT == FMT_W4 && t > 3) t = 3;
-    if (t <= 1) return QIFT_FUSED(1, 4);
-    if (t == 2) return QIFT_FUSED(2, 4);
-    if (t == 3) return QIFT_FUSED(3, 4);
+    if (t <= 1) return QIFT_FUSED(1);
+    if (t == 2) return QIFT_FUSED(2);
+    if (t == 3) return QIFT_FUSED(3);
     if constexpr (FMT != FMT_W4) {
-      if (t == 4) return QIFT_FUSED(4, 4);
-      if (t == 5) return QIFT_FUSED(5, 4);
-      return QIFT_FUSED(6, 4);
+      if (t == 4) return QIFT_FUSED(4);
+      if (t == 5) return QIFT_FUSED(5);
+      return QIFT_FUSED(6);
     }
     return hipErrorInvalidValue;
   } else {
-    if constexpr (FMT == FMT_W4) return QIFT_FUSED(1, 8);
-    else return QIFT_FUSED(1, 16);
+    return QIFT_FUSED(1);
   }
 #undef QIFT_FUSED
 }
