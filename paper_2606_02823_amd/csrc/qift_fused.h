@@ -67,9 +67,10 @@ constexpr bool act_slices() { return NTILES == 1 && T <= 2; }
 template <int NTILES, int T>
 constexpr int fused_threads() { return act_slices<NTILES, T>() ? 512 : 64 * (4 + k_slices<NTILES>()); }
 
-// 256-k units per wave and tile loaded in one batch.
+// 256-k units per wave and tile loaded in one batch: every unit of a slice (4 per rotation tile
+// with 4 slices), except W4 at K > 8192 (8 units per batch: its units take twice the registers).
 template <int FMT, int NTILES>
-constexpr int units_per_batch() { return NTILES == 1 ? 2 : FMT == mma::FMT_W4 ? 8 : 16; }
+constexpr int units_per_batch() { return NTILES == 1 ? 2 : FMT == mma::FMT_W4 && NTILES > 2 ? 8 : 4 * NTILES; }
 
 // The exchange buffers, reused after the MFMAs for the K-slice partial sums of T tiles.
 template <int NTILES, int T>
@@ -216,6 +217,15 @@ __global__ __launch_bounds__((fused_threads<NTILES, T>())) void k_fused_decode(
       for (int u = 0; u < UPT; ++u) load_b(u, bq[u]);
 #pragma unroll
       for (int u = 0; u < UPT; ++u) unit_mfmas(u, bq[u]);
+    } else if constexpr (UPT == 4 * NTILES) {
+      // one batch of every unit a slice can have; units past the slice or past K run on zeros
+      v4i bq[2][4];   // double buffer: the next unit's operands are read during this unit's MFMAs
+      load_b(0, bq[0]);
+#pragma unroll
+      for (int u = 0; u < UPT; ++u) {
+        if (u + 1 < UPT) load_b(u + 1, bq[(u + 1) & 1]);
+        unit_mfmas(u, bq[u & 1]);
+      }
     } else {
       for (int b = 0; b * UPT < NC; ++b) {
         if (b > 0) load_batch(b);
@@ -226,6 +236,7 @@ __global__ __launch_bounds__((fused_threads<NTILES, T>())) void k_fused_decode(
           const int uu = b * UPT + u;
           if (uu >= NC || kq0 + (uu << 8) >= K) break;     // wave-uniform
           if (u + 1 < UPT) load_b(uu + 1, bq[(u + 1) & 1]);
+          __builtin_amdgcn_sched_barrier(0);   // the next unit's reads go out before these MFMAs
           unit_mfmas(u, bq[u & 1]);
         }
       }

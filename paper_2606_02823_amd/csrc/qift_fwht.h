@@ -252,25 +252,25 @@ __device__ __attribute__((noinline)) int quant_exact(double ax, double f, int64_
   return (int)(q < 7 ? q : 7);
 }
 
-// Rounding of 16 values.  The fp64 quotient v = |X| c1 is within 1e-13 of the
-// exact 7 den |X| / (num A) (v <= 112), so unless v lies within 1e-9 of a
-// half-integer its nearest integer is rint(v).  That branch-free fast path
-// covers all 16 values; only when some lane of the wave has a value that
-// close to a half (a wave-uniform, rare branch) are those values redone with
-// the exact int64 test.
+// Rounding of 16 values.  The fp64 quotient v = X c1 is within 1e-13 of the
+// exact 7 den X / (num A) (|v| <= 112), so unless v lies within 1e-9 of a
+// half-integer its nearest integer is rint(v); round-half-even is odd-symmetric,
+// so rounding the signed quotient gives sign(X) times the rounded magnitude.
+// That branch-free fast path covers all 16 values; only when some lane of the
+// wave has a value that close to a half (a wave-uniform, rare branch) are those
+// values redone with the exact int64 test.
 __device__ __forceinline__ void quant16(const double (&v)[16], const QuantParams& p, int (&q)[16]) {
   int near = 0;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
-    const double vv = fabs(v[e]) * p.c1;   // c1 = 0 when A = 0, giving q = 0
-    // vv + 1.5 * 2^52 rounds vv to the nearest integer (ties to even) into the low word, since
-    // 0 <= vv < 2^31; subtracting the constant again gives that integer as a double, exactly
+    const double vv = v[e] * p.c1;   // c1 = 0 when A = 0, giving q = 0
+    // vv + 1.5 * 2^52 rounds vv to the nearest integer (ties to even) into the low word as a
+    // two's-complement int32, since |vv| < 2^31; subtracting the constant again gives that
+    // integer as a double, exactly
     const double tt = vv + 0x1.8p52;
     const double r = tt - 0x1.8p52;
     near |= fabs(vv - r) > 0.5 - 1e-9;
-    const int ri = __double2loint(tt);
-    const int qq = ri < 7 ? ri : 7;
-    q[e] = v[e] < 0.0 ? -qq : qq;
+    q[e] = min(max(__double2loint(tt), -7), 7);   // one v_med3_i32
   }
   if (__any(near)) {
 #pragma unroll
