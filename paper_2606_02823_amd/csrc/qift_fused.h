@@ -3,32 +3,26 @@
 // computed in the kernel from the fp16 tokens (Sec. 3.1 for the rotation and
 // the per-token quantizer, Sec. 3.6 for the integer dot product).
 //
-// The workgroup owns T consecutive 16-row tiles and cuts K into NS slices;
-// each slice wave owns one slice of K of every tile.  Waves 0-3 (activation
+// The workgroup owns T consecutive 16-row tiles.  Waves 0-3 (activation
 // waves) load the tokens, rotate them exactly in fp64 registers
 // (qift_fwht.h), find the absmax, quantize and write the int8 codes to LDS;
 // they synchronize only among themselves (an LDS counter), so their
-// arithmetic never waits for the other waves.  Three shapes of workgroup:
-//   * tokens of one rotation tile, T <= 2 (light weight stream): 8 waves, all
-//     of them slice waves (NS = 8).  The activation waves issue the loads of
-//     their slice once the first token has arrived; with few loads per CU
-//     the memory pipeline accepts them at once;
-//   * tokens of one rotation tile, T >= 3: 12 waves, the activation waves and
-//     8 slice waves (waves 4-11).  The activation waves issue no weight loads:
-//     a wave that issues loads into a full memory pipeline stalls until they
-//     are accepted, and here the pipeline is full for microseconds;
-//   * longer tokens (the activation waves need all their registers): 8 waves,
-//     4 slice waves (waves 4-7).
-// Slice waves that are not activation waves issue their weight loads at once
-// and wait at one barrier for the codes, so the weight stream overlaps the
-// whole activation phase.  After the barrier every slice wave runs the MFMAs
-// of its slice; with NS = 8 two per SIMD, so one wave's decode arithmetic
+// arithmetic never waits for the other waves, and they issue no weight loads
+// (a wave that issues loads into a full memory pipeline stalls until they are
+// accepted).  The NS weight waves that follow cut K into NS slices, one per
+// wave, of every tile: 8 for tokens of one rotation tile (12 waves, 3 per
+// SIMD), else 4 (the activation waves of longer tokens need the registers of
+// 2 waves per SIMD).  They issue their weight loads at once (for long tokens
+// just after the token loads have gone out, so x is not queued behind the
+// weight stream) and wait at one barrier for the codes, so the weight stream
+// overlaps the whole activation phase.  After the barrier they run the MFMAs
+// of their slices; with NS = 8 two per SIMD, so one wave's decode arithmetic
 // overlaps the other's MFMAs.
 // The MFMAs read the codes from LDS once per 64-k group and reuse them across
 // the T tiles; consecutive MFMAs go to independent accumulators, so they
-// pipeline instead of waiting on each other.  MNZ weights are decoded by bit plane (one
-// AND per packed word and plane, qift_mma.h), with the codes stored in the
-// matching planar order in LDS and one accumulator per plane.
+// pipeline instead of waiting on each other.  MNZ weights are decoded by bit
+// plane (one AND per packed word and plane, qift_mma.h), with the codes stored
+// in the matching planar order in LDS and one accumulator per plane.
 // The K-slices of each tile meet in LDS and wave j < T stores tile j
 // (4 consecutive outputs per lane, epilogue in qift_mma.h); the storing lanes
 // load their four s_w values at kernel start.
@@ -55,17 +49,13 @@ constexpr int kXchBytes = dev::Tile<256, 16>::LDS_DOUBLES * 8;   // one exchange
 template <int NTILES>
 constexpr int xch_count() { return NTILES > 1 ? 2 : 1; }
 
-// K-slices: 8 for tokens of one rotation tile (whose activation waves fit in the registers of 3
-// waves per SIMD), else 4.
+// Weight waves, one per K-slice: 8 for tokens of one rotation tile (whose activation waves fit in
+// the registers of 3 waves per SIMD), else 4.
 template <int NTILES>
 constexpr int k_slices() { return NTILES == 1 ? 8 : 4; }
 
-// Whether the activation waves own slices 0-3 (tokens of one tile, T <= 2).
-template <int NTILES, int T>
-constexpr bool act_slices() { return NTILES == 1 && T <= 2; }
-
-template <int NTILES, int T>
-constexpr int fused_threads() { return act_slices<NTILES, T>() ? 512 : 64 * (4 + k_slices<NTILES>()); }
+template <int NTILES>
+constexpr int fused_threads() { return 64 * (4 + k_slices<NTILES>()); }
 
 // 256-k units per wave and tile loaded in one batch: every unit of a slice (4 per rotation tile
 // with 4 slices), except W4 at K > 8192 (8 units per batch: its units take twice the registers).
@@ -79,13 +69,13 @@ constexpr int xch_region() {
                                                                             : k_slices<NTILES>() * T * 1024;
 }
 
-// LDS bytes after the codes: exchange region, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, counter,
+// LDS bytes after the codes: exchange region, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, 2 counters,
 // and 64 zero bytes (the activation operand of k-groups past K).
 template <int NTILES, int T>
 constexpr int tail_bytes() { return xch_region<NTILES, T>() + 64 + 128 + 64 + 16 + 64; }
 
 template <int FMT, int NTILES, int T, int LC>
-__global__ __launch_bounds__((fused_threads<NTILES, T>())) void k_fused_decode(
+__global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
     const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
     const uint16_t* __restrict__ x, int L, int num, int den, double denom,
     int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
@@ -111,15 +101,18 @@ __global__ __launch_bounds__((fused_threads<NTILES, T>())) void k_fused_decode(
   unsigned* ctr = reinterpret_cast<unsigned*>(tl + 64 + 128 + 64);
   int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 64 + 128 + 64 + 16);
 
-  if (tid == 0) *ctr = 0u;
+  unsigned* xflag = ctr + 1;   // activation waves whose token loads have gone out
+  if (tid == 0) {
+    ctr[0] = 0u;
+    xflag[0] = 0u;
+  }
   if (tid < 4) reinterpret_cast<uint4*>(zero64)[tid] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();   // nothing is in flight yet: this costs only the launch skew of the waves
 
   const int tile0 = blockIdx.x * T;
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
   const int NC = (K + NS * 256 - 1) / (NS * 256);   // 256-k units per K-slice
-  constexpr bool ACTS = act_slices<NTILES, T>();
-  const int slice = ACTS ? wave : wave - 4;          // K-slice of this wave (negative: none)
+  const int slice = wave - 4;                        // K-slice of this wave (negative: none)
   const int kq0 = slice * NC * 256;                  // first k of the slice
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
   uint32_t rowoff[T];
@@ -155,11 +148,11 @@ __global__ __launch_bounds__((fused_threads<NTILES, T>())) void k_fused_decode(
     dev::TokenRaw<NTILES> raw;
     dev::load_token_raw<256, NTILES>(raw, x, K);
     swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
-    if constexpr (ACTS) {
-      // loads of this wave's slice, issued once the first token is in: waiting for the token then
-      // never waits for weights in flight (vmcnt counts in issue order)
-      dev::wait_token(raw);
-      load_batch(0);
+    if constexpr (NTILES > 1) {
+      // long tokens: the weight waves wait for this before issuing, so the token's loads reach the
+      // memory pipeline ahead of the weight stream (which has time to spare until the codes are in)
+      asm volatile("" ::: "memory");
+      if (lane == 0) __hip_atomic_fetch_add(xflag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
     for (int m = 0; m < M; ++m) {
       dev::TokenRaw<NTILES> cur = raw;
@@ -174,6 +167,12 @@ __global__ __launch_bounds__((fused_threads<NTILES, T>())) void k_fused_decode(
     }
   } else {
     // ---- weight waves: the first batch of weights (zeros for rows past N and k past K)
+    if constexpr (NTILES > 1) {
+      for (int spin = 0; spin < (1 << 20); ++spin)   // bounded: a lost flag costs time, never a hang
+        if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(xflag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) >= 4u)
+          break;
+      asm volatile("" ::: "memory");
+    }
     swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
     load_batch(0);
   }
@@ -311,7 +310,7 @@ hipError_t launch_t(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (attr != hipSuccess) return attr;
   }
-  hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, LC>), dim3(grid), dim3(fused_threads<NTILES, T>()), shmem, s, P, sw, (int)N,
+  hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, LC>), dim3(grid), dim3(fused_threads<NTILES>()), shmem, s, P, sw, (int)N,
                      (int)K, x, L, num, den, denom, aq, sc, sm, (int)M, Kpad, y, acc_out);
   return hipGetLastError();
 }

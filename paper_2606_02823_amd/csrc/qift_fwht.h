@@ -363,17 +363,6 @@ __device__ __forceinline__ void load_token_raw(TokenRaw<NTILES>& raw, const uint
   }
 }
 
-// Waits until the token registers have arrived; no memory access is moved across this point.
-template <int NTILES>
-__device__ __forceinline__ void wait_token(const TokenRaw<NTILES>& raw) {
-#pragma unroll
-  for (int tau = 0; tau < NTILES; ++tau)
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-      asm volatile("" ::"v"(raw.d[tau][h].x), "v"(raw.d[tau][h].y), "v"(raw.d[tau][h].z), "v"(raw.d[tau][h].w)
-                   : "memory");
-}
-
 __device__ __forceinline__ void unpack_fp16(double (&v)[16], const uint4 (&d)[2]) {
   const uint32_t w[8] = {d[0].x, d[0].y, d[0].z, d[0].w, d[1].x, d[1].y, d[1].z, d[1].w};
 #pragma unroll
