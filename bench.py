@@ -187,6 +187,83 @@ class PrefillStack:
                 qift.linear(ws[i], act, out=self.outs[i])
 
 
+class SweepStack:
+    """32 distinct seeded layers of one config at M tokens: cfg2 (LLaMA-3.1-8B, MNZ; q|k|v, o, gate|up,
+    down) or cfg3 (LLaMA-3.1-8B MLP, PoT; gate|up, down).  M <= 4 runs the fused rotate+linear entry,
+    larger M one rotate_quant_act per input and the linear on its codes (decode kernel up to M = 16,
+    the MFMA GEMM beyond)."""
+
+    def __init__(self, torch, qift, synth, cfg, M, layers=32):
+        self.torch, self.qift, self.synth = torch, qift, synth
+        self.cfg, self.M, self.layers = cfg, M, layers
+        c = synth.CONFIGS[cfg]
+        sh = {s.name: s for s in c.linears}
+        self.plan = [("gate_up", sh["gate"].N + sh["up"].N, sh["gate"].K, sh["gate"].block, 2),
+                     ("down", sh["down"].N, sh["down"].K, sh["down"].block, 3)]
+        if "q" in sh:
+            self.plan = [("qkv", sh["q"].N + sh["k"].N + sh["v"].N, sh["q"].K, sh["q"].block, 0),
+                         ("o", sh["o"].N, sh["o"].K, sh["o"].block, 1)] + self.plan
+        self.fmt = c.fmt_of_layer[0]
+        self.fused = M <= qift.FUSED_MAX_M
+
+    def setup(self):
+        torch, qift, synth = self.torch, self.qift, self.synth
+        dev = torch.device("cuda")
+        c = synth.CONFIGS[self.cfg]
+        self.weights = []
+        for layer in range(self.layers):
+            ws = []
+            for slot, (name, N, K, b, site) in enumerate(self.plan):
+                lev = synth.draw_levels_torch(self.fmt, N, K, seed=3_000_017 * layer + 101 * self.cfg + slot,
+                                              device=dev)
+                sc = torch.from_numpy(synth.draw_scales(self.fmt, N, cfg=self.cfg, layer=layer, slot=slot)).to(dev)
+                ws.append(qift.pack_w2(lev, sc, self.fmt, check=False))
+                del lev
+            self.weights.append(ws)
+        self.x = [torch.from_numpy(synth.config_activations(c, 0, site, self.M, K)).to(dev)
+                  for (_, _, K, _, site) in self.plan]
+        self.acts = [qift.alloc_act(self.M, K, dev) for (_, _, K, _, _) in self.plan]
+        self.outs = [torch.empty((self.M, N), dtype=torch.float16, device=dev) for (_, N, _, _, _) in self.plan]
+        torch.cuda.synchronize()
+        self.packed_bytes = sum(w.nbytes for ws in self.weights for w in ws)
+        self.ops = self.layers * sum(2 * self.M * N * K for (_, N, K, _, _) in self.plan)
+
+    def step(self):
+        qift = self.qift
+        for layer in range(self.layers):
+            ws = self.weights[layer]
+            for i, (name, N, K, b, site) in enumerate(self.plan):
+                if self.fused:
+                    qift.rotate_quant_linear(ws[i], self.x[i], b, out=self.outs[i])
+                else:
+                    act = qift.rotate_quant_act(self.x[i], b, out=self.acts[i])
+                    qift.w2a4_linear(ws[i], act, out=self.outs[i])
+
+
+def stack_sweep(torch, qift, synth, reps=20):
+    """Tokens/s and packed GB/s of the cfg2 stack at M in {1, 4, 16} and the cfg3 PoT MLP stack at
+    M in {1, 8, 64} (hipGraph replays, inputs resident)."""
+    rows = []
+    for cfg, Ms in ((2, (1, 4, 16)), (3, (1, 8, 64))):
+        for M in Ms:
+            st = SweepStack(torch, qift, synth, cfg, M)
+            st.setup()
+            st.step()
+            torch.cuda.synchronize()
+            dt = _time_graph(torch, st.step, reps)
+            gbs = st.packed_bytes / dt / 1e9
+            c = synth.CONFIGS[cfg]
+            rows.append({"config": c.label, "M": M, "layers": st.layers,
+                         "linears": "+".join(n for n, *_ in st.plan),
+                         "path": "fused rotate_quant_linear" if st.fused else "rotate_quant_act + w2a4_linear",
+                         "ms_per_step": round(dt * 1e3, 4), "tokens_per_s": round(M / dt, 1),
+                         "packed_GBs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+                         "int8_tops": round(st.ops / dt / 1e12, 2)})
+            st = None
+            torch.cuda.empty_cache()
+    return rows
+
+
 def _time_graph(torch, fn, reps):
     """Mean seconds per replay of a graph holding fn's launches (one warm replay first)."""
     g = torch.cuda.CUDAGraph()
@@ -320,6 +397,8 @@ def main():
                     help="decode step as separate rotate_quant_act + w2a4_linear launches")
     ap.add_argument("--no-per-shape", action="store_true",
                     help="skip the per-shape replica loops and the read probe")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the cfg2 (M 1/4/16) and cfg3 PoT (M 1/8/64) stack sweep")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run 1 GiB device copies (HBM byte-counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -409,6 +488,11 @@ def main():
     if not args.no_per_shape:
         out["read_probe"] = read_probe(torch, qift)
         out["decode_per_shape"] = decode_per_shape(torch, qift, synth)
+        torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- cfg2 / cfg3 stacks at several M
+    if not args.no_sweep:
+        out["stack_sweep"] = stack_sweep(torch, qift, synth)
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- prefill

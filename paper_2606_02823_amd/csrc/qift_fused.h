@@ -82,7 +82,9 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
     int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
   constexpr bool PLANAR = FMT == FMT_MNZ;                   // plane decode, codes in planar layout
-  constexpr int NA = PLANAR ? 4 : T >= 3 ? 1 : 4 / T;     // accumulators per tile (MNZ: one per plane)
+  // accumulators per tile (MNZ: one per bit plane, planes 0 and 3 sharing one from 4 tiles on, where
+  // registers are scarce and the MFMA chains are long enough)
+  constexpr int NA = PLANAR ? (T >= 4 ? 3 : 4) : T >= 3 ? 1 : 4 / T;
   constexpr int NS = k_slices<NTILES>();
   constexpr int UPT = units_per_batch<FMT, NTILES>();
   extern __shared__ __align__(16) unsigned char smem[];
@@ -204,7 +206,10 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
 #pragma unroll
         for (int j = 0; j < T; ++j) {
           // MNZ: operand s2 is bit-plane s2 of the unit's four words; else word s2
-          if constexpr (PLANAR) acc[j][s2] = mfma_i8(decode_plane(w[j][u][0], s2), cur[s2], acc[j][s2]);
+          if constexpr (PLANAR) {
+            const int a = NA == 3 && s2 == 3 ? 0 : s2;
+            acc[j][a] = mfma_i8(decode_plane(w[j][u][0], s2), cur[s2], acc[j][a]);
+          }
           else acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), cur[s2], acc[j][s2 % NA]);
         }
     };
@@ -270,7 +275,8 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
     for (int j = 0; j < T; ++j) {
       v4i s;
       if constexpr (PLANAR) {
-        s = combine_planes(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+        if constexpr (NA == 3) s = combine_planes(acc[j][0], acc[j][1], acc[j][2]);
+        else s = combine_planes(acc[j][0], acc[j][1], acc[j][2], acc[j][NA - 1]);
       } else {
         s = acc[j][0];
 #pragma unroll
@@ -354,7 +360,8 @@ hipError_t launch_nt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K
     if constexpr (FMT != FMT_W4) {
       if (t == 4) return QIFT_FUSED(4);
       if (t == 5) return QIFT_FUSED(5);
-      return QIFT_FUSED(6);
+      if (t == 6) return QIFT_FUSED(6);
+      return QIFT_FUSED(7);
     }
     return hipErrorInvalidValue;
   } else {

@@ -94,7 +94,8 @@ __device__ __forceinline__ v4i decode_unit(const uint4 (&u)[FMT == FMT_W4 ? 2 : 
 // the codes of the same k as B operand (the planar code layout) and one
 // accumulator per plane, the unit's code dot product is
 //     D = acc0 + acc1 / 4 + acc2 / 16 + acc3,
-// where every division is exact (acc_t is 4^t times an integer sum).
+// where every division is exact (acc_t is 4^t times an integer sum).  Planes
+// 0 and 3 carry the same factor, so they may share one accumulator.
 __device__ __forceinline__ v4i decode_plane(const uint4& u, int t) {
   if (t == 3)
     return v4i{(int)((u.x >> 6) & 0x03030303u), (int)((u.y >> 6) & 0x03030303u),
@@ -107,6 +108,14 @@ __device__ __forceinline__ v4i combine_planes(const v4i& a0, const v4i& a1, cons
   v4i d;
 #pragma unroll
   for (int r = 0; r < 4; ++r) d[r] = a0[r] + (a1[r] >> 2) + (a2[r] >> 4) + a3[r];
+  return d;
+}
+
+// The same with planes 0 and 3 accumulated together in a03.
+__device__ __forceinline__ v4i combine_planes(const v4i& a03, const v4i& a1, const v4i& a2) {
+  v4i d;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) d[r] = a03[r] + (a1[r] >> 2) + (a2[r] >> 4);
   return d;
 }
 

@@ -20,6 +20,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libqift.so")
 
 W2_MNZ, W2_POT, W4_SYM = 0, 1, 2
+FUSED_MAX_M = 4   # tokens per call of the fused rotate_quant_linear entry (limits in qift.h)
 LAYOUT_V1 = 1
 
 STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR_SPEC",

@@ -294,7 +294,7 @@ def test_decode_activation_paths(Q, M, K, b):
 FUSED_SHAPES = [(512, 256, 256), (1000, 1088, 64), (4096, 4096, 4096), (2064, 11008, 64),
                 (4096, 14336, 2048), (1040, 16384, 4096), (784, 8192, 8), (8208, 4096, 4096),
                 (12288, 4096, 4096), (16400, 2048, 2048), (22016, 4096, 4096), (24592, 1024, 1024),
-                (1040, 2048, 32)]
+                (1040, 2048, 32), (6144, 4096, 4096), (28672, 4096, 4096)]
 
 
 @pytest.mark.parametrize("fmt", FMTS)
