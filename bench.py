@@ -189,9 +189,9 @@ class PrefillStack:
 
 class SweepStack:
     """32 distinct seeded layers of one config at M tokens: cfg2 (LLaMA-3.1-8B, MNZ; q|k|v, o, gate|up,
-    down) or cfg3 (LLaMA-3.1-8B MLP, PoT; gate|up, down).  M <= 4 runs the fused rotate+linear entry,
-    larger M one rotate_quant_act per input and the linear on its codes (decode kernel up to M = 16,
-    the MFMA GEMM beyond)."""
+    down) or cfg3 (LLaMA-3.1-8B MLP, PoT; gate|up, down).  M = 1 runs the fused rotate+linear entry,
+    larger M one rotate_quant_act per input and the linear on its codes (the decode kernel per block
+    of 16 tokens up to M = 64)."""
 
     def __init__(self, torch, qift, synth, cfg, M, layers=32):
         self.torch, self.qift, self.synth = torch, qift, synth
@@ -204,7 +204,7 @@ class SweepStack:
             self.plan = [("qkv", sh["q"].N + sh["k"].N + sh["v"].N, sh["q"].K, sh["q"].block, 0),
                          ("o", sh["o"].N, sh["o"].K, sh["o"].block, 1)] + self.plan
         self.fmt = c.fmt_of_layer[0]
-        self.fused = M <= qift.FUSED_MAX_M
+        self.fused = M == 1   # fused entry at one token; for more, one rotation per input then the linear
 
     def setup(self):
         torch, qift, synth = self.torch, self.qift, self.synth

@@ -50,43 +50,52 @@ template <int NTILES>
 constexpr int xch_count() { return NTILES > 1 ? 2 : 1; }
 
 // Weight waves, one per K-slice: 8 for tokens of one rotation tile (whose activation waves fit in
-// the registers of 3 waves per SIMD), else 4.
-template <int NTILES>
-constexpr int k_slices() { return NTILES == 1 ? 8 : 4; }
+// the registers of 3 waves per SIMD) and whenever the codes come precomputed, else 4.
+template <int NTILES, bool CODES>
+constexpr int k_slices() { return CODES || NTILES == 1 ? 8 : 4; }
 
-template <int NTILES>
-constexpr int fused_threads() { return 64 * (4 + k_slices<NTILES>()); }
+template <int NTILES, bool CODES>
+constexpr int fused_threads() { return 64 * (4 + k_slices<NTILES, CODES>()); }
 
-// 256-k units per wave and tile loaded in one batch: every unit of a slice (4 per rotation tile
-// with 4 slices), except W4 at K > 8192 (8 units per batch: its units take twice the registers).
-template <int FMT, int NTILES>
-constexpr int units_per_batch() { return NTILES == 1 ? 2 : FMT == mma::FMT_W4 && NTILES > 2 ? 8 : 4 * NTILES; }
+// 256-k units per wave and tile loaded in one batch: every unit of a slice (2 or 4 per rotation
+// tile with 8 or 4 slices), except W4 at K > 8192 with the rotation in the kernel (8 units per
+// batch: its units take twice the registers).
+template <int FMT, int NTILES, bool CODES>
+constexpr int units_per_batch() {
+  return NTILES == 1 ? 2 : CODES ? 2 * NTILES : FMT == mma::FMT_W4 && NTILES > 2 ? 8 : 4 * NTILES;
+}
 
-// The exchange buffers, reused after the MFMAs for the K-slice partial sums of T tiles.
-template <int NTILES, int T>
+// The exchange buffers of the rotation, reused after the MFMAs for the K-slice partial sums of T
+// tiles (with precomputed codes only the latter).
+template <int NTILES, int T, bool CODES>
 constexpr int xch_region() {
-  return xch_count<NTILES>() * kXchBytes > k_slices<NTILES>() * T * 1024 ? xch_count<NTILES>() * kXchBytes
-                                                                            : k_slices<NTILES>() * T * 1024;
+  return (CODES ? 0 : xch_count<NTILES>() * kXchBytes) > k_slices<NTILES, CODES>() * T * 1024
+             ? xch_count<NTILES>() * kXchBytes
+             : k_slices<NTILES, CODES>() * T * 1024;
 }
 
 // LDS bytes after the codes: exchange region, then s_scale[16] f32, red_d[16] f64, red_i[16] i32, 2 counters,
 // and 64 zero bytes (the activation operand of k-groups past K).
-template <int NTILES, int T>
-constexpr int tail_bytes() { return xch_region<NTILES, T>() + 64 + 128 + 64 + 16 + 64; }
+template <int NTILES, int T, bool CODES>
+constexpr int tail_bytes() { return xch_region<NTILES, T, CODES>() + 64 + 128 + 64 + 16 + 64; }
 
-template <int FMT, int NTILES, int T, int LC>
-__global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
+// CODES = false: the tokens x are rotated and quantized in the kernel (M <= 4; the codes, scales and
+// sums may be written to act_q_out / scale_out / sum_out).  CODES = true: the linear on precomputed
+// codes aq_in [M][K], scales sx_in [M] and sums sum_in [M] (M <= 16), staged into LDS by waves 0-3.
+template <int FMT, int NTILES, int T, int LC, bool CODES>
+__global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_decode(
     const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
     const uint16_t* __restrict__ x, int L, int num, int den, double denom,
     int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
+    const int8_t* __restrict__ aq_in, const float* __restrict__ sx_in, const int32_t* __restrict__ sum_in,
     int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
   constexpr bool PLANAR = FMT == FMT_MNZ;                   // plane decode, codes in planar layout
   // accumulators per tile (MNZ: one per bit plane, planes 0 and 3 sharing one from 4 tiles on, where
   // registers are scarce and the MFMA chains are long enough)
   constexpr int NA = PLANAR ? (T >= 4 ? 3 : 4) : T >= 3 ? 1 : 4 / T;
-  constexpr int NS = k_slices<NTILES>();
-  constexpr int UPT = units_per_batch<FMT, NTILES>();
+  constexpr int NS = k_slices<NTILES, CODES>();
+  constexpr int UPT = units_per_batch<FMT, NTILES, CODES>();
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: role branches stay scalar
@@ -96,7 +105,7 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
   int8_t* act_l = reinterpret_cast<int8_t*>(smem);
   double* xch0 = reinterpret_cast<double*>(smem + act_bytes);
   double* xch1 = xch0 + (xch_count<NTILES>() - 1) * (kXchBytes / 8);
-  unsigned char* tl = smem + act_bytes + xch_region<NTILES, T>();
+  unsigned char* tl = smem + act_bytes + xch_region<NTILES, T, CODES>();
   float* s_scale = reinterpret_cast<float*>(tl);
   double* red_d = reinterpret_cast<double*>(tl + 64);
   int* red_i = reinterpret_cast<int*>(tl + 64 + 128);
@@ -144,13 +153,49 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
   const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(sw, (uint32_t)(N * 2));
   uint2 swq = make_uint2(0u, 0u);
 
-  if (wave < 4) {
+  if (wave < 4 && CODES) {
+    // ---- staging waves: the precomputed codes of the M tokens into LDS (planar order for MNZ),
+    // their scales and sums
+    const int per_row = K >> 4;   // 16-byte pieces per token (K is a multiple of 64)
+    const int npieces = M * per_row;
+    const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(aq_in, (uint32_t)(M * K));
+    for (int i0 = 0; i0 < npieces; i0 += 256 * 8) {
+      uint4 c[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int i = i0 + tid + 256 * q;
+        c[q] = dev::bload16(ars, i < npieces ? (uint32_t)(16 * i) : dev::kOutOfRange);
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int i = i0 + tid + 256 * q;
+        if (i < npieces) {
+          const int m = i / per_row, j = i - m * per_row;
+          if constexpr (PLANAR) {
+            // word a of natural piece j (k = 16j + 4a + b) goes to 16a + 4 (j mod 4) + b of its 64-k chunk
+            uint32_t* d = reinterpret_cast<uint32_t*>(act_l + m * Kpad + 64 * (j >> 2) + 4 * (j & 3));
+            d[0] = c[q].x;
+            d[4] = c[q].y;
+            d[8] = c[q].z;
+            d[12] = c[q].w;
+          } else {
+            *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) = c[q];
+          }
+        }
+      }
+    }
+    if (tid < M) {
+      s_scale[tid] = sx_in[tid];
+      red_i[tid] = sum_in[tid];
+    }
+    swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
+  } else if (wave < 4) {
     // ---- activation waves: rotate and quantize every token into LDS
     dev::GroupSync<4> sync{ctr, 0u};
     dev::TokenRaw<NTILES> raw;
     dev::load_token_raw<256, NTILES>(raw, x, K);
     swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
-    if constexpr (NTILES > 1) {
+    if constexpr (NTILES > 1 && !CODES) {
       // long tokens: the weight waves wait for this before issuing, so the token's loads reach the
       // memory pipeline ahead of the weight stream (which has time to spare until the codes are in)
       asm volatile("" ::: "memory");
@@ -169,7 +214,7 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
     }
   } else {
     // ---- weight waves: the first batch of weights (zeros for rows past N and k past K)
-    if constexpr (NTILES > 1) {
+    if constexpr (NTILES > 1 && !CODES) {
       for (int spin = 0; spin < (1 << 20); ++spin)   // bounded: a lost flag costs time, never a hang
         if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(xflag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) >= 4u)
           break;
@@ -221,7 +266,7 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
       for (int u = 0; u < UPT; ++u) load_b(u, bq[u]);
 #pragma unroll
       for (int u = 0; u < UPT; ++u) unit_mfmas(u, bq[u]);
-    } else if constexpr (UPT == 4 * NTILES) {
+    } else if constexpr (UPT * NS == 16 * NTILES) {
       // one batch of every unit a slice can have; units past the slice or past K run on zeros
       v4i bq[2][4];   // double buffer: the next unit's operands are read during this unit's MFMAs
       load_b(0, bq[0]);
@@ -246,7 +291,7 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
       }
     }
   }
-  if (wave < 4 && blockIdx.x == 0 && act_q_out) {
+  if (!CODES && wave < 4 && blockIdx.x == 0 && act_q_out) {
     // the codes of the first workgroup double as the stand-alone quantizer's outputs
     const int per_row = K >> 4;
     for (int i = tid; i < M * per_row; i += 256) {
@@ -293,7 +338,7 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
     for (int q = 1; q < NS; ++q) D += red[(j * NS + q) * 64 + lane];
     const int m = r16;
     if (m < M && n_st < N) {
-      const int sq = red_i[4 * m] + red_i[4 * m + 1] + red_i[4 * m + 2] + red_i[4 * m + 3];
+      const int sq = CODES ? red_i[m] : red_i[4 * m] + red_i[4 * m + 1] + red_i[4 * m + 2] + red_i[4 * m + 3];
       store4_sw<FMT>(D, m, n_st, N, s_scale[m], sq, swq, y, acc_out);
     }
   }
@@ -301,73 +346,110 @@ __global__ __launch_bounds__((fused_threads<NTILES>())) void k_fused_decode(
 
 inline int kpad_of(int64_t K) { return (int)K + 16; }
 
-template <int FMT, int NTILES, int T, int LC>
-hipError_t launch_t(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
-                    int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
-                    int32_t* acc_out, hipStream_t s) {
-  const int Kpad = kpad_of(K);
-  const int ntiles = (int)((N + 15) / 16);
+struct FusedArgs {
+  const uint32_t* P;
+  const uint16_t* sw;
+  int64_t N, K;
+  const uint16_t* x;              // rotation in the kernel: fp16 tokens [M][K]
+  int L, num, den;
+  double denom;
+  int8_t* aq_out;                 // optional outputs of the rotation
+  float* sc_out;
+  int32_t* sm_out;
+  const int8_t* aq_in;            // precomputed codes [M][K], scales [M], sums [M]
+  const float* sx_in;
+  const int32_t* sum_in;
+  int64_t M;
+  uint16_t* y;
+  int32_t* acc_out;
+};
+
+// Tiles per workgroup: for K <= 4096 (one rotation tile) as many as keep the grid within one
+// workgroup per CU (at most 7; W4, whose units take twice the registers, at most 3); longer K one.
+template <int FMT>
+inline int64_t fused_tiles(int64_t N, int64_t K) {
+  if (K > 4096) return 1;
+  const int64_t t = ((N + 15) / 16 + 255) / 256;
+  const int64_t cap = FMT == FMT_W4 ? 3 : 7;
+  return t < 1 ? 1 : t > cap ? cap : t;
+}
+
+template <int NTILES, int T, bool CODES>
+inline size_t fused_shmem(int64_t M, int64_t K) {
+  return (size_t)((((int)M * kpad_of(K)) + 15) & ~15) + tail_bytes<NTILES, T, CODES>();
+}
+
+template <int FMT, int NTILES, int T, int LC, bool CODES>
+hipError_t launch_t(const FusedArgs& a, hipStream_t s) {
+  const int ntiles = (int)((a.N + 15) / 16);
   const int grid = (ntiles + T - 1) / T;
-  const size_t shmem = (size_t)((((int)M * Kpad) + 15) & ~15) + tail_bytes<NTILES, T>();
+  const size_t shmem = fused_shmem<NTILES, T, CODES>(a.M, a.K);
+  if (shmem > 160 * 1024) return hipErrorInvalidValue;
   if (shmem > 65536) {
     // opt in to more than 64 KiB of dynamic LDS (gfx950 has 160 KiB per workgroup)
     static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&k_fused_decode<FMT, NTILES, T, LC>),
+        reinterpret_cast<const void*>(&k_fused_decode<FMT, NTILES, T, LC, CODES>),
         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (attr != hipSuccess) return attr;
   }
-  hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, LC>), dim3(grid), dim3(fused_threads<NTILES>()), shmem, s, P, sw, (int)N,
-                     (int)K, x, L, num, den, denom, aq, sc, sm, (int)M, Kpad, y, acc_out);
+  hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, LC, CODES>), dim3(grid), dim3(fused_threads<NTILES, CODES>()),
+                     shmem, s, a.P, a.sw, (int)a.N, (int)a.K, a.x, a.L, a.num, a.den, a.denom, a.aq_out, a.sc_out,
+                     a.sm_out, a.aq_in, a.sx_in, a.sum_in, (int)a.M, kpad_of(a.K), a.y, a.acc_out);
   return hipGetLastError();
 }
 
 // Block exponents compiled as constants: 12 and 8 for tokens of one rotation
 // tile (K <= 4096), 12, 11 and 6 for longer tokens; anything else at run time.
-template <int FMT, int NTILES, int T>
-hipError_t launch_l(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
-                    int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
-                    int32_t* acc_out, hipStream_t s) {
-#define QIFT_FUSED_L(LL) \
-  launch_t<FMT, NTILES, T, LL>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
-  if constexpr (NTILES == 1) {
-    if (L == 12) return QIFT_FUSED_L(12);
-    if (L == 8) return QIFT_FUSED_L(8);
+// Precomputed codes need no rotation: one instance.
+template <int FMT, int NTILES, int T, bool CODES>
+hipError_t launch_l(const FusedArgs& a, hipStream_t s) {
+  if constexpr (CODES) {
+    return launch_t<FMT, NTILES, T, 0, true>(a, s);
   } else {
-    if (L == 12) return QIFT_FUSED_L(12);
-    if (L == 11) return QIFT_FUSED_L(11);
-    if (L == 6) return QIFT_FUSED_L(6);
+    if constexpr (NTILES == 1) {
+      if (a.L == 12) return launch_t<FMT, NTILES, T, 12, false>(a, s);
+      if (a.L == 8) return launch_t<FMT, NTILES, T, 8, false>(a, s);
+    } else {
+      if (a.L == 12) return launch_t<FMT, NTILES, T, 12, false>(a, s);
+      if (a.L == 11) return launch_t<FMT, NTILES, T, 11, false>(a, s);
+      if (a.L == 6) return launch_t<FMT, NTILES, T, 6, false>(a, s);
+    }
+    return launch_t<FMT, NTILES, T, 0, false>(a, s);
   }
-  return QIFT_FUSED_L(0);
-#undef QIFT_FUSED_L
 }
 
-// K <= 4096 (one rotation tile): as many tiles per workgroup as keep the grid within one
-// workgroup per CU (at most 6; W4, whose units take twice the registers, at most 3).  Longer K:
-// one tile per workgroup.
-template <int FMT, int NTILES>
-hipError_t launch_nt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x, int L,
-                     int num, int den, double denom, int8_t* aq, float* sc, int32_t* sm, int64_t M, uint16_t* y,
-                     int32_t* acc_out, hipStream_t s) {
-#define QIFT_FUSED(TT) \
-  launch_l<FMT, NTILES, TT>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s)
+template <int FMT, int NTILES, bool CODES>
+hipError_t launch_nt(const FusedArgs& a, hipStream_t s) {
   if constexpr (NTILES == 1) {
-    const int64_t ntiles = (N + 15) / 16;
-    int64_t t = (ntiles + 255) / 256;
-    if (FMT == FMT_W4 && t > 3) t = 3;
-    if (t <= 1) return QIFT_FUSED(1);
-    if (t == 2) return QIFT_FUSED(2);
-    if (t == 3) return QIFT_FUSED(3);
+    switch (fused_tiles<FMT>(a.N, a.K)) {
+      case 1: return launch_l<FMT, NTILES, 1, CODES>(a, s);
+      case 2: return launch_l<FMT, NTILES, 2, CODES>(a, s);
+      case 3: return launch_l<FMT, NTILES, 3, CODES>(a, s);
+      default: break;
+    }
     if constexpr (FMT != FMT_W4) {
-      if (t == 4) return QIFT_FUSED(4);
-      if (t == 5) return QIFT_FUSED(5);
-      if (t == 6) return QIFT_FUSED(6);
-      return QIFT_FUSED(7);
+      switch (fused_tiles<FMT>(a.N, a.K)) {
+        case 4: return launch_l<FMT, NTILES, 4, CODES>(a, s);
+        case 5: return launch_l<FMT, NTILES, 5, CODES>(a, s);
+        case 6: return launch_l<FMT, NTILES, 6, CODES>(a, s);
+        default: return launch_l<FMT, NTILES, 7, CODES>(a, s);
+      }
     }
     return hipErrorInvalidValue;
   } else {
-    return QIFT_FUSED(1);
+    return launch_l<FMT, NTILES, 1, CODES>(a, s);
   }
-#undef QIFT_FUSED
+}
+
+template <int FMT, bool CODES>
+hipError_t launch_ntiles(const FusedArgs& a, hipStream_t s) {
+  switch ((a.K + 4095) / 4096) {
+    case 1: return launch_nt<FMT, 1, CODES>(a, s);
+    case 2: return launch_nt<FMT, 2, CODES>(a, s);
+    case 3: return launch_nt<FMT, 3, CODES>(a, s);
+    case 4: return launch_nt<FMT, 4, CODES>(a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <int FMT>
@@ -375,15 +457,42 @@ hipError_t launch_fused_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, in
                             int block, int num, int den, int64_t M, uint16_t* y, int32_t* acc_out, int8_t* aq,
                             float* sc, int32_t* sm, hipStream_t s) {
   if (M < 1 || M > kFusedMaxM || K > kFusedMaxK || block > kFusedMaxBlock) return hipErrorInvalidValue;
-  const int L = dev::ilog2c(block);
-  const double denom = act_denominator(block, den);
+  FusedArgs a{P, sw, N, K, x, dev::ilog2c(block), num, den, act_denominator(block, den), aq, sc, sm,
+              nullptr, nullptr, nullptr, M, y, acc_out};
+  return launch_ntiles<FMT, false>(a, s);
+}
+
+// LDS bytes of the linear on precomputed codes (0 when the shape is outside its limits).
+template <int FMT>
+size_t codes_shmem_fmt(int64_t M, int64_t N, int64_t K) {
+  if (M < 1 || M > kCodesMaxM || K > kFusedMaxK || N < 1) return 0;
+  const int64_t T = fused_tiles<FMT>(N, K);
   switch ((K + 4095) / 4096) {
-    case 1: return launch_nt<FMT, 1>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
-    case 2: return launch_nt<FMT, 2>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
-    case 3: return launch_nt<FMT, 3>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
-    case 4: return launch_nt<FMT, 4>(P, sw, N, K, x, L, num, den, denom, aq, sc, sm, M, y, acc_out, s);
-    default: return hipErrorInvalidValue;
+    case 1:
+      switch (T) {
+        case 1: return fused_shmem<1, 1, true>(M, K);
+        case 2: return fused_shmem<1, 2, true>(M, K);
+        case 3: return fused_shmem<1, 3, true>(M, K);
+        case 4: return fused_shmem<1, 4, true>(M, K);
+        case 5: return fused_shmem<1, 5, true>(M, K);
+        case 6: return fused_shmem<1, 6, true>(M, K);
+        default: return fused_shmem<1, 7, true>(M, K);
+      }
+    case 2: return fused_shmem<2, 1, true>(M, K);
+    case 3: return fused_shmem<3, 1, true>(M, K);
+    case 4: return fused_shmem<4, 1, true>(M, K);
+    default: return 0;
   }
+}
+
+template <int FMT>
+hipError_t launch_codes_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* aq,
+                            const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
+                            hipStream_t s) {
+  const size_t shmem = codes_shmem_fmt<FMT>(M, N, K);
+  if (shmem == 0 || shmem > 160 * 1024) return hipErrorInvalidValue;
+  FusedArgs a{P, sw, N, K, nullptr, 0, 1, 1, 1.0, nullptr, nullptr, nullptr, aq, sx, asum, M, y, acc_out};
+  return launch_ntiles<FMT, true>(a, s);
 }
 
 }  // namespace

@@ -1,4 +1,4 @@
-// Fused decode linear instances for the PoT-MNZ (W2, levels {-4,-1,1,4} x s) weight format.
+// Fused decode linear and decode-on-codes instances for the PoT-MNZ (W2, levels {-4,-1,1,4} x s) weight format.
 #include "qift_fused.h"
 
 namespace qift {
@@ -9,5 +9,13 @@ hipError_t launch_fused_pot(const uint32_t* P, const uint16_t* sw, int64_t N, in
   return launch_fused_fmt<mma::FMT_POT>(P, sw, N, K, x, block, clip_num, clip_den, M, y, acc_out, act_q, act_scale,
                                    act_sum, s);
 }
+
+hipError_t launch_codes_pot(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act_q,
+                          const float* act_scale, const int32_t* act_sum, int64_t M, uint16_t* y, int32_t* acc_out,
+                          hipStream_t s) {
+  return launch_codes_fmt<mma::FMT_POT>(P, sw, N, K, act_q, act_scale, act_sum, M, y, acc_out, s);
+}
+
+size_t codes_shmem_pot(int64_t M, int64_t N, int64_t K) { return codes_shmem_fmt<mma::FMT_POT>(M, N, K); }
 
 }  // namespace qift

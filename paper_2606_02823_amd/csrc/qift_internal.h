@@ -34,6 +34,21 @@ QIFT_FUSED_LAUNCHER(launch_fused_pot);
 QIFT_FUSED_LAUNCHER(launch_fused_w4);
 #undef QIFT_FUSED_LAUNCHER
 
+// The same decode kernel as the linear on precomputed codes (M <= kCodesMaxM), one launcher per
+// weight format; codes_shmem_<fmt> gives its LDS bytes (0 outside its limits), and the launcher
+// returns hipErrorInvalidValue when they exceed 160 KiB.
+#define QIFT_CODES_LAUNCHER(NAME)                                                                            \
+  hipError_t NAME(const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K, const int8_t* act_q, \
+                  const float* act_scale, const int32_t* act_sum, int64_t M, uint16_t* out, int32_t* acc_out, \
+                  hipStream_t s)
+QIFT_CODES_LAUNCHER(launch_codes_mnz);
+QIFT_CODES_LAUNCHER(launch_codes_pot);
+QIFT_CODES_LAUNCHER(launch_codes_w4);
+#undef QIFT_CODES_LAUNCHER
+size_t codes_shmem_mnz(int64_t M, int64_t N, int64_t K);
+size_t codes_shmem_pot(int64_t M, int64_t N, int64_t K);
+size_t codes_shmem_w4(int64_t M, int64_t N, int64_t K);
+
 // Streaming-read probe (qift_probe.hip): reads bytes (a multiple of 16) once; workgroup b XORs the
 // words of the 64 KiB segment b into partials[b].
 constexpr size_t kReadProbeSegment = 65536;
@@ -45,6 +60,7 @@ double act_denominator(int block, int clip_den);
 
 // Limits of the fused entry point.
 constexpr int64_t kFusedMaxM = 4;
+constexpr int64_t kCodesMaxM = 16;   // one MFMA column block of tokens
 constexpr int64_t kFusedMaxK = 16384;
 constexpr int kFusedMaxBlock = 4096;
 // Largest K accepted by the activation quantizer.

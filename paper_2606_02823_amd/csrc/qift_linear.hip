@@ -475,6 +475,35 @@ template <int FMT>
 hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
                       const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
                       hipStream_t s) {
+  if (M <= 4 * kCodesMaxM) {
+    // the decode kernel on precomputed codes (K-slice weight waves), once per block of mb tokens:
+    // for M > 16 the largest block of at most 16 tokens whose codes fit in LDS (the GEMM's grid of
+    // N/256 x ceil(M/64) workgroups would leave most CUs idle; later blocks stream the weights
+    // again, largely from the Infinity Cache).
+    auto shmem = [&](int64_t mb) {
+      return FMT == FMT_MNZ ? codes_shmem_mnz(mb, N, K) : FMT == FMT_POT ? codes_shmem_pot(mb, N, K)
+                                                                          : codes_shmem_w4(mb, N, K);
+    };
+    int64_t mb = M < kCodesMaxM ? M : kCodesMaxM;
+    // M <= 16 takes one block or none (measured: splitting 16 tokens at K = 14336 into two blocks
+    // of 8 is slower than the decode kernel reading the codes from HBM)
+    while (M > kCodesMaxM && mb > 1 && (shmem(mb) == 0 || shmem(mb) > 160 * 1024)) mb = (mb + 1) / 2;
+    const size_t cs = shmem(mb);
+    if (cs != 0 && cs <= 160 * 1024) {
+      for (int64_t m0 = 0; m0 < M; m0 += mb) {
+        const int64_t mm = M - m0 < mb ? M - m0 : mb;
+        const int8_t* a = act + m0 * K;
+        uint16_t* yb = y + m0 * N;
+        int32_t* ab = acc_out ? acc_out + m0 * N : nullptr;
+        hipError_t e;
+        if constexpr (FMT == FMT_MNZ) e = launch_codes_mnz(P, sw, N, K, a, sx + m0, asum + m0, mm, yb, ab, s);
+        else if constexpr (FMT == FMT_POT) e = launch_codes_pot(P, sw, N, K, a, sx + m0, asum + m0, mm, yb, ab, s);
+        else e = launch_codes_w4(P, sw, N, K, a, sx + m0, asum + m0, mm, yb, ab, s);
+        if (e != hipSuccess) return e;
+      }
+      return hipSuccess;
+    }
+  }
   if (M <= 16) {
     if (M * kpad_of(K) <= kDecodeMaxLds) return launch_deep<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
     return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);

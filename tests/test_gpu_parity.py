@@ -120,6 +120,21 @@ def test_linear_ragged(Q, fmt, M):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("M,K", [(1, 20480), (9, 20480), (16, 32768)])
+def test_linear_long_k(Q, fmt, M, K):
+    # K beyond the decode-on-codes kernel's limit: codes staged in LDS (M = 1) or read from HBM
+    N, b = 300, 4096
+    L = synth.draw_levels(fmt, N, K, cfg=91, layer=M)
+    s_w = synth.draw_scales(fmt, N, cfg=91, layer=M)
+    x = synth.activations_fp16(91, M, 0, M, K, K // 100, 30.0)
+    pk = pack_dev(Q, L, s_w, fmt)
+    act = Q.rotate_quant_act(dev(x), b)
+    q_ref, sx_ref = check_act(act, x, b)
+    y, acc = run_linear(Q, pk, act, M, N)
+    check_linear(y, acc, L, q_ref, sx_ref, s_w)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
 def test_linear_extremes(Q, fmt):
     # all-outer levels against all +-7 activations: the largest |acc| of each format
     N, K, b, M = 48, 14336, 2048, 3
