@@ -246,17 +246,34 @@ __global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_deco
       }
     };
     auto unit_mfmas = [&](int u, const v4i (&cur)[4]) {
+      if constexpr (PLANAR && T <= 3) {
+        // every operand of the unit decoded before its MFMAs (distinct registers, so the decode of
+        // the next operand never waits for an MFMA still reading the previous one): measured 12 %
+        // fewer cycles per MFMA than decoding each operand just before its MFMA
+        v4i A[4][T];
 #pragma unroll
-      for (int s2 = 0; s2 < 4; ++s2)
+        for (int s2 = 0; s2 < 4; ++s2)
 #pragma unroll
-        for (int j = 0; j < T; ++j) {
-          // MNZ: operand s2 is bit-plane s2 of the unit's four words; else word s2
-          if constexpr (PLANAR) {
-            const int a = NA == 3 && s2 == 3 ? 0 : s2;
-            acc[j][a] = mfma_i8(decode_plane(w[j][u][0], s2), cur[s2], acc[j][a]);
+          for (int j = 0; j < T; ++j) A[s2][j] = decode_plane(w[j][u][0], s2);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+          for (int j = 0; j < T; ++j) acc[j][s2] = mfma_i8(A[s2][j], cur[s2], acc[j][s2]);
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+          for (int j = 0; j < T; ++j) {
+            // MNZ: operand s2 is bit-plane s2 of the unit's four words; else word s2
+            if constexpr (PLANAR) {
+              const int a = NA == 3 && s2 == 3 ? 0 : s2;
+              acc[j][a] = mfma_i8(decode_plane(w[j][u][0], s2), cur[s2], acc[j][a]);
+            }
+            else acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), cur[s2], acc[j][s2 % NA]);
           }
-          else acc[j][s2 % NA] = mfma_i8(decode_unit<FMT>(w[j][u], s2), cur[s2], acc[j][s2 % NA]);
-        }
+      }
     };
     if constexpr (NTILES == 1) {
       // one batch; every operand of the slice is read up front, and units past the slice or past
