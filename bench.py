@@ -509,12 +509,24 @@ def main():
         torch.cuda.synchronize()
         pms = a.elapsed_time(b) / args.prefill_steps
         tops = pre.ops / (pms * 1e-3) / 1e12
+        # per linear shape and weight format: one layer's launch of each, replayed in a graph
+        per_shape = []
+        for layer in sorted({0, args.layers - 1}):
+            fname = "W4" if pre.c.fmt_of_layer[layer] == qift.W4_SYM else "W2 MNZ"
+            for i, (name, N, K, blk, site) in enumerate(pre.plan):
+                w = pre.weights[layer][i]
+                qift.rotate_quant_act(pre.x[i], blk, out=pre.acts[i])
+                dt = _time_graph(torch, lambda: qift.linear(w, pre.acts[i], out=pre.outs[i]), 10)
+                ops = 2 * pre.M * N * K
+                per_shape.append({"linear": name, "format": fname, "N": N, "K": K, "us": round(dt * 1e6, 2),
+                                  "int8_tops": round(ops / dt / 1e12, 2),
+                                  "pct_int8_peak": round(100 * ops / dt / 1e12 / INT8_PEAK_TOPS, 2)})
         out["prefill"] = {"workload": "LLaMA-3.1-8B-shaped prefill, M=2048, layers 0-15 W4 / 16-31 W2 MNZ, "
                                       "4 rotate_quant_act + 4 linears per layer (q|k|v and gate|up stacked "
                                       "along N)",
                           "ms_per_step": round(pms, 3), "int8_tops": round(tops, 2),
                           "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
-                          "steps": args.prefill_steps}
+                          "steps": args.prefill_steps, "per_shape": per_shape}
         pre = None
         torch.cuda.empty_cache()
 
