@@ -273,45 +273,46 @@ __global__ __launch_bounds__(256) void k_decode_deep(
   }
 }
 
-// ===========================================================================
-// Prefill kernel: tiles of 256 weight rows x 16*MTILES*WM tokens.
-//
-// Workgroup = 4*WM waves; wave w owns weight rows [64 (w mod 4), +64) of the
-// tile (4 MFMA row tiles) and the 16*MTILES tokens of its column group
-// w / 4 (MTILES column tiles), i.e. 4*MTILES int32 accumulator tiles.  K
-// advances in 256-k steps: the activation tile [16*MTILES*WM][256] int8 is
-// double-buffered in LDS (global loads for step k+1 are issued before the
-// MFMAs of step k) and shared by all waves, and each wave reads its own
-// packed weights straight into registers (one 16-byte load per lane per row
-// tile: 4 MFMAs' worth of A operands), also one step ahead.  With WM = 2 the
-// two waves on a SIMD hide each other's load latency while the workgroup
-// keeps a 256 x 128 tile (the waves of a column pair read the same weight
-// rows, the second read mostly from cache).
-// ===========================================================================
-constexpr int kGemmBK = 256;
-constexpr int kGemmLdsRow = kGemmBK + 16;   // padded row (bytes) of the LDS activation tile
+constexpr int kGemmBK = 256;   // k per step of the prefill GEMM
 
-template <int FMT, int MTILES, int WM>
-__global__ __launch_bounds__(256 * WM) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
+// ===========================================================================
+// Prefill kernel: tiles of 256 weight rows x 64 tokens, 256-k steps.
+//
+// Workgroup = 4 waves; wave w owns weight rows [64 w, +64) of the tile (4
+// MFMA row tiles) and all 64 tokens (4 column tiles): 16 int32 accumulator
+// tiles.  Each wave reads its own packed weights straight into registers
+// (one 16-byte load per lane per row tile: 4 MFMAs' worth of A operands) one
+// step ahead, alternating between two register sets (the k loop is unrolled
+// by two).  The activation tile [64][256] int8 is double-buffered in LDS and
+// filled one step ahead by direct-to-LDS buffer loads (no staging
+// registers), so a W2 wave fits the registers of 3 waves per SIMD (OCC = 3:
+// three workgroups per CU hide each other's load latency and barriers; W4,
+// with twice the weight registers, runs 2).  The tile has no row padding:
+// the 16-byte column c of row r sits in slot c ^ (r mod 16) of the row, so
+// the 16 rows an MFMA operand read touches fall in distinct banks.  The two
+// buffers are distinct arrays, so the compiler can tell that the loads into
+// one never alias the operand reads from the other and waits for them only
+// at the end of the step.
+// ===========================================================================
+template <int FMT, int OCC>
+__global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                    int N, int K, const int8_t* __restrict__ act,
                                                    const float* __restrict__ sx, const int32_t* __restrict__ asum,
                                                    int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
-  constexpr int NT = 256 * WM;
-  constexpr int BM = 16 * MTILES * WM;
-  constexpr int TILE_BYTES = BM * kGemmLdsRow;
-  constexpr int STAGE_U4 = BM * (kGemmBK / 16) / NT;   // 16-byte activation loads per thread per step
-  __shared__ __align__(16) int8_t lds[2][TILE_BYTES];
+  constexpr int BM = 64;
+  // two distinct arrays (not one indexed by the step's parity), so that the compiler can tell that
+  // the direct-to-LDS loads into one never alias the operand reads from the other
+  __shared__ __align__(16) int8_t lds0[BM * kGemmBK];
+  __shared__ __align__(16) int8_t lds1[BM * kGemmBK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int n_base = blockIdx.x * 256 + (wave & 3) * 64;
+  const int n_base = blockIdx.x * 256 + wave * 64;
   const int m_base = blockIdx.y * BM;
-  const int t_base = (wave >> 2) * MTILES;   // first column tile of this wave
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
   const int KT = (K + kGemmBK - 1) / kGemmBK;
 
-  // weight rows of this lane (one per row tile); zeros for rows past N and k past K
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
   uint32_t rowoff[4];
   bool rowok[4];
@@ -331,76 +332,70 @@ __global__ __launch_bounds__(256 * WM) void k_gemm(const uint32_t* __restrict__ 
       for (int h = 0; h < NH; ++h) w[j][h] = dev::bload16(wrs, off + 16 * h);
     }
   };
-  // activation staging: thread tid moves 16-byte pieces i = tid + NT q of the [BM][256] tile
-  // (the activation block of this workgroup's tokens; zeros past M and K)
+  // activation tile of step kt into lds[buf]: wave w moves rows 16w .. 16w + 15 (4 loads of 1 KB, 4
+  // rows each; lane l of a load fills slot l of the kilobyte, i.e. row 4q + l / 16, slot l mod 16)
   const int mrows = M - m_base < BM ? M - m_base : BM;
   const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act + (int64_t)m_base * K, (uint32_t)(mrows * K));
-  auto load_a = [&](uint4 (&st)[STAGE_U4], int kt) {
+  auto issue_a = [&](int kt, int8_t* dst) {
 #pragma unroll
-    for (int q = 0; q < STAGE_U4; ++q) {
-      const int i = tid + NT * q;
-      const int row = i >> 4, col = (i & 15) * 16;
-      const int k = kt * kGemmBK + col;
-      st[q] = dev::bload16(ars, (row < mrows && k < K) ? (uint32_t)(row * K + k) : dev::kOutOfRange);
-    }
-  };
-  auto store_a = [&](const uint4 (&st)[STAGE_U4], int buf) {
-#pragma unroll
-    for (int q = 0; q < STAGE_U4; ++q) {
-      const int i = tid + NT * q;
-      const int row = i >> 4, col = (i & 15) * 16;
-      *reinterpret_cast<uint4*>(&lds[buf][row * kGemmLdsRow + col]) = st[q];
+    for (int q = 0; q < 4; ++q) {
+      const int chunk = 4 * wave + q;
+      const int row = 4 * chunk + (lane >> 4);
+      const int col = (lane & 15) ^ (row & 15);
+      const int k = kt * kGemmBK + 16 * col;
+      const uint32_t off = row < mrows && k < K ? (uint32_t)(row * K + k) : dev::kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ars, (__attribute__((address_space(3))) void*)(dst + 1024 * chunk), 16, off, 0, 0, 0);
     }
   };
 
-  v4i acc[4][MTILES];
+  v4i acc[4][4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int t = 0; t < MTILES; ++t) acc[j][t] = v4i{0, 0, 0, 0};
+    for (int t = 0; t < 4; ++t) acc[j][t] = v4i{0, 0, 0, 0};
 
-  uint4 wcur[4][NH], wnxt[4][NH];
-  uint4 st[STAGE_U4];
-  load_w(wcur, 0);
-  load_a(st, 0);
-  store_a(st, 0);
-  __syncthreads();
-
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
+  // one step: prefetch step kt+1 (activations into lds[buf ^ 1], weights into wn), MFMAs of step kt
+  // from lds[buf] and wc; the k loop is unrolled by two so the weight registers alternate instead of
+  // being copied
+  auto step = [&](int kt, const int8_t* tileb, int8_t* nextb, const uint4 (&wc)[4][NH], uint4 (&wn)[4][NH]) {
     const bool more = kt + 1 < KT;
     if (more) {
-      load_w(wnxt, kt + 1);
-      load_a(st, kt + 1);
+      issue_a(kt + 1, nextb);   // the other buffer: every wave finished reading it before the last barrier
+      load_w(wn, kt + 1);
     }
-    const int8_t* tileb = lds[buf];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       v4i a[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) a[j] = decode_unit<FMT>(wcur[j], s);
+      for (int j = 0; j < 4; ++j) a[j] = decode_unit<FMT>(wc[j], s);
 #pragma unroll
-      for (int t = 0; t < MTILES; ++t) {
-        const uint4 bb =
-            *reinterpret_cast<const uint4*>(&tileb[(16 * (t_base + t) + r16) * kGemmLdsRow + 64 * g + 16 * s]);
+      for (int t = 0; t < 4; ++t) {
+        const int row = 16 * t + r16;
+        const uint4 bb = *reinterpret_cast<const uint4*>(&tileb[row * kGemmBK + 16 * ((4 * g + s) ^ (row & 15))]);
         const v4i b = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[j][t] = mfma_i8(a[j], b, acc[j][t]);
       }
     }
-    if (more) {
-      store_a(st, buf ^ 1);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int h = 0; h < NH; ++h) wcur[j][h] = wnxt[j][h];
-    }
+    // this wave's loads of step kt+1 have landed (vmcnt(0) with lgkmcnt and expcnt untouched)
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
+  };
+
+  uint4 wa[4][NH], wb[4][NH];
+  issue_a(0, lds0);
+  load_w(wa, 0);
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  for (int kt = 0; kt < KT; kt += 2) {
+    step(kt, lds0, lds1, wa, wb);
+    if (kt + 1 < KT) step(kt + 1, lds1, lds0, wb, wa);
   }
 
 #pragma unroll
-  for (int t = 0; t < MTILES; ++t) {
-    const int m = m_base + 16 * (t_base + t) + r16;
+  for (int t = 0; t < 4; ++t) {
+    const int m = m_base + 16 * t + r16;
     if (m < M) {
       const float s_x = sx[m];
       const int sq = asum[m];
@@ -509,12 +504,12 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
     return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
   }
   const unsigned gx = (unsigned)((N + 255) / 256);
-  // 256 x 64 tiles at every M: two workgroups per CU (2 waves per SIMD) hide each other's load
-  // latency and barriers.  Measured slower at M = 2048: one-wave-per-SIMD 256 x 128 tiles (with 4 or
-  // 8 waves per workgroup), 256 x 32 tiles, and a variant staging the activations through a 3-stage
-  // LDS ring with direct-to-LDS loads and the weights two steps ahead
-  hipLaunchKernelGGL((k_gemm<FMT, 4, 1>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P, sw, (int)N,
-                     (int)K, act, sx, asum, (int)M, y, acc_out);
+  // 256 x 64 tiles at every M, 3 (W2) or 2 (W4) workgroups per CU.  Measured slower at M = 2048:
+  // one-wave-per-SIMD 256 x 128 tiles (with 4 or 8 waves per workgroup), 256 x 32 tiles, activations
+  // staged through registers (2 workgroups per CU: W2 q,k,v 72 -> 58 us, gate,up 272 -> 228 us with
+  // direct-to-LDS loads at 3 per CU), and W4 at 3 per CU (register spills)
+  hipLaunchKernelGGL((k_gemm<FMT, FMT == FMT_W4 ? 2 : 3>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P,
+                     sw, (int)N, (int)K, act, sx, asum, (int)M, y, acc_out);
   return hipGetLastError();
 }
 
