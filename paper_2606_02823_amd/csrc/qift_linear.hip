@@ -273,45 +273,63 @@ __global__ __launch_bounds__(256) void k_decode_deep(
   }
 }
 
-constexpr int kGemmBK = 256;   // k per step of the prefill GEMM
+// k per step of the prefill GEMM: every lane loads one 16-byte group of each of its weight rows per
+// step (64 W2 or 32 W4 weights), i.e. S MFMA operands of 16 k per lane group
+template <int FMT>
+constexpr int gemm_ops() { return FMT == FMT_W4 ? 2 : 4; }
+template <int FMT>
+constexpr int gemm_bk() { return 64 * gemm_ops<FMT>(); }
+
+// MFMA operand s of a lane's 16-byte weight group: 16 weights as int8 bytes in natural k order
+template <int FMT>
+__device__ __forceinline__ v4i gemm_operand(const uint4& u, int s) {
+  if constexpr (FMT == FMT_W4) return s ? decode_w4(u.z, u.w) : decode_w4(u.x, u.y);
+  else return decode_w2<FMT>(s == 0 ? u.x : s == 1 ? u.y : s == 2 ? u.z : u.w);
+}
 
 // ===========================================================================
-// Prefill kernel: tiles of 256 weight rows x 64 tokens, 256-k steps.
+// Prefill kernel: tiles of 256 weight rows x 16 TT tokens, BK-k steps (BK = 256 for W2, 128 for W4).
 //
 // Workgroup = 4 waves; wave w owns weight rows [64 w, +64) of the tile (4
-// MFMA row tiles) and all 64 tokens (4 column tiles): 16 int32 accumulator
+// MFMA row tiles) and all tokens (TT column tiles): 4 TT int32 accumulator
 // tiles.  Each wave reads its own packed weights straight into registers
-// (one 16-byte load per lane per row tile: 4 MFMAs' worth of A operands) one
-// step ahead, alternating between two register sets (the k loop is unrolled
-// by two).  The activation tile [64][256] int8 is double-buffered in LDS and
-// filled one step ahead by direct-to-LDS buffer loads (no staging
-// registers), so a W2 wave fits the registers of 3 waves per SIMD (OCC = 3:
-// three workgroups per CU hide each other's load latency and barriers; W4,
-// with twice the weight registers, runs 2).  The tile has no row padding:
-// the 16-byte column c of row r sits in slot c ^ (r mod 16) of the row, so
-// the 16 rows an MFMA operand read touches fall in distinct banks.  The two
-// buffers are distinct arrays, so the compiler can tell that the loads into
-// one never alias the operand reads from the other and waits for them only
-// at the end of the step.
+// (one 16-byte load per lane per row tile and step: S MFMAs' worth of A
+// operands) one step ahead, alternating between two register sets (the k
+// loop is unrolled by two).  W4 steps over half as many k as W2, so both
+// formats hold the same weight registers and a wave fits 3 per SIMD (OCC =
+// 3: three workgroups per CU hide each other's load latency and barriers).
+// The activation tile [16 TT][BK] int8 is double-buffered in LDS and filled
+// one step ahead by direct-to-LDS buffer loads (no staging registers).  The
+// tile has no row padding: the 16-byte column c of row r sits in slot
+// c ^ (r mod SL) of the row (SL = BK / 16 slots), which spreads the rows an
+// MFMA operand read touches over the banks.  The two buffers are distinct
+// arrays, so the compiler can tell that the loads into one never alias the
+// operand reads from the other and waits for them only at the end of the
+// step.
 // ===========================================================================
-template <int FMT, int OCC>
+template <int FMT, int OCC, int TT>
 __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                    int N, int K, const int8_t* __restrict__ act,
                                                    const float* __restrict__ sx, const int32_t* __restrict__ asum,
                                                    int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
-  constexpr int NH = FMT == FMT_W4 ? 2 : 1;
-  constexpr int BM = 64;
+  constexpr int S = gemm_ops<FMT>();
+  constexpr int BK = gemm_bk<FMT>();
+  constexpr int SL = BK / 16;            // 16-byte slots per activation row
+  constexpr int RPC = 1024 / BK;         // activation rows per direct-to-LDS load (1 KB)
+  constexpr int BM = 16 * TT;            // tokens per workgroup: every wave covers all of them
+  constexpr int NQ = BM * BK / 4096;     // direct-to-LDS loads per wave and step
+  static_assert(NQ >= 1 && RPC * SL == 64, "tile geometry");
   // two distinct arrays (not one indexed by the step's parity), so that the compiler can tell that
   // the direct-to-LDS loads into one never alias the operand reads from the other
-  __shared__ __align__(16) int8_t lds0[BM * kGemmBK];
-  __shared__ __align__(16) int8_t lds1[BM * kGemmBK];
+  __shared__ __align__(16) int8_t lds0[BM * BK];
+  __shared__ __align__(16) int8_t lds1[BM * BK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int n_base = blockIdx.x * 256 + wave * 64;
   const int m_base = blockIdx.y * BM;
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
-  const int KT = (K + kGemmBK - 1) / kGemmBK;
+  const int KT = (K + BK - 1) / BK;
 
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
   uint32_t rowoff[4];
@@ -322,57 +340,57 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
     rowok[j] = n < N;
     rowoff[j] = (uint32_t)(n * rowbytes);
   }
-  auto load_w = [&](uint4 (&w)[4][NH], int kt) {
-    const int k0 = kt * kGemmBK + 64 * g;
+  // lane group g of step kt covers k = kt BK + (BK / 4) g .. + BK / 4 - 1: 16 bytes of either format
+  auto load_w = [&](uint4 (&w)[4], int kt) {
+    const int k0 = kt * BK + (BK / 4) * g;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const bool ok = rowok[j] && k0 < K;
-      const uint32_t off = ok ? rowoff[j] + (uint32_t)(FMT == FMT_W4 ? k0 / 2 : k0 / 4) : dev::kOutOfRange;
-#pragma unroll
-      for (int h = 0; h < NH; ++h) w[j][h] = dev::bload16(wrs, off + 16 * h);
+      w[j] = dev::bload16(wrs, ok ? rowoff[j] + (uint32_t)(64 * kt + 16 * g) : dev::kOutOfRange);
     }
   };
-  // activation tile of step kt into lds[buf]: wave w moves rows 16w .. 16w + 15 (4 loads of 1 KB, 4
-  // rows each; lane l of a load fills slot l of the kilobyte, i.e. row 4q + l / 16, slot l mod 16)
+  // activation tile of step kt into lds[buf]: wave w moves rows RPC NQ w .. RPC NQ (w + 1) - 1 (NQ loads
+  // of 1 KB, RPC rows each; lane l of a load fills slot l of the kilobyte, i.e. row RPC q + l / SL,
+  // slot l mod SL)
   const int mrows = M - m_base < BM ? M - m_base : BM;
   const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act + (int64_t)m_base * K, (uint32_t)(mrows * K));
   auto issue_a = [&](int kt, int8_t* dst) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int chunk = 4 * wave + q;
-      const int row = 4 * chunk + (lane >> 4);
-      const int col = (lane & 15) ^ (row & 15);
-      const int k = kt * kGemmBK + 16 * col;
+    for (int q = 0; q < NQ; ++q) {
+      const int chunk = NQ * wave + q;
+      const int row = RPC * chunk + lane / SL;
+      const int col = (lane % SL) ^ (row % SL);
+      const int k = kt * BK + 16 * col;
       const uint32_t off = row < mrows && k < K ? (uint32_t)(row * K + k) : dev::kOutOfRange;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           ars, (__attribute__((address_space(3))) void*)(dst + 1024 * chunk), 16, off, 0, 0, 0);
     }
   };
 
-  v4i acc[4][4];
+  v4i acc[4][TT];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[j][t] = v4i{0, 0, 0, 0};
+    for (int t = 0; t < TT; ++t) acc[j][t] = v4i{0, 0, 0, 0};
 
   // one step: prefetch step kt+1 (activations into lds[buf ^ 1], weights into wn), MFMAs of step kt
   // from lds[buf] and wc; the k loop is unrolled by two so the weight registers alternate instead of
-  // being copied
-  auto step = [&](int kt, const int8_t* tileb, int8_t* nextb, const uint4 (&wc)[4][NH], uint4 (&wn)[4][NH]) {
+  // being copied.  MFMA s of lane group g covers k = kt BK + 16 (S g + s) .. + 15 (slot S g + s).
+  auto step = [&](int kt, const int8_t* tileb, int8_t* nextb, const uint4 (&wc)[4], uint4 (&wn)[4]) {
     const bool more = kt + 1 < KT;
     if (more) {
       issue_a(kt + 1, nextb);   // the other buffer: every wave finished reading it before the last barrier
       load_w(wn, kt + 1);
     }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < S; ++s) {
       v4i a[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) a[j] = decode_unit<FMT>(wc[j], s);
+      for (int j = 0; j < 4; ++j) a[j] = gemm_operand<FMT>(wc[j], s);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+      for (int t = 0; t < TT; ++t) {
         const int row = 16 * t + r16;
-        const uint4 bb = *reinterpret_cast<const uint4*>(&tileb[row * kGemmBK + 16 * ((4 * g + s) ^ (row & 15))]);
+        const uint4 bb = *reinterpret_cast<const uint4*>(&tileb[row * BK + 16 * ((S * g + s) ^ (row % SL))]);
         const v4i b = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[j][t] = mfma_i8(a[j], b, acc[j][t]);
@@ -383,7 +401,7 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
     __syncthreads();
   };
 
-  uint4 wa[4][NH], wb[4][NH];
+  uint4 wa[4], wb[4];
   issue_a(0, lds0);
   load_w(wa, 0);
   __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -394,7 +412,7 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
   }
 
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
+  for (int t = 0; t < TT; ++t) {
     const int m = m_base + 16 * t + r16;
     if (m < M) {
       const float s_x = sx[m];
@@ -504,12 +522,21 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
     return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
   }
   const unsigned gx = (unsigned)((N + 255) / 256);
-  // 256 x 64 tiles at every M, 3 (W2) or 2 (W4) workgroups per CU.  Measured slower at M = 2048:
-  // one-wave-per-SIMD 256 x 128 tiles (with 4 or 8 waves per workgroup), 256 x 32 tiles, activations
-  // staged through registers (2 workgroups per CU: W2 q,k,v 72 -> 58 us, gate,up 272 -> 228 us with
-  // direct-to-LDS loads at 3 per CU), and W4 at 3 per CU (register spills)
-  hipLaunchKernelGGL((k_gemm<FMT, FMT == FMT_W4 ? 2 : 3>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P,
-                     sw, (int)N, (int)K, act, sx, asum, (int)M, y, acc_out);
+  // 256 x 64 tiles, three workgroups per CU.  W4 on grids that fill the chip at least twice over with
+  // 256 x 128 tiles (two per CU) takes those instead: half the weight loads and decode per MFMA
+  // (stacked gate|up at M = 2048: 318 -> 264 us).  W2 does not gain from them (222 -> 225 us), and
+  // smaller grids lose to the idle CUs (q,k,v W4 74 -> 78 us).  Also measured slower at M = 2048: 256 x 32 tiles and activations staged through
+  // registers.
+  if constexpr (FMT == FMT_W4) {
+    const unsigned gy8 = (unsigned)((M + 127) / 128);
+    if ((uint64_t)gx * gy8 >= 1024) {
+      hipLaunchKernelGGL((k_gemm<FMT, 2, 8>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum,
+                         (int)M, y, acc_out);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((k_gemm<FMT, 3, 4>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P, sw, (int)N,
+                     (int)K, act, sx, asum, (int)M, y, acc_out);
   return hipGetLastError();
 }
 

@@ -275,6 +275,33 @@ def test_cfg4_prefill_sampled(Q, fmt, name):
     _config_linear(Q, 4, layer, shp, fmt, 2048, rows=rows, tokens=tokens)
 
 
+@pytest.mark.parametrize("fmt", [levels.FMT_W4_SYM, levels.FMT_W2_MNZ])
+def test_cfg4_row_concatenated(Q, fmt):
+    # gate|up stacked along N (28672 rows), as the prefill benchmark launches it: the widest GEMM grid
+    shp = synth.LinearShape("gate", 28672, 4096, 4096)
+    layer = 1 if fmt == levels.FMT_W4_SYM else 17
+    rng = np.random.default_rng(7 + fmt)
+    rows = np.sort(rng.choice(shp.N, size=96, replace=False))
+    rows[0], rows[-1] = 0, shp.N - 1
+    tokens = np.sort(rng.choice(2048, size=48, replace=False))
+    tokens[0], tokens[-1] = 0, 2047
+    _config_linear(Q, 4, layer, shp, fmt, 2048, rows=rows, tokens=tokens)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_linear_wide_grid_ragged(Q, fmt):
+    # a grid wide enough for the 128-token W4 tiles, with ragged rows, tokens and a half k-step
+    N, K, b, M = 16400, 1088, 64, 2000
+    L = synth.draw_levels(fmt, N, K, cfg=94)
+    s_w = synth.draw_scales(fmt, N, cfg=94)
+    x = synth.activations_fp16(94, 0, 0, M, K, 11, 30.0)
+    pk = pack_dev(Q, L, s_w, fmt)
+    act = Q.rotate_quant_act(dev(x), b)
+    q_ref, sx_ref = check_act(act, x, b)
+    y, acc = run_linear(Q, pk, act, M, N)
+    check_linear(y, acc, L, q_ref, sx_ref, s_w)
+
+
 def test_linear_deterministic(Q):
     N, K, M = 4096, 14336, 16
     L = synth.draw_levels(levels.FMT_W2_MNZ, N, K, cfg=93)
