@@ -47,6 +47,11 @@ DECODE_KERNEL_FUSED = "k_fused_decode<0, *, *, *>"   # MNZ decode kernel with th
 DECODE_KERNEL = "k_decode_deep<0, 1, 1, *>"          # MNZ decode kernel on staged act_q
 
 
+def _stage(name: str) -> None:
+    """Progress marker on stderr (stdout carries only the JSON line)."""
+    print(f"[bench] {name}", file=sys.stderr, flush=True)
+
+
 def _sources_hash() -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_02823_amd", "csrc")
@@ -413,6 +418,7 @@ def main():
     torch.cuda.set_device(0)
 
     # ---------------------------------------------------------------- decode (headline)
+    _stage("decode step")
     dec = DecodeStack(torch, qift, synth, layers=args.layers, M=1, fused=not args.unfused)
     dec.setup()
     dec.step()                                   # eager warm-up
@@ -486,17 +492,20 @@ def main():
 
     # ---------------------------------------------------------------- per-shape loops, read probe
     if not args.no_per_shape:
+        _stage("read probe and per-shape decode loops")
         out["read_probe"] = read_probe(torch, qift)
         out["decode_per_shape"] = decode_per_shape(torch, qift, synth)
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- cfg2 / cfg3 stacks at several M
     if not args.no_sweep:
+        _stage("stack sweep")
         out["stack_sweep"] = stack_sweep(torch, qift, synth)
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- prefill
     if not args.no_prefill:
+        _stage("prefill")
         pre = PrefillStack(torch, qift, synth, layers=args.layers)
         pre.setup()
         pre.step()
@@ -531,6 +540,7 @@ def main():
         torch.cuda.empty_cache()
 
     if args.copy_probe:
+        _stage("copy probe")
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(4):
@@ -540,6 +550,7 @@ def main():
 
     # ---------------------------------------------------------------- CPU oracle baseline
     if not args.no_cpu:
+        _stage("cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline(synth)
     else:
         out["cpu_baseline"] = None
