@@ -324,7 +324,8 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
   __shared__ __align__(16) int8_t lds0[BM * BK];
   __shared__ __align__(16) int8_t lds1[BM * BK];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index as a scalar, so that the LDS destinations of the direct-to-LDS loads are scalar too
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int n_base = blockIdx.x * 256 + wave * 64;
   const int m_base = blockIdx.y * BM;
@@ -332,36 +333,43 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
   const int KT = (K + BK - 1) / BK;
 
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
-  uint32_t rowoff[4];
-  bool rowok[4];
+  // Load offsets are a per-lane base (the out-of-range offset for rows past N, which stays out of
+  // range with any step's k added) plus the step's k offset.  Lane group g of step kt covers
+  // k = kt BK + (BK / 4) g .. + BK / 4 - 1: bytes 64 kt + 16 g .. + 15 of the row in either format.
+  // In a last step past K the lanes beyond K read the next row (or zeros): their activations are
+  // zero, so those weights add nothing.
+  uint32_t wbase[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int n = n_base + 16 * j + r16;
-    rowok[j] = n < N;
-    rowoff[j] = (uint32_t)(n * rowbytes);
+    wbase[j] = n < N ? (uint32_t)(n * rowbytes) + 16u * g : dev::kOutOfRange;
   }
-  // lane group g of step kt covers k = kt BK + (BK / 4) g .. + BK / 4 - 1: 16 bytes of either format
   auto load_w = [&](uint4 (&w)[4], int kt) {
-    const int k0 = kt * BK + (BK / 4) * g;
+    const uint32_t ko = 64u * (uint32_t)kt;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const bool ok = rowok[j] && k0 < K;
-      w[j] = dev::bload16(wrs, ok ? rowoff[j] + (uint32_t)(64 * kt + 16 * g) : dev::kOutOfRange);
-    }
+    for (int j = 0; j < 4; ++j) w[j] = dev::bload16(wrs, wbase[j] + ko);
   };
   // activation tile of step kt into lds[buf]: wave w moves rows RPC NQ w .. RPC NQ (w + 1) - 1 (NQ loads
   // of 1 KB, RPC rows each; lane l of a load fills slot l of the kilobyte, i.e. row RPC q + l / SL,
   // slot l mod SL)
   const int mrows = M - m_base < BM ? M - m_base : BM;
   const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act + (int64_t)m_base * K, (uint32_t)(mrows * K));
+  uint32_t abase[NQ];   // row K + 16 col, or out of range for rows past M
+  int acol[NQ];         // 16 col: the lane's k inside a step
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int row = RPC * (NQ * wave + q) + lane / SL;
+    acol[q] = 16 * ((lane % SL) ^ (row % SL));
+    abase[q] = row < mrows ? (uint32_t)(row * K + acol[q]) : dev::kOutOfRange;
+  }
   auto issue_a = [&](int kt, int8_t* dst) {
+    const int ko = kt * BK;
+    const bool tail = ko + BK > K;   // the last step of a K that is not a multiple of BK
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int chunk = NQ * wave + q;
-      const int row = RPC * chunk + lane / SL;
-      const int col = (lane % SL) ^ (row % SL);
-      const int k = kt * BK + 16 * col;
-      const uint32_t off = row < mrows && k < K ? (uint32_t)(row * K + k) : dev::kOutOfRange;
+      uint32_t off = abase[q] + (uint32_t)ko;
+      if (tail && acol[q] + ko >= K) off = dev::kOutOfRange;   // columns past K read as zeros
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           ars, (__attribute__((address_space(3))) void*)(dst + 1024 * chunk), 16, off, 0, 0, 0);
     }
