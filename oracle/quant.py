@@ -160,12 +160,15 @@ def quantize_pot_mse(W_rot: np.ndarray):
 
 
 def rne(v: np.ndarray) -> np.ndarray:
-    """Round half to even, written out: floor(v + 1/2), lowered by one on an exact half with odd result."""
+    """Round half to even, written out on |v| (the rounding is odd-symmetric): f = floor(|v|) and the
+    fractional part |v| - f, which is exact in fp64; round up when it exceeds 1/2, or equals 1/2 with
+    f odd.  (Adding 1/2 before the floor would itself round for |v| within an ulp below a half.)"""
     v = np.asarray(v, dtype=np.float64)
-    f = np.floor(v + 0.5)
-    half = (f - v) == 0.5
-    odd = np.mod(f, 2.0) == 1.0
-    return f - (half & odd)
+    a = np.abs(v)
+    f = np.floor(a)
+    frac = a - f
+    up = (frac > 0.5) | ((frac == 0.5) & (np.mod(f, 2.0) == 1.0))
+    return np.copysign(f + up, v)
 
 
 def quantize_w4_absmax(W_rot: np.ndarray):

@@ -57,6 +57,23 @@ def test_w4_hand_case_and_ties():
     assert quant.rne(np.array([0.5, 1.5, 2.5, -2.5, 2.4999, -0.5])).tolist() == [0, 2, 2, -2, 2, 0]
 
 
+def test_rne_exact_next_to_halves():
+    # values an ulp away from a half round by which side of the half they are on (Eq. (1) with the
+    # round-half-to-even reading), and integers stay put even where adding 1/2 first would itself
+    # round (odd integers from 2^52 on)
+    below = np.nextafter(0.5, 0.0)
+    hand = {below: 0.0, -below: 0.0, np.nextafter(1.5, 0.0): 1.0, np.nextafter(2.5, 3.0): 3.0,
+            np.nextafter(-2.5, -3.0): -3.0, 0.5: 0.0, 1.5: 2.0, 2.5: 2.0, 3.5: 4.0, -1.5: -2.0,
+            2.0 ** 52 + 1.0: 2.0 ** 52 + 1.0, -(2.0 ** 52 + 3.0): -(2.0 ** 52 + 3.0), 6.5: 6.0, -6.5: -6.0, 7.4999: 7.0}
+    got = quant.rne(np.array(list(hand)))
+    assert got.tolist() == list(hand.values())
+    # against IEEE rint, an independent implementation, on values crowded around halves
+    rng = np.random.default_rng(5)
+    k = rng.integers(-20, 20, 4000).astype(np.float64) + 0.5
+    v = np.concatenate([k, np.nextafter(k, np.inf), np.nextafter(k, -np.inf), rng.normal(0, 8, 4000)])
+    assert np.array_equal(quant.rne(v), np.rint(v))
+
+
 def test_pot_search_matches_bruteforce_candidates():
     rng = np.random.default_rng(2)
     W = 0.02 * rng.standard_t(5, size=(6, 256))
