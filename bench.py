@@ -347,6 +347,56 @@ def decode_per_shape(torch, qift, synth, min_bytes=1 << 30, reps=10):
     return rows
 
 
+FP64_VECTOR_PEAK_TFLOPS = 78.6
+POT_FLOPS_PER_WEIGHT = 64 * 5   # per candidate: w / s, compare, s * level, w - s * level, d * d + acc
+
+
+def weight_quantizer(torch, qift, synth, reps=5):
+    """The GPU weight quantizer on one LLaMA-3.1-8B layer (its 7 linears, 218M fp32 weights) per
+    format: rotation, per-row scale and levels (the offline step before packing; hipGraph replays,
+    weights resident).  MNZ and W4 move 4 B in + 1 B out per weight (HBM roofline); the PoT scale
+    search is fp64 arithmetic, priced at 5 flops per candidate and weight against the fp64 vector
+    peak."""
+    c = synth.CONFIGS[2]
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2)
+    mats = []
+    for s in c.linears:
+        # 0.02 * Student-t(5): z / sqrt(chi2_5 / 5)
+        z = torch.randn((s.N, s.K), device=dev, generator=gen)
+        chi = torch.zeros_like(z)
+        for _ in range(5):
+            chi.add_(torch.randn((s.N, s.K), device=dev, generator=gen).square_())
+        W = (0.02 * z / torch.sqrt(chi / 5.0)).contiguous()
+        del z, chi
+        mats.append((W, s.block, torch.empty((s.N, s.K), dtype=torch.int8, device=dev),
+                     torch.empty(s.N, dtype=torch.float16, device=dev)))
+    weights = sum(W.numel() for W, *_ in mats)
+    rows = sum(W.shape[0] for W, *_ in mats)
+    out = {"workload": "one LLaMA-3.1-8B layer: q, k, v, o, gate, up, down (218,103,808 fp32 weights; "
+                       "4096 blocks for K 4096, 7 blocks of 2048 for K 14336)"}
+    for fmt, name in ((qift.W2_MNZ, "W2 MNZ (RMS)"), (qift.W2_POT, "W2 PoT (64-candidate MSE)"),
+                      (qift.W4_SYM, "W4 (absmax/7)")):
+        def layer():
+            for W, b, L, S in mats:
+                qift.quantize_weights(W, b, fmt, levels=L, scales=S)
+        dt = _time_graph(torch, layer, reps)
+        gbs = (5 * weights + 2 * rows) / dt / 1e9
+        rec = {"ms_per_layer": round(dt * 1e3, 3), "gweights_per_s": round(weights / dt / 1e9, 2),
+               "GBs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)}
+        if fmt == qift.W2_POT:
+            tf = POT_FLOPS_PER_WEIGHT * weights / dt / 1e12
+            rec["roofline"] = {"bound": "alu", "achieved": round(tf, 2), "peak": FP64_VECTOR_PEAK_TFLOPS,
+                               "unit": "TFLOP/s", "frac": round(tf / FP64_VECTOR_PEAK_TFLOPS, 4)}
+        else:
+            rec["roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        out[name] = rec
+    del mats
+    return out
+
+
 def cpu_baseline(synth, budget_s=20.0):
     """The oracle as it stands, on one cfg1 layer at M=1 (4 act quantizations + 7 linears)."""
     import numpy as np
@@ -402,6 +452,7 @@ def main():
                     help="decode step as separate rotate_quant_act + w2a4_linear launches")
     ap.add_argument("--no-per-shape", action="store_true",
                     help="skip the per-shape replica loops and the read probe")
+    ap.add_argument("--no-wquant", action="store_true", help="skip the weight quantizer timing")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the cfg2 (M 1/4/16) and cfg3 PoT (M 1/8/64) stack sweep")
     ap.add_argument("--copy-probe", action="store_true",
@@ -501,6 +552,12 @@ def main():
     if not args.no_sweep:
         _stage("stack sweep")
         out["stack_sweep"] = stack_sweep(torch, qift, synth)
+        torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- offline weight quantizer
+    if not args.no_wquant:
+        _stage("weight quantizer")
+        out["weight_quantizer"] = weight_quantizer(torch, qift, synth)
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- prefill

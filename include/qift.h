@@ -145,6 +145,36 @@ int qift_pack_w4(const int8_t *levels, const uint16_t *scales, int64_t N, int64_
                  qift_stream_t stream);
 
 /*
+ * Offline weight quantization, the step before packing (Sec. 3.1 rotation;
+ * Sec. 3.3, Sec. 3.5 and Sec. 4.5.1 per-channel scales; Eq. (1) for W4).
+ * For each row n of W:
+ *   w      = (I_{K/b} (x) H_b) W[n, :] / sqrt(b)   in fp64 (the orthonormal
+ *            rotation that the online activation rotation undoes);
+ *   MNZ    s_w = fp16(RMS(w) / 2); level +3 if w/s_w > 2, +1 if 0 <= w/s_w
+ *          <= 2, -1 if -2 <= w/s_w < 0, -3 below (Eqs. (13)-(14));
+ *   PoT    s_w = fp16(c* max|w| / 4) with c* the first minimiser over the 64
+ *          candidates c_j = 0.2 + 0.8 j / 63 of sum (w - s level)^2; level
+ *          sign(w) * (4 if |w/s| > 5/2 else 1), sign(0) = + (Eq. (17));
+ *   W4     s_w = fp16(max|w| / 7), q = clip(rne(w / s_w), -7, 7) (Eq. (1)).
+ * fp16 means round to nearest, ties to even; levels are assigned against the
+ * stored fp16 scale; a row whose stored scale is 0 gets level +1 (W2) or 0
+ * (W4).  The rotation of fp32 rows is not exact: its last bits depend on the
+ * order of the sums, which can move a value that lies within rounding of a
+ * threshold, or a near-tie of two PoT candidates, to the other side.
+ * Arguments:
+ *   W       fp32 [N][spec.K], finite.
+ *   spec    K (multiple of 64, at most 16384), block b (power of two,
+ *           2..4096, dividing K); clip_num = clip_den = 1.
+ *   fmt     QIFT_W2_MNZ, QIFT_W2_POT or QIFT_W4_SYM.
+ *   levels  out: int8 [N][K], the input of qift_pack_w2 / qift_pack_w4.
+ *   scales  out: fp16 s_w[N].
+ * Limits: N * K < 2^31.
+ */
+int qift_quantize_weights(const float *W, int64_t N, qift_hadamard_spec spec,
+                          int32_t fmt, int8_t *levels, uint16_t *scales,
+                          qift_stream_t stream);
+
+/*
  * Online Hadamard rotation + per-token symmetric INT4 quantization
  * (Sec. 3.1; Sec. 4.1 "Quantization configuration").  For each token m:
  *   X      = (I_{K/b} (x) H_b) x[m]   computed exactly (each fp16 input is an

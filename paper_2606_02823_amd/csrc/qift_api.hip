@@ -88,6 +88,20 @@ int qift_pack_w4(const int8_t* levels, const uint16_t* scales, int64_t N, int64_
   return st;
 }
 
+int qift_quantize_weights(const float* W, int64_t N, qift_hadamard_spec spec, int32_t fmt, int8_t* levels,
+                          uint16_t* scales, qift_stream_t stream) {
+  if (!W || !levels || !scales) return QIFT_ERR_NULL;
+  if (fmt != QIFT_W2_MNZ && fmt != QIFT_W2_POT && fmt != QIFT_W4_SYM) return QIFT_ERR_FORMAT;
+  if (!shape_ok(N, spec.K) || spec.K > qift::kWquantMaxK) return QIFT_ERR_SHAPE;
+  // 32-bit offsets of the level stores and row loads
+  if (N * spec.K >= (int64_t(1) << 31)) return QIFT_ERR_SHAPE;
+  const int32_t b = spec.block;
+  if (b < 2 || b > 4096 || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
+  if (spec.clip_num != 1 || spec.clip_den != 1) return QIFT_ERR_SPEC;
+  if (!aligned16(W) || !aligned16(levels) || !aligned16(scales)) return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_quantize_weights(W, N, spec.K, b, fmt, levels, scales, (hipStream_t)stream));
+}
+
 int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,
                           float* act_scale, int32_t* act_sum, qift_stream_t stream) {
   if (!x || !act_q || !act_scale || !act_sum) return QIFT_ERR_NULL;

@@ -13,6 +13,12 @@ hipError_t launch_pack_w2(const int8_t* levels, int64_t N, int64_t K, int fmt, u
 hipError_t launch_pack_w4(const int8_t* levels, int64_t N, int64_t K, uint32_t* packed,
                           int32_t* invalid_count, hipStream_t s);
 
+// Offline weight rotation + per-row scale + nearest level (qift_wquant.hip); fmt is a format constant
+// of qift_mma.h, block a power of two up to 4096 dividing K <= kWquantMaxK.
+constexpr int64_t kWquantMaxK = 16384;
+hipError_t launch_quantize_weights(const float* W, int64_t N, int64_t K, int block, int fmt, int8_t* levels,
+                                   uint16_t* scales, hipStream_t s);
+
 // Rotation + INT4 quantization (qift_act.hip)
 hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num,
                                    int clip_den, int8_t* act_q, float* act_scale, int32_t* act_sum,

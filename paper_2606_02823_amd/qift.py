@@ -28,7 +28,7 @@ STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR
           -8: "QIFT_ERR_WORKSPACE"}
 
 # every symbol declared in include/qift.h
-EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_rotate_quant_act",
+EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_rotate_quant_act",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w4a4_linear", "qift_w4a4_linear_ex",
            "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
            "qift_last_hip_error", "qift_version")
@@ -69,6 +69,7 @@ def lib():
         "qift_packed_bytes": (sz, [i32, i64, i64]),
         "qift_pack_w2": (ctypes.c_int, [vp, vp, i64, i64, i32, vp, pw, vp, vp]),
         "qift_pack_w4": (ctypes.c_int, [vp, vp, i64, i64, vp, pw, vp, vp]),
+        "qift_quantize_weights": (ctypes.c_int, [vp, i64, HadamardSpec, i32, vp, vp, vp]),
         "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
         "qift_w2a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
@@ -205,6 +206,24 @@ def alloc_act(M: int, K: int, device="cuda") -> QAct:
     return QAct(torch.empty((M, K), dtype=torch.int8, device=device),
                 torch.empty(M, dtype=torch.float32, device=device),
                 torch.empty(M, dtype=torch.int32, device=device))
+
+
+def quantize_weights(W: torch.Tensor, block: int, fmt: int, levels: torch.Tensor | None = None,
+                     scales: torch.Tensor | None = None, stream=None):
+    """Rotate the rows of fp32 W [N, K] by the block Hadamard, take the format's per-row scale and the
+    nearest levels (the input of pack_w2 / pack_w4).  Returns (levels int8 [N, K], scales fp16 [N])."""
+    N, K = W.shape
+    _dev(W, torch.float32, (N, K), "W")
+    if levels is None:
+        levels = torch.empty((N, K), dtype=torch.int8, device=W.device)
+    if scales is None:
+        scales = torch.empty(N, dtype=torch.float16, device=W.device)
+    _dev(levels, torch.int8, (N, K), "levels")
+    _dev(scales, torch.float16, (N,), "scales")
+    st = lib().qift_quantize_weights(W.data_ptr(), N, HadamardSpec(K, block, 1, 1), int(fmt), levels.data_ptr(),
+                                     scales.data_ptr(), _stream(stream))
+    _check("qift_quantize_weights", st)
+    return levels, scales
 
 
 def rotate_quant_act(x: torch.Tensor, block: int, clip=(1, 1), out: QAct | None = None, stream=None) -> QAct:

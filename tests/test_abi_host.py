@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -58,6 +58,25 @@ def test_packed_bytes(L):
 
 def _spec(K=256, block=256, num=1, den=1):
     return qift.HadamardSpec(K, block, num, den)
+
+
+def test_quantize_weights_validation(L):
+    f = L.qift_quantize_weights
+    mnz, pot, w4 = qift.W2_MNZ, qift.W2_POT, qift.W4_SYM
+    assert f(None, 8, _spec(), mnz, A, A, None) == E_NULL
+    assert f(A, 8, _spec(), pot, None, A, None) == E_NULL
+    assert f(A, 8, _spec(), w4, A, None, None) == E_NULL
+    assert f(A, 8, _spec(), 7, A, A, None) == E_FORMAT
+    assert f(A, 0, _spec(), mnz, A, A, None) == E_SHAPE
+    assert f(A, 8, _spec(K=100, block=4), mnz, A, A, None) == E_SHAPE
+    assert f(A, 8, _spec(K=16448, block=64), mnz, A, A, None) == E_SHAPE     # K > 16384
+    assert f(A, 1 << 18, _spec(K=8192, block=64), mnz, A, A, None) == E_SHAPE   # N K >= 2^31
+    assert f(A, 8, _spec(block=48), mnz, A, A, None) == E_SPEC
+    assert f(A, 8, _spec(K=8192, block=8192), mnz, A, A, None) == E_SPEC    # block above 4096
+    assert f(A, 8, _spec(K=192, block=128), mnz, A, A, None) == E_SPEC      # block does not divide K
+    assert f(A, 8, _spec(num=9, den=10), w4, A, A, None) == E_SPEC          # no clip on weights
+    assert f(MIS, 8, _spec(), mnz, A, A, None) == E_ALIGN
+    assert f(A, 8, _spec(), mnz, MIS, A, None) == E_ALIGN
 
 
 def test_rotate_quant_act_validation(L):
