@@ -582,11 +582,18 @@ def main():
             for i, (name, N, K, blk, site) in enumerate(pre.plan):
                 w = pre.weights[layer][i]
                 qift.rotate_quant_act(pre.x[i], blk, out=pre.acts[i])
-                dt = _time_graph(torch, lambda: qift.linear(w, pre.acts[i], out=pre.outs[i]), 10)
                 ops = 2 * pre.M * N * K
-                per_shape.append({"linear": name, "format": fname, "N": N, "K": K, "us": round(dt * 1e6, 2),
-                                  "int8_tops": round(ops / dt / 1e12, 2),
-                                  "pct_int8_peak": round(100 * ops / dt / 1e12 / INT8_PEAK_TOPS, 2)})
+                # the int8 MFMA kernel; for MNZ also the FP4 x FP6 scaled-MFMA kernel (its workspace
+                # selects it; the FP6 re-coding of the activations is inside the timed call)
+                variants = [("int8 MFMA", None)]
+                if qift.workspace_bytes(w, pre.M):
+                    variants.append(("FP4 x FP6 MFMA", torch.empty(qift.workspace_bytes(w, pre.M),
+                                                                   dtype=torch.uint8, device="cuda")))
+                for path, ws in variants:
+                    dt = _time_graph(torch, lambda: qift.linear(w, pre.acts[i], out=pre.outs[i], workspace=ws), 10)
+                    per_shape.append({"linear": name, "format": fname, "path": path, "N": N, "K": K,
+                                      "us": round(dt * 1e6, 2), "int8_tops": round(ops / dt / 1e12, 2),
+                                      "pct_int8_peak": round(100 * ops / dt / 1e12 / INT8_PEAK_TOPS, 2)})
         out["prefill"] = {"workload": "LLaMA-3.1-8B-shaped prefill, M=2048, layers 0-15 W4 / 16-31 W2 MNZ, "
                                       "4 rotate_quant_act + 4 linears per layer (q|k|v and gate|up stacked "
                                       "along N)",

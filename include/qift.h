@@ -215,8 +215,15 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
 /*
  * Same as qift_w2a4_linear, and additionally:
  *   acc_out    out, nullable: int32 [M][N], the exact accumulators.
- *   workspace, workspace_bytes   device scratch of at least
- *              qift_workspace_bytes(w, M) bytes (nullable when that is 0).
+ *   workspace, workspace_bytes   optional device scratch (16-byte aligned).
+ *              NULL / 0 runs the int8 MFMA kernels.  With at least
+ *              qift_workspace_bytes(w, M) bytes, where that is not 0 (MNZ
+ *              weights, M > 64), the activations are re-coded to FP6 E2M3
+ *              in it and the prefill contraction runs on the FP4 x FP6
+ *              scaled MFMA: the MNZ code c read as FP4 E2M1 is c / 2 and
+ *              every partial sum stays exact in fp32, so the results are
+ *              bit-identical.  A non-zero size below the query is
+ *              QIFT_ERR_WORKSPACE.  The workspace is overwritten.
  */
 int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
                         const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
@@ -261,7 +268,8 @@ int qift_rotate_quant_linear(const qift_packed_w *w, const uint16_t *x, int64_t 
  */
 int qift_hbm_read_probe(const void *buf, size_t bytes, uint32_t *partials, qift_stream_t stream);
 
-/* Workspace bytes the _ex calls need for this weight and M (host query). */
+/* Workspace bytes that select the FP4 x FP6 prefill kernel in the _ex calls for this weight and
+ * M (M * 3K/4 for MNZ weights at M > 64), 0 where no workspace is used (host query). */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
 
 /* Static text for a status code. */

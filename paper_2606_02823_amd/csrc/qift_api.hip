@@ -47,9 +47,14 @@ int linear_common(const qift_packed_w* w, bool w4, const int8_t* act_q, const fl
                   size_t ws_bytes, qift_stream_t stream) {
   int st = check_linear(w, w4, act_q, act_scale, act_sum, M, out, acc_out);
   if (st != QIFT_OK) return st;
-  if (ws_bytes < qift_workspace_bytes(w, M) || (ws_bytes > 0 && !ws)) return QIFT_ERR_WORKSPACE;
+  // the workspace is optional: none selects the int8 kernels, one of at least qift_workspace_bytes
+  // the FP4 x FP6 prefill kernel where that query is not 0
+  const size_t need = qift_workspace_bytes(w, M);
+  if (ws_bytes > 0 && (!ws || ws_bytes < need)) return QIFT_ERR_WORKSPACE;
+  if (ws && !aligned16(ws)) return QIFT_ERR_ALIGN;
+  void* use = ws_bytes > 0 && need > 0 ? ws : nullptr;
   return hip_status(qift::launch_linear(w->fmt, w->packed, w->scales, w->N, w->K, act_q, act_scale,
-                                        act_sum, M, out, acc_out, (hipStream_t)stream));
+                                        act_sum, M, out, acc_out, use, (hipStream_t)stream));
 }
 
 }  // namespace
@@ -171,9 +176,9 @@ int qift_hbm_read_probe(const void* buf, size_t bytes, uint32_t* partials, qift_
 }
 
 size_t qift_workspace_bytes(const qift_packed_w* w, int64_t M) {
-  (void)w;
-  (void)M;
-  return 0;
+  if (!w || w->fmt != QIFT_W2_MNZ || !shape_ok(w->N, w->K) || M < qift::kGemmF4MinM || M >= (int64_t(1) << 31))
+    return 0;
+  return qift::gemm_f4_workspace(M, w->K);
 }
 
 const char* qift_status_string(int status) {

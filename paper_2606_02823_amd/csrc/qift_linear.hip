@@ -494,8 +494,11 @@ hipError_t launch_deep(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t
 
 template <int FMT>
 hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
-                      const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out,
+                      const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
                       hipStream_t s) {
+  if constexpr (FMT == FMT_MNZ) {
+    if (ws && M >= kGemmF4MinM) return launch_gemm_f4(P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
+  }
   if (M <= 4 * kCodesMaxM) {
     // the decode kernel on precomputed codes (K-slice weight waves), once per block of mb tokens:
     // for M > 16 the largest block of at most 16 tokens whose codes fit in LDS (the GEMM's grid of
@@ -552,11 +555,14 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
 
 hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
-                         uint16_t* out, int32_t* acc_out, hipStream_t s) {
+                         uint16_t* out, int32_t* acc_out, void* ws, hipStream_t s) {
   switch (fmt) {
-    case FMT_MNZ: return launch_fmt<FMT_MNZ>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, s);
-    case FMT_POT: return launch_fmt<FMT_POT>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, s);
-    case FMT_W4: return launch_fmt<FMT_W4>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, s);
+    case FMT_MNZ:
+      return launch_fmt<FMT_MNZ>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, ws, s);
+    case FMT_POT:
+      return launch_fmt<FMT_POT>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, nullptr, s);
+    case FMT_W4:
+      return launch_fmt<FMT_W4>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, nullptr, s);
     default: return hipErrorInvalidValue;
   }
 }

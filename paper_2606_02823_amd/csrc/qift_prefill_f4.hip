@@ -1,0 +1,216 @@
+// Prefill linear for MNZ weights on the CDNA4 scaled MFMA with FP4 (E2M1) weights and FP6 (E2M3)
+// activations, v_mfma_scale_f32_16x16x128_f8f6f4 with unit scales (E8M0 127).
+//
+// Exactness: an MNZ code c in 0..3 read as the E2M1 nibble 0b00cc is c / 2 (0, 0.5, 1, 1.5) and
+// the INT4 codes -7..7 are exact in E2M3, so every product is c q / 2 and every partial sum a
+// multiple of 1/2 below 2^23: the fp32 accumulator holds D = sum c q / 2 exactly, and the integer
+// accumulator of the method is acc = 2 (2 D) - 3 sum q (Sec. 3.3: level = 2 c - 3).  Results are
+// bit-identical to the int8 path.
+//
+// Operand layouts (measured on gfx950): A lane (row r, group g) nibble i <-> k = 32 g + i of the
+// MFMA's 128; B lane (column m, group g) element i at bits 6 i .. 6 i + 5 of its 192 bits <-> the
+// same k; D as for the int8 MFMA.  A lane takes its 32 weights from two packed words with two masks
+// per word (w & 0x33333333, (w >> 2) & 0x33333333): nibble 8 D + i of the operand then holds the
+// code of word k-offset kperm(8 D + i) = 16 (D >> 1) + 4 (D & 1) + 8 (i & 1) + (i >> 1), and the
+// FP6 activations are stored in that order inside each 32-k group (k_act_fp6).
+#include "qift_fwht.h"
+#include "qift_internal.h"
+#include "qift_mma.h"
+
+namespace qift {
+namespace {
+
+using namespace mma;
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kF6GroupBytes = 24;   // 32 FP6 codes
+constexpr int kF6StepBytes = 192;   // 256 k of one token
+
+__host__ __device__ constexpr int kperm(int n) {
+  return 16 * ((n >> 3) >> 1) + 4 * ((n >> 3) & 1) + 8 * (n & 1) + ((n & 7) >> 1);
+}
+
+// act_q int8 [M][K] -> FP6 E2M3 codes [M][K / 32][24 bytes], element n of group G = code of
+// k = 32 G + kperm(n).  One thread per group.
+__global__ __launch_bounds__(256) void k_act_fp6(const int8_t* __restrict__ act_q, int M, int K,
+                                                 uint8_t* __restrict__ act6) {
+  const int groups = K >> 5;
+  const int G = blockIdx.x * 256 + threadIdx.x;
+  if (G >= groups) return;
+  for (int m = blockIdx.y; m < M; m += gridDim.y) {
+    const uint4* src = reinterpret_cast<const uint4*>(act_q + (int64_t)m * K + 32 * G);
+    const uint4 lo = src[0], hi = src[1];
+    const uint32_t wq[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    uint32_t out[6] = {0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int n = 0; n < 32; ++n) {
+      const int k = kperm(n);
+      const int q = (int)(int8_t)(wq[k >> 2] >> (8 * (k & 3)));
+      const int a = q < 0 ? -q : q;
+      // E2M3 (bias 1) of 0..7: 0, 1.0, 2.0, 1.5 * 2, 4.0, 1.25 * 4, 1.5 * 4, 1.75 * 4
+      const uint32_t mag = a == 0 ? 0u : a == 1 ? 0x08u : a == 2 ? 0x10u : a == 3 ? 0x14u
+                         : 0x18u + 2u * (uint32_t)(a - 4);
+      const uint32_t code = mag | (q < 0 ? 0x20u : 0u);
+      const int bit = 6 * n;
+      out[bit >> 5] |= code << (bit & 31);
+      if ((bit & 31) > 26) out[(bit >> 5) + 1] |= code >> (32 - (bit & 31));
+    }
+    uint2* dst = reinterpret_cast<uint2*>(act6 + (int64_t)m * (3 * (K >> 2)) + kF6GroupBytes * G);
+    dst[0] = make_uint2(out[0], out[1]);
+    dst[1] = make_uint2(out[2], out[3]);
+    dst[2] = make_uint2(out[4], out[5]);
+  }
+}
+
+// Tiles of 256 weight rows x 64 tokens x 256 k, 4 waves (64 rows x 64 tokens each), three
+// workgroups per CU: the structure of the int8 prefill kernel (weights one step ahead in
+// alternating register sets, activations by direct-to-LDS loads into two distinct buffers) with
+// two 16x16x128 MFMAs per row tile and step instead of four 16x16x64 ones.  The step's FP6 row is
+// 192 bytes: twelve 16-byte chunks in a 256-byte LDS row, chunk c of row r in slot c ^ (r mod 16)
+// (the four spare slots receive zeros).
+template <int OCC>
+__global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
+                                                      int N, int K, const uint8_t* __restrict__ act6,
+                                                      const float* __restrict__ sx, const int32_t* __restrict__ asum,
+                                                      int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+  constexpr int BM = 64, BK = 256;
+  __shared__ __align__(16) uint8_t lds0[BM * 256];
+  __shared__ __align__(16) uint8_t lds1[BM * 256];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int n_base = blockIdx.x * 256 + wave * 64;
+  const int m_base = blockIdx.y * BM;
+  const int rowbytes = K / 4, row6 = 3 * (K / 4);
+  const int KT = (K + BK - 1) / BK;
+
+  // weights: as in the int8 kernel (lanes past K in a last partial step meet zero activations)
+  const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)N * (uint32_t)rowbytes);
+  uint32_t wbase[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int n = n_base + 16 * j + r16;
+    wbase[j] = n < N ? (uint32_t)n * (uint32_t)rowbytes + 16u * g : dev::kOutOfRange;
+  }
+  auto load_w = [&](uint4 (&w)[4], int kt) {
+    const uint32_t ko = 64u * (uint32_t)kt;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = dev::bload16(wrs, wbase[j] + ko);
+  };
+  // activations: load q moves 1 KB = rows 4 (4 wave + q) .. + 3; lane l fills slot l mod 16 of row
+  // 4 (4 wave + q) + l / 16 with the row's chunk (l mod 16) ^ (row mod 16), zeros for chunks >= 12
+  const int mrows = M - m_base < BM ? M - m_base : BM;
+  const __amdgpu_buffer_rsrc_t ars = dev::make_rsrc(act6 + (int64_t)m_base * row6, (uint32_t)(mrows * row6));
+  uint32_t abase[4];
+  int acol[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int row = 4 * (4 * wave + q) + (lane >> 4);
+    const int c = (lane & 15) ^ (row & 15);
+    acol[q] = 16 * c;
+    abase[q] = row < mrows && c < 12 ? (uint32_t)(row * row6 + 16 * c) : dev::kOutOfRange;
+  }
+  auto issue_a = [&](int kt, uint8_t* dst) {
+    const int ko = kt * kF6StepBytes;
+    const bool tail = ko + kF6StepBytes > row6;   // the last step of a K that is not a multiple of 256
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int chunk = 4 * wave + q;
+      uint32_t off = abase[q] + (uint32_t)ko;
+      if (tail && acol[q] + ko >= row6) off = dev::kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ars, (__attribute__((address_space(3))) void*)(dst + 1024 * chunk), 16, off, 0, 0, 0);
+    }
+  };
+
+  v4f acc[4][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[j][t] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  // MFMA kb of lane group g covers k = kt 256 + 64 g + 32 kb + kperm(0 .. 31): words 2 kb, 2 kb + 1
+  // of the lane's 16 bytes, and FP6 group 2 g + kb of the step
+  auto step = [&](int kt, const uint8_t* tileb, uint8_t* nextb, const uint4 (&wc)[4], uint4 (&wn)[4]) {
+    if (kt + 1 < KT) {
+      issue_a(kt + 1, nextb);
+      load_w(wn, kt + 1);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      v8i a[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t w0 = kb ? wc[j].z : wc[j].x, w1 = kb ? wc[j].w : wc[j].y;
+        a[j] = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u), (int)(w1 & 0x33333333u),
+                   (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int row = 16 * t + r16;
+        const uint8_t* rp = tileb + row * 256;
+        uint2 pc[3];
+#pragma unroll
+        for (int p = 0; p < 3; ++p) {
+          const int off = kF6GroupBytes * (2 * g + kb) + 8 * p;   // never crosses a 16-byte chunk
+          pc[p] = *reinterpret_cast<const uint2*>(rp + 16 * ((off >> 4) ^ r16) + (off & 15));
+        }
+        const v8i b = v8i{(int)pc[0].x, (int)pc[0].y, (int)pc[1].x, (int)pc[1].y, (int)pc[2].x, (int)pc[2].y, 0, 0};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[j][t] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[j], b, acc[j][t], 4, 2, 0, 127, 0, 127);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // this wave's loads of step kt+1 have landed
+    __syncthreads();
+  };
+
+  uint4 wa[4], wb[4];
+  issue_a(0, lds0);
+  load_w(wa, 0);
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  for (int kt = 0; kt < KT; kt += 2) {
+    step(kt, lds0, lds1, wa, wb);
+    if (kt + 1 < KT) step(kt + 1, lds1, lds0, wb, wa);
+  }
+
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int m = m_base + 16 * t + r16;
+    if (m < M) {
+      const float s_x = sx[m];
+      const int sq = asum[m];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // 2 D = sum c q exactly (an integer below 2^24)
+        const v4i D = v4i{(int)(2.f * acc[j][t][0]), (int)(2.f * acc[j][t][1]), (int)(2.f * acc[j][t][2]),
+                          (int)(2.f * acc[j][t][3])};
+        store4<FMT_MNZ>(D, m, n_base + 16 * j + 4 * g, N, s_x, sq, sw, y, acc_out);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+size_t gemm_f4_workspace(int64_t M, int64_t K) { return (size_t)M * (size_t)(3 * (K / 4)); }
+
+hipError_t launch_gemm_f4(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act_q,
+                          const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
+                          hipStream_t s) {
+  uint8_t* act6 = static_cast<uint8_t*>(ws);
+  const int groups = (int)(K / 32);
+  const unsigned gy = (unsigned)(M < 65535 ? M : 65535);
+  hipLaunchKernelGGL(k_act_fp6, dim3((unsigned)((groups + 255) / 256), gy), dim3(256), 0, s, act_q, (int)M, (int)K,
+                     act6);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_gemm_f4<3>), dim3((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64)), dim3(256), 0, s, P,
+                     sw, (int)N, (int)K, act6, sx, asum, (int)M, y, acc_out);
+  return hipGetLastError();
+}
+
+}  // namespace qift

@@ -255,6 +255,8 @@ def _linear(name: str, w: Packed, act: QAct, out, acc_out, workspace, stream):
         _dev(acc_out, torch.int32, (M, w.N), "acc_out")
     v = w.cview()
     L = lib()
+    if workspace is not None:
+        _dev(workspace, torch.uint8, (workspace.numel(),), "workspace")
     if acc_out is None and workspace is None:
         st = getattr(L, name)(ctypes.byref(v), act.q.data_ptr(), act.scale.data_ptr(), act.sum.data_ptr(),
                               M, out.data_ptr(), _stream(stream))

@@ -121,6 +121,16 @@ def test_linear_validation(L):
     assert w2x(P(_pw()), A, A, A, 4, A, MIS, None, 0, None) == E_ALIGN
     assert w2x(P(_pw()), A, A, A, 4, A, None, None, 64, None) == E_WS
     assert L.qift_workspace_bytes(P(_pw()), 4) == 0
+    # the workspace that selects the FP4 x FP6 prefill kernel: MNZ at M > 64, M * 3K/4 bytes
+    K = _pw().K
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 64) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 65) == 65 * 3 * (K // 4)
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT)), 65) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM)), 65) == 0
+    need = 100 * 3 * (K // 4)
+    assert w2x(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 100, A, None, A, need - 16, None) == E_WS
+    assert w2x(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 100, A, None, None, need, None) == E_WS
+    assert w2x(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 100, A, None, MIS, need, None) == E_ALIGN
 
 
 def test_fused_validation(L):

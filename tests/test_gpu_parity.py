@@ -119,6 +119,25 @@ def test_linear_ragged(Q, fmt, M):
     check_linear(y, acc, L, q_ref, sx_ref, s_w)
 
 
+@pytest.mark.parametrize("M,K", [(65, 1088), (130, 1088), (300, 4096), (200, 14336)])
+def test_mnz_prefill_int8_and_fp4_paths(Q, M, K):
+    # MNZ at M > 64: the int8 GEMM (no workspace) and the FP4 x FP6 GEMM (FP6 activations in a
+    # workspace of workspace_bytes), ragged rows and tokens, K with a partial last step
+    fmt, N, b = levels.FMT_W2_MNZ, 1000, 64
+    L = synth.draw_levels(fmt, N, K, cfg=97, layer=M)
+    s_w = synth.draw_scales(fmt, N, cfg=97, layer=M)
+    x = synth.activations_fp16(97, M, 0, M, K, K // 100, 30.0)
+    pk = pack_dev(Q, L, s_w, fmt)
+    act = Q.rotate_quant_act(dev(x), b)
+    q_ref, sx_ref = check_act(act, x, b)
+    assert Q.workspace_bytes(pk, M) == M * 3 * (K // 4)
+    for ws in (None, torch.empty(Q.workspace_bytes(pk, M), dtype=torch.uint8, device="cuda")):
+        acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+        y = Q.linear(pk, act, acc_out=acc, workspace=ws)
+        torch.cuda.synchronize()
+        check_linear(y, acc, L, q_ref, sx_ref, s_w)
+
+
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("M,K", [(1, 20480), (9, 20480), (16, 32768)])
 def test_linear_long_k(Q, fmt, M, K):
