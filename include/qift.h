@@ -268,6 +268,51 @@ int qift_rotate_quant_linear(const qift_packed_w *w, const uint16_t *x, int64_t 
  */
 int qift_hbm_read_probe(const void *buf, size_t bytes, uint32_t *partials, qift_stream_t stream);
 
+/*
+ * KV4: the four-bit key/value cache of the W2A4/KV4 setting (Sec. 4.1
+ * "Quantization configuration": asymmetric key and value quantization with
+ * clipping ratio 0.95) with the conventional asymmetric quantizer of
+ * Sec. 3.3 Eq. (15), q = clip(round(x / s) + z, 0, 15), x_hat = s (q - z).
+ * One group per token and KV head (head_dim = 128 values).  In fp32, in this
+ * order, rounding half to even:
+ *   x_max = c * max(max x, 0), x_min = c * min(min x, 0), c = fp32(0.95);
+ *   s = (x_max - x_min) / 15 (1 for a group of zeros); z = round(-x_min / s);
+ *   q = clip(round(x / s) + z, 0, 15).
+ *   x        fp16 [groups][128].
+ *   codes    out: uint8 [groups][64], value 2i in the low nibble of byte i.
+ *   scales   out: fp32 s [groups].   zeros   out: uint8 z [groups].
+ */
+int qift_kv4_quant(const uint16_t *x, int64_t groups, int32_t head_dim, uint8_t *codes,
+                   float *scales, uint8_t *zeros, qift_stream_t stream);
+
+/* Workspace bytes of qift_kv4_attention_decode (0 for an unsupported shape). */
+size_t qift_kv4_attention_workspace_bytes(int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                                          int64_t T);
+
+/*
+ * One decode step of grouped-query attention over a KV4 cache (Sec. 1: the
+ * decode stream is weights plus KV cache).  For batch b and query head h,
+ * with KV head kv = h / (Hq / Hkv):
+ *   out[b][h] = sum_t softmax_t( q[b][h] . k_hat[b][t][kv] / sqrt(128) )
+ *               * v_hat[b][t][kv],   x_hat = s (code - z) per group,
+ * in fp32 (scores, exponentials and sums) with an fp16 result; the result is
+ * within rounding of the exact softmax of the reconstructed cache.
+ *   q        fp16 [B][Hq][128], the new token's queries.
+ *   k_*, v_* the cache as written by qift_kv4_quant for groups [B][T][Hkv]:
+ *            codes uint8 [B][T][Hkv][64], scales fp32 and zeros uint8
+ *            [B][T][Hkv].
+ *   out      out: fp16 [B][Hq][128].
+ *   workspace  device scratch of qift_kv4_attention_workspace_bytes bytes
+ *            (per 256 cached tokens and query head: 128 partial sums, the
+ *            chunk's maximum score and sum of exponentials).
+ * Limits: head_dim = 128, Hq / Hkv in {1, 2, 4, 8}, B and Hkv <= 65535.
+ */
+int qift_kv4_attention_decode(const uint16_t *q, int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                              int64_t T, const uint8_t *k_codes, const float *k_scales,
+                              const uint8_t *k_zeros, const uint8_t *v_codes, const float *v_scales,
+                              const uint8_t *v_zeros, uint16_t *out, void *workspace,
+                              size_t workspace_bytes, qift_stream_t stream);
+
 /* Workspace bytes that select the FP4 x FP6 prefill kernel in the _ex calls for this weight and
  * M (M * 3K/4 for MNZ weights at M > 64), 0 where no workspace is used (host query). */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);

@@ -107,6 +107,42 @@ int qift_quantize_weights(const float* W, int64_t N, qift_hadamard_spec spec, in
   return hip_status(qift::launch_quantize_weights(W, N, spec.K, b, fmt, levels, scales, (hipStream_t)stream));
 }
 
+int qift_kv4_quant(const uint16_t* x, int64_t groups, int32_t head_dim, uint8_t* codes, float* scales,
+                   uint8_t* zeros, qift_stream_t stream) {
+  if (!x || !codes || !scales || !zeros) return QIFT_ERR_NULL;
+  if (head_dim != 128 || groups < 1 || groups >= (int64_t(1) << 40)) return QIFT_ERR_SHAPE;
+  if (!aligned16(x) || !aligned16(codes) || !aligned16(scales) || !aligned16(zeros)) return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_kv4_quant(x, groups, codes, scales, zeros, (hipStream_t)stream));
+}
+
+namespace {
+bool kv4_attn_shape_ok(int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim, int64_t T) {
+  if (head_dim != 128 || B < 1 || B > 65535 || Hkv < 1 || Hkv > 65535 || Hq < Hkv || Hq % Hkv) return false;
+  const int32_t G = Hq / Hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return false;
+  return T >= 1 && T < (int64_t(1) << 36);
+}
+}  // namespace
+
+size_t qift_kv4_attention_workspace_bytes(int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim, int64_t T) {
+  if (!kv4_attn_shape_ok(B, Hq, Hkv, head_dim, T)) return 0;
+  return qift::kv4_attention_workspace(B, Hq, T);
+}
+
+int qift_kv4_attention_decode(const uint16_t* q, int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim, int64_t T,
+                              const uint8_t* k_codes, const float* k_scales, const uint8_t* k_zeros,
+                              const uint8_t* v_codes, const float* v_scales, const uint8_t* v_zeros, uint16_t* out,
+                              void* workspace, size_t workspace_bytes, qift_stream_t stream) {
+  if (!q || !k_codes || !k_scales || !k_zeros || !v_codes || !v_scales || !v_zeros || !out) return QIFT_ERR_NULL;
+  if (!kv4_attn_shape_ok(B, Hq, Hkv, head_dim, T)) return QIFT_ERR_SHAPE;
+  if (!workspace || workspace_bytes < qift::kv4_attention_workspace(B, Hq, T)) return QIFT_ERR_WORKSPACE;
+  if (!aligned16(q) || !aligned16(k_codes) || !aligned16(k_scales) || !aligned16(k_zeros) || !aligned16(v_codes) ||
+      !aligned16(v_scales) || !aligned16(v_zeros) || !aligned16(out) || !aligned16(workspace))
+    return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_kv4_attention(q, B, Hq, Hkv, T, k_codes, k_scales, k_zeros, v_codes, v_scales,
+                                               v_zeros, out, workspace, (hipStream_t)stream));
+}
+
 int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,
                           float* act_scale, int32_t* act_sum, qift_stream_t stream) {
   if (!x || !act_q || !act_scale || !act_sum) return QIFT_ERR_NULL;

@@ -28,7 +28,8 @@ STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR
           -8: "QIFT_ERR_WORKSPACE"}
 
 # every symbol declared in include/qift.h
-EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_rotate_quant_act",
+EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_kv4_quant",
+           "qift_kv4_attention_workspace_bytes", "qift_kv4_attention_decode", "qift_rotate_quant_act",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w4a4_linear", "qift_w4a4_linear_ex",
            "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
            "qift_last_hip_error", "qift_version")
@@ -70,6 +71,10 @@ def lib():
         "qift_pack_w2": (ctypes.c_int, [vp, vp, i64, i64, i32, vp, pw, vp, vp]),
         "qift_pack_w4": (ctypes.c_int, [vp, vp, i64, i64, vp, pw, vp, vp]),
         "qift_quantize_weights": (ctypes.c_int, [vp, i64, HadamardSpec, i32, vp, vp, vp]),
+        "qift_kv4_quant": (ctypes.c_int, [vp, i64, i32, vp, vp, vp, vp]),
+        "qift_kv4_attention_workspace_bytes": (sz, [i64, i32, i32, i32, i64]),
+        "qift_kv4_attention_decode": (ctypes.c_int, [vp, i64, i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                                     vp]),
         "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
         "qift_w2a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
@@ -224,6 +229,55 @@ def quantize_weights(W: torch.Tensor, block: int, fmt: int, levels: torch.Tensor
                                      scales.data_ptr(), _stream(stream))
     _check("qift_quantize_weights", st)
     return levels, scales
+
+
+class KV4:
+    """A KV4 cache tensor: codes uint8 [..., 64], scales fp32 [...], zeros uint8 [...]."""
+
+    def __init__(self, codes: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor):
+        self.codes, self.scales, self.zeros = codes, scales, zeros
+
+
+def kv4_quant(x: torch.Tensor, out: KV4 | None = None, stream=None) -> KV4:
+    """Asymmetric 4-bit quantization of fp16 x [..., 128], one group per trailing vector."""
+    lead = tuple(x.shape[:-1])
+    _dev(x, torch.float16, lead + (128,), "x")
+    if out is None:
+        out = KV4(torch.empty(lead + (64,), dtype=torch.uint8, device=x.device),
+                  torch.empty(lead, dtype=torch.float32, device=x.device),
+                  torch.empty(lead, dtype=torch.uint8, device=x.device))
+    _dev(out.codes, torch.uint8, lead + (64,), "codes")
+    _dev(out.scales, torch.float32, lead, "scales")
+    _dev(out.zeros, torch.uint8, lead, "zeros")
+    groups = x.numel() // 128
+    st = lib().qift_kv4_quant(x.data_ptr(), groups, 128, out.codes.data_ptr(), out.scales.data_ptr(),
+                              out.zeros.data_ptr(), _stream(stream))
+    _check("qift_kv4_quant", st)
+    return out
+
+
+def kv4_attention_decode(q: torch.Tensor, k: KV4, v: KV4, out=None, workspace=None, stream=None) -> torch.Tensor:
+    """One decode step of grouped-query attention: q fp16 [B, Hq, 128] over the KV4 cache k, v of
+    groups [B, T, Hkv]; returns fp16 [B, Hq, 128]."""
+    B, Hq, d = q.shape
+    _dev(q, torch.float16, (B, Hq, 128), "q")
+    T, Hkv = k.codes.shape[1], k.codes.shape[2]
+    for name, c in (("k", k), ("v", v)):
+        _dev(c.codes, torch.uint8, (B, T, Hkv, 64), name + ".codes")
+        _dev(c.scales, torch.float32, (B, T, Hkv), name + ".scales")
+        _dev(c.zeros, torch.uint8, (B, T, Hkv), name + ".zeros")
+    if out is None:
+        out = torch.empty((B, Hq, 128), dtype=torch.float16, device=q.device)
+    _dev(out, torch.float16, (B, Hq, 128), "out")
+    need = int(lib().qift_kv4_attention_workspace_bytes(B, Hq, Hkv, 128, T))
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    st = lib().qift_kv4_attention_decode(q.data_ptr(), B, Hq, Hkv, 128, T, k.codes.data_ptr(), k.scales.data_ptr(),
+                                         k.zeros.data_ptr(), v.codes.data_ptr(), v.scales.data_ptr(),
+                                         v.zeros.data_ptr(), out.data_ptr(), workspace.data_ptr(),
+                                         workspace.numel() * workspace.element_size(), _stream(stream))
+    _check("qift_kv4_attention_decode", st)
+    return out
 
 
 def rotate_quant_act(x: torch.Tensor, block: int, clip=(1, 1), out: QAct | None = None, stream=None) -> QAct:

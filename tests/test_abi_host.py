@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 18
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -77,6 +77,26 @@ def test_quantize_weights_validation(L):
     assert f(A, 8, _spec(num=9, den=10), w4, A, A, None) == E_SPEC          # no clip on weights
     assert f(MIS, 8, _spec(), mnz, A, A, None) == E_ALIGN
     assert f(A, 8, _spec(), mnz, MIS, A, None) == E_ALIGN
+
+
+def test_kv4_validation(L):
+    fq = L.qift_kv4_quant
+    assert fq(None, 4, 128, A, A, A, None) == E_NULL
+    assert fq(A, 4, 64, A, A, A, None) == E_SHAPE          # head_dim 128 only
+    assert fq(A, 0, 128, A, A, A, None) == E_SHAPE
+    assert fq(A, 4, 128, A, MIS, A, None) == E_ALIGN
+    ws = L.qift_kv4_attention_workspace_bytes
+    assert ws(2, 32, 8, 128, 1000) == 2 * 32 * 4 * 130 * 4   # 4 chunks of 256 tokens, 130 floats each
+    assert ws(1, 32, 8, 64, 1000) == 0
+    assert ws(1, 24, 8, 128, 1000) == 0                       # Hq / Hkv = 3
+    f = L.qift_kv4_attention_decode
+    good = ws(1, 32, 8, 128, 1000)
+    assert f(A, 1, 32, 8, 128, 1000, A, A, A, A, A, None, A, A, good, None) == E_NULL
+    assert f(A, 1, 32, 8, 128, 0, A, A, A, A, A, A, A, A, good, None) == E_SHAPE
+    assert f(A, 1, 32, 6, 128, 1000, A, A, A, A, A, A, A, A, good, None) == E_SHAPE
+    assert f(A, 1, 32, 8, 128, 1000, A, A, A, A, A, A, A, A, good - 4, None) == E_WS
+    assert f(A, 1, 32, 8, 128, 1000, A, A, A, A, A, A, A, None, good, None) == E_WS
+    assert f(A, 1, 32, 8, 128, 1000, A, A, MIS, A, A, A, A, A, good, None) == E_ALIGN
 
 
 def test_rotate_quant_act_validation(L):

@@ -1,0 +1,78 @@
+"""GPU KV4 cache (qift_kv4_quant) and decode attention over it (qift_kv4_attention_decode) against
+the oracle, through the C ABI.
+
+The quantizer's codes, fp32 scales and zero-points must equal the oracle's bit for bit (both decide
+in fp32, in the same order).  The attention output is fp16 from fp32 arithmetic; it is compared
+with the oracle's fp64 softmax over the reconstructed cache, per query head, against a tolerance
+derived from the arithmetic: the fp16 rounding of the output (2^-11 relative) plus fp32 sums, far
+below 1e-3 of the head's largest output.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import kv4 as okv4
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def Q():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_02823_amd import qift
+    qift.lib()
+    return qift
+
+
+def groups_fp16(rng, n):
+    x = rng.normal(0, 1, (n, 128))
+    x[::5] *= rng.uniform(0.001, 30, (x[::5].shape[0], 1))
+    x[1::7] = np.abs(x[1::7])            # all non-negative
+    x[2::7] = -np.abs(x[2::7])           # all non-positive
+    x[3::11] = 0.0                        # groups of zeros
+    x[4::13] *= 1e-6                      # tiny (fp16 subnormals)
+    x[5::17, 3] = 900.0                   # one outlier
+    return x.astype(np.float16)
+
+
+def unpack(codes):
+    c = codes.astype(np.uint8)
+    out = np.empty(c.shape[:-1] + (2 * c.shape[-1],), dtype=np.uint8)
+    out[..., 0::2] = c & 15
+    out[..., 1::2] = c >> 4
+    return out
+
+
+def test_kv4_quant_bitexact(Q):
+    rng = np.random.default_rng(11)
+    x = groups_fp16(rng, 3001)
+    c = Q.kv4_quant(torch.from_numpy(x).cuda())
+    torch.cuda.synchronize()
+    q_ref, s_ref, z_ref = okv4.kv4_quant(x)
+    assert np.array_equal(c.scales.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(c.zeros.cpu().numpy(), z_ref)
+    assert np.array_equal(unpack(c.codes.cpu().numpy()), q_ref)
+    assert np.array_equal(c.codes.cpu().numpy(), okv4.pack_nibbles(q_ref))
+
+
+@pytest.mark.parametrize("B,T,Hq,Hkv", [(1, 1, 32, 8), (2, 255, 32, 8), (1, 256, 32, 8), (2, 257, 16, 8),
+                                        (1, 1000, 8, 8), (1, 4100, 64, 8), (3, 700, 32, 8)])
+def test_kv4_attention_decode(Q, B, T, Hq, Hkv):
+    rng = np.random.default_rng(B * 100003 + T)
+    K = groups_fp16(rng, B * T * Hkv).reshape(B, T, Hkv, 128)
+    V = rng.normal(0, 1, (B, T, Hkv, 128)).astype(np.float16)
+    q = (rng.normal(0, 1, (B, Hq, 128)) * rng.uniform(0.2, 3, (B, Hq, 1))).astype(np.float16)
+    k = Q.kv4_quant(torch.from_numpy(K).cuda())
+    v = Q.kv4_quant(torch.from_numpy(V).cuda())
+    y = Q.kv4_attention_decode(torch.from_numpy(q).cuda(), k, v)
+    torch.cuda.synchronize()
+    kq, ks, kz = okv4.kv4_quant(K)
+    vq, vs, vz = okv4.kv4_quant(V)
+    assert np.array_equal(unpack(k.codes.cpu().numpy()), kq) and np.array_equal(unpack(v.codes.cpu().numpy()), vq)
+    ref = okv4.attention_decode(q, okv4.kv4_dequant(kq, ks, kz), okv4.kv4_dequant(vq, vs, vz))
+    got = y.cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref).max(axis=-1) / np.abs(ref).max(axis=-1)
+    assert err.max() <= TOL, err.max()
