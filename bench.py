@@ -397,6 +397,51 @@ def weight_quantizer(torch, qift, synth, reps=5):
     return out
 
 
+def kv4_attention(torch, qift, reps=10, layers=32):
+    """KV4 caches of the 32 layers of LLaMA-3.1-8B (32 query heads, 8 KV heads, head_dim 128): one
+    decode step's attention over T cached tokens for B sequences, i.e. 32 launches over 32 distinct
+    caches in one hipGraph (HBM roofline: each 4-bit cache is read once, 64 B of codes + 4 B scale
+    + 1 B zero-point per token, KV head and tensor); and the quantizer writing one layer's cache of
+    T tokens (fp16 in, KV4 out)."""
+    dev = torch.device("cuda")
+    Hq, Hkv = 32, 8
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4)
+    rows = []
+    for B, T in ((1, 4096), (1, 32768), (16, 4096)):
+        caches = []
+        for _ in range(layers):
+            K = torch.randn((B, T, Hkv, 128), device=dev, generator=gen).half()
+            V = torch.randn((B, T, Hkv, 128), device=dev, generator=gen).half()
+            caches.append((qift.kv4_quant(K), qift.kv4_quant(V)))
+        q = torch.randn((B, Hq, 128), device=dev, generator=gen).half()
+        y = torch.empty((B, Hq, 128), dtype=torch.float16, device=dev)
+        ws = torch.empty(qift.lib().qift_kv4_attention_workspace_bytes(B, Hq, Hkv, 128, T), dtype=torch.uint8,
+                         device=dev)
+
+        def step():
+            for k, v in caches:
+                qift.kv4_attention_decode(q, k, v, out=y, workspace=ws)
+        dt = _time_graph(torch, step, reps) / layers
+        cache = 2 * B * T * Hkv * (64 + 4 + 1)
+        gbs = (cache + 4 * B * Hq * 128) / dt / 1e9
+        k, v = caches[0]
+
+        def quant():
+            for _ in range(4):
+                qift.kv4_quant(K, out=k)
+                qift.kv4_quant(V, out=v)
+        dq = _time_graph(torch, quant, reps) / 4
+        qgbs = (2 * B * T * Hkv * 256 + cache) / dq / 1e9
+        rows.append({"B": B, "T": T, "attention_us_per_layer": round(dt * 1e6, 2), "cache_bytes_per_layer": cache,
+                     "attention_GBs": round(gbs, 1), "attention_pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+                     "quant_us_per_layer": round(dq * 1e6, 2), "quant_GBs": round(qgbs, 1)})
+        del K, V, caches, ws
+        torch.cuda.empty_cache()
+    return {"workload": "LLaMA-3.1-8B attention at decode, 32 layers: Hq 32, Hkv 8, head_dim 128, KV4 cache "
+                        "(clip 0.95), T cached tokens per sequence, B sequences", "rows": rows}
+
+
 def cpu_baseline(synth, budget_s=20.0):
     """The oracle as it stands, on one cfg1 layer at M=1 (4 act quantizations + 7 linears)."""
     import numpy as np
@@ -453,6 +498,7 @@ def main():
     ap.add_argument("--no-per-shape", action="store_true",
                     help="skip the per-shape replica loops and the read probe")
     ap.add_argument("--no-wquant", action="store_true", help="skip the weight quantizer timing")
+    ap.add_argument("--no-kv4", action="store_true", help="skip the KV4 attention timing")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the cfg2 (M 1/4/16) and cfg3 PoT (M 1/8/64) stack sweep")
     ap.add_argument("--copy-probe", action="store_true",
@@ -558,6 +604,12 @@ def main():
     if not args.no_wquant:
         _stage("weight quantizer")
         out["weight_quantizer"] = weight_quantizer(torch, qift, synth)
+        torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- KV4 cache and decode attention
+    if not args.no_kv4:
+        _stage("KV4 attention")
+        out["kv4_attention"] = kv4_attention(torch, qift)
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- prefill

@@ -305,7 +305,8 @@ size_t qift_kv4_attention_workspace_bytes(int64_t B, int32_t Hq, int32_t Hkv, in
  *   workspace  device scratch of qift_kv4_attention_workspace_bytes bytes
  *            (per 256 cached tokens and query head: 128 partial sums, the
  *            chunk's maximum score and sum of exponentials).
- * Limits: head_dim = 128, Hq / Hkv in {1, 2, 4, 8}, B and Hkv <= 65535.
+ * Limits: head_dim = 128, Hq / Hkv in {1, 2, 4, 8}, B and Hkv <= 65535,
+ * T * Hkv * 64 < 2^31.
  */
 int qift_kv4_attention_decode(const uint16_t *q, int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
                               int64_t T, const uint8_t *k_codes, const float *k_scales,

@@ -120,7 +120,8 @@ bool kv4_attn_shape_ok(int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim, int
   if (head_dim != 128 || B < 1 || B > 65535 || Hkv < 1 || Hkv > 65535 || Hq < Hkv || Hq % Hkv) return false;
   const int32_t G = Hq / Hkv;
   if (G != 1 && G != 2 && G != 4 && G != 8) return false;
-  return T >= 1 && T < (int64_t(1) << 36);
+  // 32-bit offsets into one sequence's cache: T Hkv 64 bytes of codes below 2^31
+  return T >= 1 && T * Hkv * 64 < (int64_t(1) << 31);
 }
 }  // namespace
 

@@ -157,9 +157,27 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
   }
   __syncthreads();
 
-  // ---- values: lane l covers dimensions 8 (l mod 16) .. + 7 of tokens 64 wave + 4 j + l / 16
+  // ---- values: lane l covers dimensions 8 (l mod 16) .. + 7 of tokens 64 wave + 4 j + l / 16.  All
+  // sixteen tokens' codes, scales and zero-points are loaded first (range-checked buffer loads: zeros
+  // past T, where the weights are 0 as well), then accumulated.
   {
     const int dq = lane & 15, ts = lane >> 4;
+    const int64_t row0 = (b * T) * Hkv + kv;   // cache row of token 0; token t is row0 + t Hkv
+    const uint32_t rows = (uint32_t)(T * Hkv);   // T Hkv 64 < 2^31: checked by the host
+    const __amdgpu_buffer_rsrc_t crs = dev::make_rsrc(vc + row0 * (kD / 2), rows * (kD / 2));
+    const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(vs + row0, rows * 4u);
+    const __amdgpu_buffer_rsrc_t zrs = dev::make_rsrc(vz + row0, rows);
+    uint32_t vw[16];
+    float vsc[16], vzz[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int64_t t = t0 + 64 * wave + 4 * j + ts;
+      const bool ok = t < T;
+      const uint32_t r = (uint32_t)(t * Hkv);   // rows from row0
+      vw[j] = __builtin_amdgcn_raw_buffer_load_b32(crs, ok ? r * (kD / 2) + 4u * dq : dev::kOutOfRange, 0, 0);
+      vsc[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srs, ok ? 4u * r : dev::kOutOfRange, 0, 0));
+      vzz[j] = (float)__builtin_amdgcn_raw_buffer_load_b8(zrs, ok ? r : dev::kOutOfRange, 0, 0);
+    }
     float acc[G][8], accz[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -167,27 +185,22 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
 #pragma unroll
       for (int i = 0; i < 8; ++i) acc[g][i] = 0.f;
     }
+#pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int tl = 64 * wave + 4 * j + ts;
-      const int64_t t = t0 + tl;
-      if (t < T) {
-        const int64_t row = (b * T + t) * Hkv + kv;
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(vc + row * (kD / 2) + 4 * dq);
-        const float s = vs[row], z = (float)vz[row];
-        const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;
-        float cv[8];
+      const uint32_t lo = vw[j] & 0x0F0F0F0Fu, hi = (vw[j] >> 4) & 0x0F0F0F0Fu;
+      float cv[8];
 #pragma unroll
-        for (int by = 0; by < 4; ++by) {
-          cv[2 * by] = (float)((lo >> (8 * by)) & 0xFFu);
-          cv[2 * by + 1] = (float)((hi >> (8 * by)) & 0xFFu);
-        }
+      for (int by = 0; by < 4; ++by) {
+        cv[2 * by] = (float)((lo >> (8 * by)) & 0xFFu);
+        cv[2 * by + 1] = (float)((hi >> (8 * by)) & 0xFFu);
+      }
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float ps = pr[g][tl] * s;
-          accz[g] = fmaf(ps, z, accz[g]);
+      for (int g = 0; g < G; ++g) {
+        const float ps = pr[g][tl] * vsc[j];
+        accz[g] = fmaf(ps, vzz[j], accz[g]);
 #pragma unroll
-          for (int i = 0; i < 8; ++i) acc[g][i] = fmaf(ps, cv[i], acc[g][i]);
-        }
+        for (int i = 0; i < 8; ++i) acc[g][i] = fmaf(ps, cv[i], acc[g][i]);
       }
     }
 #pragma unroll
@@ -218,26 +231,44 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
   }
 }
 
-// out[b][kv G + g][:] = sum_c e^(m_c - M) part_c / sum_c e^(m_c - M) l_c,  M = max_c m_c
+// out[b][kv G + g][:] = sum_c e^(m_c - M) part_c / sum_c e^(m_c - M) l_c,  M = max_c m_c.
+// Workgroup (kv G + g, b), thread dd: the maximum by a block reduction, then per tile of 128 chunks
+// the chunk weights once into LDS and the sum over the tile (independent, coalesced loads).
 template <int G>
-__global__ __launch_bounds__(256) void k_kv4_merge(const float* __restrict__ part, int Hq, int Hkv, int nchunks,
-                                                   uint16_t* __restrict__ y) {
-  const int kv = blockIdx.x;
+__global__ __launch_bounds__(kD) void k_kv4_merge(const float* __restrict__ part, int Hq, int Hkv, int nchunks,
+                                                  uint16_t* __restrict__ y) {
+  __shared__ float red[kD / 64];
+  __shared__ float ew[kD], lw[kD];
+  const int dd = threadIdx.x, lane = dd & 63, wave = dd >> 6;
+  const int kv = blockIdx.x / G, g = blockIdx.x % G;
   const int64_t b = blockIdx.y;
-  const float* base = part + (((int64_t)b * Hkv + kv) * nchunks) * G * kPart;
-  for (int i = threadIdx.x; i < G * kD; i += 256) {
-    const int g = i / kD, dd = i % kD;
-    float M = -INFINITY;
-    for (int c = 0; c < nchunks; ++c) M = fmaxf(M, base[(c * G + g) * kPart + kD]);
-    float L = 0.f, acc = 0.f;
-    for (int c = 0; c < nchunks; ++c) {
-      const float* r = base + (c * G + g) * kPart;
+  const float* base = part + (((int64_t)b * Hkv + kv) * nchunks) * G * kPart + g * kPart;
+  const int64_t cstride = (int64_t)G * kPart;
+  float M = -INFINITY;
+  for (int c = dd; c < nchunks; c += kD) M = fmaxf(M, base[c * cstride + kD]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  if (lane == 0) red[wave] = M;
+  __syncthreads();
+  M = fmaxf(red[0], red[1]);
+  float acc = 0.f, L = 0.f;
+  for (int c0 = 0; c0 < nchunks; c0 += kD) {
+    __syncthreads();   // the previous tile's weights have been read
+    if (c0 + dd < nchunks) {
+      const float* r = base + (c0 + dd) * cstride;
       const float e = expf(r[kD] - M);
-      L = fmaf(r[kD + 1], e, L);
-      acc = fmaf(r[dd], e, acc);
+      ew[dd] = e;
+      lw[dd] = r[kD + 1] * e;
     }
-    y[(b * Hq + (int64_t)kv * G + g) * kD + dd] = __half_as_ushort(__float2half_rn(acc / L));
+    __syncthreads();
+    const int n = nchunks - c0 < kD ? nchunks - c0 : kD;
+#pragma unroll 8
+    for (int i = 0; i < n; ++i) {
+      acc = fmaf(base[(c0 + i) * cstride + dd], ew[i], acc);
+      L += lw[i];
+    }
   }
+  y[(b * Hq + (int64_t)kv * G + g) * kD + dd] = __half_as_ushort(__float2half_rn(acc / L));
 }
 
 template <int G>
@@ -249,7 +280,8 @@ hipError_t launch_attn_g(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t 
                      Hkv, T, kc, ks, kz, vc, vs, vz, part, nchunks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_kv4_merge<G>), dim3((unsigned)Hkv, (unsigned)B), dim3(256), 0, s, part, Hq, Hkv, nchunks, y);
+  hipLaunchKernelGGL((k_kv4_merge<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(kD), 0, s, part, Hq, Hkv, nchunks,
+                     y);
   return hipGetLastError();
 }
 
