@@ -18,9 +18,9 @@
 // k_kv4_merge combines the chunks.  The reconstruction is folded into the sums:
 //   q . k_t = s_t (sum_i code_{t,i} q_i - z_t sum_i q_i),
 //   sum_t p_t v_t = sum_t (p_t s_t) code_t - sum_t p_t s_t z_t,
-// so the key phase (one cached token per lane: a dot product without cross-lane reductions)
-// converts codes to fp32 and multiplies, and the value phase (lanes over dimensions, four token
-// streams per wave) accumulates with one multiply-add per code.
+// so the key phase multiplies codes (exact in fp16) by the queries on the f16 MFMA, 16 tokens x
+// 32 dimensions per instruction, and the value phase (lanes over dimensions, four token streams
+// per wave) accumulates with one multiply-add per code.
 #include "qift_fwht.h"
 #include "qift_internal.h"
 
@@ -29,6 +29,28 @@ namespace {
 
 constexpr int kD = 128;         // head dimension
 constexpr int kChunk = 256;     // cached tokens per workgroup
+
+typedef _Float16 v2h __attribute__((ext_vector_type(2)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
+
+// Eight 4-bit codes (byte m holds the codes of elements 2m and 2m + 1 in its low and high nibble)
+// as exact fp16 values: each byte's nibbles go to the two halves of a word, OR 0x6400 makes them
+// 1024 + code, and a packed subtraction of 1024 leaves the code.
+__device__ __forceinline__ v8h codes_to_f16(uint32_t w) {
+  const uint32_t w4 = w >> 4;
+  v8h r;
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const uint32_t sel = (uint32_t)m | (0x0Cu << 8) | ((4u + m) << 16) | (0x0Cu << 24);
+    const uint32_t bits = (__builtin_amdgcn_perm(w4, w, sel) & 0x000F000Fu) | 0x64006400u;
+    const v2h h = __builtin_bit_cast(v2h, bits) - v2h{(_Float16)1024.f, (_Float16)1024.f};
+    r[2 * m] = h[0];
+    r[2 * m + 1] = h[1];
+  }
+  return r;
+}
 
 __global__ __launch_bounds__(256) void k_kv4_quant(const uint16_t* __restrict__ x, int64_t groups,
                                                    uint8_t* __restrict__ codes, float* __restrict__ scales,
@@ -69,68 +91,115 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
                                                   const uint8_t* __restrict__ kz, const uint8_t* __restrict__ vc,
                                                   const float* __restrict__ vs, const uint8_t* __restrict__ vz,
                                                   float* __restrict__ part, int nchunks) {
-  __shared__ float qs[kD][G];            // the group's queries / sqrt(d), dimension-major
-  __shared__ float qsum[G];
-  __shared__ float pr[G][kChunk];        // scores, then exp(score - m)
-  __shared__ float stat[G][2];
-  __shared__ float red[4][G][kD];
+  constexpr int Gp = G < 4 ? 4 : G;      // heads per value-phase output row, padded to a float4
+  __shared__ float pr[G][kChunk];        // scores, then P_t f_g (below)
+  __shared__ float sz[4][kChunk];        // key scale, key zero-point, value scale, value zero-point
+  __shared__ float stat[G][4];           // m, l, Z, 2^24 / f_g
+  // value codes, 64 bytes per token with the 16-byte slots of row r XOR-swizzled by (r / 4) mod 4
+  // (the transposed reads below then hit 32 distinct banks per 16 lanes); once a wave has read its
+  // 64 rows it reuses them for its partial sums [dimension][Gp]
+  __shared__ __attribute__((aligned(16))) uint32_t vl[kChunk * (kD / 8)];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int chunk = blockIdx.x, kv = blockIdx.y;
   const int64_t b = blockIdx.z;
   const int64_t t0 = (int64_t)chunk * kChunk;
+  const int nt = (int)(T - t0 < kChunk ? T - t0 : kChunk);   // tokens of this chunk
+  const int64_t row0 = (b * T) * Hkv + kv;     // cache row of token 0; token t is row0 + t Hkv
+  const uint32_t rows = (uint32_t)(T * Hkv);   // T Hkv 64 < 2^31: checked by the host, so 32-bit
+  const uint32_t rc = (uint32_t)t0 * (uint32_t)Hkv;   // offsets below cannot wrap
+  const __amdgpu_buffer_rsrc_t kcr = dev::make_rsrc(kc + row0 * (kD / 2), rows * (kD / 2));
+  const __amdgpu_buffer_rsrc_t vcr = dev::make_rsrc(vc + row0 * (kD / 2), rows * (kD / 2));
+  const __amdgpu_buffer_rsrc_t ksr = dev::make_rsrc(ks + row0, rows * 4u);
+  const __amdgpu_buffer_rsrc_t vsr = dev::make_rsrc(vs + row0, rows * 4u);
+  const __amdgpu_buffer_rsrc_t kzr = dev::make_rsrc(kz + row0, rows);
+  const __amdgpu_buffer_rsrc_t vzr = dev::make_rsrc(vz + row0, rows);
 
-  const float rsd = 1.0f / sqrtf((float)kD);
-  for (int i = tid; i < kD * G; i += 256) {
-    const int g = i / kD, dd = i % kD;
-    qs[dd][g] = __half2float(__ushort_as_half(q[(b * Hq + (int64_t)kv * G + g) * kD + dd])) * rsd;
-  }
-  __syncthreads();
-  if (tid < G) {
-    float sum = 0.f;
-    for (int dd = 0; dd < kD; ++dd) sum += qs[dd][tid];
-    qsum[tid] = sum;
-  }
-  __syncthreads();
-
-  // ---- scores: one cached token per lane
+  // ---- every load of the chunk is issued before any is used, so a workgroup waits on HBM once.
+  // Range-checked buffer loads return zeros for tokens past T (their weights are zeroed below).
+  // Thread tid: scale and zero-point of token t0 + tid, key and value.
+  float own[4];
   {
-    const int64_t t = t0 + 64 * wave + lane;
-    float sc[G];
-    if (t < T) {
-      const int64_t row = (b * T + t) * Hkv + kv;
-      const uint4* src = reinterpret_cast<const uint4*>(kc + row * (kD / 2));
-      float acc[G];
+    const bool ok = tid < nt;
+    const uint32_t r = rc + (uint32_t)tid * Hkv;
+    own[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ksr, ok ? 4u * r : dev::kOutOfRange, 0, 0));
+    own[1] = (float)__builtin_amdgcn_raw_buffer_load_b8(kzr, ok ? r : dev::kOutOfRange, 0, 0);
+    own[2] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(vsr, ok ? 4u * r : dev::kOutOfRange, 0, 0));
+    own[3] = (float)__builtin_amdgcn_raw_buffer_load_b8(vzr, ok ? r : dev::kOutOfRange, 0, 0);
+  }
+  // Key phase operands, lane (c, kg) = (lane mod 16, lane / 16): the B operand holds the G queries
+  // (columns >= G zero), lane group kg of k-step st covering dimensions 32 kg + 8 st .. + 7; the A
+  // operand of tile i is 16 tokens' codes, a lane loading the 16 bytes of dimensions 32 kg .. + 31 of
+  // token 64 wave + 16 i + c (the MFMA pairs A and B element by element within a lane group, so
+  // any assignment of dimensions to k-steps that both operands share gives the same sum).
+  const int c = lane & 15, kg = lane >> 4;
+  v8h qb[4];
 #pragma unroll
-      for (int g = 0; g < G; ++g) acc[g] = 0.f;
+  for (int st = 0; st < 4; ++st) {
+    if (c < G) {
+      const uint4 u = *reinterpret_cast<const uint4*>(q + (b * Hq + (int64_t)kv * G + c) * kD + 32 * kg + 8 * st);
+      qb[st] = __builtin_bit_cast(v8h, u);
+    } else {
+      qb[st] = v8h{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+  }
+  uint4 kw[4];
 #pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) {
-        const uint4 w = src[c4];
-        const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+  for (int tile = 0; tile < 4; ++tile) {
+    const int tl = 64 * wave + 16 * tile + c;
+    kw[tile] = dev::bload16(kcr, tl < nt ? (rc + (uint32_t)tl * Hkv) * (kD / 2) + 16u * kg : dev::kOutOfRange);
+  }
+  // Value codes of the wave's 64 tokens: load u, lane l takes 16-byte slot l mod 4 of token
+  // 64 wave + 16 u + l / 4 (it goes to LDS before the value phase).
+  uint4 vq[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint32_t lo = ww[k] & 0x0F0F0F0Fu, hi = (ww[k] >> 4) & 0x0F0F0F0Fu;
+  for (int u = 0; u < 4; ++u) {
+    const int tl = 64 * wave + 16 * u + (lane >> 2);
+    vq[u] = dev::bload16(vcr, tl < nt ? (rc + (uint32_t)tl * Hkv) * (kD / 2) + 16u * (lane & 3) : dev::kOutOfRange);
+  }
+
+  // sum of query head c's (fp16) components, for the zero-point term: the lane's 32, then over kg
+  float qsum = 0.f;
 #pragma unroll
-          for (int by = 0; by < 4; ++by) {
-            const int j = 16 * c4 + 4 * k + by;   // byte j holds values 2j (low) and 2j + 1 (high)
-            const float ce = (float)((lo >> (8 * by)) & 0xFFu), co = (float)((hi >> (8 * by)) & 0xFFu);
+  for (int st = 0; st < 4; ++st)
 #pragma unroll
-            for (int g = 0; g < G; ++g) acc[g] = fmaf(co, qs[2 * j + 1][g], fmaf(ce, qs[2 * j][g], acc[g]));
-          }
+    for (int e = 0; e < 8; ++e) qsum += (float)qb[st][e];
+  qsum += __shfl_xor(qsum, 16);
+  qsum += __shfl_xor(qsum, 32);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) sz[i][tid] = own[i];
+  __syncthreads();
+
+  // ---- scores on the f16 MFMA: per 16 tokens, D[token][head] = sum over the 128 dimensions of
+  // code x query (4 MFMAs of 32 dimensions); q . k_t = s_t (D - z_t sum q).
+  {
+    const float rsd = 1.0f / sqrtf((float)kD);
+#pragma unroll
+    for (int tile = 0; tile < 4; ++tile) {
+      const uint32_t ww[4] = {kw[tile].x, kw[tile].y, kw[tile].z, kw[tile].w};
+      v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 4; ++st) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(codes_to_f16(ww[st]), qb[st], acc, 0, 0, 0);
+      // D: lane (c, kg) holds tokens 16 tile + 4 kg + i of head c
+      if (c < G) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tl = 64 * wave + 16 * tile + 4 * kg + i;
+          pr[c][tl] = tl < nt ? sz[0][tl] * (acc[i] - sz[1][tl] * qsum) * rsd : -INFINITY;
         }
       }
-      const float s = ks[row], z = (float)kz[row];
-#pragma unroll
-      for (int g = 0; g < G; ++g) sc[g] = s * (acc[g] - z * qsum[g]);
-    } else {
-#pragma unroll
-      for (int g = 0; g < G; ++g) sc[g] = -INFINITY;
     }
+  }
 #pragma unroll
-    for (int g = 0; g < G; ++g) pr[g][64 * wave + lane] = sc[g];
+  for (int u = 0; u < 4; ++u) {
+    const int row = 64 * wave + 16 * u + (lane >> 2);   // (row / 4) mod 4 = (lane / 16) mod 4
+    *reinterpret_cast<uint4*>(&vl[row * (kD / 8) + 4 * ((lane & 3) ^ ((lane >> 4) & 3))]) = vq[u];
   }
   __syncthreads();
 
-  // ---- the chunk's softmax statistics, one wave per head
+  // ---- the chunk's softmax statistics, one wave per head: m, l = sum_t e_t with e_t = exp(score_t
+  // - m), and for the value phase P_t = e_t s_t and Z = sum_t P_t z_t.  pr receives P_t f_g with f_g
+  // the power of two that puts the chunk's largest P in [2^14, 2^15): the value phase splits it into
+  // two fp16 parts without overflow and with the small terms far above the fp16 subnormal range.
   for (int g = wave; g < G; g += 4) {
     float v[kChunk / 64];
     float m = -INFINITY;
@@ -141,89 +210,105 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-    float l = 0.f;
+    float l = 0.f, zs = 0.f, pm = __FLT_MIN__;
 #pragma unroll
     for (int i = 0; i < kChunk / 64; ++i) {
+      const int tl = 64 * i + lane;
       const float e = v[i] == -INFINITY ? 0.f : expf(v[i] - m);
-      pr[g][64 * i + lane] = e;
+      const float P = e * sz[2][tl];
+      v[i] = P;
+      pm = fmaxf(pm, P);
       l += e;
+      zs = fmaf(P, sz[3][tl], zs);
     }
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o);
+    for (int o = 32; o >= 1; o >>= 1) {
+      l += __shfl_xor(l, o);
+      zs += __shfl_xor(zs, o);
+      pm = fmaxf(pm, __shfl_xor(pm, o));
+    }
+    const int ex = ilogbf(pm);   // pm normal: P of the top token is its scale s > 0
+    const float f = ldexpf(1.0f, 14 - ex);
+#pragma unroll
+    for (int i = 0; i < kChunk / 64; ++i) pr[g][64 * i + lane] = v[i] * f;
     if (lane == 0) {
       stat[g][0] = m;
       stat[g][1] = l;
+      stat[g][2] = zs;
+      stat[g][3] = ldexpf(1.0f, 10 + ex);   // 2^24 / f
     }
   }
   __syncthreads();
 
-  // ---- values: lane l covers dimensions 8 (l mod 16) .. + 7 of tokens 64 wave + 4 j + l / 16.  All
-  // sixteen tokens' codes, scales and zero-points are loaded first (range-checked buffer loads: zeros
-  // past T, where the weights are 0 as well), then accumulated.
+  // ---- values on the f16 MFMA: D[head][dim] = sum over the wave's 64 tokens of A[head][token]
+  // B[token][dim], A = P f (rows >= G zero) as an fp16 high part plus an fp16 low part (two MFMAs,
+  // 2^-22 relative), B = the codes.  The transposing LDS read gives lane (i, kg) = (lane mod 16,
+  // lane / 16) the 16 codes of dimension 16 dt + i for tokens 64 wave + 16 kg + 0 .. 15 (the rows
+  // that the 16 lanes of its group address), nibble n for token n.  A code masked in place within
+  // a 16-bit half is an exact fp16 subnormal: code 2^-24 (bits 0-3 of the half) or code 2^-20
+  // (bits 4-7), so B element e is nibble NIB[e] of its word and the A element it meets carries 1/16
+  // for the second kind; D = 2^-24 sum_t P_t f code_t.  Z is subtracted when the partial is written.
   {
-    const int dq = lane & 15, ts = lane >> 4;
-    const int64_t row0 = (b * T) * Hkv + kv;   // cache row of token 0; token t is row0 + t Hkv
-    const uint32_t rows = (uint32_t)(T * Hkv);   // T Hkv 64 < 2^31: checked by the host
-    const __amdgpu_buffer_rsrc_t crs = dev::make_rsrc(vc + row0 * (kD / 2), rows * (kD / 2));
-    const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(vs + row0, rows * 4u);
-    const __amdgpu_buffer_rsrc_t zrs = dev::make_rsrc(vz + row0, rows);
-    uint32_t vw[16];
-    float vsc[16], vzz[16];
+    const int i16 = lane & 15, kg = lane >> 4;
+    constexpr int NIB[8] = {0, 4, 1, 5, 2, 6, 3, 7};
+    v8h ahi[2], alo[2];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int64_t t = t0 + 64 * wave + 4 * j + ts;
-      const bool ok = t < T;
-      const uint32_t r = (uint32_t)(t * Hkv);   // rows from row0
-      vw[j] = __builtin_amdgcn_raw_buffer_load_b32(crs, ok ? r * (kD / 2) + 4u * dq : dev::kOutOfRange, 0, 0);
-      vsc[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(srs, ok ? 4u * r : dev::kOutOfRange, 0, 0));
-      vzz[j] = (float)__builtin_amdgcn_raw_buffer_load_b8(zrs, ok ? r : dev::kOutOfRange, 0, 0);
-    }
-    float acc[G][8], accz[G];
+    for (int st = 0; st < 2; ++st) {
+      float pv[8];
+      if (i16 < G) {
+        const float4 x0 = *reinterpret_cast<const float4*>(&pr[i16][64 * wave + 16 * kg + 8 * st]);
+        const float4 x1 = *reinterpret_cast<const float4*>(&pr[i16][64 * wave + 16 * kg + 8 * st + 4]);
+        pv[0] = x0.x; pv[1] = x0.y; pv[2] = x0.z; pv[3] = x0.w;
+        pv[4] = x1.x; pv[5] = x1.y; pv[6] = x1.z; pv[7] = x1.w;
+      } else {
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      accz[g] = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc[g][i] = 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int tl = 64 * wave + 4 * j + ts;
-      const uint32_t lo = vw[j] & 0x0F0F0F0Fu, hi = (vw[j] >> 4) & 0x0F0F0F0Fu;
-      float cv[8];
-#pragma unroll
-      for (int by = 0; by < 4; ++by) {
-        cv[2 * by] = (float)((lo >> (8 * by)) & 0xFFu);
-        cv[2 * by + 1] = (float)((hi >> (8 * by)) & 0xFFu);
+        for (int e = 0; e < 8; ++e) pv[e] = 0.f;
       }
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float ps = pr[g][tl] * vsc[j];
-        accz[g] = fmaf(ps, vzz[j], accz[g]);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[g][i] = fmaf(ps, cv[i], acc[g][i]);
+      for (int e = 0; e < 8; e += 2) {
+        const float x = (e & 2) ? pv[NIB[e]] * 0.0625f : pv[NIB[e]];
+        const float y = (e & 2) ? pv[NIB[e + 1]] * 0.0625f : pv[NIB[e + 1]];
+        const v2h h = __builtin_bit_cast(v2h, __builtin_amdgcn_cvt_pkrtz(x, y));
+        const v2h r = __builtin_bit_cast(v2h, __builtin_amdgcn_cvt_pkrtz(x - (float)h[0], y - (float)h[1]));
+        ahi[st][e] = h[0];
+        ahi[st][e + 1] = h[1];
+        alo[st][e] = r[0];
+        alo[st][e + 1] = r[1];
       }
     }
+    const int row = 64 * wave + 16 * kg + i16;   // the row this lane addresses
+    v4f acc[8];
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+    for (int dt = 0; dt < 8; ++dt) {
+      const uint32_t off = row * (kD / 8) + 4 * ((dt >> 1) ^ ((row >> 2) & 3)) + 2 * (dt & 1);
+      const v2i t = __builtin_amdgcn_ds_read_tr4_b64_v2i32((__attribute__((address_space(3))) v2i*)(vl + off));
+      acc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        float v = acc[g][i] - accz[g];
-        v += __shfl_xor(v, 16);
-        v += __shfl_xor(v, 32);
-        acc[g][i] = v;
+      for (int st = 0; st < 2; ++st) {
+        const uint32_t w = st ? (uint32_t)t.y : (uint32_t)t.x, w8 = w >> 8;
+        const uint4 hb = {w & 0x000F000Fu, w & 0x00F000F0u, w8 & 0x000F000Fu, w8 & 0x00F000F0u};
+        const v8h bv = __builtin_bit_cast(v8h, hb);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ahi[st], bv, acc[dt], 0, 0, 0);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(alo[st], bv, acc[dt], 0, 0, 0);
       }
-    if (lane < 16) {
+    }
+    // D lane (i16, kg) holds heads 4 kg .. 4 kg + 3 of dimension 16 dt + i16; the wave's own rows
+    // take them (its transposed reads above are done: a wave's LDS operations complete in order)
+    if (4 * kg < G) {
+      float* red = reinterpret_cast<float*>(vl) + 64 * wave * (kD / 8);
 #pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) red[wave][g][8 * dq + i] = acc[g][i];
+      for (int dt = 0; dt < 8; ++dt)
+        *reinterpret_cast<v4f*>(&red[(16 * dt + i16) * Gp + 4 * kg]) = acc[dt];
     }
   }
   __syncthreads();
   float* out = part + ((((int64_t)b * Hkv + kv) * nchunks + chunk) * G) * kPart;
+  const float* red = reinterpret_cast<const float*>(vl);
+  constexpr int kWaveRed = 64 * (kD / 8);   // floats per wave's region
   for (int i = tid; i < G * kD; i += 256) {
-    const int g = i / kD, dd = i % kD;
-    out[g * kPart + dd] = (red[0][g][dd] + red[1][g][dd]) + (red[2][g][dd] + red[3][g][dd]);
+    const int g = i / kD, dd = i % kD, o = dd * Gp + g;
+    const float sum = (red[o] + red[kWaveRed + o]) + (red[2 * kWaveRed + o] + red[3 * kWaveRed + o]);
+    out[g * kPart + dd] = sum * stat[g][3] - stat[g][2];
   }
   if (tid < G) {
     out[tid * kPart + kD] = stat[tid][0];
