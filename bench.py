@@ -401,43 +401,49 @@ def kv4_attention(torch, qift, reps=10, layers=32):
     """KV4 caches of the 32 layers of LLaMA-3.1-8B (32 query heads, 8 KV heads, head_dim 128): one
     decode step's attention over T cached tokens for B sequences, i.e. 32 launches over 32 distinct
     caches in one hipGraph (HBM roofline: each 4-bit cache is read once, 64 B of codes + 4 B scale
-    + 1 B zero-point per token, KV head and tensor); and the quantizer writing one layer's cache of
-    T tokens (fp16 in, KV4 out)."""
+    + 1 B zero-point per token, KV head and tensor), for both cache row orders (head-major
+    [B, Hkv, T], token-major [B, T, Hkv]); and the quantizer writing one layer's cache of T tokens
+    (fp16 in, KV4 out)."""
     dev = torch.device("cuda")
     Hq, Hkv = 32, 8
     gen = torch.Generator(device=dev)
     gen.manual_seed(4)
     rows = []
     for B, T in ((1, 4096), (1, 32768), (16, 4096)):
-        caches = []
-        for _ in range(layers):
-            K = torch.randn((B, T, Hkv, 128), device=dev, generator=gen).half()
-            V = torch.randn((B, T, Hkv, 128), device=dev, generator=gen).half()
-            caches.append((qift.kv4_quant(K), qift.kv4_quant(V)))
-        q = torch.randn((B, Hq, 128), device=dev, generator=gen).half()
-        y = torch.empty((B, Hq, 128), dtype=torch.float16, device=dev)
-        ws = torch.empty(qift.lib().qift_kv4_attention_workspace_bytes(B, Hq, Hkv, 128, T), dtype=torch.uint8,
-                         device=dev)
+        for head_major in (True, False):
+            shape = (B, Hkv, T, 128) if head_major else (B, T, Hkv, 128)
+            caches = []
+            for _ in range(layers):
+                K = torch.randn(shape, device=dev, generator=gen).half()
+                V = torch.randn(shape, device=dev, generator=gen).half()
+                caches.append((qift.kv4_quant(K), qift.kv4_quant(V)))
+            q = torch.randn((B, Hq, 128), device=dev, generator=gen).half()
+            y = torch.empty((B, Hq, 128), dtype=torch.float16, device=dev)
+            ws = torch.empty(qift.lib().qift_kv4_attention_workspace_bytes(B, Hq, Hkv, 128, T), dtype=torch.uint8,
+                             device=dev)
 
-        def step():
-            for k, v in caches:
-                qift.kv4_attention_decode(q, k, v, out=y, workspace=ws)
-        dt = _time_graph(torch, step, reps) / layers
-        cache = 2 * B * T * Hkv * (64 + 4 + 1)
-        gbs = (cache + 4 * B * Hq * 128) / dt / 1e9
-        k, v = caches[0]
+            def step():
+                for k, v in caches:
+                    qift.kv4_attention_decode(q, k, v, out=y, workspace=ws, head_major=head_major)
+            dt = _time_graph(torch, step, reps) / layers
+            cache = 2 * B * T * Hkv * (64 + 4 + 1)
+            gbs = (cache + 4 * B * Hq * 128) / dt / 1e9
+            row = {"B": B, "T": T, "layout": "head-major" if head_major else "token-major",
+                   "attention_us_per_layer": round(dt * 1e6, 2), "cache_bytes_per_layer": cache,
+                   "attention_GBs": round(gbs, 1), "attention_pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)}
+            if head_major:
+                k, v = caches[0]
 
-        def quant():
-            for _ in range(4):
-                qift.kv4_quant(K, out=k)
-                qift.kv4_quant(V, out=v)
-        dq = _time_graph(torch, quant, reps) / 4
-        qgbs = (2 * B * T * Hkv * 256 + cache) / dq / 1e9
-        rows.append({"B": B, "T": T, "attention_us_per_layer": round(dt * 1e6, 2), "cache_bytes_per_layer": cache,
-                     "attention_GBs": round(gbs, 1), "attention_pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
-                     "quant_us_per_layer": round(dq * 1e6, 2), "quant_GBs": round(qgbs, 1)})
-        del K, V, caches, ws
-        torch.cuda.empty_cache()
+                def quant():
+                    for _ in range(4):
+                        qift.kv4_quant(K, out=k)
+                        qift.kv4_quant(V, out=v)
+                dq = _time_graph(torch, quant, reps) / 4
+                row["quant_us_per_layer"] = round(dq * 1e6, 2)
+                row["quant_GBs"] = round((2 * B * T * Hkv * 256 + cache) / dq / 1e9, 1)
+            rows.append(row)
+            del K, V, caches, ws
+            torch.cuda.empty_cache()
     return {"workload": "LLaMA-3.1-8B attention at decode, 32 layers: Hq 32, Hkv 8, head_dim 128, KV4 cache "
                         "(clip 0.95), T cached tokens per sequence, B sequences", "rows": rows}
 

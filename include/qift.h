@@ -289,18 +289,26 @@ int qift_kv4_quant(const uint16_t *x, int64_t groups, int32_t head_dim, uint8_t 
 size_t qift_kv4_attention_workspace_bytes(int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
                                           int64_t T);
 
+/* Cache row orders of qift_kv4_attention_decode (a row is one token's key or value vector of
+ * one KV head: 64 code bytes, one scale, one zero-point).  Token-major [B][T][Hkv] is the order
+ * of a [B, T, Hkv, 128] tensor, as one decode step appends a token; head-major [B][Hkv][T] keeps
+ * each KV head's tokens contiguous, which the attention reads as one stream per workgroup
+ * (measured faster: the token-major order interleaves KV heads at 64-byte granularity). */
+enum { QIFT_KV4_TOKEN_MAJOR = 0, QIFT_KV4_HEAD_MAJOR = 1 };
+
 /*
  * One decode step of grouped-query attention over a KV4 cache (Sec. 1: the
  * decode stream is weights plus KV cache).  For batch b and query head h,
  * with KV head kv = h / (Hq / Hkv):
- *   out[b][h] = sum_t softmax_t( q[b][h] . k_hat[b][t][kv] / sqrt(128) )
- *               * v_hat[b][t][kv],   x_hat = s (code - z) per group,
+ *   out[b][h] = sum_t softmax_t( q[b][h] . k_hat[b, t, kv] / sqrt(128) )
+ *               * v_hat[b, t, kv],   x_hat = s (code - z) per group,
  * in fp32 (scores, exponentials and sums) with an fp16 result; the result is
  * within rounding of the exact softmax of the reconstructed cache.
  *   q        fp16 [B][Hq][128], the new token's queries.
- *   k_*, v_* the cache as written by qift_kv4_quant for groups [B][T][Hkv]:
- *            codes uint8 [B][T][Hkv][64], scales fp32 and zeros uint8
- *            [B][T][Hkv].
+ *   layout   QIFT_KV4_TOKEN_MAJOR or QIFT_KV4_HEAD_MAJOR (QIFT_ERR_SPEC otherwise).
+ *   k_*, v_* the cache as written by qift_kv4_quant for groups in that row
+ *            order: codes uint8 [rows][64], scales fp32 and zeros uint8
+ *            [rows], rows = [B][T][Hkv] or [B][Hkv][T].
  *   out      out: fp16 [B][Hq][128].
  *   workspace  device scratch of qift_kv4_attention_workspace_bytes bytes
  *            (per 256 cached tokens and query head: 128 partial sums, the
@@ -309,7 +317,7 @@ size_t qift_kv4_attention_workspace_bytes(int64_t B, int32_t Hq, int32_t Hkv, in
  * T * Hkv * 64 < 2^31.
  */
 int qift_kv4_attention_decode(const uint16_t *q, int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
-                              int64_t T, const uint8_t *k_codes, const float *k_scales,
+                              int64_t T, int32_t layout, const uint8_t *k_codes, const float *k_scales,
                               const uint8_t *k_zeros, const uint8_t *v_codes, const float *v_scales,
                               const uint8_t *v_zeros, uint16_t *out, void *workspace,
                               size_t workspace_bytes, qift_stream_t stream);

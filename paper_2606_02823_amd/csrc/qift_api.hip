@@ -131,16 +131,17 @@ size_t qift_kv4_attention_workspace_bytes(int64_t B, int32_t Hq, int32_t Hkv, in
 }
 
 int qift_kv4_attention_decode(const uint16_t* q, int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim, int64_t T,
-                              const uint8_t* k_codes, const float* k_scales, const uint8_t* k_zeros,
+                              int32_t layout, const uint8_t* k_codes, const float* k_scales, const uint8_t* k_zeros,
                               const uint8_t* v_codes, const float* v_scales, const uint8_t* v_zeros, uint16_t* out,
                               void* workspace, size_t workspace_bytes, qift_stream_t stream) {
   if (!q || !k_codes || !k_scales || !k_zeros || !v_codes || !v_scales || !v_zeros || !out) return QIFT_ERR_NULL;
   if (!kv4_attn_shape_ok(B, Hq, Hkv, head_dim, T)) return QIFT_ERR_SHAPE;
+  if (layout != QIFT_KV4_TOKEN_MAJOR && layout != QIFT_KV4_HEAD_MAJOR) return QIFT_ERR_SPEC;
   if (!workspace || workspace_bytes < qift::kv4_attention_workspace(B, Hq, T)) return QIFT_ERR_WORKSPACE;
   if (!aligned16(q) || !aligned16(k_codes) || !aligned16(k_scales) || !aligned16(k_zeros) || !aligned16(v_codes) ||
       !aligned16(v_scales) || !aligned16(v_zeros) || !aligned16(out) || !aligned16(workspace))
     return QIFT_ERR_ALIGN;
-  return hip_status(qift::launch_kv4_attention(q, B, Hq, Hkv, T, k_codes, k_scales, k_zeros, v_codes, v_scales,
+  return hip_status(qift::launch_kv4_attention(q, B, Hq, Hkv, T, layout == QIFT_KV4_HEAD_MAJOR, k_codes, k_scales, k_zeros, v_codes, v_scales,
                                                v_zeros, out, workspace, (hipStream_t)stream));
 }
 

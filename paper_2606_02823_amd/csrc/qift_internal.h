@@ -20,13 +20,14 @@ hipError_t launch_quantize_weights(const float* W, int64_t N, int64_t K, int blo
                                    uint16_t* scales, hipStream_t s);
 
 // KV4 cache quantizer and decode attention over it (qift_kv4.hip); head dimension 128, Hq / Hkv in
-// {1, 2, 4, 8}; ws holds kv4_attention_workspace(B, Hq, T) bytes.
+// {1, 2, 4, 8}; cache rows [B][T][Hkv] or, head_major, [B][Hkv][T]; ws holds
+// kv4_attention_workspace(B, Hq, T) bytes.
 size_t kv4_attention_workspace(int64_t B, int64_t Hq, int64_t T);
 hipError_t launch_kv4_quant(const uint16_t* x, int64_t groups, uint8_t* codes, float* scales, uint8_t* zeros,
                             hipStream_t s);
-hipError_t launch_kv4_attention(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t T, const uint8_t* kc,
-                                const float* ks, const uint8_t* kz, const uint8_t* vc, const float* vs,
-                                const uint8_t* vz, uint16_t* y, void* ws, hipStream_t s);
+hipError_t launch_kv4_attention(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t T, int head_major,
+                                const uint8_t* kc, const float* ks, const uint8_t* kz, const uint8_t* vc,
+                                const float* vs, const uint8_t* vz, uint16_t* y, void* ws, hipStream_t s);
 
 // Rotation + INT4 quantization (qift_act.hip)
 hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num,

@@ -16,11 +16,12 @@
 // Workgroup (chunk, kv, b) covers 256 cached tokens for the G query heads of one KV head and
 // writes its unnormalized partial output with the chunk's maximum score and sum of exponentials;
 // k_kv4_merge combines the chunks.  The reconstruction is folded into the sums:
-//   q . k_t = s_t (sum_i code_{t,i} q_i - z_t sum_i q_i),
+//   q . k_t = s_t sum_i (code_{t,i} - z_t) q_i,
 //   sum_t p_t v_t = sum_t (p_t s_t) code_t - sum_t p_t s_t z_t,
-// so the key phase multiplies codes (exact in fp16) by the queries on the f16 MFMA, 16 tokens x
-// 32 dimensions per instruction, and the value phase (lanes over dimensions, four token streams
-// per wave) accumulates with one multiply-add per code.
+// so both phases run on the f16 MFMA with the codes as exact fp16 operands: the key phase codes x
+// queries (16 tokens x 32 dimensions per instruction), the value phase P = p s (split into two fp16
+// parts) x codes (16 heads x 32 tokens x 16 dimensions), its operands read from LDS with the 4-bit
+// transposing read.  A workgroup issues all its loads first and waits on HBM once.
 #include "qift_fwht.h"
 #include "qift_internal.h"
 
@@ -35,21 +36,34 @@ typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef int v2i __attribute__((ext_vector_type(2)));
 
-// Eight 4-bit codes (byte m holds the codes of elements 2m and 2m + 1 in its low and high nibble)
-// as exact fp16 values: each byte's nibbles go to the two halves of a word, OR 0x6400 makes them
-// 1024 + code, and a packed subtraction of 1024 leaves the code.
-__device__ __forceinline__ v8h codes_to_f16(uint32_t w) {
-  const uint32_t w4 = w >> 4;
-  v8h r;
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const uint32_t sel = (uint32_t)m | (0x0Cu << 8) | ((4u + m) << 16) | (0x0Cu << 24);
-    const uint32_t bits = (__builtin_amdgcn_perm(w4, w, sel) & 0x000F000Fu) | 0x64006400u;
-    const v2h h = __builtin_bit_cast(v2h, bits) - v2h{(_Float16)1024.f, (_Float16)1024.f};
-    r[2 * m] = h[0];
-    r[2 * m + 1] = h[1];
-  }
-  return r;
+// Eight 4-bit codes of a word (nibble n at bits 4n) as MFMA fp16 operands without conversion: a code
+// masked in place within a 16-bit half is an exact fp16 subnormal, code 2^-24 (bits 0-3 of the half)
+// or code 2^-20 (bits 4-7).  Element e is nibble kNib[e]; elements with e & 2 carry the 2^-20 kind,
+// so the other operand's element e takes a factor 1/16 there and the product sums are 2^-24 times
+// the code sums.  The f16 MFMA sums products of subnormal inputs less precisely than those of
+// normal ones (measured on gfx950: about 9e-7 against 6e-8 of the sum of |products|), which the
+// value phase can afford (its error is linear in the output) and the scores cannot.
+constexpr int kNib[8] = {0, 4, 1, 5, 2, 6, 3, 7};
+__device__ __forceinline__ v8h codes_f16(uint32_t w) {
+  const uint32_t w8 = w >> 8;
+  const uint4 h = {w & 0x000F000Fu, w & 0x00F000F0u, w8 & 0x000F000Fu, w8 & 0x00F000F0u};
+  return __builtin_bit_cast(v8h, h);
+}
+
+// Eight 4-bit codes of one group minus its zero-point z, as exact normal fp16 values: a byte
+// permute puts each code below an 0x64 byte (the fp16 value 1024 + code) and a packed subtraction
+// of 1024 + z leaves code - z.  Element e is nibble kNibK[e] of the word.
+constexpr int kNibK[8] = {0, 2, 4, 6, 1, 3, 5, 7};
+__device__ __forceinline__ v8h codes_minus_z(uint32_t w, v2h base) {
+  const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;   // byte m: nibble 2m / 2m + 1
+  const uint32_t k64 = 0x64646464u;
+  // selector bytes 0-3 pick from the second operand, 4-7 from the first (all 0x64)
+  const uint32_t s01 = 0x04010400u, s23 = 0x04030402u;
+  const v2h h0 = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(k64, lo, s01)) - base;   // nibbles 0, 2
+  const v2h h1 = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(k64, lo, s23)) - base;   // nibbles 4, 6
+  const v2h h2 = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(k64, hi, s01)) - base;   // nibbles 1, 3
+  const v2h h3 = __builtin_bit_cast(v2h, __builtin_amdgcn_perm(k64, hi, s23)) - base;   // nibbles 5, 7
+  return v8h{h0[0], h0[1], h1[0], h1[1], h2[0], h2[1], h3[0], h3[1]};
 }
 
 __global__ __launch_bounds__(256) void k_kv4_quant(const uint16_t* __restrict__ x, int64_t groups,
@@ -90,7 +104,7 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
                                                   const uint8_t* __restrict__ kc, const float* __restrict__ ks,
                                                   const uint8_t* __restrict__ kz, const uint8_t* __restrict__ vc,
                                                   const float* __restrict__ vs, const uint8_t* __restrict__ vz,
-                                                  float* __restrict__ part, int nchunks) {
+                                                  float* __restrict__ part, int nchunks, int head_major) {
   constexpr int Gp = G < 4 ? 4 : G;      // heads per value-phase output row, padded to a float4
   __shared__ float pr[G][kChunk];        // scores, then P_t f_g (below)
   __shared__ float sz[4][kChunk];        // key scale, key zero-point, value scale, value zero-point
@@ -104,9 +118,11 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
   const int64_t b = blockIdx.z;
   const int64_t t0 = (int64_t)chunk * kChunk;
   const int nt = (int)(T - t0 < kChunk ? T - t0 : kChunk);   // tokens of this chunk
-  const int64_t row0 = (b * T) * Hkv + kv;     // cache row of token 0; token t is row0 + t Hkv
-  const uint32_t rows = (uint32_t)(T * Hkv);   // T Hkv 64 < 2^31: checked by the host, so 32-bit
-  const uint32_t rc = (uint32_t)t0 * (uint32_t)Hkv;   // offsets below cannot wrap
+  // cache row of token t: row0 + t rs, rows ordered [B][T][Hkv] (token-major) or [B][Hkv][T]
+  const uint32_t rs = head_major ? 1u : (uint32_t)Hkv;
+  const int64_t row0 = head_major ? ((int64_t)b * Hkv + kv) * T : (b * T) * Hkv + kv;
+  const uint32_t rows = (uint32_t)(T * rs);    // T Hkv 64 < 2^31: checked by the host, so 32-bit
+  const uint32_t rc = (uint32_t)t0 * rs;       // offsets below cannot wrap
   const __amdgpu_buffer_rsrc_t kcr = dev::make_rsrc(kc + row0 * (kD / 2), rows * (kD / 2));
   const __amdgpu_buffer_rsrc_t vcr = dev::make_rsrc(vc + row0 * (kD / 2), rows * (kD / 2));
   const __amdgpu_buffer_rsrc_t ksr = dev::make_rsrc(ks + row0, rows * 4u);
@@ -120,33 +136,30 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
   float own[4];
   {
     const bool ok = tid < nt;
-    const uint32_t r = rc + (uint32_t)tid * Hkv;
+    const uint32_t r = rc + (uint32_t)tid * rs;
     own[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ksr, ok ? 4u * r : dev::kOutOfRange, 0, 0));
     own[1] = (float)__builtin_amdgcn_raw_buffer_load_b8(kzr, ok ? r : dev::kOutOfRange, 0, 0);
     own[2] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(vsr, ok ? 4u * r : dev::kOutOfRange, 0, 0));
     own[3] = (float)__builtin_amdgcn_raw_buffer_load_b8(vzr, ok ? r : dev::kOutOfRange, 0, 0);
   }
-  // Key phase operands, lane (c, kg) = (lane mod 16, lane / 16): the B operand holds the G queries
-  // (columns >= G zero), lane group kg of k-step st covering dimensions 32 kg + 8 st .. + 7; the A
-  // operand of tile i is 16 tokens' codes, a lane loading the 16 bytes of dimensions 32 kg .. + 31 of
-  // token 64 wave + 16 i + c (the MFMA pairs A and B element by element within a lane group, so
-  // any assignment of dimensions to k-steps that both operands share gives the same sum).
+  // Key phase operands, lane (c, kg) = (lane mod 16, lane / 16): the A operand of tile i is 16
+  // tokens' codes, a lane loading the 16 bytes of dimensions 32 kg .. + 31 of token 64 wave + 16 i + c,
+  // word st holding dimensions 32 kg + 8 st + n in nibble n; the B operand holds the G queries
+  // (columns >= G zero) with element e of k-step st = dimension 32 kg + 8 st + kNibK[e] (the MFMA
+  // pairs A and B element by element within a lane group).
+  // (branch-free range-checked loads: a branch here would make the compiler wait for every load
+  // issued so far before the code loads below are issued)
   const int c = lane & 15, kg = lane >> 4;
-  v8h qb[4];
+  const __amdgpu_buffer_rsrc_t qr = dev::make_rsrc(q + (b * Hq + (int64_t)kv * G) * kD, G * kD * 2u);
+  uint4 qu[4];
 #pragma unroll
-  for (int st = 0; st < 4; ++st) {
-    if (c < G) {
-      const uint4 u = *reinterpret_cast<const uint4*>(q + (b * Hq + (int64_t)kv * G + c) * kD + 32 * kg + 8 * st);
-      qb[st] = __builtin_bit_cast(v8h, u);
-    } else {
-      qb[st] = v8h{0, 0, 0, 0, 0, 0, 0, 0};
-    }
-  }
+  for (int st = 0; st < 4; ++st)
+    qu[st] = dev::bload16(qr, c < G ? 2u * (c * kD + 32 * kg + 8 * st) : dev::kOutOfRange);
   uint4 kw[4];
 #pragma unroll
   for (int tile = 0; tile < 4; ++tile) {
     const int tl = 64 * wave + 16 * tile + c;
-    kw[tile] = dev::bload16(kcr, tl < nt ? (rc + (uint32_t)tl * Hkv) * (kD / 2) + 16u * kg : dev::kOutOfRange);
+    kw[tile] = dev::bload16(kcr, tl < nt ? (rc + (uint32_t)tl * rs) * (kD / 2) + 16u * kg : dev::kOutOfRange);
   }
   // Value codes of the wave's 64 tokens: load u, lane l takes 16-byte slot l mod 4 of token
   // 64 wave + 16 u + l / 4 (it goes to LDS before the value phase).
@@ -154,37 +167,39 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int tl = 64 * wave + 16 * u + (lane >> 2);
-    vq[u] = dev::bload16(vcr, tl < nt ? (rc + (uint32_t)tl * Hkv) * (kD / 2) + 16u * (lane & 3) : dev::kOutOfRange);
+    vq[u] = dev::bload16(vcr, tl < nt ? (rc + (uint32_t)tl * rs) * (kD / 2) + 16u * (lane & 3) : dev::kOutOfRange);
   }
 
-  // sum of query head c's (fp16) components, for the zero-point term: the lane's 32, then over kg
-  float qsum = 0.f;
+  v8h qb[4];
 #pragma unroll
-  for (int st = 0; st < 4; ++st)
+  for (int st = 0; st < 4; ++st) {
+    const v8h qraw = __builtin_bit_cast(v8h, qu[st]);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qsum += (float)qb[st][e];
-  qsum += __shfl_xor(qsum, 16);
-  qsum += __shfl_xor(qsum, 32);
+    for (int e = 0; e < 8; ++e) qb[st][e] = qraw[kNibK[e]];
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) sz[i][tid] = own[i];
   __syncthreads();
 
   // ---- scores on the f16 MFMA: per 16 tokens, D[token][head] = sum over the 128 dimensions of
-  // code x query (4 MFMAs of 32 dimensions); q . k_t = s_t (D - z_t sum q).
+  // (code - z_t) x query (4 MFMAs of 32 dimensions, every operand exact); q . k_t = s_t D.
   {
     const float rsd = 1.0f / sqrtf((float)kD);
 #pragma unroll
     for (int tile = 0; tile < 4; ++tile) {
       const uint32_t ww[4] = {kw[tile].x, kw[tile].y, kw[tile].z, kw[tile].w};
+      const _Float16 zb = (_Float16)(1024.0f + sz[1][64 * wave + 16 * tile + c]);   // exact: z <= 15
+      const v2h base = {zb, zb};
       v4f acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int st = 0; st < 4; ++st) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(codes_to_f16(ww[st]), qb[st], acc, 0, 0, 0);
+      for (int st = 0; st < 4; ++st)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(codes_minus_z(ww[st], base), qb[st], acc, 0, 0, 0);
       // D: lane (c, kg) holds tokens 16 tile + 4 kg + i of head c
       if (c < G) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int tl = 64 * wave + 16 * tile + 4 * kg + i;
-          pr[c][tl] = tl < nt ? sz[0][tl] * (acc[i] - sz[1][tl] * qsum) * rsd : -INFINITY;
+          pr[c][tl] = tl < nt ? sz[0][tl] * acc[i] * rsd : -INFINITY;
         }
       }
     }
@@ -244,13 +259,11 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
   // B[token][dim], A = P f (rows >= G zero) as an fp16 high part plus an fp16 low part (two MFMAs,
   // 2^-22 relative), B = the codes.  The transposing LDS read gives lane (i, kg) = (lane mod 16,
   // lane / 16) the 16 codes of dimension 16 dt + i for tokens 64 wave + 16 kg + 0 .. 15 (the rows
-  // that the 16 lanes of its group address), nibble n for token n.  A code masked in place within
-  // a 16-bit half is an exact fp16 subnormal: code 2^-24 (bits 0-3 of the half) or code 2^-20
-  // (bits 4-7), so B element e is nibble NIB[e] of its word and the A element it meets carries 1/16
-  // for the second kind; D = 2^-24 sum_t P_t f code_t.  Z is subtracted when the partial is written.
+  // that the 16 lanes of its group address), nibble n for token n.  B element e is the code of
+  // token kNib[e] of the word (codes_f16), and the A element it meets carries 1/16 where e & 2:
+  // D = 2^-24 sum_t P_t f code_t.  Z is subtracted when the partial is written.
   {
     const int i16 = lane & 15, kg = lane >> 4;
-    constexpr int NIB[8] = {0, 4, 1, 5, 2, 6, 3, 7};
     v8h ahi[2], alo[2];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
@@ -266,8 +279,8 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
       }
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
-        const float x = (e & 2) ? pv[NIB[e]] * 0.0625f : pv[NIB[e]];
-        const float y = (e & 2) ? pv[NIB[e + 1]] * 0.0625f : pv[NIB[e + 1]];
+        const float x = (e & 2) ? pv[kNib[e]] * 0.0625f : pv[kNib[e]];
+        const float y = (e & 2) ? pv[kNib[e + 1]] * 0.0625f : pv[kNib[e + 1]];
         const v2h h = __builtin_bit_cast(v2h, __builtin_amdgcn_cvt_pkrtz(x, y));
         const v2h r = __builtin_bit_cast(v2h, __builtin_amdgcn_cvt_pkrtz(x - (float)h[0], y - (float)h[1]));
         ahi[st][e] = h[0];
@@ -285,9 +298,7 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
       acc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
-        const uint32_t w = st ? (uint32_t)t.y : (uint32_t)t.x, w8 = w >> 8;
-        const uint4 hb = {w & 0x000F000Fu, w & 0x00F000F0u, w8 & 0x000F000Fu, w8 & 0x00F000F0u};
-        const v8h bv = __builtin_bit_cast(v8h, hb);
+        const v8h bv = codes_f16(st ? (uint32_t)t.y : (uint32_t)t.x);
         acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ahi[st], bv, acc[dt], 0, 0, 0);
         acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(alo[st], bv, acc[dt], 0, 0, 0);
       }
@@ -359,10 +370,10 @@ __global__ __launch_bounds__(kD) void k_kv4_merge(const float* __restrict__ part
 template <int G>
 hipError_t launch_attn_g(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t T, const uint8_t* kc,
                          const float* ks, const uint8_t* kz, const uint8_t* vc, const float* vs,
-                         const uint8_t* vz, uint16_t* y, float* part, hipStream_t s) {
+                         const uint8_t* vz, uint16_t* y, float* part, int head_major, hipStream_t s) {
   const int nchunks = (int)((T + kChunk - 1) / kChunk);
   hipLaunchKernelGGL((k_kv4_attn<G>), dim3((unsigned)nchunks, (unsigned)Hkv, (unsigned)B), dim3(256), 0, s, q, Hq,
-                     Hkv, T, kc, ks, kz, vc, vs, vz, part, nchunks);
+                     Hkv, T, kc, ks, kz, vc, vs, vz, part, nchunks, head_major);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_kv4_merge<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(kD), 0, s, part, Hq, Hkv, nchunks,
@@ -383,15 +394,15 @@ hipError_t launch_kv4_quant(const uint16_t* x, int64_t groups, uint8_t* codes, f
   return hipGetLastError();
 }
 
-hipError_t launch_kv4_attention(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t T, const uint8_t* kc,
-                                const float* ks, const uint8_t* kz, const uint8_t* vc, const float* vs,
-                                const uint8_t* vz, uint16_t* y, void* ws, hipStream_t s) {
+hipError_t launch_kv4_attention(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t T, int head_major,
+                                const uint8_t* kc, const float* ks, const uint8_t* kz, const uint8_t* vc,
+                                const float* vs, const uint8_t* vz, uint16_t* y, void* ws, hipStream_t s) {
   float* part = static_cast<float*>(ws);
   switch (Hq / Hkv) {
-    case 1: return launch_attn_g<1>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, s);
-    case 2: return launch_attn_g<2>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, s);
-    case 4: return launch_attn_g<4>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, s);
-    case 8: return launch_attn_g<8>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, s);
+    case 1: return launch_attn_g<1>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, head_major, s);
+    case 2: return launch_attn_g<2>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, head_major, s);
+    case 4: return launch_attn_g<4>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, head_major, s);
+    case 8: return launch_attn_g<8>(q, B, Hq, Hkv, T, kc, ks, kz, vc, vs, vz, y, part, head_major, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -73,7 +73,7 @@ def lib():
         "qift_quantize_weights": (ctypes.c_int, [vp, i64, HadamardSpec, i32, vp, vp, vp]),
         "qift_kv4_quant": (ctypes.c_int, [vp, i64, i32, vp, vp, vp, vp]),
         "qift_kv4_attention_workspace_bytes": (sz, [i64, i32, i32, i32, i64]),
-        "qift_kv4_attention_decode": (ctypes.c_int, [vp, i64, i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+        "qift_kv4_attention_decode": (ctypes.c_int, [vp, i64, i32, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                                      vp]),
         "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
@@ -256,23 +256,34 @@ def kv4_quant(x: torch.Tensor, out: KV4 | None = None, stream=None) -> KV4:
     return out
 
 
-def kv4_attention_decode(q: torch.Tensor, k: KV4, v: KV4, out=None, workspace=None, stream=None) -> torch.Tensor:
+KV4_TOKEN_MAJOR, KV4_HEAD_MAJOR = 0, 1
+
+
+def kv4_attention_decode(q: torch.Tensor, k: KV4, v: KV4, out=None, workspace=None, head_major=False,
+                         stream=None) -> torch.Tensor:
     """One decode step of grouped-query attention: q fp16 [B, Hq, 128] over the KV4 cache k, v of
-    groups [B, T, Hkv]; returns fp16 [B, Hq, 128]."""
+    groups [B, T, Hkv] (token-major) or, head_major, [B, Hkv, T]; returns fp16 [B, Hq, 128]."""
     B, Hq, d = q.shape
     _dev(q, torch.float16, (B, Hq, 128), "q")
-    T, Hkv = k.codes.shape[1], k.codes.shape[2]
+    if head_major:
+        Hkv, T = k.codes.shape[1], k.codes.shape[2]
+        rows = (B, Hkv, T)
+    else:
+        T, Hkv = k.codes.shape[1], k.codes.shape[2]
+        rows = (B, T, Hkv)
     for name, c in (("k", k), ("v", v)):
-        _dev(c.codes, torch.uint8, (B, T, Hkv, 64), name + ".codes")
-        _dev(c.scales, torch.float32, (B, T, Hkv), name + ".scales")
-        _dev(c.zeros, torch.uint8, (B, T, Hkv), name + ".zeros")
+        _dev(c.codes, torch.uint8, rows + (64,), name + ".codes")
+        _dev(c.scales, torch.float32, rows, name + ".scales")
+        _dev(c.zeros, torch.uint8, rows, name + ".zeros")
     if out is None:
         out = torch.empty((B, Hq, 128), dtype=torch.float16, device=q.device)
     _dev(out, torch.float16, (B, Hq, 128), "out")
     need = int(lib().qift_kv4_attention_workspace_bytes(B, Hq, Hkv, 128, T))
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
-    st = lib().qift_kv4_attention_decode(q.data_ptr(), B, Hq, Hkv, 128, T, k.codes.data_ptr(), k.scales.data_ptr(),
+    st = lib().qift_kv4_attention_decode(q.data_ptr(), B, Hq, Hkv, 128, T,
+                                         KV4_HEAD_MAJOR if head_major else KV4_TOKEN_MAJOR,
+                                         k.codes.data_ptr(), k.scales.data_ptr(),
                                          k.zeros.data_ptr(), v.codes.data_ptr(), v.scales.data_ptr(),
                                          v.zeros.data_ptr(), out.data_ptr(), workspace.data_ptr(),
                                          workspace.numel() * workspace.element_size(), _stream(stream))

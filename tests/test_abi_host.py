@@ -91,12 +91,15 @@ def test_kv4_validation(L):
     assert ws(1, 24, 8, 128, 1000) == 0                       # Hq / Hkv = 3
     f = L.qift_kv4_attention_decode
     good = ws(1, 32, 8, 128, 1000)
-    assert f(A, 1, 32, 8, 128, 1000, A, A, A, A, A, None, A, A, good, None) == E_NULL
-    assert f(A, 1, 32, 8, 128, 0, A, A, A, A, A, A, A, A, good, None) == E_SHAPE
-    assert f(A, 1, 32, 6, 128, 1000, A, A, A, A, A, A, A, A, good, None) == E_SHAPE
-    assert f(A, 1, 32, 8, 128, 1000, A, A, A, A, A, A, A, A, good - 4, None) == E_WS
-    assert f(A, 1, 32, 8, 128, 1000, A, A, A, A, A, A, A, None, good, None) == E_WS
-    assert f(A, 1, 32, 8, 128, 1000, A, A, MIS, A, A, A, A, A, good, None) == E_ALIGN
+    for lay in (0, 1):                                        # token-major, head-major
+        assert f(A, 1, 32, 8, 128, 1000, lay, A, A, A, A, A, None, A, A, good, None) == E_NULL
+        assert f(A, 1, 32, 8, 128, 0, lay, A, A, A, A, A, A, A, A, good, None) == E_SHAPE
+        assert f(A, 1, 32, 6, 128, 1000, lay, A, A, A, A, A, A, A, A, good, None) == E_SHAPE
+        assert f(A, 1, 32, 8, 128, 1000, lay, A, A, A, A, A, A, A, A, good - 4, None) == E_WS
+        assert f(A, 1, 32, 8, 128, 1000, lay, A, A, A, A, A, A, A, None, good, None) == E_WS
+        assert f(A, 1, 32, 8, 128, 1000, lay, A, A, MIS, A, A, A, A, A, good, None) == E_ALIGN
+    assert f(A, 1, 32, 8, 128, 1000, 2, A, A, A, A, A, A, A, A, good, None) == E_SPEC
+    assert f(A, 1, 32, 8, 128, 1000, -1, A, A, A, A, A, A, A, A, good, None) == E_SPEC
 
 
 def test_rotate_quant_act_validation(L):
