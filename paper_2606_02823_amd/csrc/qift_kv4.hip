@@ -11,11 +11,11 @@
 // Codes are packed two per byte, value 2i in the low nibble of byte i: the cache holds 64 bytes
 // of codes, an fp32 scale and a zero-point byte per token and KV head.
 //
-// Decode attention (k_kv4_attn, k_kv4_merge): for query head h and KV head h / G (G = Hq / Hkv),
+// Decode attention (k_kv4_attn, then k_kv4_merge_serial or k_kv4_merge): for query head h and KV head h / G (G = Hq / Hkv),
 //   out_h = sum_t softmax_t(q_h . k_t / sqrt(d)) v_t.
 // Workgroup (chunk, kv, b) covers 256 cached tokens for the G query heads of one KV head and
 // writes its unnormalized partial output with the chunk's maximum score and sum of exponentials;
-// k_kv4_merge combines the chunks.  The reconstruction is folded into the sums:
+// the merge kernel combines the chunks.  The reconstruction is folded into the sums:
 //   q . k_t = s_t sum_i (code_{t,i} - z_t) q_i,
 //   sum_t p_t v_t = sum_t (p_t s_t) code_t - sum_t p_t s_t z_t,
 // so both phases run on the f16 MFMA with the codes as exact fp16 operands: the key phase codes x
@@ -328,10 +328,12 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
 }
 
 // out[b][kv G + g][:] = sum_c e^(m_c - M) part_c / sum_c e^(m_c - M) l_c,  M = max_c m_c.
-// Workgroup (kv G + g, b), thread dd: the maximum by a block reduction, then per tile of 128 chunks
-// the chunk weights once into LDS and the sum over the tile (independent, coalesced loads).
+// Up to kMergeSerialMax chunks: workgroup (kv G + g, b), thread dd: the maximum by a block
+// reduction, then per tile of 128 chunks the chunk weights once into LDS and the sum over the tile
+// (independent, coalesced loads).
+constexpr int kMergeSerialMax = 63;
 template <int G>
-__global__ __launch_bounds__(kD) void k_kv4_merge(const float* __restrict__ part, int Hq, int Hkv, int nchunks,
+__global__ __launch_bounds__(kD) void k_kv4_merge_serial(const float* __restrict__ part, int Hq, int Hkv, int nchunks,
                                                   uint16_t* __restrict__ y) {
   __shared__ float red[kD / 64];
   __shared__ float ew[kD], lw[kD];
@@ -367,6 +369,51 @@ __global__ __launch_bounds__(kD) void k_kv4_merge(const float* __restrict__ part
   y[(b * Hq + (int64_t)kv * G + g) * kD + dd] = __half_as_ushort(__float2half_rn(acc / L));
 }
 
+// The same for more chunks: workgroup (kv G + g, b) of S x 128 threads (S = blockDim.x / 128 <=
+// kMergeSlices slices, about 8 chunks each): the maximum by a block reduction, then slice j sums
+// chunks j, j + S, ... (thread dd of the slice: output dimension dd), and the slices' sums are
+// added through LDS.
+constexpr int kMergeSlices = 8;
+template <int G>
+__global__ __launch_bounds__(kMergeSlices * kD) void k_kv4_merge(const float* __restrict__ part, int Hq, int Hkv,
+                                                                 int nchunks, uint16_t* __restrict__ y) {
+  __shared__ float red[kMergeSlices * kD / 64];
+  __shared__ float sacc[kMergeSlices][kD];
+  __shared__ float sl[kMergeSlices];
+  const int nthreads = blockDim.x, S = nthreads / kD;
+  const int tid = threadIdx.x, dd = tid % kD, slice = tid / kD, lane = tid & 63, wave = tid >> 6;
+  const int kv = blockIdx.x / G, g = blockIdx.x % G;
+  const int64_t b = blockIdx.y;
+  const float* base = part + (((int64_t)b * Hkv + kv) * nchunks) * G * kPart + g * kPart;
+  const int64_t cstride = (int64_t)G * kPart;
+  float M = -INFINITY;
+  for (int c = tid; c < nchunks; c += nthreads) M = fmaxf(M, base[c * cstride + kD]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  if (lane == 0) red[wave] = M;
+  __syncthreads();
+  for (int w = 0; w < nthreads / 64; ++w) M = fmaxf(M, red[w]);
+  float acc = 0.f, L = 0.f;
+#pragma unroll 4
+  for (int c = slice; c < nchunks; c += S) {
+    const float* r = base + c * cstride;
+    const float e = expf(r[kD] - M);
+    acc = fmaf(r[dd], e, acc);
+    L = fmaf(r[kD + 1], e, L);
+  }
+  sacc[slice][dd] = acc;
+  if (dd == 0) sl[slice] = L;
+  __syncthreads();
+  if (tid < kD) {
+    float a = 0.f, l = 0.f;
+    for (int j = 0; j < S; ++j) {
+      a += sacc[j][tid];
+      l += sl[j];
+    }
+    y[(b * Hq + (int64_t)kv * G + g) * kD + tid] = __half_as_ushort(__float2half_rn(a / l));
+  }
+}
+
 template <int G>
 hipError_t launch_attn_g(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t T, const uint8_t* kc,
                          const float* ks, const uint8_t* kz, const uint8_t* vc, const float* vs,
@@ -376,8 +423,14 @@ hipError_t launch_attn_g(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t 
                      Hkv, T, kc, ks, kz, vc, vs, vz, part, nchunks, head_major);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_kv4_merge<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(kD), 0, s, part, Hq, Hkv, nchunks,
-                     y);
+  if (nchunks <= kMergeSerialMax) {
+    hipLaunchKernelGGL((k_kv4_merge_serial<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(kD), 0, s, part, Hq,
+                       Hkv, nchunks, y);
+  } else {
+    const int slices = nchunks / 8 > kMergeSlices ? kMergeSlices : nchunks / 8;
+    hipLaunchKernelGGL((k_kv4_merge<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(slices * kD), 0, s, part, Hq,
+                       Hkv, nchunks, y);
+  }
   return hipGetLastError();
 }
 
