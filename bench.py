@@ -52,10 +52,15 @@ def _stage(name: str) -> None:
     print(f"[bench] {name}", file=sys.stderr, flush=True)
 
 
+# the files the MNZ decode kernel is compiled and launched from
+DECODE_SOURCES = ("qift_api.hip", "qift_fused.h", "qift_fused_mnz.hip", "qift_fwht.h", "qift_internal.h", "qift_mma.h")
+
+
 def _sources_hash() -> str:
+    """Digest of the decode kernel's sources: a committed traffic record is used only while it matches."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_02823_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in DECODE_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
