@@ -198,6 +198,21 @@ int qift_rotate_quant_act(const uint16_t *x, int64_t M, qift_hadamard_spec spec,
                           qift_stream_t stream);
 
 /*
+ * qift_rotate_quant_act for bf16 activations (x: bf16 bits [M][spec.K]), for
+ * callers whose models run in bf16 (the paper's full-precision reference is
+ * fp16); same arguments, errors and results.
+ * Each bf16 value is widened exactly; the rotation and the rounding decisions
+ * are exact, as for fp16, when every value of a token lies on the fp16 grid:
+ * zero, or a magnitude in [2^-17, 2^16) (a bf16 has 8 significant bits, so
+ * such a value is a multiple of 2^-24).  Values outside that range are
+ * outside the contract (the codes may then differ from the exact rounding at
+ * near-ties).
+ */
+int qift_rotate_quant_act_bf16(const uint16_t *x, int64_t M, qift_hadamard_spec spec,
+                               int8_t *act_q, float *act_scale, int32_t *act_sum,
+                               qift_stream_t stream);
+
+/*
  * Quantized linear with 2-bit weights (Sec. 1; Sec. 3.6):
  *   acc[m][n] = sum_k level[n][k] * act_q[m][k]   exact int32
  *   y[m][n]   = fp16( fp32( fp32(acc) * act_scale[m] ) * fp32(s_w[n]) )

@@ -42,14 +42,16 @@ def hadamard(b: int) -> np.ndarray:
 def rotate_act_units(x: np.ndarray, b: int) -> np.ndarray:
     """Exact ``X = (I (x) H_b) x`` per token, in integer units of 2^-24.
 
-    ``x`` is fp16 [M, K].  Each fp16 value times 2^24 is an integer of
-    magnitude below 2^40, so every partial sum of at most 2^13 of them stays
-    below 2^53 and the fp64 product below is exact in any summation order.
-    Returns int64 [M, K].
+    ``x`` is fp16 [M, K], or any float array whose values lie on the same grid
+    (multiples of 2^-24 of magnitude below 2^16: every fp16, and every bf16 of
+    magnitude in [2^-17, 2^16) or zero, bf16 having 8 significant bits).  Each
+    value times 2^24 is then an integer of magnitude below 2^40, so every
+    partial sum of at most 2^13 of them stays below 2^53 and the fp64 product
+    below is exact in any summation order.  Returns int64 [M, K].
     """
     x = np.asarray(x)
-    if x.dtype != np.float16:
-        raise TypeError("activations must be fp16")
+    if x.dtype.kind != "f":
+        raise TypeError("activations must be floating point")
     M, K = x.shape
     check_block(K, b)
     if b > 8192:
@@ -57,6 +59,8 @@ def rotate_act_units(x: np.ndarray, b: int) -> np.ndarray:
     xu = x.astype(np.float64) * 2.0 ** 24
     if not np.all(np.isfinite(xu)):
         raise ValueError("non-finite activation")
+    if x.dtype != np.float16 and not (np.all(xu == np.round(xu)) and np.all(np.abs(xu) < 2.0 ** 40)):
+        raise ValueError("activation off the 2^-24 grid or not below 2^16 in magnitude")
     H = hadamard(b).astype(np.float64)
     X = (xu.reshape(M, K // b, b) @ H).reshape(M, K)   # H symmetric: x_blk @ H == H @ x_blk
     Xi = X.astype(np.int64)

@@ -25,7 +25,7 @@
 namespace qift {
 namespace {
 
-template <int NT, int NTILES>
+template <int NT, int NTILES, bool BF16>
 __global__ __launch_bounds__(NT) void k_rotate_quant_act(const uint16_t* __restrict__ x, int64_t K, int L,
                                                          int num, int den, double denom,
                                                          int8_t* __restrict__ act_q,
@@ -38,7 +38,7 @@ __global__ __launch_bounds__(NT) void k_rotate_quant_act(const uint16_t* __restr
   const int64_t m = blockIdx.x;
   int sum_q;
   float scale;
-  dev::quant_token<NT, NTILES>(x + m * K, K, L, num, den, denom, lds, red_d, red_i, act_q + m * K,
+  dev::quant_token<NT, NTILES, BF16>(x + m * K, K, L, num, den, denom, lds, red_d, red_i, act_q + m * K,
                                    sum_q, scale);
   if (threadIdx.x == 0) {
     act_sum[m] = sum_q;
@@ -46,7 +46,7 @@ __global__ __launch_bounds__(NT) void k_rotate_quant_act(const uint16_t* __restr
   }
 }
 
-template <int NTILES, int LC>
+template <int NTILES, int LC, bool BF16>
 __global__ __launch_bounds__(256) void k_act_tokens(const uint16_t* __restrict__ x, int M, int64_t K, int L,
                                                     int num, int den, double denom, int8_t* __restrict__ act_q,
                                                     float* __restrict__ act_scale, int32_t* __restrict__ act_sum) {
@@ -68,8 +68,8 @@ __global__ __launch_bounds__(256) void k_act_tokens(const uint16_t* __restrict__
     if (kPrefetch && m + (int)gridDim.x < M)
       dev::load_token_raw<256, NTILES>(raw, x + (int64_t)(m + gridDim.x) * K, K);
     __syncthreads();   // the previous token's codes have been copied out and its partial sums read
-    const double A = dev::quant_token_group<NTILES, LC, false>(cur, K, L, num, den, xch, xch, red_d, red_i, sync,
-                                                              codes);
+    const double A = dev::quant_token_group<NTILES, LC, false, dev::BlockSync, BF16>(cur, K, L, num, den, xch, xch,
+                                                                                   red_d, red_i, sync, codes);
     __syncthreads();   // codes and partial sums are in LDS
 #pragma unroll
     for (int tau = 0; tau < NTILES; ++tau) {
@@ -85,13 +85,13 @@ __global__ __launch_bounds__(256) void k_act_tokens(const uint16_t* __restrict__
   }
 }
 
-template <int NTILES, int LC>
+template <int NTILES, int LC, bool BF16>
 hipError_t launch_tokens_l(const uint16_t* x, int64_t M, int64_t K, int L, int num, int den, double denom,
                            int8_t* q, float* sc, int32_t* sum, hipStream_t s) {
   // persistent grid: every workgroup that fits on the chip at once (queried once per instance)
   static const int resident = [] {
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&k_act_tokens<NTILES, LC>),
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&k_act_tokens<NTILES, LC, BF16>),
                                                      256, 0) != hipSuccess || per_cu < 1)
       per_cu = 1;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -100,35 +100,35 @@ hipError_t launch_tokens_l(const uint16_t* x, int64_t M, int64_t K, int L, int n
     return per_cu * cus;
   }();
   const unsigned grid = (unsigned)(M < resident ? M : resident);
-  hipLaunchKernelGGL((k_act_tokens<NTILES, LC>), dim3(grid), dim3(256), 0, s, x, (int)M, K, L, num, den, denom, q,
+  hipLaunchKernelGGL((k_act_tokens<NTILES, LC, BF16>), dim3(grid), dim3(256), 0, s, x, (int)M, K, L, num, den, denom, q,
                      sc, sum);
   return hipGetLastError();
 }
 
 // block exponents compiled as constants: 12, 11, 8 and 6; anything else at run time
-template <int NTILES>
+template <int NTILES, bool BF16>
 hipError_t launch_tokens(const uint16_t* x, int64_t M, int64_t K, int L, int num, int den, double denom,
                          int8_t* q, float* sc, int32_t* sum, hipStream_t s) {
   switch (L) {
-    case 12: return launch_tokens_l<NTILES, 12>(x, M, K, L, num, den, denom, q, sc, sum, s);
-    case 11: return launch_tokens_l<NTILES, 11>(x, M, K, L, num, den, denom, q, sc, sum, s);
-    case 8: return launch_tokens_l<NTILES, 8>(x, M, K, L, num, den, denom, q, sc, sum, s);
-    case 6: return launch_tokens_l<NTILES, 6>(x, M, K, L, num, den, denom, q, sc, sum, s);
-    default: return launch_tokens_l<NTILES, 0>(x, M, K, L, num, den, denom, q, sc, sum, s);
+    case 12: return launch_tokens_l<NTILES, 12, BF16>(x, M, K, L, num, den, denom, q, sc, sum, s);
+    case 11: return launch_tokens_l<NTILES, 11, BF16>(x, M, K, L, num, den, denom, q, sc, sum, s);
+    case 8: return launch_tokens_l<NTILES, 8, BF16>(x, M, K, L, num, den, denom, q, sc, sum, s);
+    case 6: return launch_tokens_l<NTILES, 6, BF16>(x, M, K, L, num, den, denom, q, sc, sum, s);
+    default: return launch_tokens_l<NTILES, 0, BF16>(x, M, K, L, num, den, denom, q, sc, sum, s);
   }
 }
 
-template <int NT>
+template <int NT, bool BF16>
 hipError_t launch_nt(const uint16_t* x, int64_t M, int64_t K, int L, int num, int den, double denom,
                      int8_t* q, float* sc, int32_t* sum, hipStream_t s) {
   const int64_t T = 16 * NT;
   const int nt = (int)((K + T - 1) / T);
   const dim3 grid((unsigned)M), block(NT);
   switch (nt) {
-    case 1: hipLaunchKernelGGL((k_rotate_quant_act<NT, 1>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
-    case 2: hipLaunchKernelGGL((k_rotate_quant_act<NT, 2>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
-    case 3: hipLaunchKernelGGL((k_rotate_quant_act<NT, 3>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
-    case 4: hipLaunchKernelGGL((k_rotate_quant_act<NT, 4>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
+    case 1: hipLaunchKernelGGL((k_rotate_quant_act<NT, 1, BF16>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
+    case 2: hipLaunchKernelGGL((k_rotate_quant_act<NT, 2, BF16>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
+    case 3: hipLaunchKernelGGL((k_rotate_quant_act<NT, 3, BF16>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
+    case 4: hipLaunchKernelGGL((k_rotate_quant_act<NT, 4, BF16>), grid, block, 0, s, x, K, L, num, den, denom, q, sc, sum); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -141,20 +141,27 @@ double act_denominator(int block, int clip_den) {
   return ((double)clip_den * 7.0) * sqrt((double)block);
 }
 
-hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num,
-                                   int clip_den, int8_t* act_q, float* act_scale, int32_t* act_sum,
-                                   hipStream_t s) {
+template <bool BF16>
+hipError_t launch_rqa(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num, int clip_den, int8_t* act_q,
+                      float* act_scale, int32_t* act_sum, hipStream_t s) {
   const int L = dev::ilog2c(block);
   const double denom = act_denominator(block, clip_den);
   if (block <= 4096 && K <= 4 * 4096) {
     switch ((K + 4095) / 4096) {
-      case 1: return launch_tokens<1>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
-      case 2: return launch_tokens<2>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
-      case 3: return launch_tokens<3>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
-      default: return launch_tokens<4>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
+      case 1: return launch_tokens<1, BF16>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
+      case 2: return launch_tokens<2, BF16>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
+      case 3: return launch_tokens<3, BF16>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
+      default: return launch_tokens<4, BF16>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
     }
   }
-  return launch_nt<512>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
+  return launch_nt<512, BF16>(x, M, K, L, clip_num, clip_den, denom, act_q, act_scale, act_sum, s);
+}
+
+hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num,
+                                   int clip_den, int8_t* act_q, float* act_scale, int32_t* act_sum,
+                                   hipStream_t s, bool bf16) {
+  return bf16 ? launch_rqa<true>(x, M, K, block, clip_num, clip_den, act_q, act_scale, act_sum, s)
+              : launch_rqa<false>(x, M, K, block, clip_num, clip_den, act_q, act_scale, act_sum, s);
 }
 
 }  // namespace qift

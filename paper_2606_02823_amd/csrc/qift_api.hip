@@ -145,8 +145,9 @@ int qift_kv4_attention_decode(const uint16_t* q, int64_t B, int32_t Hq, int32_t 
                                                v_zeros, out, workspace, (hipStream_t)stream));
 }
 
-int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,
-                          float* act_scale, int32_t* act_sum, qift_stream_t stream) {
+namespace {
+int rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q, float* act_scale,
+                     int32_t* act_sum, qift_stream_t stream, bool bf16) {
   if (!x || !act_q || !act_scale || !act_sum) return QIFT_ERR_NULL;
   if (M < 1 || M >= (int64_t(1) << 31) || spec.K < 64 || spec.K % 64 || spec.K > qift::kActMaxK)
     return QIFT_ERR_SHAPE;
@@ -156,7 +157,18 @@ int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec,
   if (!aligned16(x) || !aligned16(act_q) || !aligned16(act_scale) || !aligned16(act_sum))
     return QIFT_ERR_ALIGN;
   return hip_status(qift::launch_rotate_quant_act(x, M, spec.K, b, spec.clip_num, spec.clip_den, act_q,
-                                                  act_scale, act_sum, (hipStream_t)stream));
+                                                  act_scale, act_sum, (hipStream_t)stream, bf16));
+}
+}  // namespace
+
+int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,
+                          float* act_scale, int32_t* act_sum, qift_stream_t stream) {
+  return rotate_quant_act(x, M, spec, act_q, act_scale, act_sum, stream, false);
+}
+
+int qift_rotate_quant_act_bf16(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,
+                               float* act_scale, int32_t* act_sum, qift_stream_t stream) {
+  return rotate_quant_act(x, M, spec, act_q, act_scale, act_sum, stream, true);
 }
 
 int qift_w2a4_linear(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,

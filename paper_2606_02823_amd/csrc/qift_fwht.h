@@ -372,11 +372,27 @@ __device__ __forceinline__ void unpack_fp16(double (&v)[16], const uint4 (&d)[2]
   }
 }
 
+// bf16 bits are the upper half of the fp32 value: exact in fp32, then in fp64
+__device__ __forceinline__ void unpack_bf16(double (&v)[16], const uint4 (&d)[2]) {
+  const uint32_t w[8] = {d[0].x, d[0].y, d[0].z, d[0].w, d[1].x, d[1].y, d[1].z, d[1].w};
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const uint32_t bits = (e & 1) ? (w[e >> 1] & 0xFFFF0000u) : (w[e >> 1] << 16);
+    v[e] = (double)__uint_as_float(bits);
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ void unpack16(double (&v)[16], const uint4 (&d)[2]) {
+  if constexpr (BF16) unpack_bf16(v, d);
+  else unpack_fp16(v, d);
+}
+
 // Rotate + quantize one token of K <= NTILES * T elements from its raw bits.
 // Writes the int8 codes (16 per thread per tile, natural order, one 16-byte
 // store) to dst (global or LDS, 16-byte aligned rows) and returns sum_q and
 // the scale.  All NT threads must call it.
-template <int NT, int NTILES>
+template <int NT, int NTILES, bool BF16 = false>
 __device__ __forceinline__ void quant_token_raw(const TokenRaw<NTILES>& raw, int64_t K, int L, int num, int den,
                                                 double denom, double* lds, double* red_d, int* red_i,
                                                 int8_t* dst, int& sum_q, float& scale) {
@@ -386,7 +402,7 @@ __device__ __forceinline__ void quant_token_raw(const TokenRaw<NTILES>& raw, int
   double amax = 0.0;
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
-    unpack_fp16(v[tau], raw.d[tau]);
+    unpack16<BF16>(v[tau], raw.d[tau]);
     fwht_tile<NT, 16, true>(v[tau], lds, t, L);
 #pragma unroll
     for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[tau][e]));
@@ -458,7 +474,7 @@ __device__ __forceinline__ void store_codes(int8_t* dst, const int (&q)[16], int
 // exponent L = LC at compile time (every butterfly stage and exchange is then
 // straight-line code); LC = 0 takes L at run time.  With xch0 == xch1 (one
 // exchange buffer) every tile after the first starts with a sync instead.
-template <int NTILES, int LC, bool PLANAR, typename Sync>
+template <int NTILES, int LC, bool PLANAR, typename Sync, bool BF16 = false>
 __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw, int64_t K, int L_rt, int num,
                                                     int den, double* xch0, double* xch1, double* red_d,
                                                     int* red_i, Sync& sync, int8_t* dst) {
@@ -470,7 +486,7 @@ __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw,
   int wend = 0;
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
-    unpack_fp16(v[tau], raw.d[tau]);
+    unpack16<BF16>(v[tau], raw.d[tau]);
     if (tau > 0 && xch0 == xch1 && L > 6) sync();   // the previous tile's exchange reads are done
     wend = fwht_tile_s<256, 16, false>(v[tau], (tau & 1) ? xch1 : xch0, t, L, sync);
 #pragma unroll
@@ -509,13 +525,13 @@ __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw,
   return A;
 }
 
-template <int NT, int NTILES>
+template <int NT, int NTILES, bool BF16 = false>
 __device__ __forceinline__ void quant_token(const uint16_t* xr, int64_t K, int L, int num, int den,
                                             double denom, double* lds, double* red_d, int* red_i,
                                             int8_t* dst, int& sum_q, float& scale) {
   TokenRaw<NTILES> raw;
   load_token_raw<NT, NTILES>(raw, xr, K);
-  quant_token_raw<NT, NTILES>(raw, K, L, num, den, denom, lds, red_d, red_i, dst, sum_q, scale);
+  quant_token_raw<NT, NTILES, BF16>(raw, K, L, num, den, denom, lds, red_d, red_i, dst, sum_q, scale);
 }
 
 }  // namespace dev

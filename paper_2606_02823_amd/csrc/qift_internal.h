@@ -32,7 +32,7 @@ hipError_t launch_kv4_attention(const uint16_t* q, int64_t B, int Hq, int Hkv, i
 // Rotation + INT4 quantization (qift_act.hip)
 hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num,
                                    int clip_den, int8_t* act_q, float* act_scale, int32_t* act_sum,
-                                   hipStream_t s);
+                                   hipStream_t s, bool bf16 = false);   // x fp16, or bf16 bits
 
 // Quantized linear (qift_linear.hip).  fmt selects the decode.  ws (nullable) holds at least
 // gemm_f4_workspace(M, K) bytes: with it, MNZ weights at M > 64 run the FP4 x FP6 MFMA kernel.

@@ -30,6 +30,7 @@ STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR
 # every symbol declared in include/qift.h
 EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_kv4_quant",
            "qift_kv4_attention_workspace_bytes", "qift_kv4_attention_decode", "qift_rotate_quant_act",
+           "qift_rotate_quant_act_bf16",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w4a4_linear", "qift_w4a4_linear_ex",
            "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
            "qift_last_hip_error", "qift_version")
@@ -76,6 +77,7 @@ def lib():
         "qift_kv4_attention_decode": (ctypes.c_int, [vp, i64, i32, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                                      vp]),
         "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
+        "qift_rotate_quant_act_bf16": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
         "qift_w2a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
         "qift_w4a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
@@ -292,18 +294,20 @@ def kv4_attention_decode(q: torch.Tensor, k: KV4, v: KV4, out=None, workspace=No
 
 
 def rotate_quant_act(x: torch.Tensor, block: int, clip=(1, 1), out: QAct | None = None, stream=None) -> QAct:
-    """Exact block-Hadamard rotation + per-token INT4 quantization of fp16 x [M, K]."""
+    """Exact block-Hadamard rotation + per-token INT4 quantization of fp16 or bf16 x [M, K]."""
     M, K = x.shape
-    _dev(x, torch.float16, (M, K), "x")
+    bf16 = x.dtype == torch.bfloat16
+    _dev(x, torch.bfloat16 if bf16 else torch.float16, (M, K), "x")
     if out is None:
         out = alloc_act(M, K, x.device)
     _dev(out.q, torch.int8, (M, K), "act_q")
     _dev(out.scale, torch.float32, (M,), "act_scale")
     _dev(out.sum, torch.int32, (M,), "act_sum")
     spec = HadamardSpec(K, block, int(clip[0]), int(clip[1]))
-    st = lib().qift_rotate_quant_act(x.data_ptr(), M, spec, out.q.data_ptr(), out.scale.data_ptr(),
-                                     out.sum.data_ptr(), _stream(stream))
-    _check("qift_rotate_quant_act", st)
+    name = "qift_rotate_quant_act_bf16" if bf16 else "qift_rotate_quant_act"
+    st = getattr(lib(), name)(x.data_ptr(), M, spec, out.q.data_ptr(), out.scale.data_ptr(), out.sum.data_ptr(),
+                              _stream(stream))
+    _check(name, st)
     return out
 
 

@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -102,8 +102,9 @@ def test_kv4_validation(L):
     assert f(A, 1, 32, 8, 128, 1000, -1, A, A, A, A, A, A, A, A, good, None) == E_SPEC
 
 
-def test_rotate_quant_act_validation(L):
-    f = L.qift_rotate_quant_act
+@pytest.mark.parametrize("entry", ["qift_rotate_quant_act", "qift_rotate_quant_act_bf16"])
+def test_rotate_quant_act_validation(L, entry):
+    f = getattr(L, entry)
     assert f(None, 4, _spec(), A, A, A, None) == E_NULL
     assert f(A, 4, _spec(), A, A, None, None) == E_NULL
     assert f(A, 0, _spec(), A, A, A, None) == E_SHAPE

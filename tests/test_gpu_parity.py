@@ -234,6 +234,25 @@ def test_rotate_quant_act_clip_ratio(Q, clip):
     check_act(act, x, b, clip)
 
 
+def _bf16_on_grid(rng, M, K, lo, hi):
+    """bf16 activations on the 2^-24 grid (the exact-rotation contract), rows at mixed scales."""
+    x = torch.from_numpy(rng.normal(0, 1, (M, K)) * rng.uniform(lo, hi, (M, 1))).to(torch.bfloat16)
+    x[x.abs() < 2.0 ** -17] = 0
+    return x
+
+
+@pytest.mark.parametrize("M,K,b", [(5, 4096, 4096), (3, 11008, 64), (9, 8192, 128), (2, 32768, 4096),
+                                   (1, 14336, 2048)])
+def test_rotate_quant_act_bf16(Q, M, K, b):
+    """bf16 input (qift_rotate_quant_act_bf16): bit-exact against the oracle on the same values."""
+    rng = np.random.default_rng(M * 7919 + K)
+    x = _bf16_on_grid(rng, M, K, 1e-3, 400.0)
+    x[0, :3] = torch.tensor([2.0 ** -17, 65280.0, -1.5], dtype=torch.bfloat16)
+    for clip in ((1, 1), (9, 10)):
+        act = Q.rotate_quant_act(x.cuda(), b, clip=clip)
+        check_act(act, x.float().numpy(), b, clip)
+
+
 # ----------------------------------------------------------------------------- full-size configs
 
 

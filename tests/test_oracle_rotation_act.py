@@ -150,3 +150,30 @@ def test_act_quant_zero_token():
     assert not q[0].any() and s_x[0] == 0 and sq[0] == 0
     # a single spike spreads to +-1 * 1 over its block: every entry hits |q| = 7
     assert np.all(np.abs(q[1, :64]) == 7) and not q[1, 64:].any()
+
+
+def _bf16(a):
+    """Round float32 values to bf16 (nearest even on the upper 16 bits) and return them as float32."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
+    return u.astype(np.uint32).view(np.float32)
+
+
+def test_act_quant_bf16_inputs_on_the_grid():
+    """bf16 activations (a deployment variant; the paper's reference is fp16) on the 2^-24 grid rotate exactly: the
+    results equal the fp16 path's on the same values (every such bf16 is also an fp16), and the
+    rounding decisions stay exact integers; values off the grid are refused."""
+    rng = np.random.default_rng(5)
+    x = _bf16(rng.normal(0, 1, (6, 512)) * rng.uniform(1e-3, 300, (6, 1)))
+    x[np.abs(x) < 2.0 ** -17] = 0.0                       # keep every value on the grid
+    x[0, :4] = [2.0 ** -17, -(2.0 ** -17), 65280.0, -3.0]   # grid ends: bf16 min on the grid, max below 2^16
+    assert np.array_equal(x.astype(np.float16).astype(np.float32), x)   # exact in fp16 as well
+    for clip in ((1, 1), (9, 10)):
+        a = quant.act_quant(x, 128, clip)
+        c = quant.act_quant(x.astype(np.float16), 128, clip)
+        for u, v in zip(a, c):
+            assert np.array_equal(u, v)
+    with pytest.raises(ValueError):
+        quant.act_quant(np.full((1, 128), 2.0 ** -25, dtype=np.float32), 128)   # half a grid step
+    with pytest.raises(ValueError):
+        quant.act_quant(np.full((1, 128), 65536.0, dtype=np.float32), 128)      # 2^16
