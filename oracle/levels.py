@@ -31,8 +31,11 @@ W4 = tuple(range(-7, 8))
 FMT_W2_MNZ = 0
 FMT_W2_POT = 1
 FMT_W4_SYM = 2
+# any four levels read through a table indexed by the 2-bit code (the reference grids of Sec. 3.3,
+# which are not integers): the packed "levels" are the codes themselves
+FMT_W2_LUT = 3
 
-CODE_LEVELS = {FMT_W2_MNZ: MNZ_HALF, FMT_W2_POT: POT}
+CODE_LEVELS = {FMT_W2_MNZ: MNZ_HALF, FMT_W2_POT: POT, FMT_W2_LUT: (0, 1, 2, 3)}
 
 
 def mirror_family(r: float):
