@@ -352,6 +352,57 @@ def decode_per_shape(torch, qift, synth, min_bytes=1 << 30, reps=10):
     return rows
 
 
+# the reference grids of Sec. 3.3: Lloyd-Max (Eq. (9)) and NF2 (Eq. (10))
+LLOYD_GRID = (-1.5104, -0.4528, 0.4528, 1.5104)
+NF2_GRID = (-1.0, -0.2525685, 0.2525685, 1.0)
+
+
+def lut_decode(torch, qift, synth, min_bytes=1 << 29, reps=10):
+    """The level-table linear (W2_LUT: the Lloyd-Max and NF2 reference grids) at the cfg1 decode
+    shapes, M = 1 on precomputed activation codes, looped over >= min_bytes of distinct code
+    replicas; the integer MNZ linear on the same replicas beside it."""
+    c = synth.CONFIGS[1]
+    sh = {s.name: s for s in c.linears}
+    plan = [("q,k,v", 3 * sh["q"].N, sh["q"].K, sh["q"].block, 0), ("o", sh["o"].N, sh["o"].K, sh["o"].block, 1),
+            ("gate,up", 2 * sh["gate"].N, sh["gate"].K, sh["gate"].block, 2),
+            ("down", sh["down"].N, sh["down"].K, sh["down"].block, 3)]
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(11)
+    rows = []
+    for name, N, K, b, site in plan:
+        codes = torch.randint(0, 4, (N, K), dtype=torch.int8, device=dev, generator=gen)
+        sc = torch.from_numpy(synth.draw_scales(qift.W2_MNZ, N, cfg=1, layer=0, slot=site)).to(dev)
+        base = qift.pack_w2(codes, sc, qift.W2_LUT, check=False)
+        del codes
+        R = -(-min_bytes // base.nbytes)
+        reps_w = [qift.Packed(qift.W2_LUT, N, K, base.words.clone(), sc) for _ in range(R)]
+        reps_i = [qift.Packed(qift.W2_MNZ, N, K, w.words, sc) for w in reps_w]
+        x = torch.from_numpy(synth.config_activations(c, 0, site, 1, K)).to(dev)
+        act = qift.rotate_quant_act(x, b)
+        y = torch.empty((1, N), dtype=torch.float16, device=dev)
+        total = R * base.nbytes
+        row = {"linear": name, "N": N, "K": K, "packed_bytes": base.nbytes, "replicas": R}
+        for gname, grid in (("lloyd", LLOYD_GRID), ("nf2", NF2_GRID)):
+            def run(grid=grid):
+                for w in reps_w:
+                    qift.w2a4_lut_linear(w, grid, act, out=y)
+            t = _time_graph(torch, run, reps)
+            row[gname + "_us"] = round(t / R * 1e6, 2)
+            row[gname + "_GBs"] = round(total / t / 1e9, 1)
+
+        def mnz():
+            for w in reps_i:
+                qift.w2a4_linear(w, act, out=y)
+        t = _time_graph(torch, mnz, reps)
+        row["mnz_integer_us"] = round(t / R * 1e6, 2)
+        rows.append(row)
+        del reps_w, reps_i, base
+        torch.cuda.empty_cache()
+    return {"workload": "LLaMA-2-7B-shaped decode linears (cfg1), M = 1, activation codes precomputed; "
+                        "random 2-bit codes (the kernel's work does not depend on them)", "rows": rows}
+
+
 FP64_VECTOR_PEAK_TFLOPS = 78.6
 POT_FLOPS_PER_WEIGHT = 64 * 5   # per candidate: w / s, compare, s * level, w - s * level, d * d + acc
 
@@ -510,6 +561,7 @@ def main():
                     help="skip the per-shape replica loops and the read probe")
     ap.add_argument("--no-wquant", action="store_true", help="skip the weight quantizer timing")
     ap.add_argument("--no-kv4", action="store_true", help="skip the KV4 attention timing")
+    ap.add_argument("--no-lut", action="store_true", help="skip the level-table linear timing")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the cfg2 (M 1/4/16) and cfg3 PoT (M 1/8/64) stack sweep")
     ap.add_argument("--copy-probe", action="store_true",
@@ -621,6 +673,11 @@ def main():
     if not args.no_kv4:
         _stage("KV4 attention")
         out["kv4_attention"] = kv4_attention(torch, qift)
+        torch.cuda.empty_cache()
+
+    if not args.no_lut:
+        _stage("level-table linear")
+        out["lut_decode"] = lut_decode(torch, qift, synth)
         torch.cuda.empty_cache()
 
     # ---------------------------------------------------------------- prefill

@@ -20,6 +20,10 @@
  *   QIFT_W4_SYM  symmetric 4-bit integers -7..7 (Eq. (1) with b = 4, used on
  *                the symmetric range); the sibling format of the L-layer
  *                W2/W4 schedule (Sec. 4.4).
+ *   QIFT_W2_LUT  any four levels given as an fp16 table indexed by the 2-bit
+ *                code, for the non-integer reference grids of Sec. 3.3
+ *                (Lloyd-Max Eq. (9), NF2 Eq. (10)); only qift_pack_w2 (with
+ *                the codes 0..3 as "levels") and qift_w2a4_lut_linear take it.
  *
  * Conventions shared by every call:
  *   - fp16 values travel as uint16_t bit patterns (IEEE binary16).
@@ -66,7 +70,7 @@ enum {
 };
 
 /* ---- level-set formats and packed layouts ----------------------------- */
-enum { QIFT_W2_MNZ = 0, QIFT_W2_POT = 1, QIFT_W4_SYM = 2 };
+enum { QIFT_W2_MNZ = 0, QIFT_W2_POT = 1, QIFT_W4_SYM = 2, QIFT_W2_LUT = 3 };
 
 /*
  * QIFT_LAYOUT_V1 word layouts (uint32 words, little-endian, row-major):
@@ -123,7 +127,8 @@ size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K);
  *                 (PoT).  Passing levels rather than codes keeps this
  *                 boundary independent of the code assignment.
  *   scales        fp16 s_w[N]; not read, recorded in *out.
- *   fmt           QIFT_W2_MNZ or QIFT_W2_POT.
+ *   fmt           QIFT_W2_MNZ or QIFT_W2_POT; or QIFT_W2_LUT, where the
+ *                 "levels" are the codes 0..3 (table indices) themselves.
  *   packed        out: uint32 [N][K/16].
  *   out           host, out, nullable: filled with the view of the result.
  *   invalid_count device int32, nullable.  When given, the call first sets it
@@ -243,6 +248,28 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
 int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
                         const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
                         void *workspace, size_t workspace_bytes, qift_stream_t stream);
+
+/*
+ * Quantized linear over a four-level fp16 table (fmt QIFT_W2_LUT), for the
+ * non-integer reference grids of Sec. 3.3 (Lloyd-Max, NF2):
+ *   t[m][n] = sum_k lut[code[n][k]] * act_q[m][k]        exact
+ *   y[m][n] = fp16( fp32( fp32(t) * act_scale[m] ) * fp32(s_w[n]) )
+ * i.e. the epilogue of qift_w2a4_linear with t in place of the accumulator.
+ *   w        host: packed code words (qift_pack_w2 with QIFT_W2_LUT).
+ *   lut      host: 4 fp16 bit patterns, the level of codes 0..3; each finite
+ *            with magnitude <= 256 (QIFT_ERR_SPEC otherwise).
+ *   act_q, act_scale, act_sum   as for qift_w2a4_linear.
+ *   out      out: fp16 y [M][N].
+ * t is computed as L0 sum q + (L1 - L0) sum c q + (L2 - 2 L1 + L0) sum b1 q
+ * + (L3 - L2 - L1 + L0) sum b0 b1 q over the code bits c = b0 + 2 b1, with the
+ * three sums on the int8 MFMA: every term is then an exact fp64 multiple of
+ * 2^-24 below 2^53, so the results are bit-exact.
+ * Limits: K a multiple of 256 and at most 16384; M <= 1048560.  One kernel for
+ * all M (workgroups of 16 rows x 16 tokens); no tiled prefill form.
+ */
+int qift_w2a4_lut_linear(const qift_packed_w *w, const uint16_t *lut, const int8_t *act_q,
+                         const float *act_scale, const int32_t *act_sum, int64_t M, uint16_t *out,
+                         qift_stream_t stream);
 
 /* The W4 sibling (fmt QIFT_W4_SYM); same arguments and results. */
 int qift_w4a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,

@@ -20,6 +20,18 @@ inline int hip_status(hipError_t e) {
 }
 
 inline bool is_w2(int32_t fmt) { return fmt == QIFT_W2_MNZ || fmt == QIFT_W2_POT; }
+// 2-bit formats that pack into QW2v1 words (the integer sets and the level-table codes)
+inline bool is_qw2(int32_t fmt) { return is_w2(fmt) || fmt == QIFT_W2_LUT; }
+
+// IEEE binary16 bits -> double, exactly (non-finite values come back as inf / nan)
+double half_bits_to_double(uint16_t h) {
+  const int sign = h >> 15, e = (h >> 10) & 31, f = h & 1023;
+  double v;
+  if (e == 31) v = f ? NAN : INFINITY;
+  else if (e == 0) v = ldexp((double)f, -24);
+  else v = ldexp((double)(1024 + f), e - 25);
+  return sign ? -v : v;
+}
 
 inline bool shape_ok(int64_t N, int64_t K) {
   // K: multiple of 64; sizes kept below 2^31 per dimension (int indexing inside tiles)
@@ -63,7 +75,7 @@ extern "C" {
 
 size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K) {
   if (!shape_ok(N, K)) return 0;
-  if (is_w2(fmt)) return (size_t)(N * (K / 4));
+  if (is_qw2(fmt)) return (size_t)(N * (K / 4));
   if (fmt == QIFT_W4_SYM) return (size_t)(N * (K / 2));
   return 0;
 }
@@ -71,7 +83,7 @@ size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K) {
 int qift_pack_w2(const int8_t* levels, const uint16_t* scales, int64_t N, int64_t K, int32_t fmt,
                  uint32_t* packed, qift_packed_w* out, int32_t* invalid_count, qift_stream_t stream) {
   if (!levels || !packed) return QIFT_ERR_NULL;
-  if (!is_w2(fmt)) return QIFT_ERR_FORMAT;
+  if (!is_qw2(fmt)) return QIFT_ERR_FORMAT;
   if (!shape_ok(N, K)) return QIFT_ERR_SHAPE;
   if (!aligned16(levels) || !aligned16(packed) || (scales && !aligned16(scales)) ||
       (invalid_count && (reinterpret_cast<uintptr_t>(invalid_count) & 3u)))
@@ -164,6 +176,25 @@ int rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8
 int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,
                           float* act_scale, int32_t* act_sum, qift_stream_t stream) {
   return rotate_quant_act(x, M, spec, act_q, act_scale, act_sum, stream, false);
+}
+
+int qift_w2a4_lut_linear(const qift_packed_w* w, const uint16_t* lut, const int8_t* act_q, const float* act_scale,
+                         const int32_t* act_sum, int64_t M, uint16_t* out, qift_stream_t stream) {
+  if (!w || !lut || !act_q || !act_scale || !act_sum || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
+  if (w->layout != QIFT_LAYOUT_V1 || w->fmt != QIFT_W2_LUT) return QIFT_ERR_FORMAT;
+  // K: whole 256-k blocks, and at most 2^14 for the exact fp64 combination; token blocks of 16 in grid.y
+  if (!shape_ok(w->N, w->K) || w->K % 256 || w->K > 16384 || M < 1 || M > 16 * 65535) return QIFT_ERR_SHAPE;
+  if (qift_packed_bytes(w->fmt, w->N, w->K) >= (size_t(1) << 31)) return QIFT_ERR_SHAPE;
+  double L[4];
+  for (int i = 0; i < 4; ++i) {
+    L[i] = half_bits_to_double(lut[i]);
+    if (!(fabs(L[i]) <= 256.0)) return QIFT_ERR_SPEC;   // also rejects inf and nan
+  }
+  if (!aligned16(w->packed) || !aligned16(w->scales) || !aligned16(act_q) || !aligned16(act_scale) ||
+      !aligned16(act_sum) || !aligned16(out))
+    return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_lut_linear(w->packed, w->scales, w->N, w->K, L, act_q, act_scale, act_sum, M, out,
+                                            (hipStream_t)stream));
 }
 
 int qift_rotate_quant_act_bf16(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q,

@@ -29,6 +29,11 @@ hipError_t launch_kv4_attention(const uint16_t* q, int64_t B, int Hq, int Hkv, i
                                 const uint8_t* kc, const float* ks, const uint8_t* kz, const uint8_t* vc,
                                 const float* vs, const uint8_t* vz, uint16_t* y, void* ws, hipStream_t s);
 
+// Linear over a four-level fp16 table (qift_lut.hip): lut holds the table entries exactly
+hipError_t launch_lut_linear(const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K, const double lut[4],
+                             const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
+                             uint16_t* out, hipStream_t s);
+
 // Rotation + INT4 quantization (qift_act.hip)
 hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num,
                                    int clip_den, int8_t* act_q, float* act_scale, int32_t* act_sum,

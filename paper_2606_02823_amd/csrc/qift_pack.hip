@@ -72,9 +72,9 @@ int grid_for(int64_t items) {
 
 hipError_t launch_pack_w2(const int8_t* levels, int64_t N, int64_t K, int fmt, uint32_t* packed,
                           int32_t* invalid_count, hipStream_t s) {
-  // ascending level lists: MNZ at half scale, and PoT-MNZ
-  const int l[2][4] = {{-3, -1, 1, 3}, {-4, -1, 1, 4}};
-  const int* L = l[fmt == 1 ? 1 : 0];
+  // ascending level lists: MNZ at half scale, PoT-MNZ, and the codes themselves (level table)
+  const int l[3][4] = {{-3, -1, 1, 3}, {-4, -1, 1, 4}, {0, 1, 2, 3}};
+  const int* L = l[fmt == 1 ? 1 : fmt == 3 ? 2 : 0];
   const int64_t words = N * (K / 16);
   if (invalid_count) hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(1), 0, s, invalid_count);
   hipLaunchKernelGGL(k_pack_w2, dim3(grid_for(words)), dim3(256), 0, s, levels, words, packed,

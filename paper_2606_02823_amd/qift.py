@@ -19,7 +19,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libqift.so")
 
-W2_MNZ, W2_POT, W4_SYM = 0, 1, 2
+W2_MNZ, W2_POT, W4_SYM, W2_LUT = 0, 1, 2, 3
 FUSED_MAX_M = 4   # tokens per call of the fused rotate_quant_linear entry (limits in qift.h)
 LAYOUT_V1 = 1
 
@@ -31,7 +31,7 @@ STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR
 EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_kv4_quant",
            "qift_kv4_attention_workspace_bytes", "qift_kv4_attention_decode", "qift_rotate_quant_act",
            "qift_rotate_quant_act_bf16",
-           "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w4a4_linear", "qift_w4a4_linear_ex",
+           "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w2a4_lut_linear", "qift_w4a4_linear", "qift_w4a4_linear_ex",
            "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
            "qift_last_hip_error", "qift_version")
 
@@ -79,6 +79,7 @@ def lib():
         "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_rotate_quant_act_bf16": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
+        "qift_w2a4_lut_linear": (ctypes.c_int, [pw, vp, vp, vp, vp, i64, vp, vp]),
         "qift_w2a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
         "qift_w4a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
         "qift_w4a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
@@ -153,7 +154,8 @@ def workspace_bytes(w: Packed, M: int) -> int:
 
 def pack_w2(levels: torch.Tensor, scales: torch.Tensor, fmt: int = W2_MNZ, out: torch.Tensor | None = None,
             invalid_count: torch.Tensor | None = None, check: bool = True, stream=None) -> Packed:
-    """Pack int8 levels [N, K] ({-3,-1,1,3} MNZ or {-4,-1,1,4} PoT) into QW2v1 words.
+    """Pack int8 levels [N, K] ({-3,-1,1,3} MNZ or {-4,-1,1,4} PoT; for W2_LUT the codes 0..3) into
+    QW2v1 words.
 
     With ``check`` (default) a device counter of out-of-set levels is read back
     after the stream completes and a ValueError is raised when it is non-zero.
@@ -341,6 +343,28 @@ def _linear(name: str, w: Packed, act: QAct, out, acc_out, workspace, stream):
 def w2a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:
     """fp16 y [M, N] of the 2-bit quantized linear (MNZ or PoT weights)."""
     return _linear("qift_w2a4_linear", w, act, out, acc_out, workspace, stream)
+
+
+def w2a4_lut_linear(w: Packed, lut, act: QAct, out=None, stream=None) -> torch.Tensor:
+    """fp16 y [M, N] of the linear over a four-level table (W2_LUT code words); ``lut`` is the four
+    levels (any sequence of numbers, rounded once to fp16, or an fp16 tensor)."""
+    M, K = act.q.shape
+    if K != w.K:
+        raise ValueError(f"activation width {K} != weight K {w.K}")
+    _dev(act.scale, torch.float32, (M,), "act_scale")
+    _dev(act.sum, torch.int32, (M,), "act_sum")
+    if out is None:
+        out = torch.empty((M, w.N), dtype=torch.float16, device=act.q.device)
+    _dev(out, torch.float16, (M, w.N), "out")
+    bits = torch.as_tensor(lut, dtype=torch.float64).to(torch.float16).cpu().contiguous().view(torch.int16)
+    if bits.shape != (4,):
+        raise ValueError("lut must hold four levels")
+    table = (ctypes.c_uint16 * 4)(*[int(b) & 0xFFFF for b in bits.tolist()])
+    v = w.cview()
+    st = lib().qift_w2a4_lut_linear(ctypes.byref(v), table, act.q.data_ptr(), act.scale.data_ptr(),
+                                    act.sum.data_ptr(), M, out.data_ptr(), _stream(stream))
+    _check("qift_w2a4_lut_linear", st)
+    return out
 
 
 def w4a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:

@@ -7,6 +7,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 from paper_2606_02823_amd import qift
@@ -34,7 +35,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 20
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -199,3 +200,25 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(qift, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         qift.lib()
+
+
+def test_lut_linear_validation(L):
+    f = L.qift_w2a4_lut_linear
+    P = ctypes.byref
+    half = lambda *v: (ctypes.c_uint16 * 4)(*[int(np.float16(x).view(np.uint16)) for x in v])
+    good = half(-1.5104, -0.4528, 0.4528, 1.5104)
+    lw = lambda **kw: _pw(fmt=qift.W2_LUT, K=kw.pop("K", 4096), **kw)
+    assert L.qift_packed_bytes(qift.W2_LUT, 8, 4096) == 8 * 1024
+    assert f(None, good, A, A, A, 4, A, None) == E_NULL
+    assert f(P(lw()), None, A, A, A, 4, A, None) == E_NULL
+    assert f(P(lw()), good, A, A, None, 4, A, None) == E_NULL
+    assert f(P(_pw(fmt=qift.W2_MNZ, K=4096)), good, A, A, A, 4, A, None) == E_FORMAT   # integer formats: no table
+    assert f(P(lw(K=4160)), good, A, A, A, 4, A, None) == E_SHAPE                     # K not a multiple of 256
+    assert f(P(lw(K=16640)), good, A, A, A, 4, A, None) == E_SHAPE                    # K above 16384
+    assert f(P(lw()), good, A, A, A, 0, A, None) == E_SHAPE
+    assert f(P(lw()), half(0, 1, 2, 257), A, A, A, 4, A, None) == E_SPEC             # above 256
+    assert f(P(lw()), half(0, 1, 2, np.inf), A, A, A, 4, A, None) == E_SPEC
+    assert f(P(lw()), half(0, 1, np.nan, 2), A, A, A, 4, A, None) == E_SPEC
+    assert f(P(lw()), good, A, A, A, 4, MIS, None) == E_ALIGN
+    # the integer linears refuse the table format
+    assert L.qift_w2a4_linear(P(lw()), A, A, A, 4, A, None) == E_FORMAT
