@@ -2,8 +2,9 @@
 // Sec. 4.1 configuration: clipping ratio 0.95 for keys and values) and one decode step of
 // grouped-query attention that reads it.
 //
-// Quantizer (k_kv4_quant): one 64-lane wave per group of 128 values (one token's key or value
-// vector of one KV head), lane l holding values 2l and 2l + 1.  In fp32, in this order, rounding
+// Quantizer (k_kv4_quant): 16 lanes per group of 128 values (one token's key or value vector of
+// one KV head), lane j holding values 8j .. 8j + 7 (one 16-byte load, one 4-byte store of their
+// codes), 4 groups per wave and step of a grid-stride loop.  In fp32, in this order, rounding
 // half to even:
 //   x_max = c max(max x, 0), x_min = c min(min x, 0) with c = fp32(0.95),
 //   s = (x_max - x_min) / 15 (1 for a group of zeros), z = round(-x_min / s),
@@ -69,29 +70,44 @@ __device__ __forceinline__ v8h codes_minus_z(uint32_t w, v2h base) {
 __global__ __launch_bounds__(256) void k_kv4_quant(const uint16_t* __restrict__ x, int64_t groups,
                                                    uint8_t* __restrict__ codes, float* __restrict__ scales,
                                                    uint8_t* __restrict__ zeros) {
-  const int lane = threadIdx.x & 63;
-  const int64_t grp = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (grp >= groups) return;   // whole waves leave together; no barrier follows
-  const uint32_t pair = reinterpret_cast<const uint32_t*>(x + grp * kD)[lane];
-  const float a = __half2float(__ushort_as_half((uint16_t)(pair & 0xFFFFu)));
-  const float b = __half2float(__ushort_as_half((uint16_t)(pair >> 16)));
-  float mx = fmaxf(a, b), mn = fminf(a, b);
+  const int lane = threadIdx.x & 63, j = lane & 15;
+  const int64_t quads = (groups + 3) / 4;
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
+  for (int64_t wq = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wq < quads; wq += nwaves) {
+    const int64_t grp = wq * 4 + (lane >> 4);
+    const bool ok = grp < groups;   // lanes of a missing group run along with zeros (the shuffles need them)
+    uint4 u = {0u, 0u, 0u, 0u};
+    if (ok) u = reinterpret_cast<const uint4*>(x + grp * kD)[j];
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    float v[8];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    mx = fmaxf(mx, __shfl_xor(mx, o));
-    mn = fminf(mn, __shfl_xor(mn, o));
-  }
-  const float c = 0.95f;
-  const float x_max = fmaxf(mx, 0.f) * c, x_min = fminf(mn, 0.f) * c;
-  float s = (x_max - x_min) / 15.f;
-  if (s == 0.f) s = 1.f;
-  const float z = fminf(fmaxf(rintf(-x_min / s), 0.f), 15.f);
-  const int qa = (int)fminf(fmaxf(rintf(a / s) + z, 0.f), 15.f);
-  const int qb = (int)fminf(fmaxf(rintf(b / s) + z, 0.f), 15.f);
-  codes[grp * (kD / 2) + lane] = (uint8_t)(qa | (qb << 4));
-  if (lane == 0) {
-    scales[grp] = s;
-    zeros[grp] = (uint8_t)z;
+    for (int e = 0; e < 8; ++e) v[e] = __half2float(__ushort_as_half((uint16_t)(w[e >> 1] >> (16 * (e & 1)))));
+    float mx = v[0], mn = v[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) {
+      mx = fmaxf(mx, v[e]);
+      mn = fminf(mn, v[e]);
+    }
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) {   // within the 16 lanes of the group
+      mx = fmaxf(mx, __shfl_xor(mx, o));
+      mn = fminf(mn, __shfl_xor(mn, o));
+    }
+    const float c = 0.95f;
+    const float x_max = fmaxf(mx, 0.f) * c, x_min = fminf(mn, 0.f) * c;
+    float s = (x_max - x_min) / 15.f;
+    if (s == 0.f) s = 1.f;
+    const float z = fminf(fmaxf(rintf(-x_min / s), 0.f), 15.f);
+    uint32_t packed = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) packed |= (uint32_t)(int)fminf(fmaxf(rintf(v[e] / s) + z, 0.f), 15.f) << (4 * e);
+    if (ok) {
+      reinterpret_cast<uint32_t*>(codes + grp * (kD / 2))[j] = packed;   // values 8j .. 8j + 7
+      if (j == 0) {
+        scales[grp] = s;
+        zeros[grp] = (uint8_t)z;
+      }
+    }
   }
 }
 
@@ -443,7 +459,10 @@ size_t kv4_attention_workspace(int64_t B, int64_t Hq, int64_t T) {
 
 hipError_t launch_kv4_quant(const uint16_t* x, int64_t groups, uint8_t* codes, float* scales, uint8_t* zeros,
                             hipStream_t s) {
-  hipLaunchKernelGGL(k_kv4_quant, dim3((unsigned)((groups + 3) / 4)), dim3(256), 0, s, x, groups, codes, scales, zeros);
+  // 16 groups per workgroup step; a grid-stride loop beyond 8 workgroups per CU
+  const int64_t wgs = (groups + 15) / 16;
+  hipLaunchKernelGGL(k_kv4_quant, dim3((unsigned)(wgs < 2048 ? wgs : 2048)), dim3(256), 0, s, x, groups, codes, scales,
+                     zeros);
   return hipGetLastError();
 }
 
