@@ -66,6 +66,20 @@ def _sources_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def _environment(torch):
+    """GPU, target, ROCm/HIP and torch versions, and the clocks rocm-smi reports (a child process)."""
+    props = torch.cuda.get_device_properties(0)
+    env = {"gpu": torch.cuda.get_device_name(0), "arch": getattr(props, "gcnArchName", None),
+           "hip": torch.version.hip, "torch": torch.__version__, "cus": props.multi_processor_count}
+    try:
+        import subprocess
+        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)
+        env["clocks"] = [ln.strip() for ln in r.stdout.splitlines() if "clk" in ln.lower() and "(" in ln][:8]
+    except Exception as e:   # the tool may be missing; the bench line does not depend on it
+        env["clocks"] = f"unavailable: {type(e).__name__}"
+    return env
+
+
 def _traffic_record():
     """HBM bytes per launch of the decode kernel from the committed rocprofv3 PMC summary.
 
@@ -608,6 +622,17 @@ def main():
     wall = time.perf_counter() - wall0
     ms = t0.elapsed_time(t1) / args.steps
     gbs = dec.packed_bytes / (ms * 1e-3) / 1e9
+    # the distribution of single steps (each replay between its own events), after the timed region
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in ev:
+        a.record()
+        run()
+        b.record()
+    torch.cuda.synchronize()
+    one = sorted(a.elapsed_time(b) for a, b in ev)
+    pct = lambda f: one[min(len(one) - 1, int(round(f * (len(one) - 1))))]
+    step_dist = {"median_ms": round(pct(0.5), 4), "p10_ms": round(pct(0.1), 4), "p90_ms": round(pct(0.9), 4),
+                 "single_steps": len(one)}
 
     # per-launch duration of the decode kernel: HIP events around back-to-back replays of a graph
     # holding just this step's linear launches (same stream, shapes and weights); inside a graph
@@ -645,7 +670,9 @@ def main():
            "tokens_per_s": round(dec.M / (ms * 1e-3), 1),
            "host_wall_s": round(wall, 3),
            "stack_kernel_sum_ms": round(stack_kernel_sum_ms, 4),
-           "roofline": roofline}
+           "step_ms_distribution": step_dist,
+           "roofline": roofline,
+           "env": _environment(torch)}
     del graph
     dec = None
     torch.cuda.empty_cache()
