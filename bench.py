@@ -553,10 +553,46 @@ def cpu_baseline(synth, budget_s=20.0):
         if time.perf_counter() - t0 > budget_s / 2 or n >= 2:
             break
     dt = (time.perf_counter() - t0) / n
+
+    def parts(with_pack):
+        """Seconds of one layer's activation quantizations and linears, measured apart, and of packing
+        the levels of one 4096 x 4096 linear (its own rate, not scaled to the layer)."""
+        a0 = time.perf_counter()
+        qa = {site: quant.act_quant(x, b) for site, (x, b) in sites.items()}
+        a1 = time.perf_counter()
+        for s, P, sw in prepared:
+            q, sx, _, _ = qa[synth.SITE_OF[s.name]]
+            olin.linear(P, sw, olev.FMT_W2_MNZ, s.K, q, sx)
+        a2 = time.perf_counter()
+        r = {"act_quant_s": round(a1 - a0, 3), "linears_s": round(a2 - a1, 3),
+             "layer_GBs": round(packed / (a2 - a0) / 1e9, 4)}
+        if with_pack:
+            p0 = time.perf_counter()
+            P = opack.pack_qw2(pack_levels, olev.FMT_W2_MNZ)
+            p1 = time.perf_counter()
+            r["pack_4096x4096_s"] = round(p1 - p0, 3)
+            r["pack_GBs_of_packed"] = round(P.nbytes / (p1 - p0) / 1e9, 4)
+        return r
+
+    sq = next(s for s in c.linears if s.name == "q")
+    pack_levels = synth.draw_levels(olev.FMT_W2_MNZ, sq.N, sq.K, cfg=1, layer=0, slot=synth.LINEAR_ID["q"])
+    detail = {"all_threads": parts(True)}
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(1):
+            detail["one_thread"] = parts(False)
+    except Exception as e:  # pragma: no cover
+        detail["one_thread"] = f"unavailable: {type(e).__name__}"
+    try:
+        with open("/proc/cpuinfo") as f:
+            detail["cpu_model"] = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:  # pragma: no cover
+        detail["cpu_model"] = None
     return {"value": round(packed / dt / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
             "sample": f"one cfg1 layer (7 linears, 4 activation quantizations) at M=1, {n} timed pass(es) "
                       f"of {dt:.2f} s after one warm-up; {packed} packed bytes per pass; host has "
-                      f"{os.cpu_count()} logical CPUs"}
+                      f"{os.cpu_count()} logical CPUs",
+            "detail": detail}
 
 
 def main():
