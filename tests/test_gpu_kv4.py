@@ -112,3 +112,26 @@ def test_kv4_attention_sharp_softmax(Q, head_major):
     err = np.abs(y.cpu().numpy().astype(np.float64) - ref).max(axis=-1) / np.abs(ref).max(axis=-1)
     print(f"sharp softmax head_major={head_major}: max rel err {err.max():.2e}")
     assert err.max() <= TOL, err.max()
+
+
+@pytest.mark.parametrize("B,T,sample", [(16, 4096, (0, 9, 15)), (1, 32768, (0,))], ids=["B16-T4096", "B1-T32768"])
+def test_kv4_attention_bench_sizes(Q, B, T, sample):
+    """The benchmarked configurations (Hq 32, Hkv 8, head-major cache, the launch the bench times): the
+    whole batch runs on the GPU, the oracle checks the sampled sequences, every query head."""
+    Hq, Hkv = 32, 8
+    rng = np.random.default_rng(B * 7 + T)
+    K = rng.normal(0, 1, (B, Hkv, T, 128)).astype(np.float16)      # head-major rows
+    V = rng.normal(0, 1, (B, Hkv, T, 128)).astype(np.float16)
+    q = (rng.normal(0, 1, (B, Hq, 128)) * rng.uniform(0.2, 3, (B, Hq, 1))).astype(np.float16)
+    k = Q.kv4_quant(torch.from_numpy(K).cuda())
+    v = Q.kv4_quant(torch.from_numpy(V).cuda())
+    y = Q.kv4_attention_decode(torch.from_numpy(q).cuda(), k, v, head_major=True).cpu().numpy().astype(np.float64)
+    for b in sample:
+        Kt = K[b:b + 1].transpose(0, 2, 1, 3)                     # [1, T, Hkv, 128]
+        Vt = V[b:b + 1].transpose(0, 2, 1, 3)
+        kq, ks, kz = okv4.kv4_quant(Kt)
+        vq, vs, vz = okv4.kv4_quant(Vt)
+        ref = okv4.attention_decode(q[b:b + 1], okv4.kv4_dequant(kq, ks, kz), okv4.kv4_dequant(vq, vs, vz))
+        err = np.abs(y[b:b + 1] - ref).max(axis=-1) / np.abs(ref).max(axis=-1)
+        print(f"B={B} T={T} b={b}: max rel err {err.max():.2e}")
+        assert err.max() <= TOL, (b, err.max())
