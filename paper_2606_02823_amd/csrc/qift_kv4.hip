@@ -12,7 +12,7 @@
 // Codes are packed two per byte, value 2i in the low nibble of byte i: the cache holds 64 bytes
 // of codes, an fp32 scale and a zero-point byte per token and KV head.
 //
-// Decode attention (k_kv4_attn, then k_kv4_merge_serial or k_kv4_merge): for query head h and KV head h / G (G = Hq / Hkv),
+// Decode attention (k_kv4_attn, then a merge kernel: k_kv4_merge_regs, k_kv4_merge_serial or k_kv4_merge): for query head h and KV head h / G (G = Hq / Hkv),
 //   out_h = sum_t softmax_t(q_h . k_t / sqrt(d)) v_t.
 // Workgroup (chunk, kv, b) covers 256 cached tokens for the G query heads of one KV head and
 // writes its unnormalized partial output with the chunk's maximum score and sum of exponentials;
@@ -344,6 +344,38 @@ __global__ __launch_bounds__(256) void k_kv4_attn(const uint16_t* __restrict__ q
 }
 
 // out[b][kv G + g][:] = sum_c e^(m_c - M) part_c / sum_c e^(m_c - M) l_c,  M = max_c m_c.
+// Up to NC chunks: thread dd loads its value and every chunk's m and l at once (independent loads,
+// one wait on memory), then reduces in registers.
+template <int G, int NC>
+__global__ __launch_bounds__(kD) void k_kv4_merge_regs(const float* __restrict__ part, int Hq, int Hkv, int nchunks,
+                                                       uint16_t* __restrict__ y) {
+  const int dd = threadIdx.x;
+  const int kv = blockIdx.x / G, g = blockIdx.x % G;
+  const int64_t b = blockIdx.y;
+  const float* base = part + (((int64_t)b * Hkv + kv) * nchunks) * G * kPart + g * kPart;
+  const int64_t cstride = (int64_t)G * kPart;
+  float pv[NC], mv[NC], lv[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const bool ok = c < nchunks;   // chunks past the count: weight 0
+    const float* r = base + (ok ? c : 0) * cstride;
+    pv[c] = r[dd];
+    mv[c] = ok ? r[kD] : -INFINITY;
+    lv[c] = r[kD + 1];
+  }
+  float M = mv[0];
+#pragma unroll
+  for (int c = 1; c < NC; ++c) M = fmaxf(M, mv[c]);
+  float acc = 0.f, L = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const float e = c < nchunks ? expf(mv[c] - M) : 0.f;
+    acc = fmaf(pv[c], e, acc);
+    L = fmaf(lv[c], e, L);
+  }
+  y[(b * Hq + (int64_t)kv * G + g) * kD + dd] = __half_as_ushort(__float2half_rn(acc / L));
+}
+
 // Up to kMergeSerialMax chunks: workgroup (kv G + g, b), thread dd: the maximum by a block
 // reduction, then per tile of 128 chunks the chunk weights once into LDS and the sum over the tile
 // (independent, coalesced loads).
@@ -439,7 +471,14 @@ hipError_t launch_attn_g(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t 
                      Hkv, T, kc, ks, kz, vc, vs, vz, part, nchunks, head_major);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (nchunks <= kMergeSerialMax) {
+  const dim3 mgrid((unsigned)(Hkv * G), (unsigned)B);
+  if (nchunks <= 8) {
+    hipLaunchKernelGGL((k_kv4_merge_regs<G, 8>), mgrid, dim3(kD), 0, s, part, Hq, Hkv, nchunks, y);
+  } else if (nchunks <= 16) {
+    hipLaunchKernelGGL((k_kv4_merge_regs<G, 16>), mgrid, dim3(kD), 0, s, part, Hq, Hkv, nchunks, y);
+  } else if (nchunks <= 32) {
+    hipLaunchKernelGGL((k_kv4_merge_regs<G, 32>), mgrid, dim3(kD), 0, s, part, Hq, Hkv, nchunks, y);
+  } else if (nchunks <= kMergeSerialMax) {
     hipLaunchKernelGGL((k_kv4_merge_serial<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(kD), 0, s, part, Hq,
                        Hkv, nchunks, y);
   } else {
