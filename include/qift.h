@@ -344,8 +344,12 @@ enum { QIFT_KV4_TOKEN_MAJOR = 0, QIFT_KV4_HEAD_MAJOR = 1 };
  * with KV head kv = h / (Hq / Hkv):
  *   out[b][h] = sum_t softmax_t( q[b][h] . k_hat[b, t, kv] / sqrt(128) )
  *               * v_hat[b, t, kv],   x_hat = s (code - z) per group,
- * in fp32 (scores, exponentials and sums) with an fp16 result; the result is
- * within rounding of the exact softmax of the reconstructed cache.
+ * with an fp16 result.  Scores: exact fp16 operands (code - z, the queries)
+ * summed in fp32 on the f16 MFMA; exponentials and statistics in fp32; value
+ * sums: p * s split into two fp16 parts (2^-21 relative) times the codes,
+ * summed in fp32.  Per query head the result is within (2^-11 + 1.1e-4) of
+ * the head's largest output of the exact softmax over the reconstructed
+ * cache (the fp16 rounding of the output being the 2^-11).
  *   q        fp16 [B][Hq][128], the new token's queries.
  *   layout   QIFT_KV4_TOKEN_MAJOR or QIFT_KV4_HEAD_MAJOR (QIFT_ERR_SPEC otherwise).
  *   k_*, v_* the cache as written by qift_kv4_quant for groups in that row
