@@ -160,6 +160,36 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
 #pragma unroll 1
       for (int j = 0; j < 64; ++j) {
         const double s = pot_candidate(j) * a / 4.0;
+        // The outer level is taken where the rounded quotient |w| / s exceeds 2.5.  The sign of
+        // fma(-2.5, s, |w|) is the exact sign of |w| - 2.5 s, which decides the same way except for
+        // |w| / s in (2.5, 2.5 + 2^-52] (the quotient rounds down to 2.5 there): those few values, and
+        // only those, within 2^-51 s above the threshold, are decided by the division itself (a
+        // wave-uniform branch, rarely taken).
+        uint32_t outer[NTILES], near_any = 0;
+#pragma unroll
+        for (int tau = 0; tau < NTILES; ++tau) {
+          outer[tau] = 0;
+          uint32_t nr = 0;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const double r = fma(-2.5, s, fabs(v[tau][e]));
+            outer[tau] |= (uint32_t)(r > 0.0) << e;
+            nr |= (uint32_t)(r > 0.0 && r <= 0x1p-51 * s) << e;
+          }
+          near_any |= valid[tau] ? nr : 0u;
+        }
+        if (__any(near_any != 0)) {
+#pragma unroll
+          for (int tau = 0; tau < NTILES; ++tau)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const double r = fma(-2.5, s, fabs(v[tau][e]));
+              if (valid[tau] && r > 0.0 && r <= 0x1p-51 * s) {
+                const bool o = fabs(v[tau][e] / s) > 2.5;
+                outer[tau] = (outer[tau] & ~(1u << e)) | ((uint32_t)o << e);
+              }
+            }
+        }
         double acc = 0.0;
 #pragma unroll
         for (int tau = 0; tau < NTILES; ++tau) {
@@ -167,9 +197,8 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const double w = v[tau][e];
-            const double u = w / s;
-            const double mag = fabs(u) > 2.5 ? 4.0 : 1.0;
-            const double d = w - s * (u >= 0.0 ? mag : -mag);
+            const double mag = (outer[tau] >> e) & 1u ? 4.0 : 1.0;
+            const double d = w - s * (w >= 0.0 ? mag : -mag);
             acc += d * d;
           }
         }
