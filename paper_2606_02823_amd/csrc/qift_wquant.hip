@@ -118,12 +118,21 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
   }
   // ---- rotate every block of b (blocks past K are zeros and stay zeros), then / sqrt(b)
   dev::BlockSync sync;
+  // sqrt(b) a power of two (b = 4^k): dividing by it is the exact product with its reciprocal
+  int sqe;
+  const bool sq_pow2 = frexp(sqrtb, &sqe) == 0.5;
+  const double inv_sqrtb = 1.0 / sqrtb;
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
     if (tau > 0) __syncthreads();   // the previous tile's last exchange reads are done
     dev::fwht_tile_s<256, 16, true>(v[tau], xch, t, L, sync);
+    if (sq_pow2) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) v[tau][e] = v[tau][e] / sqrtb;
+      for (int e = 0; e < 16; ++e) v[tau][e] = v[tau][e] * inv_sqrtb;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) v[tau][e] = v[tau][e] / sqrtb;
+    }
   }
 
   // ---- scale
@@ -220,31 +229,58 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
   }
   if (t == 0) scales[n] = sw;
 
-  // ---- levels against the stored scale
+  // ---- levels against the stored scale, decided as by the rounded quotient u = w / s_w:
+  //   MNZ |u| > 2 -> 3, PoT |u| > 2.5 -> 4 (else 1, sign of w), W4 q = clamp(rint(u), -7, 7).
+  // Without the division where the decision is clear: for the two-level sets the exact sign of
+  // fma(-thr, s_w, |w|) (the quotient and the real ratio can disagree only within 2^-51 s_w above
+  // the threshold); for W4 the product with 1/s_w rounded to q0, kept when the residual w - q0 s_w
+  // lies clearly inside half a step.  The rest (a wave-uniform branch, rarely taken) divide.
   const double s_w = half_value(sw);
+  const double inv_sw = s_w > 0.0 ? 1.0 / s_w : 0.0;
+  constexpr double thr = FMT == FMT_MNZ ? 2.0 : 2.5;
+  constexpr int hi = FMT == FMT_MNZ ? 3 : 4;
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
     if (!valid[tau]) continue;
-    uint32_t wd[4] = {0, 0, 0, 0};
+    int q[16];
+    uint32_t nr = 0;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      int q;
+      const double w = v[tau][e];
       if constexpr (FMT == FMT_W4) {
-        q = 0;
-        if (s_w > 0.0) {
-          const double r = rint(v[tau][e] / s_w);
-          q = (int)fmin(fmax(r, -7.0), 7.0);
-        }
+        const double q0 = rint(w * inv_sw);
+        const double res = fma(-q0, s_w, w);
+        q[e] = (int)fmin(fmax(q0, -7.0), 7.0);
+        nr |= (uint32_t)(fabs(res) >= (0.5 - 0x1p-45) * s_w) << e;
       } else {
-        q = 1;
-        if (s_w > 0.0) {
-          const double u = v[tau][e] / s_w;
-          const int mag = FMT == FMT_MNZ ? (fabs(u) > 2.0 ? 3 : 1) : (fabs(u) > 2.5 ? 4 : 1);
-          q = u >= 0.0 ? mag : -mag;
+        const double r = fma(-thr, s_w, fabs(w));
+        const int mag = r > 0.0 ? hi : 1;
+        q[e] = w >= 0.0 ? mag : -mag;
+        nr |= (uint32_t)(r > 0.0 && r <= 0x1p-51 * s_w) << e;
+      }
+    }
+    if (s_w > 0.0) {
+      if (__any(nr != 0)) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          if ((nr >> e) & 1u) {
+            const double u = v[tau][e] / s_w;
+            if constexpr (FMT == FMT_W4) {
+              q[e] = (int)fmin(fmax(rint(u), -7.0), 7.0);
+            } else {
+              const int mag = fabs(u) > thr ? hi : 1;
+              q[e] = u >= 0.0 ? mag : -mag;
+            }
+          }
         }
       }
-      wd[e >> 2] |= ((uint32_t)q & 0xFFu) << (8 * (e & 3));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) q[e] = FMT == FMT_W4 ? 0 : 1;
     }
+    uint32_t wd[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) wd[e >> 2] |= ((uint32_t)q[e] & 0xFFu) << (8 * (e & 3));
     *reinterpret_cast<uint4*>(levels + n * K + tau * S::T + 16 * t) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
   }
 }
