@@ -98,9 +98,25 @@ __global__ __launch_bounds__(256) void k_kv4_quant(const uint16_t* __restrict__ 
     float s = (x_max - x_min) / 15.f;
     if (s == 0.f) s = 1.f;
     const float z = fminf(fmaxf(rintf(-x_min / s), 0.f), 15.f);
+    // rint of the rounded quotient v / s without the division where it is clear: q0 = rint(v (1/s))
+    // is that value when the residual v - q0 s lies inside half a step by more than the quotient's
+    // rounding (|v / s| < 32 here); the others (a wave-uniform branch, rarely taken) divide
+    const float inv = 1.0f / s;
+    float qf[8];
+    bool nr = false;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      qf[e] = rintf(v[e] * inv);
+      nr |= fabsf(fmaf(-qf[e], s, v[e])) >= (0.5f - 0x1p-16f) * s;
+    }
+    if (__any(nr)) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (fabsf(fmaf(-qf[e], s, v[e])) >= (0.5f - 0x1p-16f) * s) qf[e] = rintf(v[e] / s);
+    }
     uint32_t packed = 0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) packed |= (uint32_t)(int)fminf(fmaxf(rintf(v[e] / s) + z, 0.f), 15.f) << (4 * e);
+    for (int e = 0; e < 8; ++e) packed |= (uint32_t)(int)fminf(fmaxf(qf[e] + z, 0.f), 15.f) << (4 * e);
     if (ok) {
       reinterpret_cast<uint32_t*>(codes + grp * (kD / 2))[j] = packed;   // values 8j .. 8j + 7
       if (j == 0) {

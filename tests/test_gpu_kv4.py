@@ -135,3 +135,33 @@ def test_kv4_attention_bench_sizes(Q, B, T, sample):
         err = np.abs(y[b:b + 1] - ref).max(axis=-1) / np.abs(ref).max(axis=-1)
         print(f"B={B} T={T} b={b}: max rel err {err.max():.2e}")
         assert err.max() <= TOL, (b, err.max())
+
+
+def test_kv4_quant_exact_half_quotients(Q):
+    """Groups whose values sit exactly on x = (k + 1/2) s (found by searching fp16 ranges whose fp32
+    step s makes those products fp16 values): every code is decided at a tie, where the GPU's
+    fast path must hand over to the division."""
+    c32 = np.float32(0.95)
+    groups = []
+    for bits in range(0x3C00, 0x5000):                 # x_max in [1, 32)
+        x_max = np.uint16(bits).view(np.float16)
+        s = np.float32(np.float32(np.float32(x_max) * c32) / np.float32(15))
+        ties = [np.float32((k + 0.5) * np.float64(s)) for k in range(0, 15)]
+        exact = [t for t in ties if float(np.float16(t)) == float(t) and 0 < t < float(x_max)]
+        if len(exact) >= 3:
+            g = np.zeros(128, dtype=np.float16)
+            g[0] = x_max
+            vals = np.array(exact, dtype=np.float16)
+            g[1:] = np.resize(vals, 127)
+            groups.append(g)
+        if len(groups) >= 64:
+            break
+    assert len(groups) >= 8, len(groups)
+    x = np.stack(groups)
+    c = Q.kv4_quant(torch.from_numpy(x).cuda())
+    torch.cuda.synchronize()
+    q_ref, s_ref, z_ref = okv4.kv4_quant(x)
+    t = x.astype(np.float32) / s_ref[:, None]
+    assert np.mean(t[:, 1:] == np.round(t[:, 1:] - 0.5) + 0.5) > 0.9      # the quotients are half-integers
+    assert np.array_equal(c.scales.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(unpack(c.codes.cpu().numpy()), q_ref)
