@@ -64,7 +64,8 @@ def test_kv4_quant_bitexact(Q):
 @pytest.mark.parametrize("head_major", [False, True], ids=["token_major", "head_major"])
 @pytest.mark.parametrize("B,T,Hq,Hkv", [(1, 1, 32, 8), (2, 255, 32, 8), (1, 256, 32, 8), (2, 257, 16, 8),
                                         (1, 1000, 8, 8), (1, 4100, 64, 8), (3, 700, 32, 8), (2, 513, 4, 2),
-                                        (4, 2100, 32, 8), (2, 4500, 16, 8), (1, 10000, 32, 8)])
+                                        (4, 2100, 32, 8), (2, 4500, 16, 8), (1, 10000, 32, 8),
+                                        (1, 140000, 8, 1)])
 def test_kv4_attention_decode(Q, B, T, Hq, Hkv, head_major):
     rng = np.random.default_rng(B * 100003 + T)
     K = groups_fp16(rng, B * T * Hkv).reshape(B, T, Hkv, 128)
@@ -165,3 +166,27 @@ def test_kv4_quant_exact_half_quotients(Q):
     assert np.mean(t[:, 1:] == np.round(t[:, 1:] - 0.5) + 0.5) > 0.9      # the quotients are half-integers
     assert np.array_equal(c.scales.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
     assert np.array_equal(unpack(c.codes.cpu().numpy()), q_ref)
+
+
+def test_kv4_attention_workspace_reuse(Q):
+    """One workspace serves consecutive calls of different T and B (the partials of one call never
+    leak into the next): every call, repeated, matches the oracle."""
+    Hq, Hkv = 32, 8
+    cases = [(2, 3000), (1, 300), (2, 5000), (1, 1), (2, 256), (1, 4097)]
+    need = max(int(Q.lib().qift_kv4_attention_workspace_bytes(B, Hq, Hkv, 128, T)) for B, T in cases)
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")   # stale contents
+    for B, T in cases:
+        rng = np.random.default_rng(B * 31 + T)
+        K = groups_fp16(rng, B * T * Hkv).reshape(B, T, Hkv, 128)
+        V = rng.normal(0, 1, (B, T, Hkv, 128)).astype(np.float16)
+        q = (rng.normal(0, 1, (B, Hq, 128)) * rng.uniform(0.2, 3, (B, Hq, 1))).astype(np.float16)
+        k = Q.kv4_quant(torch.from_numpy(K).cuda())
+        v = Q.kv4_quant(torch.from_numpy(V).cuda())
+        kq, ks, kz = okv4.kv4_quant(K)
+        vq, vs, vz = okv4.kv4_quant(V)
+        ref = okv4.attention_decode(q, okv4.kv4_dequant(kq, ks, kz), okv4.kv4_dequant(vq, vs, vz))
+        for rep in range(2):
+            y = Q.kv4_attention_decode(torch.from_numpy(q).cuda(), k, v, workspace=ws)
+            err = np.abs(y.cpu().numpy().astype(np.float64) - ref).max(axis=-1) / np.abs(ref).max(axis=-1)
+            print(f"reused workspace B={B} T={T} call {rep}: max rel err {err.max():.2e}")
+            assert err.max() <= TOL, (B, T, rep, err.max())
