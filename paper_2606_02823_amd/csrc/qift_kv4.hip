@@ -12,7 +12,7 @@
 // Codes are packed two per byte, value 2i in the low nibble of byte i: the cache holds 64 bytes
 // of codes, an fp32 scale and a zero-point byte per token and KV head.
 //
-// Decode attention (k_kv4_attn, then a merge kernel: k_kv4_merge_regs, k_kv4_merge_serial or k_kv4_merge): for query head h and KV head h / G (G = Hq / Hkv),
+// Decode attention (k_kv4_attn, then a merge kernel: k_kv4_merge_regs or k_kv4_merge): for query head h and KV head h / G (G = Hq / Hkv),
 //   out_h = sum_t softmax_t(q_h . k_t / sqrt(d)) v_t.
 // Workgroup (chunk, kv, b) covers 256 cached tokens for the G query heads of one KV head and
 // writes its unnormalized partial output with the chunk's maximum score and sum of exponentials;
@@ -392,87 +392,64 @@ __global__ __launch_bounds__(kD) void k_kv4_merge_regs(const float* __restrict__
   y[(b * Hq + (int64_t)kv * G + g) * kD + dd] = __half_as_ushort(__float2half_rn(acc / L));
 }
 
-// Up to kMergeSerialMax chunks: workgroup (kv G + g, b), thread dd: the maximum by a block
-// reduction, then per tile of 128 chunks the chunk weights once into LDS and the sum over the tile
-// (independent, coalesced loads).
-constexpr int kMergeSerialMax = 63;
-template <int G>
-__global__ __launch_bounds__(kD) void k_kv4_merge_serial(const float* __restrict__ part, int Hq, int Hkv, int nchunks,
-                                                  uint16_t* __restrict__ y) {
-  __shared__ float red[kD / 64];
-  __shared__ float ew[kD], lw[kD];
-  const int dd = threadIdx.x, lane = dd & 63, wave = dd >> 6;
-  const int kv = blockIdx.x / G, g = blockIdx.x % G;
-  const int64_t b = blockIdx.y;
-  const float* base = part + (((int64_t)b * Hkv + kv) * nchunks) * G * kPart + g * kPart;
-  const int64_t cstride = (int64_t)G * kPart;
-  float M = -INFINITY;
-  for (int c = dd; c < nchunks; c += kD) M = fmaxf(M, base[c * cstride + kD]);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  if (lane == 0) red[wave] = M;
-  __syncthreads();
-  M = fmaxf(red[0], red[1]);
-  float acc = 0.f, L = 0.f;
-  for (int c0 = 0; c0 < nchunks; c0 += kD) {
-    __syncthreads();   // the previous tile's weights have been read
-    if (c0 + dd < nchunks) {
-      const float* r = base + (c0 + dd) * cstride;
-      const float e = expf(r[kD] - M);
-      ew[dd] = e;
-      lw[dd] = r[kD + 1] * e;
-    }
-    __syncthreads();
-    const int n = nchunks - c0 < kD ? nchunks - c0 : kD;
-#pragma unroll 8
-    for (int i = 0; i < n; ++i) {
-      acc = fmaf(base[(c0 + i) * cstride + dd], ew[i], acc);
-      L += lw[i];
-    }
-  }
-  y[(b * Hq + (int64_t)kv * G + g) * kD + dd] = __half_as_ushort(__float2half_rn(acc / L));
-}
-
-// The same for more chunks: workgroup (kv G + g, b) of S x 128 threads (S = blockDim.x / 128 <=
-// kMergeSlices slices, about 8 chunks each): the maximum by a block reduction, then slice j sums
-// chunks j, j + S, ... (thread dd of the slice: output dimension dd), and the slices' sums are
-// added through LDS.
+// More chunks: workgroup (kv G + g, b) of S x 128 threads (S = blockDim.x / 128 <= kMergeSlices).
+// Slice j takes batches of kMergeBatch chunks (chunks j kMergeBatch + i, then S kMergeBatch further
+// on, ...), each batch's values and statistics loaded at once (one wait on memory per batch) and
+// folded into the slice's running maximum and sums; the slices' results are rescaled to the common
+// maximum through LDS.
 constexpr int kMergeSlices = 8;
+constexpr int kMergeBatch = 16;
 template <int G>
 __global__ __launch_bounds__(kMergeSlices * kD) void k_kv4_merge(const float* __restrict__ part, int Hq, int Hkv,
                                                                  int nchunks, uint16_t* __restrict__ y) {
-  __shared__ float red[kMergeSlices * kD / 64];
   __shared__ float sacc[kMergeSlices][kD];
-  __shared__ float sl[kMergeSlices];
-  const int nthreads = blockDim.x, S = nthreads / kD;
-  const int tid = threadIdx.x, dd = tid % kD, slice = tid / kD, lane = tid & 63, wave = tid >> 6;
+  __shared__ float sm[kMergeSlices], sl[kMergeSlices];
+  const int S = blockDim.x / kD;
+  const int tid = threadIdx.x, dd = tid % kD, slice = tid / kD;
   const int kv = blockIdx.x / G, g = blockIdx.x % G;
   const int64_t b = blockIdx.y;
   const float* base = part + (((int64_t)b * Hkv + kv) * nchunks) * G * kPart + g * kPart;
   const int64_t cstride = (int64_t)G * kPart;
-  float M = -INFINITY;
-  for (int c = tid; c < nchunks; c += nthreads) M = fmaxf(M, base[c * cstride + kD]);
+  float m = -INFINITY, acc = 0.f, L = 0.f;
+  for (int c0 = slice * kMergeBatch; c0 < nchunks; c0 += S * kMergeBatch) {
+    float pv[kMergeBatch], mv[kMergeBatch], lv[kMergeBatch];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  if (lane == 0) red[wave] = M;
-  __syncthreads();
-  for (int w = 0; w < nthreads / 64; ++w) M = fmaxf(M, red[w]);
-  float acc = 0.f, L = 0.f;
-#pragma unroll 4
-  for (int c = slice; c < nchunks; c += S) {
-    const float* r = base + c * cstride;
-    const float e = expf(r[kD] - M);
-    acc = fmaf(r[dd], e, acc);
-    L = fmaf(r[kD + 1], e, L);
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const bool ok = c0 + i < nchunks;      // chunks past the count: weight 0
+      const float* r = base + (ok ? c0 + i : c0) * cstride;
+      pv[i] = r[dd];
+      mv[i] = ok ? r[kD] : -INFINITY;
+      lv[i] = r[kD + 1];
+    }
+    float mb = mv[0];                        // chunk c0 exists: mb and the new maximum are finite
+#pragma unroll
+    for (int i = 1; i < kMergeBatch; ++i) mb = fmaxf(mb, mv[i]);
+    const float mn = fmaxf(m, mb);
+    const float sc = expf(m - mn);           // 0 for the first batch (m = -inf)
+    acc *= sc;
+    L *= sc;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const float e = c0 + i < nchunks ? expf(mv[i] - mn) : 0.f;
+      acc = fmaf(pv[i], e, acc);
+      L = fmaf(lv[i], e, L);
+    }
+    m = mn;
   }
   sacc[slice][dd] = acc;
-  if (dd == 0) sl[slice] = L;
+  if (dd == 0) {
+    sm[slice] = m;
+    sl[slice] = L;
+  }
   __syncthreads();
   if (tid < kD) {
+    float M = sm[0];
+    for (int j = 1; j < S; ++j) M = fmaxf(M, sm[j]);
     float a = 0.f, l = 0.f;
     for (int j = 0; j < S; ++j) {
-      a += sacc[j][tid];
-      l += sl[j];
+      const float e = expf(sm[j] - M);       // 0 for a slice without chunks (sm = -inf, M finite)
+      a = fmaf(sacc[j][tid], e, a);
+      l = fmaf(sl[j], e, l);
     }
     y[(b * Hq + (int64_t)kv * G + g) * kD + tid] = __half_as_ushort(__float2half_rn(a / l));
   }
@@ -494,11 +471,10 @@ hipError_t launch_attn_g(const uint16_t* q, int64_t B, int Hq, int Hkv, int64_t 
     hipLaunchKernelGGL((k_kv4_merge_regs<G, 16>), mgrid, dim3(kD), 0, s, part, Hq, Hkv, nchunks, y);
   } else if (nchunks <= 32) {
     hipLaunchKernelGGL((k_kv4_merge_regs<G, 32>), mgrid, dim3(kD), 0, s, part, Hq, Hkv, nchunks, y);
-  } else if (nchunks <= kMergeSerialMax) {
-    hipLaunchKernelGGL((k_kv4_merge_serial<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(kD), 0, s, part, Hq,
-                       Hkv, nchunks, y);
   } else {
-    const int slices = nchunks / 8 > kMergeSlices ? kMergeSlices : nchunks / 8;
+    // slices of kMergeBatch chunks, at most kMergeSlices
+    const int want = (nchunks + kMergeBatch - 1) / kMergeBatch;
+    const int slices = want > kMergeSlices ? kMergeSlices : want;
     hipLaunchKernelGGL((k_kv4_merge<G>), dim3((unsigned)(Hkv * G), (unsigned)B), dim3(slices * kD), 0, s, part, Hq,
                        Hkv, nchunks, y);
   }
