@@ -65,7 +65,8 @@ def test_kv4_quant_bitexact(Q):
 @pytest.mark.parametrize("B,T,Hq,Hkv", [(1, 1, 32, 8), (2, 255, 32, 8), (1, 256, 32, 8), (2, 257, 16, 8),
                                         (1, 1000, 8, 8), (1, 4100, 64, 8), (3, 700, 32, 8), (2, 513, 4, 2),
                                         (4, 2100, 32, 8), (2, 4500, 16, 8), (1, 10000, 32, 8),
-                                        (1, 8300, 32, 8), (2, 33000, 8, 2), (1, 140000, 8, 1)])
+                                        (1, 8300, 32, 8), (2, 33000, 8, 2), (1, 140000, 8, 1),
+                                        (1, 9000, 8, 8), (2, 9000, 16, 8)])
 def test_kv4_attention_decode(Q, B, T, Hq, Hkv, head_major):
     rng = np.random.default_rng(B * 100003 + T)
     K = groups_fp16(rng, B * T * Hkv).reshape(B, T, Hkv, 128)
