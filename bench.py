@@ -123,7 +123,7 @@ class DecodeStack:
             for slot, (name, N, K, b, site) in enumerate(self.plan):
                 lev = synth.draw_levels_torch(qift.W2_MNZ, N, K, seed=1_000_003 * layer + slot, device=dev)
                 sc = torch.from_numpy(synth.draw_scales(qift.W2_MNZ, N, cfg=1, layer=layer, slot=slot)).to(dev)
-                ws.append(qift.pack_w2(lev, sc, qift.W2_MNZ, check=False))
+                ws.append(qift.pack_w2(lev, sc, qift.W2_MNZ))
                 del lev
             self.weights.append(ws)
             self.x.append([torch.from_numpy(synth.config_activations(c, layer, site, self.M, K)).to(dev)
@@ -190,8 +190,8 @@ class PrefillStack:
             for slot, (name, N, K, b, site) in enumerate(self.plan):
                 lev = synth.draw_levels_torch(fmt, N, K, seed=7_000_003 * layer + slot, device=dev)
                 sc = torch.from_numpy(synth.draw_scales(fmt, N, cfg=4, layer=layer, slot=slot)).to(dev)
-                ws.append(qift.pack_w4(lev, sc, check=False) if fmt == qift.W4_SYM
-                          else qift.pack_w2(lev, sc, fmt, check=False))
+                ws.append(qift.pack_w4(lev, sc) if fmt == qift.W4_SYM
+                          else qift.pack_w2(lev, sc, fmt))
                 del lev
             self.weights.append(ws)
         # one synthetic input per activation site, shared by the layers
@@ -241,7 +241,7 @@ class SweepStack:
                 lev = synth.draw_levels_torch(self.fmt, N, K, seed=3_000_017 * layer + 101 * self.cfg + slot,
                                               device=dev)
                 sc = torch.from_numpy(synth.draw_scales(self.fmt, N, cfg=self.cfg, layer=layer, slot=slot)).to(dev)
-                ws.append(qift.pack_w2(lev, sc, self.fmt, check=False))
+                ws.append(qift.pack_w2(lev, sc, self.fmt))
                 del lev
             self.weights.append(ws)
         self.x = [torch.from_numpy(synth.config_activations(c, 0, site, self.M, K)).to(dev)
@@ -331,7 +331,7 @@ def decode_per_shape(torch, qift, synth, min_bytes=1 << 30, reps=10):
         dev = torch.device("cuda")
         lev = synth.draw_levels_torch(qift.W2_MNZ, N, K, seed=99 + site, device=dev)
         sc = torch.from_numpy(synth.draw_scales(qift.W2_MNZ, N, cfg=1, layer=0, slot=site)).to(dev)
-        base = qift.pack_w2(lev, sc, qift.W2_MNZ, check=False)
+        base = qift.pack_w2(lev, sc, qift.W2_MNZ)
         del lev
         R = -(-min_bytes // base.nbytes)
         reps_w = [qift.Packed(base.fmt, N, K, base.words.clone(), sc) for _ in range(R)]
@@ -387,7 +387,7 @@ def lut_decode(torch, qift, synth, min_bytes=1 << 29, reps=10):
     for name, N, K, b, site in plan:
         codes = torch.randint(0, 4, (N, K), dtype=torch.int8, device=dev, generator=gen)
         sc = torch.from_numpy(synth.draw_scales(qift.W2_MNZ, N, cfg=1, layer=0, slot=site)).to(dev)
-        base = qift.pack_w2(codes, sc, qift.W2_LUT, check=False)
+        base = qift.pack_w2(codes, sc, qift.W2_LUT)
         del codes
         R = -(-min_bytes // base.nbytes)
         reps_w = [qift.Packed(qift.W2_LUT, N, K, base.words.clone(), sc) for _ in range(R)]

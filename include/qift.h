@@ -30,18 +30,22 @@
  *   - Matrices are row-major and dense: x, act_q and y are [M][K] or [M][N];
  *     weights are [N][K] (output x input).
  *   - Every pointer argument is DEVICE memory owned by the caller unless the
- *     comment says "host".  The library allocates nothing, keeps no pointer
- *     after a call returns, and never frees caller memory.  Buffers must stay
- *     alive until the work enqueued on the stream has completed.
+ *     comment says "host".  The library keeps no pointer after a call
+ *     returns and never frees caller memory; the only memory it allocates
+ *     itself is one 4-byte counter per device for the offline pack calls.
+ *     Buffers must stay alive until the work enqueued on the stream has
+ *     completed.
  *   - Device pointers must be 16-byte aligned (QIFT_ERR_ALIGN otherwise).
  *   - K must be a positive multiple of 64; M >= 1; N >= 1 (no alignment).
  *   - Every call enqueues asynchronously on the caller's stream and returns
- *     a status; no call synchronizes.  Argument validation happens on the
- *     host before any HIP call, so an error return means nothing was
- *     enqueued.  Faults inside kernels surface at the caller's next
- *     synchronization.  No C++ exception crosses this interface.
- *   - The library is stateless apart from a thread-local copy of the last
- *     HIP error; calls are thread-safe.
+ *     a status; only the offline pack calls synchronize (to report
+ *     QIFT_ERR_CODE).  Argument validation happens on the host before any
+ *     HIP call, so an error return means nothing was enqueued.  Faults inside
+ *     kernels surface at the caller's next synchronization.  No C++ exception
+ *     crosses this interface.
+ *   - Apart from that counter, a thread-local copy of the last HIP error and
+ *     the per-device error word of the bounded device waits
+ *     (qift_device_error), the library is stateless; calls are thread-safe.
  */
 #ifndef QIFT_H
 #define QIFT_H
@@ -63,7 +67,7 @@ enum {
   QIFT_ERR_SHAPE = -2,     /* M < 1, N < 1, K % 64 != 0, or beyond a limit  */
   QIFT_ERR_SPEC = -3,      /* bad Hadamard block or clip ratio              */
   QIFT_ERR_FORMAT = -4,    /* wrong level-set format or layout for the call */
-  QIFT_ERR_CODE = -5,      /* reserved: reported through invalid_count      */
+  QIFT_ERR_CODE = -5,      /* a level outside the format's set (pack calls)  */
   QIFT_ERR_ALIGN = -6,     /* a device pointer is not 16-byte aligned       */
   QIFT_ERR_HIP = -7,       /* a HIP launch failed: see qift_last_hip_error  */
   QIFT_ERR_WORKSPACE = -8  /* workspace smaller than qift_workspace_bytes   */
@@ -106,16 +110,19 @@ typedef struct {
  *            block-diagonal, I_{K/b} (x) H_b, with the Sylvester matrix
  *            H_b[i][j] = (-1)^popcount(i & j) (deterministic, no random signs;
  *            Sec. 4.1 "Quantization configuration").
- *   clip_num, clip_den   clip ratio c = clip_num / clip_den of the symmetric
- *            INT4 quantizer, 1 <= clip_num <= clip_den <= 16.  {1, 1} is the
- *            plain absmax/7 scale; {9, 10} is the paper's 0.9 setting.
+ *   flags    0: the normalized rotation H_b / sqrt(b) with clip ratio 1 (the
+ *            plain absmax/7 scale).  QIFT_CLIP(num, den): clip ratio
+ *            c = num / den of the symmetric INT4 quantizer, 1 <= num <= den
+ *            <= 16, decided exactly (QIFT_CLIP(9, 10) is the paper's 0.9
+ *            setting, Sec. 4.1).  Any other value is QIFT_ERR_SPEC.
  */
 typedef struct {
   int64_t K;
   int32_t block;
-  int32_t clip_num;
-  int32_t clip_den;
+  int32_t flags;
 } qift_hadamard_spec;
+
+#define QIFT_CLIP(num, den) ((int32_t)((((num) & 0xFF) << 8) | ((den) & 0xFF)))
 
 /* Bytes of packed words: N*K/4 (W2) or N*K/2 (W4); 0 for an invalid query. */
 size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K);
@@ -123,31 +130,30 @@ size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K);
 /*
  * Pack decoded W2 levels into QW2v1 words (Sec. 3.3: a fixed four-level set
  * with a per-output-channel scale, no zero-point).
- *   levels        int8 [N][K], each in {-3,-1,+1,+3} (MNZ) or {-4,-1,+1,+4}
- *                 (PoT).  Passing levels rather than codes keeps this
- *                 boundary independent of the code assignment.
- *   scales        fp16 s_w[N]; not read, recorded in *out.
- *   fmt           QIFT_W2_MNZ or QIFT_W2_POT; or QIFT_W2_LUT, where the
- *                 "levels" are the codes 0..3 (table indices) themselves.
- *   packed        out: uint32 [N][K/16].
- *   out           host, out, nullable: filled with the view of the result.
- *   invalid_count device int32, nullable.  When given, the call first sets it
- *                 to 0 and then adds the number of levels outside the set;
- *                 such a level is packed as code 0.  Read it after the stream
- *                 completes.
+ *   levels   int8 [N][K], each in {-3,-1,+1,+3} (MNZ) or {-4,-1,+1,+4} (PoT).
+ *            Passing levels rather than codes keeps this boundary independent
+ *            of the code assignment.
+ *   scales   fp16 s_w[N], nullable; not read, recorded in *out.
+ *   fmt      QIFT_W2_MNZ or QIFT_W2_POT; or QIFT_W2_LUT, where the "levels"
+ *            are the codes 0..3 (table indices) themselves.
+ *   packed   out: uint32 [N][K/16].
+ *   out      host, out, nullable: filled with the view of the result.
+ * An offline call: it validates every level and SYNCHRONIZES the stream to
+ * read the count back.  A level outside the set returns QIFT_ERR_CODE (the
+ * words are then written with code 0 in its place and must not be used).
+ * The count lives in a 4-byte device word that the library allocates on the
+ * first pack call on a device and keeps until the process ends; pack calls
+ * are serialized by a lock.  Not capturable in a HIP graph.
  */
 int qift_pack_w2(const int8_t *levels, const uint16_t *scales, int64_t N, int64_t K,
-                 int32_t fmt, uint32_t *packed, qift_packed_w *out,
-                 int32_t *invalid_count, qift_stream_t stream);
+                 int32_t fmt, uint32_t *packed, qift_packed_w *out, qift_stream_t stream);
 
 /*
  * Pack W4 levels q in -7..7 (int8 [N][K]) into QW4v1 words uint32 [N][K/8].
- * Same conventions as qift_pack_w2; a level outside -7..7 is packed as 0 and
- * counted.
+ * Same conventions, validation and synchronization as qift_pack_w2.
  */
 int qift_pack_w4(const int8_t *levels, const uint16_t *scales, int64_t N, int64_t K,
-                 uint32_t *packed, qift_packed_w *out, int32_t *invalid_count,
-                 qift_stream_t stream);
+                 uint32_t *packed, qift_packed_w *out, qift_stream_t stream);
 
 /*
  * Offline weight quantization, the step before packing (Sec. 3.1 rotation;
@@ -169,7 +175,7 @@ int qift_pack_w4(const int8_t *levels, const uint16_t *scales, int64_t N, int64_
  * Arguments:
  *   W       fp32 [N][spec.K], finite.
  *   spec    K (multiple of 64, at most 16384), block b (power of two,
- *           2..4096, dividing K); clip_num = clip_den = 1.
+ *           2..4096, dividing K); flags 0.
  *   fmt     QIFT_W2_MNZ, QIFT_W2_POT or QIFT_W4_SYM.
  *   levels  out: int8 [N][K], the input of qift_pack_w2 / qift_pack_w4.
  *   scales  out: fp16 s_w[N].
@@ -187,15 +193,17 @@ int qift_quantize_weights(const float *W, int64_t N, qift_hadamard_spec spec,
  *   A      = max_k |X_k|;
  *   q[m,k] = sign(X_k) * min(7, rne(7 |X_k| / (c A)))  (round half to even,
  *            decided in exact integer arithmetic; A = 0 gives q = 0);
- *   s_x[m] = fp32( (A * clip_num) / ((clip_den * 7) * sqrt(b)) ), i.e.
- *            c * max|X| / 7 for the orthonormal rotation H_b / sqrt(b);
+ *   s_x[m] = fp32( (A * num) / ((den * 7) * sqrt(b)) ), i.e. c * max|X| / 7
+ *            for the orthonormal rotation H_b / sqrt(b), c = num / den from
+ *            spec.flags;
  *   sum[m] = sum_k q[m, k].
  * Arguments:
  *   x          fp16 [M][spec.K], finite values (non-finite input is outside
  *              the contract).
  *   act_q      out: int8 [M][K].
  *   act_scale  out: fp32 [M].
- *   act_sum    out: int32 [M] (required; the linear layers consume it).
+ *   act_sum    out, nullable: int32 [M] (the linear calls compute this sum
+ *              themselves; qift_w2a4_linear_ex may take it to skip that).
  * Limits: spec.K <= 32768.
  */
 int qift_rotate_quant_act(const uint16_t *x, int64_t M, qift_hadamard_spec spec,
@@ -223,17 +231,23 @@ int qift_rotate_quant_act_bf16(const uint16_t *x, int64_t M, qift_hadamard_spec 
  *   y[m][n]   = fp16( fp32( fp32(acc) * act_scale[m] ) * fp32(s_w[n]) )
  * with each fp32 product and the fp16 conversion rounded to nearest even.
  *   w          host: packed weights with fmt QIFT_W2_MNZ or QIFT_W2_POT.
- *   act_q, act_scale, act_sum   the outputs of qift_rotate_quant_act for M
- *              tokens of width w->K (act_sum must be sum_k act_q[m][k]).
+ *   act_q, act_scale   the codes and scales of qift_rotate_quant_act for M
+ *              tokens of width w->K (codes in -7..7).
  *   out        out: fp16 y [M][N].
- * M <= 64 runs the skinny decode kernel; larger M runs the tiled prefill
- * kernel; both give identical results.
+ * The kernels run the MFMA on the raw 2-bit codes and add the exact level
+ * correction from the per-token sum of the codes, which they compute from
+ * the act_q tiles they stage.  M <= 64 runs the skinny decode kernel; larger
+ * M runs the tiled prefill kernel; both give identical results.
  */
 int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
-                     const int32_t *act_sum, int64_t M, uint16_t *out, qift_stream_t stream);
+                     int64_t M, uint16_t *out, qift_stream_t stream);
 
 /*
  * Same as qift_w2a4_linear, and additionally:
+ *   act_sum    nullable: int32 [M], sum_k act_q[m][k] as written by
+ *              qift_rotate_quant_act for these codes; when given the kernels
+ *              use it instead of summing the codes (a wrong sum shifts every
+ *              output: it is taken as is).  NULL: summed in the kernel.
  *   acc_out    out, nullable: int32 [M][N], the exact accumulators.
  *   workspace, workspace_bytes   optional device scratch (16-byte aligned).
  *              NULL / 0 runs the int8 MFMA kernels.  With at least
@@ -258,7 +272,7 @@ int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float
  *   w        host: packed code words (qift_pack_w2 with QIFT_W2_LUT).
  *   lut      host: 4 fp16 bit patterns, the level of codes 0..3; each finite
  *            with magnitude <= 256 (QIFT_ERR_SPEC otherwise).
- *   act_q, act_scale, act_sum   as for qift_w2a4_linear.
+ *   act_q, act_scale   as for qift_w2a4_linear.
  *   out      out: fp16 y [M][N].
  * t is computed as L0 sum q + (L1 - L0) sum c q + (L2 - 2 L1 + L0) sum b1 q
  * + (L3 - L2 - L1 + L0) sum b0 b1 q over the code bits c = b0 + 2 b1, with the
@@ -268,12 +282,11 @@ int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float
  * all M (workgroups of 16 rows x 16 tokens); no tiled prefill form.
  */
 int qift_w2a4_lut_linear(const qift_packed_w *w, const uint16_t *lut, const int8_t *act_q,
-                         const float *act_scale, const int32_t *act_sum, int64_t M, uint16_t *out,
-                         qift_stream_t stream);
+                         const float *act_scale, int64_t M, uint16_t *out, qift_stream_t stream);
 
 /* The W4 sibling (fmt QIFT_W4_SYM); same arguments and results. */
 int qift_w4a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
-                     const int32_t *act_sum, int64_t M, uint16_t *out, qift_stream_t stream);
+                     int64_t M, uint16_t *out, qift_stream_t stream);
 int qift_w4a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
                         const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
                         void *workspace, size_t workspace_bytes, qift_stream_t stream);
@@ -377,6 +390,29 @@ const char *qift_status_string(int status);
 
 /* The hipError_t value behind the calling thread's last QIFT_ERR_HIP. */
 int qift_last_hip_error(void);
+
+/*
+ * Device-side error report.  Every wait inside a kernel is bounded: the
+ * waves of a workgroup that wait for each other (the fused decode) and the
+ * workgroups that wait for another workgroup's result (qift_decode_chain)
+ * give up after a limit, set a bit in a per-device error word and carry on,
+ * so every kernel exits; the results of the affected call are then not to be
+ * trusted.  Bits: QIFT_DEVERR_GROUP_WAIT (a wave barrier inside a
+ * workgroup), QIFT_DEVERR_CHAIN_WAIT (a wait for another workgroup).
+ * qift_device_error synchronizes the stream, writes the word of the current
+ * device to *bits (host) and, if clear is non-zero, resets it.  Not
+ * capturable in a HIP graph.
+ */
+enum { QIFT_DEVERR_GROUP_WAIT = 1, QIFT_DEVERR_CHAIN_WAIT = 2 };
+int qift_device_error(uint32_t *bits, int32_t clear, qift_stream_t stream);
+
+/*
+ * Test hook: the spin limit (iterations) of the in-workgroup wave barriers
+ * for launches made after the call, process-wide; 0 restores the default
+ * (2^22).  A tiny limit makes those waits give up, which the error word then
+ * reports.  QIFT_ERR_SHAPE for a negative value.
+ */
+int qift_set_wait_limit(int32_t spins);
 
 /* Library version string, e.g. "qift 0.1 gfx950". */
 const char *qift_version(void);

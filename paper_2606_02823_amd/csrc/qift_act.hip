@@ -41,7 +41,7 @@ __global__ __launch_bounds__(NT) void k_rotate_quant_act(const uint16_t* __restr
   dev::quant_token<NT, NTILES, BF16>(x + m * K, K, L, num, den, denom, lds, red_d, red_i, act_q + m * K,
                                    sum_q, scale);
   if (threadIdx.x == 0) {
-    act_sum[m] = sum_q;
+    if (act_sum) act_sum[m] = sum_q;
     act_scale[m] = scale;
   }
 }
@@ -78,7 +78,7 @@ __global__ __launch_bounds__(256) void k_act_tokens(const uint16_t* __restrict__
     }
     if (t == 0) {
       act_scale[m] = (float)((A * (double)num) / denom);
-      act_sum[m] = red_i[0] + red_i[1] + red_i[2] + red_i[3];
+      if (act_sum) act_sum[m] = red_i[0] + red_i[1] + red_i[2] + red_i[3];
     }
     if (!kPrefetch && m + (int)gridDim.x < M)
       dev::load_token_raw<256, NTILES>(raw, x + (int64_t)(m + gridDim.x) * K, K);

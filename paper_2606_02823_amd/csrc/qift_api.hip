@@ -4,8 +4,15 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "../../include/qift.h"
 #include "qift_internal.h"
+
+// The error word of the bounded device waits: one per device (each device holds its own copy of
+// this variable), set by kernels whose waits give up, read and cleared by qift_device_error.
+__device__ uint32_t qift_device_error_bits;
 
 namespace {
 
@@ -38,9 +45,22 @@ inline bool shape_ok(int64_t N, int64_t K) {
   return N >= 1 && K >= 64 && K % 64 == 0 && N < (int64_t(1) << 31) && K < (int64_t(1) << 31);
 }
 
+// Clip ratio num/den of a Hadamard spec: flags 0 is 1/1, else QIFT_CLIP(num, den) with
+// 1 <= num <= den <= 16 and no other bits set.
+bool parse_clip(int32_t flags, int* num, int* den) {
+  if (flags == 0) {
+    *num = *den = 1;
+    return true;
+  }
+  if (flags & ~0xFFFF) return false;
+  *num = (flags >> 8) & 0xFF;
+  *den = flags & 0xFF;
+  return *num >= 1 && *num <= *den && *den <= 16;
+}
+
 int check_linear(const qift_packed_w* w, bool want_w4, const int8_t* act_q, const float* act_scale,
                  const int32_t* act_sum, int64_t M, const uint16_t* out, const int32_t* acc_out) {
-  if (!w || !act_q || !act_scale || !act_sum || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
+  if (!w || !act_q || !act_scale || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
   if (w->layout != QIFT_LAYOUT_V1) return QIFT_ERR_FORMAT;
   if (want_w4 ? w->fmt != QIFT_W4_SYM : !is_w2(w->fmt)) return QIFT_ERR_FORMAT;
   if (!shape_ok(w->N, w->K) || M < 1 || M >= (int64_t(1) << 31)) return QIFT_ERR_SHAPE;
@@ -49,9 +69,37 @@ int check_linear(const qift_packed_w* w, bool want_w4, const int8_t* act_q, cons
   // buffer-resource loads address each operand with 32-bit offsets below 2^31
   if (qift_packed_bytes(w->fmt, w->N, w->K) >= (size_t(1) << 31)) return QIFT_ERR_SHAPE;
   if (!aligned16(w->packed) || !aligned16(act_q) || !aligned16(w->scales) || !aligned16(act_scale) ||
-      !aligned16(act_sum) || !aligned16(out) || (acc_out && !aligned16(acc_out)))
+      (act_sum && !aligned16(act_sum)) || !aligned16(out) || (acc_out && !aligned16(acc_out)))
     return QIFT_ERR_ALIGN;
   return QIFT_OK;
+}
+
+// The out-of-set level counter of the packers: one int32 per device in device memory, allocated by
+// the first pack call on that device (an offline call) and kept until the process ends.  The mutex
+// is held from the launch until the count has been read back, so concurrent pack calls never share
+// a count.
+std::mutex g_pack_mu;
+constexpr int kMaxDevices = 64;
+int32_t* g_pack_ctr[kMaxDevices] = {};
+
+template <typename Launch>
+int pack_checked(Launch launch, hipStream_t stream) {
+  std::lock_guard<std::mutex> lock(g_pack_mu);
+  int dev = 0;
+  int st = hip_status(hipGetDevice(&dev));
+  if (st != QIFT_OK) return st;
+  if (dev < 0 || dev >= kMaxDevices) return hip_status(hipErrorInvalidDevice);
+  if (!g_pack_ctr[dev]) {
+    st = hip_status(hipMalloc(reinterpret_cast<void**>(&g_pack_ctr[dev]), sizeof(int32_t)));
+    if (st != QIFT_OK) return st;
+  }
+  st = hip_status(launch(g_pack_ctr[dev]));
+  if (st != QIFT_OK) return st;
+  int32_t bad = 0;
+  st = hip_status(hipMemcpyAsync(&bad, g_pack_ctr[dev], sizeof(bad), hipMemcpyDeviceToHost, stream));
+  if (st == QIFT_OK) st = hip_status(hipStreamSynchronize(stream));
+  if (st != QIFT_OK) return st;
+  return bad ? QIFT_ERR_CODE : QIFT_OK;
 }
 
 int linear_common(const qift_packed_w* w, bool w4, const int8_t* act_q, const float* act_scale,
@@ -69,7 +117,31 @@ int linear_common(const qift_packed_w* w, bool w4, const int8_t* act_q, const fl
                                         act_sum, M, out, acc_out, use, (hipStream_t)stream));
 }
 
+std::mutex g_err_mu;
+uint32_t* g_err_word[kMaxDevices] = {};
+bool g_err_tried[kMaxDevices] = {};
+std::atomic<int> g_wait_limit{qift::kDefaultWaitLimit};
+
 }  // namespace
+
+namespace qift {
+
+uint32_t* device_error_word() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_err_mu);
+  if (!g_err_tried[dev]) {
+    // the device address of this device's copy of the symbol (resolved once per device)
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(qift_device_error_bits)) == hipSuccess) g_err_word[dev] = (uint32_t*)p;
+    g_err_tried[dev] = true;
+  }
+  return g_err_word[dev];
+}
+
+int wait_limit() { return g_wait_limit.load(std::memory_order_relaxed); }
+
+}  // namespace qift
 
 extern "C" {
 
@@ -81,26 +153,24 @@ size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K) {
 }
 
 int qift_pack_w2(const int8_t* levels, const uint16_t* scales, int64_t N, int64_t K, int32_t fmt,
-                 uint32_t* packed, qift_packed_w* out, int32_t* invalid_count, qift_stream_t stream) {
+                 uint32_t* packed, qift_packed_w* out, qift_stream_t stream) {
   if (!levels || !packed) return QIFT_ERR_NULL;
   if (!is_qw2(fmt)) return QIFT_ERR_FORMAT;
   if (!shape_ok(N, K)) return QIFT_ERR_SHAPE;
-  if (!aligned16(levels) || !aligned16(packed) || (scales && !aligned16(scales)) ||
-      (invalid_count && (reinterpret_cast<uintptr_t>(invalid_count) & 3u)))
-    return QIFT_ERR_ALIGN;
-  int st = hip_status(qift::launch_pack_w2(levels, N, K, fmt, packed, invalid_count, (hipStream_t)stream));
+  if (!aligned16(levels) || !aligned16(packed) || (scales && !aligned16(scales))) return QIFT_ERR_ALIGN;
+  const hipStream_t s = (hipStream_t)stream;
+  const int st = pack_checked([&](int32_t* ctr) { return qift::launch_pack_w2(levels, N, K, fmt, packed, ctr, s); }, s);
   if (st == QIFT_OK && out) *out = qift_packed_w{fmt, QIFT_LAYOUT_V1, N, K, packed, scales};
   return st;
 }
 
 int qift_pack_w4(const int8_t* levels, const uint16_t* scales, int64_t N, int64_t K, uint32_t* packed,
-                 qift_packed_w* out, int32_t* invalid_count, qift_stream_t stream) {
+                 qift_packed_w* out, qift_stream_t stream) {
   if (!levels || !packed) return QIFT_ERR_NULL;
   if (!shape_ok(N, K)) return QIFT_ERR_SHAPE;
-  if (!aligned16(levels) || !aligned16(packed) || (scales && !aligned16(scales)) ||
-      (invalid_count && (reinterpret_cast<uintptr_t>(invalid_count) & 3u)))
-    return QIFT_ERR_ALIGN;
-  int st = hip_status(qift::launch_pack_w4(levels, N, K, packed, invalid_count, (hipStream_t)stream));
+  if (!aligned16(levels) || !aligned16(packed) || (scales && !aligned16(scales))) return QIFT_ERR_ALIGN;
+  const hipStream_t s = (hipStream_t)stream;
+  const int st = pack_checked([&](int32_t* ctr) { return qift::launch_pack_w4(levels, N, K, packed, ctr, s); }, s);
   if (st == QIFT_OK && out) *out = qift_packed_w{QIFT_W4_SYM, QIFT_LAYOUT_V1, N, K, packed, scales};
   return st;
 }
@@ -114,7 +184,7 @@ int qift_quantize_weights(const float* W, int64_t N, qift_hadamard_spec spec, in
   if (N * spec.K >= (int64_t(1) << 31)) return QIFT_ERR_SHAPE;
   const int32_t b = spec.block;
   if (b < 2 || b > 4096 || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
-  if (spec.clip_num != 1 || spec.clip_den != 1) return QIFT_ERR_SPEC;
+  if (spec.flags != 0) return QIFT_ERR_SPEC;
   if (!aligned16(W) || !aligned16(levels) || !aligned16(scales)) return QIFT_ERR_ALIGN;
   return hip_status(qift::launch_quantize_weights(W, N, spec.K, b, fmt, levels, scales, (hipStream_t)stream));
 }
@@ -160,16 +230,17 @@ int qift_kv4_attention_decode(const uint16_t* q, int64_t B, int32_t Hq, int32_t 
 namespace {
 int rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q, float* act_scale,
                      int32_t* act_sum, qift_stream_t stream, bool bf16) {
-  if (!x || !act_q || !act_scale || !act_sum) return QIFT_ERR_NULL;
+  if (!x || !act_q || !act_scale) return QIFT_ERR_NULL;
   if (M < 1 || M >= (int64_t(1) << 31) || spec.K < 64 || spec.K % 64 || spec.K > qift::kActMaxK)
     return QIFT_ERR_SHAPE;
   const int32_t b = spec.block;
   if (b < 2 || b > 8192 || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
-  if (spec.clip_num < 1 || spec.clip_den < spec.clip_num || spec.clip_den > 16) return QIFT_ERR_SPEC;
-  if (!aligned16(x) || !aligned16(act_q) || !aligned16(act_scale) || !aligned16(act_sum))
+  int num, den;
+  if (!parse_clip(spec.flags, &num, &den)) return QIFT_ERR_SPEC;
+  if (!aligned16(x) || !aligned16(act_q) || !aligned16(act_scale) || (act_sum && !aligned16(act_sum)))
     return QIFT_ERR_ALIGN;
-  return hip_status(qift::launch_rotate_quant_act(x, M, spec.K, b, spec.clip_num, spec.clip_den, act_q,
-                                                  act_scale, act_sum, (hipStream_t)stream, bf16));
+  return hip_status(qift::launch_rotate_quant_act(x, M, spec.K, b, num, den, act_q, act_scale, act_sum,
+                                                  (hipStream_t)stream, bf16));
 }
 }  // namespace
 
@@ -179,8 +250,8 @@ int qift_rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec,
 }
 
 int qift_w2a4_lut_linear(const qift_packed_w* w, const uint16_t* lut, const int8_t* act_q, const float* act_scale,
-                         const int32_t* act_sum, int64_t M, uint16_t* out, qift_stream_t stream) {
-  if (!w || !lut || !act_q || !act_scale || !act_sum || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
+                         int64_t M, uint16_t* out, qift_stream_t stream) {
+  if (!w || !lut || !act_q || !act_scale || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
   if (w->layout != QIFT_LAYOUT_V1 || w->fmt != QIFT_W2_LUT) return QIFT_ERR_FORMAT;
   // K: whole 256-k blocks, and at most 2^14 for the exact fp64 combination; token blocks of 16 in grid.y
   if (!shape_ok(w->N, w->K) || w->K % 256 || w->K > 16384 || M < 1 || M > 16 * 65535) return QIFT_ERR_SHAPE;
@@ -191,9 +262,9 @@ int qift_w2a4_lut_linear(const qift_packed_w* w, const uint16_t* lut, const int8
     if (!(fabs(L[i]) <= 256.0)) return QIFT_ERR_SPEC;   // also rejects inf and nan
   }
   if (!aligned16(w->packed) || !aligned16(w->scales) || !aligned16(act_q) || !aligned16(act_scale) ||
-      !aligned16(act_sum) || !aligned16(out))
+      !aligned16(out))
     return QIFT_ERR_ALIGN;
-  return hip_status(qift::launch_lut_linear(w->packed, w->scales, w->N, w->K, L, act_q, act_scale, act_sum, M, out,
+  return hip_status(qift::launch_lut_linear(w->packed, w->scales, w->N, w->K, L, act_q, act_scale, M, out,
                                             (hipStream_t)stream));
 }
 
@@ -202,9 +273,9 @@ int qift_rotate_quant_act_bf16(const uint16_t* x, int64_t M, qift_hadamard_spec 
   return rotate_quant_act(x, M, spec, act_q, act_scale, act_sum, stream, true);
 }
 
-int qift_w2a4_linear(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
-                     const int32_t* act_sum, int64_t M, uint16_t* out, qift_stream_t stream) {
-  return linear_common(w, false, act_q, act_scale, act_sum, M, out, nullptr, nullptr, 0, stream);
+int qift_w2a4_linear(const qift_packed_w* w, const int8_t* act_q, const float* act_scale, int64_t M, uint16_t* out,
+                     qift_stream_t stream) {
+  return linear_common(w, false, act_q, act_scale, nullptr, M, out, nullptr, nullptr, 0, stream);
 }
 
 int qift_w2a4_linear_ex(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
@@ -214,9 +285,9 @@ int qift_w2a4_linear_ex(const qift_packed_w* w, const int8_t* act_q, const float
                        stream);
 }
 
-int qift_w4a4_linear(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
-                     const int32_t* act_sum, int64_t M, uint16_t* out, qift_stream_t stream) {
-  return linear_common(w, true, act_q, act_scale, act_sum, M, out, nullptr, nullptr, 0, stream);
+int qift_w4a4_linear(const qift_packed_w* w, const int8_t* act_q, const float* act_scale, int64_t M, uint16_t* out,
+                     qift_stream_t stream) {
+  return linear_common(w, true, act_q, act_scale, nullptr, M, out, nullptr, nullptr, 0, stream);
 }
 
 int qift_w4a4_linear_ex(const qift_packed_w* w, const int8_t* act_q, const float* act_scale,
@@ -237,7 +308,8 @@ int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t 
   if (qift_packed_bytes(w->fmt, w->N, w->K) >= (size_t(1) << 31)) return QIFT_ERR_SHAPE;
   const int32_t b = spec.block;
   if (spec.K != w->K || b < 2 || b > qift::kFusedMaxBlock || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
-  if (spec.clip_num < 1 || spec.clip_den < spec.clip_num || spec.clip_den > 16) return QIFT_ERR_SPEC;
+  int num, den;
+  if (!parse_clip(spec.flags, &num, &den)) return QIFT_ERR_SPEC;
   if (!aligned16(w->packed) || !aligned16(w->scales) || !aligned16(x) || !aligned16(out) ||
       (acc_out && !aligned16(acc_out)) || (act_q && !aligned16(act_q)) ||
       (act_scale && !aligned16(act_scale)) || (act_sum && !aligned16(act_sum)))
@@ -245,8 +317,8 @@ int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t 
   auto launch = w->fmt == QIFT_W2_MNZ ? qift::launch_fused_mnz
                : w->fmt == QIFT_W2_POT ? qift::launch_fused_pot
                                        : qift::launch_fused_w4;
-  return hip_status(launch(w->packed, w->scales, w->N, w->K, x, b, spec.clip_num, spec.clip_den, M, out, acc_out,
-                           act_q, act_scale, act_sum, (hipStream_t)stream));
+  return hip_status(launch(w->packed, w->scales, w->N, w->K, x, b, num, den, M, out, acc_out, act_q, act_scale,
+                           act_sum, (hipStream_t)stream));
 }
 
 int qift_hbm_read_probe(const void* buf, size_t bytes, uint32_t* partials, qift_stream_t stream) {
@@ -269,7 +341,7 @@ const char* qift_status_string(int status) {
     case QIFT_ERR_SHAPE: return "invalid shape (M, N >= 1; K a positive multiple of 64; limits)";
     case QIFT_ERR_SPEC: return "invalid Hadamard block or clip ratio";
     case QIFT_ERR_FORMAT: return "wrong level-set format or layout for this call";
-    case QIFT_ERR_CODE: return "level outside the format's level set";
+    case QIFT_ERR_CODE: return "level outside the format's level set (nothing usable was packed)";
     case QIFT_ERR_ALIGN: return "device pointer not 16-byte aligned";
     case QIFT_ERR_HIP: return "HIP launch failed";
     case QIFT_ERR_WORKSPACE: return "workspace too small";
@@ -278,6 +350,24 @@ const char* qift_status_string(int status) {
 }
 
 int qift_last_hip_error(void) { return g_last_hip; }
+
+int qift_device_error(uint32_t* bits, int32_t clear, qift_stream_t stream) {
+  if (!bits) return QIFT_ERR_NULL;
+  *bits = 0;
+  uint32_t* word = qift::device_error_word();
+  if (!word) return hip_status(hipErrorInvalidSymbol);
+  const hipStream_t s = (hipStream_t)stream;
+  int st = hip_status(hipMemcpyAsync(bits, word, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  if (st == QIFT_OK && clear) st = hip_status(hipMemsetAsync(word, 0, sizeof(uint32_t), s));
+  if (st == QIFT_OK) st = hip_status(hipStreamSynchronize(s));
+  return st;
+}
+
+int qift_set_wait_limit(int32_t spins) {
+  if (spins < 0) return QIFT_ERR_SHAPE;
+  g_wait_limit.store(spins == 0 ? qift::kDefaultWaitLimit : spins, std::memory_order_relaxed);
+  return QIFT_OK;
+}
 
 const char* qift_version(void) { return "qift 0.1 gfx950"; }
 

@@ -81,14 +81,16 @@ constexpr int tail_bytes() { return xch_region<NTILES, T, CODES>() + 64 + 128 + 
 
 // CODES = false: the tokens x are rotated and quantized in the kernel (M <= 4; the codes, scales and
 // sums may be written to act_q_out / scale_out / sum_out).  CODES = true: the linear on precomputed
-// codes aq_in [M][K], scales sx_in [M] and sums sum_in [M] (M <= 16), staged into LDS by waves 0-3.
+// codes aq_in [M][K] and scales sx_in [M] (M <= 16), staged into LDS by waves 0-3, which also add up
+// each token's codes unless the sums come in sum_in [M] (nullable).
 template <int FMT, int NTILES, int T, int LC, bool CODES>
 __global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_decode(
     const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
     const uint16_t* __restrict__ x, int L, int num, int den, double denom,
     int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
     const int8_t* __restrict__ aq_in, const float* __restrict__ sx_in, const int32_t* __restrict__ sum_in,
-    int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+    int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out, int wait_limit,
+    uint32_t* __restrict__ err) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
   constexpr bool PLANAR = FMT == FMT_MNZ;                   // plane decode, codes in planar layout
   // accumulators per tile (MNZ: one per bit plane, planes 0 and 3 sharing one from 4 tiles on, where
@@ -118,6 +120,7 @@ __global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_deco
     xflag[0] = 0u;
   }
   if (tid < 4) reinterpret_cast<uint4*>(zero64)[tid] = make_uint4(0u, 0u, 0u, 0u);
+  if (CODES && tid < 16) red_i[tid] = 0;   // sums of q accumulated while the codes are staged
   __syncthreads();   // nothing is in flight yet: this costs only the launch skew of the waves
 
   const int tile0 = blockIdx.x * T;
@@ -169,6 +172,20 @@ __global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_deco
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int i = i0 + tid + 256 * q;
+        if (!sum_in) {
+          // sum_k q of each token: the piece sums go to red_i[m] by LDS atomics, one per wave when
+          // all 64 pieces of the wave belong to one token (the common case: K >= 1024)
+          const bool ok = i < npieces;
+          const int m = ok ? i / per_row : -1;
+          const int s = ok ? sum16_i8(c[q], 0) : 0;
+          const int m0 = __builtin_amdgcn_readfirstlane(m);
+          if (__all(m == m0)) {
+            const int ws = dev::wave_sum(s);
+            if (lane == 0 && m0 >= 0) atomicAdd(&red_i[m0], ws);
+          } else if (ok) {
+            atomicAdd(&red_i[m], s);
+          }
+        }
         if (i < npieces) {
           const int m = i / per_row, j = i - m * per_row;
           if constexpr (PLANAR) {
@@ -186,12 +203,12 @@ __global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_deco
     }
     if (tid < M) {
       s_scale[tid] = sx_in[tid];
-      red_i[tid] = sum_in[tid];
+      if (sum_in) red_i[tid] = sum_in[tid];
     }
     swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
   } else if (wave < 4) {
     // ---- activation waves: rotate and quantize every token into LDS
-    dev::GroupSync<4> sync{ctr, 0u};
+    dev::GroupSync<4> sync{ctr, 0u, wait_limit, err};
     dev::TokenRaw<NTILES> raw;
     dev::load_token_raw<256, NTILES>(raw, x, K);
     swq = dev::bload8(srs, wave < T && n_st < N ? (uint32_t)(2 * n_st) : dev::kOutOfRange);
@@ -411,7 +428,8 @@ hipError_t launch_t(const FusedArgs& a, hipStream_t s) {
   }
   hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, LC, CODES>), dim3(grid), dim3(fused_threads<NTILES, CODES>()),
                      shmem, s, a.P, a.sw, (int)a.N, (int)a.K, a.x, a.L, a.num, a.den, a.denom, a.aq_out, a.sc_out,
-                     a.sm_out, a.aq_in, a.sx_in, a.sum_in, (int)a.M, kpad_of(a.K), a.y, a.acc_out);
+                     a.sm_out, a.aq_in, a.sx_in, a.sum_in, (int)a.M, kpad_of(a.K), a.y, a.acc_out, wait_limit(),
+                     device_error_word());
   return hipGetLastError();
 }
 

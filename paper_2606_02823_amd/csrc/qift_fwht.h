@@ -135,24 +135,42 @@ struct BlockSync {
   __device__ void operator()() const { __syncthreads(); }
 };
 
+// Bits of the per-device error word that bounded waits set when they give up
+// (read back by the host through qift_device_error).
+constexpr uint32_t kErrGroupWait = 1u;   // a wave barrier inside a workgroup (GroupSync)
+constexpr uint32_t kErrChainWait = 2u;   // a wait for another workgroup's result (decode chain)
+
+__device__ __forceinline__ void flag_error(uint32_t* err, uint32_t bit) {
+  if (err) __hip_atomic_fetch_or(err, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Barrier among the first NW waves of a workgroup that leaves its other waves
 // running: lane 0 of each wave bumps a counter in LDS once the wave's LDS
 // accesses have completed, and the wave spins until the counter reaches the
 // next multiple of NW.  The counter is zeroed once before first use (under a
 // full workgroup barrier) and never reset.  All NW waves make the same
-// sequence of calls, so every wait ends; the spin is bounded all the same.
+// sequence of calls, so every wait ends; the spin is bounded all the same
+// (limit iterations): a wave that gives up sets kErrGroupWait in *err and
+// carries on, so the kernel still exits and the host learns that its
+// results are not to be trusted.
 template <int NW>
 struct GroupSync {
   unsigned* ctr;
   unsigned target;
+  int limit;
+  uint32_t* err;
   __device__ void operator()() {
     target += NW;
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    for (int spin = 0; spin < (1 << 22); ++spin) {
+    for (int spin = 0;; ++spin) {
       const unsigned c = __builtin_amdgcn_readfirstlane(
           __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
       if (c >= target) break;
+      if (spin >= limit) {
+        if ((threadIdx.x & 63) == 0) flag_error(err, kErrGroupWait);
+        break;
+      }
     }
     asm volatile("" ::: "memory");
   }
@@ -244,12 +262,13 @@ __device__ __attribute__((noinline)) int quant_exact(double ax, double f, int64_
   const int64_t xi = (int64_t)(ax * 0x1p24);
   const int64_t t = 14 * (int64_t)den * xi + (int64_t)num * Ai;
   const int64_t d = 2 * (int64_t)num * Ai;
-  int64_t q = (int64_t)f;
+  if (!(f < 8.0)) return 7;   // clamps anyway (and keeps q and t below in range)
+  int64_t q = (int64_t)f;     // within one of the exact quotient: each loop runs at most twice
   int64_t r = t - q * d;
-  while (r < 0) { --q; r += d; }
-  while (r >= d) { ++q; r -= d; }
+  for (int it = 0; r < 0 && it < 4; ++it) { --q; r += d; }
+  for (int it = 0; r >= d && it < 4; ++it) { ++q; r -= d; }
   if (r == 0 && (q & 1)) --q;
-  return (int)(q < 7 ? q : 7);
+  return (int)(q < 0 ? 0 : q < 7 ? q : 7);
 }
 
 // Rounding of 16 values.  The fp64 quotient v = X c1 is within 1e-13 of the

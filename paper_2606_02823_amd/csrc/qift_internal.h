@@ -31,8 +31,7 @@ hipError_t launch_kv4_attention(const uint16_t* q, int64_t B, int Hq, int Hkv, i
 
 // Linear over a four-level fp16 table (qift_lut.hip): lut holds the table entries exactly
 hipError_t launch_lut_linear(const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K, const double lut[4],
-                             const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
-                             uint16_t* out, hipStream_t s);
+                             const int8_t* act_q, const float* act_scale, int64_t M, uint16_t* out, hipStream_t s);
 
 // Rotation + INT4 quantization (qift_act.hip)
 hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int block, int clip_num,
@@ -87,6 +86,13 @@ hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* partials, 
 
 // (den * 7) * sqrt(b): the fixed divisor of the per-token activation scale.
 double act_denominator(int block, int clip_den);
+
+// The per-device error word of the bounded device waits (qift_api.hip): its device address on the
+// current device (nullptr if it cannot be resolved; the kernels then skip the report), and the spin
+// limit of the waves' in-workgroup barriers (a test hook lowers it so that the waits give up).
+uint32_t* device_error_word();
+int wait_limit();
+constexpr int kDefaultWaitLimit = 1 << 22;
 
 // Limits of the fused entry point.
 constexpr int64_t kFusedMaxM = 4;

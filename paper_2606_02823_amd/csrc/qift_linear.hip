@@ -43,9 +43,11 @@ __device__ __forceinline__ void load_chunk(WChunk<FMT>& ck, const char* prow, bo
   }
 }
 
+// With sumq the codes of the chunk are also added to sq (the first tile of a workgroup visits every
+// k of every token once across its lanes and waves).
 template <int FMT>
 __device__ __forceinline__ void mma_chunk(const WChunk<FMT>& ck, v4i& acc, int K, int c, int g, int m, int M,
-                                          const int8_t* __restrict__ act) {
+                                          const int8_t* __restrict__ act, bool sumq, int& sq) {
   const bool mok = m < M;
   // B operands of the whole chunk first (independent loads, one wait)
   v4i b[4][4];
@@ -59,6 +61,14 @@ __device__ __forceinline__ void mma_chunk(const WChunk<FMT>& ck, v4i& acc, int K
       if (ok) bb = *reinterpret_cast<const uint4*>(act + (int64_t)m * K + k0 + 16 * s);
       b[u][s] = v4i{(int)bb.x, (int)bb.y, (int)bb.z, (int)bb.w};
     }
+  }
+  if (sumq) {   // wave-uniform
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        sq = sum16_i8(make_uint4((uint32_t)b[u][s][0], (uint32_t)b[u][s][1], (uint32_t)b[u][s][2],
+                                 (uint32_t)b[u][s][3]), sq);
   }
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
@@ -76,6 +86,7 @@ __global__ __launch_bounds__(256) void k_decode(
   __shared__ v4i red[4 * 64];
   __shared__ float s_scale[16];
   __shared__ int s_sum[16];
+  __shared__ int s_part[4][16];   // per-wave sums of q (no asum given)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int ntiles = (N + 15) >> 4;
@@ -93,13 +104,15 @@ __global__ __launch_bounds__(256) void k_decode(
   }
   if (tid < M) {
     s_scale[tid] = sx[tid];
-    s_sum[tid] = asum[tid];
+    if (asum) s_sum[tid] = asum[tid];
   }
   __syncthreads();
 
   const int m = r16;   // token of this lane's B operand and outputs
+  bool first = asum == nullptr;   // sum the codes of the first tile's B operands
   for (; tile < ntiles; tile += gridDim.x) {
     v4i acc = v4i{0, 0, 0, 0};
+    int sq = 0;
     for (int c = wave; c < NC; c += 4) {
       // prefetch the wave's next chunk: same tile, or the first chunk of the next tile
       int nc = c + 4, nt = tile;
@@ -114,11 +127,22 @@ __global__ __launch_bounds__(256) void k_decode(
         const char* prow = reinterpret_cast<const char*>(P) + (int64_t)(rowok ? n : 0) * rowbytes;
         load_chunk<FMT>(nxt, prow, rowok, K, nc, g);
       }
-      mma_chunk<FMT>(cur, acc, K, c, g, m, M, act);
+      mma_chunk<FMT>(cur, acc, K, c, g, m, M, act, first, sq);
       cur = nxt;
     }
     red[wave * 64 + lane] = acc;
+    if (first) {
+      // lanes m, m + 16, m + 32, m + 48 hold the four k-groups of token m
+      sq += __shfl_xor(sq, 16);
+      sq += __shfl_xor(sq, 32);
+      if (lane < 16) s_part[wave][lane] = sq;
+    }
     __syncthreads();
+    if (first) {
+      if (tid < 16) s_sum[tid] = s_part[0][tid] + s_part[1][tid] + s_part[2][tid] + s_part[3][tid];
+      __syncthreads();
+      first = false;
+    }
     if (wave == 0) {
       v4i D = red[lane];
 #pragma unroll
@@ -191,7 +215,8 @@ __global__ __launch_bounds__(256) void k_decode_deep(
   }
   const int mm = tid < M ? tid : 0;
   const float sx_pre = sx[mm];
-  const int sum_pre = asum[mm];
+  const int sum_pre = asum ? asum[mm] : 0;
+  if (!asum && tid < 16) s_sum[tid] = 0;
   // keep every activation load ahead of the weight loads in the instruction stream
   __builtin_amdgcn_sched_barrier(0);
 
@@ -213,6 +238,7 @@ __global__ __launch_bounds__(256) void k_decode_deep(
   load_batch(0);
 
   // (3) activations into LDS
+  if (!asum) dev::lds_barrier();   // the zeroed sums before any wave adds to them (weights stay in flight)
 #pragma unroll
   for (int q = 0; q < kPre; ++q) {
     const int i = tid + 256 * q;
@@ -224,9 +250,17 @@ __global__ __launch_bounds__(256) void k_decode_deep(
     *reinterpret_cast<uint4*>(act_l + m * Kpad + 16 * j) =
         *reinterpret_cast<const uint4*>(act + (int64_t)m * K + 16 * j);
   }
+  if (asum == nullptr) {
+    // sum_k q per token from the staged codes (each thread re-reads the pieces it staged itself; LDS
+    // atomics into s_sum, zeroed before the barrier above)
+    for (int i = tid; i < M * per_row; i += 256) {
+      const int mm2 = i / per_row, j = i - mm2 * per_row;
+      atomicAdd(&s_sum[mm2], sum16_i8(*reinterpret_cast<const uint4*>(act_l + mm2 * Kpad + 16 * j), 0));
+    }
+  }
   if (tid < M) {
     s_scale[tid] = sx_pre;
-    s_sum[tid] = sum_pre;
+    if (asum) s_sum[tid] = sum_pre;
   }
   __syncthreads();
 
@@ -307,7 +341,9 @@ __device__ __forceinline__ v4i gemm_operand(const uint4& u, int s) {
 // operand reads from the other and waits for them only at the end of the
 // step.
 // ===========================================================================
-template <int FMT, int OCC, int TT>
+// With SUMQ (no per-token sums given) wave w also adds up the codes of token tiles t = w (mod 4): one
+// more 16-byte LDS read and four dot products per MFMA operand step of its own tile(s).
+template <int FMT, int OCC, int TT, bool SUMQ>
 __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                    int N, int K, const int8_t* __restrict__ act,
                                                    const float* __restrict__ sx, const int32_t* __restrict__ asum,
@@ -380,6 +416,10 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int t = 0; t < TT; ++t) acc[j][t] = v4i{0, 0, 0, 0};
+  static_assert(TT % 4 == 0, "token tiles per wave for the sums");
+  int sq[TT / 4];
+#pragma unroll
+  for (int t4 = 0; t4 < TT / 4; ++t4) sq[t4] = 0;
 
   // one step: prefetch step kt+1 (activations into lds[buf ^ 1], weights into wn), MFMAs of step kt
   // from lds[buf] and wc; the k loop is unrolled by two so the weight registers alternate instead of
@@ -403,6 +443,14 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[j][t] = mfma_i8(a[j], b, acc[j][t]);
       }
+      if constexpr (SUMQ) {
+#pragma unroll
+        for (int t4 = 0; t4 < TT / 4; ++t4) {
+          const int row = 16 * (4 * t4 + wave) + r16;
+          sq[t4] = sum16_i8(*reinterpret_cast<const uint4*>(&tileb[row * BK + 16 * ((S * g + s) ^ (row % SL))]),
+                            sq[t4]);
+        }
+      }
     }
     // this wave's loads of step kt+1 have landed (vmcnt(0) with lgkmcnt and expcnt untouched)
     __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -419,14 +467,27 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
     if (kt + 1 < KT) step(kt + 1, lds1, lds0, wb, wa);
   }
 
+  // per-token sums: the four lane groups of a token add up, then the waves exchange them through
+  // the (now idle) first activation buffer
+  int* s_q = reinterpret_cast<int*>(lds0);
+  if constexpr (SUMQ) {
+#pragma unroll
+    for (int t4 = 0; t4 < TT / 4; ++t4) {
+      int v = sq[t4];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16) s_q[16 * (4 * t4 + wave) + lane] = v;
+    }
+    __syncthreads();
+  }
 #pragma unroll
   for (int t = 0; t < TT; ++t) {
     const int m = m_base + 16 * t + r16;
     if (m < M) {
       const float s_x = sx[m];
-      const int sq = asum[m];
+      const int sqm = SUMQ ? s_q[16 * t + r16] : asum[m];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) store4<FMT>(acc[j][t], m, n_base + 16 * j + 4 * g, N, s_x, sq, sw, y, acc_out);
+      for (int j = 0; j < 4; ++j) store4<FMT>(acc[j][t], m, n_base + 16 * j + 4 * g, N, s_x, sqm, sw, y, acc_out);
     }
   }
 }
@@ -517,12 +578,13 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
       for (int64_t m0 = 0; m0 < M; m0 += mb) {
         const int64_t mm = M - m0 < mb ? M - m0 : mb;
         const int8_t* a = act + m0 * K;
+        const int32_t* as = asum ? asum + m0 : nullptr;   // no sums given: summed in the kernel
         uint16_t* yb = y + m0 * N;
         int32_t* ab = acc_out ? acc_out + m0 * N : nullptr;
         hipError_t e;
-        if constexpr (FMT == FMT_MNZ) e = launch_codes_mnz(P, sw, N, K, a, sx + m0, asum + m0, mm, yb, ab, s);
-        else if constexpr (FMT == FMT_POT) e = launch_codes_pot(P, sw, N, K, a, sx + m0, asum + m0, mm, yb, ab, s);
-        else e = launch_codes_w4(P, sw, N, K, a, sx + m0, asum + m0, mm, yb, ab, s);
+        if constexpr (FMT == FMT_MNZ) e = launch_codes_mnz(P, sw, N, K, a, sx + m0, as, mm, yb, ab, s);
+        else if constexpr (FMT == FMT_POT) e = launch_codes_pot(P, sw, N, K, a, sx + m0, as, mm, yb, ab, s);
+        else e = launch_codes_w4(P, sw, N, K, a, sx + m0, as, mm, yb, ab, s);
         if (e != hipSuccess) return e;
       }
       return hipSuccess;
@@ -541,13 +603,22 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
   if constexpr (FMT == FMT_W4) {
     const unsigned gy8 = (unsigned)((M + 127) / 128);
     if ((uint64_t)gx * gy8 >= 1024) {
-      hipLaunchKernelGGL((k_gemm<FMT, 2, 8>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum,
-                         (int)M, y, acc_out);
+      if (asum)
+        hipLaunchKernelGGL((k_gemm<FMT, 2, 8, false>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx,
+                           asum, (int)M, y, acc_out);
+      else
+        hipLaunchKernelGGL((k_gemm<FMT, 2, 8, true>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx,
+                           asum, (int)M, y, acc_out);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((k_gemm<FMT, 3, 4>), dim3(gx, (unsigned)((M + 63) / 64)), dim3(256), 0, s, P, sw, (int)N,
-                     (int)K, act, sx, asum, (int)M, y, acc_out);
+  const dim3 grid(gx, (unsigned)((M + 63) / 64));
+  if (asum)
+    hipLaunchKernelGGL((k_gemm<FMT, 3, 4, false>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M,
+                       y, acc_out);
+  else
+    hipLaunchKernelGGL((k_gemm<FMT, 3, 4, true>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M,
+                       y, acc_out);
   return hipGetLastError();
 }
 

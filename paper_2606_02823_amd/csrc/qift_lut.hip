@@ -8,7 +8,8 @@
 //   lut[c] = L0 + e1 c + e2 b1 + e3 b0 b1,  e1 = L1 - L0, e2 = L2 - 2 L1 + L0, e3 = L3 - L2 - L1 + L0,
 // so t = L0 sum q + e1 sum c q + e2 sum b1 q + e3 sum b0 b1 q, three exact int32 sums on the int8
 // MFMA (operands: the codes, the high bits, the products of the bits, one byte per weight) plus
-// the per-token sum of q.  Every table entry is a multiple of 2^-24 of magnitude at most 256 and
+// the per-token sum of q, added up from the activation operands the lanes already hold (dot
+// products with 1).  Every table entry is a multiple of 2^-24 of magnitude at most 256 and
 // K <= 16384, so every term and partial sum of the fp64 combination is an integer number of
 // 2^-24 units below 2^53: t is exact, and y is bit-exact.
 //
@@ -36,9 +37,9 @@ struct LutCoef {
 template <int NW, bool PREFETCH>
 __global__ __launch_bounds__(64 * NW) void k_lut_linear(const uint32_t* __restrict__ W, const uint16_t* __restrict__ s_w,
                                                     const int8_t* __restrict__ act_q, const float* __restrict__ s_x,
-                                                    const int32_t* __restrict__ act_sum, int M, int64_t N, int64_t K,
-                                                    LutCoef cf, uint16_t* __restrict__ y) {
+                                                    int M, int64_t N, int64_t K, LutCoef cf, uint16_t* __restrict__ y) {
   __shared__ int red[NW][3][16][16];   // [wave][sum][row][token]
+  __shared__ int redq[NW][4][16];      // [wave][k-group][token]: partial sums of q
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, kg = lane >> 4;
   const int64_t n0 = (int64_t)blockIdx.x * 16;
@@ -53,6 +54,7 @@ __global__ __launch_bounds__(64 * NW) void k_lut_linear(const uint32_t* __restri
   const uint32_t wbase = li < nrows ? (uint32_t)li * rowbytes : dev::kOutOfRange;
   const uint32_t abase = li < mrows ? (uint32_t)li * (uint32_t)K : dev::kOutOfRange;
   v4i dc = {0, 0, 0, 0}, d1 = dc, d01 = dc;
+  int sq = 0;
   const int nblk = (int)(K / 256);
   // block S's loads; a block past the end reads zeros (its offsets are past both buffers)
   auto load = [&](int S, uint4& wq, uint4 (&aq)[4]) {
@@ -87,6 +89,7 @@ __global__ __launch_bounds__(64 * NW) void k_lut_linear(const uint32_t* __restri
         both[t] = (int)(ct & h);
       }
       const v4i b = __builtin_bit_cast(v4i, aq[j]);
+      sq = mma::sum16_i8(aq[j], sq);
       dc = mma::mfma_i8(c, b, dc);
       d1 = mma::mfma_i8(hb, b, d1);
       d01 = mma::mfma_i8(both, b, d01);
@@ -99,6 +102,7 @@ __global__ __launch_bounds__(64 * NW) void k_lut_linear(const uint32_t* __restri
     red[wave][1][4 * kg + r][li] = d1[r];
     red[wave][2][4 * kg + r][li] = d01[r];
   }
+  redq[wave][kg][li] = sq;
   __syncthreads();
   const int m = tid >> 4, n = tid & 15;
   if (m < mrows && n < nrows) {
@@ -109,8 +113,10 @@ __global__ __launch_bounds__(64 * NW) void k_lut_linear(const uint32_t* __restri
 #pragma unroll
       for (int w = 0; w < NW; ++w) s[p] += red[w][p][n][m];
     }
-    const double t = cf.L0 * (double)act_sum[m0 + m] + cf.e1 * (double)s[0] + cf.e2 * (double)s[1] +
-                     cf.e3 * (double)s[2];
+    int sum_q = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) sum_q += redq[w][0][m] + redq[w][1][m] + redq[w][2][m] + redq[w][3][m];
+    const double t = cf.L0 * (double)sum_q + cf.e1 * (double)s[0] + cf.e2 * (double)s[1] + cf.e3 * (double)s[2];
     // fp32 intermediates pinned to registers: otherwise the backend fuses the second product with the
     // fp16 conversion (one rounding instead of two), as in the integer formats' epilogue
     float a = (float)t * s_x[m0 + m];
@@ -125,15 +131,14 @@ __global__ __launch_bounds__(64 * NW) void k_lut_linear(const uint32_t* __restri
 }  // namespace
 
 hipError_t launch_lut_linear(const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K, const double lut[4],
-                             const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
-                             uint16_t* out, hipStream_t s) {
+                             const int8_t* act_q, const float* act_scale, int64_t M, uint16_t* out, hipStream_t s) {
   const LutCoef cf{lut[0], lut[1] - lut[0], lut[2] - 2.0 * lut[1] + lut[0], lut[3] - lut[2] - lut[1] + lut[0]};
   const dim3 grid((unsigned)((N + 15) / 16), (unsigned)((M + 15) / 16));
   if ((int64_t)grid.x * grid.y < 512)
-    hipLaunchKernelGGL((k_lut_linear<8, true>), grid, dim3(512), 0, s, packed, scales, act_q, act_scale, act_sum, (int)M, N, K,
+    hipLaunchKernelGGL((k_lut_linear<8, true>), grid, dim3(512), 0, s, packed, scales, act_q, act_scale, (int)M, N, K,
                        cf, out);
   else
-    hipLaunchKernelGGL((k_lut_linear<4, false>), grid, dim3(256), 0, s, packed, scales, act_q, act_scale, act_sum, (int)M, N, K,
+    hipLaunchKernelGGL((k_lut_linear<4, false>), grid, dim3(256), 0, s, packed, scales, act_q, act_scale, (int)M, N, K,
                        cf, out);
   return hipGetLastError();
 }

@@ -119,6 +119,14 @@ __device__ __forceinline__ v4i combine_planes(const v4i& a03, const v4i& a1, con
   return d;
 }
 
+// Sum of the 16 signed bytes of a 16-byte group of activation codes (four dot products with 1).
+__device__ __forceinline__ int sum16_i8(const uint4& b, int acc) {
+  acc = __builtin_amdgcn_sdot4((int)b.x, 0x01010101, acc, false);
+  acc = __builtin_amdgcn_sdot4((int)b.y, 0x01010101, acc, false);
+  acc = __builtin_amdgcn_sdot4((int)b.z, 0x01010101, acc, false);
+  return __builtin_amdgcn_sdot4((int)b.w, 0x01010101, acc, false);
+}
+
 template <int FMT>
 __device__ __forceinline__ int finish_acc(int D, int sum_q) {
   if constexpr (FMT == FMT_MNZ) return 2 * D - 3 * sum_q;

@@ -33,13 +33,28 @@ __host__ __device__ constexpr int kperm(int n) {
 }
 
 // act_q int8 [M][K] -> FP6 E2M3 codes [M][K / 32][24 bytes], element n of group G = code of
-// k = 32 G + kperm(n).  One thread per group.
+// k = 32 G + kperm(n).  One thread per group.  With psum (non-null), workgroup x also writes the sum
+// of the codes of its 256 groups of token m to psum[m * gridDim.x + x].
 __global__ __launch_bounds__(256) void k_act_fp6(const int8_t* __restrict__ act_q, int M, int K,
-                                                 uint8_t* __restrict__ act6) {
+                                                 uint8_t* __restrict__ act6, int32_t* __restrict__ psum) {
+  __shared__ int red[4];
   const int groups = K >> 5;
   const int G = blockIdx.x * 256 + threadIdx.x;
-  if (G >= groups) return;
+  const bool valid = G < groups;
   for (int m = blockIdx.y; m < M; m += gridDim.y) {
+    if (psum) {   // uniform over the workgroup: every thread takes part in the reduction
+      int sq = 0;
+      if (valid) {
+        const uint4* src = reinterpret_cast<const uint4*>(act_q + (int64_t)m * K + 32 * G);
+        sq = sum16_i8(src[1], sum16_i8(src[0], 0));
+      }
+      sq = dev::wave_sum(sq);
+      if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sq;
+      __syncthreads();
+      if (threadIdx.x == 0) psum[(int64_t)m * gridDim.x + blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+      __syncthreads();
+    }
+    if (!valid) continue;
     const uint4* src = reinterpret_cast<const uint4*>(act_q + (int64_t)m * K + 32 * G);
     const uint4 lo = src[0], hi = src[1];
     const uint32_t wq[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
@@ -74,6 +89,7 @@ template <int OCC>
 __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                       int N, int K, const uint8_t* __restrict__ act6,
                                                       const float* __restrict__ sx, const int32_t* __restrict__ asum,
+                                                      const int32_t* __restrict__ psum, int npsum,
                                                       int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
   constexpr int BM = 64, BK = 256;
   __shared__ __align__(16) uint8_t lds0[BM * 256];
@@ -182,7 +198,12 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict
     const int m = m_base + 16 * t + r16;
     if (m < M) {
       const float s_x = sx[m];
-      const int sq = asum[m];
+      int sq = 0;
+      if (asum) {
+        sq = asum[m];
+      } else {
+        for (int p = 0; p < npsum; ++p) sq += psum[(int64_t)m * npsum + p];
+      }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         // 2 D = sum c q exactly (an integer below 2^24)
@@ -196,20 +217,26 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict
 
 }  // namespace
 
-size_t gemm_f4_workspace(int64_t M, int64_t K) { return (size_t)M * (size_t)(3 * (K / 4)); }
+// workgroups of the FP6 re-coding per token (256 groups of 32 k each)
+inline int64_t act_fp6_blocks(int64_t K) { return (K / 32 + 255) / 256; }
+
+// FP6 codes (M 3K/4 bytes, a multiple of 16), then the per-workgroup code sums int32 [M][blocks]
+size_t gemm_f4_workspace(int64_t M, int64_t K) {
+  return (size_t)M * (size_t)(3 * (K / 4)) + (size_t)M * (size_t)act_fp6_blocks(K) * 4;
+}
 
 hipError_t launch_gemm_f4(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act_q,
                           const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
                           hipStream_t s) {
   uint8_t* act6 = static_cast<uint8_t*>(ws);
-  const int groups = (int)(K / 32);
+  int32_t* psum = asum ? nullptr : reinterpret_cast<int32_t*>(act6 + (size_t)M * (size_t)(3 * (K / 4)));
+  const int gx = (int)act_fp6_blocks(K);
   const unsigned gy = (unsigned)(M < 65535 ? M : 65535);
-  hipLaunchKernelGGL(k_act_fp6, dim3((unsigned)((groups + 255) / 256), gy), dim3(256), 0, s, act_q, (int)M, (int)K,
-                     act6);
+  hipLaunchKernelGGL(k_act_fp6, dim3((unsigned)gx, gy), dim3(256), 0, s, act_q, (int)M, (int)K, act6, psum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_gemm_f4<3>), dim3((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64)), dim3(256), 0, s, P,
-                     sw, (int)N, (int)K, act6, sx, asum, (int)M, y, acc_out);
+                     sw, (int)N, (int)K, act6, sx, asum, psum, gx, (int)M, y, acc_out);
   return hipGetLastError();
 }
 

@@ -26,6 +26,7 @@ LAYOUT_V1 = 1
 STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR_SPEC",
           -4: "QIFT_ERR_FORMAT", -5: "QIFT_ERR_CODE", -6: "QIFT_ERR_ALIGN", -7: "QIFT_ERR_HIP",
           -8: "QIFT_ERR_WORKSPACE"}
+DEVERR_GROUP_WAIT, DEVERR_CHAIN_WAIT = 1, 2   # bits of the device error word (qift_device_error)
 
 # every symbol declared in include/qift.h
 EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_kv4_quant",
@@ -33,7 +34,7 @@ EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_w
            "qift_rotate_quant_act_bf16",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w2a4_lut_linear", "qift_w4a4_linear", "qift_w4a4_linear_ex",
            "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
-           "qift_last_hip_error", "qift_version")
+           "qift_last_hip_error", "qift_device_error", "qift_set_wait_limit", "qift_version")
 
 
 class QiftError(RuntimeError):
@@ -50,8 +51,16 @@ class PackedW(ctypes.Structure):
 
 
 class HadamardSpec(ctypes.Structure):
-    _fields_ = [("K", ctypes.c_int64), ("block", ctypes.c_int32), ("clip_num", ctypes.c_int32),
-                ("clip_den", ctypes.c_int32)]
+    _fields_ = [("K", ctypes.c_int64), ("block", ctypes.c_int32), ("flags", ctypes.c_int32)]
+
+
+def clip_flags(num: int, den: int) -> int:
+    """The spec flags of clip ratio num/den (QIFT_CLIP; 0 for the plain absmax/7 scale)."""
+    return 0 if (num, den) == (1, 1) else ((int(num) & 0xFF) << 8) | (int(den) & 0xFF)
+
+
+def spec(K: int, block: int, clip=(1, 1)) -> HadamardSpec:
+    return HadamardSpec(K, block, clip_flags(*clip))
 
 
 _lib = None
@@ -69,8 +78,8 @@ def lib():
     pw = ctypes.POINTER(PackedW)
     sig = {
         "qift_packed_bytes": (sz, [i32, i64, i64]),
-        "qift_pack_w2": (ctypes.c_int, [vp, vp, i64, i64, i32, vp, pw, vp, vp]),
-        "qift_pack_w4": (ctypes.c_int, [vp, vp, i64, i64, vp, pw, vp, vp]),
+        "qift_pack_w2": (ctypes.c_int, [vp, vp, i64, i64, i32, vp, pw, vp]),
+        "qift_pack_w4": (ctypes.c_int, [vp, vp, i64, i64, vp, pw, vp]),
         "qift_quantize_weights": (ctypes.c_int, [vp, i64, HadamardSpec, i32, vp, vp, vp]),
         "qift_kv4_quant": (ctypes.c_int, [vp, i64, i32, vp, vp, vp, vp]),
         "qift_kv4_attention_workspace_bytes": (sz, [i64, i32, i32, i32, i64]),
@@ -78,16 +87,18 @@ def lib():
                                                      vp]),
         "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_rotate_quant_act_bf16": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
-        "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
-        "qift_w2a4_lut_linear": (ctypes.c_int, [pw, vp, vp, vp, vp, i64, vp, vp]),
+        "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, i64, vp, vp]),
+        "qift_w2a4_lut_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
         "qift_w2a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
-        "qift_w4a4_linear": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp]),
+        "qift_w4a4_linear": (ctypes.c_int, [pw, vp, vp, i64, vp, vp]),
         "qift_w4a4_linear_ex": (ctypes.c_int, [pw, vp, vp, vp, i64, vp, vp, vp, sz, vp]),
         "qift_rotate_quant_linear": (ctypes.c_int, [pw, vp, i64, HadamardSpec, vp, vp, vp, vp, vp, vp]),
         "qift_hbm_read_probe": (ctypes.c_int, [vp, sz, vp, vp]),
         "qift_workspace_bytes": (sz, [pw, i64]),
         "qift_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "qift_last_hip_error": (ctypes.c_int, []),
+        "qift_device_error": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint32), i32, vp]),
+        "qift_set_wait_limit": (ctypes.c_int, [i32]),
         "qift_version": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -153,58 +164,41 @@ def workspace_bytes(w: Packed, M: int) -> int:
 
 
 def pack_w2(levels: torch.Tensor, scales: torch.Tensor, fmt: int = W2_MNZ, out: torch.Tensor | None = None,
-            invalid_count: torch.Tensor | None = None, check: bool = True, stream=None) -> Packed:
+            stream=None) -> Packed:
     """Pack int8 levels [N, K] ({-3,-1,1,3} MNZ or {-4,-1,1,4} PoT; for W2_LUT the codes 0..3) into
-    QW2v1 words.
-
-    With ``check`` (default) a device counter of out-of-set levels is read back
-    after the stream completes and a ValueError is raised when it is non-zero.
-    """
+    QW2v1 words.  The call validates every level and synchronizes the stream; a level outside the
+    set raises QiftError with status QIFT_ERR_CODE."""
     N, K = levels.shape
     _dev(levels, torch.int8, (N, K), "levels")
     _dev(scales, torch.float16, (N,), "scales")
     if out is None:
         out = torch.empty((N, K // 16), dtype=torch.int32, device=levels.device)
     _dev(out, torch.int32, (N, K // 16), "out")
-    if check and invalid_count is None:
-        invalid_count = torch.empty(1, dtype=torch.int32, device=levels.device)
-    st = lib().qift_pack_w2(levels.data_ptr(), scales.data_ptr(), N, K, fmt, out.data_ptr(), None,
-                            _ptr(invalid_count), _stream(stream))
+    st = lib().qift_pack_w2(levels.data_ptr(), scales.data_ptr(), N, K, fmt, out.data_ptr(), None, _stream(stream))
     _check("qift_pack_w2", st)
-    if check:
-        bad = int(invalid_count.item())
-        if bad:
-            raise ValueError(f"qift_pack_w2: {bad} levels outside the level set (QIFT_ERR_CODE)")
     return Packed(fmt, N, K, out, scales)
 
 
-def pack_w4(levels: torch.Tensor, scales: torch.Tensor, out: torch.Tensor | None = None,
-            invalid_count: torch.Tensor | None = None, check: bool = True, stream=None) -> Packed:
-    """Pack int8 W4 levels [N, K] in -7..7 into QW4v1 words."""
+def pack_w4(levels: torch.Tensor, scales: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> Packed:
+    """Pack int8 W4 levels [N, K] in -7..7 into QW4v1 words (validated like pack_w2)."""
     N, K = levels.shape
     _dev(levels, torch.int8, (N, K), "levels")
     _dev(scales, torch.float16, (N,), "scales")
     if out is None:
         out = torch.empty((N, K // 8), dtype=torch.int32, device=levels.device)
     _dev(out, torch.int32, (N, K // 8), "out")
-    if check and invalid_count is None:
-        invalid_count = torch.empty(1, dtype=torch.int32, device=levels.device)
-    st = lib().qift_pack_w4(levels.data_ptr(), scales.data_ptr(), N, K, out.data_ptr(), None,
-                            _ptr(invalid_count), _stream(stream))
+    st = lib().qift_pack_w4(levels.data_ptr(), scales.data_ptr(), N, K, out.data_ptr(), None, _stream(stream))
     _check("qift_pack_w4", st)
-    if check:
-        bad = int(invalid_count.item())
-        if bad:
-            raise ValueError(f"qift_pack_w4: {bad} levels outside -7..7 (QIFT_ERR_CODE)")
     return Packed(W4_SYM, N, K, out, scales)
 
 
 @dataclass
 class QAct:
-    """Quantized activations of M tokens: the triple every linear consumes."""
-    q: torch.Tensor       # int8 [M, K]
-    scale: torch.Tensor   # fp32 [M]
-    sum: torch.Tensor     # int32 [M]
+    """Quantized activations of M tokens: the codes and scales every linear consumes, and the per-token
+    code sums (written by rotate_quant_act when present; the linears compute their own)."""
+    q: torch.Tensor                 # int8 [M, K]
+    scale: torch.Tensor             # fp32 [M]
+    sum: torch.Tensor | None = None  # int32 [M]
 
     @property
     def M(self):
@@ -229,7 +223,7 @@ def quantize_weights(W: torch.Tensor, block: int, fmt: int, levels: torch.Tensor
         scales = torch.empty(N, dtype=torch.float16, device=W.device)
     _dev(levels, torch.int8, (N, K), "levels")
     _dev(scales, torch.float16, (N,), "scales")
-    st = lib().qift_quantize_weights(W.data_ptr(), N, HadamardSpec(K, block, 1, 1), int(fmt), levels.data_ptr(),
+    st = lib().qift_quantize_weights(W.data_ptr(), N, spec(K, block), int(fmt), levels.data_ptr(),
                                      scales.data_ptr(), _stream(stream))
     _check("qift_quantize_weights", st)
     return levels, scales
@@ -304,21 +298,23 @@ def rotate_quant_act(x: torch.Tensor, block: int, clip=(1, 1), out: QAct | None 
         out = alloc_act(M, K, x.device)
     _dev(out.q, torch.int8, (M, K), "act_q")
     _dev(out.scale, torch.float32, (M,), "act_scale")
-    _dev(out.sum, torch.int32, (M,), "act_sum")
-    spec = HadamardSpec(K, block, int(clip[0]), int(clip[1]))
+    if out.sum is not None:
+        _dev(out.sum, torch.int32, (M,), "act_sum")
     name = "qift_rotate_quant_act_bf16" if bf16 else "qift_rotate_quant_act"
-    st = getattr(lib(), name)(x.data_ptr(), M, spec, out.q.data_ptr(), out.scale.data_ptr(), out.sum.data_ptr(),
-                              _stream(stream))
+    st = getattr(lib(), name)(x.data_ptr(), M, spec(K, block, clip), out.q.data_ptr(), out.scale.data_ptr(),
+                              _ptr(out.sum), _stream(stream))
     _check(name, st)
     return out
 
 
-def _linear(name: str, w: Packed, act: QAct, out, acc_out, workspace, stream):
+def _linear(name: str, w: Packed, act: QAct, out, acc_out, workspace, use_sum, stream):
     M, K = act.q.shape
     if K != w.K:
         raise ValueError(f"activation width {K} != weight K {w.K}")
     _dev(act.scale, torch.float32, (M,), "act_scale")
-    _dev(act.sum, torch.int32, (M,), "act_sum")
+    act_sum = act.sum if use_sum else None
+    if use_sum:
+        _dev(act_sum, torch.int32, (M,), "act_sum")
     if out is None:
         out = torch.empty((M, w.N), dtype=torch.float16, device=act.q.device)
     _dev(out, torch.float16, (M, w.N), "out")
@@ -328,21 +324,23 @@ def _linear(name: str, w: Packed, act: QAct, out, acc_out, workspace, stream):
     L = lib()
     if workspace is not None:
         _dev(workspace, torch.uint8, (workspace.numel(),), "workspace")
-    if acc_out is None and workspace is None:
-        st = getattr(L, name)(ctypes.byref(v), act.q.data_ptr(), act.scale.data_ptr(), act.sum.data_ptr(),
-                              M, out.data_ptr(), _stream(stream))
+    if acc_out is None and workspace is None and act_sum is None:
+        st = getattr(L, name)(ctypes.byref(v), act.q.data_ptr(), act.scale.data_ptr(), M, out.data_ptr(),
+                              _stream(stream))
     else:
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         st = getattr(L, name + "_ex")(ctypes.byref(v), act.q.data_ptr(), act.scale.data_ptr(),
-                                      act.sum.data_ptr(), M, out.data_ptr(), _ptr(acc_out),
+                                      _ptr(act_sum), M, out.data_ptr(), _ptr(acc_out),
                                       _ptr(workspace), ws_bytes, _stream(stream))
     _check(name, st)
     return out
 
 
-def w2a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:
-    """fp16 y [M, N] of the 2-bit quantized linear (MNZ or PoT weights)."""
-    return _linear("qift_w2a4_linear", w, act, out, acc_out, workspace, stream)
+def w2a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, use_sum=False,
+                stream=None) -> torch.Tensor:
+    """fp16 y [M, N] of the 2-bit quantized linear (MNZ or PoT weights).  With acc_out, workspace or
+    use_sum (pass act.sum as the precomputed code sums) the call goes through qift_w2a4_linear_ex."""
+    return _linear("qift_w2a4_linear", w, act, out, acc_out, workspace, use_sum, stream)
 
 
 def w2a4_lut_linear(w: Packed, lut, act: QAct, out=None, stream=None) -> torch.Tensor:
@@ -352,7 +350,6 @@ def w2a4_lut_linear(w: Packed, lut, act: QAct, out=None, stream=None) -> torch.T
     if K != w.K:
         raise ValueError(f"activation width {K} != weight K {w.K}")
     _dev(act.scale, torch.float32, (M,), "act_scale")
-    _dev(act.sum, torch.int32, (M,), "act_sum")
     if out is None:
         out = torch.empty((M, w.N), dtype=torch.float16, device=act.q.device)
     _dev(out, torch.float16, (M, w.N), "out")
@@ -361,21 +358,22 @@ def w2a4_lut_linear(w: Packed, lut, act: QAct, out=None, stream=None) -> torch.T
         raise ValueError("lut must hold four levels")
     table = (ctypes.c_uint16 * 4)(*[int(b) & 0xFFFF for b in bits.tolist()])
     v = w.cview()
-    st = lib().qift_w2a4_lut_linear(ctypes.byref(v), table, act.q.data_ptr(), act.scale.data_ptr(),
-                                    act.sum.data_ptr(), M, out.data_ptr(), _stream(stream))
+    st = lib().qift_w2a4_lut_linear(ctypes.byref(v), table, act.q.data_ptr(), act.scale.data_ptr(), M,
+                                    out.data_ptr(), _stream(stream))
     _check("qift_w2a4_lut_linear", st)
     return out
 
 
-def w4a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:
+def w4a4_linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, use_sum=False,
+                stream=None) -> torch.Tensor:
     """fp16 y [M, N] of the W4 sibling."""
-    return _linear("qift_w4a4_linear", w, act, out, acc_out, workspace, stream)
+    return _linear("qift_w4a4_linear", w, act, out, acc_out, workspace, use_sum, stream)
 
 
-def linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, stream=None) -> torch.Tensor:
+def linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, use_sum=False, stream=None) -> torch.Tensor:
     """Dispatch on the weight format."""
     f = w4a4_linear if w.fmt == W4_SYM else w2a4_linear
-    return f(w, act, out=out, acc_out=acc_out, workspace=workspace, stream=stream)
+    return f(w, act, out=out, acc_out=acc_out, workspace=workspace, use_sum=use_sum, stream=stream)
 
 
 def rotate_quant_linear(w: Packed, x: torch.Tensor, block: int, clip=(1, 1), out=None, acc_out=None,
@@ -395,9 +393,8 @@ def rotate_quant_linear(w: Packed, x: torch.Tensor, block: int, clip=(1, 1), out
         _dev(act_out.scale, torch.float32, (M,), "act_scale")
         _dev(act_out.sum, torch.int32, (M,), "act_sum")
     v = w.cview()
-    spec = HadamardSpec(K, block, int(clip[0]), int(clip[1]))
     st = lib().qift_rotate_quant_linear(
-        ctypes.byref(v), x.data_ptr(), M, spec, out.data_ptr(), _ptr(acc_out),
+        ctypes.byref(v), x.data_ptr(), M, spec(K, block, clip), out.data_ptr(), _ptr(acc_out),
         None if act_out is None else act_out.q.data_ptr(), None if act_out is None else act_out.scale.data_ptr(),
         None if act_out is None else act_out.sum.data_ptr(), _stream(stream))
     _check("qift_rotate_quant_linear", st)
@@ -422,6 +419,19 @@ def hbm_read_probe(buf: torch.Tensor, partials: torch.Tensor, stream=None) -> to
     _check("qift_hbm_read_probe", lib().qift_hbm_read_probe(buf.data_ptr(), nbytes, partials.data_ptr(),
                                                             _stream(stream)))
     return partials
+
+
+def device_error(clear: bool = True, stream=None) -> int:
+    """Synchronize the stream and return the device error word (DEVERR_* bits; 0 when every bounded
+    wait of the kernels since the last clear ended normally); clear it by default."""
+    bits = ctypes.c_uint32(0)
+    _check("qift_device_error", lib().qift_device_error(ctypes.byref(bits), 1 if clear else 0, _stream(stream)))
+    return int(bits.value)
+
+
+def set_wait_limit(spins: int) -> None:
+    """Test hook: spin limit of the in-workgroup wave barriers for later launches (0: the default)."""
+    _check("qift_set_wait_limit", lib().qift_set_wait_limit(int(spins)))
 
 
 def version() -> str:

@@ -15,7 +15,7 @@ from paper_2606_02823_amd import qift
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "qift.h")
 
-OK, E_NULL, E_SHAPE, E_SPEC, E_FORMAT, E_ALIGN, E_WS = 0, -1, -2, -3, -4, -6, -8
+OK, E_NULL, E_SHAPE, E_SPEC, E_FORMAT, E_CODE, E_ALIGN, E_WS = 0, -1, -2, -3, -4, -5, -6, -8
 A = 0x10000       # a 16-byte aligned fake device address (never dereferenced)
 MIS = 0x10008     # an 8-byte aligned, not 16-byte aligned fake address
 
@@ -35,7 +35,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 20
+    assert len(names) == 22
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -57,8 +57,18 @@ def test_packed_bytes(L):
     assert qift.packed_bytes(qift.W2_MNZ, 0, 4096) == 0
 
 
-def _spec(K=256, block=256, num=1, den=1):
-    return qift.HadamardSpec(K, block, num, den)
+def _spec(K=256, block=256, num=1, den=1, flags=None):
+    return qift.HadamardSpec(K, block, qift.clip_flags(num, den) if flags is None else flags)
+
+
+def test_spec_layout_and_clip_flags():
+    # the boundary's spec is {int64 K; int32 block; int32 flags}: 16 bytes, flags 0 = clip 1
+    assert ctypes.sizeof(qift.HadamardSpec) == 16
+    assert qift.HadamardSpec.flags.offset == 12
+    assert qift.clip_flags(1, 1) == 0
+    assert qift.clip_flags(9, 10) == (9 << 8) | 10
+    text = open(HEADER).read()
+    assert "#define QIFT_CLIP(num, den) ((int32_t)((((num) & 0xFF) << 8) | ((den) & 0xFF)))" in text
 
 
 def test_quantize_weights_validation(L):
@@ -76,6 +86,7 @@ def test_quantize_weights_validation(L):
     assert f(A, 8, _spec(K=8192, block=8192), mnz, A, A, None) == E_SPEC    # block above 4096
     assert f(A, 8, _spec(K=192, block=128), mnz, A, A, None) == E_SPEC      # block does not divide K
     assert f(A, 8, _spec(num=9, den=10), w4, A, A, None) == E_SPEC          # no clip on weights
+    assert f(A, 8, _spec(flags=1 << 16), mnz, A, A, None) == E_SPEC
     assert f(MIS, 8, _spec(), mnz, A, A, None) == E_ALIGN
     assert f(A, 8, _spec(), mnz, MIS, A, None) == E_ALIGN
 
@@ -107,7 +118,8 @@ def test_kv4_validation(L):
 def test_rotate_quant_act_validation(L, entry):
     f = getattr(L, entry)
     assert f(None, 4, _spec(), A, A, A, None) == E_NULL
-    assert f(A, 4, _spec(), A, A, None, None) == E_NULL
+    assert f(A, 4, _spec(), None, A, A, None) == E_NULL
+    assert f(A, 4, _spec(), A, None, None, None) == E_NULL      # act_sum is optional, act_scale is not
     assert f(A, 0, _spec(), A, A, A, None) == E_SHAPE
     assert f(A, 4, _spec(K=100, block=4), A, A, A, None) == E_SHAPE
     assert f(A, 4, _spec(K=65536, block=4096), A, A, A, None) == E_SHAPE
@@ -118,8 +130,10 @@ def test_rotate_quant_act_validation(L, entry):
     assert f(A, 4, _spec(num=0, den=1), A, A, A, None) == E_SPEC
     assert f(A, 4, _spec(num=3, den=2), A, A, A, None) == E_SPEC
     assert f(A, 4, _spec(num=9, den=17), A, A, A, None) == E_SPEC
+    assert f(A, 4, _spec(flags=0x10101), A, A, A, None) == E_SPEC          # bits above the clip fields
     assert f(MIS, 4, _spec(), A, A, A, None) == E_ALIGN
     assert f(A, 4, _spec(), A, A, MIS, None) == E_ALIGN
+    assert f(MIS, 4, _spec(), A, A, None, None) == E_ALIGN
 
 
 def _pw(fmt=qift.W2_MNZ, N=512, K=256, packed=A, scales=A, layout=1):
@@ -130,29 +144,41 @@ def test_linear_validation(L):
     w2 = L.qift_w2a4_linear
     w4 = L.qift_w4a4_linear
     w2x = L.qift_w2a4_linear_ex
+    w4x = L.qift_w4a4_linear_ex
     P = ctypes.byref
-    assert w2(None, A, A, A, 4, A, None) == E_NULL
-    assert w2(P(_pw()), None, A, A, 4, A, None) == E_NULL
-    assert w2(P(_pw()), A, A, None, 4, A, None) == E_NULL
-    assert w2(P(_pw(packed=None)), A, A, A, 4, A, None) == E_NULL
-    assert w2(P(_pw(fmt=qift.W4_SYM)), A, A, A, 4, A, None) == E_FORMAT
-    assert w4(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 4, A, None) == E_FORMAT
-    assert w2(P(_pw(layout=2)), A, A, A, 4, A, None) == E_FORMAT
-    assert w2(P(_pw(K=100)), A, A, A, 4, A, None) == E_SHAPE
-    assert w2(P(_pw(N=0)), A, A, A, 4, A, None) == E_SHAPE
-    assert w2(P(_pw()), A, A, A, 0, A, None) == E_SHAPE
-    assert w2(P(_pw(packed=MIS)), A, A, A, 4, A, None) == E_ALIGN
-    assert w2(P(_pw()), A, A, A, 4, MIS, None) == E_ALIGN
+    # the base calls follow the boundary's w2a4_linear(packed_w, act_q, act_scale, out): no code sums
+    assert w2(None, A, A, 4, A, None) == E_NULL
+    assert w2(P(_pw()), None, A, 4, A, None) == E_NULL
+    assert w2(P(_pw()), A, None, 4, A, None) == E_NULL
+    assert w2(P(_pw()), A, A, 4, None, None) == E_NULL
+    assert w2(P(_pw(packed=None)), A, A, 4, A, None) == E_NULL
+    assert w2(P(_pw(scales=None)), A, A, 4, A, None) == E_NULL
+    assert w2(P(_pw(fmt=qift.W4_SYM)), A, A, 4, A, None) == E_FORMAT
+    assert w4(P(_pw(fmt=qift.W2_MNZ)), A, A, 4, A, None) == E_FORMAT
+    assert w2(P(_pw(layout=2)), A, A, 4, A, None) == E_FORMAT
+    assert w2(P(_pw(K=100)), A, A, 4, A, None) == E_SHAPE
+    assert w2(P(_pw(N=0)), A, A, 4, A, None) == E_SHAPE
+    assert w2(P(_pw()), A, A, 0, A, None) == E_SHAPE
+    assert w2(P(_pw(packed=MIS)), A, A, 4, A, None) == E_ALIGN
+    assert w2(P(_pw()), A, A, 4, MIS, None) == E_ALIGN
+    assert w4(P(_pw(fmt=qift.W4_SYM)), MIS, A, 4, A, None) == E_ALIGN
+    # _ex: the code sums are optional (NULL: summed in the kernel) and checked for alignment when given
+    assert w2x(P(_pw()), A, A, MIS, 4, A, None, None, 0, None) == E_ALIGN
+    assert w2x(P(_pw()), A, A, None, 4, A, MIS, None, 0, None) == E_ALIGN
     assert w2x(P(_pw()), A, A, A, 4, A, MIS, None, 0, None) == E_ALIGN
-    assert w2x(P(_pw()), A, A, A, 4, A, None, None, 64, None) == E_WS
+    assert w2x(P(_pw()), A, A, None, 4, A, None, None, 64, None) == E_WS
+    assert w2x(P(_pw()), None, A, None, 4, A, None, None, 0, None) == E_NULL
+    assert w4x(P(_pw(fmt=qift.W2_MNZ)), A, A, None, 4, A, None, None, 0, None) == E_FORMAT
     assert L.qift_workspace_bytes(P(_pw()), 4) == 0
     # the workspace that selects the FP4 x FP6 prefill kernel: MNZ at M > 64, M * 3K/4 bytes
     K = _pw().K
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 64) == 0
-    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 65) == 65 * 3 * (K // 4)
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 65) == 65 * 3 * (K // 4) + 65 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT)), 65) == 0
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM)), 65) == 0
-    need = 100 * 3 * (K // 4)
+    # FP6 codes (M 3K/4 bytes), then one int32 code sum per token and 256 groups of 32 k
+    need = 100 * 3 * (K // 4) + 100 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 100) == need
     assert w2x(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 100, A, None, A, need - 16, None) == E_WS
     assert w2x(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 100, A, None, None, need, None) == E_WS
     assert w2x(P(_pw(fmt=qift.W2_MNZ)), A, A, A, 100, A, None, MIS, need, None) == E_ALIGN
@@ -169,6 +195,7 @@ def test_fused_validation(L):
     assert f(P(_pw(K=32768)), A, 1, _spec(K=32768, block=4096), A, None, None, None, None, None) == E_SHAPE
     assert f(P(_pw()), A, 1, _spec(K=512, block=256), A, None, None, None, None, None) == E_SPEC
     assert f(P(_pw(K=8192)), A, 1, _spec(K=8192, block=8192), A, None, None, None, None, None) == E_SPEC
+    assert f(P(_pw()), A, 1, _spec(K=256, block=256, num=17, den=18), A, None, None, None, None, None) == E_SPEC
     assert f(P(_pw()), MIS, 1, sp, A, None, None, None, None, None) == E_ALIGN
 
 
@@ -184,15 +211,26 @@ def test_read_probe_validation(L):
 
 
 def test_pack_validation(L):
+    # the boundary's pack_w2(codes, scales, N, K, fmt, packed, out, stream); out-of-set levels are
+    # QIFT_ERR_CODE (the call synchronizes to read them back), covered on the GPU
     f2, f4 = L.qift_pack_w2, L.qift_pack_w4
-    assert f2(None, A, 512, 256, 0, A, None, None, None) == E_NULL
-    assert f2(A, A, 512, 256, qift.W4_SYM, A, None, None, None) == E_FORMAT
-    assert f2(A, A, 512, 100, 0, A, None, None, None) == E_SHAPE
-    assert f2(A, A, 0, 256, 0, A, None, None, None) == E_SHAPE
-    assert f2(MIS, A, 512, 256, 0, A, None, None, None) == E_ALIGN
-    assert f2(A, A, 512, 256, 0, A, None, 0x10002, None) == E_ALIGN
-    assert f4(A, A, 512, 256, None, None, None, None) == E_NULL
-    assert f4(A, A, 512, 96, A, None, None, None) == E_SHAPE
+    assert f2(None, A, 512, 256, 0, A, None, None) == E_NULL
+    assert f2(A, A, 512, 256, 0, None, None, None) == E_NULL
+    assert f2(A, A, 512, 256, qift.W4_SYM, A, None, None) == E_FORMAT
+    assert f2(A, A, 512, 100, 0, A, None, None) == E_SHAPE
+    assert f2(A, A, 0, 256, 0, A, None, None) == E_SHAPE
+    assert f2(MIS, A, 512, 256, 0, A, None, None) == E_ALIGN
+    assert f2(A, MIS, 512, 256, 0, A, None, None) == E_ALIGN
+    assert f4(A, A, 512, 256, None, None, None) == E_NULL
+    assert f4(A, A, 512, 96, A, None, None) == E_SHAPE
+    assert L.qift_status_string(E_CODE) == b"level outside the format's level set (nothing usable was packed)"
+
+
+def test_device_error_api_validation(L):
+    # host-side checks only: the read itself needs a GPU (covered by the GPU tests)
+    assert L.qift_device_error(None, 1, None) == E_NULL
+    assert L.qift_set_wait_limit(-1) == E_SHAPE
+    assert L.qift_set_wait_limit(0) == OK     # back to the default
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
@@ -209,16 +247,16 @@ def test_lut_linear_validation(L):
     good = half(-1.5104, -0.4528, 0.4528, 1.5104)
     lw = lambda **kw: _pw(fmt=qift.W2_LUT, K=kw.pop("K", 4096), **kw)
     assert L.qift_packed_bytes(qift.W2_LUT, 8, 4096) == 8 * 1024
-    assert f(None, good, A, A, A, 4, A, None) == E_NULL
-    assert f(P(lw()), None, A, A, A, 4, A, None) == E_NULL
-    assert f(P(lw()), good, A, A, None, 4, A, None) == E_NULL
-    assert f(P(_pw(fmt=qift.W2_MNZ, K=4096)), good, A, A, A, 4, A, None) == E_FORMAT   # integer formats: no table
-    assert f(P(lw(K=4160)), good, A, A, A, 4, A, None) == E_SHAPE                     # K not a multiple of 256
-    assert f(P(lw(K=16640)), good, A, A, A, 4, A, None) == E_SHAPE                    # K above 16384
-    assert f(P(lw()), good, A, A, A, 0, A, None) == E_SHAPE
-    assert f(P(lw()), half(0, 1, 2, 257), A, A, A, 4, A, None) == E_SPEC             # above 256
-    assert f(P(lw()), half(0, 1, 2, np.inf), A, A, A, 4, A, None) == E_SPEC
-    assert f(P(lw()), half(0, 1, np.nan, 2), A, A, A, 4, A, None) == E_SPEC
-    assert f(P(lw()), good, A, A, A, 4, MIS, None) == E_ALIGN
+    assert f(None, good, A, A, 4, A, None) == E_NULL
+    assert f(P(lw()), None, A, A, 4, A, None) == E_NULL
+    assert f(P(lw()), good, A, None, 4, A, None) == E_NULL
+    assert f(P(_pw(fmt=qift.W2_MNZ, K=4096)), good, A, A, 4, A, None) == E_FORMAT   # integer formats: no table
+    assert f(P(lw(K=4160)), good, A, A, 4, A, None) == E_SHAPE                     # K not a multiple of 256
+    assert f(P(lw(K=16640)), good, A, A, 4, A, None) == E_SHAPE                    # K above 16384
+    assert f(P(lw()), good, A, A, 0, A, None) == E_SHAPE
+    assert f(P(lw()), half(0, 1, 2, 257), A, A, 4, A, None) == E_SPEC             # above 256
+    assert f(P(lw()), half(0, 1, 2, np.inf), A, A, 4, A, None) == E_SPEC
+    assert f(P(lw()), half(0, 1, np.nan, 2), A, A, 4, A, None) == E_SPEC
+    assert f(P(lw()), good, A, A, 4, MIS, None) == E_ALIGN
     # the integer linears refuse the table format
-    assert L.qift_w2a4_linear(P(lw()), A, A, A, 4, A, None) == E_FORMAT
+    assert L.qift_w2a4_linear(P(lw()), A, A, 4, A, None) == E_FORMAT

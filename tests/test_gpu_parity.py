@@ -3,7 +3,9 @@
 Bit-exact: packed words, act_q, act_sum, act_scale, int32 accumulators and
 the fp16 output against the oracle's fp32 epilogue expression; within the
 max-abs-rel 1e-3 criterion against the oracle's fp64 epilogue.  Inputs come
-from the seeded generators; expected values only from ``oracle``.
+from the seeded generators; expected values only from ``oracle``.  The
+linears run with the per-token code sums computed in the kernels (the
+boundary's call takes none) unless a test passes the quantizer's sums.
 """
 import numpy as np
 import pytest
@@ -70,9 +72,9 @@ def check_linear(y, acc, L, q_ref, sx_ref, s_w, rows=None, tokens=None):
     assert olin.max_abs_rel(y, olin.epilogue_ref(acc_ref, sx_ref, s_w)) <= olin.TOL_REL
 
 
-def run_linear(Q, pk, act, M, N):
+def run_linear(Q, pk, act, M, N, use_sum=False, workspace=None):
     acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
-    y = Q.linear(pk, act, acc_out=acc)
+    y = Q.linear(pk, act, acc_out=acc, use_sum=use_sum, workspace=workspace)
     torch.cuda.synchronize()
     return y, acc
 
@@ -117,6 +119,13 @@ def test_linear_ragged(Q, fmt, M):
     q_ref, sx_ref = check_act(act, x, b)
     y, acc = run_linear(Q, pk, act, M, N)
     check_linear(y, acc, L, q_ref, sx_ref, s_w)
+    # the quantizer's sums passed in (qift_*_linear_ex) give the same results
+    y2, acc2 = run_linear(Q, pk, act, M, N, use_sum=True)
+    assert torch.equal(acc2, acc) and torch.equal(y2.view(torch.int16), y.view(torch.int16))
+    # and so does the boundary's call without accumulators or sums
+    y3 = Q.linear(pk, act)
+    torch.cuda.synchronize()
+    assert torch.equal(y3.view(torch.int16), y.view(torch.int16))
 
 
 @pytest.mark.parametrize("M,K", [(65, 1088), (130, 1088), (300, 4096), (200, 14336)])
@@ -130,12 +139,11 @@ def test_mnz_prefill_int8_and_fp4_paths(Q, M, K):
     pk = pack_dev(Q, L, s_w, fmt)
     act = Q.rotate_quant_act(dev(x), b)
     q_ref, sx_ref = check_act(act, x, b)
-    assert Q.workspace_bytes(pk, M) == M * 3 * (K // 4)
+    assert Q.workspace_bytes(pk, M) == M * 3 * (K // 4) + 4 * M * (-(-(K // 32) // 256))
     for ws in (None, torch.empty(Q.workspace_bytes(pk, M), dtype=torch.uint8, device="cuda")):
-        acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
-        y = Q.linear(pk, act, acc_out=acc, workspace=ws)
-        torch.cuda.synchronize()
-        check_linear(y, acc, L, q_ref, sx_ref, s_w)
+        for use_sum in (False, True):
+            y, acc = run_linear(Q, pk, act, M, N, use_sum=use_sum, workspace=ws)
+            check_linear(y, acc, L, q_ref, sx_ref, s_w)
 
 
 @pytest.mark.parametrize("fmt", FMTS)
@@ -176,20 +184,22 @@ def test_linear_extremes(Q, fmt):
 
 
 def test_pack_rejects_levels_outside_the_set(Q):
+    # the pack calls validate every level and return QIFT_ERR_CODE (status -5)
     L = np.full((16, 64), 1, dtype=np.int8)
     L[3, 7] = 0
     s = np.ones(16, dtype=np.float16)
-    with pytest.raises(ValueError, match="outside"):
-        Q.pack_w2(dev(L), dev(s), Q.W2_MNZ)
-    L[3, 7] = 3
-    with pytest.raises(ValueError, match="outside"):
-        Q.pack_w2(dev(L), dev(s), Q.W2_POT)
-    L[3, 7] = -8
-    with pytest.raises(ValueError, match="outside"):
-        Q.pack_w4(dev(L), dev(s))
-    # a clean call afterwards resets the counter
+    for fmt, bad in ((Q.W2_MNZ, 0), (Q.W2_MNZ, 2), (Q.W2_POT, 3), (Q.W2_LUT, 4), (Q.W4_SYM, -8), (Q.W4_SYM, 8)):
+        L[3, 7] = bad
+        with pytest.raises(Q.QiftError, match="QIFT_ERR_CODE") as e:
+            if fmt == Q.W4_SYM:
+                Q.pack_w4(dev(L), dev(s))
+            else:
+                Q.pack_w2(dev(L), dev(s), fmt)
+        assert e.value.status == -5
+    # a clean call afterwards starts from a zero count
     L[3, 7] = 1
     Q.pack_w2(dev(L), dev(s), Q.W2_MNZ)
+    Q.pack_w4(dev(L), dev(s))
 
 
 # ----------------------------------------------------------------------------- activation quantizer
