@@ -311,6 +311,79 @@ int qift_rotate_quant_linear(const qift_packed_w *w, const uint16_t *x, int64_t 
                              int32_t *act_sum, qift_stream_t stream);
 
 /*
+ * Decode chain: a whole decode step of a layer stack (Sec. 1: at decode the step streams every
+ * quantized weight once per token) as ONE launch of a persistent kernel.  Each link is the fused
+ * rotate + quantize + linear of qift_rotate_quant_linear (Sec. 3.1 rotation and per-token INT4
+ * quantizer, Sec. 3.3 / 3.6 integer dot product, scales in the epilogue) whose input is either the
+ * chain input x or a slice of an earlier link's output; the kernel honours those dependencies
+ * with per-link arrival counters in the workspace, while the weight stream of the next link runs
+ * ahead of them.  Results are bit-identical to calling qift_rotate_quant_linear link by link.
+ *
+ *   qift_chain_link   (host) one linear:
+ *     w          the weights (fmt MNZ, PoT or W4; one format for the whole chain).
+ *     block      Hadamard block of the link's input (power of two, 2..4096, dividing w.K).
+ *     flags      clip flags of the input's quantizer, as qift_hadamard_spec.flags.
+ *     in_link    index of the link whose output is this link's input (lower than this link's
+ *                index), or -1 for the chain input x (then w.K must equal the chain's K0).
+ *     in_offset  first element taken from each token's row of that output: the input is
+ *                elements [in_offset, in_offset + w.K) (a multiple of 8; 0 for the chain input).
+ *     out        device, out: fp16 y [M][w.N]; the outputs of all links must be disjoint.
+ *     acc_out    device, out, nullable: int32 [M][w.N] accumulators.
+ *   qift_chain        (host) the prepared chain, filled by qift_chain_prepare: a view of the
+ *                workspace plus the launch geometry.  The caller keeps the workspace alive, and
+ *                the weights and output buffers the links name, while it uses the chain.
+ */
+typedef struct {
+  qift_packed_w w;
+  int32_t block;
+  int32_t flags;
+  int32_t in_link;
+  int32_t reserved;          /* 0 */
+  int64_t in_offset;
+  uint16_t *out;
+  int32_t *acc_out;
+} qift_chain_link;
+
+typedef struct {
+  int32_t fmt, n_links;
+  int32_t M, K0;             /* tokens per call, width of the chain input */
+  int32_t grid, kmax;        /* workgroups (one per CU), largest K of the links */
+  int32_t any_long, reserved;
+  const void *table;         /* device: the link table (in the workspace) */
+  uint32_t *counters;        /* device: n_links + 1 arrival counters (in the workspace) */
+} qift_chain;
+
+/* Workspace bytes of a chain of n_links links (0 for n_links outside 1..4096). */
+size_t qift_chain_workspace_bytes(int32_t n_links);
+
+/*
+ * Validate the links, write the link table and zeroed counters into the workspace and fill
+ * *chain.  An offline call: it SYNCHRONIZES the stream (the table is copied from host memory);
+ * not capturable in a HIP graph.
+ *   links      host: n_links links (1 <= n_links <= 4096).
+ *   M          tokens per call, 1..4.
+ *   K0         width of the chain input x.
+ *   workspace  device, 16-byte aligned, at least qift_chain_workspace_bytes(n_links) bytes.
+ *   chain      host, out.
+ * Errors: QIFT_ERR_NULL, QIFT_ERR_FORMAT (mixed or unknown formats), QIFT_ERR_SHAPE (K above
+ * 16384, an input slice past the producer's row, overlapping outputs, M outside 1..4, or LDS
+ * beyond 160 KiB), QIFT_ERR_SPEC (block or flags), QIFT_ERR_ALIGN, QIFT_ERR_WORKSPACE.
+ */
+int qift_chain_prepare(const qift_chain_link *links, int32_t n_links, int64_t M, int64_t K0, void *workspace,
+                       size_t workspace_bytes, qift_chain *chain, qift_stream_t stream);
+
+/*
+ * Run one decode step of a prepared chain on the tokens x (device, fp16 [M][K0], 16-byte
+ * aligned, not overlapping any link's output).  Asynchronous; capturable in a HIP graph (one
+ * kernel launch).  The grid is one workgroup per CU and relies on all of them running at once:
+ * calls must not overlap one another on a device (they share the chain's counters, and a
+ * concurrent kernel that holds CUs delays the grid).  A wait that gives up (another workgroup not
+ * heard from within about a second) sets QIFT_DEVERR_CHAIN_WAIT in the device error word
+ * (qift_device_error) and the results of that call are not to be trusted.
+ */
+int qift_decode_chain(const qift_chain *chain, const uint16_t *x, qift_stream_t stream);
+
+/*
  * Measurement helper, not part of the method: the achievable HBM read
  * bandwidth, the floor of the decode kernels' weight streams.  Reads the
  * device buffer buf[0 .. bytes) once with 16-byte loads spread over every CU;
@@ -333,9 +406,12 @@ int qift_hbm_read_probe(const void *buf, size_t bytes, uint32_t *partials, qift_
  *   x_max = c * max(max x, 0), x_min = c * min(min x, 0), c = fp32(0.95);
  *   s = (x_max - x_min) / 15 (1 for a group of zeros); z = round(-x_min / s);
  *   q = clip(round(x / s) + z, 0, 15).
- *   x        fp16 [groups][128].
- *   codes    out: uint8 [groups][64], value 2i in the low nibble of byte i.
- *   scales   out: fp32 s [groups].   zeros   out: uint8 z [groups].
+ *   x        fp16 [groups][128], 16-byte aligned.
+ *   codes    out: uint8 [groups][64], value 2i in the low nibble of byte i;
+ *            4-byte aligned.
+ *   scales   out: fp32 s [groups], 4-byte aligned.
+ *   zeros    out: uint8 z [groups], any alignment (so a view of a cache at
+ *            any token position, e.g. one appended decode token, is valid).
  */
 int qift_kv4_quant(const uint16_t *x, int64_t groups, int32_t head_dim, uint8_t *codes,
                    float *scales, uint8_t *zeros, qift_stream_t stream);

@@ -94,6 +94,42 @@ uint32_t* device_error_word();
 int wait_limit();
 constexpr int kDefaultWaitLimit = 1 << 22;
 
+// Persistent decode chain (qift_chain.h, qift_chain_<fmt>.hip): one link of a prepared chain as the
+// kernel reads it (written to device memory by the prepare call).
+struct ChainDesc {
+  const uint32_t* P;     // packed words [N][K/16] (W2) or [N][K/8] (W4)
+  const uint16_t* sw;    // fp16 s_w [N]
+  const uint16_t* x;     // input of token 0 (nullptr: the chain input); token m at x + m * xstride
+  uint16_t* y;           // fp16 output [M][N]
+  int32_t* acc;          // nullable int32 [M][N]
+  double denom;          // (den * 7) * sqrt(block)
+  int32_t N, K, L, num, den, in_link, xstride, tiles;
+};
+constexpr int kChainMaxM = 4;
+// Hadamard blocks of the chain's links: 64, 256, 2048 and 4096 (the block exponent is compiled in)
+inline bool chain_block_ok(int block) { return block == 64 || block == 256 || block == 2048 || block == 4096; }
+constexpr int kChainMaxK = 16384;
+constexpr int kChainMaxLinks = 4096;
+constexpr int kChainTailBytes = 480;
+constexpr int kChainXchBytes = (4096 + 512) * 8;   // one rotation exchange buffer (a 4096-tile, padded)
+// Exchange / partial-sum region: partial sums of 8 slices x 7 (W4: 3) tiles, or one exchange buffer
+// per activation group (two when a link has K > 4096).
+inline size_t chain_xch_bytes(bool any_long, bool w4) {
+  const size_t part = (size_t)8 * (w4 ? 3 : 7) * 1024;
+  const size_t xch = (any_long ? 2 : 1) * (size_t)kChainXchBytes;
+  return part > xch ? part : xch;
+}
+inline size_t chain_lds_bytes(int64_t M, int64_t Kmax, bool any_long, bool w4) {
+  return (size_t)((M * (Kmax + 16) + 15) & ~int64_t(15)) + chain_xch_bytes(any_long, w4) + kChainTailBytes;
+}
+#define QIFT_CHAIN_LAUNCHER(NAME)                                                                              \
+  hipError_t NAME(const ChainDesc* links, int n_links, const uint16_t* x0, int M, int Kmax, bool any_long, int grid, \
+                  unsigned* counters, hipStream_t s)
+QIFT_CHAIN_LAUNCHER(launch_chain_mnz);
+QIFT_CHAIN_LAUNCHER(launch_chain_pot);
+QIFT_CHAIN_LAUNCHER(launch_chain_w4);
+#undef QIFT_CHAIN_LAUNCHER
+
 // Limits of the fused entry point.
 constexpr int64_t kFusedMaxM = 4;
 constexpr int64_t kCodesMaxM = 16;   // one MFMA column block of tokens

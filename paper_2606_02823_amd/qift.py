@@ -34,7 +34,8 @@ EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_w
            "qift_rotate_quant_act_bf16",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w2a4_lut_linear", "qift_w4a4_linear", "qift_w4a4_linear_ex",
            "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
-           "qift_last_hip_error", "qift_device_error", "qift_set_wait_limit", "qift_version")
+           "qift_last_hip_error", "qift_device_error", "qift_set_wait_limit", "qift_chain_workspace_bytes",
+           "qift_chain_prepare", "qift_decode_chain", "qift_version")
 
 
 class QiftError(RuntimeError):
@@ -61,6 +62,18 @@ def clip_flags(num: int, den: int) -> int:
 
 def spec(K: int, block: int, clip=(1, 1)) -> HadamardSpec:
     return HadamardSpec(K, block, clip_flags(*clip))
+
+
+class ChainLinkC(ctypes.Structure):
+    _fields_ = [("w", PackedW), ("block", ctypes.c_int32), ("flags", ctypes.c_int32), ("in_link", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("in_offset", ctypes.c_int64), ("out", ctypes.c_void_p),
+                ("acc_out", ctypes.c_void_p)]
+
+
+class ChainC(ctypes.Structure):
+    _fields_ = [("fmt", ctypes.c_int32), ("n_links", ctypes.c_int32), ("M", ctypes.c_int32), ("K0", ctypes.c_int32),
+                ("grid", ctypes.c_int32), ("kmax", ctypes.c_int32), ("any_long", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("table", ctypes.c_void_p), ("counters", ctypes.c_void_p)]
 
 
 _lib = None
@@ -99,6 +112,10 @@ def lib():
         "qift_last_hip_error": (ctypes.c_int, []),
         "qift_device_error": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint32), i32, vp]),
         "qift_set_wait_limit": (ctypes.c_int, [i32]),
+        "qift_chain_workspace_bytes": (sz, [i32]),
+        "qift_chain_prepare": (ctypes.c_int, [ctypes.POINTER(ChainLinkC), i32, i64, i64, vp, sz, ctypes.POINTER(ChainC),
+                                              vp]),
+        "qift_decode_chain": (ctypes.c_int, [ctypes.POINTER(ChainC), vp, vp]),
         "qift_version": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -399,6 +416,47 @@ def rotate_quant_linear(w: Packed, x: torch.Tensor, block: int, clip=(1, 1), out
         None if act_out is None else act_out.sum.data_ptr(), _stream(stream))
     _check("qift_rotate_quant_linear", st)
     return out
+
+
+@dataclass
+class ChainLink:
+    """One linear of a decode chain: weights, the Hadamard block (and clip) of its input, and where the
+    input comes from (in_link = -1: the chain input; else elements [in_offset, in_offset + K) of that
+    link's output rows)."""
+    w: Packed
+    block: int
+    in_link: int = -1
+    in_offset: int = 0
+    clip: tuple = (1, 1)
+
+
+class Chain:
+    """A prepared decode chain (qift_chain_prepare): its workspace, the output buffer of every link and,
+    with acc=True, the int32 accumulators.  run(x) performs one decode step (one kernel launch)."""
+
+    def __init__(self, links, M: int, acc: bool = False, device="cuda", stream=None):
+        self.links = list(links)
+        self.M = M
+        self.K0 = self.links[0].w.K
+        self.outs = [torch.empty((M, l.w.N), dtype=torch.float16, device=device) for l in self.links]
+        self.accs = [torch.empty((M, l.w.N), dtype=torch.int32, device=device) for l in self.links] if acc else None
+        n = len(self.links)
+        nbytes = int(lib().qift_chain_workspace_bytes(n))
+        if nbytes == 0:
+            raise ValueError(f"a chain holds 1..4096 links, got {n}")
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        arr = (ChainLinkC * n)()
+        for i, l in enumerate(self.links):
+            arr[i] = ChainLinkC(l.w.cview(), l.block, clip_flags(*l.clip), l.in_link, 0, l.in_offset,
+                                self.outs[i].data_ptr(), None if acc is False else self.accs[i].data_ptr())
+        self.c = ChainC()
+        _check("qift_chain_prepare", lib().qift_chain_prepare(arr, n, M, self.K0, self.workspace.data_ptr(), nbytes,
+                                                               ctypes.byref(self.c), _stream(stream)))
+
+    def run(self, x: torch.Tensor, stream=None):
+        _dev(x, torch.float16, (self.M, self.K0), "x")
+        _check("qift_decode_chain", lib().qift_decode_chain(ctypes.byref(self.c), x.data_ptr(), _stream(stream)))
+        return self.outs
 
 
 READ_PROBE_SEGMENT = 65536   # bytes read by one workgroup of the read probe

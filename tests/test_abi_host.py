@@ -35,7 +35,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 22
+    assert len(names) == 25
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -96,7 +96,9 @@ def test_kv4_validation(L):
     assert fq(None, 4, 128, A, A, A, None) == E_NULL
     assert fq(A, 4, 64, A, A, A, None) == E_SHAPE          # head_dim 128 only
     assert fq(A, 0, 128, A, A, A, None) == E_SHAPE
-    assert fq(A, 4, 128, A, MIS, A, None) == E_ALIGN
+    assert fq(MIS, 4, 128, A, A, A, None) == E_ALIGN        # x: 16-byte loads
+    assert fq(A, 4, 128, 0x10002, A, A, None) == E_ALIGN    # codes: 4-byte words
+    assert fq(A, 4, 128, A, 0x10002, A, None) == E_ALIGN    # scales: fp32
     ws = L.qift_kv4_attention_workspace_bytes
     assert ws(2, 32, 8, 128, 1000) == 2 * 32 * 4 * 130 * 4   # 4 chunks of 256 tokens, 130 floats each
     assert ws(1, 32, 8, 64, 1000) == 0

@@ -61,6 +61,30 @@ def test_kv4_quant_bitexact(Q):
     assert np.array_equal(c.codes.cpu().numpy(), okv4.pack_nibbles(q_ref))
 
 
+def test_kv4_quant_one_token_into_a_cache_view(Q):
+    # one decode step appends token t of a token-major [B, T, Hkv] cache: its zero-points start at
+    # byte (b T + t) Hkv, 8-byte but not 16-byte aligned for odd t with Hkv = 8
+    B, T, Hkv = 2, 5, 8
+    rng = np.random.default_rng(5)
+    cache = Q.KV4(torch.zeros((B, T, Hkv, 64), dtype=torch.uint8, device="cuda"),
+                  torch.zeros((B, T, Hkv), dtype=torch.float32, device="cuda"),
+                  torch.zeros((B, T, Hkv), dtype=torch.uint8, device="cuda"))
+    misaligned = 0
+    for b, t in ((0, 3), (1, 1), (1, 4)):
+        x = groups_fp16(rng, Hkv)
+        view = Q.KV4(cache.codes[b, t], cache.scales[b, t], cache.zeros[b, t])
+        misaligned += view.zeros.data_ptr() % 16 != 0
+        Q.kv4_quant(torch.from_numpy(x).cuda(), out=view)
+        torch.cuda.synchronize()
+        q_ref, s_ref, z_ref = okv4.kv4_quant(x)
+        assert np.array_equal(cache.scales[b, t].cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
+        assert np.array_equal(cache.zeros[b, t].cpu().numpy(), z_ref)
+        assert np.array_equal(cache.codes[b, t].cpu().numpy(), okv4.pack_nibbles(q_ref))
+    assert misaligned >= 1   # (b T + t) Hkv = 24 and 72 bytes: not 16-byte aligned
+    # the other rows are untouched
+    assert int(cache.zeros[0, 0].sum().item()) == 0 and float(cache.scales[1, 0].abs().sum().item()) == 0.0
+
+
 @pytest.mark.parametrize("head_major", [False, True], ids=["token_major", "head_major"])
 @pytest.mark.parametrize("B,T,Hq,Hkv", [(1, 1, 32, 8), (2, 255, 32, 8), (1, 256, 32, 8), (2, 257, 16, 8),
                                         (1, 1000, 8, 8), (1, 4100, 64, 8), (3, 700, 32, 8), (2, 513, 4, 2),
