@@ -321,7 +321,8 @@ int qift_rotate_quant_linear(const qift_packed_w *w, const uint16_t *x, int64_t 
  *
  *   qift_chain_link   (host) one linear:
  *     w          the weights (fmt MNZ, PoT or W4; one format for the whole chain).
- *     block      Hadamard block of the link's input (power of two, 2..4096, dividing w.K).
+ *     block      Hadamard block of the link's input: 64, 256, 2048 or 4096 (the blocks of the
+ *                LLaMA-shaped stacks, compiled in), dividing w.K.
  *     flags      clip flags of the input's quantizer, as qift_hadamard_spec.flags.
  *     in_link    index of the link whose output is this link's input (lower than this link's
  *                index), or -1 for the chain input x (then w.K must equal the chain's K0).
@@ -348,26 +349,33 @@ typedef struct {
   int32_t fmt, n_links;
   int32_t M, K0;             /* tokens per call, width of the chain input */
   int32_t grid, kmax;        /* workgroups (one per CU), largest K of the links */
-  int32_t any_long, reserved;
+  int32_t region0, reserved; /* LDS bytes of the activation group's work region */
   const void *table;         /* device: the link table (in the workspace) */
-  uint32_t *counters;        /* device: n_links + 1 arrival counters (in the workspace) */
+  uint32_t *counters;        /* device: arrival count and run number (in the workspace) */
 } qift_chain;
 
-/* Workspace bytes of a chain of n_links links (0 for n_links outside 1..4096). */
-size_t qift_chain_workspace_bytes(int32_t n_links);
+/*
+ * Workspace bytes of a chain (host links, n_links of them, M tokens): the link table, two counters,
+ * and for every link whose output another link reads, that output again as tagged words
+ * (M x ceil(N/2) x 8 bytes: two fp16 values and the 32-bit tag of the producing call and link).
+ * 0 for a chain that qift_chain_prepare would reject.
+ */
+size_t qift_chain_workspace_bytes(const qift_chain_link *links, int32_t n_links, int64_t M);
 
 /*
- * Validate the links, write the link table and zeroed counters into the workspace and fill
- * *chain.  An offline call: it SYNCHRONIZES the stream (the table is copied from host memory);
- * not capturable in a HIP graph.
+ * Validate the links, write the link table, the counters and zeroed tagged buffers into the
+ * workspace and fill *chain.  An offline call: it SYNCHRONIZES the stream (the table is copied
+ * from host memory); not capturable in a HIP graph.
  *   links      host: n_links links (1 <= n_links <= 4096).
- *   M          tokens per call, 1..4.
+ *   M          tokens per call, 1..4, as far as one workgroup's LDS holds M tokens' codes next to
+ *              the stash of the longest link's rotation tiles (a K = 14336 link: M = 1).
  *   K0         width of the chain input x.
- *   workspace  device, 16-byte aligned, at least qift_chain_workspace_bytes(n_links) bytes.
+ *   workspace  device, 16-byte aligned, at least qift_chain_workspace_bytes(links, n_links, M).
  *   chain      host, out.
  * Errors: QIFT_ERR_NULL, QIFT_ERR_FORMAT (mixed or unknown formats), QIFT_ERR_SHAPE (K above
  * 16384, an input slice past the producer's row, overlapping outputs, M outside 1..4, or LDS
- * beyond 160 KiB), QIFT_ERR_SPEC (block or flags), QIFT_ERR_ALIGN, QIFT_ERR_WORKSPACE.
+ * beyond 160 KiB), QIFT_ERR_SPEC (block not one of 64, 256, 2048, 4096, or bad flags),
+ * QIFT_ERR_ALIGN, QIFT_ERR_WORKSPACE.
  */
 int qift_chain_prepare(const qift_chain_link *links, int32_t n_links, int64_t M, int64_t K0, void *workspace,
                        size_t workspace_bytes, qift_chain *chain, qift_stream_t stream);
@@ -376,9 +384,10 @@ int qift_chain_prepare(const qift_chain_link *links, int32_t n_links, int64_t M,
  * Run one decode step of a prepared chain on the tokens x (device, fp16 [M][K0], 16-byte
  * aligned, not overlapping any link's output).  Asynchronous; capturable in a HIP graph (one
  * kernel launch).  The grid is one workgroup per CU and relies on all of them running at once:
- * calls must not overlap one another on a device (they share the chain's counters, and a
- * concurrent kernel that holds CUs delays the grid).  A wait that gives up (another workgroup not
- * heard from within about a second) sets QIFT_DEVERR_CHAIN_WAIT in the device error word
+ * calls must not overlap one another on a device (they share the chain's counters and tagged
+ * buffers, and a concurrent kernel that holds CUs delays the grid).  A link waits for its input
+ * words to carry the producing link's tag of this call; a wait that gives up (the call not done
+ * within about a second) sets QIFT_DEVERR_CHAIN_WAIT in the device error word
  * (qift_device_error) and the results of that call are not to be trusted.
  */
 int qift_decode_chain(const qift_chain *chain, const uint16_t *x, qift_stream_t stream);

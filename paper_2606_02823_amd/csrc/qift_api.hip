@@ -329,45 +329,46 @@ int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t 
 // ---- decode chain -------------------------------------------------------------------------------
 
 namespace {
-size_t chain_table_bytes(int32_t n) { return ((size_t)n * sizeof(qift::ChainDesc) + 255) & ~size_t(255); }
-size_t chain_counter_bytes(int32_t n) { return ((size_t)(n + 1) * sizeof(uint32_t) + 15) & ~size_t(15); }
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+constexpr size_t kChainCounterBytes = 256;   // the arrival count and the run number, padded
 
-// Host-side checks of a chain and the device link table (every check before any HIP call).
-int chain_build(const qift_chain_link* links, int32_t n, int64_t M, int64_t K0, std::vector<qift::ChainDesc>& d,
-                int64_t* kmax_out, bool* any_long_out) {
+// Host-side checks of a chain and the device link table (every check before any HIP call).  With a
+// workspace base, the tagged output buffers of the links whose output another link reads are laid
+// out after the table and the counters; *ws_bytes receives the workspace size either way.
+int chain_build(const qift_chain_link* links, int32_t n, int64_t M, int64_t K0, unsigned char* ws,
+                std::vector<qift::ChainDesc>& d, size_t* ws_bytes, int64_t* kmax_out, int* region0) {
   if (!links) return QIFT_ERR_NULL;
   if (n < 1 || n > qift::kChainMaxLinks) return QIFT_ERR_SHAPE;
   if (M < 1 || M > qift::kChainMaxM || K0 < 64 || K0 % 64 || K0 > qift::kChainMaxK) return QIFT_ERR_SHAPE;
   const int32_t fmt = links[0].w.fmt;
   if (!(is_w2(fmt) || fmt == QIFT_W4_SYM)) return QIFT_ERR_FORMAT;
   d.assign((size_t)n, qift::ChainDesc{});
+  std::vector<char> consumed((size_t)n, 0);
   int64_t kmax = 0;
-  bool any_long = false;
   for (int32_t i = 0; i < n; ++i) {
     const qift_chain_link& l = links[i];
     const qift_packed_w& w = l.w;
     if (!w.packed || !w.scales || !l.out) return QIFT_ERR_NULL;
     if (w.layout != QIFT_LAYOUT_V1 || w.fmt != fmt) return QIFT_ERR_FORMAT;
-    if (!shape_ok(w.N, w.K) || w.K > qift::kChainMaxK) return QIFT_ERR_SHAPE;
-    if (qift_packed_bytes(fmt, w.N, w.K) >= (size_t(1) << 31) || M * w.N * 2 >= (int64_t(1) << 31))
+    // N below 2^26 keeps the kernel's tile split (tiles x (CUs + 1)) in 32 bits
+    if (!shape_ok(w.N, w.K) || w.K > qift::kChainMaxK || w.N >= (int64_t(1) << 26)) return QIFT_ERR_SHAPE;
+    if (qift_packed_bytes(fmt, w.N, w.K) >= (size_t(1) << 31) || M * w.N * 8 >= (int64_t(1) << 31))
       return QIFT_ERR_SHAPE;
     const int32_t b = l.block;
     int num, den;
     if (!qift::chain_block_ok(b) || w.K % b || l.reserved != 0 || !parse_clip(l.flags, &num, &den))
       return QIFT_ERR_SPEC;
     if (l.in_link < -1 || l.in_link >= i) return QIFT_ERR_SHAPE;
-    int64_t xstride = w.K;
     if (l.in_link < 0) {
       if (w.K != K0 || l.in_offset != 0) return QIFT_ERR_SHAPE;
     } else {
       const int64_t Nin = links[l.in_link].w.N;
       if (l.in_offset < 0 || l.in_offset % 8 || l.in_offset + w.K > Nin) return QIFT_ERR_SHAPE;
-      if (M > 1 && Nin % 8) return QIFT_ERR_SHAPE;   // every token's input row stays 16-byte aligned
-      xstride = Nin;
+      consumed[(size_t)l.in_link] = 1;
     }
     if (!aligned16(w.packed) || !aligned16(w.scales) || !aligned16(l.out) || (l.acc_out && !aligned16(l.acc_out)))
       return QIFT_ERR_ALIGN;
-    // the outputs (and accumulator outputs) of different links are disjoint
+    // the outputs of different links are disjoint
     const uintptr_t a0 = reinterpret_cast<uintptr_t>(l.out), a1 = a0 + (uintptr_t)(M * w.N * 2);
     for (int32_t j = 0; j < i; ++j) {
       const uintptr_t b0 = reinterpret_cast<uintptr_t>(links[j].out), b1 = b0 + (uintptr_t)(M * links[j].w.N * 2);
@@ -376,7 +377,6 @@ int chain_build(const qift_chain_link* links, int32_t n, int64_t M, int64_t K0, 
     qift::ChainDesc& e = d[(size_t)i];
     e.P = w.packed;
     e.sw = w.scales;
-    e.x = l.in_link < 0 ? nullptr : links[l.in_link].out + l.in_offset;
     e.y = l.out;
     e.acc = l.acc_out;
     e.denom = qift::act_denominator(b, den);
@@ -386,64 +386,85 @@ int chain_build(const qift_chain_link* links, int32_t n, int64_t M, int64_t K0, 
     e.num = num;
     e.den = den;
     e.in_link = l.in_link;
-    e.xstride = (int32_t)xstride;
+    e.xoff = (int32_t)l.in_offset;
+    e.ywords = (int32_t)((w.N + 1) / 2);
     e.tiles = (int32_t)((w.N + 15) / 16);
     kmax = w.K > kmax ? w.K : kmax;
-    any_long = any_long || w.K > 4096;
   }
-  if (qift::chain_lds_bytes(M, kmax, any_long, fmt == QIFT_W4_SYM) > 160 * 1024) return QIFT_ERR_SHAPE;
+  // workspace: link table, counters, then the tagged outputs of the links that are read
+  size_t off = align256((size_t)n * sizeof(qift::ChainDesc)) + kChainCounterBytes;
+  for (int32_t i = 0; i < n; ++i) {
+    if (!consumed[(size_t)i]) continue;
+    d[(size_t)i].ty = ws ? reinterpret_cast<uint64_t*>(ws + off) : nullptr;
+    off += align256((size_t)M * (size_t)d[(size_t)i].ywords * 8);
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t in = d[(size_t)i].in_link;
+    if (in >= 0) {
+      d[(size_t)i].tx = d[(size_t)in].ty;
+      d[(size_t)i].xwords = d[(size_t)in].ywords;
+    }
+  }
+  *ws_bytes = off;
+  *region0 = qift::chain_region0((int)((kmax + 4095) / 4096), fmt == QIFT_W4_SYM);
+  if (qift::chain_lds_bytes(M, kmax, *region0) > 160 * 1024) return QIFT_ERR_SHAPE;
   *kmax_out = kmax;
-  *any_long_out = any_long;
-  return QIFT_OK;
-}
-
-int chain_upload(const std::vector<qift::ChainDesc>& d, int32_t n, int64_t M, int64_t K0, int fmt, int64_t kmax,
-                 bool any_long, void* table, uint32_t* counters, qift_chain* chain, hipStream_t s) {
-  int dev = 0, cus = 0;
-  int st = hip_status(hipGetDevice(&dev));
-  if (st == QIFT_OK) st = hip_status(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-  if (st != QIFT_OK) return st;
-  if (cus < 1) return hip_status(hipErrorInvalidDevice);
-  st = hip_status(hipMemcpyAsync(table, d.data(), (size_t)n * sizeof(qift::ChainDesc), hipMemcpyHostToDevice, s));
-  if (st == QIFT_OK) st = hip_status(hipMemsetAsync(counters, 0, chain_counter_bytes(n), s));
-  if (st == QIFT_OK) st = hip_status(hipStreamSynchronize(s));
-  if (st != QIFT_OK) return st;
-  *chain = qift_chain{fmt, n, (int32_t)M, (int32_t)K0, cus, (int32_t)kmax, any_long ? 1 : 0, 0, table, counters};
   return QIFT_OK;
 }
 }  // namespace
 
-size_t qift_chain_workspace_bytes(int32_t n_links) {
-  if (n_links < 1 || n_links > qift::kChainMaxLinks) return 0;
-  return chain_table_bytes(n_links) + chain_counter_bytes(n_links);
+size_t qift_chain_workspace_bytes(const qift_chain_link* links, int32_t n_links, int64_t M) {
+  std::vector<qift::ChainDesc> d;
+  size_t bytes = 0;
+  int64_t kmax = 0;
+  int r0 = 0;
+  if (!links || n_links < 1 || n_links > qift::kChainMaxLinks) return 0;
+  if (chain_build(links, n_links, M, links[0].w.K, nullptr, d, &bytes, &kmax, &r0) != QIFT_OK) return 0;
+  return bytes;
 }
 
 int qift_chain_prepare(const qift_chain_link* links, int32_t n_links, int64_t M, int64_t K0, void* workspace,
                        size_t workspace_bytes, qift_chain* chain, qift_stream_t stream) {
   if (!links || !workspace || !chain) return QIFT_ERR_NULL;
-  std::vector<qift::ChainDesc> d;
-  int64_t kmax = 0;
-  bool any_long = false;
-  int st = chain_build(links, n_links, M, K0, d, &kmax, &any_long);
-  if (st != QIFT_OK) return st;
-  if (workspace_bytes < qift_chain_workspace_bytes(n_links)) return QIFT_ERR_WORKSPACE;
   if (!aligned16(workspace)) return QIFT_ERR_ALIGN;
+  std::vector<qift::ChainDesc> d;
+  size_t need = 0;
+  int64_t kmax = 0;
+  int r0 = 0;
   unsigned char* ws = static_cast<unsigned char*>(workspace);
-  return chain_upload(d, n_links, M, K0, links[0].w.fmt, kmax, any_long, ws,
-                      reinterpret_cast<uint32_t*>(ws + chain_table_bytes(n_links)), chain, (hipStream_t)stream);
+  int st = chain_build(links, n_links, M, K0, ws, d, &need, &kmax, &r0);
+  if (st != QIFT_OK) return st;
+  if (workspace_bytes < need) return QIFT_ERR_WORKSPACE;
+  int dev = 0, cus = 0;
+  st = hip_status(hipGetDevice(&dev));
+  if (st == QIFT_OK) st = hip_status(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  if (st != QIFT_OK) return st;
+  if (cus < 1) return hip_status(hipErrorInvalidDevice);
+  const hipStream_t s = (hipStream_t)stream;
+  const size_t table = align256((size_t)n_links * sizeof(qift::ChainDesc));
+  uint32_t* counters = reinterpret_cast<uint32_t*>(ws + table);
+  static const uint32_t start[2] = {0u, 1u};   // arrival count 0, run number 1 (tags of zeroed words are 0)
+  st = hip_status(hipMemcpyAsync(ws, d.data(), (size_t)n_links * sizeof(qift::ChainDesc), hipMemcpyHostToDevice, s));
+  if (st == QIFT_OK) st = hip_status(hipMemsetAsync(ws + table, 0, need - table, s));
+  if (st == QIFT_OK) st = hip_status(hipMemcpyAsync(counters, start, sizeof(start), hipMemcpyHostToDevice, s));
+  if (st == QIFT_OK) st = hip_status(hipStreamSynchronize(s));
+  if (st != QIFT_OK) return st;
+  *chain = qift_chain{links[0].w.fmt, n_links, (int32_t)M, (int32_t)K0, cus, (int32_t)kmax, r0, 0, ws, counters};
+  return QIFT_OK;
 }
 
 int qift_decode_chain(const qift_chain* c, const uint16_t* x, qift_stream_t stream) {
   if (!c || !x || !c->table || !c->counters) return QIFT_ERR_NULL;
   if (c->n_links < 1 || c->n_links > qift::kChainMaxLinks || c->M < 1 || c->M > qift::kChainMaxM || c->grid < 1 ||
-      c->kmax < 64 || c->kmax > qift::kChainMaxK || c->K0 < 64 || c->K0 > c->kmax)
+      c->kmax < 64 || c->kmax > qift::kChainMaxK || c->K0 < 64 || c->K0 > c->kmax || c->region0 < 0 ||
+      qift::chain_lds_bytes(c->M, c->kmax, c->region0) > 160 * 1024)
     return QIFT_ERR_SHAPE;
   if (!(is_w2(c->fmt) || c->fmt == QIFT_W4_SYM)) return QIFT_ERR_FORMAT;
-  if (!aligned16(x) || !aligned16(c->table) || (reinterpret_cast<uintptr_t>(c->counters) & 3u)) return QIFT_ERR_ALIGN;
+  if (!aligned16(x) || !aligned16(c->table) || !aligned16(c->counters)) return QIFT_ERR_ALIGN;
   auto launch = c->fmt == QIFT_W2_MNZ ? qift::launch_chain_mnz : c->fmt == QIFT_W2_POT ? qift::launch_chain_pot
                                                                                        : qift::launch_chain_w4;
-  return hip_status(launch(static_cast<const qift::ChainDesc*>(c->table), c->n_links, x, c->M, c->kmax,
-                           c->any_long != 0, c->grid, reinterpret_cast<unsigned*>(c->counters), (hipStream_t)stream));
+  return hip_status(launch(static_cast<const qift::ChainDesc*>(c->table), c->n_links, x, c->M, c->kmax, c->region0,
+                           c->grid, reinterpret_cast<unsigned*>(c->counters), (hipStream_t)stream));
 }
 
 int qift_hbm_read_probe(const void* buf, size_t bytes, uint32_t* partials, qift_stream_t stream) {

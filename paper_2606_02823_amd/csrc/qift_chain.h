@@ -34,9 +34,9 @@ namespace qift {
 constexpr int kChainWaves = 12;
 constexpr int kChainThreads = 64 * kChainWaves;
 constexpr int kChainShortK = 4096;   // one rotation tile: 4 activation waves, 8 K-slices
-// LDS after the codes and the exchange / partial-sum region (kChainTailBytes): s_scale[4] f32,
-// red_d[4][8] f64, red_i[4][8] i32, ctr[4] u32, 64 zero bytes
-static_assert(kChainTailBytes == 16 + 256 + 128 + 16 + 64, "tail layout");
+// LDS tail (kChainTailBytes): s_scale[2][4] f32, red_d[2][4][8] f64, red_i[2][4][8] i32, ctr[4] u32,
+// 64 zero bytes
+static_assert(kChainTailBytes == 32 + 512 + 256 + 16 + 64, "tail layout");
 
 template <int FMT>
 constexpr int chain_tmax() { return FMT == mma::FMT_W4 ? 3 : 7; }   // tiles per chunk, K <= 4096
@@ -53,9 +53,12 @@ struct Geom {
   bool lng;
 };
 
+// Tiles of a link owned by workgroup wg of G: [wg T / G, (wg + 1) T / G) (32-bit arithmetic: the host
+// keeps T (G + 1) below 2^32).
 __device__ __forceinline__ Geom geom(const ChainDesc& d, int wg, int G, int tmax_short) {
   Geom r;
-  const int a = (int)((int64_t)wg * d.tiles / G), b = (int)((int64_t)(wg + 1) * d.tiles / G);
+  const uint32_t tiles = (uint32_t)d.tiles;
+  const int a = (int)(((uint32_t)wg * tiles) / (uint32_t)G), b = (int)(((uint32_t)(wg + 1) * tiles) / (uint32_t)G);
   r.t0 = a;
   r.T = b - a;
   r.lng = d.K > kChainShortK;
@@ -67,14 +70,14 @@ __device__ __forceinline__ Geom geom(const ChainDesc& d, int wg, int G, int tmax
 // ---------------------------------------------------------------------------------------------
 // weight waves
 
-// Loads of one chunk of T tiles into wr (unit-major, the order the MFMAs consume them).  Short
-// links: 8 slices of NC <= 2 units of 256 k; long links: 4 slices of NC <= 16 units (W4: batch b
-// of 8).  Rows past N and k past K read zeros (out-of-range offsets).
+// Loads of one chunk of T tiles into wr (unit-major, the order the MFMAs consume them): 8 K-slices,
+// of NC <= 2 units of 256 k (K <= 4096) or NC <= 8 units (K <= 16384, one tile).  Rows past N and
+// k past K read zeros (out-of-range offsets).
 template <int FMT, int T, bool LONG>
 __device__ __forceinline__ void load_chunk(uint4 (&wr)[16], const ChainDesc& d, int tile0, int slice, int batch) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
-  constexpr int NS = LONG ? 4 : 8;
-  constexpr int UPT = LONG ? (FMT == FMT_W4 ? 8 : 16) : 2;
+  constexpr int NS = 8;
+  constexpr int UPT = LONG ? 8 : 2;
   static_assert(T * UPT * NH <= 16, "weight registers");
   const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
   const int K = d.K, N = d.N;
@@ -140,8 +143,8 @@ __device__ __forceinline__ void mfma_chunk(uint4 (&wr)[16], const ChainDesc& d, 
                                            const int8_t* act_l, int Kpad, int M, const int8_t* zero64,
                                            v4i* red) {
   constexpr int NH = FMT == FMT_W4 ? 2 : 1;
-  constexpr int NS = LONG ? 4 : 8;
-  constexpr int UPT = LONG ? (FMT == FMT_W4 ? 8 : 16) : 2;
+  constexpr int NS = 8;
+  constexpr int UPT = LONG ? 8 : 2;
   constexpr bool PLANAR = FMT == FMT_MNZ;
   // accumulators per tile: MNZ one per bit plane up to 3 tiles, from 4 tiles on two (decode_plane2)
   constexpr bool TWO = PLANAR && T >= 4;
@@ -193,20 +196,12 @@ __device__ __forceinline__ void mfma_chunk(uint4 (&wr)[16], const ChainDesc& d, 
 #pragma unroll
     for (int u = 0; u < UPT; ++u) unit_mfmas(u, bq[u]);
   } else {
-    constexpr int NB = FMT == FMT_W4 ? 2 : 1;   // batches of UPT units (W4 holds 8 units at a time)
+    v4i bq[2][4];   // the next unit's operands are read during this unit's MFMAs
+    load_b(0, bq[0]);
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      if (b > 0) {
-        if (b * UPT >= NC) break;   // wave-uniform
-        load_chunk<FMT, 1, true>(wr, d, tile0, slice, b);
-      }
-      v4i bq[2][4];   // the next unit's operands are read during this unit's MFMAs
-      load_b(b * UPT, bq[0]);
-#pragma unroll
-      for (int u = 0; u < UPT; ++u) {
-        if (u + 1 < UPT) load_b(b * UPT + u + 1, bq[(u + 1) & 1]);
-        unit_mfmas(u, bq[u & 1]);
-      }
+    for (int u = 0; u < UPT; ++u) {
+      if (u + 1 < UPT) load_b(u + 1, bq[(u + 1) & 1]);
+      unit_mfmas(u, bq[u & 1]);
     }
   }
 #pragma unroll
@@ -253,104 +248,208 @@ __device__ __forceinline__ void mfma_chunk_rt(uint4 (&wr)[16], const ChainDesc& 
 // ---------------------------------------------------------------------------------------------
 // activation waves
 
-// Raw fp16 bits of tiles [tau0, tau0 + ntg) of one token, 16 consecutive elements per thread of
-// the group (t = 0..255), read with agent-coherent loads (the producer may sit on another XCD).
-template <int NTG>
-__device__ __forceinline__ void load_tiles_sc1(dev::TokenRaw<NTG>& raw, const uint16_t* xr, int K, int tau0, int ntg,
-                                               int t) {
-  const __amdgpu_buffer_rsrc_t r = dev::make_rsrc(xr, (uint32_t)(K * 2));
+// One token's input for the activation group: 16 consecutive elements of each of the NT rotation
+// tiles per thread (fp16 bits, 32 bytes per tile), element e = 4096 tau + 16 t + i.  The chain input
+// x0 is read directly; a link's output is read from its tagged words (two fp16 values and a 32-bit
+// tag per 8 bytes, written with agent-coherent stores) with agent-coherent loads, every tile's loads
+// at once, until every word carries the producing link's tag of this call: the data and its
+// readiness arrive in the same access, so no separate flag or counter is needed.  The wait is
+// bounded by the deadline (100 MHz ticks); a wave that gives up sets kErrChainWait.
+__device__ __forceinline__ void fetch_tiles(uint4 (&raw)[4][2], const ChainDesc& d, const uint16_t* x0, int m, int NT,
+                                            int t, uint32_t tag, long long deadline, uint32_t* err) {
+  typedef unsigned v2u __attribute__((ext_vector_type(2)));
+  if (d.in_link < 0) {
+    const __amdgpu_buffer_rsrc_t r = dev::make_rsrc(x0 + (int64_t)m * d.K, (uint32_t)(d.K * 2));
 #pragma unroll
-  for (int tau = 0; tau < NTG; ++tau) {
-    const int base = (tau0 + tau) * 4096 + 16 * t;   // elements past K (or past the group's tiles) read zeros
-    const uint32_t off = tau < ntg && base < K ? (uint32_t)(base * 2) : dev::kOutOfRange;
-    const auto a = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 16);
-    const auto b = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 16);
-    raw.d[tau][0] = make_uint4(a[0], a[1], a[2], a[3]);
-    raw.d[tau][1] = make_uint4(b[0], b[1], b[2], b[3]);
+    for (int tau = 0; tau < 4; ++tau) {
+      const int e0 = tau * 4096 + 16 * t;
+      const uint32_t off = tau < NT && e0 < d.K ? (uint32_t)(e0 * 2) : dev::kOutOfRange;   // past K: zeros
+      raw[tau][0] = dev::bload16(r, off);
+      raw[tau][1] = dev::bload16(r, off + 16);
+    }
+    return;
+  }
+  const __amdgpu_buffer_rsrc_t r = dev::make_rsrc(d.tx + (int64_t)m * d.xwords, (uint32_t)(d.xwords * 8));
+  uint32_t off[4];
+#pragma unroll
+  for (int tau = 0; tau < 4; ++tau) {
+    const int e0 = tau * 4096 + 16 * t;
+    off[tau] = tau < NT && e0 < d.K ? (uint32_t)((d.xoff + e0) / 2) * 8u : dev::kOutOfRange;
+  }
+  // A lane's eight words of a tile are one 16-row tile of the producing link, stored by one wave of
+  // one workgroup: wait on the last of them (one load per tile per round, with a pause between
+  // rounds, so that the polling does not crowd the memory pipeline that this CU's own stores use),
+  // then read them all and check every tag.
+  for (;;) {
+    bool seen = true;
+#pragma unroll
+    for (int tau = 0; tau < 4; ++tau) {
+      const v2u v = __builtin_amdgcn_raw_buffer_load_b64(r, off[tau] + 56, 0, 16);
+      seen = seen && (off[tau] == dev::kOutOfRange || v[1] == tag);
+    }
+    if (__all(seen) || wall_clock64() > deadline) break;
+    __builtin_amdgcn_s_sleep(8);
+  }
+  for (;;) {
+    v2u w[4][8];
+#pragma unroll
+    for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) w[tau][q] = __builtin_amdgcn_raw_buffer_load_b64(r, off[tau] + 8 * q, 0, 16);
+    bool ok = true;
+#pragma unroll
+    for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) ok = ok && (off[tau] == dev::kOutOfRange || w[tau][q][1] == tag);
+    const bool done = __all(ok);
+    const bool late = !done && wall_clock64() > deadline;
+    if (done || late) {
+      if (late && (threadIdx.x & 63) == 0) dev::flag_error(err, dev::kErrChainWait);
+#pragma unroll
+      for (int tau = 0; tau < 4; ++tau) {
+        raw[tau][0] = make_uint4(w[tau][0][0], w[tau][1][0], w[tau][2][0], w[tau][3][0]);
+        raw[tau][1] = make_uint4(w[tau][4][0], w[tau][5][0], w[tau][6][0], w[tau][7][0]);
+      }
+      return;
+    }
+    __builtin_amdgcn_s_sleep(8);
   }
 }
 
-// Rotation + quantization of the group's tiles [tau0, tau0 + ntg) of one token (the steps of
-// dev::quant_token_group, for a group of four waves that may own only part of the token).  The
-// group's waves synchronize through gsync; the absmax of all ngroups groups meets in red_d through
-// gall.  Codes go to dst at code_pos<PLANAR>; the group's code sums to red_i[4 gi + w].
-template <int NTG, int LC, bool PLANAR, typename GS, typename GA>
-__device__ __forceinline__ double quant_tiles(const dev::TokenRaw<NTG>& raw, int ntg, int tau0, int K, int L_rt,
-                                              int num, int den, double* xch, double* red_d, int* red_i, int gi,
-                                              int ngroups, GS& gsync, GA& gall, int8_t* dst) {
+// Quantize 16 transformed values of tile tg and store their codes (the layout the transform ended
+// in, at code_pos<PLANAR>); returns their sum.
+template <bool PLANAR>
+__device__ __forceinline__ int codes16(const double (&v)[16], const dev::QuantParams& p, int wend, int tg, int K, int t,
+                                       int8_t* dst) {
   using S = dev::Tile<256, 16>;
-  const int L = LC > 0 ? LC : L_rt;
-  const int t = threadIdx.x & 255, lane = t & 63, w = t >> 6;
-  double v[NTG][16];
+  int q[16];
+  dev::quant16(v, p, q);
+  int qs = 0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) qs += q[e];
+  int8_t* tile_dst = dst + tg * S::T;
+  if ((tg + 1) * S::T <= K) {
+    if (wend == 0) dev::store_codes<0, PLANAR>(tile_dst, q, t);
+    else if (wend == 4) dev::store_codes<4, PLANAR>(tile_dst, q, t);
+    else dev::store_codes<8, PLANAR>(tile_dst, q, t);
+  } else if (wend == 0) {
+    if (tg * S::T + 16 * t < K) dev::store_codes<0, PLANAR>(tile_dst, q, t);   // K is a multiple of 64
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int i = wend == 4 ? dev::win_elem<4>(t) + (e << 4) : dev::win_elem<8>(t) + (e << 8);
+      if (tg * S::T + i < K) tile_dst[dev::code_pos<PLANAR>(i)] = (int8_t)q[e];
+    }
+  }
+  return qs;
+}
+
+// Rotation + quantization of one token's NT rotation tiles (NT <= 4) by the four activation waves
+// (the steps of dev::quant_token_group).  Only one tile's values are held in registers: the exact
+// fp64 values of the tiles transformed before the last wait in the LDS stash (element-major, so
+// each lane touches its own bank) until the absmax is known.  The waves synchronize through gsync;
+// their code sums go to red_i[w].  Before it polls for its input the group waits (consumed) until
+// the weight waves are done with the previous link: their stores are then issued ahead of the
+// polling loads (polling that overlapped them was measured to starve them), and the previous link's
+// partial sums, which share the group's LDS region, have been read.
+template <int LC, bool PLANAR, typename GS>
+__device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t* x0, int m, int NT, uint32_t tag,
+                                              long long deadline, uint32_t* err, GS& gsync, double* xch,
+                                              double* stash, int8_t* dst, double* red_d, int* red_i,
+                                              const unsigned* consumed, unsigned consumed_target) {
+  // the thread index as an opaque value: the per-thread LDS addresses derived from it are computed
+  // here, per call, instead of being hoisted out of the link loop (where dozens of them would stay
+  // live across the whole loop and spill)
+  int t = threadIdx.x & 255;
+  asm volatile("" : "+v"(t));
+  const int lane = t & 63, w = t >> 6;
+  if (consumed) {
+    // the weight waves are done with the previous link: its partial sums (which share this group's
+    // LDS region) are read and its stores are issued, ahead of the polling loads below
+    for (;;) {
+      const unsigned c = __builtin_amdgcn_readfirstlane(
+          __hip_atomic_load(consumed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+      if (c >= consumed_target) break;
+      if (wall_clock64() > deadline) {
+        if (lane == 0) dev::flag_error(err, dev::kErrGroupWait);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    asm volatile("" ::: "memory");
+  }
+  uint4 raw[4][2];
+  fetch_tiles(raw, d, x0, m, NT, t, tag, deadline, err);
+  double v[16];
   double amax = 0.0;
   int wend = 0;
 #pragma unroll
-  for (int tau = 0; tau < NTG; ++tau) {
-    if (tau < ntg) {
-      dev::unpack16<false>(v[tau], raw.d[tau]);
-      if (tau > 0 && L > 6) gsync();   // one exchange buffer per group: the previous tile's reads are done
-      wend = dev::fwht_tile_s<256, 16, false>(v[tau], xch, t, L, gsync);
+  for (int tau = 0; tau < 4; ++tau) {
+    if (tau < NT) {
+      if (tau > 0) {
+        double* st = stash + (tau - 1) * 4096;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[tau][e]));
+        for (int e = 0; e < 16; ++e) st[e * 256 + t] = v[e];
+        if (LC > 6) gsync();   // one exchange buffer: the previous tile's reads are done
+      }
+      dev::unpack16<false>(v, raw[tau]);
+      wend = dev::fwht_tile_s<256, 16, false>(v, xch, t, LC, gsync);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
     }
   }
   amax = dev::wave_max(amax);
-  if (lane == 0) red_d[4 * gi + w] = amax;
-  gall();
-  double A = red_d[0];
-  for (int q = 1; q < 4 * ngroups; ++q) A = fmax(A, red_d[q]);
-  const dev::QuantParams p = dev::make_qparams(A, num, den);
-  int qs = 0;
+  if (lane == 0) red_d[w] = amax;
+  gsync();
+  const double A = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
+  const dev::QuantParams p = dev::make_qparams(A, d.num, d.den);
+  int qs = codes16<PLANAR>(v, p, wend, NT - 1, d.K, t, dst);
 #pragma unroll
-  for (int tau = 0; tau < NTG; ++tau) {
-    if (tau < ntg) {
-      int q[16];
-      dev::quant16(v[tau], p, q);
+  for (int tau = 0; tau < 3; ++tau) {
+    if (tau < NT - 1) {
+      const double* st = stash + tau * 4096;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) qs += q[e];
-      const int tg = tau0 + tau;
-      int8_t* tile_dst = dst + tg * S::T;
-      if ((tg + 1) * S::T <= K) {
-        if (wend == 0) dev::store_codes<0, PLANAR>(tile_dst, q, t);
-        else if (wend == 4) dev::store_codes<4, PLANAR>(tile_dst, q, t);
-        else dev::store_codes<8, PLANAR>(tile_dst, q, t);
-      } else if (wend == 0) {
-        if (tg * S::T + 16 * t < K) dev::store_codes<0, PLANAR>(tile_dst, q, t);   // K is a multiple of 64
-      } else {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int i = wend == 4 ? dev::win_elem<4>(t) + (e << 4) : dev::win_elem<8>(t) + (e << 8);
-          if (tg * S::T + i < K) tile_dst[dev::code_pos<PLANAR>(i)] = (int8_t)q[e];
-        }
-      }
+      for (int e = 0; e < 16; ++e) v[e] = st[e * 256 + t];
+      qs += codes16<PLANAR>(v, p, wend, tau, d.K, t, dst);
     }
   }
   qs = dev::wave_sum(qs);
-  if (lane == 0) red_i[4 * gi + w] = qs;
+  if (lane == 0) red_i[w] = qs;
   return A;
 }
 
-// The activation phase of one link for one group: every token of the link.
-template <int NTG, int LC, bool PLANAR, typename GS, typename GA>
-__device__ __forceinline__ void act_phase(const ChainDesc& d, const uint16_t* xin, int xstride, int M, int ntg, int tau0,
-                                          int gi, int ngroups, GS& gsync, GA& gall, double* xch, int8_t* act_l,
-                                          int Kpad, double* red_d, int* red_i, float* s_scale) {
-  const int t = threadIdx.x & 255;
+// The activation phase of one link: every token; the scale of token m goes to s_scale[m].
+template <bool PLANAR, typename GS>
+__device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0, int M, uint32_t tag,
+                                         long long deadline, uint32_t* err, GS& gsync, double* xch, double* stash,
+                                         int8_t* act_l, int Kpad, double* red_d, int* red_i, float* s_scale,
+                                         const unsigned* consumed, unsigned consumed_target) {
+  const int NT = (d.K + 4095) / 4096;
   for (int m = 0; m < M; ++m) {
-    dev::TokenRaw<NTG> cur;
-    load_tiles_sc1<NTG>(cur, xin + (int64_t)m * xstride, d.K, tau0, ntg, t);
-    const double A = quant_tiles<NTG, LC, PLANAR>(cur, ntg, tau0, d.K, d.L, d.num, d.den, xch, red_d + 8 * m,
-                                                  red_i + 8 * m, gi, ngroups, gsync, gall, act_l + m * Kpad);
+    double A;
+    const unsigned* cw = m == 0 ? consumed : nullptr;
+    // the block sizes compiled in (chain_block_ok): every butterfly stage is straight-line code
+    switch (d.L) {
+      case 12: A = quant_group<12, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+                                           red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
+      case 11: A = quant_group<11, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+                                           red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
+      case 8: A = quant_group<8, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+                                         red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
+      default: A = quant_group<6, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+                                          red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
+    }
     if (threadIdx.x == 0) s_scale[m] = (float)((A * (double)d.num) / d.denom);
   }
 }
 
-// y[m][n0 .. n0 + 3] (and the accumulators) with agent-coherent stores: the consumers of this link
-// may run on other XCDs.
+// y[m][n0 .. n0 + 3] (fp16, and the accumulators) and, for the links whose output another link
+// reads, the same four values as two tagged words with agent-coherent stores.
 template <int FMT>
-__device__ __forceinline__ void store4_sc1(const v4i& D, int m, int n0, int N, float s_x, int sum_q, uint2 swq,
-                                           __amdgpu_buffer_rsrc_t yr, int32_t* __restrict__ acc_out) {
+__device__ __forceinline__ void store4_chain(const v4i& D, const ChainDesc& d, int m, int n0, float s_x, int sum_q,
+                                             uint2 swq, __amdgpu_buffer_rsrc_t tyr, uint32_t tag) {
   typedef unsigned v2u __attribute__((ext_vector_type(2)));
+  const int N = d.N;
   const uint16_t swv[4] = {(uint16_t)(swq.x & 0xFFFFu), (uint16_t)(swq.x >> 16), (uint16_t)(swq.y & 0xFFFFu),
                            (uint16_t)(swq.y >> 16)};
   int a[4];
@@ -360,16 +459,24 @@ __device__ __forceinline__ void store4_sc1(const v4i& D, int m, int n0, int N, f
     a[r] = finish_acc<FMT>(D[r], sum_q);
     h[r] = n0 + r < N ? epilogue(a[r], s_x, swv[r]) : 0;
   }
+  const uint32_t lo = (uint32_t)h[0] | ((uint32_t)h[1] << 16), hi = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+  if (d.ty) {
+    const int w0 = n0 >> 1;   // n0 is a multiple of 4; words past the row are past the buffer range
+    const uint32_t off = (uint32_t)(m * d.ywords + w0) * 8u;
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{lo, tag}, tyr, w0 < d.ywords ? off : dev::kOutOfRange, 0, 16);
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{hi, tag}, tyr, w0 + 1 < d.ywords ? off + 8 : dev::kOutOfRange, 0, 16);
+  }
+  uint16_t* __restrict__ y = d.y;
+  int32_t* __restrict__ acc_out = d.acc;
   const int64_t o = (int64_t)m * N + n0;
   if (n0 + 3 < N && (o & 3) == 0) {
-    __builtin_amdgcn_raw_buffer_store_b64(
-        v2u{(uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16)}, yr, (int)(2 * o), 0, 16);
+    *reinterpret_cast<uint2*>(y + o) = make_uint2(lo, hi);
     if (acc_out) *reinterpret_cast<int4*>(acc_out + o) = make_int4(a[0], a[1], a[2], a[3]);
   } else {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       if (n0 + r < N) {
-        __builtin_amdgcn_raw_buffer_store_b16(h[r], yr, (int)(2 * (o + r)), 0, 16);
+        y[o + r] = h[r];
         if (acc_out) acc_out[o + r] = a[r];
       }
     }
@@ -381,86 +488,24 @@ __device__ __forceinline__ void store4_sc1(const v4i& D, int m, int n0, int N, f
 // ---------------------------------------------------------------------------------------------
 // the kernel
 //
-// The waves run one of three loops over the links, each taking the same sequence of workgroup
-// barriers (per link: codes ready, then per chunk of tiles: partial sums ready, and between chunks:
-// partial sums read), so that a wave's registers hold only what its own roles need:
-//   waves 0-3   activation group 0, then the K-slice reduction, epilogue, stores and publishing;
-//   waves 4-7   activation group 1 on links with K > 4096, else weight slices 0-3 of 8;
-//   waves 8-11  weight slices: 0-3 of 4 on links with K > 4096, else 4-7 of 8.
-namespace chain {
-
-// Input of link i: wave 0 waits until every workgroup has stored its share of the producing link,
-// then releases the other activation waves of the workgroup through LDS (in_ready = i + 1).  Wave 0
-// gets here only after the previous link's publishing barrier of waves 0-3, i.e. after their last
-// reads of the partial sums, scales and code sums that this link's activation phase overwrites.
-__device__ __forceinline__ void wait_input(const ChainDesc& d, int i, int wave, unsigned* counters, unsigned G,
-                                           unsigned* in_ready, long long wait_ticks, uint32_t* err) {
-  const int lane = threadIdx.x & 63;
-  const long long t_start = wall_clock64();
-  if (wave == 0) {
-    if (d.in_link >= 0) {
-      unsigned* c = counters + d.in_link;
-      for (;;) {
-        const unsigned v = __builtin_amdgcn_readfirstlane(__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        if (v >= G) break;
-        if (wall_clock64() - t_start > wait_ticks) {
-          if (lane == 0) dev::flag_error(err, dev::kErrChainWait);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-    }
-    if (lane == 0) __hip_atomic_store(in_ready, (unsigned)(i + 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  } else {
-    for (;;) {
-      const unsigned v =
-          __builtin_amdgcn_readfirstlane(__hip_atomic_load(in_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
-      if (v >= (unsigned)(i + 1)) break;
-      if (wall_clock64() - t_start > 2 * wait_ticks) {
-        if (lane == 0) dev::flag_error(err, dev::kErrChainWait);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  asm volatile("" ::: "memory");
-}
-
-// The activation phase of link i for group gi (0: waves 0-3, 1: waves 4-7, links with K > 4096).
-template <bool PLANAR, typename GS>
-__device__ __forceinline__ void link_act(const ChainDesc& d, bool lng, int gi, const uint16_t* x0, int M, GS& gsync,
-                                         dev::GroupSync<8>& gs8, double* xch, int8_t* act_l, int Kpad, double* red_d,
-                                         int* red_i, float* s_scale) {
-  const uint16_t* xin = d.in_link < 0 ? x0 : d.x;
-  const int xstride = d.in_link < 0 ? d.K : d.xstride;
-  // the block sizes compiled in (chain_block_ok): every butterfly stage is straight-line code
-  if (!lng) {
-    switch (d.L) {
-      case 12: act_phase<1, 12, PLANAR>(d, xin, xstride, M, 1, 0, 0, 1, gsync, gsync, xch, act_l, Kpad, red_d, red_i, s_scale); break;
-      case 11: act_phase<1, 11, PLANAR>(d, xin, xstride, M, 1, 0, 0, 1, gsync, gsync, xch, act_l, Kpad, red_d, red_i, s_scale); break;
-      case 8: act_phase<1, 8, PLANAR>(d, xin, xstride, M, 1, 0, 0, 1, gsync, gsync, xch, act_l, Kpad, red_d, red_i, s_scale); break;
-      default: act_phase<1, 6, PLANAR>(d, xin, xstride, M, 1, 0, 0, 1, gsync, gsync, xch, act_l, Kpad, red_d, red_i, s_scale); break;
-    }
-    return;
-  }
-  // group 0 takes the first ceil(NT / 2) rotation tiles, group 1 the rest
-  const int NT = (d.K + 4095) / 4096, h = (NT + 1) / 2;
-  const int tau0 = gi ? h : 0, ntg = gi ? NT - h : h;
-  double* xg = xch + gi * (kXchBytes / 8);
-  switch (d.L) {
-    case 12: act_phase<2, 12, PLANAR>(d, xin, xstride, M, ntg, tau0, gi, 2, gsync, gs8, xg, act_l, Kpad, red_d, red_i, s_scale); break;
-    case 11: act_phase<2, 11, PLANAR>(d, xin, xstride, M, ntg, tau0, gi, 2, gsync, gs8, xg, act_l, Kpad, red_d, red_i, s_scale); break;
-    case 8: act_phase<2, 8, PLANAR>(d, xin, xstride, M, ntg, tau0, gi, 2, gsync, gs8, xg, act_l, Kpad, red_d, red_i, s_scale); break;
-    default: act_phase<2, 6, PLANAR>(d, xin, xstride, M, ntg, tau0, gi, 2, gsync, gs8, xg, act_l, Kpad, red_d, red_i, s_scale); break;
-  }
-}
-
-}  // namespace chain
-
+// Waves 0-3 (the activation group) and waves 4-11 (the weight waves, K-slices of 1/8 of K) run two
+// loops over the links that take the same sequence of workgroup barriers (per link: codes ready,
+// then per chunk of tiles: partial sums ready, and between chunks: partial sums read), so that a
+// wave's registers hold only what its own role needs.  The activation group goes on to the next
+// link's input as soon as this link's codes are in; after the MFMAs, weight wave 4 + j adds the
+// K-slices of tile j of the chunk, applies the epilogue and stores it, and only then issues the next
+// link's weight loads, so the stores are not queued behind them.
+// LDS: the codes [M][Kpad]; the activation group's region (its exchange buffer and the stash of up
+// to three rotation tiles), aliased by the K-slice partial sums: the group writes it for the next
+// link only once the 8 weight waves have counted themselves done with them; then the tail: s_scale,
+// red_d and red_i double-buffered by link parity (the next link's activation phase runs while this
+// link's are still read), the wave-barrier counter, the weight waves' count and 64 zero bytes.
+// Tags: the call's run number r (read at the start; the last workgroup to finish advances it) gives
+// link i the tag r n + i + 1, distinct from every earlier call's tag for the same words.
 template <int FMT>
 __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc* __restrict__ links, int n_links,
                                                                 const uint16_t* __restrict__ x0, int M, int Kpad,
-                                                                int xch_bytes, unsigned* __restrict__ counters,
+                                                                int region0, unsigned* __restrict__ counters,
                                                                 int wait_limit, long long wait_ticks,
                                                                 uint32_t* __restrict__ err) {
   using namespace chain;
@@ -475,154 +520,132 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   const int act_bytes = (M * Kpad + 15) & ~15;
   int8_t* act_l = reinterpret_cast<int8_t*>(smem);
   double* xch = reinterpret_cast<double*>(smem + act_bytes);
-  v4i* red = reinterpret_cast<v4i*>(xch);   // the K-slice partial sums reuse the exchange region
-  unsigned char* tl = smem + act_bytes + xch_bytes;
-  float* s_scale = reinterpret_cast<float*>(tl);
-  double* red_d = reinterpret_cast<double*>(tl + 16);
-  int* red_i = reinterpret_cast<int*>(tl + 16 + 256);
-  unsigned* ctr = reinterpret_cast<unsigned*>(tl + 16 + 256 + 128);   // group 0, group 1, both, input-ready
-  int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 16 + 256 + 128 + 16);
+  double* stash = xch + kXchBytes / 8;
+  v4i* red = reinterpret_cast<v4i*>(xch);   // the K-slice partial sums reuse the activation region
+  unsigned char* tl = smem + act_bytes + region0;
+  float* s_scale = reinterpret_cast<float*>(tl);                 // [2][4]
+  double* red_d = reinterpret_cast<double*>(tl + 32);            // [2][4][8]
+  int* red_i = reinterpret_cast<int*>(tl + 32 + 512);            // [2][4][8]
+  unsigned* ctr = reinterpret_cast<unsigned*>(tl + 32 + 512 + 256);   // [0] wave barrier, [3] weight waves done
+  int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 32 + 512 + 256 + 16);
   if (tid < 4) {
     ctr[tid] = 0u;
     reinterpret_cast<uint4*>(zero64)[tid] = make_uint4(0u, 0u, 0u, 0u);
   }
+  const unsigned run = __builtin_amdgcn_readfirstlane(
+      __hip_atomic_load(counters + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  const uint32_t tag_base = run * (uint32_t)n_links;
+  const long long deadline = wall_clock64() + wait_ticks;   // every wait of this call ends by then
   __syncthreads();
-  unsigned* in_ready = ctr + 3;   // 1 + the last link whose input is ready
+  unsigned* consumed = ctr + 3;   // bumped by each weight wave once it is done with a link's partial sums
 
   if (wave < 4) {
-    // ================= waves 0-3: activation group 0, reduction, epilogue, publishing
-    dev::GroupSync<4> gs0{ctr + 0, 0u, wait_limit, err};
-    dev::GroupSync<8> gs8{ctr + 2, 0u, wait_limit, err};
+    // ================= waves 0-3: the activation group
+    dev::GroupSync<4> gs{ctr + 0, 0u, wait_limit, err};
     for (int i = 0; i < n_links; ++i) {
       const ChainDesc& d = links[i];
       const Geom gm = geom(d, wg, G, TMAX);
-      uint2 swq[2] = {make_uint2(0u, 0u), make_uint2(0u, 0u)};
-      if (gm.T > 0) {
-        wait_input(d, i, wave, counters, (unsigned)G, in_ready, wait_ticks, err);
-        link_act<PLANAR>(d, gm.lng, 0, x0, M, gs0, gs8, xch, act_l, Kpad, red_d, red_i, s_scale);
-        // fp16 scales of the first chunk's tiles wave and wave + 4, in flight during the MFMAs
-        const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(d.sw, (uint32_t)(d.N * 2));
-        const int T0 = gm.T < gm.tmax ? gm.T : gm.tmax;
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-          const int j = wave + 4 * r, n = (gm.t0 + j) * 16 + 4 * g;
-          swq[r] = dev::bload8(srs, j < T0 && n < d.N ? (uint32_t)(2 * n) : dev::kOutOfRange);
-        }
-      }
+      const int par = i & 1;
+      if (gm.T > 0)
+        act_link<PLANAR>(d, x0, M, tag_base + (uint32_t)(d.in_link + 1), deadline, err, gs, xch, stash, act_l, Kpad,
+                         red_d + 32 * par, red_i + 32 * par, s_scale + 4 * par, consumed, 8u * (unsigned)i);
       dev::lds_barrier();   // codes, scales and code sums are in LDS
-      const __amdgpu_buffer_rsrc_t yr = dev::make_rsrc(d.y, (uint32_t)(M * d.N * 2));
-      const int NS = gm.lng ? 4 : 8, ngr = gm.lng ? 8 : 4;
       for (int c = 0; c < gm.nchunks; ++c) {
-        const int tile0 = gm.t0 + c * gm.tmax;
-        const int Tc = gm.T - c * gm.tmax < gm.tmax ? gm.T - c * gm.tmax : gm.tmax;
-        dev::lds_barrier();   // the slices' partial sums are in LDS
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-          const int j = wave + 4 * r;
-          if (j < Tc) {
-            v4i D = red[(j * NS) * 64 + lane];
-            for (int q = 1; q < NS; ++q) D += red[(j * NS + q) * 64 + lane];
-            const int m = r16, n0 = (tile0 + j) * 16 + 4 * g;
-            if (c > 0) {
-              const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(d.sw, (uint32_t)(d.N * 2));
-              swq[r] = dev::bload8(srs, n0 < d.N ? (uint32_t)(2 * n0) : dev::kOutOfRange);
-            }
-            if (m < M && n0 < d.N) {
-              int sq = 0;
-              for (int q = 0; q < ngr; ++q) sq += red_i[8 * m + q];
-              store4_sc1<FMT>(D, m, n0, d.N, s_scale[m], sq, swq[r], yr, d.acc);
-            }
-          }
-        }
-        if (c + 1 < gm.nchunks) dev::lds_barrier();   // the partial sums have been read
+        dev::lds_barrier();                           // partial sums are in LDS
+        if (c + 1 < gm.nchunks) dev::lds_barrier();   // partial sums have been read
       }
-      // publish: this workgroup's share of link i is stored (stores complete, then the counter)
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      gs0();
-      if (wave == 0 && lane == 0) __hip_atomic_fetch_add(counters + i, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   } else {
-    // ================= waves 4-11: weight slices (and, waves 4-7, activation group 1 on long links)
-    dev::GroupSync<4> gs1{ctr + 1, 0u, wait_limit, err};
-    dev::GroupSync<8> gs8{ctr + 2, 0u, wait_limit, err};
-    const bool mixed = wave < 8;
-    auto slice_of = [&](bool lng) { return lng ? (mixed ? -1 : wave - 8) : wave - 4; };
+    // ================= waves 4-11: weight slices, then the reduction, epilogue and stores
+    const int slice = wave - 4;
     uint4 wr[16];
+    uint2 swq = make_uint2(0u, 0u);
     auto prefetch = [&](const ChainDesc& dn) {   // the first chunk of a link, for this wave's slice
       const Geom gn = geom(dn, wg, G, TMAX);
-      const int sn = slice_of(gn.lng);
-      if (sn >= 0 && gn.T > 0) {
+      if (gn.T > 0) {
         const int T0 = gn.T < gn.tmax ? gn.T : gn.tmax;
-        if (gn.lng) load_chunk_rt<FMT, true>(wr, dn, gn.t0, T0, sn);
-        else load_chunk_rt<FMT, false>(wr, dn, gn.t0, T0, sn);
+        if (gn.lng) load_chunk_rt<FMT, true>(wr, dn, gn.t0, T0, slice);
+        else load_chunk_rt<FMT, false>(wr, dn, gn.t0, T0, slice);
+        // fp16 scales of the tile this wave stores (tile `slice` of the chunk)
+        const int n = (gn.t0 + slice) * 16 + 4 * g;
+        const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(dn.sw, (uint32_t)(dn.N * 2));
+        swq = dev::bload8(srs, slice < T0 && n < dn.N ? (uint32_t)(2 * n) : dev::kOutOfRange);
       }
     };
     prefetch(links[0]);
     for (int i = 0; i < n_links; ++i) {
       const ChainDesc& d = links[i];
       const Geom gm = geom(d, wg, G, TMAX);
-      const int slice = slice_of(gm.lng);
-      if (mixed && gm.lng) {
-        if (gm.T > 0) {
-          wait_input(d, i, wave, counters, (unsigned)G, in_ready, wait_ticks, err);
-          link_act<PLANAR>(d, true, 1, x0, M, gs1, gs8, xch, act_l, Kpad, red_d, red_i, s_scale);
-        }
-        // the weight registers hold nothing on this path: let the compiler drop them
-#pragma unroll
-        for (int k = 0; k < 16; ++k) asm volatile("" : "=v"(wr[k]));
-      }
+      const int par = i & 1;
       dev::lds_barrier();   // codes are in LDS; this wave's weight loads stay in flight
+      const uint32_t tag_out = tag_base + (uint32_t)(i + 1);
+      const __amdgpu_buffer_rsrc_t tyr = dev::make_rsrc(d.ty, (uint32_t)(M * d.ywords * 8));
       for (int c = 0; c < gm.nchunks; ++c) {
         const int tile0 = gm.t0 + c * gm.tmax;
         const int Tc = gm.T - c * gm.tmax < gm.tmax ? gm.T - c * gm.tmax : gm.tmax;
-        if (slice >= 0) {
-          if (c > 0) {
-            if (gm.lng) load_chunk_rt<FMT, true>(wr, d, tile0, Tc, slice);
-            else load_chunk_rt<FMT, false>(wr, d, tile0, Tc, slice);
-          }
-          if (gm.lng) mfma_chunk_rt<FMT, true>(wr, d, tile0, Tc, slice, act_l, Kpad, M, zero64, red);
-          else mfma_chunk_rt<FMT, false>(wr, d, tile0, Tc, slice, act_l, Kpad, M, zero64, red);
+        if (c > 0) {
+          if (gm.lng) load_chunk_rt<FMT, true>(wr, d, tile0, Tc, slice);
+          else load_chunk_rt<FMT, false>(wr, d, tile0, Tc, slice);
         }
+        if (gm.lng) mfma_chunk_rt<FMT, true>(wr, d, tile0, Tc, slice, act_l, Kpad, M, zero64, red);
+        else mfma_chunk_rt<FMT, false>(wr, d, tile0, Tc, slice, act_l, Kpad, M, zero64, red);
         dev::lds_barrier();   // the slices' partial sums are in LDS
+        if (slice < Tc) {
+          // this wave's tile: add the K-slices, apply the epilogue and store
+          const int n0 = (tile0 + slice) * 16 + 4 * g, m = r16;
+          if (c > 0) {
+            const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(d.sw, (uint32_t)(d.N * 2));
+            swq = dev::bload8(srs, n0 < d.N ? (uint32_t)(2 * n0) : dev::kOutOfRange);
+          }
+          v4i D = red[(slice * 8) * 64 + lane];
+#pragma unroll
+          for (int q = 1; q < 8; ++q) D += red[(slice * 8 + q) * 64 + lane];
+          if (m < M && n0 < d.N) {
+            const int* ri = red_i + 32 * par + 8 * m;
+            store4_chain<FMT>(D, d, m, n0, s_scale[4 * par + m], ri[0] + ri[1] + ri[2] + ri[3], swq, tyr, tag_out);
+          }
+        }
         if (c + 1 < gm.nchunks) dev::lds_barrier();   // the partial sums have been read
       }
+      // done with this link's partial sums (the LDS reads have returned)
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      if (lane == 0) __hip_atomic_fetch_add(consumed, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       // every weight register has been consumed: no entry stays live into the next MFMA phase
 #pragma unroll
       for (int k = 0; k < 16; ++k) asm volatile("" : "=v"(wr[k]));
-      if (i + 1 < n_links) prefetch(links[i + 1]);   // the next link's weights stream during its wait
+      if (i + 1 < n_links) prefetch(links[i + 1]);   // behind this wave's stores: the next link's weights
     }
   }
 
-  // the last workgroup to finish returns the counters to zero for the next call (every workgroup has
-  // passed all of its waits by then)
+  // the last workgroup to finish resets the arrival count and advances the run number (every
+  // workgroup has read the run number at its start and passed all of its waits by then)
   __syncthreads();
   if (wave == 0) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this workgroup's counter increments have been performed
     unsigned prev = 0;
-    if (lane == 0) prev = __hip_atomic_fetch_add(counters + n_links, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0) prev = __hip_atomic_fetch_add(counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     prev = __builtin_amdgcn_readfirstlane(prev);
-    if (prev == (unsigned)G - 1) {
-      for (int k = lane; k <= n_links; k += 64) __hip_atomic_store(counters + k, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == (unsigned)G - 1 && lane == 0) {
+      __hip_atomic_store(counters, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(counters + 1, run + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
 
 template <int FMT>
-hipError_t launch_chain_fmt(const ChainDesc* links, int n_links, const uint16_t* x0, int M, int Kmax, bool any_long,
+hipError_t launch_chain_fmt(const ChainDesc* links, int n_links, const uint16_t* x0, int M, int Kmax, int region0,
                             int grid, unsigned* counters, hipStream_t s) {
   const int Kpad = Kmax + 16;
-  const int xch = (int)chain_xch_bytes(any_long, FMT == mma::FMT_W4);
-  const size_t shmem = chain_lds_bytes(M, Kmax, any_long, FMT == mma::FMT_W4);
+  const size_t shmem = chain_lds_bytes(M, Kmax, region0);
   if (shmem > 160 * 1024) return hipErrorInvalidValue;
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_decode_chain<FMT>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   if (attr != hipSuccess) return attr;
   const int limit = wait_limit();
   // bounded waits for other workgroups: wait_limit spins of the in-workgroup barriers correspond to
-  // 25 ticks of the 100 MHz real-time clock each (about 1 s at the default)
+  // 25 ticks of the 100 MHz real-time clock each (about 1 s for the whole call at the default)
   const long long ticks = (long long)limit * 25;
   hipLaunchKernelGGL((k_decode_chain<FMT>), dim3(grid), dim3(kChainThreads), shmem, s, links, n_links, x0, M, Kpad,
-                     xch, counters, limit, ticks, device_error_word());
+                     region0, counters, limit, ticks, device_error_word());
   return hipGetLastError();
 }
 

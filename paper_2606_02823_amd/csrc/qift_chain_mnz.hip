@@ -4,9 +4,9 @@
 
 namespace qift {
 
-hipError_t launch_chain_mnz(const ChainDesc* links, int n_links, const uint16_t* x0, int M, int Kmax, bool any_long,
+hipError_t launch_chain_mnz(const ChainDesc* links, int n_links, const uint16_t* x0, int M, int Kmax, int region0,
                           int grid, unsigned* counters, hipStream_t s) {
-  return launch_chain_fmt<mma::FMT_MNZ>(links, n_links, x0, M, Kmax, any_long, grid, counters, s);
+  return launch_chain_fmt<mma::FMT_MNZ>(links, n_links, x0, M, Kmax, region0, grid, counters, s);
 }
 
 }  // namespace qift

@@ -95,35 +95,40 @@ int wait_limit();
 constexpr int kDefaultWaitLimit = 1 << 22;
 
 // Persistent decode chain (qift_chain.h, qift_chain_<fmt>.hip): one link of a prepared chain as the
-// kernel reads it (written to device memory by the prepare call).
+// kernel reads it (written to device memory by the prepare call).  A link whose output another link
+// reads also writes it as tagged words ty [M][ywords] (two fp16 values in the low half, the tag in
+// the high half of each 8 bytes); its consumers read element k of token m from word (xoff + k) / 2 of
+// row m of tx (rows of xwords words).
 struct ChainDesc {
   const uint32_t* P;     // packed words [N][K/16] (W2) or [N][K/8] (W4)
   const uint16_t* sw;    // fp16 s_w [N]
-  const uint16_t* x;     // input of token 0 (nullptr: the chain input); token m at x + m * xstride
+  const uint64_t* tx;    // tagged input words (nullptr: the chain input)
+  uint64_t* ty;          // tagged output words (nullptr: no link reads this output)
   uint16_t* y;           // fp16 output [M][N]
   int32_t* acc;          // nullable int32 [M][N]
   double denom;          // (den * 7) * sqrt(block)
-  int32_t N, K, L, num, den, in_link, xstride, tiles;
+  int32_t N, K, L, num, den, in_link, xoff, xwords, ywords, tiles;
 };
 constexpr int kChainMaxM = 4;
 // Hadamard blocks of the chain's links: 64, 256, 2048 and 4096 (the block exponent is compiled in)
 inline bool chain_block_ok(int block) { return block == 64 || block == 256 || block == 2048 || block == 4096; }
 constexpr int kChainMaxK = 16384;
 constexpr int kChainMaxLinks = 4096;
-constexpr int kChainTailBytes = 480;
+constexpr int kChainTailBytes = 880;
 constexpr int kChainXchBytes = (4096 + 512) * 8;   // one rotation exchange buffer (a 4096-tile, padded)
-// Exchange / partial-sum region: partial sums of 8 slices x 7 (W4: 3) tiles, or one exchange buffer
-// per activation group (two when a link has K > 4096).
-inline size_t chain_xch_bytes(bool any_long, bool w4) {
-  const size_t part = (size_t)8 * (w4 ? 3 : 7) * 1024;
-  const size_t xch = (any_long ? 2 : 1) * (size_t)kChainXchBytes;
-  return part > xch ? part : xch;
+constexpr int kChainStashBytes = 4096 * 8;         // one rotation tile of fp64 values
+// LDS region of the activation group: its exchange buffer and a stash of NT - 1 rotation tiles (NT
+// the most tiles of a link, K <= 4096 NT each), aliased by the K-slice partial sums (8 slices x 7,
+// W4 3, tiles).
+inline int chain_region0(int max_tiles, bool w4) {
+  const int own = kChainXchBytes + (max_tiles - 1) * kChainStashBytes, part = 8 * (w4 ? 3 : 7) * 1024;
+  return own > part ? own : part;
 }
-inline size_t chain_lds_bytes(int64_t M, int64_t Kmax, bool any_long, bool w4) {
-  return (size_t)((M * (Kmax + 16) + 15) & ~int64_t(15)) + chain_xch_bytes(any_long, w4) + kChainTailBytes;
+inline size_t chain_lds_bytes(int64_t M, int64_t Kmax, int region0) {
+  return (size_t)((M * (Kmax + 16) + 15) & ~int64_t(15)) + (size_t)region0 + kChainTailBytes;
 }
-#define QIFT_CHAIN_LAUNCHER(NAME)                                                                              \
-  hipError_t NAME(const ChainDesc* links, int n_links, const uint16_t* x0, int M, int Kmax, bool any_long, int grid, \
+#define QIFT_CHAIN_LAUNCHER(NAME)                                                                                \
+  hipError_t NAME(const ChainDesc* links, int n_links, const uint16_t* x0, int M, int Kmax, int region0, int grid, \
                   unsigned* counters, hipStream_t s)
 QIFT_CHAIN_LAUNCHER(launch_chain_mnz);
 QIFT_CHAIN_LAUNCHER(launch_chain_pot);

@@ -72,7 +72,7 @@ class ChainLinkC(ctypes.Structure):
 
 class ChainC(ctypes.Structure):
     _fields_ = [("fmt", ctypes.c_int32), ("n_links", ctypes.c_int32), ("M", ctypes.c_int32), ("K0", ctypes.c_int32),
-                ("grid", ctypes.c_int32), ("kmax", ctypes.c_int32), ("any_long", ctypes.c_int32),
+                ("grid", ctypes.c_int32), ("kmax", ctypes.c_int32), ("region0", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("table", ctypes.c_void_p), ("counters", ctypes.c_void_p)]
 
 
@@ -112,7 +112,7 @@ def lib():
         "qift_last_hip_error": (ctypes.c_int, []),
         "qift_device_error": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint32), i32, vp]),
         "qift_set_wait_limit": (ctypes.c_int, [i32]),
-        "qift_chain_workspace_bytes": (sz, [i32]),
+        "qift_chain_workspace_bytes": (sz, [ctypes.POINTER(ChainLinkC), i32, i64]),
         "qift_chain_prepare": (ctypes.c_int, [ctypes.POINTER(ChainLinkC), i32, i64, i64, vp, sz, ctypes.POINTER(ChainC),
                                               vp]),
         "qift_decode_chain": (ctypes.c_int, [ctypes.POINTER(ChainC), vp, vp]),
@@ -441,14 +441,12 @@ class Chain:
         self.outs = [torch.empty((M, l.w.N), dtype=torch.float16, device=device) for l in self.links]
         self.accs = [torch.empty((M, l.w.N), dtype=torch.int32, device=device) for l in self.links] if acc else None
         n = len(self.links)
-        nbytes = int(lib().qift_chain_workspace_bytes(n))
-        if nbytes == 0:
-            raise ValueError(f"a chain holds 1..4096 links, got {n}")
-        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
         arr = (ChainLinkC * n)()
         for i, l in enumerate(self.links):
             arr[i] = ChainLinkC(l.w.cview(), l.block, clip_flags(*l.clip), l.in_link, 0, l.in_offset,
                                 self.outs[i].data_ptr(), None if acc is False else self.accs[i].data_ptr())
+        nbytes = int(lib().qift_chain_workspace_bytes(arr, n, M))
+        self.workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
         self.c = ChainC()
         _check("qift_chain_prepare", lib().qift_chain_prepare(arr, n, M, self.K0, self.workspace.data_ptr(), nbytes,
                                                                ctypes.byref(self.c), _stream(stream)))

@@ -100,10 +100,10 @@ def llama31_layers(fmt, layers, seed0=0):
     return specs
 
 
-@pytest.mark.parametrize("M", [1, 4])
-def test_chain_two_llama31_layers_mnz(Q, M):
+def test_chain_two_llama31_layers_mnz(Q):
     """Two LLaMA-3.1-8B decode layers chained (8 links, the real shapes and dependencies): bit-exact,
     on three runs with different inputs (the second and third would expose stale reads)."""
+    M = 1
     specs = llama31_layers(levels.FMT_W2_MNZ, 2)
     chain, _ = build(Q, specs, M)
     for r in range(3):
@@ -125,15 +125,47 @@ def mixed_specs(fmt):
             Spec(fmt, 2064, 8192, 2048, 5, 64, 7)]
 
 
-@pytest.mark.parametrize("fmt,M", [(levels.FMT_W2_MNZ, 1), (levels.FMT_W2_MNZ, 3), (levels.FMT_W2_POT, 1),
-                                   (levels.FMT_W4_SYM, 3)])
-def test_chain_mixed_shapes(Q, fmt, M):
+def multi_token_specs(fmt):
+    """Links with K <= 8192 (several tokens per call fit in LDS): 1 and 2 rotation tiles, every block,
+    idle workgroups and several chunks."""
+    return [Spec(fmt, 1040, 4096, 4096, -1, 0, 11),
+            Spec(fmt, 8208, 1024, 256, 0, 8, 12),
+            Spec(fmt, 20000, 8192, 2048, 1, 8, 13),
+            Spec(fmt, 4112, 4096, 4096, 2, 4000, 14),
+            Spec(fmt, 30000, 4096, 64, 3, 0, 15),
+            Spec(fmt, 496, 8192, 4096, 4, 2048, 16)]
+
+
+@pytest.mark.parametrize("fmt", [levels.FMT_W2_MNZ, levels.FMT_W2_POT, levels.FMT_W4_SYM])
+def test_chain_mixed_shapes(Q, fmt):
+    M = 1
     specs = mixed_specs(fmt)
     chain, _ = build(Q, specs, M)
     for r in range(2):
         x = synth.activations_fp16(82, 10 * fmt + r, 0, M, 4096, 41, 30.0)
         check_run(Q, chain, specs, x)
     assert Q.device_error() == 0
+
+
+@pytest.mark.parametrize("fmt,M", [(levels.FMT_W2_MNZ, 4), (levels.FMT_W2_POT, 2), (levels.FMT_W4_SYM, 3)])
+def test_chain_multi_token(Q, fmt, M):
+    specs = multi_token_specs(fmt)
+    chain, _ = build(Q, specs, M)
+    for r in range(2):
+        x = synth.activations_fp16(86, 10 * fmt + r, 0, M, 4096, 41, 30.0)
+        check_run(Q, chain, specs, x)
+    assert Q.device_error() == 0
+
+
+def test_chain_rejects_what_does_not_fit(Q):
+    # two tokens next to a K = 14336 link exceed one workgroup's LDS; a block the kernel was not
+    # compiled for is refused
+    specs = llama31_layers(levels.FMT_W2_MNZ, 1, seed0=50)
+    with pytest.raises(Q.QiftError, match="QIFT_ERR_SHAPE"):
+        build(Q, specs, 2)
+    specs = [Spec(levels.FMT_W2_MNZ, 512, 4096, 1024, -1, 0, 51)]
+    with pytest.raises(Q.QiftError, match="QIFT_ERR_SPEC"):
+        build(Q, specs, 1)
 
 
 def test_chain_graph_replay(Q):
@@ -191,7 +223,7 @@ def test_chain_wait_gives_up_and_is_reported(Q):
 
 def test_chain_matches_fused_entry(Q):
     """Each link of a chain equals qift_rotate_quant_linear on the same input, bit for bit."""
-    specs = mixed_specs(levels.FMT_W2_POT)[:3]
+    specs = multi_token_specs(levels.FMT_W2_POT)[:4]
     chain, pks = build(Q, specs, 2)
     x = synth.activations_fp16(85, 0, 0, 2, 4096, 41, 30.0)
     chain.run(_dev(x))
