@@ -356,15 +356,15 @@ typedef struct {
 
 /*
  * Workspace bytes of a chain (host links, n_links of them, M tokens): the link table, two counters,
- * and for every link whose output another link reads, that output again as tagged words
- * (M x ceil(N/2) x 8 bytes: two fp16 values and the 32-bit tag of the producing call and link).
+ * and for every link whose output another link reads, two exchange copies of that output
+ * (2 x M x N8 fp16 values, N8 = N rounded up to a multiple of 8), each buffer 256-byte aligned.
  * 0 for a chain that qift_chain_prepare would reject.
  */
 size_t qift_chain_workspace_bytes(const qift_chain_link *links, int32_t n_links, int64_t M);
 
 /*
- * Validate the links, write the link table, the counters and zeroed tagged buffers into the
- * workspace and fill *chain.  An offline call: it SYNCHRONIZES the stream (the table is copied
+ * Validate the links, write the link table, the counters and the exchange copies (every value
+ * marked not written, 0xFFFF) into the workspace and fill *chain.  An offline call: it SYNCHRONIZES the stream (the table is copied
  * from host memory); not capturable in a HIP graph.
  *   links      host: n_links links (1 <= n_links <= 4096).
  *   M          tokens per call, 1..4, as far as one workgroup's LDS holds M tokens' codes next to
@@ -384,9 +384,11 @@ int qift_chain_prepare(const qift_chain_link *links, int32_t n_links, int64_t M,
  * Run one decode step of a prepared chain on the tokens x (device, fp16 [M][K0], 16-byte
  * aligned, not overlapping any link's output).  Asynchronous; capturable in a HIP graph (one
  * kernel launch).  The grid is one workgroup per CU and relies on all of them running at once:
- * calls must not overlap one another on a device (they share the chain's counters and tagged
- * buffers, and a concurrent kernel that holds CUs delays the grid).  A link waits for its input
- * words to carry the producing link's tag of this call; a wait that gives up (the call not done
+ * calls must not overlap one another on a device (they share the chain's counters and exchange
+ * buffers, and a concurrent kernel that holds CUs delays the grid).  Call r (counted from 1 by the
+ * chain) writes copy r mod 2 of each exchange buffer and marks the other copy not written; a link
+ * waits until none of its input values in copy r mod 2 is 0xFFFF (a NaN output reaches the next
+ * link as the quiet NaN 0xFE00).  A wait that gives up (the call not done
  * within about a second) sets QIFT_DEVERR_CHAIN_WAIT in the device error word
  * (qift_device_error) and the results of that call are not to be trusted.
  */

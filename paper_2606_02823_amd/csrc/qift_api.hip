@@ -333,8 +333,9 @@ size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 constexpr size_t kChainCounterBytes = 256;   // the arrival count and the run number, padded
 
 // Host-side checks of a chain and the device link table (every check before any HIP call).  With a
-// workspace base, the tagged output buffers of the links whose output another link reads are laid
-// out after the table and the counters; *ws_bytes receives the workspace size either way.
+// workspace base, the exchange buffers of the links whose output another link reads (two copies of
+// the fp16 output, rows padded to 8 values) are laid out after the table and the counters;
+// *ws_bytes receives the workspace size either way.
 int chain_build(const qift_chain_link* links, int32_t n, int64_t M, int64_t K0, unsigned char* ws,
                 std::vector<qift::ChainDesc>& d, size_t* ws_bytes, int64_t* kmax_out, int* region0) {
   if (!links) return QIFT_ERR_NULL;
@@ -387,22 +388,22 @@ int chain_build(const qift_chain_link* links, int32_t n, int64_t M, int64_t K0, 
     e.den = den;
     e.in_link = l.in_link;
     e.xoff = (int32_t)l.in_offset;
-    e.ywords = (int32_t)((w.N + 1) / 2);
+    e.ystride = (int32_t)((w.N + 7) & ~int64_t(7));
     e.tiles = (int32_t)((w.N + 15) / 16);
     kmax = w.K > kmax ? w.K : kmax;
   }
-  // workspace: link table, counters, then the tagged outputs of the links that are read
+  // workspace: link table, counters, then the exchange buffers of the links that are read
   size_t off = align256((size_t)n * sizeof(qift::ChainDesc)) + kChainCounterBytes;
   for (int32_t i = 0; i < n; ++i) {
     if (!consumed[(size_t)i]) continue;
-    d[(size_t)i].ty = ws ? reinterpret_cast<uint64_t*>(ws + off) : nullptr;
-    off += align256((size_t)M * (size_t)d[(size_t)i].ywords * 8);
+    d[(size_t)i].ty = ws ? reinterpret_cast<uint16_t*>(ws + off) : nullptr;
+    off += align256(2 * (size_t)M * (size_t)d[(size_t)i].ystride * 2);
   }
   for (int32_t i = 0; i < n; ++i) {
     const int32_t in = d[(size_t)i].in_link;
     if (in >= 0) {
       d[(size_t)i].tx = d[(size_t)in].ty;
-      d[(size_t)i].xwords = d[(size_t)in].ywords;
+      d[(size_t)i].xstride = d[(size_t)in].ystride;
     }
   }
   *ws_bytes = off;
@@ -443,9 +444,10 @@ int qift_chain_prepare(const qift_chain_link* links, int32_t n_links, int64_t M,
   const hipStream_t s = (hipStream_t)stream;
   const size_t table = align256((size_t)n_links * sizeof(qift::ChainDesc));
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws + table);
-  static const uint32_t start[2] = {0u, 1u};   // arrival count 0, run number 1 (tags of zeroed words are 0)
+  static const uint32_t start[2] = {0u, 1u};   // arrival count 0, run number 1
   st = hip_status(hipMemcpyAsync(ws, d.data(), (size_t)n_links * sizeof(qift::ChainDesc), hipMemcpyHostToDevice, s));
-  if (st == QIFT_OK) st = hip_status(hipMemsetAsync(ws + table, 0, need - table, s));
+  // every exchange value starts as not written (0xFFFF)
+  if (st == QIFT_OK) st = hip_status(hipMemsetAsync(ws + table, 0xFF, need - table, s));
   if (st == QIFT_OK) st = hip_status(hipMemcpyAsync(counters, start, sizeof(start), hipMemcpyHostToDevice, s));
   if (st == QIFT_OK) st = hip_status(hipStreamSynchronize(s));
   if (st != QIFT_OK) return st;

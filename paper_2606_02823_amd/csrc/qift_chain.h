@@ -79,7 +79,12 @@ __device__ __forceinline__ void load_chunk(uint4 (&wr)[16], const ChainDesc& d, 
   constexpr int NS = 8;
   constexpr int UPT = LONG ? 8 : 2;
   static_assert(T * UPT * NH <= 16, "weight registers");
-  const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+  // opaque lane index: the row offsets are computed per call rather than hoisted out of the link loop
+  // (kept live across it they spill, and each spill reload's wait on the vector memory counter would
+  // also wait for the loads just issued, one pair at a time)
+  int lane = threadIdx.x & 63;
+  asm volatile("" : "+v"(lane));
+  const int r16 = lane & 15, g = lane >> 4;
   const int K = d.K, N = d.N;
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
   const int NC = (K + NS * 256 - 1) / (NS * 256);
@@ -250,69 +255,59 @@ __device__ __forceinline__ void mfma_chunk_rt(uint4 (&wr)[16], const ChainDesc& 
 
 // One token's input for the activation group: 16 consecutive elements of each of the NT rotation
 // tiles per thread (fp16 bits, 32 bytes per tile), element e = 4096 tau + 16 t + i.  The chain input
-// x0 is read directly; a link's output is read from its tagged words (two fp16 values and a 32-bit
-// tag per 8 bytes, written with agent-coherent stores) with agent-coherent loads, every tile's loads
-// at once, until every word carries the producing link's tag of this call: the data and its
-// readiness arrive in the same access, so no separate flag or counter is needed.  The wait is
-// bounded by the deadline (100 MHz ticks); a wave that gives up sets kErrChainWait.
-__device__ __forceinline__ void fetch_tiles(uint4 (&raw)[4][2], const ChainDesc& d, const uint16_t* x0, int m, int NT,
-                                            int t, uint32_t tag, long long deadline, uint32_t* err) {
-  typedef unsigned v2u __attribute__((ext_vector_type(2)));
-  if (d.in_link < 0) {
-    const __amdgpu_buffer_rsrc_t r = dev::make_rsrc(x0 + (int64_t)m * d.K, (uint32_t)(d.K * 2));
+// x0 is read directly.  A link's output is read from its exchange copy of this call (the copy of the
+// call's parity, written with agent-coherent stores) with agent-coherent loads, every tile's loads
+// at once, until none of a wave's values is the not-written pattern kUnwritten: the data and its
+// readiness arrive in the same access, so no flag or counter is needed.  Each lane reads its 16
+// consecutive inputs as two 16-byte loads.  The wait is bounded by the deadline (100 MHz ticks); a
+// wave that gives up sets kErrChainWait.
+// 1 if a value of the 8 in a is kUnwritten (branch-free: the loads of a polling round stay in flight
+// together)
+__device__ __forceinline__ uint32_t unwritten8(const uint4& a) {
+  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+  uint32_t bad = 0;
 #pragma unroll
-    for (int tau = 0; tau < 4; ++tau) {
-      const int e0 = tau * 4096 + 16 * t;
-      const uint32_t off = tau < NT && e0 < d.K ? (uint32_t)(e0 * 2) : dev::kOutOfRange;   // past K: zeros
-      raw[tau][0] = dev::bload16(r, off);
-      raw[tau][1] = dev::bload16(r, off + 16);
-    }
-    return;
-  }
-  const __amdgpu_buffer_rsrc_t r = dev::make_rsrc(d.tx + (int64_t)m * d.xwords, (uint32_t)(d.xwords * 8));
+  for (int k = 0; k < 4; ++k) bad |= (uint32_t)((w[k] & 0xFFFFu) == kUnwritten) | (uint32_t)(w[k] >= 0xFFFF0000u);
+  return bad;
+}
+
+__device__ __forceinline__ void fetch_tiles(uint4 (&raw)[4][2], const ChainDesc& d, const uint16_t* x0, int M, int m,
+                                            int NT, int t, int par, long long deadline, uint32_t* err) {
+  typedef unsigned v4u __attribute__((ext_vector_type(4)));
+  const bool from_x0 = d.in_link < 0;
+  const uint16_t* src = from_x0 ? x0 + (int64_t)m * d.K : d.tx + ((int64_t)par * M + m) * d.xstride + d.xoff;
+  const __amdgpu_buffer_rsrc_t r = dev::make_rsrc(src, (uint32_t)(d.K * 2));   // past K: zeros
   uint32_t off[4];
 #pragma unroll
   for (int tau = 0; tau < 4; ++tau) {
     const int e0 = tau * 4096 + 16 * t;
-    off[tau] = tau < NT && e0 < d.K ? (uint32_t)((d.xoff + e0) / 2) * 8u : dev::kOutOfRange;
+    off[tau] = tau < NT && e0 < d.K ? (uint32_t)(e0 * 2) : dev::kOutOfRange;
   }
-  // A lane's eight words of a tile are one 16-row tile of the producing link, stored by one wave of
-  // one workgroup: wait on the last of them (one load per tile per round, with a pause between
-  // rounds, so that the polling does not crowd the memory pipeline that this CU's own stores use),
-  // then read them all and check every tag.
-  for (;;) {
-    bool seen = true;
+  if (from_x0) {
 #pragma unroll
     for (int tau = 0; tau < 4; ++tau) {
-      const v2u v = __builtin_amdgcn_raw_buffer_load_b64(r, off[tau] + 56, 0, 16);
-      seen = seen && (off[tau] == dev::kOutOfRange || v[1] == tag);
+      raw[tau][0] = dev::bload16(r, off[tau]);
+      raw[tau][1] = dev::bload16(r, off[tau] + 16);
     }
-    if (__all(seen) || wall_clock64() > deadline) break;
-    __builtin_amdgcn_s_sleep(8);
+    return;
   }
   for (;;) {
-    v2u w[4][8];
 #pragma unroll
     for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
-      for (int q = 0; q < 8; ++q) w[tau][q] = __builtin_amdgcn_raw_buffer_load_b64(r, off[tau] + 8 * q, 0, 16);
-    bool ok = true;
-#pragma unroll
-    for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-      for (int q = 0; q < 8; ++q) ok = ok && (off[tau] == dev::kOutOfRange || w[tau][q][1] == tag);
-    const bool done = __all(ok);
-    const bool late = !done && wall_clock64() > deadline;
-    if (done || late) {
-      if (late && (threadIdx.x & 63) == 0) dev::flag_error(err, dev::kErrChainWait);
-#pragma unroll
-      for (int tau = 0; tau < 4; ++tau) {
-        raw[tau][0] = make_uint4(w[tau][0][0], w[tau][1][0], w[tau][2][0], w[tau][3][0]);
-        raw[tau][1] = make_uint4(w[tau][4][0], w[tau][5][0], w[tau][6][0], w[tau][7][0]);
+      for (int h = 0; h < 2; ++h) {
+        const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, off[tau] + 16 * h, 0, 16);
+        raw[tau][h] = make_uint4(v[0], v[1], v[2], v[3]);
       }
+    uint32_t bad = 0;
+#pragma unroll
+    for (int tau = 0; tau < 4; ++tau) bad |= unwritten8(raw[tau][0]) | unwritten8(raw[tau][1]);
+    if (__all(bad == 0)) return;
+    if (wall_clock64() > deadline) {
+      if ((threadIdx.x & 63) == 0) dev::flag_error(err, dev::kErrChainWait);
       return;
     }
-    __builtin_amdgcn_s_sleep(8);
+    __builtin_amdgcn_s_sleep(2);
   }
 }
 
@@ -353,7 +348,7 @@ __device__ __forceinline__ int codes16(const double (&v)[16], const dev::QuantPa
 // polling loads (polling that overlapped them was measured to starve them), and the previous link's
 // partial sums, which share the group's LDS region, have been read.
 template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t* x0, int m, int NT, uint32_t tag,
+__device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t* x0, int M, int m, int NT, int par,
                                               long long deadline, uint32_t* err, GS& gsync, double* xch,
                                               double* stash, int8_t* dst, double* red_d, int* red_i,
                                               const unsigned* consumed, unsigned consumed_target) {
@@ -379,7 +374,7 @@ __device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t
     asm volatile("" ::: "memory");
   }
   uint4 raw[4][2];
-  fetch_tiles(raw, d, x0, m, NT, t, tag, deadline, err);
+  fetch_tiles(raw, d, x0, M, m, NT, t, par, deadline, err);
   double v[16];
   double amax = 0.0;
   int wend = 0;
@@ -420,7 +415,7 @@ __device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t
 
 // The activation phase of one link: every token; the scale of token m goes to s_scale[m].
 template <bool PLANAR, typename GS>
-__device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0, int M, uint32_t tag,
+__device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0, int M, int par,
                                          long long deadline, uint32_t* err, GS& gsync, double* xch, double* stash,
                                          int8_t* act_l, int Kpad, double* red_d, int* red_i, float* s_scale,
                                          const unsigned* consumed, unsigned consumed_target) {
@@ -430,13 +425,13 @@ __device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0,
     const unsigned* cw = m == 0 ? consumed : nullptr;
     // the block sizes compiled in (chain_block_ok): every butterfly stage is straight-line code
     switch (d.L) {
-      case 12: A = quant_group<12, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+      case 12: A = quant_group<12, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
                                            red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
-      case 11: A = quant_group<11, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+      case 11: A = quant_group<11, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
                                            red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
-      case 8: A = quant_group<8, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+      case 8: A = quant_group<8, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
                                          red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
-      default: A = quant_group<6, PLANAR>(d, x0, m, NT, tag, deadline, err, gsync, xch, stash, act_l + m * Kpad,
+      default: A = quant_group<6, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
                                           red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
     }
     if (threadIdx.x == 0) s_scale[m] = (float)((A * (double)d.num) / d.denom);
@@ -444,10 +439,12 @@ __device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0,
 }
 
 // y[m][n0 .. n0 + 3] (fp16, and the accumulators) and, for the links whose output another link
-// reads, the same four values as two tagged words with agent-coherent stores.
+// reads, the same four values into this call's exchange copy (a value equal to kUnwritten, a NaN,
+// becomes the quiet NaN 0xFE00 there) and kUnwritten into the other copy (the one the next call
+// writes; its readers of the previous call have finished), both with agent-coherent stores.
 template <int FMT>
-__device__ __forceinline__ void store4_chain(const v4i& D, const ChainDesc& d, int m, int n0, float s_x, int sum_q,
-                                             uint2 swq, __amdgpu_buffer_rsrc_t tyr, uint32_t tag) {
+__device__ __forceinline__ void store4_chain(const v4i& D, const ChainDesc& d, int M, int m, int n0, float s_x,
+                                             int sum_q, uint2 swq, __amdgpu_buffer_rsrc_t tyr, int par) {
   typedef unsigned v2u __attribute__((ext_vector_type(2)));
   const int N = d.N;
   const uint16_t swv[4] = {(uint16_t)(swq.x & 0xFFFFu), (uint16_t)(swq.x >> 16), (uint16_t)(swq.y & 0xFFFFu),
@@ -461,15 +458,21 @@ __device__ __forceinline__ void store4_chain(const v4i& D, const ChainDesc& d, i
   }
   const uint32_t lo = (uint32_t)h[0] | ((uint32_t)h[1] << 16), hi = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
   if (d.ty) {
-    const int w0 = n0 >> 1;   // n0 is a multiple of 4; words past the row are past the buffer range
-    const uint32_t off = (uint32_t)(m * d.ywords + w0) * 8u;
-    __builtin_amdgcn_raw_buffer_store_b64(v2u{lo, tag}, tyr, w0 < d.ywords ? off : dev::kOutOfRange, 0, 16);
-    __builtin_amdgcn_raw_buffer_store_b64(v2u{hi, tag}, tyr, w0 + 1 < d.ywords ? off + 8 : dev::kOutOfRange, 0, 16);
+    uint32_t e[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) e[r] = h[r] == kUnwritten ? 0xFE00u : h[r];
+    const uint32_t row = (uint32_t)((par * M + m) * d.ystride), other = (uint32_t)(((1 - par) * M + m) * d.ystride);
+    const bool in = n0 < N;   // rows past N (the rest of a 16-row tile) stay out of the copies
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{e[0] | (e[1] << 16), e[2] | (e[3] << 16)}, tyr,
+                                          in ? (row + n0) * 2u : dev::kOutOfRange, 0, 16);
+    uint32_t ones;   // the not-written pattern, made here (a constant kept from earlier would be spilled)
+    asm volatile("v_mov_b32 %0, -1" : "=v"(ones));
+    __builtin_amdgcn_raw_buffer_store_b64(v2u{ones, ones}, tyr, in ? (other + n0) * 2u : dev::kOutOfRange, 0, 16);
   }
   uint16_t* __restrict__ y = d.y;
   int32_t* __restrict__ acc_out = d.acc;
   const int64_t o = (int64_t)m * N + n0;
-  if (n0 + 3 < N && (o & 3) == 0) {
+  if (n0 + 3 < N && (((uint32_t)m * (uint32_t)N + (uint32_t)n0) & 3u) == 0) {
     *reinterpret_cast<uint2*>(y + o) = make_uint2(lo, hi);
     if (acc_out) *reinterpret_cast<int4*>(acc_out + o) = make_int4(a[0], a[1], a[2], a[3]);
   } else {
@@ -500,8 +503,8 @@ __device__ __forceinline__ void store4_chain(const v4i& D, const ChainDesc& d, i
 // link only once the 8 weight waves have counted themselves done with them; then the tail: s_scale,
 // red_d and red_i double-buffered by link parity (the next link's activation phase runs while this
 // link's are still read), the wave-barrier counter, the weight waves' count and 64 zero bytes.
-// Tags: the call's run number r (read at the start; the last workgroup to finish advances it) gives
-// link i the tag r n + i + 1, distinct from every earlier call's tag for the same words.
+// Exchange copies: the call's run number r (read at the start; the last workgroup to finish advances
+// it) selects copy r mod 2 of every exchange buffer.
 template <int FMT>
 __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc* __restrict__ links, int n_links,
                                                                 const uint16_t* __restrict__ x0, int M, int Kpad,
@@ -534,7 +537,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   }
   const unsigned run = __builtin_amdgcn_readfirstlane(
       __hip_atomic_load(counters + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-  const uint32_t tag_base = run * (uint32_t)n_links;
+  const int rpar = (int)(run & 1u);
   const long long deadline = wall_clock64() + wait_ticks;   // every wait of this call ends by then
   __syncthreads();
   unsigned* consumed = ctr + 3;   // bumped by each weight wave once it is done with a link's partial sums
@@ -547,7 +550,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
       if (gm.T > 0)
-        act_link<PLANAR>(d, x0, M, tag_base + (uint32_t)(d.in_link + 1), deadline, err, gs, xch, stash, act_l, Kpad,
+        act_link<PLANAR>(d, x0, M, rpar, deadline, err, gs, xch, stash, act_l, Kpad,
                          red_d + 32 * par, red_i + 32 * par, s_scale + 4 * par, consumed, 8u * (unsigned)i);
       dev::lds_barrier();   // codes, scales and code sums are in LDS
       for (int c = 0; c < gm.nchunks; ++c) {
@@ -578,8 +581,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
       dev::lds_barrier();   // codes are in LDS; this wave's weight loads stay in flight
-      const uint32_t tag_out = tag_base + (uint32_t)(i + 1);
-      const __amdgpu_buffer_rsrc_t tyr = dev::make_rsrc(d.ty, (uint32_t)(M * d.ywords * 8));
+      const __amdgpu_buffer_rsrc_t tyr = dev::make_rsrc(d.ty, (uint32_t)(2 * M * d.ystride * 2));
       for (int c = 0; c < gm.nchunks; ++c) {
         const int tile0 = gm.t0 + c * gm.tmax;
         const int Tc = gm.T - c * gm.tmax < gm.tmax ? gm.T - c * gm.tmax : gm.tmax;
@@ -591,18 +593,23 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
         else mfma_chunk_rt<FMT, false>(wr, d, tile0, Tc, slice, act_l, Kpad, M, zero64, red);
         dev::lds_barrier();   // the slices' partial sums are in LDS
         if (slice < Tc) {
-          // this wave's tile: add the K-slices, apply the epilogue and store
-          const int n0 = (tile0 + slice) * 16 + 4 * g, m = r16;
+          // this wave's tile: add the K-slices, apply the epilogue and store.  The lane index is
+          // opaque here, so the per-lane addresses are computed in place rather than hoisted out of
+          // the link loop: kept live across it they spill, and a spill reload's wait on the vector
+          // memory counter would also wait for the agent-coherent stores issued before it.
+          int ln = threadIdx.x & 63;
+          asm volatile("" : "+v"(ln));
+          const int n0 = (tile0 + slice) * 16 + 4 * (ln >> 4), m = ln & 15;
           if (c > 0) {
             const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(d.sw, (uint32_t)(d.N * 2));
             swq = dev::bload8(srs, n0 < d.N ? (uint32_t)(2 * n0) : dev::kOutOfRange);
           }
-          v4i D = red[(slice * 8) * 64 + lane];
+          v4i D = red[(slice * 8) * 64 + ln];
 #pragma unroll
-          for (int q = 1; q < 8; ++q) D += red[(slice * 8 + q) * 64 + lane];
+          for (int q = 1; q < 8; ++q) D += red[(slice * 8 + q) * 64 + ln];
           if (m < M && n0 < d.N) {
             const int* ri = red_i + 32 * par + 8 * m;
-            store4_chain<FMT>(D, d, m, n0, s_scale[4 * par + m], ri[0] + ri[1] + ri[2] + ri[3], swq, tyr, tag_out);
+            store4_chain<FMT>(D, d, M, m, n0, s_scale[4 * par + m], ri[0] + ri[1] + ri[2] + ri[3], swq, tyr, rpar);
           }
         }
         if (c + 1 < gm.nchunks) dev::lds_barrier();   // the partial sums have been read

@@ -96,20 +96,21 @@ constexpr int kDefaultWaitLimit = 1 << 22;
 
 // Persistent decode chain (qift_chain.h, qift_chain_<fmt>.hip): one link of a prepared chain as the
 // kernel reads it (written to device memory by the prepare call).  A link whose output another link
-// reads also writes it as tagged words ty [M][ywords] (two fp16 values in the low half, the tag in
-// the high half of each 8 bytes); its consumers read element k of token m from word (xoff + k) / 2 of
-// row m of tx (rows of xwords words).
+// reads also writes it into the exchange copy ty[r mod 2] [M][ystride] of call r (and kUnwritten into
+// the other copy); its consumers read element k of token m from tx[r mod 2][m][xoff + k].
 struct ChainDesc {
   const uint32_t* P;     // packed words [N][K/16] (W2) or [N][K/8] (W4)
   const uint16_t* sw;    // fp16 s_w [N]
-  const uint64_t* tx;    // tagged input words (nullptr: the chain input)
-  uint64_t* ty;          // tagged output words (nullptr: no link reads this output)
+  const uint16_t* tx;    // the producer's exchange copies (nullptr: the chain input)
+  uint16_t* ty;          // this link's exchange copies [2][M][ystride] (nullptr: no link reads this output)
   uint16_t* y;           // fp16 output [M][N]
   int32_t* acc;          // nullable int32 [M][N]
   double denom;          // (den * 7) * sqrt(block)
-  int32_t N, K, L, num, den, in_link, xoff, xwords, ywords, tiles;
+  int32_t N, K, L, num, den, in_link, xoff, xstride, ystride, tiles;
 };
 constexpr int kChainMaxM = 4;
+// The fp16 pattern that marks an exchange value not yet written (a NaN no output carries there).
+constexpr unsigned kUnwritten = 0xFFFFu;
 // Hadamard blocks of the chain's links: 64, 256, 2048 and 4096 (the block exponent is compiled in)
 inline bool chain_block_ok(int block) { return block == 64 || block == 256 || block == 2048 || block == 4096; }
 constexpr int kChainMaxK = 16384;
