@@ -174,7 +174,11 @@ def draw_levels(fmt: int, N: int, K: int, cfg: int = 0, layer: int = 0, slot: in
     """int8 decoded levels [N, K] drawn i.i.d. from the format's level shares."""
     vals, p = _level_table(fmt)
     g = rng(cfg, layer, slot, KIND_LEVELS)
-    idx = np.searchsorted(np.cumsum(p)[:-1], g.random(size=(N, K)), side="right")
+    u = g.random(size=(N, K))
+    # bucket index = number of cumulative-share edges <= u (what a right-sided search returns)
+    idx = np.zeros((N, K), dtype=np.int8)
+    for e in np.cumsum(p)[:-1]:
+        idx += u >= e
     return vals[idx]
 
 
