@@ -468,6 +468,29 @@ int qift_kv4_attention_decode(const uint16_t *q, int64_t B, int32_t Hq, int32_t 
                               const uint8_t *v_zeros, uint16_t *out, void *workspace,
                               size_t workspace_bytes, qift_stream_t stream);
 
+/* Size of the device array behind qift_kv4_attention_decode_noalloc: 8 MiB per GPU, i.e. calls with
+ * qift_kv4_attention_workspace_bytes(B, Hq, Hkv, 128, T) up to that, B * Hq * ceil(T / 256) <= 16131
+ * partial records of 520 bytes (for example B = 1, Hq = 32 up to T = 129024). */
+#define QIFT_KV4_SCRATCH_BYTES (8u << 20)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): qift_kv4_attention_decode without a workspace argument.  The
+ * partial records live in a library-owned device array of QIFT_KV4_SCRATCH_BYTES on each GPU, held
+ * until the process ends; the call allocates nothing (no hipMalloc, hipFree or allocating library
+ * routine).  The first call on a device resolves that device's address of the array (a symbol
+ * query, not an allocation), so make one call before capturing a graph if the runtime forbids such
+ * queries during capture.  Arguments, results and errors are those of qift_kv4_attention_decode,
+ * plus QIFT_ERR_WORKSPACE when the call needs more than QIFT_KV4_SCRATCH_BYTES.  Every call on a GPU
+ * shares that GPU's array and the array keeps the last call's records: calls that overlap on one
+ * GPU (several streams or threads) race, so the caller serializes them.  Nothing in the array has
+ * to start at zero: a call writes every record its merge reads.
+ */
+int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                                      int64_t T, int32_t layout, const uint8_t *k_codes, const float *k_scales,
+                                      const uint8_t *k_zeros, const uint8_t *v_codes, const float *v_scales,
+                                      const uint8_t *v_zeros, uint16_t *out, qift_stream_t stream);
+
 /* Workspace bytes that select the FP4 x FP6 prefill kernel in the _ex calls for this weight and
  * M (M * 3K/4 for MNZ weights at M > 64), 0 where no workspace is used (host query). */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);

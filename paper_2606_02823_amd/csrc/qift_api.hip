@@ -232,6 +232,60 @@ int qift_kv4_attention_decode(const uint16_t* q, int64_t B, int32_t Hq, int32_t 
                                                v_zeros, out, workspace, (hipStream_t)stream));
 }
 
+}  // extern "C"
+
+// The device scratch of qift_kv4_attention_decode_noalloc: the split-T partial records.  Each GPU
+// holds its own copy for the life of the process; host code reaches it only through the device
+// address resolved below (the symbol's name is a host-side stand-in).
+static __device__ __align__(256) unsigned char scratch[QIFT_KV4_SCRATCH_BYTES];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kScratchDevices] = {};
+
+// The current device's address of scratch, resolved once per device with that device current.
+int scratch_address(void** out) {
+  int dev = 0;
+  int st = hip_status(hipGetDevice(&dev));
+  if (st != QIFT_OK) return st;
+  if (dev < 0 || dev >= kScratchDevices) return hip_status(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    st = hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (st != QIFT_OK) return st;
+    if (!p) return hip_status(hipErrorInvalidSymbol);
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return QIFT_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int qift_kv4_attention_decode_noalloc(const uint16_t* q, int64_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                                      int64_t T, int32_t layout, const uint8_t* k_codes, const float* k_scales,
+                                      const uint8_t* k_zeros, const uint8_t* v_codes, const float* v_scales,
+                                      const uint8_t* v_zeros, uint16_t* out, qift_stream_t stream) {
+  if (!q || !k_codes || !k_scales || !k_zeros || !v_codes || !v_scales || !v_zeros || !out) return QIFT_ERR_NULL;
+  if (!kv4_attn_shape_ok(B, Hq, Hkv, head_dim, T)) return QIFT_ERR_SHAPE;
+  if (layout != QIFT_KV4_TOKEN_MAJOR && layout != QIFT_KV4_HEAD_MAJOR) return QIFT_ERR_SPEC;
+  // every record the call writes fits in the array (no record has to start at zero: each call
+  // writes all of the records its merge reads)
+  if (qift::kv4_attention_workspace(B, Hq, T) > (size_t)QIFT_KV4_SCRATCH_BYTES) return QIFT_ERR_WORKSPACE;
+  if (!aligned16(q) || !aligned16(k_codes) || !aligned16(k_scales) || !aligned16(k_zeros) || !aligned16(v_codes) ||
+      !aligned16(v_scales) || !aligned16(v_zeros) || !aligned16(out))
+    return QIFT_ERR_ALIGN;
+  void* ws = nullptr;
+  const int st = scratch_address(&ws);
+  if (st != QIFT_OK) return st;
+  return hip_status(qift::launch_kv4_attention(q, B, Hq, Hkv, T, layout == QIFT_KV4_HEAD_MAJOR, k_codes, k_scales,
+                                               k_zeros, v_codes, v_scales, v_zeros, out, ws, (hipStream_t)stream));
+}
+
+
 namespace {
 int rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8_t* act_q, float* act_scale,
                      int32_t* act_sum, qift_stream_t stream, bool bf16) {

@@ -30,7 +30,7 @@ DEVERR_GROUP_WAIT, DEVERR_CHAIN_WAIT = 1, 2   # bits of the device error word (q
 
 # every symbol declared in include/qift.h
 EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_kv4_quant",
-           "qift_kv4_attention_workspace_bytes", "qift_kv4_attention_decode", "qift_rotate_quant_act",
+           "qift_kv4_attention_workspace_bytes", "qift_kv4_attention_decode", "qift_kv4_attention_decode_noalloc", "qift_rotate_quant_act",
            "qift_rotate_quant_act_bf16",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w2a4_lut_linear", "qift_w4a4_linear", "qift_w4a4_linear_ex",
            "qift_rotate_quant_linear", "qift_hbm_read_probe", "qift_workspace_bytes", "qift_status_string",
@@ -98,6 +98,8 @@ def lib():
         "qift_kv4_attention_workspace_bytes": (sz, [i64, i32, i32, i32, i64]),
         "qift_kv4_attention_decode": (ctypes.c_int, [vp, i64, i32, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                                      vp]),
+        "qift_kv4_attention_decode_noalloc": (ctypes.c_int, [vp, i64, i32, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp,
+                                                             vp, vp]),
         "qift_rotate_quant_act": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_rotate_quant_act_bf16": (ctypes.c_int, [vp, i64, HadamardSpec, vp, vp, vp, vp]),
         "qift_w2a4_linear": (ctypes.c_int, [pw, vp, vp, i64, vp, vp]),
@@ -303,6 +305,35 @@ def kv4_attention_decode(q: torch.Tensor, k: KV4, v: KV4, out=None, workspace=No
                                          v.zeros.data_ptr(), out.data_ptr(), workspace.data_ptr(),
                                          workspace.numel() * workspace.element_size(), _stream(stream))
     _check("qift_kv4_attention_decode", st)
+    return out
+
+
+KV4_SCRATCH_BYTES = 8 << 20   # QIFT_KV4_SCRATCH_BYTES
+
+
+def kv4_attention_decode_noalloc(q: torch.Tensor, k: KV4, v: KV4, out: torch.Tensor, head_major=False,
+                                 stream=None) -> torch.Tensor:
+    """kv4_attention_decode through the entry point that allocates nothing (its partial records in the
+    library's per-GPU array): out must be given, and calls that overlap on one GPU race."""
+    B, Hq, d = q.shape
+    _dev(q, torch.float16, (B, Hq, 128), "q")
+    if head_major:
+        Hkv, T = k.codes.shape[1], k.codes.shape[2]
+        rows = (B, Hkv, T)
+    else:
+        T, Hkv = k.codes.shape[1], k.codes.shape[2]
+        rows = (B, T, Hkv)
+    for name, c in (("k", k), ("v", v)):
+        _dev(c.codes, torch.uint8, rows + (64,), name + ".codes")
+        _dev(c.scales, torch.float32, rows, name + ".scales")
+        _dev(c.zeros, torch.uint8, rows, name + ".zeros")
+    _dev(out, torch.float16, (B, Hq, 128), "out")
+    st = lib().qift_kv4_attention_decode_noalloc(q.data_ptr(), B, Hq, Hkv, 128, T,
+                                                 KV4_HEAD_MAJOR if head_major else KV4_TOKEN_MAJOR,
+                                                 k.codes.data_ptr(), k.scales.data_ptr(), k.zeros.data_ptr(),
+                                                 v.codes.data_ptr(), v.scales.data_ptr(), v.zeros.data_ptr(),
+                                                 out.data_ptr(), _stream(stream))
+    _check("qift_kv4_attention_decode_noalloc", st)
     return out
 
 

@@ -35,7 +35,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 25
+    assert len(names) == 26
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -114,6 +114,17 @@ def test_kv4_validation(L):
         assert f(A, 1, 32, 8, 128, 1000, lay, A, A, MIS, A, A, A, A, A, good, None) == E_ALIGN
     assert f(A, 1, 32, 8, 128, 1000, 2, A, A, A, A, A, A, A, A, good, None) == E_SPEC
     assert f(A, 1, 32, 8, 128, 1000, -1, A, A, A, A, A, A, A, A, good, None) == E_SPEC
+    # the entry point without a workspace: the same checks, and calls beyond its 8 MiB array refused
+    # (all before any HIP call)
+    fn = L.qift_kv4_attention_decode_noalloc
+    for lay in (0, 1):
+        assert fn(A, 1, 32, 8, 128, 1000, lay, A, A, A, A, A, None, A, None) == E_NULL
+        assert fn(A, 1, 32, 8, 128, 0, lay, A, A, A, A, A, A, A, None) == E_SHAPE
+        assert fn(A, 1, 32, 8, 128, 1000, lay, A, A, MIS, A, A, A, A, None) == E_ALIGN
+    assert fn(A, 1, 32, 8, 128, 1000, 2, A, A, A, A, A, A, A, None) == E_SPEC
+    assert ws(1, 32, 8, 128, 129024) <= qift.KV4_SCRATCH_BYTES < ws(1, 32, 8, 128, 129025)
+    assert fn(A, 1, 32, 8, 128, 129025, 1, A, A, A, A, A, A, A, None) == E_WS
+    assert fn(A, 16, 32, 8, 128, 8192, 0, A, A, A, A, A, A, A, None) == E_WS
 
 
 @pytest.mark.parametrize("entry", ["qift_rotate_quant_act", "qift_rotate_quant_act_bf16"])
