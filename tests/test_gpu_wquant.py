@@ -1,12 +1,15 @@
 """GPU weight quantizer (qift_quantize_weights) against the oracle, through the C ABI.
 
-Levels and fp16 scales must equal the oracle's bit for bit (the oracle rotates with a dense fp64
-product, then applies quant.quantize_weights).  The rotation of an fp32 row is not exact, so the
-two sides can differ in the last bits of a rotated value; a decision taken on such bits (a value
-within rounding of a level threshold, two PoT candidates within rounding of each other) could go
-either way.  The seeded rows below contain no such case, so the comparison is exact.  Rows built
-to rotate exactly put scales on fp16 rounding ties and values on level thresholds, where both
-sides decide on identical numbers.
+The oracle rotates with a dense fp64 product, then applies quant.quantize_weights.  The rotation of
+an fp32 row is not exact, so the two sides can differ in the last bits of a rotated value, and a
+decision taken on such bits (a value within rounding of a level threshold, an unrounded scale within
+rounding of an fp16 midpoint, two PoT candidates within rounding of each other) may go either way.
+Every result is therefore checked with the validity rule of tests/wquant_rule.py: equal to the
+oracle's, or different only where the oracle's values lie within the rotation-error bound of the
+deciding threshold.  10^4 Student-t rows per format, and rows built to sit on thresholds with
+perturbations below fp64 rounding (where the two sides' sums may round differently), go through it.
+Rows built to rotate exactly put scales on fp16 rounding ties and values on level thresholds, where
+both sides decide on identical numbers and must agree bit for bit.
 """
 import numpy as np
 import pytest
@@ -14,6 +17,7 @@ import torch
 
 from oracle import hadamard, levels, quant
 from paper_2606_02823_amd import synth
+from wquant_rule import check_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -35,12 +39,17 @@ def run_gpu(Q, W, b, fmt):
     return L.cpu().numpy(), s.cpu().numpy()
 
 
-def check(Q, W, b, fmt):
+def check(Q, W, b, fmt, exact=False):
+    """GPU result against the oracle: bit for bit where the rotation is exact, else by the rule."""
     W = np.asarray(W, dtype=np.float32)
-    L_ref, s_ref = quant.quantize_weights(hadamard.rotate_weights(W.astype(np.float64), b), fmt)
     L, s = run_gpu(Q, W, b, fmt)
-    assert np.array_equal(s.view(np.uint16), s_ref.view(np.uint16)), "scales"
-    assert np.array_equal(L, L_ref), "levels"
+    if exact:
+        L_ref, s_ref = quant.quantize_weights(hadamard.rotate_weights(W.astype(np.float64), b), fmt)
+        assert np.array_equal(s.view(np.uint16), s_ref.view(np.uint16)), "scales"
+        assert np.array_equal(L, L_ref), "levels"
+    else:
+        _, _, differ = check_rows(fmt, W, b, L, s)
+        print(f"fmt {fmt}: {W.shape[0]} rows, {differ.size} differ from the oracle within the rule", flush=True)
     return L, s
 
 
@@ -78,7 +87,7 @@ def test_quantize_weights_exact_rows(Q, fmt):
             one(5e-7),                      # scales in the fp16 subnormal range
             two(38, 18), two(42, 14), two(-38, 18),   # W4: 7 and +-2.5 (to 2), 7 and 3.5 (to 4)
             two(16, 16), two(24, 8)]        # a zero and an exact midpoint after rotation
-    check(Q, np.array(rows), 64, fmt)
+    check(Q, np.array(rows), 64, fmt, exact=True)
 
 
 def test_quantize_weights_then_pack(Q):
@@ -91,3 +100,32 @@ def test_quantize_weights_then_pack(Q):
         torch.cuda.synchronize()
         L_ref, _ = quant.quantize_weights(hadamard.rotate_weights(W.astype(np.float64), 4096), fmt)
         assert np.array_equal(pk.words.cpu().numpy().view(np.uint32), opack.pack(L_ref, fmt))
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_quantize_weights_rule_ten_thousand_rows(Q, fmt):
+    W = synth.weights_fp32(98, 0, "gate", 10000, 4096)
+    check(Q, W, 4096, fmt)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_quantize_weights_rule_near_thresholds(Q, fmt):
+    # K = b = 64: rows whose large entries rotate exactly onto level thresholds, rounding ties and
+    # PoT candidate boundaries, plus entries 2^-47 .. 2^-58 times as large in the other positions,
+    # which move the exact rotated values off those points by less than fp64 rounding, so that
+    # the two sides' sums (dense product, butterflies) may round to either side
+    rng = np.random.default_rng(99 + fmt)
+    bases = []
+    for a, dd in ((38, 18), (42, 14), (-38, 18), (16, 16), (24, 8), (20, 0), (16, 0), (40, 16), (36, 20)):
+        r = np.zeros(64)
+        r[3], r[9] = a, dd
+        bases.append(r)
+    rows = []
+    for base in bases:
+        for _ in range(40):
+            r = base.copy()
+            free = np.setdiff1d(np.arange(64), [3, 9])
+            pos = rng.choice(free, size=int(rng.integers(1, 20)), replace=False)
+            r[pos] = rng.choice([-1.0, 1.0], pos.size) * 40.0 * 2.0 ** -rng.integers(47, 59, pos.size)
+            rows.append(r)
+    check(Q, np.array(rows, dtype=np.float32), 64, fmt)
