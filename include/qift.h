@@ -114,7 +114,10 @@ typedef struct {
  *            plain absmax/7 scale).  QIFT_CLIP(num, den): clip ratio
  *            c = num / den of the symmetric INT4 quantizer, 1 <= num <= den
  *            <= 16, decided exactly (QIFT_CLIP(9, 10) is the paper's 0.9
- *            setting, Sec. 4.1).  Any other value is QIFT_ERR_SPEC.
+ *            setting, Sec. 4.1).  QIFT_SPEC_BF16 may be or-ed in by the calls
+ *            that rotate activations (qift_rotate_quant_act,
+ *            qift_rotate_quant_linear): x then holds bf16 values.  Any other
+ *            value is QIFT_ERR_SPEC.
  */
 typedef struct {
   int64_t K;
@@ -123,6 +126,7 @@ typedef struct {
 } qift_hadamard_spec;
 
 #define QIFT_CLIP(num, den) ((int32_t)((((num) & 0xFF) << 8) | ((den) & 0xFF)))
+#define QIFT_SPEC_BF16 ((int32_t)(1 << 16))
 
 /* Bytes of packed words: N*K/4 (W2) or N*K/2 (W4); 0 for an invalid query. */
 size_t qift_packed_bytes(int32_t fmt, int64_t N, int64_t K);
@@ -213,13 +217,14 @@ int qift_rotate_quant_act(const uint16_t *x, int64_t M, qift_hadamard_spec spec,
 /*
  * qift_rotate_quant_act for bf16 activations (x: bf16 bits [M][spec.K]), for
  * callers whose models run in bf16 (the paper's full-precision reference is
- * fp16); same arguments, errors and results.
- * Each bf16 value is widened exactly; the rotation and the rounding decisions
- * are exact, as for fp16, when every value of a token lies on the fp16 grid:
- * zero, or a magnitude in [2^-17, 2^16) (a bf16 has 8 significant bits, so
- * such a value is a multiple of 2^-24).  Values outside that range are
- * outside the contract (the codes may then differ from the exact rounding at
- * near-ties).
+ * fp16); the same as qift_rotate_quant_act with QIFT_SPEC_BF16 in spec.flags.
+ * Any finite bf16 value is accepted.  Each is widened exactly to fp64 and X is
+ * the fp64 result of the butterfly stages over the index bits in ascending
+ * order, each sum and difference rounded to fp64; A, the codes (decided
+ * exactly on those fp64 values, ties to even), s_x and the code sums follow
+ * from X as for fp16.  On the fp16 grid (zero, or a magnitude in [2^-17, 2^16):
+ * multiples of 2^-24) every partial sum is exact, so the result is the exact
+ * rotation's, identical to the fp16 call on the same values.
  */
 int qift_rotate_quant_act_bf16(const uint16_t *x, int64_t M, qift_hadamard_spec spec,
                                int8_t *act_q, float *act_scale, int32_t *act_sum,
@@ -297,7 +302,8 @@ int qift_w4a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float
  * quantizes the tokens itself on chip while its first weight tiles stream
  * in, so the activations never make a round trip through HBM.  Results are
  * bit-identical to the two-call form.
- *   x          fp16 [M][w->K] (finite values).
+ *   x          fp16 [M][w->K] (finite values), or bf16 with QIFT_SPEC_BF16 in
+ *              spec.flags (the reading of qift_rotate_quant_act_bf16).
  *   spec       as for qift_rotate_quant_act; spec.K must equal w->K.
  *   out        out: fp16 y [M][N].
  *   acc_out    out, nullable: int32 [M][N].

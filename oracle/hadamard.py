@@ -68,6 +68,33 @@ def rotate_act_units(x: np.ndarray, b: int) -> np.ndarray:
     return Xi
 
 
+def rotate_act_staged(x: np.ndarray, b: int) -> np.ndarray:
+    """``X = (I (x) H_b) x`` per token in fp64, one butterfly stage per index bit, bits in ascending order.
+
+    Stage j pairs the elements whose block index differs only in bit j and replaces (a, c) by
+    (a + c, a - c), each rounded to fp64 (round to nearest, ties to even).  After the L = log2(b)
+    stages every element holds its +-1 combination of the block (Sylvester ordering).  Inputs are any
+    finite floats (fp16 or bf16 values, converted to fp64 exactly); on the 2^-24 grid of
+    :func:`rotate_act_units` every partial sum is exact and this equals that transform times 2^-24.
+    Returns fp64 [M, K].
+    """
+    x = np.asarray(x)
+    if x.dtype.kind != "f":
+        raise TypeError("activations must be floating point")
+    M, K = x.shape
+    check_block(K, b)
+    X = x.astype(np.float64).reshape(M, K // b, b)
+    if not np.all(np.isfinite(X)):
+        raise ValueError("non-finite activation")
+    h = 1
+    while h < b:
+        Y = X.reshape(M, K // b, b // (2 * h), 2, h)
+        lo, hi = Y[:, :, :, 0, :], Y[:, :, :, 1, :]
+        X = np.stack([lo + hi, lo - hi], axis=3).reshape(M, K // b, b)
+        h *= 2
+    return X.reshape(M, K)
+
+
 def rotate_weights(W: np.ndarray, b: int) -> np.ndarray:
     """Offline rotation of weight rows: ``W_rot[n, :] = (I (x) H_b) W[n, :] / sqrt(b)`` (fp64)."""
     W = np.asarray(W, dtype=np.float64)

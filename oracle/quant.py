@@ -78,6 +78,43 @@ def act_quant(x: np.ndarray, b: int, clip=(1, 1)):
     return q.astype(np.int8), s_x, q.sum(axis=1).astype(np.int32), X
 
 
+def act_quant_staged(x: np.ndarray, b: int, clip=(1, 1)):
+    """Rotate and quantize tokens [M, K] of any finite binary floats (bf16 activations included).
+
+    Reading for inputs off the 2^-24 grid (bf16 values below 2^-17 or from 2^16 in magnitude), where
+    the paper fixes no precision and an fp64 rotation is not exact in general: ``X`` is the fp64 value
+    of the unnormalised block transform computed stage by stage over the index bits 0, 1, ..., L - 1
+    (:func:`oracle.hadamard.rotate_act_staged`); then, exactly on those fp64 numbers taken as
+    rationals, ``A = max |X|``, ``q = sign(X) min(7, rne(7 den |X| / (num A)))`` (a half rounds to the
+    even integer), ``s_x = fp32(fp64(A num) / ((den 7) sqrt(b)))`` and ``sum_q``.  On the 2^-24 grid
+    every partial sum is exact, so this is :func:`act_quant` there.
+
+    Returns ``(q int8 [M,K], s_x fp32 [M], sum_q int32 [M], X fp64 [M,K])``.
+    """
+    from fractions import Fraction
+    num, den = int(clip[0]), int(clip[1])
+    if not (1 <= num <= den <= 16):
+        raise ValueError("clip ratio must be num/den with 1 <= num <= den <= 16")
+    X = hadamard.rotate_act_staged(x, b)
+    M, K = X.shape
+    q = np.zeros((M, K), dtype=np.int64)
+    A = np.abs(X).max(axis=1) if K else np.zeros(M)
+    for m in range(M):
+        a = Fraction(float(A[m]))
+        if a == 0:
+            continue
+        for k in range(K):
+            t = 14 * den * abs(Fraction(float(X[m, k]))) + num * a
+            d = 2 * num * a
+            q0 = t // d
+            if t % d == 0 and q0 % 2 == 1:
+                q0 -= 1
+            q0 = min(int(q0), 7)
+            q[m, k] = -q0 if X[m, k] < 0 else q0
+    s_x = ((A.astype(np.float64) * float(num)) / act_scale_denominator(b, (num, den))).astype(np.float32)
+    return q.astype(np.int8), s_x, q.sum(axis=1).astype(np.int32), X
+
+
 # ---------------------------------------------------------------------------
 # nearest level
 # ---------------------------------------------------------------------------

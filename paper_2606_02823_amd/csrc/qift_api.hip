@@ -60,6 +60,12 @@ bool parse_clip(int32_t flags, int* num, int* den) {
   return *num >= 1 && *num <= *den && *den <= 16;
 }
 
+// Flags of an activation spec: the clip ratio, and QIFT_SPEC_BF16 (the tokens are bf16 values).
+bool parse_act_flags(int32_t flags, int* num, int* den, bool* bf16) {
+  *bf16 = (flags & QIFT_SPEC_BF16) != 0;
+  return parse_clip(flags & ~QIFT_SPEC_BF16, num, den);
+}
+
 int check_linear(const qift_packed_w* w, bool want_w4, const int8_t* act_q, const float* act_scale,
                  const int32_t* act_sum, int64_t M, const uint16_t* out, const int32_t* acc_out) {
   if (!w || !act_q || !act_scale || !out || !w->packed || !w->scales) return QIFT_ERR_NULL;
@@ -295,11 +301,12 @@ int rotate_quant_act(const uint16_t* x, int64_t M, qift_hadamard_spec spec, int8
   const int32_t b = spec.block;
   if (b < 2 || b > 8192 || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
   int num, den;
-  if (!parse_clip(spec.flags, &num, &den)) return QIFT_ERR_SPEC;
+  bool flag_bf16 = false;
+  if (!parse_act_flags(spec.flags, &num, &den, &flag_bf16)) return QIFT_ERR_SPEC;
   if (!aligned16(x) || !aligned16(act_q) || !aligned16(act_scale) || (act_sum && !aligned16(act_sum)))
     return QIFT_ERR_ALIGN;
   return hip_status(qift::launch_rotate_quant_act(x, M, spec.K, b, num, den, act_q, act_scale, act_sum,
-                                                  (hipStream_t)stream, bf16));
+                                                  (hipStream_t)stream, bf16 || flag_bf16));
 }
 }  // namespace
 
@@ -368,7 +375,8 @@ int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t 
   const int32_t b = spec.block;
   if (spec.K != w->K || b < 2 || b > qift::kFusedMaxBlock || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
   int num, den;
-  if (!parse_clip(spec.flags, &num, &den)) return QIFT_ERR_SPEC;
+  bool bf16 = false;
+  if (!parse_act_flags(spec.flags, &num, &den, &bf16)) return QIFT_ERR_SPEC;
   if (!aligned16(w->packed) || !aligned16(w->scales) || !aligned16(x) || !aligned16(out) ||
       (acc_out && !aligned16(acc_out)) || (act_q && !aligned16(act_q)) ||
       (act_scale && !aligned16(act_scale)) || (act_sum && !aligned16(act_sum)))
@@ -377,7 +385,7 @@ int qift_rotate_quant_linear(const qift_packed_w* w, const uint16_t* x, int64_t 
                : w->fmt == QIFT_W2_POT ? qift::launch_fused_pot
                                        : qift::launch_fused_w4;
   return hip_status(launch(w->packed, w->scales, w->N, w->K, x, b, num, den, M, out, acc_out, act_q, act_scale,
-                           act_sum, (hipStream_t)stream));
+                           act_sum, bf16, (hipStream_t)stream));
 }
 
 // ---- decode chain -------------------------------------------------------------------------------

@@ -86,7 +86,7 @@ constexpr int tail_bytes() { return xch_region<NTILES, T, CODES>() + 64 + 128 + 
 template <int FMT, int NTILES, int T, int LC, bool CODES>
 __global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_decode(
     const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw, int N, int K,
-    const uint16_t* __restrict__ x, int L, int num, int den, double denom,
+    const uint16_t* __restrict__ x, int L, int num, int den, double denom, int xbf16,
     int8_t* __restrict__ act_q_out, float* __restrict__ scale_out, int32_t* __restrict__ sum_out,
     const int8_t* __restrict__ aq_in, const float* __restrict__ sx_in, const int32_t* __restrict__ sum_in,
     int M, int Kpad, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out, int wait_limit,
@@ -226,7 +226,7 @@ __global__ __launch_bounds__((fused_threads<NTILES, CODES>())) void k_fused_deco
         if (m > 0) dev::load_token_raw<256, NTILES>(cur, x + (int64_t)m * K, K);
       }
       const double A = dev::quant_token_group<NTILES, LC, PLANAR>(cur, K, L, num, den, xch0, xch1, red_d + 4 * m,
-                                                          red_i + 4 * m, sync, act_l + m * Kpad);
+                                                          red_i + 4 * m, sync, act_l + m * Kpad, xbf16 != 0);
       if (tid == 0) s_scale[m] = (float)((A * (double)num) / denom);
     }
   } else {
@@ -384,7 +384,7 @@ struct FusedArgs {
   const uint32_t* P;
   const uint16_t* sw;
   int64_t N, K;
-  const uint16_t* x;              // rotation in the kernel: fp16 tokens [M][K]
+  const uint16_t* x;              // rotation in the kernel: fp16 (or, with bf16, bf16) tokens [M][K]
   int L, num, den;
   double denom;
   int8_t* aq_out;                 // optional outputs of the rotation
@@ -396,6 +396,7 @@ struct FusedArgs {
   int64_t M;
   uint16_t* y;
   int32_t* acc_out;
+  bool bf16 = false;              // x holds bf16 values
 };
 
 // Tiles per workgroup: for K <= 4096 (one rotation tile) as many as keep the grid within one
@@ -427,7 +428,8 @@ hipError_t launch_t(const FusedArgs& a, hipStream_t s) {
     if (attr != hipSuccess) return attr;
   }
   hipLaunchKernelGGL((k_fused_decode<FMT, NTILES, T, LC, CODES>), dim3(grid), dim3(fused_threads<NTILES, CODES>()),
-                     shmem, s, a.P, a.sw, (int)a.N, (int)a.K, a.x, a.L, a.num, a.den, a.denom, a.aq_out, a.sc_out,
+                     shmem, s, a.P, a.sw, (int)a.N, (int)a.K, a.x, a.L, a.num, a.den, a.denom, a.bf16 ? 1 : 0,
+                     a.aq_out, a.sc_out,
                      a.sm_out, a.aq_in, a.sx_in, a.sum_in, (int)a.M, kpad_of(a.K), a.y, a.acc_out, wait_limit(),
                      device_error_word());
   return hipGetLastError();
@@ -490,10 +492,10 @@ hipError_t launch_ntiles(const FusedArgs& a, hipStream_t s) {
 template <int FMT>
 hipError_t launch_fused_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x,
                             int block, int num, int den, int64_t M, uint16_t* y, int32_t* acc_out, int8_t* aq,
-                            float* sc, int32_t* sm, hipStream_t s) {
+                            float* sc, int32_t* sm, bool bf16, hipStream_t s) {
   if (M < 1 || M > kFusedMaxM || K > kFusedMaxK || block > kFusedMaxBlock) return hipErrorInvalidValue;
   FusedArgs a{P, sw, N, K, x, dev::ilog2c(block), num, den, act_denominator(block, den), aq, sc, sm,
-              nullptr, nullptr, nullptr, M, y, acc_out};
+              nullptr, nullptr, nullptr, M, y, acc_out, bf16};
   return launch_ntiles<FMT, false>(a, s);
 }
 

@@ -5,9 +5,9 @@ namespace qift {
 
 hipError_t launch_fused_pot(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const uint16_t* x,
                           int block, int clip_num, int clip_den, int64_t M, uint16_t* y, int32_t* acc_out,
-                          int8_t* act_q, float* act_scale, int32_t* act_sum, hipStream_t s) {
+                          int8_t* act_q, float* act_scale, int32_t* act_sum, bool bf16, hipStream_t s) {
   return launch_fused_fmt<mma::FMT_POT>(P, sw, N, K, x, block, clip_num, clip_den, M, y, acc_out, act_q, act_scale,
-                                   act_sum, s);
+                                   act_sum, bf16, s);
 }
 
 hipError_t launch_codes_pot(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act_q,

@@ -240,35 +240,40 @@ __device__ __forceinline__ int fwht_tile(double (&v)[E], double* lds, int t, int
 struct QuantParams {
   double A;        // max |X| (natural units)
   double c1;       // 7 den / (num A), fp64 (estimate only)
-  int64_t Ai;      // A in units of 2^-24
   int num, den;
 };
 
 __device__ __forceinline__ QuantParams make_qparams(double A, int num, int den) {
   QuantParams p;
   p.A = A;
-  p.Ai = (int64_t)(A * 0x1p24);
-  p.c1 = p.Ai > 0 ? (7.0 * den) / ((double)num * A) : 0.0;
+  p.c1 = A > 0.0 ? (7.0 * den) / ((double)num * A) : 0.0;
   p.num = num;
   p.den = den;
   return p;
 }
 
-// Exact rounding near a half-integer: t = 14 den |X| + num A and d = 2 num A
-// in units of 2^-24; q = floor(t / d), lowered to even on an exact half.
-// Rarely executed, so it is kept out of line (the inlined copies per element
-// made the kernels larger than the instruction cache).
-__device__ __attribute__((noinline)) int quant_exact(double ax, double f, int64_t Ai, int num, int den) {
-  const int64_t xi = (int64_t)(ax * 0x1p24);
-  const int64_t t = 14 * (int64_t)den * xi + (int64_t)num * Ai;
-  const int64_t d = 2 * (int64_t)num * Ai;
+// Exact rounding near a half-integer, on the fp64 values |X| <= A taken as rationals:
+// t = 14 den |X| + num A and d = 2 num A, q = floor(t / d), lowered to even on an exact half.
+// Both are normal doubles (every nonzero rotated value is a sum of fp16 or bf16 values, at
+// least 2^-133): |X| = mx 2^ex, A = ma 2^ea with 53-bit integer mantissas and ea >= ex, so in
+// units of 2^ex, t and d are integers below 2^70 when ea - ex <= 12 (beyond that, 7 den |X| /
+// (num A) < 112 2^-11 and q = 0).  Rarely executed, so it is kept out of line (the inlined
+// copies per element made the kernels larger than the instruction cache).
+__device__ __attribute__((noinline)) int quant_exact(double ax, double A, int num, int den, double f) {
   if (!(f < 8.0)) return 7;   // clamps anyway (and keeps q and t below in range)
-  int64_t q = (int64_t)f;     // within one of the exact quotient: each loop runs at most twice
-  int64_t r = t - q * d;
-  for (int it = 0; r < 0 && it < 4; ++it) { --q; r += d; }
-  for (int it = 0; r >= d && it < 4; ++it) { ++q; r -= d; }
-  if (r == 0 && (q & 1)) --q;
-  return (int)(q < 0 ? 0 : q < 7 ? q : 7);
+  if (!(ax > 0.0)) return 0;
+  typedef unsigned __int128 u128;
+  const uint64_t bx = (uint64_t)__double_as_longlong(ax), ba = (uint64_t)__double_as_longlong(A);
+  const uint64_t mx = (bx & 0xFFFFFFFFFFFFFull) | (1ull << 52), ma = (ba & 0xFFFFFFFFFFFFFull) | (1ull << 52);
+  const int s = (int)((ba >> 52) & 0x7FF) - (int)((bx >> 52) & 0x7FF);
+  if (s > 12) return 0;
+  const u128 t = (u128)(14u * (unsigned)den) * mx + (((u128)(unsigned)num * ma) << s);
+  const u128 d = ((u128)(2u * (unsigned)num) * ma) << s;
+  int q = (int)f;             // within one of the exact quotient: each loop runs at most twice
+  for (int it = 0; it < 4 && q > 0 && (u128)q * d > t; ++it) --q;
+  for (int it = 0; it < 4 && (u128)(q + 1) * d <= t; ++it) ++q;
+  if ((u128)q * d == t && (q & 1)) --q;
+  return q < 7 ? q : 7;
 }
 
 // Rounding of 16 values.  The fp64 quotient v = X c1 is within 1e-13 of the
@@ -277,7 +282,7 @@ __device__ __attribute__((noinline)) int quant_exact(double ax, double f, int64_
 // so rounding the signed quotient gives sign(X) times the rounded magnitude.
 // That branch-free fast path covers all 16 values; only when some lane of the
 // wave has a value that close to a half (a wave-uniform, rare branch) are those
-// values redone with the exact int64 test.
+// values redone with the exact integer test.
 __device__ __forceinline__ void quant16(const double (&v)[16], const QuantParams& p, int (&q)[16]) {
   int near = 0;
 #pragma unroll
@@ -296,8 +301,8 @@ __device__ __forceinline__ void quant16(const double (&v)[16], const QuantParams
     for (int e = 0; e < 16; ++e) {
       const double ax = fabs(v[e]);
       const double vv = ax * p.c1;
-      if (p.Ai > 0 && fabs(vv - rint(vv)) > 0.5 - 1e-9) {
-        const int qq = quant_exact(ax, floor(vv), p.Ai, p.num, p.den);
+      if (p.A > 0.0 && fabs(vv - rint(vv)) > 0.5 - 1e-9) {
+        const int qq = quant_exact(ax, p.A, p.num, p.den, floor(vv));
         q[e] = v[e] < 0.0 ? -qq : qq;
       }
     }
@@ -496,7 +501,7 @@ __device__ __forceinline__ void store_codes(int8_t* dst, const int (&q)[16], int
 template <int NTILES, int LC, bool PLANAR, typename Sync, bool BF16 = false>
 __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw, int64_t K, int L_rt, int num,
                                                     int den, double* xch0, double* xch1, double* red_d,
-                                                    int* red_i, Sync& sync, int8_t* dst) {
+                                                    int* red_i, Sync& sync, int8_t* dst, bool xbf16 = false) {
   using S = Tile<256, 16>;
   const int L = LC > 0 ? LC : L_rt;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -505,7 +510,8 @@ __device__ __forceinline__ double quant_token_group(const TokenRaw<NTILES>& raw,
   int wend = 0;
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
-    unpack16<BF16>(v[tau], raw.d[tau]);
+    if (BF16 || xbf16) unpack_bf16(v[tau], raw.d[tau]);   // x bf16: a wave-uniform run-time choice
+    else unpack_fp16(v[tau], raw.d[tau]);
     if (tau > 0 && xch0 == xch1 && L > 6) sync();   // the previous tile's exchange reads are done
     wend = fwht_tile_s<256, 16, false>(v[tau], (tau & 1) ? xch1 : xch0, t, L, sync);
 #pragma unroll

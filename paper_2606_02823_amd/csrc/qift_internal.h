@@ -57,7 +57,7 @@ hipError_t launch_gemm_f4(const uint32_t* P, const uint16_t* sw, int64_t N, int6
 #define QIFT_FUSED_LAUNCHER(NAME)                                                                          \
   hipError_t NAME(const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K, const uint16_t* x, \
                   int block, int clip_num, int clip_den, int64_t M, uint16_t* out, int32_t* acc_out,       \
-                  int8_t* act_q, float* act_scale, int32_t* act_sum, hipStream_t s)
+                  int8_t* act_q, float* act_scale, int32_t* act_sum, bool bf16, hipStream_t s)
 QIFT_FUSED_LAUNCHER(launch_fused_mnz);
 QIFT_FUSED_LAUNCHER(launch_fused_pot);
 QIFT_FUSED_LAUNCHER(launch_fused_w4);

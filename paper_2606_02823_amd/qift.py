@@ -60,8 +60,11 @@ def clip_flags(num: int, den: int) -> int:
     return 0 if (num, den) == (1, 1) else ((int(num) & 0xFF) << 8) | (int(den) & 0xFF)
 
 
-def spec(K: int, block: int, clip=(1, 1)) -> HadamardSpec:
-    return HadamardSpec(K, block, clip_flags(*clip))
+SPEC_BF16 = 1 << 16   # QIFT_SPEC_BF16: the tokens are bf16 values
+
+
+def spec(K: int, block: int, clip=(1, 1), bf16: bool = False) -> HadamardSpec:
+    return HadamardSpec(K, block, clip_flags(*clip) | (SPEC_BF16 if bf16 else 0))
 
 
 class ChainLinkC(ctypes.Structure):
@@ -426,9 +429,11 @@ def linear(w: Packed, act: QAct, out=None, acc_out=None, workspace=None, use_sum
 
 def rotate_quant_linear(w: Packed, x: torch.Tensor, block: int, clip=(1, 1), out=None, acc_out=None,
                         act_out: QAct | None = None, stream=None) -> torch.Tensor:
-    """Fused rotate_quant_act + linear for M <= 4 fp16 tokens [M, K]; optional act_out receives the act triple."""
+    """Fused rotate_quant_act + linear for M <= 4 fp16 or bf16 tokens [M, K]; optional act_out receives the
+    act triple."""
     M, K = x.shape
-    _dev(x, torch.float16, (M, K), "x")
+    bf16 = x.dtype == torch.bfloat16
+    _dev(x, torch.bfloat16 if bf16 else torch.float16, (M, K), "x")
     if K != w.K:
         raise ValueError(f"activation width {K} != weight K {w.K}")
     if out is None:
@@ -442,7 +447,7 @@ def rotate_quant_linear(w: Packed, x: torch.Tensor, block: int, clip=(1, 1), out
         _dev(act_out.sum, torch.int32, (M,), "act_sum")
     v = w.cview()
     st = lib().qift_rotate_quant_linear(
-        ctypes.byref(v), x.data_ptr(), M, spec(K, block, clip), out.data_ptr(), _ptr(acc_out),
+        ctypes.byref(v), x.data_ptr(), M, spec(K, block, clip, bf16), out.data_ptr(), _ptr(acc_out),
         None if act_out is None else act_out.q.data_ptr(), None if act_out is None else act_out.scale.data_ptr(),
         None if act_out is None else act_out.sum.data_ptr(), _stream(stream))
     _check("qift_rotate_quant_linear", st)

@@ -244,23 +244,67 @@ def test_rotate_quant_act_clip_ratio(Q, clip):
     check_act(act, x, b, clip)
 
 
-def _bf16_on_grid(rng, M, K, lo, hi):
-    """bf16 activations on the 2^-24 grid (the exact-rotation contract), rows at mixed scales."""
-    x = torch.from_numpy(rng.normal(0, 1, (M, K)) * rng.uniform(lo, hi, (M, 1))).to(torch.bfloat16)
-    x[x.abs() < 2.0 ** -17] = 0
-    return x
+def _bf16_any(rng, M, K, b):
+    """bf16 activations across the finite bf16 range (no narrowing): rows of N(0, 1) at scales from
+    2^-30 to 2^30 (values below 2^-17 and from 2^16 in magnitude among them), extreme values
+    (subnormals, the largest finite magnitude), a row far below 2^-24, a row mixing 2^-120 and 2^100,
+    and a block holding only two values, whose transform alternates 7 2^-100 and 2.5 2^-100 (a
+    rounding tie off the fp16 grid)."""
+    x = rng.normal(0, 1, (M, K)) * 2.0 ** rng.uniform(-30, 30, (M, 1))
+    x[0] *= 2.0 ** -60
+    if M > 1:
+        x[1] = rng.normal(0, 1, K)
+        x[1, ::2] *= 2.0 ** -120
+        x[1, 1::2] *= 2.0 ** 100
+    if M > 2:
+        x[2] = 0
+        x[2, 0], x[2, 1] = 4.75 * 2.0 ** -100, 2.25 * 2.0 ** -100   # block 0: [7, 2.5, 7, 2.5, ...] 2^-100
+    ext = [2.0 ** -133, -(2.0 ** -126), 3.3e38, -(2.0 ** 100), 2.0 ** -17, 65280.0, 65536.0, 1e-30]
+    for m in range(3, M):
+        x[m, rng.choice(K, size=len(ext), replace=False)] = ext
+    xb = torch.from_numpy(x).to(torch.bfloat16)
+    assert torch.isfinite(xb.float()).all()
+    return xb
 
 
-@pytest.mark.parametrize("M,K,b", [(5, 4096, 4096), (3, 11008, 64), (9, 8192, 128), (2, 32768, 4096),
-                                   (1, 14336, 2048)])
+def check_act_bf16(act, x, b, clip=(1, 1)):
+    q_ref, sx_ref, sum_ref, _ = quant.act_quant_staged(x, b, clip)
+    assert np.array_equal(host(act.q), q_ref)
+    assert np.array_equal(host(act.scale).view(np.uint32), sx_ref.view(np.uint32))
+    assert np.array_equal(host(act.sum), sum_ref)
+    return q_ref, sx_ref
+
+
+@pytest.mark.parametrize("M,K,b", [(5, 4096, 4096), (4, 11008, 64), (4, 8192, 128), (4, 32768, 4096),
+                                   (4, 14336, 2048), (4, 256, 2)])
 def test_rotate_quant_act_bf16(Q, M, K, b):
-    """bf16 input (qift_rotate_quant_act_bf16): bit-exact against the oracle on the same values."""
+    """bf16 input (qift_rotate_quant_act_bf16) over the whole finite bf16 range: bit-exact against the
+    oracle's staged fp64 reading (exact on the fp16 grid)."""
     rng = np.random.default_rng(M * 7919 + K)
-    x = _bf16_on_grid(rng, M, K, 1e-3, 400.0)
-    x[0, :3] = torch.tensor([2.0 ** -17, 65280.0, -1.5], dtype=torch.bfloat16)
+    x = _bf16_any(rng, M, K, b)
     for clip in ((1, 1), (9, 10)):
         act = Q.rotate_quant_act(x.cuda(), b, clip=clip)
-        check_act(act, x.float().numpy(), b, clip)
+        check_act_bf16(act, x.float().numpy(), b, clip)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("M,N,K,b", [(1, 4096, 4096, 4096), (3, 1040, 4096, 4096), (4, 528, 14336, 2048),
+                                     (2, 640, 11008, 64)])
+def test_fused_rotate_quant_linear_bf16(Q, fmt, M, N, K, b):
+    """bf16 tokens into the fused entry (QIFT_SPEC_BF16): codes, accumulators and y bit-exact."""
+    rng = np.random.default_rng(N + K + fmt)
+    x = _bf16_any(rng, M, K, b)
+    L = synth.draw_levels(fmt, N, K, cfg=90, layer=fmt, slot=M)
+    s_w = synth.draw_scales(fmt, N, cfg=90, layer=fmt, slot=M)
+    pk = pack_dev(Q, L, s_w, fmt)
+    aq = Q.alloc_act(M, K, torch.device("cuda"))
+    acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    y = Q.rotate_quant_linear(pk, x.cuda(), b, acc_out=acc, act_out=aq)
+    torch.cuda.synchronize()
+    q_ref, sx_ref = check_act_bf16(aq, x.float().numpy(), b)
+    acc_ref = olin.int_dot(L, q_ref)
+    assert np.array_equal(host(acc), acc_ref)
+    assert np.array_equal(bits16(host(y)), bits16(olin.epilogue_fp32(acc_ref, sx_ref, s_w)))
 
 
 # ----------------------------------------------------------------------------- full-size configs
