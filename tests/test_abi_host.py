@@ -143,7 +143,7 @@ def test_rotate_quant_act_validation(L, entry):
     assert f(A, 4, _spec(num=0, den=1), A, A, A, None) == E_SPEC
     assert f(A, 4, _spec(num=3, den=2), A, A, A, None) == E_SPEC
     assert f(A, 4, _spec(num=9, den=17), A, A, A, None) == E_SPEC
-    assert f(A, 4, _spec(flags=0x10101), A, A, A, None) == E_SPEC          # bits above the clip fields
+    assert f(A, 4, _spec(flags=0x20101), A, A, A, None) == E_SPEC          # bits above the clip fields and the bf16 flag
     assert f(MIS, 4, _spec(), A, A, A, None) == E_ALIGN
     assert f(A, 4, _spec(), A, A, MIS, None) == E_ALIGN
     assert f(MIS, 4, _spec(), A, A, None, None) == E_ALIGN
@@ -210,6 +210,10 @@ def test_fused_validation(L):
     assert f(P(_pw(K=8192)), A, 1, _spec(K=8192, block=8192), A, None, None, None, None, None) == E_SPEC
     assert f(P(_pw()), A, 1, _spec(K=256, block=256, num=17, den=18), A, None, None, None, None, None) == E_SPEC
     assert f(P(_pw()), MIS, 1, sp, A, None, None, None, None, None) == E_ALIGN
+    # the bf16 flag is accepted (validation reaches the alignment check); a bit above it is not
+    bf = _spec(K=256, block=256, flags=qift.SPEC_BF16)
+    assert f(P(_pw()), MIS, 1, bf, A, None, None, None, None, None) == E_ALIGN
+    assert f(P(_pw()), A, 1, _spec(K=256, block=256, flags=1 << 17), A, None, None, None, None, None) == E_SPEC
 
 
 def test_read_probe_validation(L):
