@@ -30,6 +30,10 @@ reads the counter files of two rocprofv3 --pmc runs of this script (FETCH_SIZE, 
 with --copy-probe) and writes profiles/decode_chain_cfg2_m1_traffic.json, the HBM bytes per launch of
 the decode chain that the ``roofline`` of later runs reports while the kernel's sources are unchanged.
 
+Where a linear runs on the codes of a separate rotate_quant_act call, it is given the per-token code
+sums that call produced (the _ex form of the linear); without them the kernels add up the codes
+themselves.
+
 All inputs are seeded synthetic data resident in HBM before timing starts.
 """
 from __future__ import annotations
@@ -254,14 +258,16 @@ class PrefillStack:
             ws = self.weights[layer]
             for i, (name, N, K, b, site) in enumerate(self.plan):
                 act = qift.rotate_quant_act(self.x[i], b, out=self.acts[i])
-                qift.linear(ws[i], act, out=self.outs[i])
+                qift.linear(ws[i], act, out=self.outs[i], use_sum=True)
 
 
 class SweepStack:
     """32 distinct seeded layers of one config at M tokens: cfg2 (LLaMA-3.1-8B, MNZ; q|k|v, o, gate|up,
     down) or cfg3 (LLaMA-3.1-8B MLP, PoT; gate|up, down), every linear on a fixed synthetic input of its
-    site (no dependency between linears).  M <= 4 runs the fused rotate+linear entry, larger M one
-    rotate_quant_act per input and the linear on its codes."""
+    site (no dependency between linears).  M = 1 runs the fused rotate+linear entry, larger M one
+    rotate_quant_act per input and the linear on its codes (the fused entry also takes M = 4, but
+    measured slower there: 2.59 vs 1.58 ms for this stack, its workgroups each rotating all four
+    tokens of K = 14336)."""
 
     def __init__(self, torch, qift, synth, cfg, M, layers=32):
         self.torch, self.qift, self.synth = torch, qift, synth
@@ -274,7 +280,7 @@ class SweepStack:
             self.plan = [("qkv", sh["q"].N + sh["k"].N + sh["v"].N, sh["q"].K, sh["q"].block, 0),
                          ("o", sh["o"].N, sh["o"].K, sh["o"].block, 1)] + self.plan
         self.fmt = c.fmt_of_layer[0]
-        self.fused = M <= 4   # the fused entry takes up to 4 tokens; for more, one rotation per input
+        self.fused = M == 1   # fused entry at one token; for more, one rotation per input then the linear
 
     def setup(self):
         torch, qift, synth = self.torch, self.qift, self.synth
@@ -307,7 +313,7 @@ class SweepStack:
                     qift.rotate_quant_linear(ws[i], self.x[i], b, out=self.outs[i])
                 else:
                     act = qift.rotate_quant_act(self.x[i], b, out=self.acts[i])
-                    qift.w2a4_linear(ws[i], act, out=self.outs[i])
+                    qift.w2a4_linear(ws[i], act, out=self.outs[i], use_sum=True)
 
 
 def stack_sweep(torch, qift, synth, reps=20):
@@ -392,7 +398,7 @@ def decode_per_shape(torch, qift, synth, min_bytes=1 << 30, reps=10):
 
         def lin():
             for w in reps_w:
-                qift.w2a4_linear(w, act, out=y)
+                qift.w2a4_linear(w, act, out=y, use_sum=True)
 
         def probe():
             for w in reps_w:
@@ -452,7 +458,7 @@ def lut_decode(torch, qift, synth, min_bytes=1 << 29, reps=10):
 
         def mnz():
             for w in reps_i:
-                qift.w2a4_linear(w, act, out=y)
+                qift.w2a4_linear(w, act, out=y, use_sum=True)
         t = _time_graph(torch, mnz, reps)
         row["mnz_integer_us"] = round(t / R * 1e6, 2)
         rows.append(row)
@@ -920,7 +926,7 @@ def main():
                     variants.append(("FP4 x FP6 MFMA", torch.empty(qift.workspace_bytes(w, pre.M),
                                                                    dtype=torch.uint8, device="cuda")))
                 for path, ws in variants:
-                    dt = _time_graph(torch, lambda: qift.linear(w, pre.acts[i], out=pre.outs[i], workspace=ws), 10)
+                    dt = _time_graph(torch, lambda: qift.linear(w, pre.acts[i], out=pre.outs[i], workspace=ws, use_sum=True), 10)
                     per_shape.append({"linear": name, "format": fname, "path": path, "N": N, "K": K,
                                       "us": round(dt * 1e6, 2), "int8_tops": round(ops / dt / 1e12, 2),
                                       "pct_int8_peak": round(100 * ops / dt / 1e12 / INT8_PEAK_TOPS, 2)})

@@ -127,21 +127,6 @@ __device__ __forceinline__ void load_chunk_rt(uint4 (&wr)[16], const ChainDesc& 
   }
 }
 
-// Bit planes of a lane's four packed MNZ words with two accumulators: planes 0 and 3 as codes (factor
-// 1), planes 1 and 2 as codes times 4 (plane 2 shifted down by one field), so that
-//   D = acc03 + acc12 / 4,
-// exact since acc12 is 4 times an integer sum.  One more shift per word than qift_mma.h's
-// decode_plane, half the accumulators: the registers that a workgroup of seven 16-row tiles needs.
-__device__ __forceinline__ v4i decode_plane2(const uint4& u, int t) {
-  if (t == 0) return v4i{(int)(u.x & 0x03030303u), (int)(u.y & 0x03030303u), (int)(u.z & 0x03030303u), (int)(u.w & 0x03030303u)};
-  if (t == 1) return v4i{(int)(u.x & 0x0C0C0C0Cu), (int)(u.y & 0x0C0C0C0Cu), (int)(u.z & 0x0C0C0C0Cu), (int)(u.w & 0x0C0C0C0Cu)};
-  if (t == 2)
-    return v4i{(int)((u.x >> 2) & 0x0C0C0C0Cu), (int)((u.y >> 2) & 0x0C0C0C0Cu), (int)((u.z >> 2) & 0x0C0C0C0Cu),
-               (int)((u.w >> 2) & 0x0C0C0C0Cu)};
-  return v4i{(int)((u.x >> 6) & 0x03030303u), (int)((u.y >> 6) & 0x03030303u), (int)((u.z >> 6) & 0x03030303u),
-             (int)((u.w >> 6) & 0x03030303u)};
-}
-
 // MFMAs of one chunk; the slice's partial sums of tile j go to red[(j * NS + slice) * 64 + lane].
 template <int FMT, int T, bool LONG>
 __device__ __forceinline__ void mfma_chunk(uint4 (&wr)[16], const ChainDesc& d, int tile0, int slice,

@@ -139,6 +139,13 @@ QIFT_CHAIN_LAUNCHER(launch_chain_w4);
 // Limits of the fused entry point.
 constexpr int64_t kFusedMaxM = 4;
 constexpr int64_t kCodesMaxM = 16;   // one MFMA column block of tokens
+// Skinny decode linear (qift_skinny.hip): up to 64 tokens in one pass over the weights, codes read
+// from memory by the K-slice waves.
+constexpr int64_t kSkinnyMaxM = 64;
+constexpr int64_t kSkinnyMaxK = 16384;
+hipError_t launch_skinny(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
+                         const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
+                         uint16_t* out, int32_t* acc_out, hipStream_t s);
 constexpr int64_t kFusedMaxK = 16384;
 constexpr int kFusedMaxBlock = 4096;
 // Largest K accepted by the activation quantizer.

@@ -560,37 +560,21 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
   if constexpr (FMT == FMT_MNZ) {
     if (ws && M >= kGemmF4MinM) return launch_gemm_f4(P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
   }
-  if (M <= 4 * kCodesMaxM) {
-    // the decode kernel on precomputed codes (K-slice weight waves), once per block of mb tokens:
-    // for M > 16 the largest block of at most 16 tokens whose codes fit in LDS (the GEMM's grid of
-    // N/256 x ceil(M/64) workgroups would leave most CUs idle; later blocks stream the weights
-    // again, largely from the Infinity Cache).
-    auto shmem = [&](int64_t mb) {
-      return FMT == FMT_MNZ ? codes_shmem_mnz(mb, N, K) : FMT == FMT_POT ? codes_shmem_pot(mb, N, K)
-                                                                          : codes_shmem_w4(mb, N, K);
-    };
-    int64_t mb = M < kCodesMaxM ? M : kCodesMaxM;
-    // M <= 16 takes one block or none (measured: splitting 16 tokens at K = 14336 into two blocks
-    // of 8 is slower than the decode kernel reading the codes from HBM)
-    while (M > kCodesMaxM && mb > 1 && (shmem(mb) == 0 || shmem(mb) > 160 * 1024)) mb = (mb + 1) / 2;
-    const size_t cs = shmem(mb);
+  // 17..64 tokens: the skinny kernel, one pass over the weights (the codes of that many tokens do not
+  // fit the decode kernel's LDS, and the GEMM's grid of N/256 workgroups would leave most CUs idle)
+  if (M > kCodesMaxM && M <= kSkinnyMaxM && K <= kSkinnyMaxK)
+    return launch_skinny(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, s);
+  if (M <= kCodesMaxM) {
+    // the decode kernel on precomputed codes (K-slice weight waves, the codes staged in LDS)
+    const size_t cs = FMT == FMT_MNZ ? codes_shmem_mnz(M, N, K) : FMT == FMT_POT ? codes_shmem_pot(M, N, K)
+                                                                                  : codes_shmem_w4(M, N, K);
     if (cs != 0 && cs <= 160 * 1024) {
-      for (int64_t m0 = 0; m0 < M; m0 += mb) {
-        const int64_t mm = M - m0 < mb ? M - m0 : mb;
-        const int8_t* a = act + m0 * K;
-        const int32_t* as = asum ? asum + m0 : nullptr;   // no sums given: summed in the kernel
-        uint16_t* yb = y + m0 * N;
-        int32_t* ab = acc_out ? acc_out + m0 * N : nullptr;
-        hipError_t e;
-        if constexpr (FMT == FMT_MNZ) e = launch_codes_mnz(P, sw, N, K, a, sx + m0, as, mm, yb, ab, s);
-        else if constexpr (FMT == FMT_POT) e = launch_codes_pot(P, sw, N, K, a, sx + m0, as, mm, yb, ab, s);
-        else e = launch_codes_w4(P, sw, N, K, a, sx + m0, as, mm, yb, ab, s);
-        if (e != hipSuccess) return e;
-      }
-      return hipSuccess;
+      if constexpr (FMT == FMT_MNZ) return launch_codes_mnz(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
+      else if constexpr (FMT == FMT_POT) return launch_codes_pot(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
+      else return launch_codes_w4(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
     }
-  }
-  if (M <= 16) {
+    // codes beyond LDS (e.g. 16 tokens of K = 14336): the decode kernels that read them from memory
+    // (measured faster there than the skinny kernel with one token tile: 16 tokens at K = 14336)
     if (M * kpad_of(K) <= kDecodeMaxLds) return launch_deep<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
     return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
   }

@@ -119,6 +119,21 @@ __device__ __forceinline__ v4i combine_planes(const v4i& a03, const v4i& a1, con
   return d;
 }
 
+// Bit planes of a lane's four packed MNZ words with two accumulators: planes 0 and 3 as codes (factor
+// 1), planes 1 and 2 as codes times 4 (plane 2 shifted down by one field), so that
+//   D = acc03 + acc12 / 4,
+// exact since acc12 is 4 times an integer sum.  One more shift per word than
+// decode_plane, half the accumulators (for kernels that hold many tiles' accumulators).
+__device__ __forceinline__ v4i decode_plane2(const uint4& u, int t) {
+  if (t == 0) return v4i{(int)(u.x & 0x03030303u), (int)(u.y & 0x03030303u), (int)(u.z & 0x03030303u), (int)(u.w & 0x03030303u)};
+  if (t == 1) return v4i{(int)(u.x & 0x0C0C0C0Cu), (int)(u.y & 0x0C0C0C0Cu), (int)(u.z & 0x0C0C0C0Cu), (int)(u.w & 0x0C0C0C0Cu)};
+  if (t == 2)
+    return v4i{(int)((u.x >> 2) & 0x0C0C0C0Cu), (int)((u.y >> 2) & 0x0C0C0C0Cu), (int)((u.z >> 2) & 0x0C0C0C0Cu),
+               (int)((u.w >> 2) & 0x0C0C0C0Cu)};
+  return v4i{(int)((u.x >> 6) & 0x03030303u), (int)((u.y >> 6) & 0x03030303u), (int)((u.z >> 6) & 0x03030303u),
+             (int)((u.w >> 6) & 0x03030303u)};
+}
+
 // Sum of the 16 signed bytes of a 16-byte group of activation codes (four dot products with 1).
 __device__ __forceinline__ int sum16_i8(const uint4& b, int acc) {
   acc = __builtin_amdgcn_sdot4((int)b.x, 0x01010101, acc, false);
