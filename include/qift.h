@@ -257,12 +257,13 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
  *   workspace, workspace_bytes   optional device scratch (16-byte aligned).
  *              NULL / 0 runs the int8 MFMA kernels.  With at least
  *              qift_workspace_bytes(w, M) bytes, where that is not 0 (MNZ
- *              weights, M > 64), the activations are re-coded to FP6 E2M3
- *              in it and the prefill contraction runs on the FP4 x FP6
- *              scaled MFMA: the MNZ code c read as FP4 E2M1 is c / 2 and
- *              every partial sum stays exact in fp32, so the results are
- *              bit-identical.  A non-zero size below the query is
- *              QIFT_ERR_WORKSPACE.  The workspace is overwritten.
+ *              and PoT weights, M > 64), the activations are re-coded to FP6
+ *              E2M3 in it and the prefill contraction runs on the FP4 x FP6
+ *              scaled MFMA: the MNZ code c read as FP4 E2M1 is c / 2, the
+ *              PoT levels +-1, +-4 are E2M1 values, and every partial sum
+ *              stays exact in fp32, so the results are bit-identical.  A
+ *              non-zero size below the query is QIFT_ERR_WORKSPACE.  The
+ *              workspace is overwritten.
  */
 int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
                         const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
@@ -498,7 +499,8 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
                                       const uint8_t *v_zeros, uint16_t *out, qift_stream_t stream);
 
 /* Workspace bytes that select the FP4 x FP6 prefill kernel in the _ex calls for this weight and
- * M (M * 3K/4 for MNZ weights at M > 64), 0 where no workspace is used (host query). */
+ * M (M * 3K/4 plus the code sums, for MNZ and PoT weights at M > 64), 0 where no workspace is used
+ * (host query). */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
 
 /* Static text for a status code. */

@@ -44,13 +44,13 @@ hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
                          uint16_t* out, int32_t* acc_out, void* ws, hipStream_t s);
 
-// MNZ prefill on the FP4 x FP6 scaled MFMA (qift_prefill_f4.hip): act_q re-coded to FP6 into ws
-// (gemm_f4_workspace(M, K) bytes), then the GEMM; results identical to the int8 kernel.
+// MNZ and PoT prefill on the FP4 x FP6 scaled MFMA (qift_prefill_f4.hip): act_q re-coded to FP6
+// into ws (gemm_f4_workspace(M, K) bytes), then the GEMM; results identical to the int8 kernel.
 constexpr int64_t kGemmF4MinM = 65;
 size_t gemm_f4_workspace(int64_t M, int64_t K);
-hipError_t launch_gemm_f4(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act_q,
-                          const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
-                          hipStream_t s);
+hipError_t launch_gemm_f4(int fmt, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
+                          const int8_t* act_q, const float* sx, const int32_t* asum, int64_t M, uint16_t* y,
+                          int32_t* acc_out, void* ws, hipStream_t s);
 
 // Fused rotation + quantization + linear for a few decode tokens, one launcher
 // per weight format (qift_fused_<fmt>.hip).

@@ -557,8 +557,8 @@ template <int FMT>
 hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
                       const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
                       hipStream_t s) {
-  if constexpr (FMT == FMT_MNZ) {
-    if (ws && M >= kGemmF4MinM) return launch_gemm_f4(P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
+  if constexpr (FMT != FMT_W4) {
+    if (ws && M >= kGemmF4MinM) return launch_gemm_f4(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
   }
   // 17..64 tokens: the skinny kernel, one pass over the weights (the codes of that many tokens do not
   // fit the decode kernel's LDS, and the GEMM's grid of N/256 workgroups would leave most CUs idle)
@@ -615,7 +615,7 @@ hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales
     case FMT_MNZ:
       return launch_fmt<FMT_MNZ>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, ws, s);
     case FMT_POT:
-      return launch_fmt<FMT_POT>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, nullptr, s);
+      return launch_fmt<FMT_POT>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, ws, s);
     case FMT_W4:
       return launch_fmt<FMT_W4>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, nullptr, s);
     default: return hipErrorInvalidValue;

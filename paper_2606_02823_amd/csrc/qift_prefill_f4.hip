@@ -1,11 +1,15 @@
-// Prefill linear for MNZ weights on the CDNA4 scaled MFMA with FP4 (E2M1) weights and FP6 (E2M3)
+// Prefill linear for W2 weights on the CDNA4 scaled MFMA with FP4 (E2M1) weights and FP6 (E2M3)
 // activations, v_mfma_scale_f32_16x16x128_f8f6f4 with unit scales (E8M0 127).
 //
-// Exactness: an MNZ code c in 0..3 read as the E2M1 nibble 0b00cc is c / 2 (0, 0.5, 1, 1.5) and
+// Exactness, MNZ: a code c in 0..3 read as the E2M1 nibble 0b00cc is c / 2 (0, 0.5, 1, 1.5) and
 // the INT4 codes -7..7 are exact in E2M3, so every product is c q / 2 and every partial sum a
 // multiple of 1/2 below 2^23: the fp32 accumulator holds D = sum c q / 2 exactly, and the integer
-// accumulator of the method is acc = 2 (2 D) - 3 sum q (Sec. 3.3: level = 2 c - 3).  Results are
-// bit-identical to the int8 path.
+// accumulator of the method is acc = 2 (2 D) - 3 sum q (Sec. 3.3: level = 2 c - 3).
+// PoT-MNZ: the levels -4, -1, +1, +4 (Sec. 3.3, Eq. (17)) are themselves E2M1 values (0b1110,
+// 0b1010, 0b0010, 0b0110): for the code c = 2 b1 + b0 the nibble has sign bit !b1, exponent bits
+// (!(b1 ^ b0), 1) and mantissa 0, built from the masked code nibbles by a few bitwise operations
+// per word; every product level q and every partial sum (|sum| <= 28 K < 2^24) is an integer, so
+// the accumulator holds acc = sum level q exactly.  Results are bit-identical to the int8 path.
 //
 // Operand layouts (measured on gfx950): A lane (row r, group g) nibble i <-> k = 32 g + i of the
 // MFMA's 128; B lane (column m, group g) element i at bits 6 i .. 6 i + 5 of its 192 bits <-> the
@@ -85,7 +89,13 @@ __global__ __launch_bounds__(256) void k_act_fp6(const int8_t* __restrict__ act_
 // two 16x16x128 MFMAs per row tile and step instead of four 16x16x64 ones.  The step's FP6 row is
 // 192 bytes: twelve 16-byte chunks in a 256-byte LDS row, chunk c of row r in slot c ^ (r mod 16)
 // (the four spare slots receive zeros).
-template <int OCC>
+// FP4 operand nibbles of eight PoT codes from their masked code nibbles 0b00cc (see above)
+__device__ __forceinline__ uint32_t pot_f4(uint32_t x) {
+  const uint32_t b0 = x & 0x11111111u, b1 = (x >> 1) & 0x11111111u;
+  return ((b1 ^ 0x11111111u) << 3) | ((b1 ^ b0 ^ 0x11111111u) << 2) | 0x22222222u;
+}
+
+template <int FMT, int OCC>
 __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                       int N, int K, const uint8_t* __restrict__ act6,
                                                       const float* __restrict__ sx, const int32_t* __restrict__ asum,
@@ -160,8 +170,15 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t w0 = kb ? wc[j].z : wc[j].x, w1 = kb ? wc[j].w : wc[j].y;
-        a[j] = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u), (int)(w1 & 0x33333333u),
-                   (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+        uint32_t n0 = w0 & 0x33333333u, n1 = (w0 >> 2) & 0x33333333u, n2 = w1 & 0x33333333u,
+                 n3 = (w1 >> 2) & 0x33333333u;
+        if constexpr (FMT == FMT_POT) {
+          n0 = pot_f4(n0);
+          n1 = pot_f4(n1);
+          n2 = pot_f4(n2);
+          n3 = pot_f4(n3);
+        }
+        a[j] = v8i{(int)n0, (int)n1, (int)n2, (int)n3, 0, 0, 0, 0};
       }
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
@@ -206,10 +223,11 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        // 2 D = sum c q exactly (an integer below 2^24)
-        const v4i D = v4i{(int)(2.f * acc[j][t][0]), (int)(2.f * acc[j][t][1]), (int)(2.f * acc[j][t][2]),
-                          (int)(2.f * acc[j][t][3])};
-        store4<FMT_MNZ>(D, m, n_base + 16 * j + 4 * g, N, s_x, sq, sw, y, acc_out);
+        // MNZ: 2 D = sum c q exactly (an integer below 2^24); PoT: D = sum level q exactly
+        const float f = FMT == FMT_MNZ ? 2.f : 1.f;
+        const v4i D = v4i{(int)(f * acc[j][t][0]), (int)(f * acc[j][t][1]), (int)(f * acc[j][t][2]),
+                          (int)(f * acc[j][t][3])};
+        store4<FMT>(D, m, n_base + 16 * j + 4 * g, N, s_x, sq, sw, y, acc_out);
       }
     }
   }
@@ -225,9 +243,9 @@ size_t gemm_f4_workspace(int64_t M, int64_t K) {
   return (size_t)M * (size_t)(3 * (K / 4)) + (size_t)M * (size_t)act_fp6_blocks(K) * 4;
 }
 
-hipError_t launch_gemm_f4(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act_q,
-                          const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
-                          hipStream_t s) {
+hipError_t launch_gemm_f4(int fmt, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
+                          const int8_t* act_q, const float* sx, const int32_t* asum, int64_t M, uint16_t* y,
+                          int32_t* acc_out, void* ws, hipStream_t s) {
   uint8_t* act6 = static_cast<uint8_t*>(ws);
   int32_t* psum = asum ? nullptr : reinterpret_cast<int32_t*>(act6 + (size_t)M * (size_t)(3 * (K / 4)));
   const int gx = (int)act_fp6_blocks(K);
@@ -235,8 +253,15 @@ hipError_t launch_gemm_f4(const uint32_t* P, const uint16_t* sw, int64_t N, int6
   hipLaunchKernelGGL(k_act_fp6, dim3((unsigned)gx, gy), dim3(256), 0, s, act_q, (int)M, (int)K, act6, psum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_gemm_f4<3>), dim3((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64)), dim3(256), 0, s, P,
-                     sw, (int)N, (int)K, act6, sx, asum, psum, gx, (int)M, y, acc_out);
+  const dim3 grid((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64));
+  if (fmt == FMT_POT)
+    hipLaunchKernelGGL((k_gemm_f4<FMT_POT, 3>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum, psum, gx,
+                       (int)M, y, acc_out);
+  else if (fmt == FMT_MNZ)
+    hipLaunchKernelGGL((k_gemm_f4<FMT_MNZ, 3>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum, psum, gx,
+                       (int)M, y, acc_out);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

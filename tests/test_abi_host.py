@@ -183,11 +183,11 @@ def test_linear_validation(L):
     assert w2x(P(_pw()), None, A, None, 4, A, None, None, 0, None) == E_NULL
     assert w4x(P(_pw(fmt=qift.W2_MNZ)), A, A, None, 4, A, None, None, 0, None) == E_FORMAT
     assert L.qift_workspace_bytes(P(_pw()), 4) == 0
-    # the workspace that selects the FP4 x FP6 prefill kernel: MNZ at M > 64, M * 3K/4 bytes
+    # the workspace that selects the FP4 x FP6 prefill kernel: MNZ and PoT at M > 64, M * 3K/4 bytes
     K = _pw().K
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 64) == 0
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 65) == 65 * 3 * (K // 4) + 65 * 4
-    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT)), 65) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT)), 65) == 65 * 3 * (K // 4) + 65 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM)), 65) == 0
     # FP6 codes (M 3K/4 bytes), then one int32 code sum per token and 256 groups of 32 k
     need = 100 * 3 * (K // 4) + 100 * 4

@@ -128,13 +128,15 @@ def test_linear_ragged(Q, fmt, M):
     assert torch.equal(y3.view(torch.int16), y.view(torch.int16))
 
 
+@pytest.mark.parametrize("fmt", [levels.FMT_W2_MNZ, levels.FMT_W2_POT])
 @pytest.mark.parametrize("M,K", [(65, 1088), (130, 1088), (300, 4096), (200, 14336)])
-def test_mnz_prefill_int8_and_fp4_paths(Q, M, K):
-    # MNZ at M > 64: the int8 GEMM (no workspace) and the FP4 x FP6 GEMM (FP6 activations in a
-    # workspace of workspace_bytes), ragged rows and tokens, K with a partial last step
-    fmt, N, b = levels.FMT_W2_MNZ, 1000, 64
-    L = synth.draw_levels(fmt, N, K, cfg=97, layer=M)
-    s_w = synth.draw_scales(fmt, N, cfg=97, layer=M)
+def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, K):
+    # W2 (MNZ, PoT) at M > 64: the int8 GEMM (no workspace) and the FP4 x FP6 GEMM (FP6 activations
+    # in a workspace of workspace_bytes; the MNZ codes as c / 2, the PoT levels +-1, +-4 as E2M1
+    # values), ragged rows and tokens, K with a partial last step: both bit-identical to the oracle
+    N, b = 1000, 64
+    L = synth.draw_levels(fmt, N, K, cfg=97, layer=M + fmt)
+    s_w = synth.draw_scales(fmt, N, cfg=97, layer=M + fmt)
     x = synth.activations_fp16(97, M, 0, M, K, K // 100, 30.0)
     pk = pack_dev(Q, L, s_w, fmt)
     act = Q.rotate_quant_act(dev(x), b)
