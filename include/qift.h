@@ -190,6 +190,59 @@ int qift_quantize_weights(const float *W, int64_t N, qift_hadamard_spec spec,
                           qift_stream_t stream);
 
 /*
+ * The same quantization onto any set of the mirror family
+ *   G(r) = {-1, -r, +r, +1},  0 < r < 1   (Sec. 3.4 Eq. (18); r = 1/3 is the
+ * MNZ grid, r = 1/4 the PoT grid, r near 0.30 the Lloyd-Max optimum of the
+ * ratio study of Sec. 4.5.3), with the PoT scale rule: the outer level is 1,
+ * s_w = fp16(c* max|w|) with c* the first minimiser over the 64 candidates
+ * c_j = 0.2 + 0.8 j / 63 of sum (w - s level)^2, and against the stored
+ * scale the level is sign(w) * (1 if |w/s_w| > (1 + r)/2 else r), sign(0) = +.
+ * The result is written as codes, the indices of the ascending levels
+ * (0: -1, 1: -r, 2: +r, 3: +1); a row whose stored scale is 0 gets code 2.
+ * The codes are the input of qift_pack_w2 with QIFT_W2_LUT, and the table of
+ * qift_w2a4_lut_linear is then {-1, -r, +r, +1} in fp16 (r rounded to fp16
+ * there, the scale unchanged).  At r = 1/4 the codes are those of the PoT
+ * levels and s_w is 4 times the PoT scale.  Same rotation, arguments, limits
+ * and caveat on the rotation's rounding as qift_quantize_weights; r outside
+ * (0, 1) (or NaN) returns QIFT_ERR_SPEC.
+ */
+int qift_quantize_weights_mirror(const float *W, int64_t N, qift_hadamard_spec spec,
+                                 double r, int8_t *codes, uint16_t *scales,
+                                 qift_stream_t stream);
+
+/*
+ * Ratio scan of the mirror family (the sensitivity study of Sec. 4.5.3):
+ * for fp64 samples x[0..n) (e.g. pooled rotated weights), every ratio
+ * ratios[i] and every clip candidate cands[j]:
+ *   s         = cands[j] * max|x|;
+ *   level     = sign(x) * (1 if |x / s| > (1 + r)/2 else r), sign(0) = +;
+ *   sse[i][j] = sum over x of (x - s level)^2   (0 for all-zero x);
+ *   best[i]   = the first j minimising sse[i][j];
+ *   nmse[i]   = sse[i][best[i]] / sum x^2        (0 where sum x^2 is 0);
+ *   stats     = {max|x|, sum x^2}.
+ * Each term is formed with correctly rounded fp64 operations in that order
+ * (quotient, compare, product, difference, square; no fused multiply-add);
+ * the n-term sums are taken in a fixed order of the library's, so sse, nmse
+ * and stats agree with any other summation order to within n ulps of the sum
+ * (and best, where two candidates' errors lie closer than that, may name
+ * either).
+ * Arguments:
+ *   x        fp64 [n], finite; 1 <= n < 2^40.
+ *   ratios   host: n_ratios values in (0, 1); 1 <= n_ratios <= 1024.
+ *   cands    host: n_cands positive finite values; 1 <= n_cands <= 256.
+ *   sse      out: fp64 [n_ratios][n_cands].
+ *   nmse     out: fp64 [n_ratios].
+ *   best     out: int32 [n_ratios].
+ *   stats    out: fp64 [2].
+ * A ratio outside (0, 1) or a candidate that is not positive and finite
+ * returns QIFT_ERR_SPEC; counts outside their ranges QIFT_ERR_SHAPE.  The
+ * host arrays are read before the call returns.  Three launches on the stream.
+ */
+int qift_ratio_scan(const double *x, int64_t n, const double *ratios, int32_t n_ratios,
+                    const double *cands, int32_t n_cands, double *sse, double *nmse,
+                    int32_t *best, double *stats, qift_stream_t stream);
+
+/*
  * Online Hadamard rotation + per-token symmetric INT4 quantization
  * (Sec. 3.1; Sec. 4.1 "Quantization configuration").  For each token m:
  *   X      = (I_{K/b} (x) H_b) x[m]   computed exactly (each fp16 input is an

@@ -196,6 +196,65 @@ def quantize_pot_mse(W_rot: np.ndarray):
     return L, s_w
 
 
+def quantize_mirror_mse(W_rot: np.ndarray, r: float):
+    """Mirror-family set ``G(r) = {-1, -r, +r, +1}`` (Sec. 3.4 Eq. (18)) with the 64-candidate MSE scale of
+    the PoT rule: ``s`` over ``linspace(0.2, 1.0, 64) * max|row|`` (the outer level is 1), first
+    minimiser of ``sum (w - s * level(w, s))^2``, stored ``s_w = fp16(best)``, levels by
+    :func:`nearest_mirror` against the stored scale (inner/outer midpoint ``(1 + r) / 2``, zero to the
+    positive inner level).  Returns (codes int8 in 0..3 for the ascending levels -1, -r, +r, +1; s_w
+    fp16).  A row whose stored scale is 0 gets code 2 (+r)."""
+    levels.mirror_family(r)   # validates r
+    W = np.asarray(W_rot, dtype=np.float64)
+    N, K = W.shape
+    a = np.abs(W).max(axis=1)
+    codes = np.full((N, K), 2, dtype=np.int8)
+    s_w = np.zeros(N, dtype=np.float16)
+    for n in range(N):
+        if a[n] == 0.0:
+            continue
+        cand = POT_CANDIDATES * a[n]
+        err = np.empty(len(cand))
+        for j, s in enumerate(cand):
+            lev = nearest_mirror(W[n] / s, r, 1.0)
+            err[j] = np.sum((W[n] - s * lev) ** 2)
+        s_w[n] = fp16_scale(cand[int(np.argmin(err))])
+        codes[n] = mirror_codes(W[n], float(s_w[n]), r)
+    return codes, s_w
+
+
+def mirror_codes(w: np.ndarray, s: float, r: float) -> np.ndarray:
+    """Codes 0..3 (ascending levels -1, -r, +r, +1) of :func:`nearest_mirror` of ``w / s`` with
+    inner ``r`` and outer 1; all 2 (+r) when ``s == 0``."""
+    w = np.asarray(w, dtype=np.float64)
+    if s == 0:
+        return np.full(w.shape, 2, dtype=np.int8)
+    lev = nearest_mirror(w / s, r, 1.0)
+    return np.where(lev >= 0, np.where(lev == 1.0, 3, 2), np.where(lev == -1.0, 0, 1)).astype(np.int8)
+
+
+def ratio_scan(x: np.ndarray, ratios, cands):
+    """Ratio-scan diagnostic (Sec. 4.5.3): for each mirror ratio r, the squared error of ``G(r)`` on the
+    samples x at every scale ``c * max|x|`` of the candidate clip ratios ``cands`` (levels by
+    :func:`nearest_mirror` of ``x / s``), and the best-scale NMSE ``min_c sse / sum x^2`` (first
+    minimiser).  Returns (sse [n_ratios, n_cands], nmse [n_ratios], best index [n_ratios], (max|x|,
+    sum x^2)).  All-zero samples have no error: sse and nmse 0; nmse is 0 too where sum x^2 is 0 (squares
+    below the fp64 range)."""
+    x = np.asarray(x, dtype=np.float64).ravel()
+    a = float(np.abs(x).max())
+    sx2 = float(np.sum(x * x))
+    sse = np.zeros((len(ratios), len(cands)))
+    if a == 0.0:
+        return sse, np.zeros(len(ratios)), np.zeros(len(ratios), dtype=np.int64), (a, sx2)
+    for i, r in enumerate(ratios):
+        for j, c in enumerate(cands):
+            s = float(c) * a
+            lev = nearest_mirror(x / s, float(r), 1.0)
+            sse[i, j] = np.sum((x - s * lev) ** 2)
+    best = np.argmin(sse, axis=1)
+    nmse = sse[np.arange(len(ratios)), best] / sx2 if sx2 > 0 else np.zeros(len(ratios))
+    return sse, nmse, best, (a, sx2)
+
+
 def rne(v: np.ndarray) -> np.ndarray:
     """Round half to even, written out on |v| (the rounding is odd-symmetric): f = floor(|v|) and the
     fractional part |v| - f, which is exact in fp64; round up when it exceeds 1/2, or equals 1/2 with

@@ -197,6 +197,36 @@ int qift_quantize_weights(const float* W, int64_t N, qift_hadamard_spec spec, in
   return hip_status(qift::launch_quantize_weights(W, N, spec.K, b, fmt, levels, scales, (hipStream_t)stream));
 }
 
+int qift_quantize_weights_mirror(const float* W, int64_t N, qift_hadamard_spec spec, double r, int8_t* codes,
+                                 uint16_t* scales, qift_stream_t stream) {
+  if (!W || !codes || !scales) return QIFT_ERR_NULL;
+  if (!shape_ok(N, spec.K) || spec.K > qift::kWquantMaxK) return QIFT_ERR_SHAPE;
+  if (N * spec.K >= (int64_t(1) << 31)) return QIFT_ERR_SHAPE;
+  const int32_t b = spec.block;
+  if (b < 2 || b > 4096 || (b & (b - 1)) || spec.K % b) return QIFT_ERR_SPEC;
+  if (spec.flags != 0) return QIFT_ERR_SPEC;
+  if (!(r > 0.0 && r < 1.0)) return QIFT_ERR_SPEC;   // also rejects NaN
+  if (!aligned16(W) || !aligned16(codes) || !aligned16(scales)) return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_quantize_weights_mirror(W, N, spec.K, b, r, codes, scales, (hipStream_t)stream));
+}
+
+int qift_ratio_scan(const double* x, int64_t n, const double* ratios, int32_t n_ratios, const double* cands,
+                    int32_t n_cands, double* sse, double* nmse, int32_t* best, double* stats,
+                    qift_stream_t stream) {
+  if (!x || !ratios || !cands || !sse || !nmse || !best || !stats) return QIFT_ERR_NULL;
+  if (n < 1 || n >= (int64_t(1) << 40)) return QIFT_ERR_SHAPE;
+  if (n_ratios < 1 || n_ratios > qift::kScanMaxRatios || n_cands < 1 || n_cands > qift::kScanMaxCands)
+    return QIFT_ERR_SHAPE;
+  for (int32_t i = 0; i < n_ratios; ++i)
+    if (!(ratios[i] > 0.0 && ratios[i] < 1.0)) return QIFT_ERR_SPEC;
+  for (int32_t j = 0; j < n_cands; ++j)
+    if (!(cands[j] > 0.0 && cands[j] <= 1e300)) return QIFT_ERR_SPEC;   // positive and finite
+  if (!aligned16(x) || !aligned16(sse) || !aligned16(nmse) || !aligned16(best) || !aligned16(stats))
+    return QIFT_ERR_ALIGN;
+  return hip_status(qift::launch_ratio_scan(x, n, ratios, n_ratios, cands, n_cands, sse, nmse, best, stats,
+                                            (hipStream_t)stream));
+}
+
 int qift_kv4_quant(const uint16_t* x, int64_t groups, int32_t head_dim, uint8_t* codes, float* scales,
                    uint8_t* zeros, qift_stream_t stream) {
   if (!x || !codes || !scales || !zeros) return QIFT_ERR_NULL;

@@ -502,7 +502,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int r16 = lane & 15, g = lane >> 4;
+  const int g = lane >> 4;
   const int G = gridDim.x, wg = blockIdx.x;
 
   const int act_bytes = (M * Kpad + 15) & ~15;

@@ -18,6 +18,15 @@ hipError_t launch_pack_w4(const int8_t* levels, int64_t N, int64_t K, uint32_t* 
 constexpr int64_t kWquantMaxK = 16384;
 hipError_t launch_quantize_weights(const float* W, int64_t N, int64_t K, int block, int fmt, int8_t* levels,
                                    uint16_t* scales, hipStream_t s);
+// The same for the mirror family {-1, -r, +r, +1}, 0 < r < 1: codes 0..3 of the ascending levels.
+hipError_t launch_quantize_weights_mirror(const float* W, int64_t N, int64_t K, int block, double r, int8_t* codes,
+                                          uint16_t* scales, hipStream_t s);
+
+// Ratio scan of the mirror family over fp64 samples (qift_scan.hip); ratios and cands are host arrays
+// of at most kScanMaxRatios / kScanMaxCands values.
+constexpr int kScanRatiosPerLaunch = 32, kScanMaxCands = 256, kScanMaxRatios = 1024;
+hipError_t launch_ratio_scan(const double* x, int64_t n, const double* ratios, int n_ratios, const double* cands,
+                             int n_cands, double* sse, double* nmse, int32_t* best, double* stats, hipStream_t s);
 
 // KV4 cache quantizer and decode attention over it (qift_kv4.hip); head dimension 128, Hq / Hkv in
 // {1, 2, 4, 8}; cache rows [B][T][Hkv] or, head_major, [B][Hkv][T]; ws holds

@@ -9,7 +9,10 @@
 //   PoT  s_w = fp16 of the first minimiser, over the 64 candidates
 //        linspace(0.2, 1, 64) * max|row| / 4, of sum (w - s * level(w, s))^2,
 //        level in {-4,-1,+1,+4} by |u| > 5/2 (Eq. (17));
-//   W4   s_w = fp16(max|row| / 7), q = clip(rne(w / s_w), -7, 7) (Eq. (1)).
+//   W4   s_w = fp16(max|row| / 7), q = clip(rne(w / s_w), -7, 7) (Eq. (1));
+//   G(r) the mirror family {-1, -r, +r, +1} (Sec. 3.4 Eq. (18)) with the PoT scale search (outer
+//        level 1: candidates linspace(0.2, 1, 64) * max|row|), the outer level where |u| > (1 + r) / 2;
+//        written as codes 0..3 of the ascending levels (the level-table linear's input).
 // Readings: a value on a midpoint takes the inner level, zero the positive one;
 // a row whose stored scale is 0 gets level +1 (W2) or 0 (W4).
 //
@@ -28,6 +31,8 @@ using mma::FMT_MNZ;
 using mma::FMT_POT;
 using mma::FMT_W4;
 namespace {
+
+constexpr int FMT_MIRROR = 3;   // G(r): a run-time inner level r, codes out
 
 // fp64 -> IEEE binary16 bits, round to nearest, ties to even, overflow to infinity (from the bit
 // fields: 10 fraction bits kept, the rest rounded; below 2^-14 in units of 2^-24).
@@ -85,9 +90,19 @@ __device__ __forceinline__ double group_sum(double v, double* red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
+// The stored value of a two-magnitude set: MNZ levels +-1 / +-3, PoT +-1 / +-4, G(r) the codes
+// 1 / 0 (negative) and 2 / 3 (positive) of the ascending levels -1, -r, +r, +1.
+template <int FMT>
+__device__ __forceinline__ int level_of(bool nonneg, bool outer) {
+  if constexpr (FMT == FMT_MIRROR) return nonneg ? (outer ? 3 : 2) : (outer ? 0 : 1);
+  const int mag = outer ? (FMT == FMT_MNZ ? 3 : 4) : 1;
+  return nonneg ? mag : -mag;
+}
+
 template <int FMT, int NTILES, int LC>
 __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__ W, int K, int L_rt, double sqrtb,
-                                                       int8_t* __restrict__ levels, uint16_t* __restrict__ scales) {
+                                                       double rin, int8_t* __restrict__ levels,
+                                                       uint16_t* __restrict__ scales) {
   using S = dev::Tile<256, 16>;
   __shared__ double xch[S::LDS_DOUBLES];
   __shared__ double red[4];
@@ -163,17 +178,20 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
     if (lane == 0) red[wave] = amax;
     __syncthreads();
     const double a = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+    // PoT: levels 1, 4 at s = c max / 4, midpoint 5/2; G(r): levels r, 1 at s = c max, midpoint (1 + r) / 2
+    const double thr = FMT == FMT_MIRROR ? 0.5 * (rin + 1.0) : 2.5;
+    const double m_in = FMT == FMT_MIRROR ? rin : 1.0, m_out = FMT == FMT_MIRROR ? 1.0 : 4.0;
     if (a > 0.0) {
       // squared error of each candidate (one candidate per iteration, the waves' partial sums into
       // LDS), then the first minimum
 #pragma unroll 1
       for (int j = 0; j < 64; ++j) {
-        const double s = pot_candidate(j) * a / 4.0;
-        // The outer level is taken where the rounded quotient |w| / s exceeds 2.5.  The sign of
-        // fma(-2.5, s, |w|) is the exact sign of |w| - 2.5 s, which decides the same way except for
-        // |w| / s in (2.5, 2.5 + 2^-52] (the quotient rounds down to 2.5 there): those few values, and
-        // only those, within 2^-51 s above the threshold, are decided by the division itself (a
-        // wave-uniform branch, rarely taken).
+        const double s = FMT == FMT_MIRROR ? pot_candidate(j) * a : pot_candidate(j) * a / 4.0;
+        // The outer level is taken where the rounded quotient |w| / s exceeds thr.  The sign of
+        // fma(-thr, s, |w|) is the exact sign of |w| - thr s, which decides the same way except for
+        // |w| / s within half an ulp of thr above it (the quotient rounds down to thr there; an ulp of
+        // thr <= 5/2 is at most 2^-51): those few values, and only those, within 2^-51 s above the
+        // threshold, are decided by the division itself (a wave-uniform branch, rarely taken).
         uint32_t outer[NTILES], near_any = 0;
 #pragma unroll
         for (int tau = 0; tau < NTILES; ++tau) {
@@ -181,7 +199,7 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
           uint32_t nr = 0;
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const double r = fma(-2.5, s, fabs(v[tau][e]));
+            const double r = fma(-thr, s, fabs(v[tau][e]));
             outer[tau] |= (uint32_t)(r > 0.0) << e;
             nr |= (uint32_t)(r > 0.0 && r <= 0x1p-51 * s) << e;
           }
@@ -192,9 +210,9 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
           for (int tau = 0; tau < NTILES; ++tau)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-              const double r = fma(-2.5, s, fabs(v[tau][e]));
+              const double r = fma(-thr, s, fabs(v[tau][e]));
               if (valid[tau] && r > 0.0 && r <= 0x1p-51 * s) {
-                const bool o = fabs(v[tau][e] / s) > 2.5;
+                const bool o = fabs(v[tau][e] / s) > thr;
                 outer[tau] = (outer[tau] & ~(1u << e)) | ((uint32_t)o << e);
               }
             }
@@ -206,7 +224,7 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const double w = v[tau][e];
-            const double mag = (outer[tau] >> e) & 1u ? 4.0 : 1.0;
+            const double mag = (outer[tau] >> e) & 1u ? m_out : m_in;
             const double d = w - s * (w >= 0.0 ? mag : -mag);
             acc += d * d;
           }
@@ -224,7 +242,7 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
           best_j = j;
         }
       }
-      sw = half_bits_rne(pot_candidate(best_j) * a / 4.0);
+      sw = half_bits_rne(FMT == FMT_MIRROR ? pot_candidate(best_j) * a : pot_candidate(best_j) * a / 4.0);
     }
   }
   if (t == 0) scales[n] = sw;
@@ -237,8 +255,7 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
   // lies clearly inside half a step.  The rest (a wave-uniform branch, rarely taken) divide.
   const double s_w = half_value(sw);
   const double inv_sw = s_w > 0.0 ? 1.0 / s_w : 0.0;
-  constexpr double thr = FMT == FMT_MNZ ? 2.0 : 2.5;
-  constexpr int hi = FMT == FMT_MNZ ? 3 : 4;
+  const double thr = FMT == FMT_MNZ ? 2.0 : FMT == FMT_POT ? 2.5 : 0.5 * (rin + 1.0);
 #pragma unroll
   for (int tau = 0; tau < NTILES; ++tau) {
     if (!valid[tau]) continue;
@@ -254,8 +271,7 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
         nr |= (uint32_t)(fabs(res) >= (0.5 - 0x1p-45) * s_w) << e;
       } else {
         const double r = fma(-thr, s_w, fabs(w));
-        const int mag = r > 0.0 ? hi : 1;
-        q[e] = w >= 0.0 ? mag : -mag;
+        q[e] = level_of<FMT>(w >= 0.0, r > 0.0);
         nr |= (uint32_t)(r > 0.0 && r <= 0x1p-51 * s_w) << e;
       }
     }
@@ -268,15 +284,14 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
             if constexpr (FMT == FMT_W4) {
               q[e] = (int)fmin(fmax(rint(u), -7.0), 7.0);
             } else {
-              const int mag = fabs(u) > thr ? hi : 1;
-              q[e] = u >= 0.0 ? mag : -mag;
+              q[e] = level_of<FMT>(u >= 0.0, fabs(u) > thr);
             }
           }
         }
       }
     } else {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) q[e] = FMT == FMT_W4 ? 0 : 1;
+      for (int e = 0; e < 16; ++e) q[e] = FMT == FMT_W4 ? 0 : FMT == FMT_MIRROR ? 2 : 1;
     }
     uint32_t wd[4] = {0, 0, 0, 0};
 #pragma unroll
@@ -286,34 +301,34 @@ __global__ __launch_bounds__(256) void k_quant_weights(const float* __restrict__
 }
 
 template <int FMT, int NTILES, int LC>
-hipError_t launch_l(const float* W, int64_t N, int64_t K, int L, double sqrtb, int8_t* levels, uint16_t* scales,
-                    hipStream_t s) {
+hipError_t launch_l(const float* W, int64_t N, int64_t K, int L, double sqrtb, double r, int8_t* levels,
+                    uint16_t* scales, hipStream_t s) {
   hipLaunchKernelGGL((k_quant_weights<FMT, NTILES, LC>), dim3((unsigned)N), dim3(256), 0, s, W, (int)K, L, sqrtb,
-                     levels, scales);
+                     r, levels, scales);
   return hipGetLastError();
 }
 
 // block exponents compiled as constants: 12, 11, 8 and 6; anything else at run time
 template <int FMT, int NTILES>
-hipError_t launch_nt(const float* W, int64_t N, int64_t K, int L, double sqrtb, int8_t* levels, uint16_t* scales,
-                     hipStream_t s) {
+hipError_t launch_nt(const float* W, int64_t N, int64_t K, int L, double sqrtb, double r, int8_t* levels,
+                     uint16_t* scales, hipStream_t s) {
   switch (L) {
-    case 12: return launch_l<FMT, NTILES, 12>(W, N, K, L, sqrtb, levels, scales, s);
-    case 11: return launch_l<FMT, NTILES, 11>(W, N, K, L, sqrtb, levels, scales, s);
-    case 8: return launch_l<FMT, NTILES, 8>(W, N, K, L, sqrtb, levels, scales, s);
-    case 6: return launch_l<FMT, NTILES, 6>(W, N, K, L, sqrtb, levels, scales, s);
-    default: return launch_l<FMT, NTILES, 0>(W, N, K, L, sqrtb, levels, scales, s);
+    case 12: return launch_l<FMT, NTILES, 12>(W, N, K, L, sqrtb, r, levels, scales, s);
+    case 11: return launch_l<FMT, NTILES, 11>(W, N, K, L, sqrtb, r, levels, scales, s);
+    case 8: return launch_l<FMT, NTILES, 8>(W, N, K, L, sqrtb, r, levels, scales, s);
+    case 6: return launch_l<FMT, NTILES, 6>(W, N, K, L, sqrtb, r, levels, scales, s);
+    default: return launch_l<FMT, NTILES, 0>(W, N, K, L, sqrtb, r, levels, scales, s);
   }
 }
 
 template <int FMT>
-hipError_t launch_fmt(const float* W, int64_t N, int64_t K, int L, double sqrtb, int8_t* levels, uint16_t* scales,
-                      hipStream_t s) {
+hipError_t launch_fmt(const float* W, int64_t N, int64_t K, int L, double sqrtb, double r, int8_t* levels,
+                      uint16_t* scales, hipStream_t s) {
   switch ((K + 4095) / 4096) {
-    case 1: return launch_nt<FMT, 1>(W, N, K, L, sqrtb, levels, scales, s);
-    case 2: return launch_nt<FMT, 2>(W, N, K, L, sqrtb, levels, scales, s);
-    case 3: return launch_nt<FMT, 3>(W, N, K, L, sqrtb, levels, scales, s);
-    case 4: return launch_nt<FMT, 4>(W, N, K, L, sqrtb, levels, scales, s);
+    case 1: return launch_nt<FMT, 1>(W, N, K, L, sqrtb, r, levels, scales, s);
+    case 2: return launch_nt<FMT, 2>(W, N, K, L, sqrtb, r, levels, scales, s);
+    case 3: return launch_nt<FMT, 3>(W, N, K, L, sqrtb, r, levels, scales, s);
+    case 4: return launch_nt<FMT, 4>(W, N, K, L, sqrtb, r, levels, scales, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -325,11 +340,16 @@ hipError_t launch_quantize_weights(const float* W, int64_t N, int64_t K, int blo
   const int L = dev::ilog2c(block);
   const double sqrtb = sqrt((double)block);
   switch (fmt) {
-    case FMT_MNZ: return launch_fmt<FMT_MNZ>(W, N, K, L, sqrtb, levels, scales, s);
-    case FMT_POT: return launch_fmt<FMT_POT>(W, N, K, L, sqrtb, levels, scales, s);
-    case FMT_W4: return launch_fmt<FMT_W4>(W, N, K, L, sqrtb, levels, scales, s);
+    case FMT_MNZ: return launch_fmt<FMT_MNZ>(W, N, K, L, sqrtb, 0.0, levels, scales, s);
+    case FMT_POT: return launch_fmt<FMT_POT>(W, N, K, L, sqrtb, 0.0, levels, scales, s);
+    case FMT_W4: return launch_fmt<FMT_W4>(W, N, K, L, sqrtb, 0.0, levels, scales, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_quantize_weights_mirror(const float* W, int64_t N, int64_t K, int block, double r, int8_t* codes,
+                                          uint16_t* scales, hipStream_t s) {
+  return launch_fmt<FMT_MIRROR>(W, N, K, dev::ilog2c(block), sqrt((double)block), r, codes, scales, s);
 }
 
 }  // namespace qift

@@ -29,7 +29,8 @@ STATUS = {0: "QIFT_OK", -1: "QIFT_ERR_NULL", -2: "QIFT_ERR_SHAPE", -3: "QIFT_ERR
 DEVERR_GROUP_WAIT, DEVERR_CHAIN_WAIT = 1, 2   # bits of the device error word (qift_device_error)
 
 # every symbol declared in include/qift.h
-EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights", "qift_kv4_quant",
+EXPORTS = ("qift_packed_bytes", "qift_pack_w2", "qift_pack_w4", "qift_quantize_weights",
+           "qift_quantize_weights_mirror", "qift_ratio_scan", "qift_kv4_quant",
            "qift_kv4_attention_workspace_bytes", "qift_kv4_attention_decode", "qift_kv4_attention_decode_noalloc", "qift_rotate_quant_act",
            "qift_rotate_quant_act_bf16",
            "qift_w2a4_linear", "qift_w2a4_linear_ex", "qift_w2a4_lut_linear", "qift_w4a4_linear", "qift_w4a4_linear_ex",
@@ -97,6 +98,8 @@ def lib():
         "qift_pack_w2": (ctypes.c_int, [vp, vp, i64, i64, i32, vp, pw, vp]),
         "qift_pack_w4": (ctypes.c_int, [vp, vp, i64, i64, vp, pw, vp]),
         "qift_quantize_weights": (ctypes.c_int, [vp, i64, HadamardSpec, i32, vp, vp, vp]),
+        "qift_quantize_weights_mirror": (ctypes.c_int, [vp, i64, HadamardSpec, ctypes.c_double, vp, vp, vp]),
+        "qift_ratio_scan": (ctypes.c_int, [vp, i64, vp, i32, vp, i32, vp, vp, vp, vp, vp]),
         "qift_kv4_quant": (ctypes.c_int, [vp, i64, i32, vp, vp, vp, vp]),
         "qift_kv4_attention_workspace_bytes": (sz, [i64, i32, i32, i32, i64]),
         "qift_kv4_attention_decode": (ctypes.c_int, [vp, i64, i32, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz,
@@ -249,6 +252,44 @@ def quantize_weights(W: torch.Tensor, block: int, fmt: int, levels: torch.Tensor
                                      scales.data_ptr(), _stream(stream))
     _check("qift_quantize_weights", st)
     return levels, scales
+
+
+def quantize_weights_mirror(W: torch.Tensor, block: int, r: float, codes: torch.Tensor | None = None,
+                            scales: torch.Tensor | None = None, stream=None):
+    """Rotate the rows of fp32 W [N, K], take the 64-candidate MSE scale of the set {-1, -r, +r, +1} and
+    the nearest codes 0..3 (ascending levels; the input of pack_w2 with FMT_LUT).  Returns (codes int8
+    [N, K], scales fp16 [N])."""
+    N, K = W.shape
+    _dev(W, torch.float32, (N, K), "W")
+    if codes is None:
+        codes = torch.empty((N, K), dtype=torch.int8, device=W.device)
+    if scales is None:
+        scales = torch.empty(N, dtype=torch.float16, device=W.device)
+    _dev(codes, torch.int8, (N, K), "codes")
+    _dev(scales, torch.float16, (N,), "scales")
+    st = lib().qift_quantize_weights_mirror(W.data_ptr(), N, spec(K, block), float(r), codes.data_ptr(),
+                                            scales.data_ptr(), _stream(stream))
+    _check("qift_quantize_weights_mirror", st)
+    return codes, scales
+
+
+def ratio_scan(x: torch.Tensor, ratios, cands, stream=None):
+    """Squared error of the set {-1, -r, +r, +1} on the fp64 samples x at every scale c * max|x| of the
+    candidate clip ratios, for each ratio r.  Returns (sse fp64 [R, C], nmse fp64 [R], best int32 [R],
+    stats fp64 [2] = (max|x|, sum x^2)), all on x's device."""
+    x = x.reshape(-1)
+    _dev(x, torch.float64, (x.numel(),), "x")
+    r = (ctypes.c_double * len(ratios))(*[float(v) for v in ratios])
+    c = (ctypes.c_double * len(cands))(*[float(v) for v in cands])
+    R, C = len(ratios), len(cands)
+    sse = torch.empty((R, C), dtype=torch.float64, device=x.device)
+    nmse = torch.empty(R, dtype=torch.float64, device=x.device)
+    best = torch.empty(R, dtype=torch.int32, device=x.device)
+    stats = torch.empty(2, dtype=torch.float64, device=x.device)
+    st = lib().qift_ratio_scan(x.data_ptr(), x.numel(), r, R, c, C, sse.data_ptr(), nmse.data_ptr(),
+                               best.data_ptr(), stats.data_ptr(), _stream(stream))
+    _check("qift_ratio_scan", st)
+    return sse, nmse, best, stats
 
 
 class KV4:

@@ -35,7 +35,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 26
+    assert len(names) == 28
     assert sorted(qift.EXPORTS) == names
     for n in names:
         assert hasattr(L, n), n
@@ -89,6 +89,50 @@ def test_quantize_weights_validation(L):
     assert f(A, 8, _spec(flags=1 << 16), mnz, A, A, None) == E_SPEC
     assert f(MIS, 8, _spec(), mnz, A, A, None) == E_ALIGN
     assert f(A, 8, _spec(), mnz, MIS, A, None) == E_ALIGN
+
+
+def test_quantize_weights_mirror_validation(L):
+    f = L.qift_quantize_weights_mirror
+    assert f(None, 8, _spec(), 0.3, A, A, None) == E_NULL
+    assert f(A, 8, _spec(), 0.3, None, A, None) == E_NULL
+    assert f(A, 8, _spec(), 0.3, A, None, None) == E_NULL
+    assert f(A, 0, _spec(), 0.3, A, A, None) == E_SHAPE
+    assert f(A, 8, _spec(K=16448, block=64), 0.3, A, A, None) == E_SHAPE
+    assert f(A, 1 << 18, _spec(K=8192, block=64), 0.3, A, A, None) == E_SHAPE
+    assert f(A, 8, _spec(block=48), 0.3, A, A, None) == E_SPEC
+    assert f(A, 8, _spec(flags=1 << 16), 0.3, A, A, None) == E_SPEC
+    for r in (0.0, 1.0, -0.3, 1.5, float("nan"), float("inf")):
+        assert f(A, 8, _spec(), r, A, A, None) == E_SPEC, r
+    assert f(MIS, 8, _spec(), 0.3, A, A, None) == E_ALIGN
+    assert f(A, 8, _spec(), 0.3, A, MIS, None) == E_ALIGN
+
+
+def test_ratio_scan_validation(L):
+    f = L.qift_ratio_scan
+    dv = lambda *v: (ctypes.c_double * len(v))(*v)
+    r, c = dv(0.25, 0.3), dv(0.2, 0.5, 1.0)
+    assert f(None, 100, r, 2, c, 3, A, A, A, A, None) == E_NULL
+    assert f(A, 100, None, 2, c, 3, A, A, A, A, None) == E_NULL
+    assert f(A, 100, r, 2, None, 3, A, A, A, A, None) == E_NULL
+    for k in range(4):
+        out = [A] * 4
+        out[k] = None
+        assert f(A, 100, r, 2, c, 3, *out, None) == E_NULL
+    assert f(A, 0, r, 2, c, 3, A, A, A, A, None) == E_SHAPE
+    assert f(A, 1 << 40, r, 2, c, 3, A, A, A, A, None) == E_SHAPE
+    assert f(A, 100, r, 0, c, 3, A, A, A, A, None) == E_SHAPE
+    assert f(A, 100, dv(*([0.5] * 1025)), 1025, c, 3, A, A, A, A, None) == E_SHAPE
+    assert f(A, 100, r, 2, c, 0, A, A, A, A, None) == E_SHAPE
+    assert f(A, 100, r, 2, dv(*([0.5] * 257)), 257, A, A, A, A, None) == E_SHAPE
+    for bad in (0.0, 1.0, -0.1, float("nan")):
+        assert f(A, 100, dv(0.3, bad), 2, c, 3, A, A, A, A, None) == E_SPEC, bad
+    for bad in (0.0, -1.0, float("inf"), float("nan")):
+        assert f(A, 100, r, 2, dv(0.5, bad), 2, A, A, A, A, None) == E_SPEC, bad
+    for k in range(5):
+        ptrs = [A] * 5
+        ptrs[k] = MIS
+        x, sse, nmse, best, stats = ptrs
+        assert f(x, 100, r, 2, c, 3, sse, nmse, best, stats, None) == E_ALIGN
 
 
 def test_kv4_validation(L):

@@ -80,3 +80,55 @@ def test_other_side_of_an_exact_threshold_is_accepted(fmt, row, flips):
     far = np.array([int(v) + (2 if int(v) in flips and flips[int(v)] > int(v) else 0) for v in L[0]])
     if fmt == levels.FMT_W4_SYM:
         assert row_valid(fmt, w, d, s[0], far) is not None
+
+
+# ----------------------------------------------------------------------------- mirror family G(r)
+
+from wquant_rule import MIRROR   # noqa: E402
+
+RATIOS = [0.3, 1.0 / 3.0, 0.5]
+
+
+def _oracle_mirror(W, b, r):
+    return quant.quantize_mirror_mse(hadamard.rotate_weights(np.asarray(W, np.float64), b), r)
+
+
+@pytest.mark.parametrize("r", RATIOS)
+def test_mirror_oracle_result_passes(r):
+    W = synth.weights_fp32(98, 0, "q", 16, 512)
+    C, s = _oracle_mirror(W, 256, r)
+    _, _, differ = check_rows(MIRROR, W, 256, C, s, r)
+    assert differ.size == 0
+
+
+@pytest.mark.parametrize("r", RATIOS)
+def test_mirror_planted_code_and_scale_are_rejected(r):
+    W = synth.weights_fp32(98, 1, "q", 8, 256)
+    C, s = _oracle_mirror(W, 256, r)
+    w = hadamard.rotate_weights(W.astype(np.float64), 256)
+    # the element of row 2 farthest from both thresholds (0 and (1 + r) / 2) in units of the scale
+    u = np.abs(w[2] / float(s[2]))
+    k = int(np.argmax(np.minimum(u, np.abs(u - 0.5 * (r + 1.0)))))
+    bad = C.copy()
+    bad[2, k] = C[2, k] + 1 if C[2, k] < 3 else C[2, k] - 1
+    with pytest.raises(AssertionError, match="row 2"):
+        check_rows(MIRROR, W, 256, bad, s, r)
+    # a code two steps away (across zero) where the row is not near zero
+    bad = C.copy()
+    bad[2, k] = (C[2, k] + 2) % 4
+    with pytest.raises(AssertionError, match="row 2"):
+        check_rows(MIRROR, W, 256, bad, s, r)
+    for step in (1, 2):
+        bs = s.copy()
+        bs[4] = np.uint16(int(s[4].view(np.uint16)) + step).view(np.float16)
+        with pytest.raises(AssertionError, match="row 4"):
+            check_rows(MIRROR, W, 256, C, bs, r)
+
+
+def test_mirror_quarter_is_accepted_from_the_pot_result():
+    # at r = 1/4 the PoT levels as codes, with 4 times the PoT scale, are the mirror result
+    W = synth.weights_fp32(98, 2, "q", 12, 256)
+    L, s = _oracle(W, 256, levels.FMT_W2_POT)
+    codes = np.searchsorted(np.array([-4, -1, 1, 4]), L).astype(np.int8)
+    _, _, differ = check_rows(MIRROR, W, 256, codes, (4.0 * s.astype(np.float64)).astype(np.float16), 0.25)
+    assert differ.size == 0
