@@ -34,9 +34,9 @@ namespace qift {
 constexpr int kChainWaves = 12;
 constexpr int kChainThreads = 64 * kChainWaves;
 constexpr int kChainShortK = 4096;   // one rotation tile: 4 activation waves, 8 K-slices
-// LDS tail (kChainTailBytes): s_scale[2][4] f32, red_d[2][4][8] f64, red_i[2][4][8] i32, ctr[4] u32,
-// 64 zero bytes
-static_assert(kChainTailBytes == 32 + 512 + 256 + 16 + 64, "tail layout");
+// LDS tail (kChainTailBytes): s_scale[2][4] f32, red_d[2][4][kChainSlots] f64, red_i[2][4][kChainSlots]
+// i32, ctr[4] u32, 64 zero bytes
+static_assert(kChainTailBytes == 32 + 64 * kChainSlots + 32 * kChainSlots + 16 + 64, "tail layout");
 
 template <int FMT>
 constexpr int chain_tmax() { return FMT == mma::FMT_W4 ? 3 : 7; }   // tiles per chunk, K <= 4096
@@ -256,21 +256,22 @@ __device__ __forceinline__ uint32_t unwritten8(const uint4& a) {
   return bad;
 }
 
-__device__ __forceinline__ void fetch_tiles(uint4 (&raw)[4][2], const ChainDesc& d, const uint16_t* x0, int M, int m,
+template <int NTMAX>
+__device__ __forceinline__ void fetch_tiles(uint4 (&raw)[NTMAX][2], const ChainDesc& d, const uint16_t* x0, int M, int m,
                                             int NT, int t, int par, long long deadline, uint32_t* err) {
   typedef unsigned v4u __attribute__((ext_vector_type(4)));
   const bool from_x0 = d.in_link < 0;
   const uint16_t* src = from_x0 ? x0 + (int64_t)m * d.K : d.tx + ((int64_t)par * M + m) * d.xstride + d.xoff;
   const __amdgpu_buffer_rsrc_t r = dev::make_rsrc(src, (uint32_t)(d.K * 2));   // past K: zeros
-  uint32_t off[4];
+  uint32_t off[NTMAX];
 #pragma unroll
-  for (int tau = 0; tau < 4; ++tau) {
+  for (int tau = 0; tau < NTMAX; ++tau) {
     const int e0 = tau * 4096 + 16 * t;
     off[tau] = tau < NT && e0 < d.K ? (uint32_t)(e0 * 2) : dev::kOutOfRange;
   }
   if (from_x0) {
 #pragma unroll
-    for (int tau = 0; tau < 4; ++tau) {
+    for (int tau = 0; tau < NTMAX; ++tau) {
       raw[tau][0] = dev::bload16(r, off[tau]);
       raw[tau][1] = dev::bload16(r, off[tau] + 16);
     }
@@ -278,7 +279,7 @@ __device__ __forceinline__ void fetch_tiles(uint4 (&raw)[4][2], const ChainDesc&
   }
   for (;;) {
 #pragma unroll
-    for (int tau = 0; tau < 4; ++tau)
+    for (int tau = 0; tau < NTMAX; ++tau)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, off[tau] + 16 * h, 0, 16);
@@ -286,7 +287,7 @@ __device__ __forceinline__ void fetch_tiles(uint4 (&raw)[4][2], const ChainDesc&
       }
     uint32_t bad = 0;
 #pragma unroll
-    for (int tau = 0; tau < 4; ++tau) bad |= unwritten8(raw[tau][0]) | unwritten8(raw[tau][1]);
+    for (int tau = 0; tau < NTMAX; ++tau) bad |= unwritten8(raw[tau][0]) | unwritten8(raw[tau][1]);
     if (__all(bad == 0)) return;
     if (wall_clock64() > deadline) {
       if ((threadIdx.x & 63) == 0) dev::flag_error(err, dev::kErrChainWait);
@@ -324,102 +325,207 @@ __device__ __forceinline__ int codes16(const double (&v)[16], const dev::QuantPa
   return qs;
 }
 
-// Rotation + quantization of one token's NT rotation tiles (NT <= 4) by the four activation waves
-// (the steps of dev::quant_token_group).  Only one tile's values are held in registers: the exact
-// fp64 values of the tiles transformed before the last wait in the LDS stash (element-major, so
-// each lane touches its own bank) until the absmax is known.  The waves synchronize through gsync;
-// their code sums go to red_i[w].  Before it polls for its input the group waits (consumed) until
-// the weight waves are done with the previous link: their stores are then issued ahead of the
-// polling loads (polling that overlapped them was measured to starve them), and the previous link's
-// partial sums, which share the group's LDS region, have been read.
-template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t* x0, int M, int m, int NT, int par,
-                                              long long deadline, uint32_t* err, GS& gsync, double* xch,
-                                              double* stash, int8_t* dst, double* red_d, int* red_i,
-                                              const unsigned* consumed, unsigned consumed_target) {
+// Rotation + quantization of one token of a link with K <= 4096 (one rotation tile) by the four
+// activation waves (the steps of dev::quant_token_group).  The waves synchronize through gsync; their
+// maxima go to red_d[w] and their code sums to red_i[w].  Before it polls for its input the group waits
+// (consumed) until the weight waves are done with the previous link: their stores are then issued
+// ahead of the polling loads (polling that overlapped them was measured to starve them), and the
+// previous link's partial sums, which share the group's LDS region, have been read.
+__device__ __forceinline__ int group_thread() {
   // the thread index as an opaque value: the per-thread LDS addresses derived from it are computed
-  // here, per call, instead of being hoisted out of the link loop (where dozens of them would stay
-  // live across the whole loop and spill)
+  // per call instead of being hoisted out of the link loop (where dozens of them would stay live
+  // across the whole loop and spill)
   int t = threadIdx.x & 255;
   asm volatile("" : "+v"(t));
+  return t;
+}
+
+__device__ __forceinline__ void wait_consumed(const unsigned* consumed, unsigned target, long long deadline,
+                                              uint32_t* err) {
+  for (;;) {
+    const unsigned c = __builtin_amdgcn_readfirstlane(
+        __hip_atomic_load(consumed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+    if (c >= target) break;
+    if (wall_clock64() > deadline) {
+      if ((threadIdx.x & 63) == 0) dev::flag_error(err, dev::kErrGroupWait);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  asm volatile("" ::: "memory");
+}
+
+template <int LC, bool PLANAR, typename GS>
+__device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t* x0, int M, int m, int par,
+                                              long long deadline, uint32_t* err, GS& gsync, double* xch,
+                                              int8_t* dst, double* red_d, int* red_i, const unsigned* consumed,
+                                              unsigned consumed_target) {
+  const int t = group_thread();
   const int lane = t & 63, w = t >> 6;
-  if (consumed) {
-    // the weight waves are done with the previous link: its partial sums (which share this group's
-    // LDS region) are read and its stores are issued, ahead of the polling loads below
-    for (;;) {
-      const unsigned c = __builtin_amdgcn_readfirstlane(
-          __hip_atomic_load(consumed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
-      if (c >= consumed_target) break;
-      if (wall_clock64() > deadline) {
-        if (lane == 0) dev::flag_error(err, dev::kErrGroupWait);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-    asm volatile("" ::: "memory");
-  }
-  uint4 raw[4][2];
-  fetch_tiles(raw, d, x0, M, m, NT, t, par, deadline, err);
+  if (consumed) wait_consumed(consumed, consumed_target, deadline, err);
+  uint4 raw[1][2];
+  fetch_tiles<1>(raw, d, x0, M, m, 1, t, par, deadline, err);
   double v[16];
+  dev::unpack16<false>(v, raw[0]);
+  const int wend = dev::fwht_tile_s<256, 16, false>(v, xch, t, LC, gsync);
   double amax = 0.0;
-  int wend = 0;
 #pragma unroll
-  for (int tau = 0; tau < 4; ++tau) {
-    if (tau < NT) {
-      if (tau > 0) {
-        double* st = stash + (tau - 1) * 4096;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) st[e * 256 + t] = v[e];
-        if (LC > 6) gsync();   // one exchange buffer: the previous tile's reads are done
-      }
-      dev::unpack16<false>(v, raw[tau]);
-      wend = dev::fwht_tile_s<256, 16, false>(v, xch, t, LC, gsync);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
-    }
-  }
+  for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
   amax = dev::wave_max(amax);
   if (lane == 0) red_d[w] = amax;
   gsync();
   const double A = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
   const dev::QuantParams p = dev::make_qparams(A, d.num, d.den);
-  int qs = codes16<PLANAR>(v, p, wend, NT - 1, d.K, t, dst);
-#pragma unroll
-  for (int tau = 0; tau < 3; ++tau) {
-    if (tau < NT - 1) {
-      const double* st = stash + tau * 4096;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) v[e] = st[e * 256 + t];
-      qs += codes16<PLANAR>(v, p, wend, tau, d.K, t, dst);
-    }
-  }
+  int qs = codes16<PLANAR>(v, p, wend, 0, d.K, t, dst);
   qs = dev::wave_sum(qs);
   if (lane == 0) red_i[w] = qs;
   return A;
 }
 
-// The activation phase of one link: every token; the scale of token m goes to s_scale[m].
+// Links with K > 4096 (NT = 2..4 rotation tiles): the tiles are rotated by three groups of four waves
+// at once, the activation group (tiles 0 and 3) and the two halves of the weight waves (tiles 1 and 2),
+// whose weight loads for the link stay in flight meanwhile.  Per token:
+//   * the activation group polls for all tiles, puts tiles 1 and 2 (fp16 bits) into the other
+//     groups' exchange buffers, and the workgroup meets at a barrier;
+//   * every group rotates its tile(s) in its own exchange buffer (its own wave barrier) and writes the
+//     absmax of each wave to red_d[4 g + w]; a second workgroup barrier;
+//   * every group takes the token's max over the twelve slots and quantizes its tile(s) into the
+//     codes; code sums go to red_i[4 g + w].
+// The activation group keeps tile 0 in registers while it rotates tile 3.
+template <int LC, bool PLANAR, typename GS>
+__device__ __forceinline__ double long_group_a(const ChainDesc& d, const uint16_t* x0, int M, int m, int NT,
+                                               int par, long long deadline, uint32_t* err, GS& gsync,
+                                               double* xch, double* xch_b, double* xch_c, int8_t* dst,
+                                               double* red_d, int* red_i, const unsigned* consumed,
+                                               unsigned consumed_target) {
+  const int t = group_thread();
+  const int lane = t & 63, w = t >> 6;
+  if (consumed) wait_consumed(consumed, consumed_target, deadline, err);
+  uint4 raw[4][2];
+  fetch_tiles<4>(raw, d, x0, M, m, NT, t, par, deadline, err);
+  // the other groups' input: 32 bytes per thread at the start of their exchange buffers (their
+  // exchanges of the previous token ended before the previous token's second barrier)
+  uint4* sb = reinterpret_cast<uint4*>(xch_b);
+  sb[2 * t] = raw[1][0];
+  sb[2 * t + 1] = raw[1][1];
+  if (NT > 2) {
+    uint4* sc = reinterpret_cast<uint4*>(xch_c);
+    sc[2 * t] = raw[2][0];
+    sc[2 * t + 1] = raw[2][1];
+  }
+  dev::lds_barrier();   // the other groups' tiles are in LDS
+  double v[16];
+  dev::unpack16<false>(v, raw[0]);
+  const int wend = dev::fwht_tile_s<256, 16, false>(v, xch, t, LC, gsync);
+  double amax = 0.0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
+  double v3[16];
+  if (NT > 3) {
+    if (LC > 6) gsync();   // one exchange buffer: tile 0's exchange reads are done
+    dev::unpack16<false>(v3, raw[3]);
+    dev::fwht_tile_s<256, 16, false>(v3, xch, t, LC, gsync);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v3[e]));
+  }
+  amax = dev::wave_max(amax);
+  if (lane == 0) red_d[w] = amax;
+  dev::lds_barrier();   // every group's maxima are in LDS
+  double A = red_d[0];
+#pragma unroll
+  for (int k = 1; k < 12; ++k) A = fmax(A, red_d[k]);
+  const dev::QuantParams p = dev::make_qparams(A, d.num, d.den);
+  int qs = codes16<PLANAR>(v, p, wend, 0, d.K, t, dst);
+  if (NT > 3) qs += codes16<PLANAR>(v3, p, wend, 3, d.K, t, dst);
+  qs = dev::wave_sum(qs);
+  if (lane == 0) red_i[w] = qs;
+  return A;
+}
+
+// The weight waves' part of a long link (group gi = 1: tile 1, gi = 2: tile 2 if NT > 2), between the
+// same two workgroup barriers as the activation group's.
+template <int LC, bool PLANAR, typename GS>
+__device__ __forceinline__ void long_group_w(const ChainDesc& d, int NT, int gi, GS& gsync, double* xch_g,
+                                             int8_t* dst, double* red_d, int* red_i) {
+  const int t = group_thread();
+  const int lane = t & 63, w = t >> 6;
+  const bool has = gi < NT;
+  dev::lds_barrier();   // the group's tile is in LDS
+  double v[16];
+  double amax = 0.0;
+  int wend = 0;
+  if (has) {
+    const uint4* sg = reinterpret_cast<const uint4*>(xch_g);
+    uint4 r[2] = {sg[2 * t], sg[2 * t + 1]};
+    gsync();   // every wave of the group has its input before the exchanges overwrite it
+    dev::unpack16<false>(v, r);
+    wend = dev::fwht_tile_s<256, 16, false>(v, xch_g, t, LC, gsync);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
+  }
+  amax = dev::wave_max(amax);
+  if (lane == 0) red_d[4 * gi + w] = amax;
+  dev::lds_barrier();   // every group's maxima are in LDS
+  int qs = 0;
+  if (has) {
+    double A = red_d[0];
+#pragma unroll
+    for (int k = 1; k < 12; ++k) A = fmax(A, red_d[k]);
+    const dev::QuantParams p = dev::make_qparams(A, d.num, d.den);
+    qs = codes16<PLANAR>(v, p, wend, gi, d.K, t, dst);
+    qs = dev::wave_sum(qs);
+  }
+  if (lane == 0) red_i[4 * gi + w] = qs;
+}
+
+// The activation group's part of one link: every token; the scale of token m goes to s_scale[m].
 template <bool PLANAR, typename GS>
 __device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0, int M, int par,
-                                         long long deadline, uint32_t* err, GS& gsync, double* xch, double* stash,
-                                         int8_t* act_l, int Kpad, double* red_d, int* red_i, float* s_scale,
-                                         const unsigned* consumed, unsigned consumed_target) {
+                                         long long deadline, uint32_t* err, GS& gsync, double* xch, double* xch_b,
+                                         double* xch_c, int8_t* act_l, int Kpad, double* red_d, int* red_i,
+                                         float* s_scale, const unsigned* consumed, unsigned consumed_target) {
   const int NT = (d.K + 4095) / 4096;
   for (int m = 0; m < M; ++m) {
     double A;
     const unsigned* cw = m == 0 ? consumed : nullptr;
+    double* rd = red_d + kChainSlots * m;
+    int* ri = red_i + kChainSlots * m;
+    int8_t* dst = act_l + m * Kpad;
     // the block sizes compiled in (chain_block_ok): every butterfly stage is straight-line code
-    switch (d.L) {
-      case 12: A = quant_group<12, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
-                                           red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
-      case 11: A = quant_group<11, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
-                                           red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
-      case 8: A = quant_group<8, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
-                                         red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
-      default: A = quant_group<6, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, stash, act_l + m * Kpad,
-                                          red_d + 8 * m, red_i + 8 * m, cw, consumed_target); break;
+    if (NT > 1) {
+      switch (d.L) {
+        case 12: A = long_group_a<12, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
+        case 11: A = long_group_a<11, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
+        case 8: A = long_group_a<8, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
+        default: A = long_group_a<6, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
+      }
+    } else {
+      switch (d.L) {
+        case 12: A = quant_group<12, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 11: A = quant_group<11, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 8: A = quant_group<8, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        default: A = quant_group<6, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+      }
     }
     if (threadIdx.x == 0) s_scale[m] = (float)((A * (double)d.num) / d.denom);
+  }
+}
+
+// The weight waves' part of a long link: every token.
+template <bool PLANAR, typename GS>
+__device__ __forceinline__ void act_link_w(const ChainDesc& d, int M, int gi, GS& gsync, double* xch_g,
+                                           int8_t* act_l, int Kpad, double* red_d, int* red_i) {
+  const int NT = (d.K + 4095) / 4096;
+  for (int m = 0; m < M; ++m) {
+    double* rd = red_d + kChainSlots * m;
+    int* ri = red_i + kChainSlots * m;
+    int8_t* dst = act_l + m * Kpad;
+    switch (d.L) {
+      case 12: long_group_w<12, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
+      case 11: long_group_w<11, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
+      case 8: long_group_w<8, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
+      default: long_group_w<6, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
+    }
   }
 }
 
@@ -483,11 +589,14 @@ __device__ __forceinline__ void store4_chain(const v4i& D, const ChainDesc& d, i
 // link's input as soon as this link's codes are in; after the MFMAs, weight wave 4 + j adds the
 // K-slices of tile j of the chunk, applies the epilogue and stores it, and only then issues the next
 // link's weight loads, so the stores are not queued behind them.
-// LDS: the codes [M][Kpad]; the activation group's region (its exchange buffer and the stash of up
-// to three rotation tiles), aliased by the K-slice partial sums: the group writes it for the next
-// link only once the 8 weight waves have counted themselves done with them; then the tail: s_scale,
-// red_d and red_i double-buffered by link parity (the next link's activation phase runs while this
-// link's are still read), the wave-barrier counter, the weight waves' count and 64 zero bytes.
+// Links with K > 4096 also use the weight waves for their rotation (long_group_a / long_group_w): two
+// more workgroup barriers per token, taken by both loops.
+// LDS: the codes [M][Kpad]; the rotation region (the activation group's exchange buffer, and for
+// chains with K > 4096 those of the two weight-wave groups), aliased by the K-slice partial sums: the
+// activation group writes it for the next link only once the 8 weight waves have counted themselves
+// done with them; then the tail: s_scale, red_d and red_i double-buffered by link parity (the next
+// link's activation phase runs while this link's are still read), the wave-barrier counters (the
+// activation group's and the two weight-wave groups'), the weight waves' count and 64 zero bytes.
 // Exchange copies: the call's run number r (read at the start; the last workgroup to finish advances
 // it) selects copy r mod 2 of every exchange buffer.
 template <int FMT>
@@ -502,20 +611,21 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = lane >> 4;
   const int G = gridDim.x, wg = blockIdx.x;
 
   const int act_bytes = (M * Kpad + 15) & ~15;
   int8_t* act_l = reinterpret_cast<int8_t*>(smem);
   double* xch = reinterpret_cast<double*>(smem + act_bytes);
-  double* stash = xch + kXchBytes / 8;
-  v4i* red = reinterpret_cast<v4i*>(xch);   // the K-slice partial sums reuse the activation region
+  double* xch_b = xch + kXchBytes / 8;   // the weight-wave groups' exchange buffers (chains with K > 4096)
+  double* xch_c = xch_b + kXchBytes / 8;
+  v4i* red = reinterpret_cast<v4i*>(xch);   // the K-slice partial sums reuse the rotation region
   unsigned char* tl = smem + act_bytes + region0;
-  float* s_scale = reinterpret_cast<float*>(tl);                 // [2][4]
-  double* red_d = reinterpret_cast<double*>(tl + 32);            // [2][4][8]
-  int* red_i = reinterpret_cast<int*>(tl + 32 + 512);            // [2][4][8]
-  unsigned* ctr = reinterpret_cast<unsigned*>(tl + 32 + 512 + 256);   // [0] wave barrier, [3] weight waves done
-  int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 32 + 512 + 256 + 16);
+  constexpr int RS = 4 * kChainSlots;   // red_d / red_i entries per link parity
+  float* s_scale = reinterpret_cast<float*>(tl);                      // [2][4]
+  double* red_d = reinterpret_cast<double*>(tl + 32);                 // [2][4][kChainSlots]
+  int* red_i = reinterpret_cast<int*>(tl + 32 + 16 * RS);             // [2][4][kChainSlots]
+  unsigned* ctr = reinterpret_cast<unsigned*>(tl + 32 + 24 * RS);     // [0..2] group barriers, [3] weight waves done
+  int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 32 + 24 * RS + 16);
   if (tid < 4) {
     ctr[tid] = 0u;
     reinterpret_cast<uint4*>(zero64)[tid] = make_uint4(0u, 0u, 0u, 0u);
@@ -535,8 +645,8 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
       if (gm.T > 0)
-        act_link<PLANAR>(d, x0, M, rpar, deadline, err, gs, xch, stash, act_l, Kpad,
-                         red_d + 32 * par, red_i + 32 * par, s_scale + 4 * par, consumed, 8u * (unsigned)i);
+        act_link<PLANAR>(d, x0, M, rpar, deadline, err, gs, xch, xch_b, xch_c, act_l, Kpad, red_d + RS * par,
+                         red_i + RS * par, s_scale + 4 * par, consumed, 8u * (unsigned)i);
       dev::lds_barrier();   // codes, scales and code sums are in LDS
       for (int c = 0; c < gm.nchunks; ++c) {
         dev::lds_barrier();                           // partial sums are in LDS
@@ -546,6 +656,8 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   } else {
     // ================= waves 4-11: weight slices, then the reduction, epilogue and stores
     const int slice = wave - 4;
+    const int gi = slice < 4 ? 1 : 2;   // rotation group of long links: tile 1 or tile 2
+    dev::GroupSync<4> gsw{ctr + gi, 0u, wait_limit, err};
     uint4 wr[16];
     uint2 swq = make_uint2(0u, 0u);
     auto prefetch = [&](const ChainDesc& dn) {   // the first chunk of a link, for this wave's slice
@@ -554,8 +666,11 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
         const int T0 = gn.T < gn.tmax ? gn.T : gn.tmax;
         if (gn.lng) load_chunk_rt<FMT, true>(wr, dn, gn.t0, T0, slice);
         else load_chunk_rt<FMT, false>(wr, dn, gn.t0, T0, slice);
-        // fp16 scales of the tile this wave stores (tile `slice` of the chunk)
-        const int n = (gn.t0 + slice) * 16 + 4 * g;
+        // fp16 scales of the tile this wave stores (tile `slice` of the chunk); the lane index opaque, so
+        // that its row offset is made here rather than kept (or spilled) across the link loop
+        int ln = threadIdx.x & 63;
+        asm volatile("" : "+v"(ln));
+        const int n = (gn.t0 + slice) * 16 + 4 * (ln >> 4);
         const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(dn.sw, (uint32_t)(dn.N * 2));
         swq = dev::bload8(srs, slice < T0 && n < dn.N ? (uint32_t)(2 * n) : dev::kOutOfRange);
       }
@@ -565,6 +680,8 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const ChainDesc& d = links[i];
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
+      if (gm.lng && gm.T > 0)
+        act_link_w<PLANAR>(d, M, gi, gsw, gi == 1 ? xch_b : xch_c, act_l, Kpad, red_d + RS * par, red_i + RS * par);
       dev::lds_barrier();   // codes are in LDS; this wave's weight loads stay in flight
       const __amdgpu_buffer_rsrc_t tyr = dev::make_rsrc(d.ty, (uint32_t)(2 * M * d.ystride * 2));
       for (int c = 0; c < gm.nchunks; ++c) {
@@ -593,8 +710,13 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
 #pragma unroll
           for (int q = 1; q < 8; ++q) D += red[(slice * 8 + q) * 64 + ln];
           if (m < M && n0 < d.N) {
-            const int* ri = red_i + 32 * par + 8 * m;
-            store4_chain<FMT>(D, d, M, m, n0, s_scale[4 * par + m], ri[0] + ri[1] + ri[2] + ri[3], swq, tyr, rpar);
+            const int* ri = red_i + RS * par + kChainSlots * m;
+            int sq = ri[0] + ri[1] + ri[2] + ri[3];
+            if (gm.lng) {
+#pragma unroll
+              for (int k = 4; k < 12; ++k) sq += ri[k];
+            }
+            store4_chain<FMT>(D, d, M, m, n0, s_scale[4 * par + m], sq, swq, tyr, rpar);
           }
         }
         if (c + 1 < gm.nchunks) dev::lds_barrier();   // the partial sums have been read

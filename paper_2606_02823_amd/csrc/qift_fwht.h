@@ -87,7 +87,11 @@ __device__ __forceinline__ double dpp_f64(double x) {
 template <int B, int E>
 __device__ __forceinline__ void lane_stage(double (&v)[E]) {
   constexpr int CTRL = B == 0 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] / [2,3,0,1]
-  const double sgn = ((threadIdx.x >> B) & 1) ? -1.0 : 1.0;
+  // the lane index as an opaque value: the sign is made here, not hoisted out of a caller's loop
+  // (where it would stay live, or spill, across everything else the loop does)
+  int ln = threadIdx.x;
+  asm volatile("" : "+v"(ln));
+  const double sgn = ((ln >> B) & 1) ? -1.0 : 1.0;
 #pragma unroll
   for (int e = 0; e < E; ++e) v[e] = fma(v[e], sgn, dpp_f64<CTRL>(v[e]));
 }

@@ -124,14 +124,14 @@ constexpr unsigned kUnwritten = 0xFFFFu;
 inline bool chain_block_ok(int block) { return block == 64 || block == 256 || block == 2048 || block == 4096; }
 constexpr int kChainMaxK = 16384;
 constexpr int kChainMaxLinks = 4096;
-constexpr int kChainTailBytes = 880;
+constexpr int kChainSlots = 16;                    // per-token reduction slots (12 waves rotate long links)
+constexpr int kChainTailBytes = 32 + 96 * kChainSlots + 16 + 64;
 constexpr int kChainXchBytes = (4096 + 512) * 8;   // one rotation exchange buffer (a 4096-tile, padded)
-constexpr int kChainStashBytes = 4096 * 8;         // one rotation tile of fp64 values
-// LDS region of the activation group: its exchange buffer and a stash of NT - 1 rotation tiles (NT
-// the most tiles of a link, K <= 4096 NT each), aliased by the K-slice partial sums (8 slices x 7,
-// W4 3, tiles).
+// LDS rotation region: the activation group's exchange buffer, and for a chain with a link of more
+// than one rotation tile (K > 4096) the two weight-wave groups' as well; aliased by the K-slice
+// partial sums (8 slices x 7, W4 3, tiles).
 inline int chain_region0(int max_tiles, bool w4) {
-  const int own = kChainXchBytes + (max_tiles - 1) * kChainStashBytes, part = 8 * (w4 ? 3 : 7) * 1024;
+  const int own = (max_tiles > 1 ? 3 : 1) * kChainXchBytes, part = 8 * (w4 ? 3 : 7) * 1024;
   return own > part ? own : part;
 }
 inline size_t chain_lds_bytes(int64_t M, int64_t Kmax, int region0) {

@@ -157,12 +157,30 @@ def test_chain_multi_token(Q, fmt, M):
     assert Q.device_error() == 0
 
 
+@pytest.mark.parametrize("fmt,M", [(levels.FMT_W2_MNZ, 2), (levels.FMT_W2_POT, 3), (levels.FMT_W4_SYM, 2)])
+def test_chain_multi_token_long_links(Q, fmt, M):
+    """Several tokens through links of 3 and 4 rotation tiles (K = 11008, 14336), whose tiles the
+    activation group and the two weight-wave groups rotate at once, one token after another."""
+    specs = [Spec(fmt, 4096, 4096, 4096, -1, 0, 21),
+             Spec(fmt, 11008, 4096, 4096, 0, 0, 22),
+             Spec(fmt, 4096, 11008, 64, 1, 0, 23),
+             Spec(fmt, 14336, 4096, 4096, 2, 0, 24),
+             Spec(fmt, 2064, 14336, 2048, 3, 0, 25),
+             Spec(fmt, 9000, 2048, 256, 4, 16, 26),
+             Spec(fmt, 784, 12288, 4096, 3, 0, 27)]
+    chain, _ = build(Q, specs, M)
+    for r in range(2):
+        x = synth.activations_fp16(87, 10 * fmt + r, 0, M, 4096, 41, 30.0)
+        check_run(Q, chain, specs, x)
+    assert Q.device_error() == 0
+
+
 def test_chain_rejects_what_does_not_fit(Q):
-    # two tokens next to a K = 14336 link exceed one workgroup's LDS; a block the kernel was not
+    # four tokens next to a K = 14336 link exceed one workgroup's LDS; a block the kernel was not
     # compiled for is refused
     specs = llama31_layers(levels.FMT_W2_MNZ, 1, seed0=50)
     with pytest.raises(Q.QiftError, match="QIFT_ERR_SHAPE"):
-        build(Q, specs, 2)
+        build(Q, specs, 4)
     specs = [Spec(levels.FMT_W2_MNZ, 512, 4096, 1024, -1, 0, 51)]
     with pytest.raises(Q.QiftError, match="QIFT_ERR_SPEC"):
         build(Q, specs, 1)
