@@ -35,8 +35,8 @@ constexpr int kChainWaves = 12;
 constexpr int kChainThreads = 64 * kChainWaves;
 constexpr int kChainShortK = 4096;   // one rotation tile: 4 activation waves, 8 K-slices
 // LDS tail (kChainTailBytes): s_scale[2][4] f32, red_d[2][4][kChainSlots] f64, red_i[2][4][kChainSlots]
-// i32, ctr[4] u32, 64 zero bytes
-static_assert(kChainTailBytes == 32 + 64 * kChainSlots + 32 * kChainSlots + 16 + 64, "tail layout");
+// i32, ctr[8] u32, 64 zero bytes, the weight waves' fp16 scale slots [8][64] u32
+static_assert(kChainTailBytes == 32 + 64 * kChainSlots + 32 * kChainSlots + 32 + 64 + 8 * 256, "tail layout");
 
 template <int FMT>
 constexpr int chain_tmax() { return FMT == mma::FMT_W4 ? 3 : 7; }   // tiles per chunk, K <= 4096
@@ -82,7 +82,7 @@ __device__ __forceinline__ void load_chunk(uint4 (&wr)[16], const ChainDesc& d, 
   // opaque lane index: the row offsets are computed per call rather than hoisted out of the link loop
   // (kept live across it they spill, and each spill reload's wait on the vector memory counter would
   // also wait for the loads just issued, one pair at a time)
-  int lane = threadIdx.x & 63;
+  int lane = dev::lane_id();
   asm volatile("" : "+v"(lane));
   const int r16 = lane & 15, g = lane >> 4;
   const int K = d.K, N = d.N;
@@ -139,7 +139,10 @@ __device__ __forceinline__ void mfma_chunk(uint4 (&wr)[16], const ChainDesc& d, 
   // accumulators per tile: MNZ one per bit plane up to 3 tiles, from 4 tiles on two (decode_plane2)
   constexpr bool TWO = PLANAR && T >= 4;
   constexpr int NA = PLANAR ? (TWO ? 2 : 4) : T >= 3 ? 1 : 4 / T;
-  const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+  // opaque lane index (as in load_chunk): the operand addresses are made per call
+  int lane = dev::lane_id();
+  asm volatile("" : "+v"(lane));
+  const int r16 = lane & 15, g = lane >> 4;
   const int K = d.K;
   const int NC = (K + NS * 256 - 1) / (NS * 256);
   const int kq0 = slice * NC * 256;
@@ -290,7 +293,7 @@ __device__ __forceinline__ void fetch_tiles(uint4 (&raw)[NTMAX][2], const ChainD
     for (int tau = 0; tau < NTMAX; ++tau) bad |= unwritten8(raw[tau][0]) | unwritten8(raw[tau][1]);
     if (__all(bad == 0)) return;
     if (wall_clock64() > deadline) {
-      if ((threadIdx.x & 63) == 0) dev::flag_error(err, dev::kErrChainWait);
+      if (dev::lane_id() == 0) dev::flag_error(err, dev::kErrChainWait);
       return;
     }
     __builtin_amdgcn_s_sleep(2);
@@ -331,11 +334,11 @@ __device__ __forceinline__ int codes16(const double (&v)[16], const dev::QuantPa
 // (consumed) until the weight waves are done with the previous link: their stores are then issued
 // ahead of the polling loads (polling that overlapped them was measured to starve them), and the
 // previous link's partial sums, which share the group's LDS region, have been read.
-__device__ __forceinline__ int group_thread() {
-  // the thread index as an opaque value: the per-thread LDS addresses derived from it are computed
-  // per call instead of being hoisted out of the link loop (where dozens of them would stay live
-  // across the whole loop and spill)
-  int t = threadIdx.x & 255;
+// The thread's index within its group of four waves (gw: the wave's index in the group, uniform) as an
+// opaque value: the per-thread LDS addresses derived from it are computed per call instead of being
+// hoisted out of the link loop (where dozens of them would stay live across the whole loop and spill).
+__device__ __forceinline__ int group_thread(int gw) {
+  int t = 64 * gw + dev::lane_id();
   asm volatile("" : "+v"(t));
   return t;
 }
@@ -347,7 +350,7 @@ __device__ __forceinline__ void wait_consumed(const unsigned* consumed, unsigned
         __hip_atomic_load(consumed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
     if (c >= target) break;
     if (wall_clock64() > deadline) {
-      if ((threadIdx.x & 63) == 0) dev::flag_error(err, dev::kErrGroupWait);
+      if (dev::lane_id() == 0) dev::flag_error(err, dev::kErrGroupWait);
       break;
     }
     __builtin_amdgcn_s_sleep(1);
@@ -356,11 +359,11 @@ __device__ __forceinline__ void wait_consumed(const unsigned* consumed, unsigned
 }
 
 template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t* x0, int M, int m, int par,
+__device__ __forceinline__ double quant_group(int gw, const ChainDesc& d, const uint16_t* x0, int M, int m, int par,
                                               long long deadline, uint32_t* err, GS& gsync, double* xch,
                                               int8_t* dst, double* red_d, int* red_i, const unsigned* consumed,
                                               unsigned consumed_target) {
-  const int t = group_thread();
+  const int t = group_thread(gw);
   const int lane = t & 63, w = t >> 6;
   if (consumed) wait_consumed(consumed, consumed_target, deadline, err);
   uint4 raw[1][2];
@@ -383,22 +386,24 @@ __device__ __forceinline__ double quant_group(const ChainDesc& d, const uint16_t
 }
 
 // Links with K > 4096 (NT = 2..4 rotation tiles): the tiles are rotated by three groups of four waves
-// at once, the activation group (tiles 0 and 3) and the two halves of the weight waves (tiles 1 and 2),
-// whose weight loads for the link stay in flight meanwhile.  Per token:
-//   * the activation group polls for all tiles, puts tiles 1 and 2 (fp16 bits) into the other
-//     groups' exchange buffers, and the workgroup meets at a barrier;
-//   * every group rotates its tile(s) in its own exchange buffer (its own wave barrier) and writes the
-//     absmax of each wave to red_d[4 g + w]; a second workgroup barrier;
+// at once, the activation group (tiles 0 and 3, tile 0 kept in registers while it rotates tile 3) and
+// the two halves of the weight waves (gi = 1: tile 1, gi = 2: tile 2 if NT > 2), whose weight loads for
+// the link are in flight meanwhile.  Per token:
+//   * the activation group polls for all tiles, puts tiles 1 and 2 (fp16 bits) into the exchange
+//     buffers of groups 1 and 2 and counts them staged in LDS; the weight waves wait for that count
+//     (a wave issuing weight loads stalls at the issue while its CU's memory queue is full: the
+//     activation group does not wait for them);
+//   * every group rotates its tile(s) in an exchange buffer of its own (its own wave barrier) and writes
+//     the absmax of each wave to red_d[4 g + w]; a workgroup barrier;
 //   * every group takes the token's max over the twelve slots and quantizes its tile(s) into the
 //     codes; code sums go to red_i[4 g + w].
-// The activation group keeps tile 0 in registers while it rotates tile 3.
 template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ double long_group_a(const ChainDesc& d, const uint16_t* x0, int M, int m, int NT,
+__device__ __forceinline__ double long_group_a(int gw, const ChainDesc& d, const uint16_t* x0, int M, int m, int NT,
                                                int par, long long deadline, uint32_t* err, GS& gsync,
                                                double* xch, double* xch_b, double* xch_c, int8_t* dst,
                                                double* red_d, int* red_i, const unsigned* consumed,
-                                               unsigned consumed_target) {
-  const int t = group_thread();
+                                               unsigned consumed_target, unsigned* staged) {
+  const int t = group_thread(gw);
   const int lane = t & 63, w = t >> 6;
   if (consumed) wait_consumed(consumed, consumed_target, deadline, err);
   uint4 raw[4][2];
@@ -413,7 +418,10 @@ __device__ __forceinline__ double long_group_a(const ChainDesc& d, const uint16_
     sc[2 * t] = raw[2][0];
     sc[2 * t + 1] = raw[2][1];
   }
-  dev::lds_barrier();   // the other groups' tiles are in LDS
+  // the other groups' tiles are in LDS: each wave counts itself (no workgroup barrier, so a weight
+  // wave still issuing its loads for this link does not hold the group up)
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  if (lane == 0) __hip_atomic_fetch_add(staged, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   double v[16];
   dev::unpack16<false>(v, raw[0]);
   const int wend = dev::fwht_tile_s<256, 16, false>(v, xch, t, LC, gsync);
@@ -442,15 +450,17 @@ __device__ __forceinline__ double long_group_a(const ChainDesc& d, const uint16_
   return A;
 }
 
-// The weight waves' part of a long link (group gi = 1: tile 1, gi = 2: tile 2 if NT > 2), between the
-// same two workgroup barriers as the activation group's.
+// The weight waves' part of a long link (group gi = 1: tile 1, gi = 2: tile 2 if NT > 2): they wait
+// until the four activation waves have counted their staging writes (staged reaches stage_target),
+// then meet the activation group at the workgroup barrier after the maxima.
 template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ void long_group_w(const ChainDesc& d, int NT, int gi, GS& gsync, double* xch_g,
-                                             int8_t* dst, double* red_d, int* red_i) {
-  const int t = group_thread();
+__device__ __forceinline__ void long_group_w(int gw, const ChainDesc& d, int NT, int gi, GS& gsync, double* xch_g,
+                                             int8_t* dst, double* red_d, int* red_i, const unsigned* staged,
+                                             unsigned stage_target, long long deadline, uint32_t* err) {
+  const int t = group_thread(gw);
   const int lane = t & 63, w = t >> 6;
   const bool has = gi < NT;
-  dev::lds_barrier();   // the group's tile is in LDS
+  wait_consumed(staged, stage_target, deadline, err);   // the group's tile is in LDS
   double v[16];
   double amax = 0.0;
   int wend = 0;
@@ -478,12 +488,14 @@ __device__ __forceinline__ void long_group_w(const ChainDesc& d, int NT, int gi,
   if (lane == 0) red_i[4 * gi + w] = qs;
 }
 
+
 // The activation group's part of one link: every token; the scale of token m goes to s_scale[m].
 template <bool PLANAR, typename GS>
-__device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0, int M, int par,
+__device__ __forceinline__ void act_link(int gw, const ChainDesc& d, const uint16_t* x0, int M, int par,
                                          long long deadline, uint32_t* err, GS& gsync, double* xch, double* xch_b,
                                          double* xch_c, int8_t* act_l, int Kpad, double* red_d, int* red_i,
-                                         float* s_scale, const unsigned* consumed, unsigned consumed_target) {
+                                         float* s_scale, const unsigned* consumed, unsigned consumed_target,
+                                         unsigned* staged) {
   const int NT = (d.K + 4095) / 4096;
   for (int m = 0; m < M; ++m) {
     double A;
@@ -494,37 +506,41 @@ __device__ __forceinline__ void act_link(const ChainDesc& d, const uint16_t* x0,
     // the block sizes compiled in (chain_block_ok): every butterfly stage is straight-line code
     if (NT > 1) {
       switch (d.L) {
-        case 12: A = long_group_a<12, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
-        case 11: A = long_group_a<11, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
-        case 8: A = long_group_a<8, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
-        default: A = long_group_a<6, PLANAR>(d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target); break;
+        case 12: A = long_group_a<12, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
+        case 11: A = long_group_a<11, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
+        case 8: A = long_group_a<8, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
+        default: A = long_group_a<6, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
       }
     } else {
       switch (d.L) {
-        case 12: A = quant_group<12, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
-        case 11: A = quant_group<11, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
-        case 8: A = quant_group<8, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
-        default: A = quant_group<6, PLANAR>(d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 12: A = quant_group<12, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 11: A = quant_group<11, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 8: A = quant_group<8, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        default: A = quant_group<6, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
       }
     }
-    if (threadIdx.x == 0) s_scale[m] = (float)((A * (double)d.num) / d.denom);
+    if (gw == 0 && dev::lane_id() == 0) s_scale[m] = (float)((A * (double)d.num) / d.denom);
   }
 }
 
 // The weight waves' part of a long link: every token.
+// stage_count: the tokens of long links staged so far in this call (the same count in every wave).
 template <bool PLANAR, typename GS>
-__device__ __forceinline__ void act_link_w(const ChainDesc& d, int M, int gi, GS& gsync, double* xch_g,
-                                           int8_t* act_l, int Kpad, double* red_d, int* red_i) {
+__device__ __forceinline__ void act_link_w(int gw, const ChainDesc& d, int M, int gi, GS& gsync, double* xch_g,
+                                           int8_t* act_l, int Kpad, double* red_d, int* red_i,
+                                           const unsigned* staged, unsigned& stage_count, long long deadline,
+                                           uint32_t* err) {
   const int NT = (d.K + 4095) / 4096;
   for (int m = 0; m < M; ++m) {
     double* rd = red_d + kChainSlots * m;
     int* ri = red_i + kChainSlots * m;
     int8_t* dst = act_l + m * Kpad;
+    const unsigned tg = 4u * ++stage_count;
     switch (d.L) {
-      case 12: long_group_w<12, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
-      case 11: long_group_w<11, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
-      case 8: long_group_w<8, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
-      default: long_group_w<6, PLANAR>(d, NT, gi, gsync, xch_g, dst, rd, ri); break;
+      case 12: long_group_w<12, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
+      case 11: long_group_w<11, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
+      case 8: long_group_w<8, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
+      default: long_group_w<6, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
     }
   }
 }
@@ -589,8 +605,8 @@ __device__ __forceinline__ void store4_chain(const v4i& D, const ChainDesc& d, i
 // link's input as soon as this link's codes are in; after the MFMAs, weight wave 4 + j adds the
 // K-slices of tile j of the chunk, applies the epilogue and stores it, and only then issues the next
 // link's weight loads, so the stores are not queued behind them.
-// Links with K > 4096 also use the weight waves for their rotation (long_group_a / long_group_w): two
-// more workgroup barriers per token, taken by both loops.
+// Links with K > 4096 also use the weight waves for their rotation (long_group_a / long_group_w): one
+// more workgroup barrier per token, taken by both loops, and an LDS count of the staged tiles.
 // LDS: the codes [M][Kpad]; the rotation region (the activation group's exchange buffer, and for
 // chains with K > 4096 those of the two weight-wave groups), aliased by the K-slice partial sums: the
 // activation group writes it for the next link only once the 8 weight waves have counted themselves
@@ -609,7 +625,8 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   constexpr bool PLANAR = FMT == FMT_MNZ;
   constexpr int TMAX = chain_tmax<FMT>();
   extern __shared__ __align__(16) unsigned char smem[];
-  const int tid = threadIdx.x, lane = tid & 63;
+  // the work-item id is read here only (the loops below use dev::lane_id() and the uniform wave index)
+  const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = gridDim.x, wg = blockIdx.x;
 
@@ -624,12 +641,12 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   float* s_scale = reinterpret_cast<float*>(tl);                      // [2][4]
   double* red_d = reinterpret_cast<double*>(tl + 32);                 // [2][4][kChainSlots]
   int* red_i = reinterpret_cast<int*>(tl + 32 + 16 * RS);             // [2][4][kChainSlots]
-  unsigned* ctr = reinterpret_cast<unsigned*>(tl + 32 + 24 * RS);     // [0..2] group barriers, [3] weight waves done
-  int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 32 + 24 * RS + 16);
-  if (tid < 4) {
-    ctr[tid] = 0u;
-    reinterpret_cast<uint4*>(zero64)[tid] = make_uint4(0u, 0u, 0u, 0u);
-  }
+  // ctr: [0..2] group barriers, [3] weight waves done, [4] long-link tiles staged
+  unsigned* ctr = reinterpret_cast<unsigned*>(tl + 32 + 24 * RS);
+  int8_t* zero64 = reinterpret_cast<int8_t*>(tl + 32 + 24 * RS + 32);
+  uint32_t* sw_slots = reinterpret_cast<uint32_t*>(tl + 32 + 24 * RS + 96);   // [weight wave][64]
+  if (tid < 8) ctr[tid] = 0u;
+  if (tid < 4) reinterpret_cast<uint4*>(zero64)[tid] = make_uint4(0u, 0u, 0u, 0u);
   const unsigned run = __builtin_amdgcn_readfirstlane(
       __hip_atomic_load(counters + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
   const int rpar = (int)(run & 1u);
@@ -645,8 +662,8 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
       if (gm.T > 0)
-        act_link<PLANAR>(d, x0, M, rpar, deadline, err, gs, xch, xch_b, xch_c, act_l, Kpad, red_d + RS * par,
-                         red_i + RS * par, s_scale + 4 * par, consumed, 8u * (unsigned)i);
+        act_link<PLANAR>(wave, d, x0, M, rpar, deadline, err, gs, xch, xch_b, xch_c, act_l, Kpad, red_d + RS * par,
+                         red_i + RS * par, s_scale + 4 * par, consumed, 8u * (unsigned)i, ctr + 4);
       dev::lds_barrier();   // codes, scales and code sums are in LDS
       for (int c = 0; c < gm.nchunks; ++c) {
         dev::lds_barrier();                           // partial sums are in LDS
@@ -658,21 +675,24 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
     const int slice = wave - 4;
     const int gi = slice < 4 ? 1 : 2;   // rotation group of long links: tile 1 or tile 2
     dev::GroupSync<4> gsw{ctr + gi, 0u, wait_limit, err};
+    unsigned stage_count = 0;
     uint4 wr[16];
-    uint2 swq = make_uint2(0u, 0u);
+    // this wave's fp16 scales: the 16 of the tile it stores (tile `slice` of a link's first chunk) go
+    // straight into its LDS slot with the prefetch (a direct-to-LDS load: no register is held across
+    // the link loop), lanes 0-7 one dword each
+    uint32_t* my_sw = sw_slots + 64 * slice;
     auto prefetch = [&](const ChainDesc& dn) {   // the first chunk of a link, for this wave's slice
       const Geom gn = geom(dn, wg, G, TMAX);
       if (gn.T > 0) {
         const int T0 = gn.T < gn.tmax ? gn.T : gn.tmax;
         if (gn.lng) load_chunk_rt<FMT, true>(wr, dn, gn.t0, T0, slice);
         else load_chunk_rt<FMT, false>(wr, dn, gn.t0, T0, slice);
-        // fp16 scales of the tile this wave stores (tile `slice` of the chunk); the lane index opaque, so
-        // that its row offset is made here rather than kept (or spilled) across the link loop
-        int ln = threadIdx.x & 63;
+        int ln = dev::lane_id();
         asm volatile("" : "+v"(ln));
-        const int n = (gn.t0 + slice) * 16 + 4 * (ln >> 4);
+        const int n = (gn.t0 + slice) * 16 + 2 * ln;   // rows n, n + 1 in dword ln of the slot
         const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(dn.sw, (uint32_t)(dn.N * 2));
-        swq = dev::bload8(srs, slice < T0 && n < dn.N ? (uint32_t)(2 * n) : dev::kOutOfRange);
+        const uint32_t off = slice < T0 && ln < 8 && n < dn.N ? (uint32_t)(2 * n) : dev::kOutOfRange;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(srs, (__attribute__((address_space(3))) void*)my_sw, 4, off, 0, 0, 0);
       }
     };
     prefetch(links[0]);
@@ -681,7 +701,8 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
       if (gm.lng && gm.T > 0)
-        act_link_w<PLANAR>(d, M, gi, gsw, gi == 1 ? xch_b : xch_c, act_l, Kpad, red_d + RS * par, red_i + RS * par);
+        act_link_w<PLANAR>(slice & 3, d, M, gi, gsw, gi == 1 ? xch_b : xch_c, act_l, Kpad, red_d + RS * par,
+                           red_i + RS * par, ctr + 4, stage_count, deadline, err);
       dev::lds_barrier();   // codes are in LDS; this wave's weight loads stay in flight
       const __amdgpu_buffer_rsrc_t tyr = dev::make_rsrc(d.ty, (uint32_t)(2 * M * d.ystride * 2));
       for (int c = 0; c < gm.nchunks; ++c) {
@@ -699,12 +720,18 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
           // opaque here, so the per-lane addresses are computed in place rather than hoisted out of
           // the link loop: kept live across it they spill, and a spill reload's wait on the vector
           // memory counter would also wait for the agent-coherent stores issued before it.
-          int ln = threadIdx.x & 63;
+          int ln = dev::lane_id();
           asm volatile("" : "+v"(ln));
           const int n0 = (tile0 + slice) * 16 + 4 * (ln >> 4), m = ln & 15;
+          uint2 swq;
           if (c > 0) {
             const __amdgpu_buffer_rsrc_t srs = dev::make_rsrc(d.sw, (uint32_t)(d.N * 2));
             swq = dev::bload8(srs, n0 < d.N ? (uint32_t)(2 * n0) : dev::kOutOfRange);
+          } else {
+            // the direct-to-LDS scale load of the prefetch (issued after this wave's weight loads, which
+            // the MFMAs have consumed) has landed; rows 4 g .. 4 g + 3 are dwords 2 g, 2 g + 1
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            swq = *reinterpret_cast<const uint2*>(my_sw + 2 * (ln >> 4));
           }
           v4i D = red[(slice * 8) * 64 + ln];
 #pragma unroll
@@ -723,7 +750,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       }
       // done with this link's partial sums (the LDS reads have returned)
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      if (lane == 0) __hip_atomic_fetch_add(consumed, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (dev::lane_id() == 0) __hip_atomic_fetch_add(consumed, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       // every weight register has been consumed: no entry stays live into the next MFMA phase
 #pragma unroll
       for (int k = 0; k < 16; ++k) asm volatile("" : "=v"(wr[k]));
@@ -736,6 +763,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
   __syncthreads();
   if (wave == 0) {
     unsigned prev = 0;
+    const int lane = dev::lane_id();
     if (lane == 0) prev = __hip_atomic_fetch_add(counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     prev = __builtin_amdgcn_readfirstlane(prev);
     if (prev == (unsigned)G - 1 && lane == 0) {

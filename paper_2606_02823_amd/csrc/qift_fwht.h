@@ -84,6 +84,15 @@ __device__ __forceinline__ double dpp_f64(double x) {
                           __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xf, 0xf, false));
 }
 
+// Lane index within the wave, from the count of mask bits below the lane, made afresh at each use: it
+// reads no work-item id register and no earlier value, so nothing derived from it is kept live (or
+// spilled) across a caller's loops.
+__device__ __forceinline__ int lane_id() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 template <int B, int E>
 __device__ __forceinline__ void lane_stage(double (&v)[E]) {
   constexpr int CTRL = B == 0 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] / [2,3,0,1]

@@ -125,7 +125,7 @@ inline bool chain_block_ok(int block) { return block == 64 || block == 256 || bl
 constexpr int kChainMaxK = 16384;
 constexpr int kChainMaxLinks = 4096;
 constexpr int kChainSlots = 16;                    // per-token reduction slots (12 waves rotate long links)
-constexpr int kChainTailBytes = 32 + 96 * kChainSlots + 16 + 64;
+constexpr int kChainTailBytes = 32 + 96 * kChainSlots + 32 + 64 + 8 * 256;
 constexpr int kChainXchBytes = (4096 + 512) * 8;   // one rotation exchange buffer (a 4096-tile, padded)
 // LDS rotation region: the activation group's exchange buffer, and for a chain with a link of more
 // than one rotation tile (K > 4096) the two weight-wave groups' as well; aliased by the K-slice
