@@ -81,6 +81,11 @@ def _environment(torch):
     props = torch.cuda.get_device_properties(0)
     env = {"gpu": torch.cuda.get_device_name(0), "arch": getattr(props, "gcnArchName", None),
            "hip": torch.version.hip, "torch": torch.__version__, "cus": props.multi_processor_count}
+    if any(k.startswith("ROCPROF") for k in os.environ):
+        # under the profiler every child process initialises the GPU first, and rocm-smi (a Python
+        # script started through env) would then replace itself: not queried in profiled runs
+        env["clocks"] = "not queried under the profiler"
+        return env
     try:
         import subprocess
         r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)

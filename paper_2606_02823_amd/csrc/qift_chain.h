@@ -29,6 +29,28 @@
 #include "qift_internal.h"
 #include "qift_mma.h"
 
+// Phase stamps (a diagnostic build, -DQIFT_CHAIN_STAMPS, libqift_stamps.so): the 100 MHz wall clock
+// at marker k of link li in each workgroup, for the first 64 links of a call, kept per translation unit
+// (qift_chain_stamps_read reads the MNZ instance's).  Markers: 0 the activation group passed its
+// consumed wait, 1 its input is in, 2 its rotation is done, 3 the token's max is known, 4 its codes are
+// in LDS; 5 wave 4 passed the codes barrier, 6 its MFMAs are done, 7 it passed the partial-sums
+// barrier; 10 / 11 weight-wave group 1 starts / ends its rotation of a long link; 16 + s weight wave
+// s has issued its stores.  The stamps are stores of their own: a stamped run is a little slower.
+#ifdef QIFT_CHAIN_STAMPS
+namespace qift {
+static __device__ unsigned long long g_chain_stamps[256 * 64 * 32];
+}
+#define QIFT_STAMP(li, k)                                                                            \
+  do {                                                                                              \
+    if ((li) < 64 && blockIdx.x < 256)                                                              \
+      qift::g_chain_stamps[((size_t)blockIdx.x * 64 + (li)) * 32 + (k)] = wall_clock64();          \
+  } while (0)
+#else
+#define QIFT_STAMP(li, k) \
+  do {                    \
+  } while (0)
+#endif
+
 namespace qift {
 
 constexpr int kChainWaves = 12;
@@ -359,29 +381,34 @@ __device__ __forceinline__ void wait_consumed(const unsigned* consumed, unsigned
 }
 
 template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ double quant_group(int gw, const ChainDesc& d, const uint16_t* x0, int M, int m, int par,
+__device__ __forceinline__ double quant_group(int gw, int li, const ChainDesc& d, const uint16_t* x0, int M, int m, int par,
                                               long long deadline, uint32_t* err, GS& gsync, double* xch,
                                               int8_t* dst, double* red_d, int* red_i, const unsigned* consumed,
                                               unsigned consumed_target) {
   const int t = group_thread(gw);
   const int lane = t & 63, w = t >> 6;
   if (consumed) wait_consumed(consumed, consumed_target, deadline, err);
+  if (t == 0) QIFT_STAMP(li, 0);
   uint4 raw[1][2];
   fetch_tiles<1>(raw, d, x0, M, m, 1, t, par, deadline, err);
+  if (t == 0) QIFT_STAMP(li, 1);
   double v[16];
   dev::unpack16<false>(v, raw[0]);
   const int wend = dev::fwht_tile_s<256, 16, false>(v, xch, t, LC, gsync);
+  if (t == 0) QIFT_STAMP(li, 2);
   double amax = 0.0;
 #pragma unroll
   for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
   amax = dev::wave_max(amax);
   if (lane == 0) red_d[w] = amax;
   gsync();
+  if (t == 0) QIFT_STAMP(li, 3);
   const double A = fmax(fmax(red_d[0], red_d[1]), fmax(red_d[2], red_d[3]));
   const dev::QuantParams p = dev::make_qparams(A, d.num, d.den);
   int qs = codes16<PLANAR>(v, p, wend, 0, d.K, t, dst);
   qs = dev::wave_sum(qs);
   if (lane == 0) red_i[w] = qs;
+  if (t == 0) QIFT_STAMP(li, 4);
   return A;
 }
 
@@ -398,7 +425,7 @@ __device__ __forceinline__ double quant_group(int gw, const ChainDesc& d, const 
 //   * every group takes the token's max over the twelve slots and quantizes its tile(s) into the
 //     codes; code sums go to red_i[4 g + w].
 template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ double long_group_a(int gw, const ChainDesc& d, const uint16_t* x0, int M, int m, int NT,
+__device__ __forceinline__ double long_group_a(int gw, int li, const ChainDesc& d, const uint16_t* x0, int M, int m, int NT,
                                                int par, long long deadline, uint32_t* err, GS& gsync,
                                                double* xch, double* xch_b, double* xch_c, int8_t* dst,
                                                double* red_d, int* red_i, const unsigned* consumed,
@@ -406,8 +433,10 @@ __device__ __forceinline__ double long_group_a(int gw, const ChainDesc& d, const
   const int t = group_thread(gw);
   const int lane = t & 63, w = t >> 6;
   if (consumed) wait_consumed(consumed, consumed_target, deadline, err);
+  if (t == 0) QIFT_STAMP(li, 0);
   uint4 raw[4][2];
   fetch_tiles<4>(raw, d, x0, M, m, NT, t, par, deadline, err);
+  if (t == 0) QIFT_STAMP(li, 1);
   // the other groups' input: 32 bytes per thread at the start of their exchange buffers (their
   // exchanges of the previous token ended before the previous token's second barrier)
   uint4* sb = reinterpret_cast<uint4*>(xch_b);
@@ -436,9 +465,11 @@ __device__ __forceinline__ double long_group_a(int gw, const ChainDesc& d, const
 #pragma unroll
     for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v3[e]));
   }
+  if (t == 0) QIFT_STAMP(li, 2);
   amax = dev::wave_max(amax);
   if (lane == 0) red_d[w] = amax;
   dev::lds_barrier();   // every group's maxima are in LDS
+  if (t == 0) QIFT_STAMP(li, 3);
   double A = red_d[0];
 #pragma unroll
   for (int k = 1; k < 12; ++k) A = fmax(A, red_d[k]);
@@ -447,6 +478,7 @@ __device__ __forceinline__ double long_group_a(int gw, const ChainDesc& d, const
   if (NT > 3) qs += codes16<PLANAR>(v3, p, wend, 3, d.K, t, dst);
   qs = dev::wave_sum(qs);
   if (lane == 0) red_i[w] = qs;
+  if (t == 0) QIFT_STAMP(li, 4);
   return A;
 }
 
@@ -454,7 +486,7 @@ __device__ __forceinline__ double long_group_a(int gw, const ChainDesc& d, const
 // until the four activation waves have counted their staging writes (staged reaches stage_target),
 // then meet the activation group at the workgroup barrier after the maxima.
 template <int LC, bool PLANAR, typename GS>
-__device__ __forceinline__ void long_group_w(int gw, const ChainDesc& d, int NT, int gi, GS& gsync, double* xch_g,
+__device__ __forceinline__ void long_group_w(int gw, int li, const ChainDesc& d, int NT, int gi, GS& gsync, double* xch_g,
                                              int8_t* dst, double* red_d, int* red_i, const unsigned* staged,
                                              unsigned stage_target, long long deadline, uint32_t* err) {
   const int t = group_thread(gw);
@@ -469,7 +501,9 @@ __device__ __forceinline__ void long_group_w(int gw, const ChainDesc& d, int NT,
     uint4 r[2] = {sg[2 * t], sg[2 * t + 1]};
     gsync();   // every wave of the group has its input before the exchanges overwrite it
     dev::unpack16<false>(v, r);
+    if (t == 0 && gi == 1) QIFT_STAMP(li, 10);
     wend = dev::fwht_tile_s<256, 16, false>(v, xch_g, t, LC, gsync);
+    if (t == 0 && gi == 1) QIFT_STAMP(li, 11);
 #pragma unroll
     for (int e = 0; e < 16; ++e) amax = fmax(amax, fabs(v[e]));
   }
@@ -491,7 +525,7 @@ __device__ __forceinline__ void long_group_w(int gw, const ChainDesc& d, int NT,
 
 // The activation group's part of one link: every token; the scale of token m goes to s_scale[m].
 template <bool PLANAR, typename GS>
-__device__ __forceinline__ void act_link(int gw, const ChainDesc& d, const uint16_t* x0, int M, int par,
+__device__ __forceinline__ void act_link(int gw, int li, const ChainDesc& d, const uint16_t* x0, int M, int par,
                                          long long deadline, uint32_t* err, GS& gsync, double* xch, double* xch_b,
                                          double* xch_c, int8_t* act_l, int Kpad, double* red_d, int* red_i,
                                          float* s_scale, const unsigned* consumed, unsigned consumed_target,
@@ -506,17 +540,17 @@ __device__ __forceinline__ void act_link(int gw, const ChainDesc& d, const uint1
     // the block sizes compiled in (chain_block_ok): every butterfly stage is straight-line code
     if (NT > 1) {
       switch (d.L) {
-        case 12: A = long_group_a<12, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
-        case 11: A = long_group_a<11, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
-        case 8: A = long_group_a<8, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
-        default: A = long_group_a<6, PLANAR>(gw, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
+        case 12: A = long_group_a<12, PLANAR>(gw, li, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
+        case 11: A = long_group_a<11, PLANAR>(gw, li, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
+        case 8: A = long_group_a<8, PLANAR>(gw, li, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
+        default: A = long_group_a<6, PLANAR>(gw, li, d, x0, M, m, NT, par, deadline, err, gsync, xch, xch_b, xch_c, dst, rd, ri, cw, consumed_target, staged); break;
       }
     } else {
       switch (d.L) {
-        case 12: A = quant_group<12, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
-        case 11: A = quant_group<11, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
-        case 8: A = quant_group<8, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
-        default: A = quant_group<6, PLANAR>(gw, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 12: A = quant_group<12, PLANAR>(gw, li, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 11: A = quant_group<11, PLANAR>(gw, li, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        case 8: A = quant_group<8, PLANAR>(gw, li, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
+        default: A = quant_group<6, PLANAR>(gw, li, d, x0, M, m, par, deadline, err, gsync, xch, dst, rd, ri, cw, consumed_target); break;
       }
     }
     if (gw == 0 && dev::lane_id() == 0) s_scale[m] = (float)((A * (double)d.num) / d.denom);
@@ -526,7 +560,7 @@ __device__ __forceinline__ void act_link(int gw, const ChainDesc& d, const uint1
 // The weight waves' part of a long link: every token.
 // stage_count: the tokens of long links staged so far in this call (the same count in every wave).
 template <bool PLANAR, typename GS>
-__device__ __forceinline__ void act_link_w(int gw, const ChainDesc& d, int M, int gi, GS& gsync, double* xch_g,
+__device__ __forceinline__ void act_link_w(int gw, int li, const ChainDesc& d, int M, int gi, GS& gsync, double* xch_g,
                                            int8_t* act_l, int Kpad, double* red_d, int* red_i,
                                            const unsigned* staged, unsigned& stage_count, long long deadline,
                                            uint32_t* err) {
@@ -537,10 +571,10 @@ __device__ __forceinline__ void act_link_w(int gw, const ChainDesc& d, int M, in
     int8_t* dst = act_l + m * Kpad;
     const unsigned tg = 4u * ++stage_count;
     switch (d.L) {
-      case 12: long_group_w<12, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
-      case 11: long_group_w<11, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
-      case 8: long_group_w<8, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
-      default: long_group_w<6, PLANAR>(gw, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
+      case 12: long_group_w<12, PLANAR>(gw, li, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
+      case 11: long_group_w<11, PLANAR>(gw, li, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
+      case 8: long_group_w<8, PLANAR>(gw, li, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
+      default: long_group_w<6, PLANAR>(gw, li, d, NT, gi, gsync, xch_g, dst, rd, ri, staged, tg, deadline, err); break;
     }
   }
 }
@@ -662,7 +696,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
       if (gm.T > 0)
-        act_link<PLANAR>(wave, d, x0, M, rpar, deadline, err, gs, xch, xch_b, xch_c, act_l, Kpad, red_d + RS * par,
+        act_link<PLANAR>(wave, i, d, x0, M, rpar, deadline, err, gs, xch, xch_b, xch_c, act_l, Kpad, red_d + RS * par,
                          red_i + RS * par, s_scale + 4 * par, consumed, 8u * (unsigned)i, ctr + 4);
       dev::lds_barrier();   // codes, scales and code sums are in LDS
       for (int c = 0; c < gm.nchunks; ++c) {
@@ -701,9 +735,10 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       const Geom gm = geom(d, wg, G, TMAX);
       const int par = i & 1;
       if (gm.lng && gm.T > 0)
-        act_link_w<PLANAR>(slice & 3, d, M, gi, gsw, gi == 1 ? xch_b : xch_c, act_l, Kpad, red_d + RS * par,
+        act_link_w<PLANAR>(slice & 3, i, d, M, gi, gsw, gi == 1 ? xch_b : xch_c, act_l, Kpad, red_d + RS * par,
                            red_i + RS * par, ctr + 4, stage_count, deadline, err);
       dev::lds_barrier();   // codes are in LDS; this wave's weight loads stay in flight
+      if (wave == 4 && dev::lane_id() == 0) QIFT_STAMP(i, 5);
       const __amdgpu_buffer_rsrc_t tyr = dev::make_rsrc(d.ty, (uint32_t)(2 * M * d.ystride * 2));
       for (int c = 0; c < gm.nchunks; ++c) {
         const int tile0 = gm.t0 + c * gm.tmax;
@@ -714,7 +749,9 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
         }
         if (gm.lng) mfma_chunk_rt<FMT, true>(wr, d, tile0, Tc, slice, act_l, Kpad, M, zero64, red);
         else mfma_chunk_rt<FMT, false>(wr, d, tile0, Tc, slice, act_l, Kpad, M, zero64, red);
+        if (wave == 4 && c == 0 && dev::lane_id() == 0) QIFT_STAMP(i, 6);
         dev::lds_barrier();   // the slices' partial sums are in LDS
+        if (wave == 4 && c == 0 && dev::lane_id() == 0) QIFT_STAMP(i, 7);
         if (slice < Tc) {
           // this wave's tile: add the K-slices, apply the epilogue and store.  The lane index is
           // opaque here, so the per-lane addresses are computed in place rather than hoisted out of
@@ -751,6 +788,7 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
       // done with this link's partial sums (the LDS reads have returned)
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       if (dev::lane_id() == 0) __hip_atomic_fetch_add(consumed, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (dev::lane_id() == 0) QIFT_STAMP(i, 16 + slice);
       // every weight register has been consumed: no entry stays live into the next MFMA phase
 #pragma unroll
       for (int k = 0; k < 16; ++k) asm volatile("" : "=v"(wr[k]));

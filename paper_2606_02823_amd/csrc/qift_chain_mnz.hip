@@ -10,3 +10,12 @@ hipError_t launch_chain_mnz(const ChainDesc* links, int n_links, const uint16_t*
 }
 
 }  // namespace qift
+
+#ifdef QIFT_CHAIN_STAMPS
+// The diagnostic build's reader of the MNZ chain's phase stamps (qift_chain.h): bytes of
+// g_chain_stamps into host memory.  Not part of the product library's interface.
+extern "C" int qift_chain_stamps_read(void* host, size_t bytes) {
+  if (bytes > sizeof(qift::g_chain_stamps)) return -1;
+  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(qift::g_chain_stamps), bytes, 0, hipMemcpyDeviceToHost);
+}
+#endif
