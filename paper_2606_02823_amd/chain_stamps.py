@@ -9,14 +9,15 @@ with Hadamard blocks of 2048; MNZ weights, M = 1, real data dependencies) for `l
 last call and prints, per linear shape, the median over workgroups and over the layers after the
 first of each phase of a link (microseconds):
 
-  visible   the median producer's last store of the previous link -> this workgroup's input is in
-  spread    the last producer's last store minus the median producer's
+  visible   the median producer of the previous link is done (its stores complete) -> this
+            workgroup's input is in
+  spread    the last producer's done time minus the median producer's
   rotation  input in -> the activation group's rotation is done
   max       rotation done -> the token's max is known
   quantize  max known -> the codes are in LDS
   barrier   codes in LDS -> weight wave 4 passed the codes barrier
   mfma      that barrier -> wave 4's MFMAs are done
-  tail      MFMAs done -> the last weight wave of the workgroup has issued its stores
+  tail      MFMAs done -> the last weight wave of the workgroup is done (its stores complete)
   link      median producer to median producer
 
 The stamps are global stores of their own, so a stamped step is slightly slower than the product's.
@@ -68,7 +69,7 @@ def main(layers: int = 4) -> None:
     d = buf.reshape(N_WG, N_LINK, N_MARK)[:, :n, :].astype(np.float64)
     t0 = np.nanmin(np.where(d[:, 0, 1] > 0, d[:, 0, 1], np.nan))
     d = np.where(d > 0, (d - t0) / 100.0, np.nan)   # 100 MHz ticks -> microseconds
-    stores = np.nanmax(d[:, :, 16:24], axis=2)       # per workgroup and link: its last weight wave's stores
+    stores = np.nanmax(d[:, :, 16:24], axis=2)       # per workgroup and link: its last weight wave done
     med = lambda a: float(np.nanmedian(a))
     print(f"LLaMA-3.1-8B decode step, MNZ, M = 1, {layers} layers ({n} links), stamps of the last call; "
           f"device error bits {err}")

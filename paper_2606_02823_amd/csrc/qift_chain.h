@@ -7,22 +7,21 @@
 //
 // Grid: one workgroup per CU, 12 waves each.  Linear ("link") i of the chain is cut into 16-row
 // tiles; workgroup g owns tiles [g T / G, (g + 1) T / G) of it.  Per link:
-//   * activation waves (0-3; 0-7 for K > 4096, two groups of four sharing the rotation tiles)
-//     wait until every workgroup has published the link's input (an arrival counter per link in
-//     device memory, polled by wave 0 with agent-coherent loads, then handed on through LDS), load
-//     the token(s) with agent-coherent loads, rotate exactly in fp64, quantize and write the codes
-//     to LDS (the routines of qift_fwht.h);
-//   * weight waves (4-11, K-slices of 512 k; 8-11 for K > 4096, slices of K/4) issued their
-//     weight loads at the end of the previous link, so those bytes stream during the wait, the
-//     token load and the rotation; after the codes barrier they run the MFMAs (qift_mma.h) and
-//     write per-slice partial sums to LDS;
-//   * waves 0-3 add the slices, apply the epilogue and store y with agent-coherent (sc1) stores,
-//     wait for the stores to complete and bump the link's arrival counter.
-// Cross-XCD visibility: y is stored with sc1 (coherent at device scope) and read back by the
-// consumers with sc1 loads, and the counter is incremented only after the stores have completed,
-// so no L2 writeback or invalidation of the whole cache is needed.  Every wait is bounded (by
-// time); a wait that gives up sets a bit in the device error word and the workgroup carries on, so
-// the grid always drains.  The last workgroup to finish resets the counters for the next call.
+//   * the activation group (waves 0-3) polls for the link's input in its producer's exchange copy
+//     (agent-coherent loads until no value is the not-written pattern), rotates it exactly in fp64,
+//     finds the token's absmax, quantizes and writes the codes and code sums to LDS (the routines of
+//     qift_fwht.h); for K > 4096 the two halves of the weight waves rotate tiles 1 and 2 of the
+//     token meanwhile (the activation group stages them in LDS);
+//   * the weight waves (4-11, K-slices of 1/8 of K) issued their weight loads at the end of the
+//     previous link, so those bytes stream during the wait and the rotation; after the codes
+//     barrier they run the MFMAs (qift_mma.h) and write per-slice partial sums to LDS, and weight
+//     wave 4 + j adds the slices of tile j, applies the epilogue and stores y, and the exchange copy
+//     when another link reads this output, with agent-coherent (sc1) stores.
+// Cross-XCD visibility: data and readiness travel in the same sc1 access (an exchange value is never
+// the not-written pattern once written), so there is no flag, counter or L2 writeback per link.
+// Every wait is bounded (by time); a wait that gives up sets a bit in the device error word and the
+// workgroup carries on, so the grid always drains.  The last workgroup to finish advances the run
+// number that selects the exchange copies of the next call.
 #pragma once
 
 #include "qift_fwht.h"
@@ -35,7 +34,8 @@
 // consumed wait, 1 its input is in, 2 its rotation is done, 3 the token's max is known, 4 its codes are
 // in LDS; 5 wave 4 passed the codes barrier, 6 its MFMAs are done, 7 it passed the partial-sums
 // barrier; 10 / 11 weight-wave group 1 starts / ends its rotation of a long link; 16 + s weight wave
-// s has issued its stores.  The stamps are stores of their own: a stamped run is a little slower.
+// s has counted itself done with the link (its stores have completed).  The stamps are stores of
+// their own: a stamped run is a little slower.
 #ifdef QIFT_CHAIN_STAMPS
 namespace qift {
 static __device__ unsigned long long g_chain_stamps[256 * 64 * 32];
@@ -785,8 +785,10 @@ __global__ __launch_bounds__(kChainThreads) void k_decode_chain(const ChainDesc*
         }
         if (c + 1 < gm.nchunks) dev::lds_barrier();   // the partial sums have been read
       }
-      // done with this link's partial sums (the LDS reads have returned)
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // done with this link's partial sums (the LDS reads have returned) and with its stores: the
+      // activation group starts polling for the next link's input on this count, and polls that
+      // overlapped this CU's stores in flight were measured to slow the step by 5 %
+      __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0)
       if (dev::lane_id() == 0) __hip_atomic_fetch_add(consumed, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       if (dev::lane_id() == 0) QIFT_STAMP(i, 16 + slice);
       // every weight register has been consumed: no entry stays live into the next MFMA phase
