@@ -376,8 +376,9 @@ int qift_rotate_quant_linear(const qift_packed_w *w, const uint16_t *x, int64_t 
  * rotate + quantize + linear of qift_rotate_quant_linear (Sec. 3.1 rotation and per-token INT4
  * quantizer, Sec. 3.3 / 3.6 integer dot product, scales in the epilogue) whose input is either the
  * chain input x or a slice of an earlier link's output; the kernel honours those dependencies
- * with per-link arrival counters in the workspace, while the weight stream of the next link runs
- * ahead of them.  Results are bit-identical to calling qift_rotate_quant_linear link by link.
+ * through exchange copies of the outputs in the workspace (a consumer reads its input there until
+ * no value is the not-written pattern), while the weight stream of the next link runs ahead of
+ * them.  Results are bit-identical to calling qift_rotate_quant_linear link by link.
  *
  *   qift_chain_link   (host) one linear:
  *     w          the weights (fmt MNZ, PoT or W4; one format for the whole chain).
@@ -411,7 +412,7 @@ typedef struct {
   int32_t grid, kmax;        /* workgroups (one per CU), largest K of the links */
   int32_t region0, reserved; /* LDS bytes of the activation group's work region */
   const void *table;         /* device: the link table (in the workspace) */
-  uint32_t *counters;        /* device: arrival count and run number (in the workspace) */
+  uint32_t *counters;        /* device: finished-workgroup count and run number (in the workspace) */
 } qift_chain;
 
 /*
@@ -428,7 +429,8 @@ size_t qift_chain_workspace_bytes(const qift_chain_link *links, int32_t n_links,
  * from host memory); not capturable in a HIP graph.
  *   links      host: n_links links (1 <= n_links <= 4096).
  *   M          tokens per call, 1..4, as far as one workgroup's LDS holds M tokens' codes next to
- *              the stash of the longest link's rotation tiles (a K = 14336 link: M = 1).
+ *              the rotation buffers (three of them for a chain with a link of K > 4096: with a
+ *              K = 14336 link, M <= 3).
  *   K0         width of the chain input x.
  *   workspace  device, 16-byte aligned, at least qift_chain_workspace_bytes(links, n_links, M).
  *   chain      host, out.
