@@ -305,6 +305,9 @@ class SweepStack:
                   for (_, _, K, _, site) in self.plan]
         self.acts = [qift.alloc_act(self.M, K, dev) for (_, _, K, _, _) in self.plan]
         self.outs = [torch.empty((self.M, N), dtype=torch.float16, device=dev) for (_, N, _, _, _) in self.plan]
+        # one workspace for the linears that take one at this M (the skinny linear split over K)
+        self.need = [qift.workspace_bytes(w, self.M) for w in self.weights[0]]
+        self.ws = torch.empty(max(self.need), dtype=torch.uint8, device=dev) if max(self.need) else None
         torch.cuda.synchronize()
         self.packed_bytes = sum(w.nbytes for ws in self.weights for w in ws)
         self.ops = self.layers * sum(2 * self.M * N * K for (_, N, K, _, _) in self.plan)
@@ -318,7 +321,8 @@ class SweepStack:
                     qift.rotate_quant_linear(ws[i], self.x[i], b, out=self.outs[i])
                 else:
                     act = qift.rotate_quant_act(self.x[i], b, out=self.acts[i])
-                    qift.w2a4_linear(ws[i], act, out=self.outs[i], use_sum=True)
+                    qift.w2a4_linear(ws[i], act, out=self.outs[i], use_sum=True,
+                                     workspace=self.ws[:self.need[i]] if self.need[i] else None)
 
 
 def stack_sweep(torch, qift, synth, reps=20):

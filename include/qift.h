@@ -310,13 +310,19 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
  *   workspace, workspace_bytes   optional device scratch (16-byte aligned).
  *              NULL / 0 runs the int8 MFMA kernels.  With at least
  *              qift_workspace_bytes(w, M) bytes, where that is not 0 (MNZ
- *              and PoT weights, M > 64), the activations are re-coded to FP6
- *              E2M3 in it and the prefill contraction runs on the FP4 x FP6
- *              scaled MFMA: the MNZ code c read as FP4 E2M1 is c / 2, the
- *              PoT levels +-1, +-4 are E2M1 values, and every partial sum
- *              stays exact in fp32, so the results are bit-identical.  A
- *              non-zero size below the query is QIFT_ERR_WORKSPACE.  The
- *              workspace is overwritten.
+ *              and PoT weights):
+ *                M > 64: the activations are re-coded to FP6 E2M3 in it and
+ *                the prefill contraction runs on the FP4 x FP6 scaled MFMA:
+ *                the MNZ code c read as FP4 E2M1 is c / 2, the PoT levels
+ *                +-1, +-4 are E2M1 values, and every partial sum stays exact
+ *                in fp32;
+ *                M <= 64 (K > 4096, few 16-row tiles; up to 16 tokens only
+ *                where the codes exceed the decode kernel's LDS): the decode
+ *                linear is split over K, int32 partial sums of each K-range in
+ *                the workspace, then added and the epilogue applied.
+ *              Either way the results are bit-identical.  A non-zero size
+ *              below the query is QIFT_ERR_WORKSPACE.  The workspace is
+ *              overwritten.
  */
 int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
                         const int32_t *act_sum, int64_t M, uint16_t *out, int32_t *acc_out,
@@ -553,9 +559,12 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
                                       const uint8_t *k_zeros, const uint8_t *v_codes, const float *v_scales,
                                       const uint8_t *v_zeros, uint16_t *out, qift_stream_t stream);
 
-/* Workspace bytes that select the FP4 x FP6 prefill kernel in the _ex calls for this weight and
- * M (M * 3K/4 plus the code sums, for MNZ and PoT weights at M > 64), 0 where no workspace is used
- * (host query). */
+/* Workspace bytes that the _ex calls use for this weight and M, 0 where none is used (host
+ * query).  MNZ and PoT weights only: at M > 64 the FP4 x FP6 prefill kernel's (M * 3K/4 plus the code
+ * sums); at M <= 64 the decode linear split over K, where it applies (K > 4096 and fewer 16-row tiles
+ * than about 1000; up to 16 tokens only where the codes exceed the decode kernel's LDS): S * M * N4
+ * int32 partial sums (N4 = N rounded up to 4, 256-byte aligned) and S * M int32 code sums, S the
+ * number of K-ranges. */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
 
 /* Static text for a status code. */

@@ -155,6 +155,14 @@ constexpr int64_t kSkinnyMaxK = 16384;
 hipError_t launch_skinny(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
                          uint16_t* out, int32_t* acc_out, hipStream_t s);
+// The same split over K for W2 weights (MNZ, PoT) whose few 16-row tiles would leave every workgroup
+// reading all M x K codes for 16 or 32 rows (M <= 64; up to 16 tokens only where the decode kernel on
+// codes does not fit): ws holds skinny_workspace(fmt, N, K, M) bytes (0: no split for this linear;
+// then, or with ws null, the call above).
+size_t skinny_workspace(int fmt, int64_t N, int64_t K, int64_t M);
+hipError_t launch_skinny_ws(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
+                            const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
+                            uint16_t* out, int32_t* acc_out, void* ws, hipStream_t s);
 constexpr int64_t kFusedMaxK = 16384;
 constexpr int kFusedMaxBlock = 4096;
 // Largest K accepted by the activation quantizer.

@@ -563,7 +563,7 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
   // 17..64 tokens: the skinny kernel, one pass over the weights (the codes of that many tokens do not
   // fit the decode kernel's LDS, and the GEMM's grid of N/256 workgroups would leave most CUs idle)
   if (M > kCodesMaxM && M <= kSkinnyMaxM && K <= kSkinnyMaxK)
-    return launch_skinny(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, s);
+    return launch_skinny_ws(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
   if (M <= kCodesMaxM) {
     // the decode kernel on precomputed codes (K-slice weight waves, the codes staged in LDS)
     const size_t cs = FMT == FMT_MNZ ? codes_shmem_mnz(M, N, K) : FMT == FMT_POT ? codes_shmem_pot(M, N, K)
@@ -573,8 +573,13 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
       else if constexpr (FMT == FMT_POT) return launch_codes_pot(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
       else return launch_codes_w4(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
     }
-    // codes beyond LDS (e.g. 16 tokens of K = 14336): the decode kernels that read them from memory
-    // (measured faster there than the skinny kernel with one token tile: 16 tokens at K = 14336)
+    // codes beyond LDS (e.g. 16 tokens of K = 14336): with a workspace the skinny linear split over K;
+    // else the decode kernels that read them from memory (measured faster there than the skinny
+    // kernel unsplit with one token tile: 16 tokens at K = 14336)
+    if constexpr (FMT != FMT_W4) {
+      if (ws && skinny_workspace(FMT, N, K, M) != 0)
+        return launch_skinny_ws(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
+    }
     if (M * kpad_of(K) <= kDecodeMaxLds) return launch_deep<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
     return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
   }

@@ -233,6 +233,21 @@ def test_linear_validation(L):
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 65) == 65 * 3 * (K // 4) + 65 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT)), 65) == 65 * 3 * (K // 4) + 65 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM)), 65) == 0
+    # 17..64 tokens: the skinny linear split over K when K > 4096 and its 16-row tiles are few (4 tiles
+    # per workgroup, S ranges of K for about 256 workgroups, at most two 256-k units per K-slice):
+    # S M N4 int32 partial sums (256-byte aligned), then S M int32 code sums; none for a gate|up width
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT, N=1000, K=14336)), 64) == 14 * 64 * 1000 * 4 + 14 * 64 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=14336)), 64) == 14 * 64 * 1000 * 4 + 14 * 64 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT, N=1000, K=14336)), 17) == 952064 + 14 * 17 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 64) == 4 * 64 * 4096 * 4 + 4 * 64 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=4096)), 64) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=28672, K=4096)), 64) == 0
+    # up to 16 tokens only where the decode kernel's LDS does not hold the codes (16 x 14336 does not,
+    # 4 x 14336 and 16 x 4096 do)
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=14336)), 16) == 14 * 16 * 1000 * 4 + 14 * 16 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=14336)), 4) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT, N=1000, K=4096)), 16) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=1000, K=14336)), 64) == 0
     # FP6 codes (M 3K/4 bytes), then one int32 code sum per token and 256 groups of 32 k
     need = 100 * 3 * (K // 4) + 100 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 100) == need
