@@ -561,8 +561,8 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
 
 /* Workspace bytes that the _ex calls use for this weight and M, 0 where none is used (host
  * query).  MNZ and PoT weights only: at M > 64 the FP4 x FP6 prefill kernel's (M * 3K/4 plus the code
- * sums); at M <= 64 the decode linear split over K, where it applies (K > 4096 and fewer 16-row tiles
- * than about 1000; up to 16 tokens only where the codes exceed the decode kernel's LDS): S * M * N4
+ * sums); at M <= 64 the decode linear split over K, where it applies (K > 4096 and at most 680
+ * 16-row tiles, N <= 10880; up to 16 tokens only where the codes exceed the decode kernel's LDS): S * M * N4
  * int32 partial sums (N4 = N rounded up to 4, 256-byte aligned) and S * M int32 code sums, S the
  * number of K-ranges. */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
