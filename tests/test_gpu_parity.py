@@ -254,6 +254,18 @@ def test_rotate_quant_act_blocks(Q, K, b):
     check_act(act, x, b)
 
 
+@pytest.mark.parametrize("M,K,b", [(1, 14336, 2048), (16, 11008, 64), (256, 14336, 2048), (257, 14336, 2048),
+                                   (3, 12288, 4096), (64, 8192, 256)])
+def test_rotate_quant_act_tile_parallel(Q, M, K, b):
+    # up to 256 tokens of several 4096-tiles the tiles are rotated at once by groups of four waves,
+    # one token per workgroup; from 257 tokens on by the persistent kernel: the same codes either way
+    x = synth.activations_fp16(93, M, b, M, K, max(1, K // 100), 30.0)
+    if M > 2:
+        x[1] = 0                                            # all-zero token
+    act = Q.rotate_quant_act(dev(x), b)
+    check_act(act, x, b)
+
+
 def test_rotate_quant_act_exact_ties(Q):
     u = 2.0 ** -10
     pairs = [(9.5, 4.5), (10.5, 3.5), (7.5, 6.5), (8.5, 5.5), (4.5, 9.5)]
