@@ -33,9 +33,12 @@ using namespace mma;
 
 constexpr int kSkSlices = 8;
 
-// VGPRs of a lane's accumulators, weight groups (U units of T tiles) and one unit's codes
+// VGPRs of a lane's accumulators (MNZ by bit plane below four token tiles: two per tile pair), weight
+// groups (U units of T tiles) and one unit's codes
 template <int FMT, int T, int TT, int U>
-constexpr int sk_regs() { return T * TT * (FMT == FMT_MNZ ? 2 : 1) * 4 + U * T * (FMT == FMT_W4 ? 2 : 1) * 4 + TT * 16; }
+constexpr int sk_regs() {
+  return T * TT * (FMT == FMT_MNZ && TT < 4 ? 2 : 1) * 4 + U * T * (FMT == FMT_W4 ? 2 : 1) * 4 + TT * 16;
+}
 // a second code buffer (the next unit's loads in flight during this unit's MFMAs) where it fits
 template <int FMT, int T, int TT, int U>
 constexpr bool sk_double() { return sk_regs<FMT, T, TT, U>() + TT * 16 <= 224; }
