@@ -305,7 +305,8 @@ class SweepStack:
                   for (_, _, K, _, site) in self.plan]
         self.acts = [qift.alloc_act(self.M, K, dev) for (_, _, K, _, _) in self.plan]
         self.outs = [torch.empty((self.M, N), dtype=torch.float16, device=dev) for (_, N, _, _, _) in self.plan]
-        # one workspace for the linears that take one at this M (the skinny linear split over K)
+        # one workspace for the linears that take one at this M (the skinny linear split over K up to 64
+        # tokens, the FP4 x FP6 GEMM above)
         self.need = [qift.workspace_bytes(w, self.M) for w in self.weights[0]]
         self.ws = torch.empty(max(self.need), dtype=torch.uint8, device=dev) if max(self.need) else None
         torch.cuda.synchronize()
@@ -326,10 +327,10 @@ class SweepStack:
 
 
 def stack_sweep(torch, qift, synth, reps=20):
-    """Tokens/s and packed GB/s of the cfg2 stack at M in {1, 4, 16} and the cfg3 PoT MLP stack at
+    """Tokens/s and packed GB/s of the cfg2 stack at M in {1, 4, 16, 128} and the cfg3 PoT MLP stack at
     M in {1, 8, 64} (hipGraph replays, inputs resident)."""
     rows = []
-    for cfg, Ms in ((2, (1, 4, 16)), (3, (1, 8, 64))):
+    for cfg, Ms in ((2, (1, 4, 16, 128)), (3, (1, 8, 64))):
         for M in Ms:
             st = SweepStack(torch, qift, synth, cfg, M)
             st.setup()
@@ -783,7 +784,7 @@ def main():
     ap.add_argument("--no-kv4", action="store_true", help="skip the KV4 attention timing")
     ap.add_argument("--no-lut", action="store_true", help="skip the level-table linear timing")
     ap.add_argument("--no-sweep", action="store_true",
-                    help="skip the cfg2 (M 1/4/16) and cfg3 PoT (M 1/8/64) stack sweep")
+                    help="skip the cfg2 (M 1/4/16/128) and cfg3 PoT (M 1/8/64) stack sweep")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run 1 GiB device copies (HBM byte-counter calibration under rocprofv3)")
     ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_BYTES"),

@@ -315,7 +315,8 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
  *                the prefill contraction runs on the FP4 x FP6 scaled MFMA:
  *                the MNZ code c read as FP4 E2M1 is c / 2, the PoT levels
  *                +-1, +-4 are E2M1 values, and every partial sum stays exact
- *                in fp32;
+ *                in fp32; where its 256-row x 64-token tiles are few (about
+ *                65-1024 tokens, by N) it is split over K the same way;
  *                M <= 64 (K > 4096, few 16-row tiles; up to 16 tokens only
  *                where the codes exceed the decode kernel's LDS): the decode
  *                linear is split over K, int32 partial sums of each K-range in
@@ -560,11 +561,14 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
                                       const uint8_t *v_zeros, uint16_t *out, qift_stream_t stream);
 
 /* Workspace bytes that the _ex calls use for this weight and M, 0 where none is used (host
- * query).  MNZ and PoT weights only: at M > 64 the FP4 x FP6 prefill kernel's (M * 3K/4 plus the code
- * sums); at M <= 64 the decode linear split over K, where it applies (K > 4096 and at most 680
- * 16-row tiles, N <= 10880; up to 16 tokens only where the codes exceed the decode kernel's LDS): S * M * N4
- * int32 partial sums (N4 = N rounded up to 4, 256-byte aligned) and S * M int32 code sums, S the
- * number of K-ranges. */
+ * query).  MNZ and PoT weights only.  At M > 64 the FP4 x FP6 prefill kernel's: M * 3K/4 bytes of FP6
+ * codes and M * ceil(K / 8192) int32 code sums; where its T = ceil(N / 256) * ceil(M / 64) tiles are
+ * few, split over S = min(ceil(512 / T), floor(768 / T), floor(ceil(K / 256) / 4)) K-ranges when that
+ * is at least 2, followed (at the next multiple of 256 bytes) by S * M * N4 int32 partial sums (N4 =
+ * N rounded up to 4; S recounted after the ranges are sized).  At M <= 64 the decode linear split
+ * over K, where it applies (K > 4096 and at most 680 16-row tiles, N <= 10880; up to 16 tokens only
+ * where the codes exceed the decode kernel's LDS): S * M * N4 int32 partial sums (256-byte aligned)
+ * and S * M int32 code sums, S the number of K-ranges. */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
 
 /* Static text for a status code. */

@@ -575,7 +575,7 @@ size_t qift_workspace_bytes(const qift_packed_w* w, int64_t M) {
   if (M <= qift::kSkinnyMaxM)
     return qift::skinny_workspace(w->fmt, w->N, w->K, M);   // the skinny linear split over K
   if (M < qift::kGemmF4MinM) return 0;
-  return qift::gemm_f4_workspace(M, w->K);
+  return qift::gemm_f4_workspace(w->N, M, w->K);
 }
 
 const char* qift_status_string(int status) {

@@ -48,15 +48,16 @@ hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int 
                                    hipStream_t s, bool bf16 = false);   // x fp16, or bf16 bits
 
 // Quantized linear (qift_linear.hip).  fmt selects the decode.  ws (nullable) holds at least
-// gemm_f4_workspace(M, K) bytes: with it, MNZ weights at M > 64 run the FP4 x FP6 MFMA kernel.
+// gemm_f4_workspace(N, M, K) bytes: with it, MNZ and PoT weights at M > 64 run the FP4 x FP6 MFMA kernel.
 hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
                          uint16_t* out, int32_t* acc_out, void* ws, hipStream_t s);
 
 // MNZ and PoT prefill on the FP4 x FP6 scaled MFMA (qift_prefill_f4.hip): act_q re-coded to FP6
-// into ws (gemm_f4_workspace(M, K) bytes), then the GEMM; results identical to the int8 kernel.
+// into ws (gemm_f4_workspace(N, M, K) bytes), then the GEMM, split over K into int32 partial sums in
+// ws where its tiles are few; results identical to the int8 kernel.
 constexpr int64_t kGemmF4MinM = 65;
-size_t gemm_f4_workspace(int64_t M, int64_t K);
+size_t gemm_f4_workspace(int64_t N, int64_t M, int64_t K);
 hipError_t launch_gemm_f4(int fmt, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
                           const int8_t* act_q, const float* sx, const int32_t* asum, int64_t M, uint16_t* y,
                           int32_t* acc_out, void* ws, hipStream_t s);

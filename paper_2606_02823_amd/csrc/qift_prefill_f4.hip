@@ -20,6 +20,7 @@
 #include "qift_fwht.h"
 #include "qift_internal.h"
 #include "qift_mma.h"
+#include "qift_split.h"
 
 namespace qift {
 namespace {
@@ -95,12 +96,15 @@ __device__ __forceinline__ uint32_t pot_f4(uint32_t x) {
   return ((b1 ^ 0x11111111u) << 3) | ((b1 ^ b0 ^ 0x11111111u) << 2) | 0x22222222u;
 }
 
-template <int FMT, int OCC>
+// SPLIT: workgroup z of the grid's third dimension takes the steps [z us, (z + 1) us) of K and writes
+// its exact partial sums (int32) to part [z][M][N rounded up to 4] instead of the outputs.
+template <int FMT, int OCC, bool SPLIT>
 __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                       int N, int K, const uint8_t* __restrict__ act6,
                                                       const float* __restrict__ sx, const int32_t* __restrict__ asum,
                                                       const int32_t* __restrict__ psum, int npsum,
-                                                      int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+                                                      int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out,
+                                                      int us, int32_t* __restrict__ part) {
   constexpr int BM = 64, BK = 256;
   __shared__ __align__(16) uint8_t lds0[BM * 256];
   __shared__ __align__(16) uint8_t lds1[BM * 256];
@@ -110,7 +114,9 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict
   const int n_base = blockIdx.x * 256 + wave * 64;
   const int m_base = blockIdx.y * BM;
   const int rowbytes = K / 4, row6 = 3 * (K / 4);
-  const int KT = (K + BK - 1) / BK;
+  const int KA = (K + BK - 1) / BK;
+  const int kt0 = SPLIT ? (int)blockIdx.z * us : 0;
+  const int KT = SPLIT ? (kt0 + us < KA ? kt0 + us : KA) : KA;   // steps past this workgroup's range
 
   // weights: as in the int8 kernel (lanes past K in a last partial step meet zero activations)
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)N * (uint32_t)rowbytes);
@@ -201,15 +207,32 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict
   };
 
   uint4 wa[4], wb[4];
-  issue_a(0, lds0);
-  load_w(wa, 0);
+  issue_a(kt0, lds0);
+  load_w(wa, kt0);
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
-  for (int kt = 0; kt < KT; kt += 2) {
+  for (int kt = kt0; kt < KT; kt += 2) {
     step(kt, lds0, lds1, wa, wb);
     if (kt + 1 < KT) step(kt + 1, lds1, lds0, wb, wa);
   }
 
+  if constexpr (SPLIT) {
+    const int np = (N + 3) & ~3;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int m = m_base + 16 * t + r16;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int n0 = n_base + 16 * j + 4 * g;
+        const float f = FMT == FMT_MNZ ? 2.f : 1.f;
+        if (m < M && n0 < N)
+          *reinterpret_cast<int4*>(part + ((size_t)blockIdx.z * M + m) * np + n0) =
+              make_int4((int)(f * acc[j][t][0]), (int)(f * acc[j][t][1]), (int)(f * acc[j][t][2]),
+                        (int)(f * acc[j][t][3]));
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int m = m_base + 16 * t + r16;
@@ -238,14 +261,44 @@ __global__ __launch_bounds__(256, OCC) void k_gemm_f4(const uint32_t* __restrict
 // workgroups of the FP6 re-coding per token (256 groups of 32 k each)
 inline int64_t act_fp6_blocks(int64_t K) { return (K / 32 + 255) / 256; }
 
-// FP6 codes (M 3K/4 bytes, a multiple of 16), then the per-workgroup code sums int32 [M][blocks]
-size_t gemm_f4_workspace(int64_t M, int64_t K) {
+// Split over K where the 256 x 64 tiles leave most of the chip idle (down at 65-512 tokens: 16 x
+// ceil(M / 64) tiles of 56 steps): S ranges of at least kF4MinSteps steps, S the smallest count that
+// gives about kF4SplitTarget workgroups, and no more than kF4Resident (three workgroups on each of
+// the 256 CUs) so that the split grid is resident at once: with more, the partial sums' traffic (S M N
+// int32, written and read back) outweighs what the split hides (gate|up at 256 tokens, 448 tiles:
+// 47 -> 56 us at S = 2).  Down at 65-128 tokens: 78-81 -> 26-29 us.
+constexpr int64_t kF4SplitTarget = 512, kF4Resident = 768, kF4MinSteps = 4;
+struct F4Split {
+  int S = 1, us = 0;
+};
+inline F4Split f4_split_plan(int64_t N, int64_t M, int64_t K) {
+  F4Split p;
+  const int64_t tiles = ((N + 255) / 256) * ((M + 63) / 64), KT = (K + 255) / 256;
+  p.us = (int)KT;
+  int64_t S = (kF4SplitTarget + tiles - 1) / tiles;
+  if (S > kF4Resident / tiles) S = kF4Resident / tiles;
+  if (S > KT / kF4MinSteps) S = KT / kF4MinSteps;
+  if (S < 2) return p;
+  p.us = (int)((KT + S - 1) / S);
+  p.S = (int)((KT + p.us - 1) / p.us);
+  return p;
+}
+
+// FP6 codes (M 3K/4 bytes, a multiple of 16), then the per-workgroup code sums int32 [M][blocks];
+// split over K, the partial sums follow at the next multiple of 256 bytes.
+inline size_t f4_codes_bytes(int64_t M, int64_t K) {
   return (size_t)M * (size_t)(3 * (K / 4)) + (size_t)M * (size_t)act_fp6_blocks(K) * 4;
+}
+size_t gemm_f4_workspace(int64_t N, int64_t M, int64_t K) {
+  const F4Split p = f4_split_plan(N, M, K);
+  const size_t base = f4_codes_bytes(M, K);
+  return p.S > 1 ? (base + 255) / 256 * 256 + split::part_bytes(p.S, M, N) : base;
 }
 
 hipError_t launch_gemm_f4(int fmt, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
                           const int8_t* act_q, const float* sx, const int32_t* asum, int64_t M, uint16_t* y,
                           int32_t* acc_out, void* ws, hipStream_t s) {
+  if (fmt != FMT_POT && fmt != FMT_MNZ) return hipErrorInvalidValue;
   uint8_t* act6 = static_cast<uint8_t*>(ws);
   int32_t* psum = asum ? nullptr : reinterpret_cast<int32_t*>(act6 + (size_t)M * (size_t)(3 * (K / 4)));
   const int gx = (int)act_fp6_blocks(K);
@@ -253,15 +306,29 @@ hipError_t launch_gemm_f4(int fmt, const uint32_t* P, const uint16_t* sw, int64_
   hipLaunchKernelGGL(k_act_fp6, dim3((unsigned)gx, gy), dim3(256), 0, s, act_q, (int)M, (int)K, act6, psum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 grid((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64));
+  const F4Split p = f4_split_plan(N, M, K);
+  const dim3 grid((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64), (unsigned)p.S);
+  if (p.S > 1) {
+    int32_t* part = reinterpret_cast<int32_t*>(act6 + (f4_codes_bytes(M, K) + 255) / 256 * 256);
+    if (fmt == FMT_POT)
+      hipLaunchKernelGGL((k_gemm_f4<FMT_POT, 3, true>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum,
+                         psum, gx, (int)M, y, acc_out, p.us, part);
+    else
+      hipLaunchKernelGGL((k_gemm_f4<FMT_MNZ, 3, true>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum,
+                         psum, gx, (int)M, y, acc_out, p.us, part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // code sums of token m at psum[m gx + p]
+    return fmt == FMT_POT
+               ? split::launch_sum<FMT_POT>(part, p.S, M, N, sx, asum, psum, gx, gx, 1, sw, y, acc_out, s)
+               : split::launch_sum<FMT_MNZ>(part, p.S, M, N, sx, asum, psum, gx, gx, 1, sw, y, acc_out, s);
+  }
   if (fmt == FMT_POT)
-    hipLaunchKernelGGL((k_gemm_f4<FMT_POT, 3>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum, psum, gx,
-                       (int)M, y, acc_out);
-  else if (fmt == FMT_MNZ)
-    hipLaunchKernelGGL((k_gemm_f4<FMT_MNZ, 3>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum, psum, gx,
-                       (int)M, y, acc_out);
+    hipLaunchKernelGGL((k_gemm_f4<FMT_POT, 3, false>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum,
+                       psum, gx, (int)M, y, acc_out, 0, nullptr);
   else
-    return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_gemm_f4<FMT_MNZ, 3, false>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act6, sx, asum,
+                       psum, gx, (int)M, y, acc_out, 0, nullptr);
   return hipGetLastError();
 }
 

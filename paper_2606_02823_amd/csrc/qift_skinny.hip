@@ -20,11 +20,12 @@
 // that turns those loads into requests bounds this kernel (busy 81 % of the time for down at 64
 // tokens), so a linear with K > 4096 and few 16-row tiles (down) takes four tiles per workgroup and
 // gives each workgroup a range of K instead: workgroup (x, z) writes its int32 partial sums of tile
-// group x over unit range z to the workspace, and k_split_sum adds the ranges (integers: exact in any
+// group x over unit range z to the workspace, and the second pass (qift_split.h) adds the ranges (integers: exact in any
 // order) and applies the epilogue (down at 64 tokens: 28.9 -> 16.4 us).
 #include "qift_fwht.h"
 #include "qift_internal.h"
 #include "qift_mma.h"
+#include "qift_split.h"
 
 namespace qift {
 namespace {
@@ -212,31 +213,6 @@ __global__ __launch_bounds__(64 * kSkSlices) void k_skinny(const uint32_t* __res
   }
 }
 
-// The K-ranges of a split skinny linear added, then the epilogue: one thread per 4 outputs of a token.
-template <int FMT>
-__global__ __launch_bounds__(256) void k_split_sum(const int32_t* __restrict__ part, const int32_t* __restrict__ psum,
-                                                   int S, int M, int N, int np, const float* __restrict__ sx,
-                                                   const int32_t* __restrict__ asum, const uint16_t* __restrict__ sw,
-                                                   uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
-  const int nq = np / 4;
-  const int q = blockIdx.x * 256 + threadIdx.x;
-  if (q >= M * nq) return;
-  const int m = q / nq, n0 = (q - m * nq) * 4;
-  v4i D = v4i{0, 0, 0, 0};
-  for (int z = 0; z < S; ++z) {
-    const int4 v = *reinterpret_cast<const int4*>(part + ((size_t)z * M + m) * np + n0);
-    D += v4i{v.x, v.y, v.z, v.w};
-  }
-  int sq;
-  if (asum) {
-    sq = asum[m];
-  } else {
-    sq = 0;
-    for (int z = 0; z < S; ++z) sq += psum[z * M + m];
-  }
-  store4<FMT>(D, m, n0, N, sx[m], sq, sw, y, acc_out);
-}
-
 template <int FMT, int T, int TT, int U>
 hipError_t launch_sk(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act, const float* sx,
                      const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, hipStream_t s) {
@@ -321,9 +297,7 @@ inline SkSplit split_plan(int fmt, int64_t N, int64_t K, int64_t M) {
   return p;
 }
 
-inline size_t split_part_bytes(const SkSplit& p, int64_t M) {
-  return ((size_t)p.S * (size_t)M * (size_t)p.np * 4 + 255) / 256 * 256;
-}
+inline size_t split_part_bytes(const SkSplit& p, int64_t M, int64_t N) { return split::part_bytes(p.S, M, N); }
 
 template <int FMT, int T, int TT>
 hipError_t launch_split_t(const SkSplit& p, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
@@ -337,17 +311,15 @@ hipError_t launch_split_t(const SkSplit& p, const uint32_t* P, const uint16_t* s
     if (attr != hipSuccess) return attr;
   }
   int32_t* part = static_cast<int32_t*>(ws);
-  int32_t* psum = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + split_part_bytes(p, M));
+  int32_t* psum = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + split_part_bytes(p, M, N));
   const int64_t tiles = (N + 15) / 16;
   hipLaunchKernelGGL((k_skinny<FMT, T, TT, 2, true>), dim3((unsigned)((tiles + T - 1) / T), (unsigned)p.S),
                      dim3(64 * kSkSlices), shmem, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M, y, acc_out, p.us,
                      p.np, part, psum);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t quads = M * (p.np / 4);
-  hipLaunchKernelGGL((k_split_sum<FMT>), dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s, part, psum, p.S,
-                     (int)M, (int)N, p.np, sx, asum, sw, y, acc_out);
-  return hipGetLastError();
+  // code sums of range z at psum[z M + m]
+  return split::launch_sum<FMT>(part, p.S, M, N, sx, asum, psum, p.S, 1, (int)M, sw, y, acc_out, s);
 }
 
 template <int FMT>
@@ -369,7 +341,7 @@ size_t skinny_workspace(int fmt, int64_t N, int64_t K, int64_t M) {
   }
   const SkSplit p = split_plan(fmt, N, K, M);
   if (p.S == 0) return 0;
-  return split_part_bytes(p, M) + (size_t)p.S * (size_t)M * 4;
+  return split_part_bytes(p, M, N) + (size_t)p.S * (size_t)M * 4;
 }
 
 hipError_t launch_skinny_ws(int fmt, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,

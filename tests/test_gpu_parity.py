@@ -129,11 +129,14 @@ def test_linear_ragged(Q, fmt, M):
 
 
 @pytest.mark.parametrize("fmt", [levels.FMT_W2_MNZ, levels.FMT_W2_POT])
-@pytest.mark.parametrize("M,K", [(65, 1088), (130, 1088), (300, 4096), (200, 14336)])
+@pytest.mark.parametrize("M,K", [(65, 1088), (130, 1088), (300, 4096), (200, 14336), (96, 4160)])
 def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, K):
     # W2 (MNZ, PoT) at M > 64: the int8 GEMM (no workspace) and the FP4 x FP6 GEMM (FP6 activations
     # in a workspace of workspace_bytes; the MNZ codes as c / 2, the PoT levels +-1, +-4 as E2M1
-    # values), ragged rows and tokens, K with a partial last step: both bit-identical to the oracle
+    # values), ragged rows and tokens, K with a partial last step: both bit-identical to the oracle.
+    # 1000 rows make 4 x ceil(M / 64) tiles, so from K = 1024 on (4 steps of 256 k per range) the FP4
+    # GEMM is split over K (int32 partial sums after the FP6 codes, ranges added by a second pass);
+    # K = 4160 has 17 steps: ranges of 5, 5, 5 and 2, the last one ending in a partial step.
     N, b = 1000, 64
     L = synth.draw_levels(fmt, N, K, cfg=97, layer=M + fmt)
     s_w = synth.draw_scales(fmt, N, cfg=97, layer=M + fmt)
@@ -141,7 +144,14 @@ def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, K):
     pk = pack_dev(Q, L, s_w, fmt)
     act = Q.rotate_quant_act(dev(x), b)
     q_ref, sx_ref = check_act(act, x, b)
-    assert Q.workspace_bytes(pk, M) == M * 3 * (K // 4) + 4 * M * (-(-(K // 32) // 256))
+    codes = M * 3 * (K // 4) + 4 * M * (-(-(K // 32) // 256))
+    KT, tiles = -(-K // 256), 4 * -(-M // 64)
+    S = min(-(-512 // tiles), 768 // tiles, KT // 4)
+    if S >= 2:
+        us = -(-KT // S)
+        S = -(-KT // us)
+        codes = -(-codes // 256) * 256 + -(-(S * M * N * 4) // 256) * 256
+    assert Q.workspace_bytes(pk, M) == codes
     for ws in (None, torch.empty(Q.workspace_bytes(pk, M), dtype=torch.uint8, device="cuda")):
         for use_sum in (False, True):
             y, acc = run_linear(Q, pk, act, M, N, use_sum=use_sum, workspace=ws)
