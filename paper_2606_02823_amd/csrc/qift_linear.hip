@@ -343,7 +343,7 @@ __device__ __forceinline__ v4i gemm_operand(const uint4& u, int s) {
 // ===========================================================================
 // With SUMQ (no per-token sums given) wave w also adds up the codes of token tiles t = w (mod 4): one
 // more 16-byte LDS read and four dot products per MFMA operand step of its own tile(s).
-template <int FMT, int OCC, int TT, bool SUMQ>
+template <int FMT, int OCC, int TT, bool SUMQ, int NS>
 __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                    int N, int K, const int8_t* __restrict__ act,
                                                    const float* __restrict__ sx, const int32_t* __restrict__ asum,
@@ -359,6 +359,9 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
   // the direct-to-LDS loads into one never alias the operand reads from the other
   __shared__ __align__(16) int8_t lds0[BM * BK];
   __shared__ __align__(16) int8_t lds1[BM * BK];
+  __shared__ __align__(16) int8_t lds2[NS == 3 ? BM * BK : 16];
+  static_assert(NS == 2 || NS == 3, "pipeline depth");
+  constexpr int NL = NQ + 4;   // vector-memory loads a wave issues per step
 
   // the wave index as a scalar, so that the LDS destinations of the direct-to-LDS loads are scalar too
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -421,15 +424,20 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
 #pragma unroll
   for (int t4 = 0; t4 < TT / 4; ++t4) sq[t4] = 0;
 
-  // one step: prefetch step kt+1 (activations into lds[buf ^ 1], weights into wn), MFMAs of step kt
-  // from lds[buf] and wc; the k loop is unrolled by two so the weight registers alternate instead of
-  // being copied.  MFMA s of lane group g covers k = kt BK + 16 (S g + s) .. + 15 (slot S g + s).
-  auto step = [&](int kt, const int8_t* tileb, int8_t* nextb, const uint4 (&wc)[4], uint4 (&wn)[4]) {
-    const bool more = kt + 1 < KT;
+  // one step: prefetch step kt + NS - 1 (activations into pfb, weights into wpf), MFMAs of step kt from
+  // tileb and wc; the k loop is unrolled by NS so the weight registers rotate instead of being copied.
+  // MFMA s of lane group g covers k = kt BK + 16 (S g + s) .. + 15 (slot S g + s).
+  // With three stages the prefetch is issued on every step, past K too (activation loads out of range,
+  // weight loads of bytes no MFMA uses), so that every path issues the same loads and the compiler's
+  // wait counts stay exact across the loop.
+  auto step = [&](int kt, const int8_t* tileb, int8_t* pfb, const uint4 (&wc)[4], uint4 (&wpf)[4]) {
+    const bool more = NS == 3 || kt + 1 < KT;
     if (more) {
-      issue_a(kt + 1, nextb);   // the other buffer: every wave finished reading it before the last barrier
-      load_w(wn, kt + 1);
+      issue_a(kt + NS - 1, pfb);   // a buffer every wave finished reading before the last barrier
+      load_w(wpf, kt + NS - 1);
     }
+    // the loads stay ahead of the step's MFMAs (unguarded, the scheduler sinks them to the barrier)
+    if constexpr (NS == 3) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s = 0; s < S; ++s) {
       v4i a[4];
@@ -452,19 +460,50 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
         }
       }
     }
-    // this wave's loads of step kt+1 have landed (vmcnt(0) with lgkmcnt and expcnt untouched)
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    __syncthreads();
+    // this wave's loads of step kt+1 have landed (vmcnt with lgkmcnt and expcnt untouched): with three
+    // stages the NL loads of step kt+2 just issued may still be in flight
+    if constexpr (NS == 3) {
+      // a bare barrier (a workgroup fence would also wait for the loads of step kt+2 into LDS), after
+      // this wave's operand reads of step kt have returned: the buffer is refilled from the next step on
+      __builtin_amdgcn_s_waitcnt(0x0070 | NL);   // vmcnt(NL) lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
+    } else {
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+      __syncthreads();
+    }
   };
 
-  uint4 wa[4], wb[4];
-  issue_a(0, lds0);
-  load_w(wa, 0);
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-  __syncthreads();
-  for (int kt = 0; kt < KT; kt += 2) {
-    step(kt, lds0, lds1, wa, wb);
-    if (kt + 1 < KT) step(kt + 1, lds1, lds0, wb, wa);
+  if constexpr (NS == 2) {
+    uint4 wa[4], wb[4];
+    issue_a(0, lds0);
+    load_w(wa, 0);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+    for (int kt = 0; kt < KT; kt += 2) {
+      step(kt, lds0, lds1, wa, wb);
+      if (kt + 1 < KT) step(kt + 1, lds1, lds0, wb, wa);
+    }
+  } else {
+    uint4 w0[4], w1[4], w2[4];
+    issue_a(0, lds0);
+    load_w(w0, 0);
+    issue_a(1, lds1);
+    load_w(w1, 1);
+    __builtin_amdgcn_s_waitcnt(0x0F70 | NL);   // step 0's loads
+    __syncthreads();
+    // a loop body without conditions (the wait counts carried round the loop stay exact), then the
+    // last one or two steps
+    int kt = 0;
+    for (; kt + 3 <= KT; kt += 3) {
+      step(kt, lds0, lds2, w0, w2);
+      step(kt + 1, lds1, lds0, w1, w0);
+      step(kt + 2, lds2, lds1, w2, w1);
+    }
+    if (kt < KT) step(kt, lds0, lds2, w0, w2);
+    if (kt + 1 < KT) step(kt + 1, lds1, lds0, w1, w0);
+    // the prefetches past K have landed before any buffer is reused
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
   }
 
   // per-token sums: the four lane groups of a token add up, then the waves exchange them through
@@ -495,6 +534,15 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
+// GEMM pipeline depth and workgroups per CU of the 256 x 64 tiles, per weight format.  W4 steps over
+// 128 k (half the MFMAs of a W2 step), so one step ahead does not cover its loads: three stages at two
+// workgroups per CU (M = 512: down 111 -> 72 us, gate|up 104 -> 90, q|k|v 36 -> 30; M = 2048 within
+// 3 %).  W2 at three stages needs two workgroups per CU too, and loses more to that than it gains
+// (gate|up at M = 2048 254 -> 285 us).
+template <int FMT>
+constexpr int gemm_stages() { return FMT == FMT_W4 ? 3 : 2; }
+template <int FMT>
+constexpr int gemm_occ() { return FMT == FMT_W4 ? 2 : 3; }
 constexpr int kDecodeMaxLds = 96 * 1024;   // activation bytes staged in LDS by the decode kernel
 constexpr int kDecodeGrid = 512;           // workgroups of the decode kernel (2 per CU)
 
@@ -584,7 +632,7 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
     return launch_decode<FMT>(P, sw, N, K, act, sx, asum, M, y, acc_out, s);
   }
   const unsigned gx = (unsigned)((N + 255) / 256);
-  // 256 x 64 tiles, three workgroups per CU.  W4 on grids that fill the chip at least twice over with
+  // 256 x 64 tiles (gemm_occ, gemm_stages).  W4 on grids that fill the chip at least twice over with
   // 256 x 128 tiles (two per CU) takes those instead: half the weight loads and decode per MFMA
   // (stacked gate|up at M = 2048: 318 -> 264 us).  W2 does not gain from them (222 -> 225 us), and
   // smaller grids lose to the idle CUs (q,k,v W4 74 -> 78 us).  Also measured slower at M = 2048: 256 x 32 tiles and activations staged through
@@ -593,20 +641,20 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
     const unsigned gy8 = (unsigned)((M + 127) / 128);
     if ((uint64_t)gx * gy8 >= 1024) {
       if (asum)
-        hipLaunchKernelGGL((k_gemm<FMT, 2, 8, false>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx,
+        hipLaunchKernelGGL((k_gemm<FMT, 2, 8, false, 2>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx,
                            asum, (int)M, y, acc_out);
       else
-        hipLaunchKernelGGL((k_gemm<FMT, 2, 8, true>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx,
+        hipLaunchKernelGGL((k_gemm<FMT, 2, 8, true, 2>), dim3(gx, gy8), dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx,
                            asum, (int)M, y, acc_out);
       return hipGetLastError();
     }
   }
   const dim3 grid(gx, (unsigned)((M + 63) / 64));
   if (asum)
-    hipLaunchKernelGGL((k_gemm<FMT, 3, 4, false>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M,
+    hipLaunchKernelGGL((k_gemm<FMT, gemm_occ<FMT>(), 4, false, gemm_stages<FMT>()>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M,
                        y, acc_out);
   else
-    hipLaunchKernelGGL((k_gemm<FMT, 3, 4, true>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M,
+    hipLaunchKernelGGL((k_gemm<FMT, gemm_occ<FMT>(), 4, true, gemm_stages<FMT>()>), grid, dim3(256), 0, s, P, sw, (int)N, (int)K, act, sx, asum, (int)M,
                        y, acc_out);
   return hipGetLastError();
 }

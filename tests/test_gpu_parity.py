@@ -434,6 +434,25 @@ def test_cfg4_row_concatenated(Q, fmt):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("K", [64, 128, 320, 512, 576, 896])
+def test_gemm_pipeline_tails(Q, fmt, K):
+    # the prefill GEMM (M > 64, no workspace) over every count of k-steps that ends its pipeline
+    # differently: W4 steps over 128 k with three stages (1, 1, 3, 4, 5, 7 steps: the unrolled loop
+    # body, then one or two more, the last step partial at K = 64, 320, 576), W2 over 256 k with two
+    # (1, 1, 2, 2, 3, 4 steps); 300 rows and 200 tokens leave partial tiles both ways
+    N, M = 300, 200
+    L = synth.draw_levels(fmt, N, K, cfg=96, layer=K)
+    s_w = synth.draw_scales(fmt, N, cfg=96, layer=K)
+    x = synth.activations_fp16(96, K, 0, M, K, 7, 30.0)
+    pk = pack_dev(Q, L, s_w, fmt)
+    act = Q.rotate_quant_act(dev(x), 64)
+    q_ref, sx_ref = check_act(act, x, 64)
+    for use_sum in (False, True):
+        y, acc = run_linear(Q, pk, act, M, N, use_sum=use_sum)
+        check_linear(y, acc, L, q_ref, sx_ref, s_w)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
 def test_linear_wide_grid_ragged(Q, fmt):
     # a grid wide enough for the 128-token W4 tiles, with ragged rows, tokens and a half k-step
     N, K, b, M = 16400, 1088, 64, 2000
