@@ -350,7 +350,10 @@ int qift_w2a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float
 int qift_w2a4_lut_linear(const qift_packed_w *w, const uint16_t *lut, const int8_t *act_q,
                          const float *act_scale, int64_t M, uint16_t *out, qift_stream_t stream);
 
-/* The W4 sibling (fmt QIFT_W4_SYM); same arguments and results. */
+/* The W4 sibling (fmt QIFT_W4_SYM); same arguments and results.  The workspace of the _ex call is
+ * used above 64 tokens where qift_workspace_bytes is not 0: the int8 prefill GEMM, whose 256-row x
+ * 64-token tiles are then few (down at 65-512 tokens), is split over K into int32 partial sums in it,
+ * then the ranges are added and the epilogue applied (bit-identical). */
 int qift_w4a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
                      int64_t M, uint16_t *out, qift_stream_t stream);
 int qift_w4a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
@@ -561,14 +564,17 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
                                       const uint8_t *v_zeros, uint16_t *out, qift_stream_t stream);
 
 /* Workspace bytes that the _ex calls use for this weight and M, 0 where none is used (host
- * query).  MNZ and PoT weights only.  At M > 64 the FP4 x FP6 prefill kernel's: M * 3K/4 bytes of FP6
+ * query).  MNZ and PoT weights: at M > 64 the FP4 x FP6 prefill kernel's: M * 3K/4 bytes of FP6
  * codes and M * ceil(K / 8192) int32 code sums; where its T = ceil(N / 256) * ceil(M / 64) tiles are
  * few, split over S = min(ceil(512 / T), floor(768 / T), floor(ceil(K / 256) / 4)) K-ranges when that
  * is at least 2, followed (at the next multiple of 256 bytes) by S * M * N4 int32 partial sums (N4 =
  * N rounded up to 4; S recounted after the ranges are sized).  At M <= 64 the decode linear split
  * over K, where it applies (K > 4096 and at most 680 16-row tiles, N <= 10880; up to 16 tokens only
  * where the codes exceed the decode kernel's LDS): S * M * N4 int32 partial sums (256-byte aligned)
- * and S * M int32 code sums, S the number of K-ranges. */
+ * and S * M int32 code sums, S the number of K-ranges.  W4 weights at M > 64: the int8 GEMM split over
+ * S = min(ceil(512 / T), floor(512 / T), floor(ceil(K / 128) / 8)) K-ranges when that is at least 3
+ * (T tiles as above; S recounted after the ranges are sized), S * M * N4 int32 partial sums (256-byte
+ * aligned) and S * M int32 code sums; 0 otherwise. */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);
 
 /* Static text for a status code. */

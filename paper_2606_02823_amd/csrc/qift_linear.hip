@@ -4,6 +4,7 @@
 #include "qift_fwht.h"   // buffer-load helpers
 #include "qift_internal.h"
 #include "qift_mma.h"
+#include "qift_split.h"
 
 namespace qift {
 namespace {
@@ -343,11 +344,16 @@ __device__ __forceinline__ v4i gemm_operand(const uint4& u, int s) {
 // ===========================================================================
 // With SUMQ (no per-token sums given) wave w also adds up the codes of token tiles t = w (mod 4): one
 // more 16-byte LDS read and four dot products per MFMA operand step of its own tile(s).
-template <int FMT, int OCC, int TT, bool SUMQ, int NS>
+// SPLIT (three stages only): workgroup z of the grid's third dimension takes the steps [z us, (z + 1) us)
+// and writes its int32 accumulators to part [z][M][N rounded up to 4] (and, with SUMQ, workgroup column
+// 0 its range's code sums to psum [z][M]) instead of the outputs.
+template <int FMT, int OCC, int TT, bool SUMQ, int NS, bool SPLIT = false>
 __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ P, const uint16_t* __restrict__ sw,
                                                    int N, int K, const int8_t* __restrict__ act,
                                                    const float* __restrict__ sx, const int32_t* __restrict__ asum,
-                                                   int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out) {
+                                                   int M, uint16_t* __restrict__ y, int32_t* __restrict__ acc_out,
+                                                   int us = 0, int32_t* __restrict__ part = nullptr,
+                                                   int32_t* __restrict__ psum = nullptr) {
   constexpr int S = gemm_ops<FMT>();
   constexpr int BK = gemm_bk<FMT>();
   constexpr int SL = BK / 16;            // 16-byte slots per activation row
@@ -361,6 +367,7 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
   __shared__ __align__(16) int8_t lds1[BM * BK];
   __shared__ __align__(16) int8_t lds2[NS == 3 ? BM * BK : 16];
   static_assert(NS == 2 || NS == 3, "pipeline depth");
+  static_assert(!SPLIT || NS == 3, "a split runs three stages");
   constexpr int NL = NQ + 4;   // vector-memory loads a wave issues per step
 
   // the wave index as a scalar, so that the LDS destinations of the direct-to-LDS loads are scalar too
@@ -369,7 +376,9 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
   const int n_base = blockIdx.x * 256 + wave * 64;
   const int m_base = blockIdx.y * BM;
   const int64_t rowbytes = FMT == FMT_W4 ? (int64_t)K / 2 : (int64_t)K / 4;
-  const int KT = (K + BK - 1) / BK;
+  const int KA = (K + BK - 1) / BK;
+  const int kt0 = SPLIT ? (int)blockIdx.z * us : 0;
+  const int KT = SPLIT ? (kt0 + us < KA ? kt0 + us : KA) : KA;   // steps past this workgroup's range
 
   const __amdgpu_buffer_rsrc_t wrs = dev::make_rsrc(P, (uint32_t)(N * rowbytes));
   // Load offsets are a per-lane base (the out-of-range offset for rows past N, which stays out of
@@ -485,15 +494,15 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
     }
   } else {
     uint4 w0[4], w1[4], w2[4];
-    issue_a(0, lds0);
-    load_w(w0, 0);
-    issue_a(1, lds1);
-    load_w(w1, 1);
+    issue_a(kt0, lds0);
+    load_w(w0, kt0);
+    issue_a(kt0 + 1, lds1);
+    load_w(w1, kt0 + 1);
     __builtin_amdgcn_s_waitcnt(0x0F70 | NL);   // step 0's loads
     __syncthreads();
     // a loop body without conditions (the wait counts carried round the loop stay exact), then the
     // last one or two steps
-    int kt = 0;
+    int kt = kt0;
     for (; kt + 3 <= KT; kt += 3) {
       step(kt, lds0, lds2, w0, w2);
       step(kt + 1, lds1, lds0, w1, w0);
@@ -519,6 +528,24 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(const uint32_t* __restrict__ 
     }
     __syncthreads();
   }
+  if constexpr (SPLIT) {
+    const int np = (N + 3) & ~3;
+#pragma unroll
+    for (int t = 0; t < TT; ++t) {
+      const int m = m_base + 16 * t + r16;
+      if (m < M) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n0 = n_base + 16 * j + 4 * g;
+          if (n0 < N)
+            *reinterpret_cast<int4*>(part + ((size_t)blockIdx.z * M + m) * np + n0) =
+                make_int4(acc[j][t][0], acc[j][t][1], acc[j][t][2], acc[j][t][3]);
+        }
+        if (SUMQ && blockIdx.x == 0 && wave == 0 && g == 0) psum[(size_t)blockIdx.z * M + m] = s_q[16 * t + r16];
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int t = 0; t < TT; ++t) {
     const int m = m_base + 16 * t + r16;
@@ -543,6 +570,45 @@ template <int FMT>
 constexpr int gemm_stages() { return FMT == FMT_W4 ? 3 : 2; }
 template <int FMT>
 constexpr int gemm_occ() { return FMT == FMT_W4 ? 2 : 3; }
+// W4 above 64 tokens with a workspace, where the 256 x 64 tiles are few (down at 65-512 tokens: 16 x
+// ceil(M / 64) tiles of 112 steps): split over K like the FP4 x FP6 kernel, S ranges of at least 8
+// steps of 128 k, about 512 workgroups and no more than are resident at once (two per CU), and at
+// least three ranges (two measured no faster: gate|up at 128 tokens 31.1 -> 33.4 us, q|k|v at 512
+// 30.0 -> 32.4).  Down at 65 / 128 / 512 tokens: 71.9 / 72.5 / 74.8 -> 22.1 / 25.0 / 46.6 us; q|k|v
+// and o at 65: 26.6 -> 11.3 / 10.9.
+constexpr int64_t kW4SplitTarget = 512, kW4Resident = 512, kW4MinSteps = 8;
+struct GemmSplit {
+  int S = 1, us = 0;
+};
+inline GemmSplit w4_split_plan(int64_t N, int64_t M, int64_t K) {
+  GemmSplit p;
+  const int64_t tiles = ((N + 255) / 256) * ((M + 63) / 64), KT = (K + 127) / 128;
+  p.us = (int)KT;
+  if (M < kGemmF4MinM) return p;
+  int64_t S = (kW4SplitTarget + tiles - 1) / tiles;
+  if (S > kW4Resident / tiles) S = kW4Resident / tiles;
+  if (S > KT / kW4MinSteps) S = KT / kW4MinSteps;
+  if (S < 3) return p;
+  p.us = (int)((KT + S - 1) / S);
+  p.S = (int)((KT + p.us - 1) / p.us);
+  return p;
+}
+
+template <bool SUMQ>
+hipError_t launch_w4_split(const GemmSplit& p, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
+                           const int8_t* act, const float* sx, const int32_t* asum, int64_t M, uint16_t* y,
+                           int32_t* acc_out, void* ws, hipStream_t s) {
+  int32_t* part = static_cast<int32_t*>(ws);
+  int32_t* psum = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + split::part_bytes(p.S, M, N));
+  const dim3 grid((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64), (unsigned)p.S);
+  hipLaunchKernelGGL((k_gemm<FMT_W4, gemm_occ<FMT_W4>(), 4, SUMQ, 3, true>), grid, dim3(256), 0, s, P, sw, (int)N,
+                     (int)K, act, sx, asum, (int)M, y, acc_out, p.us, part, psum);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // code sums of range z at psum[z M + m]
+  return split::launch_sum<FMT_W4>(part, p.S, M, N, sx, asum, psum, p.S, 1, (int)M, sw, y, acc_out, s);
+}
+
 constexpr int kDecodeMaxLds = 96 * 1024;   // activation bytes staged in LDS by the decode kernel
 constexpr int kDecodeGrid = 512;           // workgroups of the decode kernel (2 per CU)
 
@@ -607,6 +673,13 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
                       hipStream_t s) {
   if constexpr (FMT != FMT_W4) {
     if (ws && M >= kGemmF4MinM) return launch_gemm_f4(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
+  } else {
+    if (ws && M >= kGemmF4MinM) {
+      const GemmSplit p = w4_split_plan(N, M, K);
+      if (p.S > 1)
+        return asum ? launch_w4_split<false>(p, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s)
+                    : launch_w4_split<true>(p, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
+    }
   }
   // 17..64 tokens: the skinny kernel, one pass over the weights (the codes of that many tokens do not
   // fit the decode kernel's LDS, and the GEMM's grid of N/256 workgroups would leave most CUs idle)
@@ -661,6 +734,11 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
 
 }  // namespace
 
+size_t w4_gemm_workspace(int64_t N, int64_t M, int64_t K) {
+  const GemmSplit p = w4_split_plan(N, M, K);
+  return p.S > 1 ? split::part_bytes(p.S, M, N) + (size_t)p.S * (size_t)M * 4 : 0;
+}
+
 hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
                          uint16_t* out, int32_t* acc_out, void* ws, hipStream_t s) {
@@ -670,7 +748,7 @@ hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales
     case FMT_POT:
       return launch_fmt<FMT_POT>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, ws, s);
     case FMT_W4:
-      return launch_fmt<FMT_W4>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, nullptr, s);
+      return launch_fmt<FMT_W4>(packed, scales, N, K, act_q, act_scale, act_sum, M, out, acc_out, ws, s);
     default: return hipErrorInvalidValue;
   }
 }

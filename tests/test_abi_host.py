@@ -262,6 +262,14 @@ def test_linear_validation(L):
     assert W(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 2048) == 2048 * 10752 + 2048 * 2 * 4
     # ragged: 1000 rows (N4 = 1000), K = 4160 (17 steps, S = 4 of 5, 5, 5, 2), 96 tokens
     assert W(P(_pw(fmt=qift.W2_POT, N=1000, K=4160)), 96) == 300032 + 4 * 96 * 1000 * 4
+    # W4 above 64 tokens: the int8 GEMM split over K where its tiles are few, S ranges of at least 8
+    # steps of 128 k, S = min(ceil(512 / tiles), 512 // tiles, steps // 8) when >= 3: S M N4 int32
+    # partial sums (256-byte aligned), then S M int32 code sums
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 128) == 14 * 128 * 4096 * 4 + 14 * 128 * 4
+    assert W(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 65) == 0        # 224 tiles: S = 2
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=4096)), 512) == 4 * 512 * 4096 * 4 + 4 * 512 * 4
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 2048) == 0
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 64) == 0
     # FP6 codes (M 3K/4 bytes), then one int32 code sum per token and 256 groups of 32 k
     need = 100 * 3 * (K // 4) + 100 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 100) == need

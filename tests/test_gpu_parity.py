@@ -158,6 +158,38 @@ def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, K):
             check_linear(y, acc, L, q_ref, sx_ref, s_w)
 
 
+@pytest.mark.parametrize("M,N,K", [(65, 300, 4160), (200, 300, 4160), (128, 1000, 14336), (96, 4096, 1088),
+                                   (130, 2064, 8192)])
+def test_w4_prefill_split_over_k(Q, M, N, K):
+    # W4 above 64 tokens with a workspace of workspace_bytes: where the 256 x 64 tiles are few the int8
+    # GEMM is split over K (S >= 3 ranges of at least 8 steps of 128 k, about 512 workgroups, at most 512):
+    # K = 4160 has 33 steps (ranges of 9, 9, 9 and 6, the last step partial); K = 1088 has 9 steps, too
+    # few to split (workspace_bytes 0).  Bit-identical to the oracle and to the call without a
+    # workspace, with and without the quantizer's code sums.
+    fmt = levels.FMT_W4_SYM
+    L = synth.draw_levels(fmt, N, K, cfg=95, layer=M)
+    s_w = synth.draw_scales(fmt, N, cfg=95, layer=M)
+    x = synth.activations_fp16(95, M, 0, M, K, 9, 30.0)
+    pk = pack_dev(Q, L, s_w, fmt)
+    act = Q.rotate_quant_act(dev(x), 64)
+    q_ref, sx_ref = check_act(act, x, 64)
+    KT, tiles = -(-K // 128), -(-N // 256) * -(-M // 64)
+    S = min(-(-512 // tiles), 512 // tiles, KT // 8)
+    need = Q.workspace_bytes(pk, M)
+    if S >= 3:
+        us = -(-KT // S)
+        S = -(-KT // us)
+        assert need == -(-(S * M * (-(-N // 4) * 4) * 4) // 256) * 256 + S * M * 4
+    else:
+        assert need == 0
+    ws = torch.empty(max(need, 16), dtype=torch.uint8, device="cuda")
+    for use_sum in (False, True):
+        y, acc = run_linear(Q, pk, act, M, N, use_sum=use_sum, workspace=ws if need else None)
+        check_linear(y, acc, L, q_ref, sx_ref, s_w)
+        y0, acc0 = run_linear(Q, pk, act, M, N, use_sum=use_sum)
+        assert torch.equal(acc, acc0) and torch.equal(y.view(torch.int16), y0.view(torch.int16))
+
+
 @pytest.mark.parametrize("fmt", [levels.FMT_W2_MNZ, levels.FMT_W2_POT])
 @pytest.mark.parametrize("M,N,K", [(17, 1000, 1088), (32, 1000, 14336), (33, 4096, 4096), (64, 1000, 14336),
                                    (64, 4096, 14336), (20, 2064, 8192), (40, 300, 16384), (64, 6144, 4096),
