@@ -47,10 +47,10 @@ hipError_t launch_rotate_quant_act(const uint16_t* x, int64_t M, int64_t K, int 
                                    int clip_den, int8_t* act_q, float* act_scale, int32_t* act_sum,
                                    hipStream_t s, bool bf16 = false);   // x fp16, or bf16 bits
 
-// Quantized linear (qift_linear.hip).  fmt selects the decode.  ws (nullable) holds at least
-// gemm_f4_workspace(N, M, K) bytes: with it, MNZ and PoT weights at M > 64 run the FP4 x FP6 MFMA kernel;
-// W4 weights at M > 64 with w4_gemm_workspace(N, M, K) bytes (0: none used) the int8 GEMM split over K.
-size_t w4_gemm_workspace(int64_t N, int64_t M, int64_t K);
+// Quantized linear (qift_linear.hip).  fmt selects the decode.  ws (nullable): at M > 64 the GEMM split
+// over K where gemm_split_workspace(fmt, N, M, K) (its bytes) is not 0, else for MNZ and PoT weights the
+// FP4 x FP6 MFMA kernel with gemm_f4_workspace(N, M, K) bytes.
+size_t gemm_split_workspace(int fmt, int64_t N, int64_t M, int64_t K);
 hipError_t launch_linear(int fmt, const uint32_t* packed, const uint16_t* scales, int64_t N, int64_t K,
                          const int8_t* act_q, const float* act_scale, const int32_t* act_sum, int64_t M,
                          uint16_t* out, int32_t* acc_out, void* ws, hipStream_t s);

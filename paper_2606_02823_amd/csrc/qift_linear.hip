@@ -570,43 +570,47 @@ template <int FMT>
 constexpr int gemm_stages() { return FMT == FMT_W4 ? 3 : 2; }
 template <int FMT>
 constexpr int gemm_occ() { return FMT == FMT_W4 ? 2 : 3; }
-// W4 above 64 tokens with a workspace, where the 256 x 64 tiles are few (down at 65-512 tokens: 16 x
-// ceil(M / 64) tiles of 112 steps): split over K like the FP4 x FP6 kernel, S ranges of at least 8
-// steps of 128 k, about 512 workgroups and no more than are resident at once (two per CU), and at
-// least three ranges (two measured no faster: gate|up at 128 tokens 31.1 -> 33.4 us, q|k|v at 512
-// 30.0 -> 32.4).  Down at 65 / 128 / 512 tokens: 71.9 / 72.5 / 74.8 -> 22.1 / 25.0 / 46.6 us; q|k|v
-// and o at 65: 26.6 -> 11.3 / 10.9.
-constexpr int64_t kW4SplitTarget = 512, kW4Resident = 512, kW4MinSteps = 8;
+// Above 64 tokens with a workspace, where the 256 x 64 tiles are few (down at 65-512 tokens: 16 x
+// ceil(M / 64) tiles, each a chain of 56 W2 or 112 W4 steps whose loads are not hidden), the GEMM is
+// split over K at three stages and two workgroups per CU: S ranges of at least 4 W2 or 8 W4 steps
+// (1024 k), about 512 workgroups and no more than are resident at once.  W2 (at 65 / 128 / 1024
+// tokens): down 78.3 / 81.0 / 98.7 -> 19.6 / 23.8 / 63.1 us, q|k|v 35.1 -> 11.6 at 65, o 35.3 -> 11.1;
+// it replaces the FP4 x FP6 kernel split the same way (down 25.4 / 29.4 / 80.3 us: the FP6 re-coding
+// is a launch of its own).  W4 takes at least three ranges (two measured no faster: gate|up at 128
+// tokens 31.1 -> 33.4 us, q|k|v at 512 30.0 -> 32.4): down at 65 / 128 / 512 tokens 71.9 / 72.5 /
+// 74.8 -> 22.1 / 25.0 / 46.6 us, q|k|v and o at 65 26.6 -> 11.3 / 10.9.
+constexpr int64_t kSplitTarget = 512, kSplitResident = 512;
 struct GemmSplit {
   int S = 1, us = 0;
 };
-inline GemmSplit w4_split_plan(int64_t N, int64_t M, int64_t K) {
+inline GemmSplit gemm_split_plan(int fmt, int64_t N, int64_t M, int64_t K) {
   GemmSplit p;
-  const int64_t tiles = ((N + 255) / 256) * ((M + 63) / 64), KT = (K + 127) / 128;
+  const int64_t bk = fmt == FMT_W4 ? 128 : 256, min_steps = fmt == FMT_W4 ? 8 : 4, min_s = fmt == FMT_W4 ? 3 : 2;
+  const int64_t tiles = ((N + 255) / 256) * ((M + 63) / 64), KT = (K + bk - 1) / bk;
   p.us = (int)KT;
   if (M < kGemmF4MinM) return p;
-  int64_t S = (kW4SplitTarget + tiles - 1) / tiles;
-  if (S > kW4Resident / tiles) S = kW4Resident / tiles;
-  if (S > KT / kW4MinSteps) S = KT / kW4MinSteps;
-  if (S < 3) return p;
+  int64_t S = (kSplitTarget + tiles - 1) / tiles;
+  if (S > kSplitResident / tiles) S = kSplitResident / tiles;
+  if (S > KT / min_steps) S = KT / min_steps;
+  if (S < min_s) return p;
   p.us = (int)((KT + S - 1) / S);
   p.S = (int)((KT + p.us - 1) / p.us);
   return p;
 }
 
-template <bool SUMQ>
-hipError_t launch_w4_split(const GemmSplit& p, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
+template <int FMT, bool SUMQ>
+hipError_t launch_gemm_split(const GemmSplit& p, const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K,
                            const int8_t* act, const float* sx, const int32_t* asum, int64_t M, uint16_t* y,
                            int32_t* acc_out, void* ws, hipStream_t s) {
   int32_t* part = static_cast<int32_t*>(ws);
   int32_t* psum = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + split::part_bytes(p.S, M, N));
   const dim3 grid((unsigned)((N + 255) / 256), (unsigned)((M + 63) / 64), (unsigned)p.S);
-  hipLaunchKernelGGL((k_gemm<FMT_W4, gemm_occ<FMT_W4>(), 4, SUMQ, 3, true>), grid, dim3(256), 0, s, P, sw, (int)N,
+  hipLaunchKernelGGL((k_gemm<FMT, 2, 4, SUMQ, 3, true>), grid, dim3(256), 0, s, P, sw, (int)N,
                      (int)K, act, sx, asum, (int)M, y, acc_out, p.us, part, psum);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // code sums of range z at psum[z M + m]
-  return split::launch_sum<FMT_W4>(part, p.S, M, N, sx, asum, psum, p.S, 1, (int)M, sw, y, acc_out, s);
+  return split::launch_sum<FMT>(part, p.S, M, N, sx, asum, psum, p.S, 1, (int)M, sw, y, acc_out, s);
 }
 
 constexpr int kDecodeMaxLds = 96 * 1024;   // activation bytes staged in LDS by the decode kernel
@@ -671,15 +675,14 @@ template <int FMT>
 hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
                       const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
                       hipStream_t s) {
-  if constexpr (FMT != FMT_W4) {
-    if (ws && M >= kGemmF4MinM) return launch_gemm_f4(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
-  } else {
-    if (ws && M >= kGemmF4MinM) {
-      const GemmSplit p = w4_split_plan(N, M, K);
-      if (p.S > 1)
-        return asum ? launch_w4_split<false>(p, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s)
-                    : launch_w4_split<true>(p, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
-    }
+  // above 64 tokens with a workspace: the GEMM split over K where that applies, else for W2 the
+  // FP4 x FP6 kernel
+  if (ws && M >= kGemmF4MinM) {
+    const GemmSplit p = gemm_split_plan(FMT, N, M, K);
+    if (p.S > 1)
+      return asum ? launch_gemm_split<FMT, false>(p, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s)
+                  : launch_gemm_split<FMT, true>(p, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
+    if constexpr (FMT != FMT_W4) return launch_gemm_f4(FMT, P, sw, N, K, act, sx, asum, M, y, acc_out, ws, s);
   }
   // 17..64 tokens: the skinny kernel, one pass over the weights (the codes of that many tokens do not
   // fit the decode kernel's LDS, and the GEMM's grid of N/256 workgroups would leave most CUs idle)
@@ -734,8 +737,8 @@ hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t 
 
 }  // namespace
 
-size_t w4_gemm_workspace(int64_t N, int64_t M, int64_t K) {
-  const GemmSplit p = w4_split_plan(N, M, K);
+size_t gemm_split_workspace(int fmt, int64_t N, int64_t M, int64_t K) {
+  const GemmSplit p = gemm_split_plan(fmt, N, M, K);
   return p.S > 1 ? split::part_bytes(p.S, M, N) + (size_t)p.S * (size_t)M * 4 : 0;
 }
 

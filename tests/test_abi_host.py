@@ -248,20 +248,24 @@ def test_linear_validation(L):
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=14336)), 4) == 0
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT, N=1000, K=4096)), 16) == 0
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=1000, K=14336)), 64) == 0
-    # above 64 tokens, where the FP4 x FP6 GEMM's 256 x 64 tiles are few it is split over K: S ranges
-    # of at least 4 steps of 256 k, S = min(ceil(512 / tiles), 768 // tiles, steps // 4) when >= 2;
-    # the FP6 codes and code sums, then at the next multiple of 256 bytes S M N4 int32 partial sums
+    # above 64 tokens, where the 256 x 64 GEMM tiles are few, the int8 GEMM is split over K: S ranges of
+    # at least 4 steps of 256 k, S = min(ceil(512 / tiles), 512 // tiles, steps // 4) when >= 2: S M N4
+    # int32 partial sums (256-byte aligned), then S M int32 code sums
     W = L.qift_workspace_bytes
     # down at 128 tokens: 32 tiles, 56 steps -> S = 14
-    assert W(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 128) == 128 * 10752 + 128 * 2 * 4 + 14 * 128 * 4096 * 4
-    # gate|up at 65 tokens: 224 tiles -> S = 3 (ranges of 6, 6 and 4 steps)
-    assert W(P(_pw(fmt=qift.W2_POT, N=28672, K=4096)), 65) == 200192 + 3 * 65 * 28672 * 4
-    # q|k|v at 1024 tokens: 384 tiles -> S = 2; 448 tiles (gate|up at 256) and 512 (down at 2048): none
+    assert W(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 128) == 14 * 128 * 4096 * 4 + 14 * 128 * 4
+    # gate|up at 65 tokens: 224 tiles -> S = 2
+    assert W(P(_pw(fmt=qift.W2_POT, N=28672, K=4096)), 65) == 2 * 65 * 28672 * 4 + 2 * 65 * 4
+    # ragged: 1000 rows (N4 = 1000), K = 4160 (17 steps, S = 4 of 5, 5, 5, 2), 96 tokens
+    assert W(P(_pw(fmt=qift.W2_POT, N=1000, K=4160)), 96) == 4 * 96 * 1000 * 4 + 4 * 96 * 4
+    # otherwise the FP4 x FP6 kernel's: FP6 codes and code sums, split over K itself where its tiles are
+    # few (S = min(ceil(512 / tiles), 768 // tiles, steps // 4) when >= 2), the partial sums following
+    # at the next multiple of 256 bytes.  q|k|v at 1024 tokens: 384 tiles -> S = 2; 65 x 5 tiles of
+    # 16400 x 2048 at 320 tokens -> S = 2; 448 tiles (gate|up at 256) and 512 (down at 2048): unsplit
     assert W(P(_pw(fmt=qift.W2_MNZ, N=6144, K=4096)), 1024) == 1024 * 3072 + 1024 * 4 + 2 * 1024 * 6144 * 4
+    assert W(P(_pw(fmt=qift.W2_MNZ, N=16400, K=2048)), 320) == 320 * 1536 + 320 * 4 + 2 * 320 * 16400 * 4
     assert W(P(_pw(fmt=qift.W2_MNZ, N=28672, K=4096)), 256) == 256 * 3072 + 256 * 4
     assert W(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 2048) == 2048 * 10752 + 2048 * 2 * 4
-    # ragged: 1000 rows (N4 = 1000), K = 4160 (17 steps, S = 4 of 5, 5, 5, 2), 96 tokens
-    assert W(P(_pw(fmt=qift.W2_POT, N=1000, K=4160)), 96) == 300032 + 4 * 96 * 1000 * 4
     # W4 above 64 tokens: the int8 GEMM split over K where its tiles are few, S ranges of at least 8
     # steps of 128 k, S = min(ceil(512 / tiles), 512 // tiles, steps // 8) when >= 3: S M N4 int32
     # partial sums (256-byte aligned), then S M int32 code sums

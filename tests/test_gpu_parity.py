@@ -129,29 +129,42 @@ def test_linear_ragged(Q, fmt, M):
 
 
 @pytest.mark.parametrize("fmt", [levels.FMT_W2_MNZ, levels.FMT_W2_POT])
-@pytest.mark.parametrize("M,K", [(65, 1088), (130, 1088), (300, 4096), (200, 14336), (96, 4160)])
-def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, K):
-    # W2 (MNZ, PoT) at M > 64: the int8 GEMM (no workspace) and the FP4 x FP6 GEMM (FP6 activations
-    # in a workspace of workspace_bytes; the MNZ codes as c / 2, the PoT levels +-1, +-4 as E2M1
-    # values), ragged rows and tokens, K with a partial last step: both bit-identical to the oracle.
-    # 1000 rows make 4 x ceil(M / 64) tiles, so from K = 1024 on (4 steps of 256 k per range) the FP4
-    # GEMM is split over K (int32 partial sums after the FP6 codes, ranges added by a second pass);
-    # K = 4160 has 17 steps: ranges of 5, 5, 5 and 2, the last one ending in a partial step.
-    N, b = 1000, 64
+@pytest.mark.parametrize("M,N,K", [(65, 1000, 1088), (130, 1000, 1088), (300, 1000, 4096), (200, 1000, 14336),
+                                   (96, 1000, 4160), (320, 16400, 2048)])
+def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, N, K):
+    # W2 (MNZ, PoT) at M > 64, ragged rows and tokens, K with a partial last step; bit-identical to the
+    # oracle on every path:
+    #   no workspace: the int8 GEMM;
+    #   a workspace of workspace_bytes where the 256 x 64 tiles are few: the int8 GEMM split over K
+    #   (S = min(ceil(512 / tiles), 512 // tiles, steps // 4) >= 2 ranges of 256-k steps; K = 4160 has
+    #   17 steps: ranges of 5, 5, 5 and 2, the last one ending in a partial step);
+    #   otherwise the FP4 x FP6 GEMM (FP6 activations in the workspace; the MNZ codes as c / 2, the PoT
+    #   levels +-1, +-4 as E2M1 values), itself split over K where S = min(ceil(512 / tiles),
+    #   768 // tiles, steps // 4) >= 2 (16400 x 2048 at 320 tokens: 325 tiles, two ranges).
+    b = 64
     L = synth.draw_levels(fmt, N, K, cfg=97, layer=M + fmt)
     s_w = synth.draw_scales(fmt, N, cfg=97, layer=M + fmt)
     x = synth.activations_fp16(97, M, 0, M, K, K // 100, 30.0)
     pk = pack_dev(Q, L, s_w, fmt)
     act = Q.rotate_quant_act(dev(x), b)
     q_ref, sx_ref = check_act(act, x, b)
-    codes = M * 3 * (K // 4) + 4 * M * (-(-(K // 32) // 256))
-    KT, tiles = -(-K // 256), 4 * -(-M // 64)
-    S = min(-(-512 // tiles), 768 // tiles, KT // 4)
-    if S >= 2:
+    KT, tiles, N4 = -(-K // 256), -(-N // 256) * -(-M // 64), -(-N // 4) * 4
+
+    def ranges(S):
+        if S < 2:
+            return 1
         us = -(-KT // S)
-        S = -(-KT // us)
-        codes = -(-codes // 256) * 256 + -(-(S * M * N * 4) // 256) * 256
-    assert Q.workspace_bytes(pk, M) == codes
+        return -(-KT // us)
+
+    S8 = ranges(min(-(-512 // tiles), 512 // tiles, KT // 4))
+    if S8 > 1:
+        expect = -(-(S8 * M * N4 * 4) // 256) * 256 + S8 * M * 4
+    else:
+        expect = M * 3 * (K // 4) + 4 * M * (-(-(K // 32) // 256))
+        S4 = ranges(min(-(-512 // tiles), 768 // tiles, KT // 4))
+        if S4 > 1:
+            expect = -(-expect // 256) * 256 + -(-(S4 * M * N4 * 4) // 256) * 256
+    assert Q.workspace_bytes(pk, M) == expect
     for ws in (None, torch.empty(Q.workspace_bytes(pk, M), dtype=torch.uint8, device="cuda")):
         for use_sum in (False, True):
             y, acc = run_linear(Q, pk, act, M, N, use_sum=use_sum, workspace=ws)
