@@ -311,8 +311,9 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
  *              NULL / 0 runs the int8 MFMA kernels.  With at least
  *              qift_workspace_bytes(w, M) bytes, where that is not 0 (MNZ
  *              and PoT weights):
- *                M > 64, where the prefill GEMM's 256-row x 64-token tiles
- *                are few (about 65-1024 tokens, by N): the int8 GEMM split
+ *                M > 64 (and N >= 16384 from M = 33 on), where the prefill
+ *                GEMM's 256-row x 64-token tiles are few (about 65-1024
+ *                tokens, by N): the int8 GEMM split
  *                over K, int32 partial sums of each K-range in the
  *                workspace, then added and the epilogue applied;
  *                M > 64 otherwise: the activations are re-coded to FP6 E2M3
@@ -321,7 +322,7 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
  *                PoT levels +-1, +-4 are E2M1 values, and every partial sum
  *                stays exact in fp32 (split over K too where its tiles are
  *                few);
- *                M <= 64 (K > 4096, few 16-row tiles; up to 16 tokens only
+ *                M <= 64 otherwise (K > 4096, few 16-row tiles; up to 16 tokens only
  *                where the codes exceed the decode kernel's LDS): the decode
  *                linear is split over K, int32 partial sums of each K-range in
  *                the workspace, then added and the epilogue applied.
@@ -569,15 +570,15 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
 /* Workspace bytes that the _ex calls use for this weight and M, 0 where none is used (host
  * query).  N4 = N rounded up to 4; T = ceil(N / 256) * ceil(M / 64) prefill tiles; a count S of
  * K-ranges is recounted once the ranges are sized (ranges of ceil(steps / S) steps).
- *   M > 64, MNZ, PoT and W4: the int8 GEMM split over S = min(ceil(512 / T), floor(512 / T),
- *     floor(steps / s0)) K-ranges when that is at least S0 (W2: 256-k steps, s0 = 4, S0 = 2; W4:
- *     128-k steps, s0 = 8, S0 = 3): S * M * N4 int32 partial sums (256-byte aligned), then S * M int32
- *     code sums.
+ *   M > 64 (MNZ, PoT and W4), and MNZ and PoT with N >= 16384 from M = 33 on: the int8 GEMM split
+ *     over S = min(ceil(512 / T), floor(512 / T), floor(steps / s0)) K-ranges when that is at least S0
+ *     (W2: 256-k steps, s0 = 4, S0 = 2; W4: 128-k steps, s0 = 8, S0 = 3): S * M * N4 int32 partial
+ *     sums (256-byte aligned), then S * M int32 code sums.
  *   M > 64 otherwise, MNZ and PoT: the FP4 x FP6 prefill kernel's M * 3K/4 bytes of FP6 codes and
  *     M * ceil(K / 8192) int32 code sums, split over S = min(ceil(512 / T), floor(768 / T),
  *     floor(ceil(K / 256) / 4)) K-ranges when that is at least 2, the S * M * N4 int32 partial sums
  *     following at the next multiple of 256 bytes; W4: 0.
- *   M <= 64, MNZ and PoT: the decode linear split over K, where it applies (K > 4096 and at most 680
+ *   M <= 64 otherwise, MNZ and PoT: the decode linear split over K, where it applies (K > 4096 and at most 680
  *     16-row tiles, N <= 10880; up to 16 tokens only where the codes exceed the decode kernel's LDS):
  *     S * M * N4 int32 partial sums (256-byte aligned) and S * M int32 code sums; W4: 0. */
 size_t qift_workspace_bytes(const qift_packed_w *w, int64_t M);

@@ -206,13 +206,16 @@ def test_w4_prefill_split_over_k(Q, M, N, K):
 @pytest.mark.parametrize("fmt", [levels.FMT_W2_MNZ, levels.FMT_W2_POT])
 @pytest.mark.parametrize("M,N,K", [(17, 1000, 1088), (32, 1000, 14336), (33, 4096, 4096), (64, 1000, 14336),
                                    (64, 4096, 14336), (20, 2064, 8192), (40, 300, 16384), (64, 6144, 4096),
-                                   (47, 28672, 4096), (16, 1000, 14336), (13, 4096, 14336), (16, 1000, 4096)])
+                                   (47, 28672, 4096), (16, 1000, 14336), (13, 4096, 14336), (16, 1000, 4096),
+                                   (32, 28672, 4096), (40, 16400, 4160)])
 def test_skinny_split_over_k(Q, fmt, M, N, K):
     # 17..64 tokens with a workspace of workspace_bytes, and up to 16 where the decode kernel's LDS does
     # not hold the codes (16 or 13 tokens of 14336): a linear with K > 4096 and few 16-row tiles runs
     # split over K (int32 partial sums of each K-range in the workspace, then added and the epilogue
-    # applied); K <= 4096 or a gate|up width needs no split (workspace_bytes 0).  Bit-identical to the
-    # oracle and to the call without a workspace, with and without the quantizer's code sums.
+    # applied); K <= 4096 needs no split (workspace_bytes 0).  From 33 tokens on a gate|up width (N >=
+    # 16384) takes the prefill GEMM split over K instead (S = min(ceil(512 / tiles), 512 // tiles,
+    # steps // 4) ranges of 256-k steps over 256 x 64 tiles).  Bit-identical to the oracle and to the call
+    # without a workspace, with and without the quantizer's code sums.
     b = 4096 if K % 4096 == 0 else (2048 if K % 2048 == 0 else 64)
     L = synth.draw_levels(fmt, N, K, cfg=98, layer=M + fmt)
     s_w = synth.draw_scales(fmt, N, cfg=98, layer=M + fmt)
@@ -221,9 +224,15 @@ def test_skinny_split_over_k(Q, fmt, M, N, K):
     act = Q.rotate_quant_act(dev(x), b)
     q_ref, sx_ref = check_act(act, x, b)
     need = Q.workspace_bytes(pk, M)
-    # the split rule: K > 4096, 4 tiles per workgroup, S = 256 / workgroups rounded, a split from S = 2
-    gx = -(-(-(-N // 16)) // 4)
-    assert (need > 0) == (K > 4096 and (256 + gx // 2) // gx >= 2)
+    if M >= 33 and N >= 16384:
+        tiles, KT = -(-N // 256), -(-K // 256)
+        S = min(-(-512 // tiles), 512 // tiles, KT // 4)
+        S = -(-KT // -(-KT // S))
+        assert need == -(-(S * M * (-(-N // 4) * 4) * 4) // 256) * 256 + S * M * 4
+    else:
+        # the skinny split rule: K > 4096, 4 tiles per workgroup, S = 256 / workgroups rounded, from S = 2
+        gx = -(-(-(-N // 16)) // 4)
+        assert (need > 0) == (K > 4096 and (256 + gx // 2) // gx >= 2)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda") if need else None
     y0, acc0 = run_linear(Q, pk, act, M, N)
     check_linear(y0, acc0, L, q_ref, sx_ref, s_w)
