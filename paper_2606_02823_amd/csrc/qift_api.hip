@@ -571,7 +571,7 @@ int qift_hbm_read_probe(const void* buf, size_t bytes, uint32_t* partials, qift_
 size_t qift_workspace_bytes(const qift_packed_w* w, int64_t M) {
   if (!w || !shape_ok(w->N, w->K) || M < 1 || M >= (int64_t(1) << 31)) return 0;
   if (w->fmt != QIFT_W2_MNZ && w->fmt != QIFT_W2_POT && w->fmt != QIFT_W4_SYM) return 0;
-  // the GEMM split over K where its tiles are few (and a wide W2 linear from 33 tokens on)
+  // the GEMM split over K where its tiles are few (and a wide linear from 33 tokens on)
   const size_t split = qift::gemm_split_workspace(w->fmt, w->N, M, w->K);
   if (split != 0 || w->fmt == QIFT_W4_SYM) return split;
   if (M <= qift::kSkinnyMaxM)   // the skinny linear split over K

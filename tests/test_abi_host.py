@@ -241,11 +241,12 @@ def test_linear_validation(L):
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT, N=1000, K=14336)), 17) == 952064 + 14 * 17 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 64) == 4 * 64 * 4096 * 4 + 4 * 64 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=4096)), 64) == 0
-    # a gate|up width from 33 tokens on: the prefill GEMM split over K (112 tiles -> S = 4); W4 and 32
-    # tokens keep the skinny kernel (no workspace)
+    # a gate|up width from 33 tokens on: the prefill GEMM split over K (112 tiles -> S = 4, W2 and W4);
+    # 32 tokens keep the skinny kernel (no workspace)
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=28672, K=4096)), 64) == 4 * 64 * 28672 * 4 + 4 * 64 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=28672, K=4096)), 32) == 0
-    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 64) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 64) == 4 * 64 * 28672 * 4 + 4 * 64 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 32) == 0
     # up to 16 tokens only where the decode kernel's LDS does not hold the codes (16 x 14336 does not,
     # 4 x 14336 and 16 x 4096 do)
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=14336)), 16) == 14 * 16 * 1000 * 4 + 14 * 16 * 4
