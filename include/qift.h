@@ -311,7 +311,8 @@ int qift_w2a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *a
  *              NULL / 0 runs the int8 MFMA kernels.  With at least
  *              qift_workspace_bytes(w, M) bytes, where that is not 0 (MNZ
  *              and PoT weights):
- *                M > 64 (and N >= 16384 from M = 33 on), where the prefill
+ *                M > 64 (and from M = 33 on N >= 16384, or N >= 4096 with
+ *                K > 4096), where the prefill
  *                GEMM's 256-row x 64-token tiles are few (about 65-1024
  *                tokens, by N): the int8 GEMM split
  *                over K, int32 partial sums of each K-range in the
@@ -570,7 +571,7 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
 /* Workspace bytes that the _ex calls use for this weight and M, 0 where none is used (host
  * query).  N4 = N rounded up to 4; T = ceil(N / 256) * ceil(M / 64) prefill tiles; a count S of
  * K-ranges is recounted once the ranges are sized (ranges of ceil(steps / S) steps).
- *   M > 64, and N >= 16384 from M = 33 on (MNZ, PoT and W4): the int8 GEMM split
+ *   M > 64, and from M = 33 on N >= 16384 or N >= 4096 with K > 4096 (MNZ, PoT and W4): the int8 GEMM split
  *     over S = min(ceil(512 / T), floor(512 / T), floor(steps / s0)) K-ranges when that is at least S0
  *     (W2: 256-k steps, s0 = 4, S0 = 2; W4: 128-k steps, s0 = 8, S0 = 3): S * M * N4 int32 partial
  *     sums (256-byte aligned), then S * M int32 code sums.

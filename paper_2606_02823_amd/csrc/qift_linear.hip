@@ -579,10 +579,13 @@ constexpr int gemm_occ() { return FMT == FMT_W4 ? 2 : 3; }
 // is a launch of its own).  W4 takes at least three ranges (two measured no faster: gate|up at 128
 // tokens 31.1 -> 33.4 us, q|k|v at 512 30.0 -> 32.4): down at 65 / 128 / 512 tokens 71.9 / 72.5 /
 // 74.8 -> 22.1 / 25.0 / 46.6 us, q|k|v and o at 65 26.6 -> 11.3 / 10.9.
-// From 33 tokens on, a wide linear (N >= 16384: gate|up) takes the split GEMM instead of the skinny
-// kernel, whose workgroups each read all M x K codes (gate|up at 33 / 64 tokens, W2 22.9 / 27.6 ->
-// 18.6 / 24.3 us, W4 35.3 / 45.2 -> 22.4 / 27.0; narrower linears lose: W2 q|k|v at 33 8.2 -> 10.1).
-constexpr int64_t kSplitTarget = 512, kSplitResident = 512, kSplitWideMinM = 33, kSplitWideMinN = 16384;
+// From 33 tokens on, a wide linear (N >= 16384: gate|up) or a long one (N >= 4096, K > 4096: down)
+// takes the split GEMM instead of the skinny kernel, whose workgroups each read all M x K codes
+// (gate|up at 33 / 64 tokens, W2 22.9 / 27.6 -> 18.6 / 24.3 us, W4 35.3 / 45.2 -> 22.4 / 27.0; down,
+// W2 12.7 / 16.1 -> 11.6 / 15.3, W4 21.6 / 30.5 -> 14.8 / 17.6).  Smaller linears lose: W2 q|k|v at 33
+// tokens 8.2 -> 10.1, 1000 x 14336 at 64 11.0 -> 12.8.
+constexpr int64_t kSplitTarget = 512, kSplitResident = 512, kSplitWideMinM = 33, kSplitWideMinN = 16384,
+                  kSplitLongMinN = 4096, kSplitLongMinK = 4097;
 struct GemmSplit {
   int S = 1, us = 0;
 };
@@ -591,7 +594,7 @@ inline GemmSplit gemm_split_plan(int fmt, int64_t N, int64_t M, int64_t K) {
   const int64_t bk = fmt == FMT_W4 ? 128 : 256, min_steps = fmt == FMT_W4 ? 8 : 4, min_s = fmt == FMT_W4 ? 3 : 2;
   const int64_t tiles = ((N + 255) / 256) * ((M + 63) / 64), KT = (K + bk - 1) / bk;
   p.us = (int)KT;
-  const bool wide = M >= kSplitWideMinM && N >= kSplitWideMinN;
+  const bool wide = M >= kSplitWideMinM && (N >= kSplitWideMinN || (N >= kSplitLongMinN && K >= kSplitLongMinK));
   if (M < kGemmF4MinM && !wide) return p;
   int64_t S = (kSplitTarget + tiles - 1) / tiles;
   if (S > kSplitResident / tiles) S = kSplitResident / tiles;
@@ -679,8 +682,8 @@ template <int FMT>
 hipError_t launch_fmt(const uint32_t* P, const uint16_t* sw, int64_t N, int64_t K, const int8_t* act,
                       const float* sx, const int32_t* asum, int64_t M, uint16_t* y, int32_t* acc_out, void* ws,
                       hipStream_t s) {
-  // with a workspace the GEMM split over K where that applies (above 64 tokens, or a wide linear from 33
-  // on), else above 64 tokens for W2 the FP4 x FP6 kernel
+  // with a workspace the GEMM split over K where that applies (above 64 tokens, or a wide or long linear
+  // from 33 on), else above 64 tokens for W2 the FP4 x FP6 kernel
   if (ws) {
     const GemmSplit p = gemm_split_plan(FMT, N, M, K);
     if (p.S > 1)

@@ -239,7 +239,9 @@ def test_linear_validation(L):
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT, N=1000, K=14336)), 64) == 14 * 64 * 1000 * 4 + 14 * 64 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=14336)), 64) == 14 * 64 * 1000 * 4 + 14 * 64 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_POT, N=1000, K=14336)), 17) == 952064 + 14 * 17 * 4
-    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 64) == 4 * 64 * 4096 * 4 + 4 * 64 * 4
+    # a down shape (N >= 4096, K > 4096) from 33 tokens on: the prefill GEMM split over K (16 tiles -> S = 14)
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 64) == 14 * 64 * 4096 * 4 + 14 * 64 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=4096, K=14336)), 32) == 4 * 32 * 4096 * 4 + 4 * 32 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=4096)), 64) == 0
     # a gate|up width from 33 tokens on: the prefill GEMM split over K (112 tiles -> S = 4, W2 and W4);
     # 32 tokens keep the skinny kernel (no workspace)
@@ -278,7 +280,8 @@ def test_linear_validation(L):
     assert W(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 65) == 0        # 224 tiles: S = 2
     assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=4096)), 512) == 4 * 512 * 4096 * 4 + 4 * 512 * 4
     assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 2048) == 0
-    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 64) == 0
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 64) == 14 * 64 * 4096 * 4 + 14 * 64 * 4
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 32) == 0
     # FP6 codes (M 3K/4 bytes), then one int32 code sum per token and 256 groups of 32 k
     need = 100 * 3 * (K // 4) + 100 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 100) == need

@@ -172,13 +172,13 @@ def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(65, 300, 4160), (200, 300, 4160), (128, 1000, 14336), (96, 4096, 1088),
-                                   (130, 2064, 8192), (40, 16400, 4160), (64, 16384, 2048)])
+                                   (130, 2064, 8192), (40, 16400, 4160), (64, 16384, 2048), (48, 4096, 14336)])
 def test_w4_prefill_split_over_k(Q, M, N, K):
     # W4 above 64 tokens with a workspace of workspace_bytes: where the 256 x 64 tiles are few the int8
     # GEMM is split over K (S >= 3 ranges of at least 8 steps of 128 k, about 512 workgroups, at most 512):
     # K = 4160 has 33 steps (ranges of 9, 9, 9 and 6, the last step partial); K = 1088 has 9 steps, too
-    # few to split (workspace_bytes 0).  From 33 tokens on a gate|up width (N >= 16384) takes the same
-    # split instead of the skinny kernel.  Bit-identical to the oracle and to the call without a
+    # few to split (workspace_bytes 0).  From 33 tokens on a gate|up width (N >= 16384) or a down shape
+    # (N >= 4096, K > 4096) takes the same split instead of the skinny kernel.  Bit-identical to the oracle and to the call without a
     # workspace, with and without the quantizer's code sums.
     fmt = levels.FMT_W4_SYM
     L = synth.draw_levels(fmt, N, K, cfg=95, layer=M)
@@ -214,7 +214,7 @@ def test_skinny_split_over_k(Q, fmt, M, N, K):
     # not hold the codes (16 or 13 tokens of 14336): a linear with K > 4096 and few 16-row tiles runs
     # split over K (int32 partial sums of each K-range in the workspace, then added and the epilogue
     # applied); K <= 4096 needs no split (workspace_bytes 0).  From 33 tokens on a gate|up width (N >=
-    # 16384) takes the prefill GEMM split over K instead (S = min(ceil(512 / tiles), 512 // tiles,
+    # 16384) or a down shape (N >= 4096, K > 4096) takes the prefill GEMM split over K instead (S = min(ceil(512 / tiles), 512 // tiles,
     # steps // 4) ranges of 256-k steps over 256 x 64 tiles).  Bit-identical to the oracle and to the call
     # without a workspace, with and without the quantizer's code sums.
     b = 4096 if K % 4096 == 0 else (2048 if K % 2048 == 0 else 64)
@@ -225,7 +225,7 @@ def test_skinny_split_over_k(Q, fmt, M, N, K):
     act = Q.rotate_quant_act(dev(x), b)
     q_ref, sx_ref = check_act(act, x, b)
     need = Q.workspace_bytes(pk, M)
-    if M >= 33 and N >= 16384:
+    if M >= 33 and (N >= 16384 or (N >= 4096 and K > 4096)):
         tiles, KT = -(-N // 256), -(-K // 256)
         S = min(-(-512 // tiles), 512 // tiles, KT // 4)
         S = -(-KT // -(-KT // S))
