@@ -357,8 +357,8 @@ int qift_w2a4_lut_linear(const qift_packed_w *w, const uint16_t *lut, const int8
                          const float *act_scale, int64_t M, uint16_t *out, qift_stream_t stream);
 
 /* The W4 sibling (fmt QIFT_W4_SYM); same arguments and results.  The workspace of the _ex call is
- * used above 64 tokens where qift_workspace_bytes is not 0: the int8 prefill GEMM split over K, as for
- * W2 (no FP4 form). */
+ * used where qift_workspace_bytes is not 0: the int8 prefill GEMM split over K, as for W2 but from 24
+ * tokens on for the wide and long linears (no FP4 form). */
 int qift_w4a4_linear(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
                      int64_t M, uint16_t *out, qift_stream_t stream);
 int qift_w4a4_linear_ex(const qift_packed_w *w, const int8_t *act_q, const float *act_scale,
@@ -571,7 +571,7 @@ int qift_kv4_attention_decode_noalloc(const uint16_t *q, int64_t B, int32_t Hq, 
 /* Workspace bytes that the _ex calls use for this weight and M, 0 where none is used (host
  * query).  N4 = N rounded up to 4; T = ceil(N / 256) * ceil(M / 64) prefill tiles; a count S of
  * K-ranges is recounted once the ranges are sized (ranges of ceil(steps / S) steps).
- *   M > 64, and from M = 33 on N >= 16384 or N >= 4096 with K > 4096 (MNZ, PoT and W4): the int8 GEMM split
+ *   M > 64, and from M = 33 (W4: 24) on N >= 16384 or N >= 4096 with K > 4096: the int8 GEMM split
  *     over S = min(ceil(512 / T), floor(512 / T), floor(steps / s0)) K-ranges when that is at least S0
  *     (W2: 256-k steps, s0 = 4, S0 = 2; W4: 128-k steps, s0 = 8, S0 = 3): S * M * N4 int32 partial
  *     sums (256-byte aligned), then S * M int32 code sums.

@@ -583,8 +583,11 @@ constexpr int gemm_occ() { return FMT == FMT_W4 ? 2 : 3; }
 // takes the split GEMM instead of the skinny kernel, whose workgroups each read all M x K codes
 // (gate|up at 33 / 64 tokens, W2 22.9 / 27.6 -> 18.6 / 24.3 us, W4 35.3 / 45.2 -> 22.4 / 27.0; down,
 // W2 12.7 / 16.1 -> 11.6 / 15.3, W4 21.6 / 30.5 -> 14.8 / 17.6).  Smaller linears lose: W2 q|k|v at 33
-// tokens 8.2 -> 10.1, 1000 x 14336 at 64 11.0 -> 12.8.
-constexpr int64_t kSplitTarget = 512, kSplitResident = 512, kSplitWideMinM = 33, kSplitWideMinN = 16384,
+// tokens 8.2 -> 10.1, 1000 x 14336 at 64 11.0 -> 12.8.  W4, whose skinny kernel reads twice the weight
+// bytes, from 24 tokens on (at 32: down 18.3 -> 14.4, gate|up 25.9 -> 22.0; at 24 a 22016-row gate|up
+// loses 17.8 -> 18.6 while the others gain 1.2-2.7 us).
+constexpr int64_t kSplitTarget = 512, kSplitResident = 512, kSplitWideMinM = 33, kSplitWideMinMW4 = 24,
+                  kSplitWideMinN = 16384,
                   kSplitLongMinN = 4096, kSplitLongMinK = 4097;
 struct GemmSplit {
   int S = 1, us = 0;
@@ -594,7 +597,8 @@ inline GemmSplit gemm_split_plan(int fmt, int64_t N, int64_t M, int64_t K) {
   const int64_t bk = fmt == FMT_W4 ? 128 : 256, min_steps = fmt == FMT_W4 ? 8 : 4, min_s = fmt == FMT_W4 ? 3 : 2;
   const int64_t tiles = ((N + 255) / 256) * ((M + 63) / 64), KT = (K + bk - 1) / bk;
   p.us = (int)KT;
-  const bool wide = M >= kSplitWideMinM && (N >= kSplitWideMinN || (N >= kSplitLongMinN && K >= kSplitLongMinK));
+  const bool wide = M >= (fmt == FMT_W4 ? kSplitWideMinMW4 : kSplitWideMinM) &&
+                    (N >= kSplitWideMinN || (N >= kSplitLongMinN && K >= kSplitLongMinK));
   if (M < kGemmF4MinM && !wide) return p;
   int64_t S = (kSplitTarget + tiles - 1) / tiles;
   if (S > kSplitResident / tiles) S = kSplitResident / tiles;

@@ -248,7 +248,8 @@ def test_linear_validation(L):
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=28672, K=4096)), 64) == 4 * 64 * 28672 * 4 + 4 * 64 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=28672, K=4096)), 32) == 0
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 64) == 4 * 64 * 28672 * 4 + 4 * 64 * 4
-    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 32) == 0
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 32) == 4 * 32 * 28672 * 4 + 4 * 32 * 4
+    assert L.qift_workspace_bytes(P(_pw(fmt=qift.W4_SYM, N=28672, K=4096)), 23) == 0
     # up to 16 tokens only where the decode kernel's LDS does not hold the codes (16 x 14336 does not,
     # 4 x 14336 and 16 x 4096 do)
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ, N=1000, K=14336)), 16) == 14 * 16 * 1000 * 4 + 14 * 16 * 4
@@ -281,7 +282,8 @@ def test_linear_validation(L):
     assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=4096)), 512) == 4 * 512 * 4096 * 4 + 4 * 512 * 4
     assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 2048) == 0
     assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 64) == 14 * 64 * 4096 * 4 + 14 * 64 * 4
-    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 32) == 0
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 24) == 14 * 24 * 4096 * 4 + 14 * 24 * 4   # W4 from 24
+    assert W(P(_pw(fmt=qift.W4_SYM, N=4096, K=14336)), 23) == 0
     # FP6 codes (M 3K/4 bytes), then one int32 code sum per token and 256 groups of 32 k
     need = 100 * 3 * (K // 4) + 100 * 4
     assert L.qift_workspace_bytes(P(_pw(fmt=qift.W2_MNZ)), 100) == need

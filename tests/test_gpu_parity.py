@@ -172,12 +172,13 @@ def test_w2_prefill_int8_and_fp4_paths(Q, fmt, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(65, 300, 4160), (200, 300, 4160), (128, 1000, 14336), (96, 4096, 1088),
-                                   (130, 2064, 8192), (40, 16400, 4160), (64, 16384, 2048), (48, 4096, 14336)])
+                                   (130, 2064, 8192), (40, 16400, 4160), (64, 16384, 2048), (48, 4096, 14336),
+                                   (24, 4096, 14336), (30, 28672, 4096)])
 def test_w4_prefill_split_over_k(Q, M, N, K):
     # W4 above 64 tokens with a workspace of workspace_bytes: where the 256 x 64 tiles are few the int8
     # GEMM is split over K (S >= 3 ranges of at least 8 steps of 128 k, about 512 workgroups, at most 512):
     # K = 4160 has 33 steps (ranges of 9, 9, 9 and 6, the last step partial); K = 1088 has 9 steps, too
-    # few to split (workspace_bytes 0).  From 33 tokens on a gate|up width (N >= 16384) or a down shape
+    # few to split (workspace_bytes 0).  From 24 tokens on a gate|up width (N >= 16384) or a down shape
     # (N >= 4096, K > 4096) takes the same split instead of the skinny kernel.  Bit-identical to the oracle and to the call without a
     # workspace, with and without the quantizer's code sums.
     fmt = levels.FMT_W4_SYM
